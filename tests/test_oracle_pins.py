@@ -1,0 +1,343 @@
+"""Pins of the float64 oracle against what the paper and the mathematics fix.
+
+Each test ties one oracle function to something other than itself: a closed
+form (SVD functional calculus, Props. 1-2 of App. D), an invariant (unit row
+norms, trace of Gamma, Frobenius norms of T), a textbook routine (Higham's
+Newton-Schulz polar iteration), a worked example of the paper (App. A), a
+special case where the sketch must be exact (Alg. 2), or the published
+known-answer vectors of Philox4x32-10.
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+
+from oracle import normpre_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+RNG = np.random.default_rng(20240917)
+
+
+def _rand(m, n, scale=1.0):
+    return RNG.standard_normal((m, n)) * scale
+
+
+# ------------------------------------------------------------------ Philox / Omega
+def test_philox_known_answer_vectors():
+    rows = [l.split() for l in open(os.path.join(GOLDEN, "philox4x32_10_kat.txt"))
+            if l.strip() and not l.startswith("#")]
+    for r in rows:
+        vals = [int(v, 16) for v in r]
+        ctr = np.array([vals[0:4]], dtype=np.uint32)
+        out = O.philox4x32_10(ctr, (vals[4], vals[5]))[0]
+        assert [int(v) for v in out] == vals[6:10]
+
+
+def test_omega_is_standard_normal():
+    om = O.sketch_omega(1337, 7, 3, 4000, 25).ravel()
+    # Kolmogorov-Smirnov distance against the N(0,1) CDF.
+    xs = np.sort(om)
+    cdf = 0.5 * (1.0 + np.vectorize(math.erf)(xs / math.sqrt(2.0)))
+    emp = np.arange(1, xs.size + 1) / xs.size
+    ks = np.max(np.abs(emp - cdf))
+    assert ks < 1.63 / math.sqrt(xs.size)          # 1% critical value
+    assert abs(om.mean()) < 5.0 / math.sqrt(om.size)
+    assert abs(om.var() - 1.0) < 0.03
+
+
+def test_omega_counter_layout():
+    # Different (t, matrix id) give independent draws; same key reproduces.
+    a = O.sketch_omega(1, 2, 3, 50, 8)
+    assert np.array_equal(a, O.sketch_omega(1, 2, 3, 50, 8))
+    assert not np.allclose(a, O.sketch_omega(1, 3, 3, 50, 8))
+    assert not np.allclose(a, O.sketch_omega(1, 2, 4, 50, 8))
+    # Element (i, j) uses linear index e = j*b + i: the first column is the
+    # leading block of the flat stream.
+    big = O.sketch_omega(1, 2, 3, 50, 8)
+    flat = O.sketch_omega(1, 2, 3, 400, 1)[:, 0]
+    assert np.allclose(big.T.ravel(), flat)
+
+
+# ------------------------------------------------------------------ momentum
+def test_momentum_matches_geometric_sum():
+    mu = 0.95
+    gs = [_rand(5, 7) for _ in range(6)]
+    m = np.zeros((5, 7))
+    for g in gs:
+        m = O.momentum_update(m, g, mu)
+    expect = sum(mu ** (len(gs) - 1 - s) * g for s, g in enumerate(gs))
+    assert np.allclose(m, expect, rtol=0, atol=1e-13)
+
+
+# ------------------------------------------------------------------ relaxed tangent
+def test_relaxed_tangent_decomposition():
+    # App. D: x = g_tan + (1 - ||w||^2) g_rad with g_rad the projection onto w.
+    m, w = _rand(9, 13), _rand(9, 13, 0.4)
+    x = O.relaxed_tangent(m, w)
+    for i in range(9):
+        wi, mi = w[i], m[i]
+        g_rad = (mi @ wi) / (wi @ wi) * wi
+        g_tan = mi - g_rad
+        assert np.allclose(x[i], g_tan + (1.0 - wi @ wi) * g_rad, atol=1e-12)
+
+
+def test_relaxed_tangent_unit_rows_is_strict_tangent():
+    m, w = _rand(6, 10), _rand(6, 10)
+    w /= np.linalg.norm(w, axis=1, keepdims=True)
+    x = O.relaxed_tangent(m, w)
+    assert np.allclose(np.sum(x * w, axis=1), 0.0, atol=1e-12)
+
+
+def test_relaxed_tangent_zero_weight_is_identity():
+    m = _rand(4, 5)
+    assert np.array_equal(O.relaxed_tangent(m, np.zeros((4, 5))), m)
+
+
+# ------------------------------------------------------------------ normalization
+def test_normalization_invariants():
+    x = _rand(12, 30)
+    x[3] = 0.0
+    psi = O.diagonal_gram_normalize(x)
+    norms = np.linalg.norm(psi, axis=1)
+    assert norms[3] == 0.0
+    assert np.allclose(np.delete(norms, 3), 1.0, atol=1e-14)
+    gamma = psi @ psi.T
+    assert np.allclose(np.delete(np.diag(gamma), 3), 1.0)
+    assert math.isclose(np.trace(gamma), 11.0, rel_tol=1e-14)
+    # Off-diagonal entries are row cosines (Sec. 2.2).
+    cos01 = x[0] @ x[1] / (np.linalg.norm(x[0]) * np.linalg.norm(x[1]))
+    assert math.isclose(gamma[0, 1], cos01, rel_tol=1e-12)
+
+
+def test_scale_dominated_rows_example():
+    # Sec. 1: one row of norm 1e4, others 1e-3 with fixed directions.  The
+    # leading Gram eigenvector follows the big row; Psi does not see scales.
+    dirs = _rand(5, 8)
+    dirs /= np.linalg.norm(dirs, axis=1, keepdims=True)
+    scales = np.array([1e4, 1e-3, 1e-3, 1e-3, 1e-3])
+    x = scales[:, None] * dirs
+    _, vecs = np.linalg.eigh(x @ x.T)
+    assert abs(vecs[0, -1]) > 1.0 - 1e-12
+    assert np.allclose(O.diagonal_gram_normalize(x), dirs, atol=1e-14)
+
+
+def test_orthogonal_rows_worked_example():
+    rows = [l.split() for l in open(os.path.join(GOLDEN, "orthogonal_rows_example.txt"))
+            if l.strip() and not l.startswith("#")]
+    a = np.array([float(r[0]) for r in rows])
+    q, _ = np.linalg.qr(_rand(6, 4))
+    x = a[:, None] * q.T                  # 4 orthogonal rows in R^6 with norms a
+    ghat = O.trace_matched_gram(x)
+    assert np.allclose(np.sort(np.linalg.eigvalsh(ghat)), [float(r[1]) for r in rows])
+    psi = O.diagonal_gram_normalize(x)
+    assert np.allclose(np.linalg.eigvalsh(psi @ psi.T), [float(r[2]) for r in rows])
+
+
+# ------------------------------------------------------------------ Newton-Schulz
+def _odd_poly(coeffs, s):
+    a, b, c = coeffs
+    return a * s + b * s ** 3 + c * s ** 5
+
+
+@pytest.mark.parametrize("shape", [(7, 19), (19, 7), (16, 16), (1, 9), (40, 90)])
+def test_newton_schulz_is_odd_functional_calculus(shape):
+    # X_{k+1} = a X + (b A + c A^2) X with A = X X^T acts on the singular values
+    # through f(s) = a s + b s^3 + c s^5 and leaves the singular vectors alone.
+    psi = O.diagonal_gram_normalize(_rand(*shape))
+    u, s, vt = np.linalg.svd(psi, full_matrices=False)
+    s = s / (np.linalg.norm(psi) + 1e-7)
+    for _ in range(5):
+        s = _odd_poly(O.MUON_NS_COEFFS, s)
+    expect = u @ np.diag(s) @ vt
+    got = O.newton_schulz(psi, 5, O.MUON_NS_COEFFS)
+    assert np.allclose(got, expect, atol=1e-12)
+
+
+def test_newton_schulz_transpose_rule():
+    psi = _rand(11, 29)
+    assert np.allclose(O.newton_schulz(psi.T), O.newton_schulz(psi).T, atol=1e-13)
+
+
+def test_cubic_newton_schulz_converges_to_polar_factor():
+    # Higham's iteration X <- 1.5 X - 0.5 X X^T X converges to msign(X) = U V^T.
+    psi = O.diagonal_gram_normalize(_rand(10, 24))
+    t = O.newton_schulz(psi, 60, O.CUBIC_NS_COEFFS)
+    assert np.allclose(t, O.msign_svd(psi), atol=1e-10)
+    # ||T^G||_F^2 = m for full row rank (App. D).
+    assert math.isclose(np.linalg.norm(t) ** 2, 10.0, rel_tol=1e-10)
+
+
+def test_newton_schulz_on_orthonormal_rows_is_proportional():
+    q, _ = np.linalg.qr(_rand(20, 6))
+    psi = q.T                                   # Gamma = I
+    t = O.newton_schulz(psi)
+    ratio = t / psi
+    assert np.allclose(ratio, ratio.flat[0])
+
+
+# ------------------------------------------------------------------ NormPre-L
+def _svd_clip_topr(psi, r):
+    """Props. 1-2: T = U diag(s') V^T, s'_i = 1 for the top-min(r, |A|) s_i > 1."""
+    u, s, vt = np.linalg.svd(psi, full_matrices=False)
+    s2 = s.copy()
+    active = np.flatnonzero(s > 1.0)[:r]
+    s2[active] = 1.0
+    return u @ np.diag(s2) @ vt
+
+
+def _correlated_psi(m, n, rank=3, noise=0.3):
+    x = _rand(m, rank) @ _rand(rank, n) + noise * _rand(m, n)
+    return O.diagonal_gram_normalize(x)
+
+
+@pytest.mark.parametrize("r", [1, 2, 4, 100])
+def test_localized_exact_matches_svd_closed_form(r):
+    psi = _correlated_psi(14, 33)
+    u_sel, lam_sel = O.localized_exact(psi, r)
+    t = O.localized_apply(psi, u_sel, lam_sel)
+    assert np.allclose(t, _svd_clip_topr(psi, r), atol=1e-12)
+
+
+def test_regularized_projection_clips_singular_values():
+    # Prop. 1 with r >= |A|: singular values min(s, 1), and T is the nearest
+    # matrix with ||T||_op <= 1 (checked against random feasible points).
+    psi = _correlated_psi(8, 20)
+    u_sel, lam_sel = O.localized_exact(psi, 8)
+    t = O.localized_apply(psi, u_sel, lam_sel)
+    s_psi = np.linalg.svd(psi, compute_uv=False)
+    s_t = np.linalg.svd(t, compute_uv=False)
+    assert np.allclose(s_t, np.minimum(s_psi, 1.0), atol=1e-12)
+    best = np.linalg.norm(t - psi)
+    for _ in range(200):
+        cand = t + 0.05 * _rand(*t.shape)
+        cand /= max(1.0, np.linalg.norm(cand, 2))
+        assert np.linalg.norm(cand - psi) >= best - 1e-12
+
+
+def test_localized_eigen_and_svd_paths_agree_and_contract():
+    psi = _correlated_psi(16, 40)
+    u_sel, lam_sel = O.localized_exact(psi, 3)
+    t = O.localized_apply(psi, u_sel, lam_sel)
+    # ||T^L||^2 = |C| + sum_{i not in C} lambda_i <= m  (App. D)
+    lam = np.sort(np.linalg.eigvalsh(psi @ psi.T))[::-1]
+    expect = len(lam_sel) + lam[len(lam_sel):].sum()
+    assert math.isclose(np.linalg.norm(t) ** 2, expect, rel_tol=1e-12)
+    assert np.linalg.norm(t) ** 2 <= 16.0 + 1e-9
+    # sigma_i(T) <= sigma_i(Psi): eig(P^L) in (0, 1]
+    assert np.all(np.linalg.svd(t, compute_uv=False) <= np.linalg.svd(psi, compute_uv=False) + 1e-12)
+
+
+def test_sketch_exact_when_rank_fits():
+    # rank(Psi) <= l: the sketch spans range(Psi) and equals exact-L.
+    m, n, k = 60, 80, 5
+    psi = O.diagonal_gram_normalize(_rand(m, k) @ _rand(k, n))
+    om = O.sketch_omega(11, 0, 0, n, 12)
+    sk = O.interaction_sketch(psi, 4, 8, 1, om)
+    resid = np.linalg.norm(psi - sk.q @ (sk.q.T @ psi)) / np.linalg.norm(psi)
+    assert resid < 1e-13
+    t_sk = O.localized_apply(psi, sk.u_sel, sk.lam_sel)
+    u_ex, lam_ex = O.localized_exact(psi, 4)
+    assert np.allclose(t_sk, O.localized_apply(psi, u_ex, lam_ex), atol=1e-11)
+
+
+def test_sketch_exact_when_l_equals_rows():
+    psi = _correlated_psi(10, 50)
+    om = O.sketch_omega(5, 1, 2, 50, 10)
+    sk = O.interaction_sketch(psi, 6, 8, 1, om)      # l = min(10, 14) = 10
+    assert sk.ell == 10
+    u_ex, lam_ex = O.localized_exact(psi, 6)
+    assert np.allclose(O.localized_apply(psi, sk.u_sel, sk.lam_sel),
+                       O.localized_apply(psi, u_ex, lam_ex), atol=1e-11)
+
+
+def test_sketch_ritz_values_interlace_and_norm_closed_form():
+    psi = _correlated_psi(120, 200, rank=8, noise=0.5)
+    om = O.sketch_omega(3, 4, 5, 200, 20)
+    sk = O.interaction_sketch(psi, 12, 8, 1, om)
+    lam = np.sort(np.linalg.eigvalsh(psi @ psi.T))[::-1]
+    assert np.all(sk.ritz_values <= lam[: sk.ritz_values.size] + 1e-10)
+    t = O.localized_apply(psi, sk.u_sel, sk.lam_sel)
+    closed = np.linalg.norm(psi) ** 2 - np.sum(sk.lam_sel - 1.0)
+    assert math.isclose(np.linalg.norm(t) ** 2, closed, rel_tol=1e-12)
+
+
+def test_sketch_basis_invariance():
+    # Rayleigh-Ritz does not depend on which orthonormal basis of span(Y) is used.
+    psi = _correlated_psi(50, 70, rank=6)
+    om = O.sketch_omega(9, 9, 9, 70, 14)
+    sk = O.interaction_sketch(psi, 6, 8, 1, om)
+    rot, _ = np.linalg.qr(_rand(14, 14))
+    q2 = sk.q @ rot
+    b2 = q2.T @ psi
+    ev, z = np.linalg.eigh(b2 @ b2.T)
+    order = np.argsort(-ev, kind="stable")[:6]
+    lam2, u2 = ev[order], q2 @ z[:, order]
+    keep = lam2 > 1.0
+    t2 = O.localized_apply(psi, u2[:, keep], lam2[keep])
+    assert np.allclose(t2, O.localized_apply(psi, sk.u_sel, sk.lam_sel), atol=1e-11)
+
+
+def test_topr_then_threshold_equals_threshold_then_topr():
+    psi = _correlated_psi(30, 45, rank=10, noise=0.2)
+    om = O.sketch_omega(2, 2, 2, 45, 13)
+    sk = O.interaction_sketch(psi, 5, 8, 1, om)
+    ev = np.linalg.eigvalsh(sk.gamma_q)
+    ev = np.sort(ev)[::-1]
+    expect = ev[ev > 1.0][:5]
+    assert np.allclose(sk.lam_sel, expect)
+
+
+# ------------------------------------------------------------------ RMS + update
+def test_rms_and_update():
+    hp = O.HParams(lr=1e-2)
+    w, g, mp = _rand(12, 20, 0.02), _rand(12, 20), _rand(12, 20)
+    for variant in ("G", "L"):
+        out = O.normpre_step(w, g, mp, 0, hp, variant)
+        assert math.isclose(np.linalg.norm(out["update"]), 0.2 * math.sqrt(240), rel_tol=1e-12)
+        # lr = 0 leaves W unchanged
+        hp0 = O.HParams(lr=0.0)
+        assert np.array_equal(O.normpre_step(w, g, mp, 0, hp0, variant)["w_new"], w)
+
+
+def test_zero_signal_gives_pure_decay():
+    hp = O.HParams(lr=0.5, weight_decay=0.1)
+    w = _rand(6, 9)
+    z = np.zeros((6, 9))
+    for variant in ("G", "L"):
+        out = O.normpre_step(w, z, z, 1, hp, variant)
+        assert np.all(out["update"] == 0.0)
+        assert np.allclose(out["w_new"], (1.0 - 0.05) * w)
+
+
+# ------------------------------------------------------------------ whole step
+@pytest.mark.parametrize("variant", ["G", "L"])
+def test_transpose_equivariance(variant):
+    w, g, mp = _rand(9, 21, 0.1), _rand(9, 21), _rand(9, 21)
+    hr = O.HParams(orientation="row", rank=3)
+    hc = O.HParams(orientation="col", rank=3)
+    a = O.normpre_step(w, g, mp, 4, hr, variant)
+    b = O.normpre_step(w.T, g.T, mp.T, 4, hc, variant)
+    assert np.allclose(a["update"], b["update"].T, atol=1e-12)
+
+
+@pytest.mark.parametrize("variant", ["G", "L"])
+def test_scale_and_row_permutation(variant):
+    hp = O.HParams(orientation="row", rank=4)
+    w, g, mp = _rand(15, 26, 0.05), _rand(15, 26), _rand(15, 26)
+    base = O.normpre_step(w, g, mp, 2, hp, variant)["update"]
+    scaled = O.normpre_step(w, 3.7 * g, 3.7 * mp, 2, hp, variant)["update"]
+    assert np.allclose(base, scaled, atol=1e-12)
+    perm = RNG.permutation(15)
+    permuted = O.normpre_step(w[perm], g[perm], mp[perm], 2, hp, variant)["update"]
+    assert np.allclose(base[perm], permuted, atol=1e-11)
+
+
+def test_orientation_alternates_with_t():
+    hp = O.HParams()
+    w, g, mp = _rand(5, 8), _rand(5, 8), _rand(5, 8)
+    assert O.normpre_step(w, g, mp, 0, hp, "G")["k"] == 0
+    assert O.normpre_step(w, g, mp, 1, hp, "G")["k"] == 1
+    # k = 1 normalises the columns of the W layout
+    psi = O.normpre_step(w, g, mp, 1, hp, "G")["psi"]
+    assert np.allclose(np.linalg.norm(psi, axis=0), 1.0)
