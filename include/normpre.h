@@ -1,0 +1,221 @@
+/*
+ * normpre.h -- C ABI of the MI355X (gfx950) NormPre optimizer-step library.
+ *
+ * One call of normpre_step() performs one step of the NormPre optimizer
+ * (Algorithm 1 of "Normalize-Then-Precondition", arXiv 2609.36692, Sec. 3.1)
+ * on a list of 2-D fp32 weight matrices that live in device memory:
+ *
+ *   M   <- mu M + G                                 (momentum)
+ *   k   =  t mod 2; rows of W (k = 0) or of W^T (k = 1) are "active"
+ *   x_i =  m_i - <m_i, w_i> w_i                     (relaxed tangent)
+ *   Psi =  D(X)^{-1} X                              (diagonal-Gram normalization, Eq. 2)
+ *   T   =  msign(Psi) by Newton-Schulz              (NormPre-G, Sec. 3.2)
+ *        or (I + U_C (Lambda_C^{-1/2} - I) U_C^T) Psi with (U_C, Lambda_C) from
+ *        the randomized interaction sketch          (NormPre-L, Alg. 2 of App. B)
+ *   W   <- W - lr (0.2 sqrt(mn) O_k^{-1}(T) / ||T||_F + wd W)   (consistent RMS)
+ *
+ * Conventions:
+ *   - Every matrix is a dense, row-major fp32 array of rows x cols elements,
+ *     4-byte aligned, on the context's device.  Pointers are device pointers.
+ *   - Host arrays (the pointer lists, shapes, hyper-parameters) are read
+ *     during the call only; the library keeps no reference to them.
+ *   - The caller owns W, G and M.  W and M are updated in place, G is read
+ *     only.  Distinct matrices must not overlap; W, G and M of one matrix
+ *     must be three distinct buffers.
+ *   - The library owns only its workspace (grown on demand, released by
+ *     normpre_destroy).  The step counter t and the seed are caller state:
+ *     restoring (W, M, t, seed) reproduces the next step exactly.
+ *   - Errors: every int-returning entry point returns NORMPRE_OK (0) or a
+ *     negative NORMPRE_ERR_* code; nothing throws or aborts across the ABI.
+ *     Argument validation happens on the host before any launch, so on an
+ *     error no device memory has been written.  The message of the last
+ *     error on a context is available from normpre_last_error().
+ *   - normpre_step() only enqueues work on the given stream and never
+ *     synchronizes; device faults surface at the caller's next
+ *     synchronization.  A context must be used by one host thread and one
+ *     stream at a time.
+ */
+#ifndef NORMPRE_H
+#define NORMPRE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- return codes ------------------------------------------------------ */
+#define NORMPRE_OK                   0
+#define NORMPRE_ERR_INVALID_ARG     (-1)  /* null pointer, bad size or value  */
+#define NORMPRE_ERR_UNSUPPORTED     (-2)  /* valid but outside this build     */
+#define NORMPRE_ERR_OOM             (-3)  /* workspace allocation failed      */
+#define NORMPRE_ERR_HIP             (-4)  /* a HIP runtime call failed        */
+#define NORMPRE_ERR_NOT_INITIALIZED (-5)  /* null or destroyed context        */
+
+/* ---- variants (Alg. 1: "optimizer variant") ----------------------------- */
+#define NORMPRE_VARIANT_G 0   /* global spectral preconditioning, Newton-Schulz */
+#define NORMPRE_VARIANT_L 1   /* localized preconditioning, randomized sketch   */
+
+/* ---- orientation modes (Sec. 3.1, alternating row/column orientation) --- */
+#define NORMPRE_ORIENT_ALTERNATING 0   /* k = t mod 2 (the paper's rule) */
+#define NORMPRE_ORIENT_ROW         1   /* always k = 0                  */
+#define NORMPRE_ORIENT_COL         2   /* always k = 1                  */
+
+/* ---- flags -------------------------------------------------------------- */
+/* Keep per-matrix intermediates of the last step for normpre_debug_fetch():
+ * fp32 Psi, the NormPre-G output T, the Ritz values and |C| of NormPre-L.
+ * Costs extra device memory and bandwidth; never set it when timing. */
+#define NORMPRE_FLAG_DEBUG         1u
+/* Record a HIP event pair around every kernel launch so that
+ * normpre_kernel_stats() can report per-kernel-class device time. */
+#define NORMPRE_FLAG_TIME_KERNELS  2u
+
+/*
+ * Hyper-parameters of one step.  Defaults (normpre_default_hparams) follow
+ * the optimizer-configuration table of App. A: mu = 0.95, 5 Newton-Schulz
+ * steps, weight decay 0.1, rank r = 32, oversampling o = 8, one power
+ * iteration p = 1, target update RMS 0.2 (Sec. 3.1), lr = 6e-4.
+ */
+typedef struct normpre_hparams {
+    float    lr;            /* eta_t, learning rate                             */
+    float    momentum;      /* mu                                               */
+    float    weight_decay;  /* lambda_wd (multiplied by lr, Alg. 1)             */
+    float    target_rms;    /* RMS of the rescaled update (0.2)                 */
+    int32_t  ns_iters;      /* Newton-Schulz iterations q (NormPre-G), 1..64    */
+    float    ns_coeffs[3];  /* quintic X <- aX + (bA + cA^2)X, A = XX^T         */
+    float    ns_eps;        /* Frobenius pre-scaling X0 = Psi / (||Psi||_F + eps) */
+    int32_t  rank;          /* spectral budget r (NormPre-L), >= 1              */
+    int32_t  oversample;    /* o >= 0; sketch width l = min(active rows, r + o) */
+    int32_t  power_iters;   /* p >= 0                                           */
+    int32_t  orientation;   /* NORMPRE_ORIENT_*                                 */
+    uint64_t seed;          /* key of the Gaussian sketch generator             */
+    int64_t  step;          /* t: orientation k = t mod 2 and sketch counter    */
+    float    norm_eps;      /* psi_i = x_i / max(||x_i||, norm_eps)             */
+    uint32_t flags;         /* NORMPRE_FLAG_*                                   */
+} normpre_hparams;
+
+typedef struct normpre_ctx normpre_ctx;
+
+/* Fills *hp with the defaults listed above.  Returns INVALID_ARG on null. */
+int normpre_default_hparams(normpre_hparams* hp);
+
+/* Creates a context bound to HIP device `device` (an ordinal).  On success
+ * *ctx receives the new context.  Allocates no workspace yet.
+ * Errors: INVALID_ARG (null ctx), HIP_ERROR (no such device). */
+int normpre_init(normpre_ctx** ctx, int device);
+
+/* Releases the context and its workspace.  Waits for work the library
+ * enqueued on its last stream.  Null is a no-op. */
+void normpre_destroy(normpre_ctx* ctx);
+
+/* Message of the last failed call on ctx ("" if none).  The string is owned
+ * by the context and valid until the next call on it.  A null ctx yields the
+ * message of the last failed call that had no context (e.g. normpre_init). */
+const char* normpre_last_error(const normpre_ctx* ctx);
+
+/*
+ * Host-only argument check, identical to the one normpre_step() performs
+ * before it launches anything.  Never touches a GPU.  shapes[2*i], shapes[2*i+1]
+ * are rows and cols of matrix i.  On failure the message is copied to msg
+ * (if msg_len > 0, truncated and NUL-terminated).
+ * Errors: INVALID_ARG (variant, num_mats < 0, shapes null, a dimension < 1,
+ * ns_iters outside 1..64, rank < 1, oversample < 0, power_iters outside
+ * 0..8, a non-finite or negative lr/weight decay, a non-finite momentum,
+ * norm_eps <= 0, unknown orientation or flags),
+ * UNSUPPORTED (a dimension above 1 << 20 or a matrix above 2^31 elements;
+ * in the row-active orientation a row longer than 32768 elements; for
+ * NormPre-L a sketch width l = min(active rows, r + o) above 384).
+ */
+int normpre_validate(int variant, int num_mats, const int64_t* shapes,
+                     const normpre_hparams* hp, char* msg, int msg_len);
+
+/*
+ * One NormPre step (Alg. 1) on num_mats matrices.
+ *   variant  : NORMPRE_VARIANT_G or NORMPRE_VARIANT_L
+ *   params   : host array of num_mats device pointers to W (updated in place)
+ *   grads    : host array of num_mats device pointers to G (read only)
+ *   momentum : host array of num_mats device pointers to M (updated in place;
+ *              zero-filled by the caller before the first step, M_0 = 0)
+ *   shapes   : host array of 2*num_mats int64: rows, cols of each matrix
+ *   hp       : hyper-parameters (hp->step is t)
+ *   stream   : a hipStream_t on the context's device (null = default stream)
+ * The sketch of matrix i uses the counter (seed, t, i): its index in this list.
+ * Matrices of equal shape are processed by shared batched launches.
+ * num_mats == 0 is a successful no-op.
+ * Errors: NOT_INITIALIZED, INVALID_ARG (as normpre_validate, plus null
+ * pointer arrays or entries, or W/G/M of one matrix aliasing), UNSUPPORTED,
+ * OOM (workspace growth), HIP_ERROR (a launch or runtime call failed).
+ */
+int normpre_step(normpre_ctx* ctx, int variant, int num_mats,
+                 float* const* params, const float* const* grads,
+                 float* const* momentum, const int64_t* shapes,
+                 const normpre_hparams* hp, void* stream);
+
+/* ---- inspection (tests, benchmarks) -------------------------------------- */
+
+#define NORMPRE_DEBUG_PSI      0  /* float[rows*cols]: fp32 Psi in W layout          */
+#define NORMPRE_DEBUG_T        1  /* float[rows*cols]: NormPre-G output T (W layout)  */
+#define NORMPRE_DEBUG_RITZ     2  /* float[min(r,l)]: Ritz values, descending          */
+#define NORMPRE_DEBUG_NSEL     3  /* int32[1]: |C|, number of selected modes           */
+#define NORMPRE_DEBUG_ELL      4  /* int32[1]: sketch width l                          */
+#define NORMPRE_DEBUG_TNORM2   5  /* float[1]: ||T||_F^2 used for the RMS scaling      */
+#define NORMPRE_DEBUG_ORIENT   6  /* int32[1]: active orientation k of the step        */
+
+/*
+ * Copies intermediate `what` (NORMPRE_DEBUG_*) of matrix `index` of the last
+ * normpre_step() made with NORMPRE_FLAG_DEBUG into host memory at host_out
+ * (capacity in bytes).  Synchronizes the step's stream.  *written receives
+ * the number of bytes copied.
+ * Errors: NOT_INITIALIZED, INVALID_ARG (no debug step recorded, index out of
+ * range, what unknown or not produced by that variant, capacity too small).
+ */
+int normpre_debug_fetch(normpre_ctx* ctx, int index, int what, void* host_out,
+                        int64_t capacity, int64_t* written);
+
+/*
+ * Writes the Gaussian sketch matrix Omega in R^{b x l} of Alg. 2 for counter
+ * (seed, step, matrix_id) as fp32 row-major b x l into device memory dev_out
+ * (b*l floats, caller-owned), on `stream`.  Element (i, j) has linear index
+ * e = j*b + i; Philox4x32-10 (Salmon et al., SC'11) block e >> 2 with counter
+ * (e >> 2, matrix_id, step mod 2^32, step >> 32) and key (seed mod 2^32,
+ * seed >> 32) yields x0..x3; Box-Muller maps (x0, x1) and (x2, x3) to two
+ * normals each with u1 = ((x >> 8) + 1) 2^-24 and u2 = (x >> 8) 2^-24;
+ * element e takes normal e mod 4 of its block.  normpre_step() uses exactly
+ * these values (rounded to fp16).
+ * Errors: INVALID_ARG (null dev_out, b < 1, l < 1), HIP_ERROR.
+ */
+int normpre_sketch_omega(uint64_t seed, int64_t step, int32_t matrix_id,
+                         int64_t b, int32_t l, float* dev_out, void* stream);
+
+/* Kernel classes reported by normpre_kernel_stats(). */
+#define NORMPRE_KCLASS_NORMALIZE   0  /* momentum + tangent + row/col normalization */
+#define NORMPRE_KCLASS_NS_GRAM     1  /* Newton-Schulz A = X X^T                     */
+#define NORMPRE_KCLASS_NS_POLY     2  /* Newton-Schulz B = bA + cA^2                 */
+#define NORMPRE_KCLASS_NS_COMBINE  3  /* Newton-Schulz X <- aX + BX                  */
+#define NORMPRE_KCLASS_G_UPDATE    4  /* RMS scaling + weight update (NormPre-G)     */
+#define NORMPRE_KCLASS_SK_STREAM   5  /* sketch products streaming Psi               */
+#define NORMPRE_KCLASS_SK_SMALL    6  /* Omega, reductions, CholQR, eigensolver      */
+#define NORMPRE_KCLASS_L_APPLY     7  /* localized apply + RMS + weight update       */
+#define NORMPRE_KCLASS_COUNT       8
+
+/*
+ * Per-kernel-class totals since the last reset, over steps made with
+ * NORMPRE_FLAG_TIME_KERNELS: launches, device milliseconds (HIP events on the
+ * step's stream around each launch), algorithmic flops and algorithmic HBM
+ * bytes (the minimum the operation must move; formulas in the design notes).
+ * Synchronizes the last step's stream.  reset != 0 clears the totals after
+ * reading them.  Any output pointer may be null.
+ * Errors: NOT_INITIALIZED, INVALID_ARG (kclass out of range), HIP_ERROR.
+ */
+int normpre_kernel_stats(normpre_ctx* ctx, int kclass, int64_t* launches,
+                         double* device_ms, double* flops, double* bytes,
+                         int reset);
+
+/* Library version string (static storage). */
+const char* normpre_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NORMPRE_H */

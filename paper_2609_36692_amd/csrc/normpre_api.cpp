@@ -1,0 +1,1022 @@
+// Host side of the NormPre C ABI (include/normpre.h): argument validation,
+// grouping of equal shapes into batched launches, the device workspace, and
+// the launch sequence of one optimizer step (Alg. 1 of the paper, with
+// Newton-Schulz for NormPre-G and Alg. 2, the randomized interaction sketch,
+// for NormPre-L).  Every numerical step runs in the gfx950 kernels of this
+// library; nothing here computes on the host.
+#include "../../include/normpre.h"
+#include "np_internal.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <string>
+#include <vector>
+
+using namespace np;
+
+namespace {
+
+thread_local std::string g_noctx_error;
+
+constexpr int64_t kMaxDim = int64_t(1) << 20;
+constexpr int64_t kMaxElems = int64_t(1) << 31;
+constexpr int kMaxRowLen = 32768;   // row-active register kernel limit
+constexpr int kMaxEll = 384;
+constexpr int kColRowChunk = 64;    // rows per block in the column-active pass
+constexpr int kGramChunk = 2048;    // length chunk of the fp64 Gram kernel
+constexpr int kMaxSplits = 16;
+constexpr int kEigSweeps = 30;
+constexpr size_t kGroupBudget = size_t(24) << 30;  // workspace bytes per group
+
+struct Fail {
+    int code;
+    std::string msg;
+};
+
+std::string fmt(const char* f, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, f);
+    vsnprintf(buf, sizeof buf, f, ap);
+    va_end(ap);
+    return buf;
+}
+
+int orientation_of(const normpre_hparams& hp) {
+    if (hp.orientation == NORMPRE_ORIENT_ROW) return 0;
+    if (hp.orientation == NORMPRE_ORIENT_COL) return 1;
+    return (int)(((hp.step % 2) + 2) % 2);
+}
+
+int sketch_width(const normpre_hparams& hp, int64_t active_rows) {
+    return (int)std::min<int64_t>(active_rows, (int64_t)hp.rank + hp.oversample);
+}
+
+// Shared by normpre_validate() and normpre_step().
+Fail validate(int variant, int num_mats, const int64_t* shapes, const normpre_hparams* hp) {
+    if (variant != NORMPRE_VARIANT_G && variant != NORMPRE_VARIANT_L)
+        return {NORMPRE_ERR_INVALID_ARG, fmt("unknown variant %d", variant)};
+    if (num_mats < 0) return {NORMPRE_ERR_INVALID_ARG, "num_mats < 0"};
+    if (!hp) return {NORMPRE_ERR_INVALID_ARG, "hparams is null"};
+    if (num_mats > 0 && !shapes) return {NORMPRE_ERR_INVALID_ARG, "shapes is null"};
+    if (!std::isfinite(hp->lr) || hp->lr < 0.f) return {NORMPRE_ERR_INVALID_ARG, "lr must be finite and >= 0"};
+    if (!std::isfinite(hp->momentum)) return {NORMPRE_ERR_INVALID_ARG, "momentum must be finite"};
+    if (!std::isfinite(hp->weight_decay) || hp->weight_decay < 0.f)
+        return {NORMPRE_ERR_INVALID_ARG, "weight_decay must be finite and >= 0"};
+    if (!std::isfinite(hp->target_rms)) return {NORMPRE_ERR_INVALID_ARG, "target_rms must be finite"};
+    if (!(hp->norm_eps > 0.f) || !std::isfinite(hp->norm_eps))
+        return {NORMPRE_ERR_INVALID_ARG, "norm_eps must be finite and > 0"};
+    if (hp->orientation < 0 || hp->orientation > 2)
+        return {NORMPRE_ERR_INVALID_ARG, fmt("unknown orientation mode %d", hp->orientation)};
+    if (hp->flags & ~(NORMPRE_FLAG_DEBUG | NORMPRE_FLAG_TIME_KERNELS))
+        return {NORMPRE_ERR_INVALID_ARG, fmt("unknown flags 0x%x", hp->flags)};
+    if (variant == NORMPRE_VARIANT_G) {
+        if (hp->ns_iters < 1 || hp->ns_iters > 64)
+            return {NORMPRE_ERR_INVALID_ARG, fmt("ns_iters %d outside 1..64", hp->ns_iters)};
+        for (int i = 0; i < 3; ++i)
+            if (!std::isfinite(hp->ns_coeffs[i])) return {NORMPRE_ERR_INVALID_ARG, "ns_coeffs must be finite"};
+        if (!std::isfinite(hp->ns_eps) || hp->ns_eps < 0.f)
+            return {NORMPRE_ERR_INVALID_ARG, "ns_eps must be finite and >= 0"};
+    } else {
+        if (hp->rank < 1) return {NORMPRE_ERR_INVALID_ARG, fmt("rank %d < 1", hp->rank)};
+        if (hp->oversample < 0) return {NORMPRE_ERR_INVALID_ARG, fmt("oversample %d < 0", hp->oversample)};
+        if (hp->power_iters < 0 || hp->power_iters > 8)
+            return {NORMPRE_ERR_INVALID_ARG, fmt("power_iters %d outside 0..8", hp->power_iters)};
+    }
+    const int k = orientation_of(*hp);
+    for (int i = 0; i < num_mats; ++i) {
+        const int64_t m = shapes[2 * i], n = shapes[2 * i + 1];
+        if (m < 1 || n < 1)
+            return {NORMPRE_ERR_INVALID_ARG, fmt("matrix %d has shape %lld x %lld", i, (long long)m, (long long)n)};
+        if (m > kMaxDim || n > kMaxDim || m * n > kMaxElems)
+            return {NORMPRE_ERR_UNSUPPORTED, fmt("matrix %d (%lld x %lld) is too large", i, (long long)m, (long long)n)};
+        if (k == 0 && n > kMaxRowLen)
+            return {NORMPRE_ERR_UNSUPPORTED,
+                    fmt("matrix %d: row-active rows of %lld elements exceed %d", i, (long long)n, kMaxRowLen)};
+        if (variant == NORMPRE_VARIANT_L) {
+            const int64_t ell = sketch_width(*hp, k == 0 ? m : n);
+            if (ell > kMaxEll)
+                return {NORMPRE_ERR_UNSUPPORTED, fmt("matrix %d: sketch width %lld exceeds %d", i, (long long)ell, kMaxEll)};
+        }
+    }
+    return {NORMPRE_OK, ""};
+}
+
+// -------------------------------------------------------------- timing ---
+struct KStat {
+    int64_t launches = 0;
+    double ms = 0, flops = 0, bytes = 0;
+};
+struct PendingEvent {
+    int kclass;
+    hipEvent_t start, stop;
+    double flops, bytes;
+};
+
+struct DebugMat {
+    int64_t rows = 0, cols = 0;
+    int variant = 0, k = 0, ell = 0, top = 0;
+    float* psi32 = nullptr;    // rows*cols
+    float* t32 = nullptr;      // rows*cols (G)
+    float* scalars = nullptr;  // [0] = ||T||^2, [1] = nsel (as int bits), ritz from [2]
+};
+
+}  // namespace
+
+struct normpre_ctx {
+    int device = 0;
+    std::string err;
+    void* ws = nullptr;
+    size_t ws_bytes = 0;
+    hipStream_t last_stream = nullptr;
+    bool have_stream = false;
+    // debug state of the last step made with NORMPRE_FLAG_DEBUG
+    std::vector<DebugMat> dbg;
+    void* dbg_mem = nullptr;
+    size_t dbg_bytes = 0;
+    bool dbg_valid = false;
+    hipStream_t dbg_stream = nullptr;
+    // per-kernel timing
+    KStat stats[NORMPRE_KCLASS_COUNT];
+    std::vector<PendingEvent> pending;
+    std::vector<hipEvent_t> event_pool;
+    bool timing = false;
+    hipStream_t stream = nullptr;
+};
+
+namespace {
+
+int set_err(normpre_ctx* ctx, int code, const std::string& msg) {
+    if (ctx) ctx->err = msg;
+    else g_noctx_error = msg;
+    return code;
+}
+
+int hip_fail(normpre_ctx* ctx, hipError_t e, const char* what) {
+    return set_err(ctx, NORMPRE_ERR_HIP, fmt("%s: %s", what, hipGetErrorString(e)));
+}
+
+hipEvent_t get_event(normpre_ctx* ctx) {
+    if (!ctx->event_pool.empty()) {
+        hipEvent_t e = ctx->event_pool.back();
+        ctx->event_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// Runs one launch, bracketed by an event pair when kernel timing is on.
+template <class F>
+hipError_t timed(normpre_ctx* ctx, int kclass, double flops, double bytes, F&& launch) {
+    if (!ctx->timing) return launch();
+    hipEvent_t a = get_event(ctx), b = get_event(ctx);
+    if (!a || !b) return hipErrorOutOfMemory;
+    hipError_t e = hipEventRecord(a, ctx->stream);
+    if (e != hipSuccess) return e;
+    e = launch();
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(b, ctx->stream);
+    if (e != hipSuccess) return e;
+    ctx->pending.push_back({kclass, a, b, flops, bytes});
+    return hipSuccess;
+}
+
+int collect_events(normpre_ctx* ctx) {
+    for (auto& p : ctx->pending) {
+        hipError_t e = hipEventSynchronize(p.stop);
+        if (e != hipSuccess) return hip_fail(ctx, e, "hipEventSynchronize");
+        float ms = 0.f;
+        e = hipEventElapsedTime(&ms, p.start, p.stop);
+        if (e != hipSuccess) return hip_fail(ctx, e, "hipEventElapsedTime");
+        KStat& s = ctx->stats[p.kclass];
+        s.launches += 1;
+        s.ms += ms;
+        s.flops += p.flops;
+        s.bytes += p.bytes;
+        ctx->event_pool.push_back(p.start);
+        ctx->event_pool.push_back(p.stop);
+    }
+    ctx->pending.clear();
+    return NORMPRE_OK;
+}
+
+// Bump allocator over the workspace (256-byte aligned slices).
+struct Arena {
+    char* base;
+    size_t off = 0;
+    size_t cap;
+    template <class T>
+    T* take(int64_t count) {
+        off = (off + 255) & ~size_t(255);
+        T* p = reinterpret_cast<T*>(base ? base + off : nullptr);
+        off += (size_t)count * sizeof(T);
+        return p;
+    }
+};
+
+struct Group {
+    int64_t m, n;
+    std::vector<int> idx;   // positions in the caller's list
+};
+
+// Workspace layout of one group; with base == nullptr it only measures.
+struct GWork {
+    // shared
+    half_t* psi;
+    float* psisq;
+    float* scale;
+    double* colpart;
+    // G
+    half_t* xb;
+    half_t* amat;
+    half_t* bmat;
+    float* sumsq;
+    // L
+    half_t* omega;
+    half_t* v16[2];
+    float* v32[2];
+    float* part;
+    double* gpart;
+    double* chol;
+    float* rinv;
+    float* kmat;
+    half_t* qlen;
+    half_t* flen;
+    float* eigs;
+    float* tnorm2;
+    float* ritz;
+    int* nsel;
+};
+
+struct Dims {
+    int64_t m, n, mp, np_, sp, lp_;
+    int k;
+    bool tall;
+    // L
+    int64_t a, b, a_pad, b_pad;
+    int ell, ellp, top;
+};
+
+Dims dims_of(int64_t m, int64_t n, int k, const normpre_hparams& hp) {
+    Dims d;
+    d.m = m;
+    d.n = n;
+    d.mp = round_up(m, kPad);
+    d.np_ = round_up(n, kPad);
+    d.sp = std::min(d.mp, d.np_);
+    d.lp_ = std::max(d.mp, d.np_);
+    d.k = k;
+    d.tall = m > n;
+    d.a = k == 0 ? m : n;
+    d.b = k == 0 ? n : m;
+    d.a_pad = k == 0 ? d.mp : d.np_;
+    d.b_pad = k == 0 ? d.np_ : d.mp;
+    d.ell = sketch_width(hp, d.a);
+    d.ellp = (int)round_up(d.ell, kEllPad);
+    d.top = std::min(hp.rank, d.ell);
+    return d;
+}
+
+int ns_tiles(const Dims& d) { return (int)((d.mp / 128) * (d.np_ / 128)); }
+
+// Split count for a skinny product with output length n_out and reduction length k_len.
+int pick_splits(int64_t tiles_per_mat, int count, int64_t k_len) {
+    int splits = 1;
+    while (splits < kMaxSplits && tiles_per_mat * count * splits < 1024 && k_len / (64 * splits * 2) >= 4)
+        splits *= 2;
+    return splits;
+}
+
+GWork carve(Arena& ar, const Dims& d, int count, int variant) {
+    GWork w{};
+    const int64_t mn = d.mp * d.np_;
+    w.psi = ar.take<half_t>(count * mn);
+    w.psisq = ar.take<float>(count * d.lp_);
+    w.scale = ar.take<float>(count * 2);
+    w.colpart = ar.take<double>(count * normalize_cols_partials((int)d.m, (int)d.np_, kColRowChunk));
+    if (variant == NORMPRE_VARIANT_G) {
+        w.xb = ar.take<half_t>(count * mn);
+        w.amat = ar.take<half_t>(count * d.sp * d.sp);
+        w.bmat = ar.take<half_t>(count * d.sp * d.sp);
+        w.sumsq = ar.take<float>(count * ns_tiles(d));
+    } else {
+        const int64_t lp = d.ellp, maxpad = d.lp_;
+        w.omega = ar.take<half_t>(count * lp * d.b_pad);
+        for (int i = 0; i < 2; ++i) {
+            w.v16[i] = ar.take<half_t>(count * lp * maxpad);
+            w.v32[i] = ar.take<float>(count * lp * maxpad);
+        }
+        w.part = ar.take<float>(count * (int64_t)kMaxSplits * lp * maxpad);
+        w.gpart = ar.take<double>(count * (int64_t)gram64_chunks(maxpad, kGramChunk) * lp * lp);
+        w.chol = ar.take<double>(count * 2 * lp * lp);
+        w.rinv = ar.take<float>(count * lp * lp);
+        w.kmat = ar.take<float>(count * lp * lp);
+        w.qlen = ar.take<half_t>(count * d.a_pad * lp);
+        w.flen = ar.take<half_t>(count * d.b_pad * lp);
+        w.eigs = ar.take<float>(count * 2 * lp * lp);
+        w.tnorm2 = ar.take<float>(count);
+        w.ritz = ar.take<float>(count * (int64_t)d.top);
+        w.nsel = ar.take<int>(count);
+    }
+    return w;
+}
+
+size_t group_bytes(const Dims& d, int count, int variant) {
+    Arena ar{nullptr, 0, 0};
+    carve(ar, d, count, variant);
+    return ar.off + 256;
+}
+
+struct StepCtx {
+    normpre_ctx* ctx;
+    hipStream_t s;
+    const normpre_hparams* hp;
+    float* const* W;
+    const float* const* G;
+    float* const* M;
+    int variant;
+    bool debug;
+};
+
+#define NP_TRY(expr, what)                                  \
+    do {                                                    \
+        hipError_t e__ = (expr);                            \
+        if (e__ != hipSuccess) return hip_fail(sc.ctx, e__, what); \
+    } while (0)
+
+PtrChunk make_chunk(const StepCtx& sc, const std::vector<int>& idx, int begin, int cnt) {
+    PtrChunk p{};
+    for (int i = 0; i < cnt; ++i) {
+        const int g = idx[begin + i];
+        p.w[i] = sc.W[g];
+        p.m[i] = sc.M[g];
+        p.g[i] = sc.G[g];
+    }
+    return p;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+bool chunk_vec_ok(const PtrChunk& p, int cnt) {
+    for (int i = 0; i < cnt; ++i)
+        if (!aligned16(p.w[i]) || !aligned16(p.m[i]) || !aligned16(p.g[i])) return false;
+    return true;
+}
+
+// Momentum + tangent + normalization for `count` matrices starting at
+// position `first` of the group list, writing the group workspace.
+int run_normalize(const StepCtx& sc, const Dims& d, const GWork& w, const std::vector<int>& idx, int first,
+                  int count, DebugMat* dbg) {
+    const int64_t mn = d.mp * d.np_;
+    const double bytes = 18.0 * (double)d.m * (double)d.n;
+    for (int c0 = 0; c0 < count; c0 += kChunk) {
+        const int cnt = std::min(kChunk, count - c0);
+        NormArgs a{};
+        a.ptrs = make_chunk(sc, idx, first + c0, cnt);
+        a.rows = (int)d.m;
+        a.cols = (int)d.n;
+        a.ld_psi = d.np_;
+        a.rows_pad = d.mp;
+        a.psi = w.psi + (int64_t)c0 * mn;
+        a.stride_psi = mn;
+        a.psisq = w.psisq + (int64_t)c0 * d.lp_;
+        a.stride_psisq = d.lp_;
+        a.mu = sc.hp->momentum;
+        a.eps = sc.hp->norm_eps;
+        a.vec_ok = chunk_vec_ok(a.ptrs, cnt);
+        if (dbg) {
+            // Debug copies are written chunk by chunk into per-matrix buffers
+            // that are contiguous in the order of the caller's list.
+            a.psi32 = dbg[idx[first + c0]].psi32;
+            a.stride_psi32 = d.m * d.n;
+            for (int i = 1; i < cnt; ++i)
+                if (dbg[idx[first + c0 + i]].psi32 != a.psi32 + i * d.m * d.n) a.psi32 = nullptr;
+            if (!a.psi32) return set_err(sc.ctx, NORMPRE_ERR_HIP, "internal: debug buffers not contiguous");
+        }
+        if (d.k == 0) {
+            NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NORMALIZE, 0.0, bytes * cnt,
+                         [&] { return launch_normalize_rows(a, cnt, sc.s); }),
+                   "normalize rows");
+        } else {
+            NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NORMALIZE, 0.0, bytes * cnt,
+                         [&] {
+                             return launch_normalize_cols(
+                                 a, cnt,
+                                 w.colpart + (int64_t)c0 * normalize_cols_partials((int)d.m, (int)d.np_, kColRowChunk),
+                                 kColRowChunk, sc.s);
+                         }),
+                   "normalize cols");
+        }
+    }
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+                 [&] {
+                     return launch_psi_scale(w.psisq, d.lp_, (int)d.a, sc.hp->ns_eps, w.scale, count, sc.s);
+                 }),
+           "psi scale");
+    return NORMPRE_OK;
+}
+
+int run_group_g(const StepCtx& sc, const Dims& d, const GWork& w, const std::vector<int>& idx, int first, int count,
+                DebugMat* dbg) {
+    int rc = run_normalize(sc, d, w, idx, first, count, dbg);
+    if (rc) return rc;
+    const normpre_hparams& hp = *sc.hp;
+    const int64_t mn = d.mp * d.np_, ss = d.sp * d.sp;
+    const double s_ = (double)std::min(d.m, d.n), l_ = (double)std::max(d.m, d.n);
+    const int q = hp.ns_iters;
+    half_t* bufs[2] = {w.psi, w.xb};
+    for (int it = 0; it < q; ++it) {
+        half_t* x = bufs[it & 1];
+        half_t* xn = bufs[(it + 1) & 1];
+        const bool first_it = it == 0, last_it = it == q - 1;
+        // A = X X^T (wide) or Y^T Y (tall), times c^2 on the first iteration.
+        {
+            Operand A{x, d.np_, mn}, B{x, d.np_, mn};
+            GemmShape sh{(int)d.sp, (int)d.sp, (int)d.lp_, 1, (int)d.lp_, 1};
+            EpiAffine e{};
+            e.out = w.amat; e.ld_out = d.sp; e.stride_out = ss;
+            e.mul = first_it ? w.scale : nullptr; e.mul_pow = first_it ? 2 : 0;
+            e.ca = 1.f; e.cs = 0.f;
+            const int layout = d.tall ? 2 : 0;
+            NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_GRAM, 2.0 * s_ * s_ * l_ * count,
+                         2.0 * (s_ * l_ + s_ * s_) * count,
+                         [&] { return launch_gemm_affine(TileCfg::Big, layout, A, B, sh, count, e, sc.s); }),
+                   "ns gram");
+        }
+        // B = b A + c A^2
+        {
+            Operand A{w.amat, d.sp, ss}, B{w.amat, d.sp, ss};
+            GemmShape sh{(int)d.sp, (int)d.sp, (int)d.sp, 1, (int)d.sp, 1};
+            EpiAffine e{};
+            e.out = w.bmat; e.ld_out = d.sp; e.stride_out = ss;
+            e.src = w.amat; e.ld_src = d.sp; e.stride_src = ss;
+            e.ca = hp.ns_coeffs[2]; e.cs = hp.ns_coeffs[1];
+            NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_POLY, 2.0 * s_ * s_ * s_ * count, 6.0 * s_ * s_ * count,
+                         [&] { return launch_gemm_affine(TileCfg::Big, 0, A, B, sh, count, e, sc.s); }),
+                   "ns poly");
+        }
+        // X <- a X + B X (wide) or Y <- a Y + Y B (tall), times c on the first iteration.
+        {
+            EpiAffine e{};
+            e.out = xn; e.ld_out = d.np_; e.stride_out = mn;
+            e.src = x; e.ld_src = d.np_; e.stride_src = mn;
+            e.mul = first_it ? w.scale : nullptr; e.mul_pow = first_it ? 1 : 0;
+            e.ca = 1.f; e.cs = hp.ns_coeffs[0];
+            e.sumsq = last_it ? w.sumsq : nullptr;
+            e.tiles_per_mat = ns_tiles(d);
+            hipError_t (*fn)(TileCfg, int, Operand, Operand, GemmShape, int, const EpiAffine&, hipStream_t) =
+                launch_gemm_affine;
+            auto go = [&]() -> hipError_t {
+                if (!d.tall) {
+                    Operand A{w.bmat, d.sp, ss}, B{x, d.np_, mn};
+                    GemmShape sh{(int)d.sp, (int)d.lp_, (int)d.sp, 1, (int)d.sp, 0};
+                    return fn(TileCfg::Big, 1, A, B, sh, count, e, sc.s);
+                }
+                Operand A{x, d.np_, mn}, B{w.bmat, d.sp, ss};
+                GemmShape sh{(int)d.lp_, (int)d.sp, (int)d.sp, 1, (int)d.sp, 0};
+                return fn(TileCfg::Big, 0, A, B, sh, count, e, sc.s);
+            };
+            NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_COMBINE, 2.0 * s_ * s_ * l_ * count,
+                         2.0 * (2.0 * s_ * l_ + s_ * s_) * count, go),
+                   "ns combine");
+        }
+    }
+    const half_t* t = bufs[q & 1];
+    for (int c0 = 0; c0 < count; c0 += kChunk) {
+        const int cnt = std::min(kChunk, count - c0);
+        GUpdateArgs a{};
+        a.ptrs = make_chunk(sc, idx, first + c0, cnt);
+        a.rows = (int)d.m;
+        a.cols = (int)d.n;
+        a.t = t + (int64_t)c0 * mn;
+        a.ld_t = d.np_;
+        a.stride_t = mn;
+        a.sumsq = w.sumsq + (int64_t)c0 * ns_tiles(d);
+        a.tiles_per_mat = ns_tiles(d);
+        a.lr = hp.lr;
+        a.wd = hp.weight_decay;
+        a.target_rms = hp.target_rms;
+        a.vec_ok = chunk_vec_ok(a.ptrs, cnt);
+        if (dbg) {
+            a.t32 = dbg[idx[first + c0]].t32;
+            a.stride_t32 = d.m * d.n;
+            a.tnorm2_out = dbg[idx[first + c0]].scalars;
+        }
+        if (dbg && cnt > 1) {
+            // one matrix per launch keeps the debug pointers simple
+            for (int i = 0; i < cnt; ++i) {
+                GUpdateArgs b = a;
+                PtrChunk pc{};
+                pc.w[0] = a.ptrs.w[i];
+                pc.m[0] = a.ptrs.m[i];
+                pc.g[0] = a.ptrs.g[i];
+                b.ptrs = pc;
+                b.t = a.t + (int64_t)i * mn;
+                b.sumsq = a.sumsq + (int64_t)i * ns_tiles(d);
+                b.t32 = dbg[idx[first + c0 + i]].t32;
+                b.tnorm2_out = dbg[idx[first + c0 + i]].scalars;
+                NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_G_UPDATE, 0.0, 10.0 * d.m * d.n,
+                             [&] { return launch_g_update(b, 1, sc.s); }),
+                       "g update");
+            }
+            continue;
+        }
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_G_UPDATE, 0.0, 10.0 * d.m * d.n * cnt,
+                     [&] { return launch_g_update(a, cnt, sc.s); }),
+               "g update");
+    }
+    return NORMPRE_OK;
+}
+
+// One sketch product over Psi with an l-major fp16 operand V (ell_pad x K):
+// out_over_active = true gives (Psi V)^T (ell_pad x a_pad), false gives
+// (Psi^T V)^T (ell_pad x b_pad).  Writes fp32 and/or scaled fp16 results.
+int sketch_product(const StepCtx& sc, const Dims& d, const GWork& w, int count, const half_t* v16, bool over_active,
+                   float* out32, half_t* out16, float scale16) {
+    const int64_t mn = d.mp * d.np_, lp = d.ellp, maxpad = d.lp_;
+    // PV: out over the rows of the W-layout Psi; PtV: over its columns.
+    const bool pv = over_active == (d.k == 0);
+    const int64_t n_out = pv ? d.mp : d.np_;
+    const int64_t k_len = pv ? d.np_ : d.mp;
+    const TileCfg cfg = lp == 128 ? TileCfg::Skinny128 : TileCfg::Skinny64;
+    const int bm = gemm_tile_m(cfg), bn = gemm_tile_n(cfg);
+    const int64_t tiles = (lp / bm) * (n_out / bn);
+    const int splits = pick_splits(tiles, count, k_len);
+    const int64_t k_chunk = round_up((k_len + splits - 1) / splits, 64);
+    const int real_splits = (int)((k_len + k_chunk - 1) / k_chunk);
+    Operand A{v16, k_len, lp * maxpad};
+    Operand B{w.psi, d.np_, mn};
+    GemmShape sh{(int)lp, (int)n_out, (int)k_len, real_splits, (int)k_chunk, 0};
+    EpiPartial e{};
+    e.out = w.part;
+    e.ld_out = n_out;
+    e.stride_split = lp * n_out;
+    e.stride_mat = (int64_t)kMaxSplits * lp * maxpad;
+    const double flops = 2.0 * d.ell * (double)d.m * (double)d.n * count;
+    const double bytes = 2.0 * (double)d.m * (double)d.n * count;
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_STREAM, flops, bytes,
+                 [&] { return launch_gemm_partial(cfg, pv ? 0 : 1, A, B, sh, count, e, sc.s); }),
+           "sketch product");
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+                 [&] {
+                     return launch_reduce_splits(w.part, real_splits, lp * n_out, (int64_t)kMaxSplits * lp * maxpad,
+                                                 (int)lp, n_out, out32, out16, scale16, lp * maxpad, count, sc.s);
+                 }),
+           "reduce splits");
+    return NORMPRE_OK;
+}
+
+// Cholesky-QR step: V (ell_pad x len fp32, l-major) -> Rinv -> M^T V outputs.
+int cholqr_step(const StepCtx& sc, const Dims& d, const GWork& w, int count, const float* v, int64_t len,
+                float* out32, half_t* out16, half_t* out16t) {
+    const int64_t lp = d.ellp, maxpad = d.lp_;
+    const int chunks = gram64_chunks(len, kGramChunk);
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+                 [&] { return launch_gram64(v, len, lp * maxpad, (int)lp, len, kGramChunk, w.gpart, count, sc.s); }),
+           "gram64");
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+                 [&] { return launch_chol_inv(w.gpart, chunks, d.ell, (int)lp, w.chol, w.rinv, count, sc.s); }),
+           "cholesky");
+    SmallMulArgs a{};
+    a.mat = w.rinv; a.stride_mat = lp * lp;
+    a.v = v; a.ld_v = len; a.stride_v = lp * maxpad;
+    a.ell = d.ell; a.ell_pad = (int)lp; a.len = len; a.len_pad = len;
+    a.out32 = out32; a.stride_out32 = lp * maxpad;
+    a.out16 = out16; a.stride_out16 = lp * maxpad;
+    a.out16t = out16t; a.stride_out16t = len * lp;
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_small_mul(a, count, sc.s); }),
+           "q = y r^-1");
+    return NORMPRE_OK;
+}
+
+float pow2_at_most_inv_sqrt(int64_t a) {
+    // 2^-ceil(log2(sqrt(a))): bounds the growth of one product with Psi.
+    int e = 0;
+    while ((int64_t(1) << (2 * e)) < a) ++e;
+    return std::ldexp(1.f, -e);
+}
+
+int run_group_l(const StepCtx& sc, const Dims& d, const GWork& w, const std::vector<int>& idx, int first, int count,
+                DebugMat* dbg) {
+    int rc = run_normalize(sc, d, w, idx, first, count, dbg);
+    if (rc) return rc;
+    const normpre_hparams& hp = *sc.hp;
+    const int64_t lp = d.ellp, maxpad = d.lp_, mn = d.mp * d.np_;
+    // Omega^T (ell_pad x b_pad), one counter per matrix: its index in the list.
+    for (int c0 = 0; c0 < count; c0 += kChunk) {
+        const int cnt = std::min(kChunk, count - c0);
+        OmegaArgs o{};
+        o.seed = hp.seed;
+        o.step = hp.step;
+        for (int i = 0; i < cnt; ++i) o.ids[i] = idx[first + c0 + i];
+        o.b = (int)d.b;
+        o.ell = d.ell;
+        o.ell_pad = (int)lp;
+        o.ld = d.b_pad;
+        o.out = w.omega + (int64_t)c0 * lp * d.b_pad;
+        o.stride = lp * d.b_pad;
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_omega_f16(o, cnt, sc.s); }),
+               "omega");
+    }
+    // Alg. 2: Y = Psi Omega; p times Y <- Psi (Psi^T Y).  The fp16 copies of
+    // Z and Y are scaled by powers of two (lambda_max <= tr Gamma <= a bounds
+    // each product), which only rescales the spanned subspace.
+    const float sc_step = pow2_at_most_inv_sqrt(d.a);
+    const int p = hp.power_iters;
+    rc = sketch_product(sc, d, w, count, w.omega, true, w.v32[0], p > 0 ? w.v16[0] : nullptr, 1.f);
+    if (rc) return rc;
+    for (int it = 0; it < p; ++it) {
+        rc = sketch_product(sc, d, w, count, w.v16[0], false, nullptr, w.v16[1], sc_step);
+        if (rc) return rc;
+        rc = sketch_product(sc, d, w, count, w.v16[1], true, w.v32[0], it + 1 < p ? w.v16[0] : nullptr, sc_step);
+        if (rc) return rc;
+    }
+    // Q = qr(Y) by two Cholesky-QR passes (fp64 Gram and factorization).
+    rc = cholqr_step(sc, d, w, count, w.v32[0], d.a_pad, w.v32[1], nullptr, nullptr);
+    if (rc) return rc;
+    rc = cholqr_step(sc, d, w, count, w.v32[1], d.a_pad, nullptr, w.v16[0], w.qlen);
+    if (rc) return rc;
+    // B = Q^T Psi (ell_pad x b_pad), Gamma_Q = B B^T, Ritz pairs and selection.
+    rc = sketch_product(sc, d, w, count, w.v16[0], false, w.v32[0], nullptr, 1.f);
+    if (rc) return rc;
+    const int chunks = gram64_chunks(d.b_pad, kGramChunk);
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+                 [&] {
+                     return launch_gram64(w.v32[0], d.b_pad, lp * maxpad, (int)lp, d.b_pad, kGramChunk, w.gpart, count,
+                                          sc.s);
+                 }),
+           "gram64 B");
+    EigArgs ea{};
+    ea.partial = w.gpart; ea.chunks = chunks;
+    ea.ell = d.ell; ea.ell_pad = (int)lp; ea.rank = hp.rank;
+    ea.scratch = w.eigs; ea.kmat = w.kmat;
+    ea.psi_scale = w.scale; ea.tnorm2 = w.tnorm2;
+    ea.ritz = w.ritz; ea.ritz_stride = d.top; ea.nsel = w.nsel;
+    ea.max_sweeps = kEigSweeps;
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_eig_select(ea, count, sc.s); }),
+           "eigensolver");
+    // F = B^T K (b_pad x ell_pad, fp16)
+    {
+        SmallMulArgs a{};
+        a.mat = w.kmat; a.stride_mat = lp * lp;
+        a.v = w.v32[0]; a.ld_v = d.b_pad; a.stride_v = lp * maxpad;
+        a.ell = d.ell; a.ell_pad = (int)lp; a.len = d.b_pad; a.len_pad = d.b_pad;
+        a.out16t = w.flen; a.stride_out16t = d.b_pad * lp;
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_small_mul(a, count, sc.s); }),
+               "f = b^t k");
+    }
+    // T = Psi + L R^T in the W layout, fused with the RMS-matched update.
+    const half_t* L = d.k == 0 ? w.qlen : w.flen;
+    const half_t* R = d.k == 0 ? w.flen : w.qlen;
+    const int64_t l_stride = (d.k == 0 ? d.a_pad : d.b_pad) * lp;
+    const int64_t r_stride = (d.k == 0 ? d.b_pad : d.a_pad) * lp;
+    for (int c0 = 0; c0 < count; c0 += kChunk) {
+        const int cnt = std::min(kChunk, count - c0);
+        Operand A{L + (int64_t)c0 * l_stride, lp, l_stride};
+        Operand B{R + (int64_t)c0 * r_stride, lp, r_stride};
+        GemmShape sh{(int)d.mp, (int)d.np_, (int)lp, 1, (int)lp, 0};
+        EpiApplyUpdate e{};
+        e.psi = w.psi + (int64_t)c0 * mn; e.ld_psi = d.np_; e.stride_psi = mn;
+        e.tnorm2 = w.tnorm2 + c0;
+        e.rows = (int)d.m; e.cols = (int)d.n;
+        e.lr = hp.lr; e.wd = hp.weight_decay; e.target_rms = hp.target_rms;
+        e.ptrs = make_chunk(sc, idx, first + c0, cnt);
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_L_APPLY, 2.0 * d.ell * (double)d.m * d.n * cnt, 10.0 * d.m * d.n * cnt,
+                     [&] { return launch_gemm_apply(A, B, sh, cnt, e, sc.s); }),
+               "apply");
+    }
+    if (dbg) {
+        for (int i = 0; i < count; ++i) {
+            DebugMat& dm = dbg[idx[first + i]];
+            NP_TRY(hipMemcpyAsync(dm.scalars, w.tnorm2 + i, sizeof(float), hipMemcpyDeviceToDevice, sc.s), "dbg");
+            NP_TRY(hipMemcpyAsync(dm.scalars + 1, w.nsel + i, sizeof(int), hipMemcpyDeviceToDevice, sc.s), "dbg");
+            NP_TRY(hipMemcpyAsync(dm.scalars + 2, w.ritz + (int64_t)i * d.top, sizeof(float) * d.top,
+                                  hipMemcpyDeviceToDevice, sc.s),
+                   "dbg");
+        }
+    }
+    return NORMPRE_OK;
+}
+
+int ensure_workspace(normpre_ctx* ctx, size_t bytes, hipStream_t s) {
+    if (bytes <= ctx->ws_bytes) return NORMPRE_OK;
+    if (ctx->ws) {
+        if (ctx->have_stream) (void)hipStreamSynchronize(ctx->last_stream);
+        (void)hipStreamSynchronize(s);
+        (void)hipFree(ctx->ws);
+        ctx->ws = nullptr;
+        ctx->ws_bytes = 0;
+    }
+    const size_t want = bytes + bytes / 8;
+    hipError_t e = hipMalloc(&ctx->ws, want);
+    if (e != hipSuccess) {
+        ctx->ws = nullptr;
+        (void)hipGetLastError();
+        return set_err(ctx, NORMPRE_ERR_OOM, fmt("workspace allocation of %zu bytes failed", want));
+    }
+    ctx->ws_bytes = want;
+    return NORMPRE_OK;
+}
+
+int prepare_debug(normpre_ctx* ctx, int num_mats, const int64_t* shapes, int variant, int k,
+                  const normpre_hparams& hp, hipStream_t s) {
+    size_t need = 0;
+    std::vector<size_t> offs(num_mats);
+    // per-matrix psi32 buffers are laid out contiguously per shape group so a
+    // chunked launch can address them with one stride
+    std::map<std::pair<int64_t, int64_t>, std::vector<int>> by_shape;
+    for (int i = 0; i < num_mats; ++i) by_shape[{shapes[2 * i], shapes[2 * i + 1]}].push_back(i);
+    std::vector<size_t> psi_off(num_mats), t_off(num_mats), sc_off(num_mats);
+    for (auto& kv : by_shape) {
+        const int64_t mn = kv.first.first * kv.first.second;
+        for (int i : kv.second) { psi_off[i] = need; need += (size_t)mn * 4; }
+        for (int i : kv.second) { t_off[i] = need; need += (size_t)mn * 4; }
+        for (int i : kv.second) { sc_off[i] = need; need += (size_t)(2 + kMaxEll) * 4; }
+    }
+    if (need > ctx->dbg_bytes) {
+        if (ctx->dbg_mem) {
+            (void)hipStreamSynchronize(s);
+            (void)hipFree(ctx->dbg_mem);
+            ctx->dbg_mem = nullptr;
+            ctx->dbg_bytes = 0;
+        }
+        if (hipMalloc(&ctx->dbg_mem, need) != hipSuccess) {
+            ctx->dbg_mem = nullptr;
+            (void)hipGetLastError();
+            return set_err(ctx, NORMPRE_ERR_OOM, "debug buffer allocation failed");
+        }
+        ctx->dbg_bytes = need;
+    }
+    ctx->dbg.assign(num_mats, DebugMat{});
+    char* base = static_cast<char*>(ctx->dbg_mem);
+    for (int i = 0; i < num_mats; ++i) {
+        DebugMat& d = ctx->dbg[i];
+        d.rows = shapes[2 * i];
+        d.cols = shapes[2 * i + 1];
+        d.variant = variant;
+        d.k = k;
+        d.ell = sketch_width(hp, k == 0 ? d.rows : d.cols);
+        d.top = std::min(hp.rank, d.ell);
+        d.psi32 = reinterpret_cast<float*>(base + psi_off[i]);
+        d.t32 = reinterpret_cast<float*>(base + t_off[i]);
+        d.scalars = reinterpret_cast<float*>(base + sc_off[i]);
+    }
+    return NORMPRE_OK;
+}
+
+// Detects overlaps between the caller's buffers (W and M are written).
+int check_aliasing(normpre_ctx* ctx, int num_mats, float* const* W, const float* const* G, float* const* M,
+                   const int64_t* shapes) {
+    struct Range {
+        uintptr_t lo, hi;
+        int mat;
+        bool written;
+    };
+    std::vector<Range> r;
+    r.reserve(3 * (size_t)num_mats);
+    for (int i = 0; i < num_mats; ++i) {
+        if (!W[i] || !G[i] || !M[i]) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, fmt("matrix %d has a null pointer", i));
+        const uintptr_t bytes = (uintptr_t)(shapes[2 * i] * shapes[2 * i + 1]) * 4u;
+        r.push_back({(uintptr_t)W[i], (uintptr_t)W[i] + bytes, i, true});
+        r.push_back({(uintptr_t)M[i], (uintptr_t)M[i] + bytes, i, true});
+        r.push_back({(uintptr_t)G[i], (uintptr_t)G[i] + bytes, i, false});
+    }
+    std::sort(r.begin(), r.end(), [](const Range& a, const Range& b) { return a.lo < b.lo; });
+    // Sweep: keep the written range reaching furthest and any range reaching furthest.
+    uintptr_t max_hi_w = 0, max_hi_any = 0;
+    int mat_w = -1, mat_any = -1;
+    for (const Range& x : r) {
+        if (x.written && x.lo < max_hi_any)
+            return set_err(ctx, NORMPRE_ERR_INVALID_ARG,
+                           fmt("buffers of matrices %d and %d overlap (a written buffer is shared)", mat_any, x.mat));
+        if (!x.written && x.lo < max_hi_w)
+            return set_err(ctx, NORMPRE_ERR_INVALID_ARG,
+                           fmt("gradient of matrix %d overlaps a written buffer of matrix %d", x.mat, mat_w));
+        if (x.hi > max_hi_any) { max_hi_any = x.hi; mat_any = x.mat; }
+        if (x.written && x.hi > max_hi_w) { max_hi_w = x.hi; mat_w = x.mat; }
+    }
+    return NORMPRE_OK;
+}
+
+}  // namespace
+
+// =========================================================== C ABI ========
+extern "C" {
+
+const char* normpre_version(void) { return "normpre-mi355x 0.1 (gfx950, fp16 MFMA, fp32 accumulate)"; }
+
+int normpre_default_hparams(normpre_hparams* hp) {
+    if (!hp) return NORMPRE_ERR_INVALID_ARG;
+    std::memset(hp, 0, sizeof *hp);
+    hp->lr = 6e-4f;
+    hp->momentum = 0.95f;
+    hp->weight_decay = 0.1f;
+    hp->target_rms = 0.2f;
+    hp->ns_iters = 5;
+    hp->ns_coeffs[0] = 3.4445f;
+    hp->ns_coeffs[1] = -4.7750f;
+    hp->ns_coeffs[2] = 2.0315f;
+    hp->ns_eps = 1e-7f;
+    hp->rank = 32;
+    hp->oversample = 8;
+    hp->power_iters = 1;
+    hp->orientation = NORMPRE_ORIENT_ALTERNATING;
+    hp->seed = 1337;
+    hp->step = 0;
+    hp->norm_eps = 1e-12f;
+    hp->flags = 0;
+    return NORMPRE_OK;
+}
+
+int normpre_init(normpre_ctx** ctx, int device) {
+    if (!ctx) return set_err(nullptr, NORMPRE_ERR_INVALID_ARG, "ctx is null");
+    *ctx = nullptr;
+    int count = 0;
+    hipError_t e = hipGetDeviceCount(&count);
+    if (e != hipSuccess || device < 0 || device >= count)
+        return set_err(nullptr, NORMPRE_ERR_HIP, fmt("no HIP device %d (%d visible)", device, e == hipSuccess ? count : 0));
+    normpre_ctx* c = new (std::nothrow) normpre_ctx();
+    if (!c) return set_err(nullptr, NORMPRE_ERR_OOM, "context allocation failed");
+    c->device = device;
+    *ctx = c;
+    return NORMPRE_OK;
+}
+
+void normpre_destroy(normpre_ctx* ctx) {
+    if (!ctx) return;
+    int prev = 0;
+    (void)hipGetDevice(&prev);
+    (void)hipSetDevice(ctx->device);
+    if (ctx->have_stream) (void)hipStreamSynchronize(ctx->last_stream);
+    for (auto& p : ctx->pending) {
+        (void)hipEventDestroy(p.start);
+        (void)hipEventDestroy(p.stop);
+    }
+    for (hipEvent_t e : ctx->event_pool) (void)hipEventDestroy(e);
+    if (ctx->ws) (void)hipFree(ctx->ws);
+    if (ctx->dbg_mem) (void)hipFree(ctx->dbg_mem);
+    (void)hipSetDevice(prev);
+    delete ctx;
+}
+
+const char* normpre_last_error(const normpre_ctx* ctx) {
+    return ctx ? ctx->err.c_str() : g_noctx_error.c_str();
+}
+
+int normpre_validate(int variant, int num_mats, const int64_t* shapes, const normpre_hparams* hp, char* msg,
+                     int msg_len) {
+    Fail f = validate(variant, num_mats, shapes, hp);
+    if (msg && msg_len > 0) {
+        std::strncpy(msg, f.msg.c_str(), (size_t)msg_len - 1);
+        msg[msg_len - 1] = '\0';
+    }
+    return f.code;
+}
+
+int normpre_step(normpre_ctx* ctx, int variant, int num_mats, float* const* params, const float* const* grads,
+                 float* const* momentum, const int64_t* shapes, const normpre_hparams* hp, void* stream) {
+    if (!ctx) return set_err(nullptr, NORMPRE_ERR_NOT_INITIALIZED, "context is null");
+    ctx->err.clear();
+    Fail f = validate(variant, num_mats, shapes, hp);
+    if (f.code) return set_err(ctx, f.code, f.msg);
+    if (num_mats == 0) return NORMPRE_OK;
+    if (!params || !grads || !momentum) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "pointer array is null");
+    int rc = check_aliasing(ctx, num_mats, params, grads, momentum, shapes);
+    if (rc) return rc;
+    hipError_t e = hipSetDevice(ctx->device);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+
+    const int k = orientation_of(*hp);
+    // Group equal shapes (first-appearance order) so each group is one batch.
+    std::vector<Group> groups;
+    {
+        std::map<std::pair<int64_t, int64_t>, int> where;
+        for (int i = 0; i < num_mats; ++i) {
+            auto key = std::make_pair(shapes[2 * i], shapes[2 * i + 1]);
+            auto it = where.find(key);
+            if (it == where.end()) {
+                where[key] = (int)groups.size();
+                groups.push_back({key.first, key.second, {i}});
+            } else {
+                groups[it->second].idx.push_back(i);
+            }
+        }
+    }
+    // Sub-batch size per group bounded by a workspace budget; the workspace
+    // is the maximum over sub-batches (they run one after the other).
+    size_t need = 0;
+    std::vector<int> batch_of(groups.size());
+    for (size_t g = 0; g < groups.size(); ++g) {
+        const Dims d = dims_of(groups[g].m, groups[g].n, k, *hp);
+        const int cnt = (int)groups[g].idx.size();
+        const size_t one = group_bytes(d, 1, variant);
+        int b = (int)std::max<size_t>(1, std::min<size_t>((size_t)cnt, kGroupBudget / std::max<size_t>(one, 1)));
+        batch_of[g] = b;
+        need = std::max(need, group_bytes(d, b, variant));
+    }
+    rc = ensure_workspace(ctx, need, s);
+    if (rc) return rc;
+    const bool debug = (hp->flags & NORMPRE_FLAG_DEBUG) != 0;
+    if (debug) {
+        rc = prepare_debug(ctx, num_mats, shapes, variant, k, *hp, s);
+        if (rc) return rc;
+    }
+    ctx->dbg_valid = false;
+    ctx->timing = (hp->flags & NORMPRE_FLAG_TIME_KERNELS) != 0;
+    ctx->stream = s;
+
+    StepCtx sc{ctx, s, hp, params, grads, momentum, variant, debug};
+    for (size_t g = 0; g < groups.size(); ++g) {
+        const Dims d = dims_of(groups[g].m, groups[g].n, k, *hp);
+        const int cnt = (int)groups[g].idx.size();
+        for (int first = 0; first < cnt; first += batch_of[g]) {
+            const int count = std::min(batch_of[g], cnt - first);
+            Arena ar{static_cast<char*>(ctx->ws), 0, ctx->ws_bytes};
+            GWork w = carve(ar, d, count, variant);
+            DebugMat* dbg = debug ? ctx->dbg.data() : nullptr;
+            rc = variant == NORMPRE_VARIANT_G ? run_group_g(sc, d, w, groups[g].idx, first, count, dbg)
+                                              : run_group_l(sc, d, w, groups[g].idx, first, count, dbg);
+            if (rc) return rc;
+        }
+    }
+    ctx->last_stream = s;
+    ctx->have_stream = true;
+    if (debug) {
+        ctx->dbg_valid = true;
+        ctx->dbg_stream = s;
+    }
+    return NORMPRE_OK;
+}
+
+int normpre_debug_fetch(normpre_ctx* ctx, int index, int what, void* host_out, int64_t capacity, int64_t* written) {
+    if (!ctx) return set_err(nullptr, NORMPRE_ERR_NOT_INITIALIZED, "context is null");
+    if (written) *written = 0;
+    if (!ctx->dbg_valid) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "no step with NORMPRE_FLAG_DEBUG recorded");
+    if (index < 0 || index >= (int)ctx->dbg.size()) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "index out of range");
+    if (!host_out) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "host_out is null");
+    const DebugMat& d = ctx->dbg[index];
+    const void* src = nullptr;
+    int64_t bytes = 0;
+    int32_t scalar = 0;
+    switch (what) {
+        case NORMPRE_DEBUG_PSI: src = d.psi32; bytes = d.rows * d.cols * 4; break;
+        case NORMPRE_DEBUG_T:
+            if (d.variant != NORMPRE_VARIANT_G) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "T is kept for NormPre-G only");
+            src = d.t32; bytes = d.rows * d.cols * 4; break;
+        case NORMPRE_DEBUG_RITZ:
+            if (d.variant != NORMPRE_VARIANT_L) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "no Ritz values for NormPre-G");
+            src = d.scalars + 2; bytes = (int64_t)d.top * 4; break;
+        case NORMPRE_DEBUG_NSEL:
+            if (d.variant != NORMPRE_VARIANT_L) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "no selection for NormPre-G");
+            src = d.scalars + 1; bytes = 4; break;
+        case NORMPRE_DEBUG_ELL:
+            if (d.variant != NORMPRE_VARIANT_L) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "no sketch for NormPre-G");
+            scalar = d.ell; bytes = 4; break;
+        case NORMPRE_DEBUG_TNORM2: src = d.scalars; bytes = 4; break;
+        case NORMPRE_DEBUG_ORIENT: scalar = d.k; bytes = 4; break;
+        default: return set_err(ctx, NORMPRE_ERR_INVALID_ARG, fmt("unknown debug item %d", what));
+    }
+    if (capacity < bytes) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, fmt("capacity %lld < %lld bytes", (long long)capacity, (long long)bytes));
+    if (!src) {
+        std::memcpy(host_out, &scalar, 4);
+    } else {
+        hipError_t e = hipSetDevice(ctx->device);
+        if (e == hipSuccess) e = hipStreamSynchronize(ctx->dbg_stream);
+        if (e == hipSuccess) e = hipMemcpy(host_out, src, (size_t)bytes, hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return hip_fail(ctx, e, "debug fetch");
+    }
+    if (written) *written = bytes;
+    return NORMPRE_OK;
+}
+
+int normpre_sketch_omega(uint64_t seed, int64_t step, int32_t matrix_id, int64_t b, int32_t l, float* dev_out,
+                         void* stream) {
+    if (!dev_out || b < 1 || l < 1) return set_err(nullptr, NORMPRE_ERR_INVALID_ARG, "bad omega arguments");
+    hipError_t e = launch_omega_f32(seed, step, matrix_id, b, l, dev_out, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return set_err(nullptr, NORMPRE_ERR_HIP, fmt("omega launch: %s", hipGetErrorString(e)));
+    return NORMPRE_OK;
+}
+
+int normpre_kernel_stats(normpre_ctx* ctx, int kclass, int64_t* launches, double* device_ms, double* flops,
+                         double* bytes, int reset) {
+    if (!ctx) return set_err(nullptr, NORMPRE_ERR_NOT_INITIALIZED, "context is null");
+    if (kclass < 0 || kclass >= NORMPRE_KCLASS_COUNT) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "kclass out of range");
+    int rc = collect_events(ctx);
+    if (rc) return rc;
+    const KStat& s = ctx->stats[kclass];
+    if (launches) *launches = s.launches;
+    if (device_ms) *device_ms = s.ms;
+    if (flops) *flops = s.flops;
+    if (bytes) *bytes = s.bytes;
+    if (reset) ctx->stats[kclass] = KStat{};
+    return NORMPRE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,360 @@
+// Streaming (HBM-bound) kernels of the NormPre step for gfx950:
+//   * momentum + relaxed tangent + diagonal-Gram normalization (Alg. 1;
+//     Sec. 3.1 for the tangent, Eq. 2 for Psi = D(X)^{-1} X), in the
+//     row-active (k = 0) and column-active (k = 1) orientations;
+//   * the Newton-Schulz pre-scale 1 / (||Psi||_F + eps);
+//   * the NormPre-G RMS-matched weight update (Sec. 3.1, "Consistent
+//     Update RMS", and the last line of Alg. 1).
+//
+// Row statistics use one fp64 pass: with d = <m, w>,
+//   ||x||^2 = ||m - d w||^2 = ||m||^2 + d^2 (||w||^2 - 2),
+// so the row (or column) is read once for the three sums and Psi is written
+// from values still held in registers (row-active case) or from a second,
+// cache-friendly pass (column-active case).
+#include "np_internal.h"
+
+namespace np {
+namespace {
+
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+__device__ __forceinline__ float wave_sum_f(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// Block-wide sum of three doubles; result valid in every thread.
+template <int NT>
+__device__ __forceinline__ void block_sum3(double& a, double& b, double& c) {
+    __shared__ double red[3][NT / 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    a = wave_sum_d(a);
+    b = wave_sum_d(b);
+    c = wave_sum_d(c);
+    if (lane == 0) { red[0][wave] = a; red[1][wave] = b; red[2][wave] = c; }
+    __syncthreads();
+    a = b = c = 0.0;
+#pragma unroll
+    for (int w = 0; w < NT / 64; ++w) { a += red[0][w]; b += red[1][w]; c += red[2][w]; }
+}
+
+// ---------------------------------------------------------------------------
+// Row-active orientation: one block per row of W; the row of M and W stays in
+// registers between the statistics and the Psi store.  VW = vector width
+// (4 when cols % 4 == 0), NV = vectors per thread.
+template <int NT, int VW, int NV, bool DBG>
+__global__ void __launch_bounds__(NT) normalize_rows_kernel(NormArgs a) {
+    const int z = blockIdx.y, row = blockIdx.x, tid = threadIdx.x;
+    half_t* prow = a.psi + (int64_t)z * a.stride_psi + (int64_t)row * a.ld_psi;
+    if (row >= a.rows) {
+        for (int64_t j = tid; j < a.ld_psi; j += NT) prow[j] = (half_t)0.f;
+        return;
+    }
+    const int64_t off = (int64_t)row * a.cols;
+    float* W = a.ptrs.w[z] + off;
+    float* M = a.ptrs.m[z] + off;
+    const float* G = a.ptrs.g[z] + off;
+    float mv[NV][VW], wv[NV][VW];
+    double smm = 0.0, smw = 0.0, sww = 0.0;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+        const int idx = (v * NT + tid) * VW;
+        if (idx < a.cols) {
+            if constexpr (VW == 4) {
+                const float4 mp = *reinterpret_cast<const float4*>(M + idx);
+                const float4 g = *reinterpret_cast<const float4*>(G + idx);
+                const float4 w = *reinterpret_cast<const float4*>(W + idx);
+                float4 m;
+                m.x = fmaf(a.mu, mp.x, g.x); m.y = fmaf(a.mu, mp.y, g.y);
+                m.z = fmaf(a.mu, mp.z, g.z); m.w = fmaf(a.mu, mp.w, g.w);
+                *reinterpret_cast<float4*>(M + idx) = m;
+                mv[v][0] = m.x; mv[v][1] = m.y; mv[v][2] = m.z; mv[v][3] = m.w;
+                wv[v][0] = w.x; wv[v][1] = w.y; wv[v][2] = w.z; wv[v][3] = w.w;
+            } else {
+                const float m = fmaf(a.mu, M[idx], G[idx]);
+                M[idx] = m;
+                mv[v][0] = m;
+                wv[v][0] = W[idx];
+            }
+#pragma unroll
+            for (int e = 0; e < VW; ++e) {
+                const double md = mv[v][e], wd = wv[v][e];
+                smm = fma(md, md, smm);
+                smw = fma(md, wd, smw);
+                sww = fma(wd, wd, sww);
+            }
+        }
+    }
+    block_sum3<NT>(smm, smw, sww);
+    const double d = smw;
+    const double nrm2 = fmax(smm + d * d * (sww - 2.0), 0.0);
+    const double nrm = sqrt(nrm2);
+    const float inv = (float)(1.0 / fmax(nrm, (double)a.eps));
+    const float df = (float)d;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+        const int idx = (v * NT + tid) * VW;
+        if (idx < a.cols) {
+            float p[VW];
+#pragma unroll
+            for (int e = 0; e < VW; ++e) p[e] = (mv[v][e] - df * wv[v][e]) * inv;
+            if constexpr (VW == 4) {
+                half_t h[4] = {(half_t)p[0], (half_t)p[1], (half_t)p[2], (half_t)p[3]};
+                *reinterpret_cast<uint2*>(prow + idx) = *reinterpret_cast<const uint2*>(h);
+                if constexpr (DBG)
+                    *reinterpret_cast<float4*>(a.psi32 + (int64_t)z * a.stride_psi32 + off + idx) =
+                        make_float4(p[0], p[1], p[2], p[3]);
+            } else {
+                prow[idx] = (half_t)p[0];
+                if constexpr (DBG) a.psi32[(int64_t)z * a.stride_psi32 + off + idx] = p[0];
+            }
+        }
+    }
+    for (int64_t j = a.cols + tid; j < a.ld_psi; j += NT) prow[j] = (half_t)0.f;
+    if (tid == 0) a.psisq[(int64_t)z * a.stride_psisq + row] = (float)(nrm2 * (double)inv * (double)inv);
+}
+
+// ---------------------------------------------------------------------------
+// Column-active orientation.  Block = 64 columns x 4 row lanes, over a chunk
+// of rows.  Pass 1 updates M and writes fp64 partial column sums; pass 2
+// combines the partials in a fixed order and writes Psi.
+constexpr int kColThreads = 256;
+
+__global__ void __launch_bounds__(kColThreads) normalize_cols_stats(NormArgs a, double* partials, int row_chunk) {
+    const int z = blockIdx.z, chunk = blockIdx.y;
+    const int cx = threadIdx.x & 63, ry = threadIdx.x >> 6;
+    const int col = blockIdx.x * 64 + cx;
+    const int r0 = chunk * row_chunk, r1 = min(a.rows, r0 + row_chunk);
+    double smm = 0.0, smw = 0.0, sww = 0.0;
+    if (col < a.cols) {
+        float* W = a.ptrs.w[z];
+        float* M = a.ptrs.m[z];
+        const float* G = a.ptrs.g[z];
+        for (int i = r0 + ry; i < r1; i += 4) {
+            const int64_t o = (int64_t)i * a.cols + col;
+            const float m = fmaf(a.mu, M[o], G[o]);
+            M[o] = m;
+            const double md = m, wd = W[o];
+            smm = fma(md, md, smm);
+            smw = fma(md, wd, smw);
+            sww = fma(wd, wd, sww);
+        }
+    }
+    __shared__ double red[3][4][64];
+    red[0][ry][cx] = smm; red[1][ry][cx] = smw; red[2][ry][cx] = sww;
+    __syncthreads();
+    if (ry == 0) {
+        const int64_t cols_pad = a.ld_psi;
+        const int nchunks = gridDim.y;
+        double* p = partials + ((int64_t)z * nchunks + chunk) * 3 * cols_pad;
+        if (col < cols_pad) {
+            for (int q = 0; q < 3; ++q)
+                p[q * cols_pad + col] = red[q][0][cx] + red[q][1][cx] + red[q][2][cx] + red[q][3][cx];
+        }
+    }
+}
+
+template <bool DBG>
+__global__ void __launch_bounds__(kColThreads) normalize_cols_apply(NormArgs a, const double* partials, int row_chunk) {
+    const int z = blockIdx.z, chunk = blockIdx.y;
+    const int cx = threadIdx.x & 63, ry = threadIdx.x >> 6;
+    const int col = blockIdx.x * 64 + cx;
+    const int64_t cols_pad = a.ld_psi;
+    const int nchunks = (a.rows + row_chunk - 1) / row_chunk;
+    half_t* P = a.psi + (int64_t)z * a.stride_psi;
+    const int r0 = chunk * row_chunk, r1 = min((int)a.rows_pad, r0 + row_chunk);
+    if (col >= a.cols) {
+        if (col < cols_pad)
+            for (int i = r0 + ry; i < r1; i += 4) P[(int64_t)i * cols_pad + col] = (half_t)0.f;
+        return;
+    }
+    double smm = 0.0, smw = 0.0, sww = 0.0;
+    const double* p = partials + (int64_t)z * nchunks * 3 * cols_pad;
+    for (int c = 0; c < nchunks; ++c) {
+        smm += p[(c * 3 + 0) * cols_pad + col];
+        smw += p[(c * 3 + 1) * cols_pad + col];
+        sww += p[(c * 3 + 2) * cols_pad + col];
+    }
+    const double d = smw;
+    const double nrm2 = fmax(smm + d * d * (sww - 2.0), 0.0);
+    const float inv = (float)(1.0 / fmax(sqrt(nrm2), (double)a.eps));
+    const float df = (float)d;
+    if (chunk == 0 && ry == 0)
+        a.psisq[(int64_t)z * a.stride_psisq + col] = (float)(nrm2 * (double)inv * (double)inv);
+    const float* W = a.ptrs.w[z];
+    const float* M = a.ptrs.m[z];
+    for (int i = r0 + ry; i < r1; i += 4) {
+        float v = 0.f;
+        if (i < a.rows) {
+            const int64_t o = (int64_t)i * a.cols + col;
+            v = (M[o] - df * W[o]) * inv;
+            if constexpr (DBG) a.psi32[(int64_t)z * a.stride_psi32 + o] = v;
+        }
+        P[(int64_t)i * cols_pad + col] = (half_t)v;
+    }
+}
+
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) psi_scale_kernel(const float* psisq, int64_t stride, int active_rows,
+                                                        float eps, float* out) {
+    const int z = blockIdx.x;
+    const float* p = psisq + (int64_t)z * stride;
+    float s = 0.f;
+    for (int i = threadIdx.x; i < active_rows; i += 256) s += p[i];
+    s = wave_sum_f(s);
+    __shared__ float red[4];
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const float tot = red[0] + red[1] + red[2] + red[3];
+        out[2 * z] = 1.f / (sqrtf(tot) + eps);
+        out[2 * z + 1] = tot;
+    }
+}
+
+// ---------------------------------------------------------------------------
+template <int VW, bool DBG>
+__global__ void __launch_bounds__(256) g_update_kernel(GUpdateArgs a) {
+    const int z = blockIdx.y;
+    // ||T||_F^2 from the per-tile partials of the last Newton-Schulz combine,
+    // summed in a fixed order (deterministic).
+    __shared__ float red[4];
+    float s = 0.f;
+    const float* sp = a.sumsq + (int64_t)z * a.tiles_per_mat;
+    for (int i = threadIdx.x; i < a.tiles_per_mat; i += 256) s += sp[i];
+    s = wave_sum_f(s);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+    __syncthreads();
+    const float t2 = red[0] + red[1] + red[2] + red[3];
+    const float scale = t2 > 0.f ? a.target_rms * sqrtf((float)a.rows * (float)a.cols) / sqrtf(t2) : 0.f;
+    if (blockIdx.x == 0 && threadIdx.x == 0 && a.tnorm2_out) a.tnorm2_out[z] = t2;
+
+    float* W = a.ptrs.w[z];
+    const half_t* T = a.t + (int64_t)z * a.stride_t;
+    const int64_t n_vec = (int64_t)a.rows * a.cols / VW;
+    const int vec_per_row = a.cols / VW;
+    for (int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x; v < n_vec; v += (int64_t)gridDim.x * 256) {
+        const int row = (int)(v / vec_per_row);
+        const int c0 = (int)(v - (int64_t)row * vec_per_row) * VW;
+        const half_t* tp = T + (int64_t)row * a.ld_t + c0;
+        float* wp = W + (int64_t)row * a.cols + c0;
+        if constexpr (VW == 4) {
+            const uint2 hraw = *reinterpret_cast<const uint2*>(tp);
+            const half_t* h = reinterpret_cast<const half_t*>(&hraw);
+            float4 w = *reinterpret_cast<float4*>(wp);
+            const float t0 = (float)h[0], t1 = (float)h[1], t2v = (float)h[2], t3 = (float)h[3];
+            w.x = w.x - a.lr * (scale * t0 + a.wd * w.x);
+            w.y = w.y - a.lr * (scale * t1 + a.wd * w.y);
+            w.z = w.z - a.lr * (scale * t2v + a.wd * w.z);
+            w.w = w.w - a.lr * (scale * t3 + a.wd * w.w);
+            *reinterpret_cast<float4*>(wp) = w;
+            if constexpr (DBG)
+                *reinterpret_cast<float4*>(a.t32 + (int64_t)z * a.stride_t32 + (int64_t)row * a.cols + c0) =
+                    make_float4(t0, t1, t2v, t3);
+        } else {
+            const float t = (float)tp[0];
+            const float w = *wp;
+            *wp = w - a.lr * (scale * t + a.wd * w);
+            if constexpr (DBG) a.t32[(int64_t)z * a.stride_t32 + (int64_t)row * a.cols + c0] = t;
+        }
+    }
+}
+
+__global__ void fill_zero_kernel(uint4* p, int64_t n16) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = make_uint4(0, 0, 0, 0);
+}
+
+template <int NT, int VW, int NV>
+hipError_t rows_launch(const NormArgs& a, int batch, hipStream_t s, bool dbg) {
+    dim3 grid((unsigned)a.rows_pad, batch);
+    if (dbg) hipLaunchKernelGGL((normalize_rows_kernel<NT, VW, NV, true>), grid, dim3(NT), 0, s, a);
+    else hipLaunchKernelGGL((normalize_rows_kernel<NT, VW, NV, false>), grid, dim3(NT), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int NT, int VW>
+hipError_t rows_pick_nv(const NormArgs& a, int batch, hipStream_t s, bool dbg) {
+    const int nv = (a.cols + NT * VW - 1) / (NT * VW);
+    if (nv <= 1) return rows_launch<NT, VW, 1>(a, batch, s, dbg);
+    if (nv <= 2) return rows_launch<NT, VW, 2>(a, batch, s, dbg);
+    if (nv <= 4) return rows_launch<NT, VW, 4>(a, batch, s, dbg);
+    if (nv <= 8) return rows_launch<NT, VW, 8>(a, batch, s, dbg);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_normalize_rows(const NormArgs& a, int batch, hipStream_t s) {
+    const bool dbg = a.psi32 != nullptr;
+    const bool vec = a.vec_ok && (a.cols % 4) == 0;
+    if (vec) {
+        if (a.cols <= 256 * 4 * 8) return rows_pick_nv<256, 4>(a, batch, s, dbg);
+        if (a.cols <= 1024 * 4 * 8) return rows_pick_nv<1024, 4>(a, batch, s, dbg);
+    } else {
+        if (a.cols <= 256 * 8) return rows_pick_nv<256, 1>(a, batch, s, dbg);
+        if (a.cols <= 1024 * 8) return rows_pick_nv<1024, 1>(a, batch, s, dbg);
+    }
+    return hipErrorInvalidValue;
+}
+
+int64_t normalize_cols_partials(int rows, int cols_pad, int row_chunk) {
+    const int nchunks = (rows + row_chunk - 1) / row_chunk;
+    return (int64_t)nchunks * 3 * cols_pad;
+}
+
+hipError_t launch_normalize_cols(const NormArgs& a, int batch, double* partials, int row_chunk, hipStream_t s) {
+    const int nchunks = (a.rows + row_chunk - 1) / row_chunk;
+    const int pad_chunks = (int)((a.rows_pad + row_chunk - 1) / row_chunk);
+    const unsigned col_blocks = (unsigned)((a.ld_psi + 63) / 64);
+    hipLaunchKernelGGL(normalize_cols_stats, dim3(col_blocks, nchunks, batch), dim3(kColThreads), 0, s,
+                       a, partials, row_chunk);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (a.psi32)
+        hipLaunchKernelGGL((normalize_cols_apply<true>), dim3(col_blocks, pad_chunks, batch), dim3(kColThreads), 0, s,
+                           a, (const double*)partials, row_chunk);
+    else
+        hipLaunchKernelGGL((normalize_cols_apply<false>), dim3(col_blocks, pad_chunks, batch), dim3(kColThreads), 0, s,
+                           a, (const double*)partials, row_chunk);
+    return hipGetLastError();
+}
+
+hipError_t launch_psi_scale(const float* psisq, int64_t stride, int active_rows, float eps, float* out,
+                            int batch, hipStream_t s) {
+    hipLaunchKernelGGL(psi_scale_kernel, dim3(batch), dim3(256), 0, s, psisq, stride, active_rows, eps, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_g_update(const GUpdateArgs& a, int batch, hipStream_t s) {
+    const int64_t n = (int64_t)a.rows * a.cols;
+    const bool vec = a.vec_ok && (a.cols % 4) == 0;
+    const int64_t work = vec ? n / 4 : n;
+    unsigned blocks = (unsigned)std::min<int64_t>((work + 255) / 256, 2048);
+    if (blocks == 0) blocks = 1;
+    dim3 grid(blocks, batch);
+    const bool dbg = a.t32 != nullptr;
+    if (vec) {
+        if (dbg) hipLaunchKernelGGL((g_update_kernel<4, true>), grid, dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((g_update_kernel<4, false>), grid, dim3(256), 0, s, a);
+    } else {
+        if (dbg) hipLaunchKernelGGL((g_update_kernel<1, true>), grid, dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((g_update_kernel<1, false>), grid, dim3(256), 0, s, a);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t s) {
+    if (bytes <= 0) return hipSuccess;
+    if (bytes % 16 || (reinterpret_cast<uintptr_t>(p) & 15)) return hipErrorInvalidValue;
+    const int64_t n16 = bytes / 16;
+    const unsigned blocks = (unsigned)std::min<int64_t>((n16 + 255) / 256, 4096);
+    hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, s, reinterpret_cast<uint4*>(p), n16);
+    return hipGetLastError();
+}
+
+}  // namespace np

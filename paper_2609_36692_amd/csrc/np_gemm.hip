@@ -1,0 +1,347 @@
+// Batched fp16 x fp16 -> fp32 MFMA GEMMs for gfx950 (v_mfma_f32_16x16x32_f16).
+//
+// One kernel template serves every dense contraction of the NormPre step:
+//   * the Newton-Schulz products A = X X^T, B = bA + cA^2, X <- aX + BX
+//     (NormPre-G, Sec. 3.2; quintic of the Muon iteration),
+//   * the sketch products Psi Omega, Psi^T Y, Psi Z, Q^T Psi of Alg. 2
+//     (NormPre-L, App. B), split along K with fp32 partials,
+//   * the localized apply T = Psi + U_C (Lambda_C^{-1/2} - I) U_C^T Psi
+//     fused with the RMS-matched weight update of Alg. 1.
+//
+// C(mm, nn) = sum_k Aop(mm, k) Bop(nn, k).  Each operand is either K-major
+// (op(r, k) = p[r*ld + k]) or MN-major (op(r, k) = p[k*ld + r]); MN-major
+// tiles are transposed in registers while they are staged into LDS, so the
+// MFMA fragment reads are always 16-byte K-contiguous.  LDS rows are 64
+// halves (128 B) with an XOR swizzle of the 16-byte chunk index, which keeps
+// both the fragment reads and the transposed stores free of bank conflicts.
+// All sizes are multiples of the tile sizes (the workspace is zero padded).
+#include "np_internal.h"
+
+namespace np {
+namespace {
+
+constexpr int BK = 64;
+
+__device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & 7; }
+__device__ __forceinline__ int lds_idx(int row, int chunk) {
+    return row * BK + ((chunk ^ swz(row)) << 3);
+}
+
+// R x 64 K-major tile: each thread moves R*8/NT chunks of 16 bytes.
+template <int R, int NT>
+struct KMajorLoader {
+    static constexpr int N = R * 8 / NT;
+    static_assert(N >= 1 && R * 8 % NT == 0, "tile too small for the block");
+    uint4 r[N];
+    __device__ __forceinline__ void load(const half_t* base, int64_t ld, int row0, int k0, int tid) {
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            const int c = tid + i * NT, row = c >> 3, ch = c & 7;
+            r[i] = *reinterpret_cast<const uint4*>(base + (int64_t)(row0 + row) * ld + k0 + ch * 8);
+        }
+    }
+    __device__ __forceinline__ void store(half_t* lds, int tid) const {
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            const int c = tid + i * NT, row = c >> 3, ch = c & 7;
+            *reinterpret_cast<uint4*>(lds + lds_idx(row, ch)) = r[i];
+        }
+    }
+};
+
+// 64 x R MN-major tile (k rows, r contiguous): each thread loads KR rows of 8
+// consecutive r, transposes the KR x 8 block in registers and writes 8 LDS
+// rows of KR halves.
+template <int R, int NT>
+struct MNMajorLoader {
+    static constexpr int KR = R * 8 / NT;
+    static_assert(KR == 2 || KR == 4 || KR == 8, "unsupported MN-major tile");
+    static constexpr int MB = R / 8;
+    uint4 r[KR];
+    __device__ __forceinline__ void load(const half_t* base, int64_t ld, int row0, int k0, int tid) {
+        const int mblk = tid % MB, kblk = tid / MB;
+#pragma unroll
+        for (int q = 0; q < KR; ++q)
+            r[q] = *reinterpret_cast<const uint4*>(base + (int64_t)(k0 + kblk * KR + q) * ld + row0 + mblk * 8);
+    }
+    __device__ __forceinline__ void store(half_t* lds, int tid) const {
+        const int mblk = tid % MB, kblk = tid / MB;
+        const int kofs = kblk * KR, chunk = kofs >> 3, within = kofs & 7;
+        uint32_t w[KR][4];
+#pragma unroll
+        for (int q = 0; q < KR; ++q) { w[q][0] = r[q].x; w[q][1] = r[q].y; w[q][2] = r[q].z; w[q][3] = r[q].w; }
+#pragma unroll
+        for (int mm = 0; mm < 8; ++mm) {
+            const int d = mm >> 1;
+            const bool hi = mm & 1;
+            uint32_t packed[KR / 2];
+#pragma unroll
+            for (int e = 0; e < KR / 2; ++e) {
+                const uint32_t lo_src = w[2 * e][d], hi_src = w[2 * e + 1][d];
+                packed[e] = hi ? ((lo_src >> 16) | (hi_src & 0xffff0000u))
+                               : ((lo_src & 0xffffu) | (hi_src << 16));
+            }
+            half_t* dst = lds + lds_idx(mblk * 8 + mm, chunk) + within;
+            if constexpr (KR == 8) {
+                *reinterpret_cast<uint4*>(dst) = make_uint4(packed[0], packed[1], packed[2], packed[3]);
+            } else if constexpr (KR == 4) {
+                *reinterpret_cast<uint2*>(dst) = make_uint2(packed[0], packed[1]);
+            } else {
+                *reinterpret_cast<uint32_t*>(dst) = packed[0];
+            }
+        }
+    }
+};
+
+template <bool MN, int R, int NT>
+struct LoaderSel { using type = KMajorLoader<R, NT>; };
+template <int R, int NT>
+struct LoaderSel<true, R, NT> { using type = MNMajorLoader<R, NT>; };
+
+__device__ __forceinline__ void decode_tile(int bid, int tiles_n, int sym, int& tm, int& tn) {
+    if (!sym) {
+        tm = bid / tiles_n;
+        tn = bid - tm * tiles_n;
+        return;
+    }
+    // Upper triangle (tm <= tn), row by row.
+    int row = 0, left = bid;
+    while (left >= tiles_n - row) { left -= tiles_n - row; ++row; }
+    tm = row;
+    tn = row + left;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+template <int BM, int BN, int WM, int WN, int LAYOUT, class Epi>
+__global__ void __launch_bounds__(WM * WN * 64)
+gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
+    constexpr int NT = WM * WN * 64;
+    constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 16, FN = TN / 16;
+    __shared__ __attribute__((aligned(16))) half_t sA[BM * BK];
+    __shared__ __attribute__((aligned(16))) half_t sB[BN * BK];
+    __shared__ float red[NT / 64];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WN, wn = wave - (wave / WN) * WN;
+    const int z = blockIdx.z, split = blockIdx.y;
+    const int tiles_n = sh.N / BN;
+    int tm, tn;
+    decode_tile(blockIdx.x, tiles_n, sh.sym, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int kbeg = split * sh.k_chunk;
+    const int kend = min(sh.K, kbeg + sh.k_chunk);
+
+    const half_t* Ab = A.ptr + (int64_t)z * A.batch_stride;
+    const half_t* Bb = B.ptr + (int64_t)z * B.batch_stride;
+    typename LoaderSel<(LAYOUT == 2), BM, NT>::type la;
+    typename LoaderSel<(LAYOUT >= 1), BN, NT>::type lb;
+
+    f32x4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    if (kbeg < kend) {
+        la.load(Ab, A.ld, m0, kbeg, tid);
+        lb.load(Bb, B.ld, n0, kbeg, tid);
+        la.store(sA, tid);
+        lb.store(sB, tid);
+        __syncthreads();
+        for (int k0 = kbeg; k0 < kend; k0 += BK) {
+            const bool more = k0 + BK < kend;
+            if (more) {
+                la.load(Ab, A.ld, m0, k0 + BK, tid);
+                lb.load(Bb, B.ld, n0, k0 + BK, tid);
+            }
+#pragma unroll
+            for (int s = 0; s < BK / 32; ++s) {
+                f16x8 af[FM], bf[FN];
+                const int chunk = s * 4 + (lane >> 4);
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+                    af[i] = *reinterpret_cast<const f16x8*>(sA + lds_idx(wm * TM + i * 16 + (lane & 15), chunk));
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    bf[j] = *reinterpret_cast<const f16x8*>(sB + lds_idx(wn * TN + j * 16 + (lane & 15), chunk));
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < FN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
+            }
+            __syncthreads();
+            if (more) {
+                la.store(sA, tid);
+                lb.store(sB, tid);
+                __syncthreads();
+            }
+        }
+    }
+
+    // Element (i, j, r) of this lane: row m0 + wm*TM + 16i + 4*(lane/16) + r,
+    // column n0 + wn*TN + 16j + lane%16.
+    const int rbase = m0 + wm * TM + 4 * (lane >> 4);
+    const int cbase = n0 + wn * TN + (lane & 15);
+
+    if constexpr (Epi::kind == EpiKind::Affine) {
+        float mul = 1.f;
+        if (epi.mul && epi.mul_pow > 0) {
+            const float f = epi.mul[2 * z];
+            mul = epi.mul_pow == 1 ? f : f * f;
+        }
+        const float ca = epi.ca * mul, cs = epi.cs * mul;
+        half_t* out = epi.out + (int64_t)z * epi.stride_out;
+        const half_t* src = epi.src ? epi.src + (int64_t)z * epi.stride_src : nullptr;
+        const bool mirror = sh.sym && tm != tn;
+        float ss = 0.f;
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const int col = cbase + j * 16;
+                half_t hv[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int row = rbase + i * 16 + r;
+                    float v = ca * acc[i][j][r];
+                    if (src) v += cs * (float)src[(int64_t)row * epi.ld_src + col];
+                    hv[r] = (half_t)v;
+                    out[(int64_t)row * epi.ld_out + col] = hv[r];
+                    const float q = (float)hv[r];
+                    ss += q * q;
+                }
+                if (mirror) {
+                    half_t* dst = out + (int64_t)col * epi.ld_out + rbase + i * 16;
+                    *reinterpret_cast<uint2*>(dst) = *reinterpret_cast<const uint2*>(hv);
+                }
+            }
+        if (epi.sumsq) {
+            ss = wave_sum(ss);
+            if (lane == 0) red[wave] = ss;
+            __syncthreads();
+            if (tid == 0) {
+                float t = 0.f;
+                for (int w = 0; w < NT / 64; ++w) t += red[w];
+                epi.sumsq[(int64_t)z * epi.tiles_per_mat + blockIdx.x] = t;
+            }
+        }
+    } else if constexpr (Epi::kind == EpiKind::Partial) {
+        float* out = epi.out + (int64_t)z * epi.stride_mat + (int64_t)split * epi.stride_split;
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    out[(int64_t)(rbase + i * 16 + r) * epi.ld_out + cbase + j * 16] = acc[i][j][r];
+    } else {
+        // NormPre-L apply + update.
+        const float t2 = epi.tnorm2[z];
+        const float scale = t2 > 0.f ? epi.target_rms * sqrtf((float)epi.rows * (float)epi.cols) / sqrtf(t2) : 0.f;
+        float* w = epi.ptrs.w[z];
+        const half_t* psi = epi.psi + (int64_t)z * epi.stride_psi;
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const int col = cbase + j * 16;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int row = rbase + i * 16 + r;
+                    if (row < epi.rows && col < epi.cols) {
+                        const float t = (float)psi[(int64_t)row * epi.ld_psi + col] + acc[i][j][r];
+                        float* p = w + (int64_t)row * epi.cols + col;
+                        const float wv = *p;
+                        *p = wv - epi.lr * (scale * t + epi.wd * wv);
+                    }
+                }
+            }
+    }
+}
+
+struct EAff : EpiAffine { static constexpr EpiKind kind = EpiKind::Affine; };
+struct EPar : EpiPartial { static constexpr EpiKind kind = EpiKind::Partial; };
+struct EApp : EpiApplyUpdate { static constexpr EpiKind kind = EpiKind::Apply; };
+
+template <int BM, int BN, int WM, int WN, int LAYOUT, class E>
+hipError_t run(Operand A, Operand B, GemmShape sh, int batch, const E& e, hipStream_t s) {
+    if (sh.M % BM || sh.N % BN || sh.K % BK || sh.k_chunk % BK || batch < 1) return hipErrorInvalidValue;
+    const int tm = sh.M / BM, tn = sh.N / BN;
+    int tiles = tm * tn;
+    if (sh.sym) {
+        if (tm != tn) return hipErrorInvalidValue;
+        tiles = tn * (tn + 1) / 2;
+    }
+    dim3 grid(tiles, sh.k_split, batch);
+    hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, LAYOUT, E>), grid, dim3(WM * WN * 64), 0, s, A, B, sh, e);
+    return hipGetLastError();
+}
+
+template <class E, int LAYOUT>
+hipError_t dispatch_cfg(TileCfg cfg, Operand A, Operand B, GemmShape sh, int batch, const E& e, hipStream_t s) {
+    switch (cfg) {
+        case TileCfg::Big:       return run<128, 128, 2, 2, LAYOUT>(A, B, sh, batch, e, s);
+        case TileCfg::Skinny64:  return run<64, 256, 1, 4, LAYOUT>(A, B, sh, batch, e, s);
+        case TileCfg::Skinny128: return run<128, 256, 2, 2, LAYOUT>(A, B, sh, batch, e, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+int gemm_tile_m(TileCfg cfg) {
+    switch (cfg) {
+        case TileCfg::Big: return 128;
+        case TileCfg::Skinny64: return 64;
+        case TileCfg::Skinny128: return 128;
+        case TileCfg::Apply: return 128;
+    }
+    return 0;
+}
+int gemm_tile_n(TileCfg cfg) {
+    switch (cfg) {
+        case TileCfg::Big: return 128;
+        case TileCfg::Apply: return 128;
+        default: return 256;
+    }
+}
+
+hipError_t launch_gemm_affine(TileCfg cfg, int layout, Operand A, Operand B, GemmShape sh,
+                              int batch, const EpiAffine& e, hipStream_t s) {
+    EAff ee;
+    static_cast<EpiAffine&>(ee) = e;
+    if (cfg != TileCfg::Big) return hipErrorInvalidValue;
+    switch (layout) {
+        case 0: return run<128, 128, 2, 2, 0>(A, B, sh, batch, ee, s);
+        case 1: return run<128, 128, 2, 2, 1>(A, B, sh, batch, ee, s);
+        case 2: return run<128, 128, 2, 2, 2>(A, B, sh, batch, ee, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemm_partial(TileCfg cfg, int layout, Operand A, Operand B, GemmShape sh,
+                               int batch, const EpiPartial& e, hipStream_t s) {
+    EPar ee;
+    static_cast<EpiPartial&>(ee) = e;
+    if (cfg == TileCfg::Big || cfg == TileCfg::Apply) return hipErrorInvalidValue;
+    switch (layout) {
+        case 0: return dispatch_cfg<EPar, 0>(cfg, A, B, sh, batch, ee, s);
+        case 1: return dispatch_cfg<EPar, 1>(cfg, A, B, sh, batch, ee, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemm_apply(Operand A, Operand B, GemmShape sh, int batch,
+                             const EpiApplyUpdate& e, hipStream_t s) {
+    EApp ee;
+    static_cast<EpiApplyUpdate&>(ee) = e;
+    return run<128, 128, 2, 2, 0>(A, B, sh, batch, ee, s);
+}
+
+}  // namespace np

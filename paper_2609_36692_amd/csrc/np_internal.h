@@ -1,0 +1,191 @@
+// Internal declarations shared by the host driver and the gfx950 kernels of
+// the NormPre library.  Not part of the public ABI (that is include/normpre.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace np {
+
+typedef _Float16 half_t;
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Every workspace matrix is padded with zeros to a multiple of this many
+// rows and columns, so the MFMA kernels never see a ragged tile.  Zero
+// padding is exact for every product in the step: padded rows/columns of
+// Psi are zero, and the Newton-Schulz map sends a zero block to zero.
+constexpr int kPad = 256;
+// The sketch width l is padded to a multiple of this (MFMA K granule).
+constexpr int kEllPad = 64;
+
+inline int64_t round_up(int64_t x, int64_t g) { return (x + g - 1) / g * g; }
+
+// Matrices handled by one launch that touches caller memory (W, G, M):
+// pointers travel in the kernel arguments, so no host-to-device copy is
+// ever needed inside a step.
+constexpr int kChunk = 32;
+struct PtrChunk {
+    float* w[kChunk];
+    float* m[kChunk];
+    const float* g[kChunk];
+};
+
+// ---------------------------------------------------------------- GEMM ---
+// C(mm, nn) = sum_k Aop(mm, k) * Bop(nn, k) in fp16 x fp16 -> fp32 MFMA.
+// K-major operand:  op(r, k) = ptr[r * ld + k]
+// MN-major operand: op(r, k) = ptr[k * ld + r]
+struct Operand {
+    const half_t* ptr;
+    int64_t ld;
+    int64_t batch_stride;
+};
+
+struct GemmShape {
+    int M, N, K;        // multiples of the tile sizes / 64
+    int k_split;        // grid.y
+    int k_chunk;        // K range per split, multiple of 64
+    int sym;            // 1: only upper-triangular tiles, mirrored on store
+};
+
+// out = mul^p * (ca * acc + cs * src), stored as fp16; optional mirror for
+// symmetric results and optional per-tile sum of squares of the output.
+struct EpiAffine {
+    half_t* out; int64_t ld_out; int64_t stride_out;
+    const half_t* src; int64_t ld_src; int64_t stride_src;
+    const float* mul; int mul_pow;      // per-matrix factor mul[z]^mul_pow
+    float ca, cs;
+    float* sumsq;                       // [z][tile] partial sums, or null
+    int tiles_per_mat;
+};
+
+// fp32 partial products of one K split: out[z][split][mm][nn]
+struct EpiPartial {
+    float* out; int64_t ld_out; int64_t stride_split; int64_t stride_mat;
+};
+
+// NormPre-L apply: T = Psi + acc in the W layout, then the RMS-matched
+// weight update W <- W - lr (s T + wd W) with s = rms sqrt(mn) / ||T||_F.
+struct EpiApplyUpdate {
+    const half_t* psi; int64_t ld_psi; int64_t stride_psi;
+    const float* tnorm2;                // per matrix ||T||_F^2 (closed form)
+    int rows, cols;                     // real sizes of W
+    float lr, wd, target_rms;
+    PtrChunk ptrs;                      // w[] used
+};
+
+enum class EpiKind { Affine, Partial, Apply };
+
+// Launchers (gemm kernels, np_gemm.hip).  `layout` selects which operands
+// are MN-major: 0 = both K-major, 1 = B MN-major, 2 = both MN-major.
+enum class TileCfg { Big, Skinny64, Skinny128, Apply };
+hipError_t launch_gemm_affine(TileCfg cfg, int layout, Operand A, Operand B,
+                              GemmShape sh, int batch, const EpiAffine& e,
+                              hipStream_t s);
+hipError_t launch_gemm_partial(TileCfg cfg, int layout, Operand A, Operand B,
+                               GemmShape sh, int batch, const EpiPartial& e,
+                               hipStream_t s);
+hipError_t launch_gemm_apply(Operand A, Operand B, GemmShape sh, int batch,
+                             const EpiApplyUpdate& e, hipStream_t s);
+int gemm_tile_m(TileCfg cfg);
+int gemm_tile_n(TileCfg cfg);
+
+// ------------------------------------------------- elementwise kernels ---
+// Momentum + relaxed tangent + diagonal-Gram normalization.
+struct NormArgs {
+    PtrChunk ptrs;
+    int rows, cols;                 // real W sizes
+    int64_t ld_psi;                 // padded row length of the Psi workspace
+    int64_t rows_pad;               // padded row count of the Psi workspace
+    half_t* psi; int64_t stride_psi;   // fp16 Psi, W layout, zero padded
+    float* psi32; int64_t stride_psi32; // optional fp32 copy (debug), ld = cols
+    float* psisq; int64_t stride_psisq; // per active row ||psi_i||^2
+    float mu, eps;
+    int vec_ok;                     // 16-byte aligned W, M, G rows
+};
+hipError_t launch_normalize_rows(const NormArgs& a, int batch, hipStream_t s);
+// Column-active orientation: stats pass + normalize pass.
+hipError_t launch_normalize_cols(const NormArgs& a, int batch, double* partials,
+                                 int row_chunk, hipStream_t s);
+int64_t normalize_cols_partials(int rows, int cols_pad, int row_chunk);
+
+// Per-matrix Newton-Schulz pre-scale c = 1 / (sqrt(sum psisq) + eps) and
+// ||Psi||_F^2: out[z*2] = c, out[z*2+1] = ||Psi||^2.
+hipError_t launch_psi_scale(const float* psisq, int64_t stride, int active_rows,
+                            float eps, float* out, int batch, hipStream_t s);
+
+// NormPre-G final step: ||T||^2 from per-tile partial sums, then
+// W <- W - lr (rms sqrt(mn) T / ||T|| + wd W).
+struct GUpdateArgs {
+    PtrChunk ptrs;
+    int rows, cols;
+    const half_t* t; int64_t ld_t; int64_t stride_t;
+    const float* sumsq; int tiles_per_mat;
+    float lr, wd, target_rms;
+    float* tnorm2_out;              // optional per-matrix ||T||^2 (debug)
+    float* t32; int64_t stride_t32; // optional fp32 copy of T (debug)
+    int vec_ok;                     // 16-byte aligned W rows
+};
+hipError_t launch_g_update(const GUpdateArgs& a, int batch, hipStream_t s);
+
+// ------------------------------------------------------ sketch kernels ---
+// Omega^T (l x b) in fp16, zero padded to (l_pad x b_pad), ld = b_pad.
+struct OmegaArgs {
+    uint64_t seed; int64_t step;
+    int ids[kChunk];            // matrix id (index in the caller's list)
+    int b, ell, ell_pad; int64_t ld;
+    half_t* out; int64_t stride;
+};
+hipError_t launch_omega_f16(const OmegaArgs& a, int batch, hipStream_t s);
+hipError_t launch_omega_f32(uint64_t seed, int64_t step, int id, int64_t b,
+                            int ell, float* out, hipStream_t s);
+
+// Sum of K-split partials -> fp32 (l_pad x len) and scaled fp16 copy.
+hipError_t launch_reduce_splits(const float* part, int splits, int64_t stride_split,
+                                int64_t stride_mat, int rows, int64_t len,
+                                float* out32, half_t* out16, float scale16,
+                                int64_t stride_out, int batch, hipStream_t s);
+
+// fp64 Gram of the rows of an l-major fp32 matrix V (l_pad x len):
+// partial[z][chunk][c][d] = sum_{j in chunk} V[c][j] V[d][j], upper tiles.
+hipError_t launch_gram64(const float* v, int64_t ld, int64_t stride_v, int ell_pad,
+                         int64_t len, int chunk_len, double* partial, int batch,
+                         hipStream_t s);
+int gram64_chunks(int64_t len, int chunk_len);
+
+// Cholesky (with dropping of numerically dependent columns) of the summed
+// Gram, then R^{-1}; writes fp32 Rinv (l_pad x l_pad, zero padded).
+hipError_t launch_chol_inv(const double* partial, int chunks, int ell, int ell_pad,
+                           double* scratch, float* rinv, int batch, hipStream_t s);
+
+// out = M^T V  (M: l_pad x l_pad fp32, V: l_pad x len fp32, l-major),
+// optional outputs: fp32 l-major, fp16 l-major, fp16 len-major (len x l_pad).
+struct SmallMulArgs {
+    const float* mat; int64_t stride_mat;
+    const float* v; int64_t ld_v; int64_t stride_v;
+    int ell, ell_pad; int64_t len, len_pad;
+    float* out32; int64_t stride_out32;          // ld = ld_v
+    half_t* out16; int64_t stride_out16;         // ld = ld_v
+    half_t* out16t; int64_t stride_out16t;       // ld = ell_pad
+};
+hipError_t launch_small_mul(const SmallMulArgs& a, int batch, hipStream_t s);
+
+// Jacobi eigensolver of Gamma_Q (summed fp64 partials), selection of the
+// top-min(r, l) Ritz values > 1, K = Z_C diag(lambda^-1/2 - 1) Z_C^T (fp32,
+// l_pad x l_pad), closed-form ||T||^2 = ||Psi||^2 - sum_C (lambda - 1).
+struct EigArgs {
+    const double* partial; int chunks;
+    int ell, ell_pad, rank;
+    float* scratch;             // 2 * l_pad * l_pad floats per matrix
+    float* kmat;                // l_pad x l_pad per matrix
+    const float* psi_scale;     // [z*2+1] = ||Psi||^2
+    float* tnorm2;              // per matrix
+    float* ritz; int ritz_stride;
+    int* nsel;
+    int max_sweeps;
+};
+hipError_t launch_eig_select(const EigArgs& a, int batch, hipStream_t s);
+
+hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t s);
+
+}  // namespace np

@@ -1,0 +1,449 @@
+// Small and latency-bound kernels of the NormPre-L randomized interaction
+// sketch (Alg. 2, App. B) for gfx950:
+//   * the Gaussian test matrix Omega (Philox4x32-10 of Salmon et al., SC'11,
+//     with the Box-Muller transform),
+//   * the deterministic reduction of K-split partial products,
+//   * fp64 Gram matrices of l-major skinny matrices (for the orthogonal
+//     basis Q = qr(Y) and for the Rayleigh-Ritz matrix Gamma_Q = B B^T),
+//   * Cholesky-QR: Cholesky of the Gram with dropping of numerically
+//     dependent columns, and the triangular inverse,
+//   * small products M^T V with an l x l matrix M,
+//   * a parallel cyclic Jacobi eigensolver for Gamma_Q followed by the
+//     selection of the top-min(r, l) Ritz values above one and the l x l
+//     matrix K = Z_C diag(lambda_C^{-1/2} - 1) Z_C^T.
+#include "np_internal.h"
+
+namespace np {
+namespace {
+
+// ------------------------------------------------------------- Philox ---
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r > 0) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
+        const uint32_t lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
+        const uint32_t lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
+        c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+    }
+    return c;
+}
+
+// Normal variate number e of the stream keyed by (seed, step, id).
+__device__ __forceinline__ float omega_value(uint64_t seed, int64_t step, uint32_t id, int64_t e) {
+    const uint4 ctr = make_uint4((uint32_t)(e >> 2), id, (uint32_t)((uint64_t)step & 0xffffffffu),
+                                 (uint32_t)((uint64_t)step >> 32));
+    const uint4 x = philox4x32_10(ctr, (uint32_t)(seed & 0xffffffffu), (uint32_t)(seed >> 32));
+    const int lane = (int)(e & 3);
+    const uint32_t a = lane < 2 ? x.x : x.z;
+    const uint32_t b = lane < 2 ? x.y : x.w;
+    const float u1 = (float)((a >> 8) + 1u) * 0x1p-24f;
+    const float u2 = (float)(b >> 8) * 0x1p-24f;
+    const float rad = sqrtf(-2.f * logf(u1));
+    float s, c;
+    sincospif(2.f * u2, &s, &c);
+    return (lane & 1) ? rad * s : rad * c;
+}
+
+__global__ void omega_f16_kernel(OmegaArgs a) {
+    const int z = blockIdx.y;
+    const int64_t total = (int64_t)a.ell_pad * a.ld;
+    half_t* out = a.out + (int64_t)z * a.stride;
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        const int c = (int)(idx / a.ld);
+        const int64_t i = idx - (int64_t)c * a.ld;
+        float v = 0.f;
+        if (c < a.ell && i < a.b) v = omega_value(a.seed, a.step, (uint32_t)a.ids[z], (int64_t)c * a.b + i);
+        out[idx] = (half_t)v;
+    }
+}
+
+__global__ void omega_f32_kernel(uint64_t seed, int64_t step, uint32_t id, int64_t b, int ell, float* out) {
+    const int64_t total = b * ell;
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        // out is b x l row-major: out[i*l + j] = Omega_ij, e = j*b + i.
+        const int64_t i = idx / ell, j = idx - i * ell;
+        out[idx] = omega_value(seed, step, id, j * b + i);
+    }
+}
+
+// ------------------------------------------------------ split reduction ---
+__global__ void reduce_splits_kernel(const float* part, int splits, int64_t stride_split, int64_t stride_mat,
+                                     int64_t n4, float* out32, half_t* out16, float scale16, int64_t stride_out) {
+    const int z = blockIdx.y;
+    const float4* p = reinterpret_cast<const float4*>(part + (int64_t)z * stride_mat);
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
+        float4 s = p[i];
+        for (int k = 1; k < splits; ++k) {
+            const float4 q = p[i + k * (stride_split / 4)];
+            s.x += q.x; s.y += q.y; s.z += q.z; s.w += q.w;
+        }
+        if (out32) reinterpret_cast<float4*>(out32 + (int64_t)z * stride_out)[i] = s;
+        if (out16) {
+            half_t h[4] = {(half_t)(s.x * scale16), (half_t)(s.y * scale16), (half_t)(s.z * scale16),
+                           (half_t)(s.w * scale16)};
+            reinterpret_cast<uint2*>(out16 + (int64_t)z * stride_out)[i] = *reinterpret_cast<const uint2*>(h);
+        }
+    }
+}
+
+// ------------------------------------------------------------ fp64 Gram ---
+// 32 x 32 output tile (tc <= td) over one chunk of the length dimension.
+__global__ void __launch_bounds__(256) gram64_kernel(const float* v, int64_t ld, int64_t stride_v, int ell_pad,
+                                                     int64_t len, int chunk_len, double* partial) {
+    const int z = blockIdx.z, chunk = blockIdx.y;
+    const int tiles = ell_pad / 32;
+    int tc = 0, left = blockIdx.x;
+    while (left >= tiles - tc) { left -= tiles - tc; ++tc; }
+    const int td = tc + left;
+    __shared__ float sc[32][65], sd[32][65];
+    const int tid = threadIdx.x, tr = tid >> 4, tcl = tid & 15;
+    const float* vz = v + (int64_t)z * stride_v;
+    double acc[2][2] = {{0.0, 0.0}, {0.0, 0.0}};
+    const int64_t j0 = (int64_t)chunk * chunk_len, j1 = min(len, j0 + chunk_len);
+    for (int64_t jb = j0; jb < j1; jb += 64) {
+        for (int q = tid; q < 32 * 64; q += 256) {
+            const int r = q >> 6, cc = q & 63;
+            const int64_t j = jb + cc;
+            sc[r][cc] = j < j1 ? vz[(int64_t)(tc * 32 + r) * ld + j] : 0.f;
+            sd[r][cc] = j < j1 ? vz[(int64_t)(td * 32 + r) * ld + j] : 0.f;
+        }
+        __syncthreads();
+#pragma unroll 8
+        for (int jj = 0; jj < 64; ++jj) {
+            const double a0 = sc[2 * tr][jj], a1 = sc[2 * tr + 1][jj];
+            const double b0 = sd[2 * tcl][jj], b1 = sd[2 * tcl + 1][jj];
+            acc[0][0] = fma(a0, b0, acc[0][0]);
+            acc[0][1] = fma(a0, b1, acc[0][1]);
+            acc[1][0] = fma(a1, b0, acc[1][0]);
+            acc[1][1] = fma(a1, b1, acc[1][1]);
+        }
+        __syncthreads();
+    }
+    const int nchunks = gridDim.y;
+    double* out = partial + ((int64_t)z * nchunks + chunk) * ell_pad * ell_pad;
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+            out[(int64_t)(tc * 32 + 2 * tr + a) * ell_pad + td * 32 + 2 * tcl + b] = acc[a][b];
+}
+
+// Element (c, d) of the summed Gram (full symmetric view of upper tiles).
+__device__ __forceinline__ double gram_at(const double* p, int chunks, int ell_pad, int c, int d) {
+    if ((c >> 5) > (d >> 5)) { const int t = c; c = d; d = t; }
+    double s = 0.0;
+    for (int k = 0; k < chunks; ++k) s += p[((int64_t)k * ell_pad + c) * ell_pad + d];
+    return s;
+}
+
+// -------------------------------------------------------- Cholesky + inverse
+// One block per matrix.  G = R^T R with R upper triangular; a pivot below
+// kDropTol * G_kk (relative to the column's own squared norm) marks the
+// column as numerically dependent: its row of R and of R^{-1} is zero, so the
+// matching column of Q = Y R^{-1} is zero and it never reaches the selection.
+constexpr double kDropTol = 1e-12;
+
+__global__ void __launch_bounds__(256) chol_inv_kernel(const double* partial, int chunks, int ell, int ell_pad,
+                                                       double* scratch, float* rinv) {
+    const int z = blockIdx.x, tid = threadIdx.x;
+    const double* p = partial + (int64_t)z * chunks * ell_pad * ell_pad;
+    double* R = scratch + (int64_t)z * 2 * ell_pad * ell_pad;
+    double* X = R + (int64_t)ell_pad * ell_pad;
+    float* out = rinv + (int64_t)z * ell_pad * ell_pad;
+    __shared__ double diag0[384];
+    __shared__ double inv_diag[384];
+    for (int q = tid; q < ell * ell; q += 256) {
+        const int c = q / ell, d = q - (q / ell) * ell;
+        R[c * ell_pad + d] = gram_at(p, chunks, ell_pad, c, d);
+    }
+    __syncthreads();
+    for (int k = tid; k < ell; k += 256) diag0[k] = R[k * ell_pad + k];
+    __syncthreads();
+    for (int k = 0; k < ell; ++k) {
+        if (tid == 0) {
+            const double piv = R[k * ell_pad + k];
+            const bool keep = diag0[k] > 0.0 && piv > kDropTol * diag0[k];
+            const double rkk = keep ? sqrt(piv) : 0.0;
+            R[k * ell_pad + k] = rkk;
+            inv_diag[k] = keep ? 1.0 / rkk : 0.0;
+        }
+        __syncthreads();
+        const double ik = inv_diag[k];
+        for (int j = k + 1 + tid; j < ell; j += 256) R[k * ell_pad + j] *= ik;
+        __syncthreads();
+        const int nrem = ell - k - 1;
+        for (int q = tid; q < nrem * nrem; q += 256) {
+            const int i = k + 1 + q / nrem, j = k + 1 + q % nrem;
+            if (j >= i) R[i * ell_pad + j] -= R[k * ell_pad + i] * R[k * ell_pad + j];
+        }
+        __syncthreads();
+    }
+    // X = R^{-1} (upper), row by row from the bottom; rows of dropped pivots stay 0.
+    for (int q = tid; q < ell_pad * ell_pad; q += 256) X[q] = 0.0;
+    __syncthreads();
+    for (int i = ell - 1; i >= 0; --i) {
+        const double ii = inv_diag[i];
+        for (int j = i + tid; j < ell; j += 256) {
+            double s;
+            if (j == i) {
+                s = ii;
+            } else {
+                s = 0.0;
+                for (int k = i + 1; k <= j; ++k) s += R[i * ell_pad + k] * X[k * ell_pad + j];
+                s = -s * ii;
+            }
+            X[i * ell_pad + j] = s;
+        }
+        __syncthreads();
+    }
+    for (int q = tid; q < ell_pad * ell_pad; q += 256) out[q] = (float)X[q];
+}
+
+// ------------------------------------------------------------- M^T V ----
+// Block: 64 columns of V, all l_pad outputs rows in groups of 64.
+__global__ void __launch_bounds__(256) small_mul_kernel(SmallMulArgs a) {
+    const int z = blockIdx.y;
+    const int64_t j0 = (int64_t)blockIdx.x * 64;
+    const int tid = threadIdx.x, jx = tid & 63, cy = tid >> 6;
+    const float* M = a.mat + (int64_t)z * a.stride_mat;
+    const float* V = a.v + (int64_t)z * a.stride_v;
+    __shared__ float sm[64][65];
+    __shared__ float sv[64][65];
+    __shared__ half_t st[64][72];
+    for (int c0 = 0; c0 < a.ell_pad; c0 += 64) {
+        float acc[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+        for (int d0 = 0; d0 < a.ell; d0 += 64) {
+            for (int q = tid; q < 64 * 64; q += 256) {
+                const int r = q >> 6, cc = q & 63;
+                const int d = d0 + r;
+                sm[r][cc] = (d < a.ell && c0 + cc < a.ell_pad) ? M[(int64_t)d * a.ell_pad + c0 + cc] : 0.f;
+                sv[r][cc] = (d < a.ell && j0 + cc < a.len_pad) ? V[(int64_t)d * a.ld_v + j0 + cc] : 0.f;
+            }
+            __syncthreads();
+            for (int dd = 0; dd < 64; ++dd) {
+                const float vv = sv[dd][jx];
+#pragma unroll
+                for (int q = 0; q < 16; ++q) acc[q] = fmaf(sm[dd][cy + 4 * q], vv, acc[q]);
+            }
+            __syncthreads();
+        }
+        const int64_t j = j0 + jx;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            const int c = c0 + cy + 4 * q;
+            if (c < a.ell_pad && j < a.len_pad) {
+                if (a.out32) a.out32[(int64_t)z * a.stride_out32 + (int64_t)c * a.ld_v + j] = acc[q];
+                if (a.out16) a.out16[(int64_t)z * a.stride_out16 + (int64_t)c * a.ld_v + j] = (half_t)acc[q];
+            }
+            st[jx][cy + 4 * q] = (half_t)acc[q];
+        }
+        if (a.out16t) {
+            __syncthreads();
+            // Write rows j of the len-major output: 64 consecutive c per row.
+            for (int q = tid; q < 64 * 64; q += 256) {
+                const int r = q >> 6, cc = q & 63;
+                const int64_t jr = j0 + r;
+                if (jr < a.len_pad && c0 + cc < a.ell_pad)
+                    a.out16t[(int64_t)z * a.stride_out16t + jr * a.ell_pad + c0 + cc] = st[r][cc];
+            }
+        }
+        __syncthreads();
+    }
+}
+
+// ------------------------------------------------------ Jacobi + select --
+constexpr int kEigLdsMax = 84;   // A and Z in LDS when 2 l^2 floats fit
+
+__device__ __forceinline__ void rr_pair(int round, int k, int n2, int& p, int& q) {
+    const int n1 = n2 - 1;
+    if (k == 0) { p = n1; q = round; }
+    else { p = (round + k) % n1; q = (round - k + n1) % n1; }
+    if (p > q) { const int t = p; p = q; q = t; }
+}
+
+__device__ __forceinline__ float block_sum_f(float v, float* red) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    return red[0] + red[1] + red[2] + red[3];
+}
+
+__global__ void __launch_bounds__(256) eig_select_kernel(EigArgs a) {
+    extern __shared__ float dyn[];
+    const int z = blockIdx.x, tid = threadIdx.x;
+    const int n = a.ell, lp = a.ell_pad;
+    float* A = n <= kEigLdsMax ? dyn : a.scratch + (int64_t)z * 2 * lp * lp;
+    float* Z = A + n * n;
+    __shared__ float cs[192], sn[192];
+    __shared__ int pp[192], qq[192];
+    __shared__ float red[4];
+    __shared__ float lam[384], fcoef[384];
+    __shared__ int rnk[384];
+    __shared__ int stop_flag;
+    const double* part = a.partial + (int64_t)z * a.chunks * lp * lp;
+    for (int q = tid; q < n * n; q += 256) {
+        const int c = q / n, d = q - (q / n) * n;
+        A[q] = (float)gram_at(part, a.chunks, lp, c, d);
+        Z[q] = c == d ? 1.f : 0.f;
+    }
+    __syncthreads();
+    const int n2 = n + (n & 1);
+    const int npairs = n2 / 2;
+    for (int sweep = 0; sweep < a.max_sweeps; ++sweep) {
+        float off = 0.f, tot = 0.f;
+        for (int q = tid; q < n * n; q += 256) {
+            const float v = A[q] * A[q];
+            tot += v;
+            if (q / n != q % n) off += v;
+        }
+        off = block_sum_f(off, red);
+        tot = block_sum_f(tot, red);
+        if (tid == 0) stop_flag = !(off > 1e-13f * tot);
+        __syncthreads();
+        if (stop_flag) break;
+        for (int round = 0; round < n2 - 1; ++round) {
+            if (tid < npairs) {
+                int p, q;
+                rr_pair(round, tid, n2, p, q);
+                float c = 1.f, s = 0.f;
+                if (q < n) {
+                    const float apq = A[p * n + q];
+                    const float app = A[p * n + p], aqq = A[q * n + q];
+                    if (fabsf(apq) > 1e-30f && fabsf(apq) > 1e-9f * sqrtf(fabsf(app * aqq))) {
+                        const float theta = (aqq - app) / (2.f * apq);
+                        float t;
+                        if (fabsf(theta) > 1e15f) t = 0.5f / theta;
+                        else t = copysignf(1.f, theta) / (fabsf(theta) + sqrtf(theta * theta + 1.f));
+                        c = 1.f / sqrtf(t * t + 1.f);
+                        s = t * c;
+                    }
+                }
+                cs[tid] = c; sn[tid] = s; pp[tid] = p; qq[tid] = q;
+            }
+            __syncthreads();
+            // rows p, q <- J^T A
+            for (int w = tid; w < npairs * n; w += 256) {
+                const int k = w / n, j = w - (w / n) * n;
+                const int p = pp[k], q = qq[k];
+                if (q >= n) continue;
+                const float c = cs[k], s = sn[k];
+                const float ap = A[p * n + j], aq = A[q * n + j];
+                A[p * n + j] = c * ap - s * aq;
+                A[q * n + j] = s * ap + c * aq;
+            }
+            __syncthreads();
+            // columns p, q <- A J and Z J
+            for (int w = tid; w < npairs * n; w += 256) {
+                const int k = w / n, i = w - (w / n) * n;
+                const int p = pp[k], q = qq[k];
+                if (q >= n) continue;
+                const float c = cs[k], s = sn[k];
+                const float ap = A[i * n + p], aq = A[i * n + q];
+                A[i * n + p] = c * ap - s * aq;
+                A[i * n + q] = s * ap + c * aq;
+                const float zp = Z[i * n + p], zq = Z[i * n + q];
+                Z[i * n + p] = c * zp - s * zq;
+                Z[i * n + q] = s * zp + c * zq;
+            }
+            __syncthreads();
+        }
+    }
+    // Ritz values, descending order with ties to the lower index.
+    for (int i = tid; i < n; i += 256) lam[i] = A[i * n + i];
+    __syncthreads();
+    const int top = min(a.rank, n);
+    for (int i = tid; i < n; i += 256) {
+        const float li = lam[i];
+        int r = 0;
+        for (int j = 0; j < n; ++j) r += (lam[j] > li) || (lam[j] == li && j < i);
+        rnk[i] = r;
+        const bool sel = r < top && li > 1.f;
+        fcoef[i] = sel ? (1.f / sqrtf(li) - 1.f) : 0.f;
+        if (r < top) a.ritz[(int64_t)z * a.ritz_stride + r] = li;
+    }
+    __syncthreads();
+    // K = Z diag(f) Z^T over the selected modes.
+    float* K = a.kmat + (int64_t)z * lp * lp;
+    for (int q = tid; q < lp * lp; q += 256) {
+        const int c = q / lp, d = q - (q / lp) * lp;
+        float s = 0.f;
+        if (c < n && d < n)
+            for (int i = 0; i < n; ++i)
+                if (fcoef[i] != 0.f) s = fmaf(Z[c * n + i] * fcoef[i], Z[d * n + i], s);
+        K[q] = s;
+    }
+    if (tid == 0) {
+        float ssum = 0.f;
+        int cnt = 0;
+        for (int i = 0; i < n; ++i)
+            if (rnk[i] < top && lam[i] > 1.f) { ssum += lam[i] - 1.f; ++cnt; }
+        a.nsel[z] = cnt;
+        a.tnorm2[z] = a.psi_scale[2 * z + 1] - ssum;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_omega_f16(const OmegaArgs& a, int batch, hipStream_t s) {
+    const int64_t total = (int64_t)a.ell_pad * a.ld;
+    const unsigned blocks = (unsigned)std::min<int64_t>((total + 255) / 256, 4096);
+    hipLaunchKernelGGL(omega_f16_kernel, dim3(blocks, batch), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_omega_f32(uint64_t seed, int64_t step, int id, int64_t b, int ell, float* out, hipStream_t s) {
+    const int64_t total = b * ell;
+    const unsigned blocks = (unsigned)std::min<int64_t>((total + 255) / 256, 4096);
+    hipLaunchKernelGGL(omega_f32_kernel, dim3(blocks), dim3(256), 0, s, seed, step, (uint32_t)id, b, ell, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_reduce_splits(const float* part, int splits, int64_t stride_split, int64_t stride_mat, int rows,
+                                int64_t len, float* out32, half_t* out16, float scale16, int64_t stride_out,
+                                int batch, hipStream_t s) {
+    if (len % 4 || stride_split % 4) return hipErrorInvalidValue;
+    const int64_t n4 = (int64_t)rows * len / 4;
+    const unsigned blocks = (unsigned)std::min<int64_t>((n4 + 255) / 256, 2048);
+    hipLaunchKernelGGL(reduce_splits_kernel, dim3(blocks, batch), dim3(256), 0, s, part, splits, stride_split,
+                       stride_mat, n4, out32, out16, scale16, stride_out);
+    return hipGetLastError();
+}
+
+int gram64_chunks(int64_t len, int chunk_len) { return (int)((len + chunk_len - 1) / chunk_len); }
+
+hipError_t launch_gram64(const float* v, int64_t ld, int64_t stride_v, int ell_pad, int64_t len, int chunk_len,
+                         double* partial, int batch, hipStream_t s) {
+    if (ell_pad % 32 || chunk_len % 64) return hipErrorInvalidValue;
+    const int tiles = ell_pad / 32;
+    dim3 grid(tiles * (tiles + 1) / 2, gram64_chunks(len, chunk_len), batch);
+    hipLaunchKernelGGL(gram64_kernel, grid, dim3(256), 0, s, v, ld, stride_v, ell_pad, len, chunk_len, partial);
+    return hipGetLastError();
+}
+
+hipError_t launch_chol_inv(const double* partial, int chunks, int ell, int ell_pad, double* scratch, float* rinv,
+                           int batch, hipStream_t s) {
+    if (ell > 384 || ell_pad > 384) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(chol_inv_kernel, dim3(batch), dim3(256), 0, s, partial, chunks, ell, ell_pad, scratch, rinv);
+    return hipGetLastError();
+}
+
+hipError_t launch_small_mul(const SmallMulArgs& a, int batch, hipStream_t s) {
+    dim3 grid((unsigned)((a.len_pad + 63) / 64), batch);
+    hipLaunchKernelGGL(small_mul_kernel, grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_eig_select(const EigArgs& a, int batch, hipStream_t s) {
+    if (a.ell > 384 || a.ell_pad > 384) return hipErrorInvalidValue;
+    const size_t lds = a.ell <= kEigLdsMax ? (size_t)2 * a.ell * a.ell * sizeof(float) : 0;
+    hipLaunchKernelGGL(eig_select_kernel, dim3(batch), dim3(256), lds, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace np

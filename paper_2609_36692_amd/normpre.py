@@ -1,0 +1,243 @@
+"""ctypes binding of libnormpre (include/normpre.h), same names as the C ABI.
+
+Argument marshalling only: every numerical step runs in the library's gfx950
+kernels.  There is no fallback: if the shared library is missing or cannot
+be loaded, every entry point raises.  Tensors are passed as raw device
+pointers; the stream defaults to torch's current stream.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Sequence
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "lib", "libnormpre.so")
+
+NORMPRE_OK = 0
+NORMPRE_ERR_INVALID_ARG = -1
+NORMPRE_ERR_UNSUPPORTED = -2
+NORMPRE_ERR_OOM = -3
+NORMPRE_ERR_HIP = -4
+NORMPRE_ERR_NOT_INITIALIZED = -5
+
+NORMPRE_VARIANT_G = 0
+NORMPRE_VARIANT_L = 1
+NORMPRE_ORIENT_ALTERNATING = 0
+NORMPRE_ORIENT_ROW = 1
+NORMPRE_ORIENT_COL = 2
+NORMPRE_FLAG_DEBUG = 1
+NORMPRE_FLAG_TIME_KERNELS = 2
+
+NORMPRE_DEBUG_PSI = 0
+NORMPRE_DEBUG_T = 1
+NORMPRE_DEBUG_RITZ = 2
+NORMPRE_DEBUG_NSEL = 3
+NORMPRE_DEBUG_ELL = 4
+NORMPRE_DEBUG_TNORM2 = 5
+NORMPRE_DEBUG_ORIENT = 6
+
+KCLASS_NAMES = ["normalize", "ns_gram", "ns_poly", "ns_combine", "g_update",
+                "sk_stream", "sk_small", "l_apply"]
+
+
+class NormPreError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"normpre error {code}: {msg}")
+        self.code = code
+
+
+class normpre_hparams(ctypes.Structure):
+    _fields_ = [
+        ("lr", ctypes.c_float),
+        ("momentum", ctypes.c_float),
+        ("weight_decay", ctypes.c_float),
+        ("target_rms", ctypes.c_float),
+        ("ns_iters", ctypes.c_int32),
+        ("ns_coeffs", ctypes.c_float * 3),
+        ("ns_eps", ctypes.c_float),
+        ("rank", ctypes.c_int32),
+        ("oversample", ctypes.c_int32),
+        ("power_iters", ctypes.c_int32),
+        ("orientation", ctypes.c_int32),
+        ("seed", ctypes.c_uint64),
+        ("step", ctypes.c_int64),
+        ("norm_eps", ctypes.c_float),
+        ("flags", ctypes.c_uint32),
+    ]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Loads libnormpre.so (once).  Raises if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built: run __graft_entry__.build() first")
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    hpp = ctypes.POINTER(normpre_hparams)
+    sig = {
+        "normpre_default_hparams": (ctypes.c_int, [hpp]),
+        "normpre_init": (ctypes.c_int, [ctypes.POINTER(P), ctypes.c_int]),
+        "normpre_destroy": (None, [P]),
+        "normpre_last_error": (ctypes.c_char_p, [P]),
+        "normpre_validate": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, i64p, hpp, ctypes.c_char_p, ctypes.c_int]),
+        "normpre_step": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int, ctypes.POINTER(P), ctypes.POINTER(P),
+                                        ctypes.POINTER(P), i64p, hpp, P]),
+        "normpre_debug_fetch": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int, P, ctypes.c_int64, i64p]),
+        "normpre_sketch_omega": (ctypes.c_int, [ctypes.c_uint64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int64,
+                                                ctypes.c_int32, P, P]),
+        "normpre_kernel_stats": (ctypes.c_int, [P, ctypes.c_int, i64p, ctypes.POINTER(ctypes.c_double),
+                                                ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
+                                                ctypes.c_int]),
+        "normpre_version": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(code: int, ctx=None):
+    if code != NORMPRE_OK:
+        raise NormPreError(code, normpre_last_error(ctx))
+
+
+def _ptr(x) -> int:
+    if isinstance(x, int):
+        return x
+    return int(x.data_ptr())
+
+
+def _stream_handle(stream):
+    if stream is None:
+        import torch
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+# ---------------------------------------------------------------- entry points
+def normpre_version() -> str:
+    return load_library().normpre_version().decode()
+
+
+def normpre_default_hparams(**overrides) -> normpre_hparams:
+    hp = normpre_hparams()
+    _check(load_library().normpre_default_hparams(ctypes.byref(hp)))
+    for k, v in overrides.items():
+        if k == "ns_coeffs":
+            hp.ns_coeffs = (ctypes.c_float * 3)(*v)
+        else:
+            setattr(hp, k, v)
+    return hp
+
+
+def normpre_init(device: int = 0):
+    ctx = ctypes.c_void_p()
+    _check(load_library().normpre_init(ctypes.byref(ctx), int(device)))
+    return ctx
+
+
+def normpre_destroy(ctx) -> None:
+    if ctx:
+        load_library().normpre_destroy(ctx)
+
+
+def normpre_last_error(ctx=None) -> str:
+    s = load_library().normpre_last_error(ctx)
+    return s.decode() if s else ""
+
+
+def _shapes_array(shapes: Sequence[Sequence[int]]):
+    flat = [int(v) for mn in shapes for v in mn]
+    return (ctypes.c_int64 * max(1, len(flat)))(*flat)
+
+
+def normpre_validate(variant: int, shapes, hp: normpre_hparams):
+    """Host-only check; returns (code, message)."""
+    buf = ctypes.create_string_buffer(512)
+    arr = _shapes_array(shapes) if shapes is not None else None
+    code = load_library().normpre_validate(int(variant), 0 if shapes is None else len(shapes), arr,
+                                           ctypes.byref(hp) if hp is not None else None, buf, 512)
+    return code, buf.value.decode()
+
+
+def normpre_step(ctx, variant: int, params, grads, momentum, hp: normpre_hparams, stream=None,
+                 shapes=None) -> None:
+    """One NormPre step on lists of fp32 device tensors (or raw pointers + shapes)."""
+    n = len(params)
+    if shapes is None:
+        shapes = [tuple(p.shape) for p in params]
+    P = ctypes.c_void_p
+    pw = (P * max(1, n))(*[_ptr(x) for x in params])
+    pg = (P * max(1, n))(*[_ptr(x) for x in grads])
+    pm = (P * max(1, n))(*[_ptr(x) for x in momentum])
+    code = load_library().normpre_step(ctx, int(variant), n, pw, pg, pm, _shapes_array(shapes),
+                                       ctypes.byref(hp), _stream_handle(stream))
+    _check(code, ctx)
+
+
+def normpre_debug_fetch(ctx, index: int, what: int, count: int, dtype=np.float32) -> np.ndarray:
+    out = np.empty(count, dtype=dtype)
+    written = ctypes.c_int64()
+    code = load_library().normpre_debug_fetch(ctx, int(index), int(what), out.ctypes.data_as(ctypes.c_void_p),
+                                              out.nbytes, ctypes.byref(written))
+    _check(code, ctx)
+    return out[: written.value // out.itemsize]
+
+
+def normpre_sketch_omega(seed: int, step: int, matrix_id: int, b: int, ell: int, out, stream=None) -> None:
+    code = load_library().normpre_sketch_omega(ctypes.c_uint64(seed), int(step), int(matrix_id), int(b), int(ell),
+                                               ctypes.c_void_p(_ptr(out)), _stream_handle(stream))
+    _check(code)
+
+
+def normpre_kernel_stats(ctx, kclass: int, reset: bool = False) -> dict:
+    launches = ctypes.c_int64()
+    ms, flops, nbytes = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    code = load_library().normpre_kernel_stats(ctx, int(kclass), ctypes.byref(launches), ctypes.byref(ms),
+                                               ctypes.byref(flops), ctypes.byref(nbytes), int(bool(reset)))
+    _check(code, ctx)
+    return {"launches": launches.value, "ms": ms.value, "flops": flops.value, "bytes": nbytes.value}
+
+
+class NormPre:
+    """Small stateful wrapper: one context, momentum buffers and step counter
+    for a list of 2-D fp32 CUDA/HIP tensors (the hidden weight matrices)."""
+
+    def __init__(self, params, variant: str = "G", device: int | None = None, **hparams):
+        import torch
+        self.params = list(params)
+        self.variant = NORMPRE_VARIANT_G if variant.upper() == "G" else NORMPRE_VARIANT_L
+        dev = self.params[0].device.index if device is None else device
+        self.ctx = normpre_init(0 if dev is None else dev)
+        self.hp = normpre_default_hparams(**hparams)
+        self.momentum = [torch.zeros_like(p) for p in self.params]
+        self.t = int(hparams.get("step", 0))
+
+    def step(self, grads, stream=None):
+        self.hp.step = self.t
+        normpre_step(self.ctx, self.variant, self.params, grads, self.momentum, self.hp, stream)
+        self.t += 1
+
+    def close(self):
+        normpre_destroy(self.ctx)
+        self.ctx = None
+
+    def __del__(self):
+        try:
+            if getattr(self, "ctx", None):
+                self.close()
+        except Exception:
+            pass

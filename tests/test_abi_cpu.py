@@ -1,0 +1,134 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads and
+exports every function include/normpre.h declares, the defaults follow the
+paper's optimizer table, and argument validation returns the documented
+codes without touching a device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "normpre.h")
+
+
+@pytest.fixture(scope="module")
+def N():
+    from paper_2609_36692_amd import normpre
+    if not os.path.exists(normpre.LIB_PATH):
+        from paper_2609_36692_amd import _build
+        _build.build_library()
+    normpre.load_library()
+    return normpre
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(normpre_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_entry_points():
+    names = _declared_functions()
+    for required in ("normpre_init", "normpre_step", "normpre_destroy", "normpre_last_error"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol(N):
+    lib = ctypes.CDLL(N.LIB_PATH)
+    missing = [n for n in _declared_functions() if not hasattr(lib, n)]
+    assert not missing, f"not exported: {missing}"
+
+
+def test_hparams_layout_matches_header(N):
+    # The struct as the C library sees it: defaults written by C, read by ctypes.
+    hp = N.normpre_default_hparams()
+    assert abs(hp.lr - 6e-4) < 1e-9
+    assert abs(hp.momentum - 0.95) < 1e-7
+    assert abs(hp.weight_decay - 0.1) < 1e-7
+    assert abs(hp.target_rms - 0.2) < 1e-7
+    assert hp.ns_iters == 5
+    assert [round(c, 4) for c in hp.ns_coeffs] == [3.4445, -4.775, 2.0315]
+    assert (hp.rank, hp.oversample, hp.power_iters) == (32, 8, 1)
+    assert hp.seed == 1337 and hp.step == 0 and hp.flags == 0
+    assert ctypes.sizeof(N.normpre_hparams) == 80
+
+
+def test_version(N):
+    assert "gfx950" in N.normpre_version()
+
+
+@pytest.mark.parametrize("variant,shapes,over,code", [
+    (0, [(768, 2304)], {}, 0),
+    (1, [(768, 2304), (3072, 768)], {}, 0),
+    (2, [(8, 8)], {}, -1),
+    (0, [(0, 8)], {}, -1),
+    (0, [(8, -1)], {}, -1),
+    (0, [(8, 8)], {"ns_iters": 0}, -1),
+    (0, [(8, 8)], {"ns_iters": 65}, -1),
+    (1, [(8, 8)], {"rank": 0}, -1),
+    (1, [(8, 8)], {"oversample": -1}, -1),
+    (1, [(8, 8)], {"power_iters": 9}, -1),
+    (0, [(8, 8)], {"lr": float("nan")}, -1),
+    (0, [(8, 8)], {"lr": -1.0}, -1),
+    (0, [(8, 8)], {"weight_decay": float("inf")}, -1),
+    (0, [(8, 8)], {"norm_eps": 0.0}, -1),
+    (0, [(8, 8)], {"orientation": 3}, -1),
+    (0, [(8, 8)], {"flags": 8}, -1),
+    (0, [(8, 40000)], {}, -2),                       # row-active row too long
+    (0, [(8, 40000)], {"orientation": 2}, 0),        # column-active is fine
+    (0, [(8, 40000)], {"step": 1}, 0),               # t odd -> column-active
+    (1, [(1024, 1024)], {"rank": 400}, -2),          # sketch width above 384
+    (1, [(100, 1024)], {"rank": 400}, 0),            # l = min(100, 408)
+    (0, [(1 << 21, 4)], {"orientation": 2}, -2),
+    (0, [], {}, 0),
+])
+def test_validate_codes(N, variant, shapes, over, code):
+    hp = N.normpre_default_hparams(**over)
+    got, msg = N.normpre_validate(variant, shapes, hp)
+    assert got == code, msg
+    if code:
+        assert msg
+
+
+def test_validate_null_arguments(N):
+    lib = N.load_library()
+    hp = N.normpre_default_hparams()
+    assert lib.normpre_validate(0, 1, None, ctypes.byref(hp), None, 0) == N.NORMPRE_ERR_INVALID_ARG
+    assert lib.normpre_validate(0, 0, None, None, None, 0) == N.NORMPRE_ERR_INVALID_ARG
+    assert lib.normpre_validate(0, -1, None, ctypes.byref(hp), None, 0) == N.NORMPRE_ERR_INVALID_ARG
+
+
+def test_entry_points_reject_null_context(N):
+    lib = N.load_library()
+    hp = N.normpre_default_hparams()
+    assert lib.normpre_step(None, 0, 0, None, None, None, None, ctypes.byref(hp), None) == \
+        N.NORMPRE_ERR_NOT_INITIALIZED
+    assert "null" in N.normpre_last_error(None)
+    assert lib.normpre_debug_fetch(None, 0, 0, None, 0, None) == N.NORMPRE_ERR_NOT_INITIALIZED
+    assert lib.normpre_kernel_stats(None, 0, None, None, None, None, 0) == N.NORMPRE_ERR_NOT_INITIALIZED
+    assert lib.normpre_init(None, 0) == N.NORMPRE_ERR_INVALID_ARG
+    lib.normpre_destroy(None)   # no-op
+    assert lib.normpre_sketch_omega(1, 0, 0, 10, 4, None, None) == N.NORMPRE_ERR_INVALID_ARG
+
+
+def test_init_without_gpu_reports_hip_error(N):
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    ctx = ctypes.c_void_p()
+    assert N.load_library().normpre_init(ctypes.byref(ctx), 0) == N.NORMPRE_ERR_HIP
+    assert not ctx.value
+    assert "device" in N.normpre_last_error(None)
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    from paper_2609_36692_amd import normpre
+    with pytest.raises(RuntimeError):
+        # A fresh load from a path with no library must raise, never fall back.
+        saved = normpre._lib
+        normpre._lib = None
+        try:
+            normpre.load_library(str(tmp_path / "missing.so"))
+        finally:
+            normpre._lib = saved
