@@ -236,7 +236,8 @@ struct GWork {
     half_t* xb;
     half_t* amat;
     half_t* bmat;
-    float* sumsq;
+    float* sumsq;           // per-tile partial sums of T^2 (both variants)
+    float* tn2;             // per-matrix ||T||_F^2
     // L
     half_t* omega;
     half_t* v16[2];
@@ -249,7 +250,6 @@ struct GWork {
     half_t* qlen;
     half_t* flen;
     float* eigs;
-    float* tnorm2;
     float* ritz;
     int* nsel;
 };
@@ -300,14 +300,17 @@ GWork carve(Arena& ar, const Dims& d, int count, int variant) {
     w.psisq = ar.take<float>(count * d.lp_);
     w.scale = ar.take<float>(count * 2);
     w.colpart = ar.take<double>(count * normalize_cols_partials((int)d.m, (int)d.np_, kColRowChunk));
+    w.sumsq = ar.take<float>(count * ns_tiles(d));
+    w.tn2 = ar.take<float>(count);
     if (variant == NORMPRE_VARIANT_G) {
         w.xb = ar.take<half_t>(count * mn);
         w.amat = ar.take<half_t>(count * d.sp * d.sp);
         w.bmat = ar.take<half_t>(count * d.sp * d.sp);
-        w.sumsq = ar.take<float>(count * ns_tiles(d));
     } else {
         const int64_t lp = d.ellp, maxpad = d.lp_;
-        w.omega = ar.take<half_t>(count * lp * d.b_pad);
+        // Every l-major skinny buffer (Omega^T included) has the per-matrix
+        // stride lp * maxpad that the sketch products assume.
+        w.omega = ar.take<half_t>(count * lp * maxpad);
         for (int i = 0; i < 2; ++i) {
             w.v16[i] = ar.take<half_t>(count * lp * maxpad);
             w.v32[i] = ar.take<float>(count * lp * maxpad);
@@ -320,7 +323,6 @@ GWork carve(Arena& ar, const Dims& d, int count, int variant) {
         w.qlen = ar.take<half_t>(count * d.a_pad * lp);
         w.flen = ar.take<half_t>(count * d.b_pad * lp);
         w.eigs = ar.take<float>(count * 2 * lp * lp);
-        w.tnorm2 = ar.take<float>(count);
         w.ritz = ar.take<float>(count * (int64_t)d.top);
         w.nsel = ar.take<int>(count);
     }
@@ -488,6 +490,9 @@ int run_group_g(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
         }
     }
     const half_t* t = bufs[q & 1];
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+                 [&] { return launch_sum_partials(w.sumsq, ns_tiles(d), w.tn2, count, sc.s); }),
+           "t norm");
     for (int c0 = 0; c0 < count; c0 += kChunk) {
         const int cnt = std::min(kChunk, count - c0);
         GUpdateArgs a{};
@@ -497,8 +502,7 @@ int run_group_g(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
         a.t = t + (int64_t)c0 * mn;
         a.ld_t = d.np_;
         a.stride_t = mn;
-        a.sumsq = w.sumsq + (int64_t)c0 * ns_tiles(d);
-        a.tiles_per_mat = ns_tiles(d);
+        a.tnorm2 = w.tn2 + c0;
         a.lr = hp.lr;
         a.wd = hp.weight_decay;
         a.target_rms = hp.target_rms;
@@ -506,7 +510,10 @@ int run_group_g(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
         if (dbg) {
             a.t32 = dbg[idx[first + c0]].t32;
             a.stride_t32 = d.m * d.n;
-            a.tnorm2_out = dbg[idx[first + c0]].scalars;
+            for (int i = 0; i < cnt; ++i)
+                NP_TRY(hipMemcpyAsync(dbg[idx[first + c0 + i]].scalars, w.tn2 + c0 + i, sizeof(float),
+                                      hipMemcpyDeviceToDevice, sc.s),
+                       "dbg");
         }
         if (dbg && cnt > 1) {
             // one matrix per launch keeps the debug pointers simple
@@ -518,9 +525,8 @@ int run_group_g(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
                 pc.g[0] = a.ptrs.g[i];
                 b.ptrs = pc;
                 b.t = a.t + (int64_t)i * mn;
-                b.sumsq = a.sumsq + (int64_t)i * ns_tiles(d);
+                b.tnorm2 = a.tnorm2 + i;
                 b.t32 = dbg[idx[first + c0 + i]].t32;
-                b.tnorm2_out = dbg[idx[first + c0 + i]].scalars;
                 NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_G_UPDATE, 0.0, 10.0 * d.m * d.n,
                              [&] { return launch_g_update(b, 1, sc.s); }),
                        "g update");
@@ -619,8 +625,8 @@ int run_group_l(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
         o.ell = d.ell;
         o.ell_pad = (int)lp;
         o.ld = d.b_pad;
-        o.out = w.omega + (int64_t)c0 * lp * d.b_pad;
-        o.stride = lp * d.b_pad;
+        o.out = w.omega + (int64_t)c0 * lp * maxpad;
+        o.stride = lp * maxpad;
         NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_omega_f16(o, cnt, sc.s); }),
                "omega");
     }
@@ -656,7 +662,6 @@ int run_group_l(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
     ea.partial = w.gpart; ea.chunks = chunks;
     ea.ell = d.ell; ea.ell_pad = (int)lp; ea.rank = hp.rank;
     ea.scratch = w.eigs; ea.kmat = w.kmat;
-    ea.psi_scale = w.scale; ea.tnorm2 = w.tnorm2;
     ea.ritz = w.ritz; ea.ritz_stride = d.top; ea.nsel = w.nsel;
     ea.max_sweeps = kEigSweeps;
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_eig_select(ea, count, sc.s); }),
@@ -676,6 +681,23 @@ int run_group_l(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
     const half_t* R = d.k == 0 ? w.flen : w.qlen;
     const int64_t l_stride = (d.k == 0 ? d.a_pad : d.b_pad) * lp;
     const int64_t r_stride = (d.k == 0 ? d.b_pad : d.a_pad) * lp;
+    // ||T||_F^2 directly from the same product (a closed form through the
+    // Ritz values cancels when Psi lies almost entirely in the selected modes).
+    {
+        Operand A{L, lp, l_stride};
+        Operand B{R, lp, r_stride};
+        GemmShape sh{(int)d.mp, (int)d.np_, (int)lp, 1, (int)lp, 0};
+        EpiApplyNorm e{};
+        e.psi = w.psi; e.ld_psi = d.np_; e.stride_psi = mn;
+        e.rows = (int)d.m; e.cols = (int)d.n;
+        e.sumsq = w.sumsq; e.tiles_per_mat = ns_tiles(d);
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_L_APPLY, 2.0 * d.ell * (double)d.m * d.n * count, 2.0 * d.m * d.n * count,
+                     [&] { return launch_gemm_apply_norm(A, B, sh, count, e, sc.s); }),
+               "apply norm");
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+                     [&] { return launch_sum_partials(w.sumsq, ns_tiles(d), w.tn2, count, sc.s); }),
+               "t norm");
+    }
     for (int c0 = 0; c0 < count; c0 += kChunk) {
         const int cnt = std::min(kChunk, count - c0);
         Operand A{L + (int64_t)c0 * l_stride, lp, l_stride};
@@ -683,7 +705,7 @@ int run_group_l(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
         GemmShape sh{(int)d.mp, (int)d.np_, (int)lp, 1, (int)lp, 0};
         EpiApplyUpdate e{};
         e.psi = w.psi + (int64_t)c0 * mn; e.ld_psi = d.np_; e.stride_psi = mn;
-        e.tnorm2 = w.tnorm2 + c0;
+        e.tnorm2 = w.tn2 + c0;
         e.rows = (int)d.m; e.cols = (int)d.n;
         e.lr = hp.lr; e.wd = hp.weight_decay; e.target_rms = hp.target_rms;
         e.ptrs = make_chunk(sc, idx, first + c0, cnt);
@@ -694,7 +716,7 @@ int run_group_l(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
     if (dbg) {
         for (int i = 0; i < count; ++i) {
             DebugMat& dm = dbg[idx[first + i]];
-            NP_TRY(hipMemcpyAsync(dm.scalars, w.tnorm2 + i, sizeof(float), hipMemcpyDeviceToDevice, sc.s), "dbg");
+            NP_TRY(hipMemcpyAsync(dm.scalars, w.tn2 + i, sizeof(float), hipMemcpyDeviceToDevice, sc.s), "dbg");
             NP_TRY(hipMemcpyAsync(dm.scalars + 1, w.nsel + i, sizeof(int), hipMemcpyDeviceToDevice, sc.s), "dbg");
             NP_TRY(hipMemcpyAsync(dm.scalars + 2, w.ritz + (int64_t)i * d.top, sizeof(float) * d.top,
                                   hipMemcpyDeviceToDevice, sc.s),

@@ -220,18 +220,8 @@ __global__ void __launch_bounds__(256) psi_scale_kernel(const float* psisq, int6
 template <int VW, bool DBG>
 __global__ void __launch_bounds__(256) g_update_kernel(GUpdateArgs a) {
     const int z = blockIdx.y;
-    // ||T||_F^2 from the per-tile partials of the last Newton-Schulz combine,
-    // summed in a fixed order (deterministic).
-    __shared__ float red[4];
-    float s = 0.f;
-    const float* sp = a.sumsq + (int64_t)z * a.tiles_per_mat;
-    for (int i = threadIdx.x; i < a.tiles_per_mat; i += 256) s += sp[i];
-    s = wave_sum_f(s);
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
-    __syncthreads();
-    const float t2 = red[0] + red[1] + red[2] + red[3];
+    const float t2 = a.tnorm2[z];
     const float scale = t2 > 0.f ? a.target_rms * sqrtf((float)a.rows * (float)a.cols) / sqrtf(t2) : 0.f;
-    if (blockIdx.x == 0 && threadIdx.x == 0 && a.tnorm2_out) a.tnorm2_out[z] = t2;
 
     float* W = a.ptrs.w[z];
     const half_t* T = a.t + (int64_t)z * a.stride_t;
@@ -262,6 +252,19 @@ __global__ void __launch_bounds__(256) g_update_kernel(GUpdateArgs a) {
             if constexpr (DBG) a.t32[(int64_t)z * a.stride_t32 + (int64_t)row * a.cols + c0] = t;
         }
     }
+}
+
+// One block per matrix; fixed-order (deterministic) sum of n partials.
+__global__ void __launch_bounds__(256) sum_partials_kernel(const float* in, int n, float* out) {
+    const int z = blockIdx.x;
+    const float* p = in + (int64_t)z * n;
+    float s = 0.f;
+    for (int i = threadIdx.x; i < n; i += 256) s += p[i];
+    s = wave_sum_f(s);
+    __shared__ float red[4];
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) out[z] = red[0] + red[1] + red[2] + red[3];
 }
 
 __global__ void fill_zero_kernel(uint4* p, int64_t n16) {
@@ -345,6 +348,11 @@ hipError_t launch_g_update(const GUpdateArgs& a, int batch, hipStream_t s) {
         if (dbg) hipLaunchKernelGGL((g_update_kernel<1, true>), grid, dim3(256), 0, s, a);
         else hipLaunchKernelGGL((g_update_kernel<1, false>), grid, dim3(256), 0, s, a);
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_sum_partials(const float* in, int n, float* out, int batch, hipStream_t s) {
+    hipLaunchKernelGGL(sum_partials_kernel, dim3(batch), dim3(256), 0, s, in, n, out);
     return hipGetLastError();
 }
 

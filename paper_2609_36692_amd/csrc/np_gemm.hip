@@ -240,6 +240,31 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
                     out[(int64_t)(rbase + i * 16 + r) * epi.ld_out + cbase + j * 16] = acc[i][j][r];
+    } else if constexpr (Epi::kind == EpiKind::ApplyNorm) {
+        const half_t* psi = epi.psi + (int64_t)z * epi.stride_psi;
+        float ss = 0.f;
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const int col = cbase + j * 16;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int row = rbase + i * 16 + r;
+                    if (row < epi.rows && col < epi.cols) {
+                        const float t = (float)psi[(int64_t)row * epi.ld_psi + col] + acc[i][j][r];
+                        ss = fmaf(t, t, ss);
+                    }
+                }
+            }
+        ss = wave_sum(ss);
+        if (lane == 0) red[wave] = ss;
+        __syncthreads();
+        if (tid == 0) {
+            float t = 0.f;
+            for (int w = 0; w < NT / 64; ++w) t += red[w];
+            epi.sumsq[(int64_t)z * epi.tiles_per_mat + blockIdx.x] = t;
+        }
     } else {
         // NormPre-L apply + update.
         const float t2 = epi.tnorm2[z];
@@ -268,6 +293,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
 struct EAff : EpiAffine { static constexpr EpiKind kind = EpiKind::Affine; };
 struct EPar : EpiPartial { static constexpr EpiKind kind = EpiKind::Partial; };
 struct EApp : EpiApplyUpdate { static constexpr EpiKind kind = EpiKind::Apply; };
+struct EAppN : EpiApplyNorm { static constexpr EpiKind kind = EpiKind::ApplyNorm; };
 
 template <int BM, int BN, int WM, int WN, int LAYOUT, class E>
 hipError_t run(Operand A, Operand B, GemmShape sh, int batch, const E& e, hipStream_t s) {
@@ -341,6 +367,13 @@ hipError_t launch_gemm_apply(Operand A, Operand B, GemmShape sh, int batch,
                              const EpiApplyUpdate& e, hipStream_t s) {
     EApp ee;
     static_cast<EpiApplyUpdate&>(ee) = e;
+    return run<128, 128, 2, 2, 0>(A, B, sh, batch, ee, s);
+}
+
+hipError_t launch_gemm_apply_norm(Operand A, Operand B, GemmShape sh, int batch,
+                                  const EpiApplyNorm& e, hipStream_t s) {
+    EAppN ee;
+    static_cast<EpiApplyNorm&>(ee) = e;
     return run<128, 128, 2, 2, 0>(A, B, sh, batch, ee, s);
 }
 

@@ -68,13 +68,21 @@ struct EpiPartial {
 // weight update W <- W - lr (s T + wd W) with s = rms sqrt(mn) / ||T||_F.
 struct EpiApplyUpdate {
     const half_t* psi; int64_t ld_psi; int64_t stride_psi;
-    const float* tnorm2;                // per matrix ||T||_F^2 (closed form)
+    const float* tnorm2;                // per matrix ||T||_F^2 (from the norm pass)
     int rows, cols;                     // real sizes of W
     float lr, wd, target_rms;
     PtrChunk ptrs;                      // w[] used
 };
 
-enum class EpiKind { Affine, Partial, Apply };
+// NormPre-L norm pass: the same T = Psi + acc, reduced to per-tile partial
+// sums of T^2 over the real rows x cols region (no write of T or W).
+struct EpiApplyNorm {
+    const half_t* psi; int64_t ld_psi; int64_t stride_psi;
+    int rows, cols;
+    float* sumsq; int tiles_per_mat;
+};
+
+enum class EpiKind { Affine, Partial, Apply, ApplyNorm };
 
 // Launchers (gemm kernels, np_gemm.hip).  `layout` selects which operands
 // are MN-major: 0 = both K-major, 1 = B MN-major, 2 = both MN-major.
@@ -87,6 +95,8 @@ hipError_t launch_gemm_partial(TileCfg cfg, int layout, Operand A, Operand B,
                                hipStream_t s);
 hipError_t launch_gemm_apply(Operand A, Operand B, GemmShape sh, int batch,
                              const EpiApplyUpdate& e, hipStream_t s);
+hipError_t launch_gemm_apply_norm(Operand A, Operand B, GemmShape sh, int batch,
+                                  const EpiApplyNorm& e, hipStream_t s);
 int gemm_tile_m(TileCfg cfg);
 int gemm_tile_n(TileCfg cfg);
 
@@ -109,6 +119,10 @@ hipError_t launch_normalize_cols(const NormArgs& a, int batch, double* partials,
                                  int row_chunk, hipStream_t s);
 int64_t normalize_cols_partials(int rows, int cols_pad, int row_chunk);
 
+// out[z] = sum_i in[z*n + i] in a fixed order (per-matrix ||T||_F^2 from
+// per-tile partial sums).
+hipError_t launch_sum_partials(const float* in, int n, float* out, int batch, hipStream_t s);
+
 // Per-matrix Newton-Schulz pre-scale c = 1 / (sqrt(sum psisq) + eps) and
 // ||Psi||_F^2: out[z*2] = c, out[z*2+1] = ||Psi||^2.
 hipError_t launch_psi_scale(const float* psisq, int64_t stride, int active_rows,
@@ -120,9 +134,8 @@ struct GUpdateArgs {
     PtrChunk ptrs;
     int rows, cols;
     const half_t* t; int64_t ld_t; int64_t stride_t;
-    const float* sumsq; int tiles_per_mat;
+    const float* tnorm2;            // per-matrix ||T||_F^2
     float lr, wd, target_rms;
-    float* tnorm2_out;              // optional per-matrix ||T||^2 (debug)
     float* t32; int64_t stride_t32; // optional fp32 copy of T (debug)
     int vec_ok;                     // 16-byte aligned W rows
 };
@@ -172,14 +185,12 @@ hipError_t launch_small_mul(const SmallMulArgs& a, int batch, hipStream_t s);
 
 // Jacobi eigensolver of Gamma_Q (summed fp64 partials), selection of the
 // top-min(r, l) Ritz values > 1, K = Z_C diag(lambda^-1/2 - 1) Z_C^T (fp32,
-// l_pad x l_pad), closed-form ||T||^2 = ||Psi||^2 - sum_C (lambda - 1).
+// l_pad x l_pad).
 struct EigArgs {
     const double* partial; int chunks;
     int ell, ell_pad, rank;
     float* scratch;             // 2 * l_pad * l_pad floats per matrix
     float* kmat;                // l_pad x l_pad per matrix
-    const float* psi_scale;     // [z*2+1] = ||Psi||^2
-    float* tnorm2;              // per matrix
     float* ritz; int ritz_stride;
     int* nsel;
     int max_sweeps;

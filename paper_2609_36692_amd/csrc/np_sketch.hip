@@ -379,12 +379,9 @@ __global__ void __launch_bounds__(256) eig_select_kernel(EigArgs a) {
         K[q] = s;
     }
     if (tid == 0) {
-        float ssum = 0.f;
         int cnt = 0;
-        for (int i = 0; i < n; ++i)
-            if (rnk[i] < top && lam[i] > 1.f) { ssum += lam[i] - 1.f; ++cnt; }
+        for (int i = 0; i < n; ++i) cnt += (rnk[i] < top && lam[i] > 1.f);
         a.nsel[z] = cnt;
-        a.tnorm2[z] = a.psi_scale[2 * z + 1] - ssum;
     }
 }
 

@@ -2,7 +2,11 @@
 
 Tolerances: fp32 normalization (Psi) 1e-4 relative Frobenius; NormPre-G
 update 2e-2 (fp16 Newton-Schulz operands, fp32 accumulation); NormPre-L update
-1e-2 and Ritz values 1e-2 relative to the largest one.  The update U is
+max(1e-2, 8 u16 kappa) and Ritz values 1e-2 relative to the largest one.
+kappa = sqrt(sum_C lambda_i) / ||T||_F is the cancellation factor of
+T = Psi + U_C (Lambda_C^{-1/2} - I) U_C^T Psi: along a selected mode T keeps
+lambda^{-1/2} of Psi, so fp16 rounding (u16 = 2^-11) of Psi, Q and B^T K is
+amplified by kappa; kappa ~ 1 when the unselected bulk dominates ||T||.  The update U is
 recovered from the weight change with lr = 1 and no weight decay, where
 W_new = W - U exactly up to fp32 rounding.
 """
@@ -23,6 +27,14 @@ pytestmark = pytest.mark.gpu
 TOL_PSI = 1e-4
 TOL_G = 2e-2
 TOL_L = 1e-2
+U16 = 2.0 ** -11
+
+
+def tol_l(ref):
+    """NormPre-L tolerance from the fp16 arithmetic of the apply (see above)."""
+    lam_sel = ref["ritz_values"][ref["ritz_values"] > 1.0][: ref["n_selected"]]
+    kappa = math.sqrt(float(np.sum(lam_sel))) / max(np.linalg.norm(ref["t"]), 1e-300)
+    return max(TOL_L, 8.0 * U16 * kappa)
 
 
 def _need_gpu():
@@ -138,13 +150,17 @@ def test_l_step_parity(ctx, shape, rank, t):
     ritz = N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_RITZ, 400)
     nsel = int(N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_NSEL, 1, np.int32)[0])
     ell = int(N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_ELL, 1, np.int32)[0])
-    _say(f"   update err {err:.3e} nsel {nsel}/{ref['n_selected']} l={ell}")
+    tol = tol_l(ref)
+    _say(f"   update err {err:.3e} (tol {tol:.2e}) nsel {nsel}/{ref['n_selected']} l={ell}")
     assert ell == ref["ell"]
     lam = ref["ritz_values"]
     assert ritz.shape == lam.shape
-    assert np.max(np.abs(ritz - lam)) <= 1e-2 * max(lam[0], 1.0)
-    assert nsel == ref["n_selected"]
-    assert err < TOL_L
+    delta = 1e-2 * max(lam[0], 1.0)
+    assert np.max(np.abs(ritz - lam)) <= delta
+    # The lambda > 1 threshold is continuous (the factor lambda^-1/2 -> 1), so a
+    # Ritz value within the Ritz tolerance of 1 may fall on either side.
+    assert int(np.sum(lam > 1 + delta)) <= nsel <= int(np.sum(lam > 1 - delta))
+    assert err < tol
     assert math.isclose(np.linalg.norm(res["u"]), 0.2 * math.sqrt(shape[0] * shape[1]), rel_tol=2e-3)
 
 
@@ -164,7 +180,7 @@ def test_mixed_shapes_and_ids_l(ctx):
     res = run_step(ctx, "L", mats, 1, rank=8)
     for i, mat in enumerate(mats):
         ref = oracle(mat, "L", 1, rank=8, matrix_id=i)
-        assert O.relative_fro(res[i]["u"], ref["update"]) < TOL_L
+        assert O.relative_fro(res[i]["u"], ref["update"]) < tol_l(ref)
 
 
 @pytest.mark.parametrize("variant", ["G", "L"])
@@ -209,7 +225,7 @@ def test_non_default_stream(ctx):
     s.synchronize()
     ref = oracle(mat, "L", 0)
     u = mat[0].double().numpy() - W.cpu().double().numpy()
-    assert O.relative_fro(u, ref["update"]) < TOL_L
+    assert O.relative_fro(u, ref["update"]) < tol_l(ref)
 
 
 def test_invalid_args_leave_buffers_untouched(ctx):
