@@ -1,0 +1,233 @@
+"""Benchmark of the NormPre optimizer step on one MI355X.
+
+A step is one NormPre-G (or NormPre-L) optimizer step over a whole synthetic
+layer stack (default: the 48 hidden matrices of GPT-2 Small), with t
+incrementing so both orientations are timed, inputs resident in HBM.
+
+Prints ONE JSON line.  `value` is NormPre-G steps/s of the stack (the metric
+also reports NS GEMM TFLOP/s and roofline fractions); NormPre-L is reported
+in `variants`.  The per-kernel roofline comes from a second timed region of
+the same K steps in which the library brackets every launch with HIP events
+on the step's stream (the clean region gives `value`).  The CPU baseline is
+the float64 oracle on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP16_TFLOPS = 2516.6   # MI355X dense fp16/bf16 MFMA (256 CU x 2.4 GHz x 4096)
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="gpt2_small")
+    p.add_argument("--variants", default="G,L")
+    p.add_argument("--rank", type=int, default=None, help="NormPre-L rank r (default: the workload's)")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-sample-layers", type=int, default=1)
+    p.add_argument("--json-out", default=None)
+    return p.parse_args()
+
+
+def kclass_totals(N, ctx):
+    out = {}
+    for k, name in enumerate(N.KCLASS_NAMES):
+        out[name] = N.normpre_kernel_stats(ctx, k, reset=True)
+    return out
+
+
+def time_variant(N, WL, torch, wl, variant, steps, warmup, rank):
+    dev = torch.device("cuda:0")
+    ws, gs, ms = WL.make_stack(wl, dev)
+    torch.cuda.synchronize()
+    ctx = N.normpre_init(0)
+    v = N.NORMPRE_VARIANT_G if variant == "G" else N.NORMPRE_VARIANT_L
+    hp = N.normpre_default_hparams(lr=wl.lr, rank=rank, oversample=wl.oversample,
+                                   power_iters=wl.power_iters)
+    t = 0
+
+    def run(n, flags):
+        nonlocal t
+        for _ in range(n):
+            hp.step = t
+            hp.flags = flags
+            N.normpre_step(ctx, v, ws, gs, ms, hp)
+            t += 1
+
+    run(warmup, 0)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # Clean timed region -> value.
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    e0.record(stream)
+    run(steps, 0)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_step = e0.elapsed_time(e1) / steps
+    # Instrumented timed region -> per-kernel-class device time.
+    kclass_totals(N, ctx)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    run(steps, N.NORMPRE_FLAG_TIME_KERNELS)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_step_instr = e0.elapsed_time(e1) / steps
+    classes = kclass_totals(N, ctx)
+    N.normpre_destroy(ctx)
+    del ws, gs, ms
+    torch.cuda.empty_cache()
+    return {"ms_per_step": ms_step, "wall_ms_per_step": 1e3 * wall / steps,
+            "ms_per_step_instrumented": ms_step_instr, "classes": classes}
+
+
+def roofline_of(cls, bound):
+    if not cls or cls["launches"] == 0 or cls["ms"] <= 0:
+        return None
+    sec = cls["ms"] / 1e3
+    if bound == "mfma":
+        ach = cls["flops"] / sec / 1e12
+        peak, unit = PEAK_FP16_TFLOPS, "TFLOP/s"
+    else:
+        ach = cls["bytes"] / sec / 1e9
+        peak, unit = PEAK_HBM_GBS, "GB/s"
+    return {"bound": bound, "achieved": round(ach, 2), "peak": peak, "unit": unit,
+            "frac": round(ach / peak, 4), "traffic": None,
+            "launches": cls["launches"], "avg_launch_us": round(1e3 * cls["ms"] / cls["launches"], 2)}
+
+
+def merge_classes(classes, names):
+    out = {"launches": 0, "ms": 0.0, "flops": 0.0, "bytes": 0.0}
+    for n in names:
+        c = classes.get(n)
+        if c:
+            for k in out:
+                out[k] += c[k]
+    return out
+
+
+def cpu_baseline(wl, variant, layers, rank):
+    """Oracle (float64 NumPy) on the first `layers` layers of the stack."""
+    import numpy as np
+    from oracle import normpre_oracle as O
+    from paper_2609_36692_amd import workloads as WL
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    per_layer = {"gpt2_small": 4, "llama_1b": 7, "qwen3_1p7b": 7}.get(wl.name, len(wl.shapes))
+    n = min(len(wl.shapes), per_layer * layers)
+    hp = O.HParams(lr=wl.lr, rank=rank, oversample=wl.oversample, power_iters=wl.power_iters)
+    mats = [WL.make_matrix(wl, i, "cpu") for i in range(n)]
+    t0 = time.perf_counter()
+    for i, (w, g, mp) in enumerate(mats):
+        O.normpre_step(w.numpy(), g.numpy(), mp.numpy(), i % 2, hp, variant, matrix_id=i)
+    dt = time.perf_counter() - t0
+    scale = len(wl.shapes) / n
+    sec_per_step = dt * scale
+    return {"value": round(1.0 / sec_per_step, 5), "unit": "steps/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{n} of {len(wl.shapes)} matrices (first {layers} layer(s)), NormPre-{variant}, "
+                      f"{dt:.2f} s measured, scaled x{scale:g} to the full stack"}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus above 1 is not supported "
+                                   "(the step shards by matrix ownership; see the design notes)"}))
+        sys.exit(2)
+    import torch
+    from paper_2609_36692_amd import normpre as N
+    from paper_2609_36692_amd import workloads as WL
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    if not os.path.exists(N.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    wl = WL.WORKLOADS[a.workload]
+    rank = a.rank or wl.rank
+    variants = [v.strip().upper() for v in a.variants.split(",") if v.strip()]
+    res = {}
+    for v in variants:
+        r = time_variant(N, WL, torch, wl, v, a.steps, a.warmup, rank)
+        cls = r["classes"]
+        if v == "G":
+            ns = merge_classes(cls, ["ns_gram", "ns_poly", "ns_combine"])
+            roof = roofline_of(ns, "mfma")
+            roof["kernel"] = "Newton-Schulz GEMMs (gram + poly + combine, fp16 MFMA)"
+        else:
+            roof = roofline_of(cls["sk_stream"], "hbm")
+            roof["kernel"] = "sketch products streaming Psi (fp16 MFMA, split-K)"
+        norm_roof = roofline_of(cls["normalize"], "hbm")
+        if norm_roof:
+            norm_roof["kernel"] = "momentum + tangent + normalization"
+        total_dev = sum(c["ms"] for c in cls.values())
+        res[v] = {
+            "steps_per_s": round(1e3 / r["ms_per_step"], 3),
+            "ms_per_step": round(r["ms_per_step"], 4),
+            "wall_ms_per_step": round(r["wall_ms_per_step"], 4),
+            "ms_per_step_instrumented": round(r["ms_per_step_instrumented"], 4),
+            "roofline": roof,
+            "normalize_roofline": norm_roof,
+            "kernel_ms_per_step": {k: round(c["ms"] / a.steps, 4) for k, c in cls.items() if c["launches"]},
+            "kernel_share": {k: round(c["ms"] / total_dev, 4) for k, c in cls.items() if c["launches"]},
+        }
+        if v == "G":
+            res[v]["ns_tflops_step"] = round(ns["flops"] / a.steps / 1e12, 4)
+            res[v]["ns_tflops_per_s_in_step"] = round(ns["flops"] / a.steps / 1e12 / (r["ms_per_step"] / 1e3), 2)
+        print(f"[bench] NormPre-{v}: {res[v]['ms_per_step']:.3f} ms/step", file=sys.stderr, flush=True)
+
+    cpu = None
+    if not a.no_cpu_baseline:
+        v0 = variants[0]
+        cpu = cpu_baseline(wl, v0, a.cpu_sample_layers, rank)
+        print(f"[bench] cpu baseline: {cpu}", file=sys.stderr, flush=True)
+
+    primary = variants[0]
+    p = res[primary]
+    line = {
+        "metric": "optimizer steps/sec per full layer stack + NS GEMM TFLOP/s, % MFMA/HBM peak",
+        "value": p["steps_per_s"],
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": p["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp16 MFMA operands, fp32 accumulate and state",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {wl.description}", "matrices": len(wl.shapes),
+                   "elements": wl.elements, "variant": f"NormPre-{primary}",
+                   "ns_iters": 5, "rank": rank, "oversample": wl.oversample,
+                   "power_iters": wl.power_iters, "parallelism": "single GPU"},
+        "roofline": p["roofline"],
+        "cpu_baseline": cpu,
+        "variants": res,
+    }
+    s = json.dumps(line)
+    if a.json_out:
+        with open(a.json_out, "w") as f:
+            f.write(s + "\n")
+    print(s)
+
+
+if __name__ == "__main__":
+    main()
