@@ -27,7 +27,7 @@ constexpr int64_t kMaxElems = int64_t(1) << 31;
 constexpr int kMaxRowLen = 32768;   // row-active register kernel limit
 constexpr int kMaxEll = 384;
 constexpr int kColRowChunk = 64;    // rows per block in the column-active pass
-constexpr int kGramChunk = 2048;    // length chunk of the fp64 Gram kernel
+constexpr int kGramMaxChunks = 32;  // at most this many length chunks in the fp64 Gram
 constexpr int kMaxSplits = 16;
 constexpr int kEigSweeps = 30;
 constexpr size_t kGroupBudget = size_t(24) << 30;  // workspace bytes per group
@@ -283,7 +283,17 @@ Dims dims_of(int64_t m, int64_t n, int k, const normpre_hparams& hp) {
     return d;
 }
 
+// Length chunk of the fp64 Gram: >= 256 for parallel blocks, at most
+// kGramMaxChunks chunks so the consumers sum few partials.
+int gram_chunk_len(int64_t len) {
+    return (int)std::max<int64_t>(256, round_up((len + kGramMaxChunks - 1) / kGramMaxChunks, 64));
+}
+
 int ns_tiles(const Dims& d) { return (int)((d.mp / 128) * (d.np_ / 128)); }
+int combine_tiles(const Dims& d, TileCfg cfg) {
+    const int64_t t = cfg == TileCfg::Big256 ? 256 : 128;
+    return (int)((d.mp / t) * (d.np_ / t));
+}
 
 // Split count for a skinny product with output length n_out and reduction length k_len.
 int pick_splits(int64_t tiles_per_mat, int count, int64_t k_len) {
@@ -316,7 +326,7 @@ GWork carve(Arena& ar, const Dims& d, int count, int variant) {
             w.v32[i] = ar.take<float>(count * lp * maxpad);
         }
         w.part = ar.take<float>(count * (int64_t)kMaxSplits * lp * maxpad);
-        w.gpart = ar.take<double>(count * (int64_t)gram64_chunks(maxpad, kGramChunk) * lp * lp);
+        w.gpart = ar.take<double>(count * (int64_t)(kGramMaxChunks + 1) * lp * lp);
         w.chol = ar.take<double>(count * 2 * lp * lp);
         w.rinv = ar.take<float>(count * lp * lp);
         w.kmat = ar.take<float>(count * lp * lp);
@@ -424,6 +434,14 @@ int run_normalize(const StepCtx& sc, const Dims& d, const GWork& w, const std::v
     return NORMPRE_OK;
 }
 
+// 256 x 256 tiles (8 waves) when a launch has enough of them to fill the
+// 256 CUs, else 128 x 128 tiles.
+TileCfg ns_cfg(int64_t M, int64_t N, bool sym, int count) {
+    const int64_t tm = M / 256, tn = N / 256;
+    const int64_t tiles = sym ? tm * (tm + 1) / 2 : tm * tn;
+    return tiles * count >= 512 ? TileCfg::Big256 : TileCfg::Big;
+}
+
 int run_group_g(const StepCtx& sc, const Dims& d, const GWork& w, const std::vector<int>& idx, int first, int count,
                 DebugMat* dbg) {
     int rc = run_normalize(sc, d, w, idx, first, count, dbg);
@@ -446,9 +464,10 @@ int run_group_g(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
             e.mul = first_it ? w.scale : nullptr; e.mul_pow = first_it ? 2 : 0;
             e.ca = 1.f; e.cs = 0.f;
             const int layout = d.tall ? 2 : 0;
+            const TileCfg cfg = ns_cfg(d.sp, d.sp, true, count);
             NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_GRAM, 2.0 * s_ * s_ * l_ * count,
                          2.0 * (s_ * l_ + s_ * s_) * count,
-                         [&] { return launch_gemm_affine(TileCfg::Big, layout, A, B, sh, count, e, sc.s); }),
+                         [&] { return launch_gemm_affine(cfg, layout, A, B, sh, count, e, sc.s); }),
                    "ns gram");
         }
         // B = b A + c A^2
@@ -459,8 +478,9 @@ int run_group_g(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
             e.out = w.bmat; e.ld_out = d.sp; e.stride_out = ss;
             e.src = w.amat; e.ld_src = d.sp; e.stride_src = ss;
             e.ca = hp.ns_coeffs[2]; e.cs = hp.ns_coeffs[1];
+            const TileCfg cfg = ns_cfg(d.sp, d.sp, true, count);
             NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_POLY, 2.0 * s_ * s_ * s_ * count, 6.0 * s_ * s_ * count,
-                         [&] { return launch_gemm_affine(TileCfg::Big, 0, A, B, sh, count, e, sc.s); }),
+                         [&] { return launch_gemm_affine(cfg, 0, A, B, sh, count, e, sc.s); }),
                    "ns poly");
         }
         // X <- a X + B X (wide) or Y <- a Y + Y B (tall), times c on the first iteration.
@@ -470,19 +490,20 @@ int run_group_g(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
             e.src = x; e.ld_src = d.np_; e.stride_src = mn;
             e.mul = first_it ? w.scale : nullptr; e.mul_pow = first_it ? 1 : 0;
             e.ca = 1.f; e.cs = hp.ns_coeffs[0];
+            const TileCfg cfg = ns_cfg(d.mp, d.np_, false, count);
             e.sumsq = last_it ? w.sumsq : nullptr;
-            e.tiles_per_mat = ns_tiles(d);
+            e.tiles_per_mat = combine_tiles(d, cfg);
             hipError_t (*fn)(TileCfg, int, Operand, Operand, GemmShape, int, const EpiAffine&, hipStream_t) =
                 launch_gemm_affine;
             auto go = [&]() -> hipError_t {
                 if (!d.tall) {
                     Operand A{w.bmat, d.sp, ss}, B{x, d.np_, mn};
                     GemmShape sh{(int)d.sp, (int)d.lp_, (int)d.sp, 1, (int)d.sp, 0};
-                    return fn(TileCfg::Big, 1, A, B, sh, count, e, sc.s);
+                    return fn(cfg, 1, A, B, sh, count, e, sc.s);
                 }
                 Operand A{x, d.np_, mn}, B{w.bmat, d.sp, ss};
                 GemmShape sh{(int)d.lp_, (int)d.sp, (int)d.sp, 1, (int)d.sp, 0};
-                return fn(TileCfg::Big, 0, A, B, sh, count, e, sc.s);
+                return fn(cfg, 0, A, B, sh, count, e, sc.s);
             };
             NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_COMBINE, 2.0 * s_ * s_ * l_ * count,
                          2.0 * (2.0 * s_ * l_ + s_ * s_) * count, go),
@@ -490,8 +511,9 @@ int run_group_g(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
         }
     }
     const half_t* t = bufs[q & 1];
+    const int t_tiles = combine_tiles(d, ns_cfg(d.mp, d.np_, false, count));
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
-                 [&] { return launch_sum_partials(w.sumsq, ns_tiles(d), w.tn2, count, sc.s); }),
+                 [&] { return launch_sum_partials(w.sumsq, t_tiles, w.tn2, count, sc.s); }),
            "t norm");
     for (int c0 = 0; c0 < count; c0 += kChunk) {
         const int cnt = std::min(kChunk, count - c0);
@@ -582,9 +604,10 @@ int sketch_product(const StepCtx& sc, const Dims& d, const GWork& w, int count, 
 int cholqr_step(const StepCtx& sc, const Dims& d, const GWork& w, int count, const float* v, int64_t len,
                 float* out32, half_t* out16, half_t* out16t) {
     const int64_t lp = d.ellp, maxpad = d.lp_;
-    const int chunks = gram64_chunks(len, kGramChunk);
+    const int chunk_len = gram_chunk_len(len);
+    const int chunks = gram64_chunks(len, chunk_len);
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
-                 [&] { return launch_gram64(v, len, lp * maxpad, (int)lp, len, kGramChunk, w.gpart, count, sc.s); }),
+                 [&] { return launch_gram64(v, len, lp * maxpad, (int)lp, len, chunk_len, w.gpart, count, sc.s); }),
            "gram64");
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
                  [&] { return launch_chol_inv(w.gpart, chunks, d.ell, (int)lp, w.chol, w.rinv, count, sc.s); }),
@@ -651,10 +674,11 @@ int run_group_l(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
     // B = Q^T Psi (ell_pad x b_pad), Gamma_Q = B B^T, Ritz pairs and selection.
     rc = sketch_product(sc, d, w, count, w.v16[0], false, w.v32[0], nullptr, 1.f);
     if (rc) return rc;
-    const int chunks = gram64_chunks(d.b_pad, kGramChunk);
+    const int b_chunk = gram_chunk_len(d.b_pad);
+    const int chunks = gram64_chunks(d.b_pad, b_chunk);
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
                  [&] {
-                     return launch_gram64(w.v32[0], d.b_pad, lp * maxpad, (int)lp, d.b_pad, kGramChunk, w.gpart, count,
+                     return launch_gram64(w.v32[0], d.b_pad, lp * maxpad, (int)lp, d.b_pad, b_chunk, w.gpart, count,
                                           sc.s);
                  }),
            "gram64 B");

@@ -21,30 +21,35 @@ namespace np {
 namespace {
 
 constexpr int BK = 64;
+// Native 16-byte vector (HIP's uint4 is a class type whose copies block
+// register promotion of the staging arrays).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & 7; }
 __device__ __forceinline__ int lds_idx(int row, int chunk) {
     return row * BK + ((chunk ^ swz(row)) << 3);
 }
 
-// R x 64 K-major tile: each thread moves R*8/NT chunks of 16 bytes.
+// R x 64 K-major tile: each thread moves R*8/NT chunks of 16 bytes.  The
+// staging registers are a plain array owned by the kernel (not a member), so
+// they stay in VGPRs.
 template <int R, int NT>
 struct KMajorLoader {
     static constexpr int N = R * 8 / NT;
     static_assert(N >= 1 && R * 8 % NT == 0, "tile too small for the block");
-    uint4 r[N];
-    __device__ __forceinline__ void load(const half_t* base, int64_t ld, int row0, int k0, int tid) {
+    static __device__ __forceinline__ void load(u32x4 (&r)[N], const half_t* base, int64_t ld, int row0, int k0,
+                                                int tid) {
+        const half_t* p = base + (int64_t)(row0 + (tid >> 3)) * ld + k0 + (tid & 7) * 8;
+        const int64_t step = (int64_t)(NT / 8) * ld;
 #pragma unroll
-        for (int i = 0; i < N; ++i) {
-            const int c = tid + i * NT, row = c >> 3, ch = c & 7;
-            r[i] = *reinterpret_cast<const uint4*>(base + (int64_t)(row0 + row) * ld + k0 + ch * 8);
-        }
+        for (int i = 0; i < N; ++i) r[i] = *reinterpret_cast<const u32x4*>(p + i * step);
     }
-    __device__ __forceinline__ void store(half_t* lds, int tid) const {
+    static __device__ __forceinline__ void store(const u32x4 (&r)[N], half_t* lds, int tid) {
 #pragma unroll
         for (int i = 0; i < N; ++i) {
-            const int c = tid + i * NT, row = c >> 3, ch = c & 7;
-            *reinterpret_cast<uint4*>(lds + lds_idx(row, ch)) = r[i];
+            const int row = (tid >> 3) + i * (NT / 8), ch = tid & 7;
+            *reinterpret_cast<u32x4*>(lds + lds_idx(row, ch)) = r[i];
         }
     }
 };
@@ -57,35 +62,32 @@ struct MNMajorLoader {
     static constexpr int KR = R * 8 / NT;
     static_assert(KR == 2 || KR == 4 || KR == 8, "unsupported MN-major tile");
     static constexpr int MB = R / 8;
-    uint4 r[KR];
-    __device__ __forceinline__ void load(const half_t* base, int64_t ld, int row0, int k0, int tid) {
+    static constexpr int N = KR;
+    static __device__ __forceinline__ void load(u32x4 (&r)[N], const half_t* base, int64_t ld, int row0, int k0,
+                                                int tid) {
         const int mblk = tid % MB, kblk = tid / MB;
+        const half_t* p = base + (int64_t)(k0 + kblk * KR) * ld + row0 + mblk * 8;
 #pragma unroll
-        for (int q = 0; q < KR; ++q)
-            r[q] = *reinterpret_cast<const uint4*>(base + (int64_t)(k0 + kblk * KR + q) * ld + row0 + mblk * 8);
+        for (int q = 0; q < KR; ++q) r[q] = *reinterpret_cast<const u32x4*>(p + q * ld);
     }
-    __device__ __forceinline__ void store(half_t* lds, int tid) const {
+    static __device__ __forceinline__ void store(const u32x4 (&r)[N], half_t* lds, int tid) {
         const int mblk = tid % MB, kblk = tid / MB;
         const int kofs = kblk * KR, chunk = kofs >> 3, within = kofs & 7;
-        uint32_t w[KR][4];
-#pragma unroll
-        for (int q = 0; q < KR; ++q) { w[q][0] = r[q].x; w[q][1] = r[q].y; w[q][2] = r[q].z; w[q][3] = r[q].w; }
 #pragma unroll
         for (int mm = 0; mm < 8; ++mm) {
             const int d = mm >> 1;
-            const bool hi = mm & 1;
             uint32_t packed[KR / 2];
 #pragma unroll
             for (int e = 0; e < KR / 2; ++e) {
-                const uint32_t lo_src = w[2 * e][d], hi_src = w[2 * e + 1][d];
-                packed[e] = hi ? ((lo_src >> 16) | (hi_src & 0xffff0000u))
-                               : ((lo_src & 0xffffu) | (hi_src << 16));
+                const uint32_t lo_src = r[2 * e][d], hi_src = r[2 * e + 1][d];
+                packed[e] = (mm & 1) ? ((lo_src >> 16) | (hi_src & 0xffff0000u))
+                                     : ((lo_src & 0xffffu) | (hi_src << 16));
             }
             half_t* dst = lds + lds_idx(mblk * 8 + mm, chunk) + within;
             if constexpr (KR == 8) {
-                *reinterpret_cast<uint4*>(dst) = make_uint4(packed[0], packed[1], packed[2], packed[3]);
+                *reinterpret_cast<u32x4*>(dst) = u32x4{packed[0], packed[1], packed[2], packed[3]};
             } else if constexpr (KR == 4) {
-                *reinterpret_cast<uint2*>(dst) = make_uint2(packed[0], packed[1]);
+                *reinterpret_cast<u32x2*>(dst) = u32x2{packed[0], packed[1]};
             } else {
                 *reinterpret_cast<uint32_t*>(dst) = packed[0];
             }
@@ -117,29 +119,47 @@ __device__ __forceinline__ float wave_sum(float v) {
     return v;
 }
 
+// Maps the hardware block order (dispatched round-robin over the 8 XCDs) to
+// a logical order in which each XCD owns one contiguous range of tiles, so
+// neighbouring tiles of a matrix share that XCD's L2.
+__device__ __forceinline__ void xcd_remap(int& bx, int& by, int& bz) {
+    const int gx = gridDim.x, gy = gridDim.y, gz = gridDim.z;
+    const int total = gx * gy * gz;
+    int lin = bx + gx * (by + gy * bz);
+    if ((total & 7) == 0) lin = (lin & 7) * (total >> 3) + (lin >> 3);
+    bx = lin % gx;
+    lin /= gx;
+    by = lin % gy;
+    bz = lin / gy;
+}
+
 template <int BM, int BN, int WM, int WN, int LAYOUT, class Epi>
 __global__ void __launch_bounds__(WM * WN * 64)
 gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     constexpr int NT = WM * WN * 64;
     constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 16, FN = TN / 16;
-    __shared__ __attribute__((aligned(16))) half_t sA[BM * BK];
-    __shared__ __attribute__((aligned(16))) half_t sB[BN * BK];
+    // Two LDS stages: the MFMAs of stage i overlap the LDS stores of stage
+    // i + 1 and the global loads of stage i + 2.
+    __shared__ __attribute__((aligned(16))) half_t sA[2][BM * BK];
+    __shared__ __attribute__((aligned(16))) half_t sB[2][BN * BK];
     __shared__ float red[NT / 64];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave - (wave / WN) * WN;
-    const int z = blockIdx.z, split = blockIdx.y;
+    int bx = blockIdx.x, split = blockIdx.y, z = blockIdx.z;
+    xcd_remap(bx, split, z);
     const int tiles_n = sh.N / BN;
     int tm, tn;
-    decode_tile(blockIdx.x, tiles_n, sh.sym, tm, tn);
+    decode_tile(bx, tiles_n, sh.sym, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
     const int kbeg = split * sh.k_chunk;
     const int kend = min(sh.K, kbeg + sh.k_chunk);
 
     const half_t* Ab = A.ptr + (int64_t)z * A.batch_stride;
     const half_t* Bb = B.ptr + (int64_t)z * B.batch_stride;
-    typename LoaderSel<(LAYOUT == 2), BM, NT>::type la;
-    typename LoaderSel<(LAYOUT >= 1), BN, NT>::type lb;
+    using LA = typename LoaderSel<(LAYOUT == 2), BM, NT>::type;
+    using LB = typename LoaderSel<(LAYOUT >= 1), BN, NT>::type;
+    u32x4 ra[LA::N], rb[LB::N];
 
     f32x4 acc[FM][FN];
 #pragma unroll
@@ -148,38 +168,42 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
         for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     if (kbeg < kend) {
-        la.load(Ab, A.ld, m0, kbeg, tid);
-        lb.load(Bb, B.ld, n0, kbeg, tid);
-        la.store(sA, tid);
-        lb.store(sB, tid);
-        __syncthreads();
-        for (int k0 = kbeg; k0 < kend; k0 += BK) {
-            const bool more = k0 + BK < kend;
-            if (more) {
-                la.load(Ab, A.ld, m0, k0 + BK, tid);
-                lb.load(Bb, B.ld, n0, k0 + BK, tid);
-            }
+        LA::load(ra, Ab, A.ld, m0, kbeg, tid);
+        LB::load(rb, Bb, B.ld, n0, kbeg, tid);
+        LA::store(ra, sA[0], tid);
+        LB::store(rb, sB[0], tid);
+        if (kbeg + BK < kend) {
+            LA::load(ra, Ab, A.ld, m0, kbeg + BK, tid);
+            LB::load(rb, Bb, B.ld, n0, kbeg + BK, tid);
+        }
+        int stage = 0;
+        for (int k0 = kbeg; k0 < kend; k0 += BK, stage ^= 1) {
+            __syncthreads();
+            const half_t* ca = sA[stage];
+            const half_t* cb = sB[stage];
 #pragma unroll
             for (int s = 0; s < BK / 32; ++s) {
                 f16x8 af[FM], bf[FN];
                 const int chunk = s * 4 + (lane >> 4);
 #pragma unroll
                 for (int i = 0; i < FM; ++i)
-                    af[i] = *reinterpret_cast<const f16x8*>(sA + lds_idx(wm * TM + i * 16 + (lane & 15), chunk));
+                    af[i] = *reinterpret_cast<const f16x8*>(ca + lds_idx(wm * TM + i * 16 + (lane & 15), chunk));
 #pragma unroll
                 for (int j = 0; j < FN; ++j)
-                    bf[j] = *reinterpret_cast<const f16x8*>(sB + lds_idx(wn * TN + j * 16 + (lane & 15), chunk));
+                    bf[j] = *reinterpret_cast<const f16x8*>(cb + lds_idx(wn * TN + j * 16 + (lane & 15), chunk));
 #pragma unroll
                 for (int i = 0; i < FM; ++i)
 #pragma unroll
                     for (int j = 0; j < FN; ++j)
                         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
             }
-            __syncthreads();
-            if (more) {
-                la.store(sA, tid);
-                lb.store(sB, tid);
-                __syncthreads();
+            if (k0 + BK < kend) {
+                LA::store(ra, sA[stage ^ 1], tid);
+                LB::store(rb, sB[stage ^ 1], tid);
+                if (k0 + 2 * BK < kend) {
+                    LA::load(ra, Ab, A.ld, m0, k0 + 2 * BK, tid);
+                    LB::load(rb, Bb, B.ld, n0, k0 + 2 * BK, tid);
+                }
             }
         }
     }
@@ -228,7 +252,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
             if (tid == 0) {
                 float t = 0.f;
                 for (int w = 0; w < NT / 64; ++w) t += red[w];
-                epi.sumsq[(int64_t)z * epi.tiles_per_mat + blockIdx.x] = t;
+                epi.sumsq[(int64_t)z * epi.tiles_per_mat + bx] = t;
             }
         }
     } else if constexpr (Epi::kind == EpiKind::Partial) {
@@ -263,7 +287,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
         if (tid == 0) {
             float t = 0.f;
             for (int w = 0; w < NT / 64; ++w) t += red[w];
-            epi.sumsq[(int64_t)z * epi.tiles_per_mat + blockIdx.x] = t;
+            epi.sumsq[(int64_t)z * epi.tiles_per_mat + bx] = t;
         }
     } else {
         // NormPre-L apply + update.
@@ -324,6 +348,7 @@ hipError_t dispatch_cfg(TileCfg cfg, Operand A, Operand B, GemmShape sh, int bat
 int gemm_tile_m(TileCfg cfg) {
     switch (cfg) {
         case TileCfg::Big: return 128;
+        case TileCfg::Big256: return 256;
         case TileCfg::Skinny64: return 64;
         case TileCfg::Skinny128: return 128;
         case TileCfg::Apply: return 128;
@@ -342,11 +367,18 @@ hipError_t launch_gemm_affine(TileCfg cfg, int layout, Operand A, Operand B, Gem
                               int batch, const EpiAffine& e, hipStream_t s) {
     EAff ee;
     static_cast<EpiAffine&>(ee) = e;
-    if (cfg != TileCfg::Big) return hipErrorInvalidValue;
-    switch (layout) {
-        case 0: return run<128, 128, 2, 2, 0>(A, B, sh, batch, ee, s);
-        case 1: return run<128, 128, 2, 2, 1>(A, B, sh, batch, ee, s);
-        case 2: return run<128, 128, 2, 2, 2>(A, B, sh, batch, ee, s);
+    if (cfg == TileCfg::Big) {
+        switch (layout) {
+            case 0: return run<128, 128, 2, 2, 0>(A, B, sh, batch, ee, s);
+            case 1: return run<128, 128, 2, 2, 1>(A, B, sh, batch, ee, s);
+            case 2: return run<128, 128, 2, 2, 2>(A, B, sh, batch, ee, s);
+        }
+    } else if (cfg == TileCfg::Big256) {
+        switch (layout) {
+            case 0: return run<256, 256, 2, 4, 0>(A, B, sh, batch, ee, s);
+            case 1: return run<256, 256, 2, 4, 1>(A, B, sh, batch, ee, s);
+            case 2: return run<256, 256, 2, 4, 2>(A, B, sh, batch, ee, s);
+        }
     }
     return hipErrorInvalidValue;
 }
@@ -355,7 +387,7 @@ hipError_t launch_gemm_partial(TileCfg cfg, int layout, Operand A, Operand B, Ge
                                int batch, const EpiPartial& e, hipStream_t s) {
     EPar ee;
     static_cast<EpiPartial&>(ee) = e;
-    if (cfg == TileCfg::Big || cfg == TileCfg::Apply) return hipErrorInvalidValue;
+    if (cfg != TileCfg::Skinny64 && cfg != TileCfg::Skinny128) return hipErrorInvalidValue;
     switch (layout) {
         case 0: return dispatch_cfg<EPar, 0>(cfg, A, B, sh, batch, ee, s);
         case 1: return dispatch_cfg<EPar, 1>(cfg, A, B, sh, batch, ee, s);

@@ -143,62 +143,72 @@ __device__ __forceinline__ double gram_at(const double* p, int chunks, int ell_p
 // kDropTol * G_kk (relative to the column's own squared norm) marks the
 // column as numerically dependent: its row of R and of R^{-1} is zero, so the
 // matching column of Q = Y R^{-1} is zero and it never reaches the selection.
+// The matrix lives in LDS (fp64, row stride l + 1) when it fits, else in a
+// global scratch slice; R^{-1} overwrites R in place, bottom row first.
 constexpr double kDropTol = 1e-12;
+constexpr int kCholLdsMax = 128;
 
-__global__ void __launch_bounds__(256) chol_inv_kernel(const double* partial, int chunks, int ell, int ell_pad,
-                                                       double* scratch, float* rinv) {
+template <int NT>
+__global__ void __launch_bounds__(NT) chol_inv_kernel(const double* partial, int chunks, int ell, int ell_pad,
+                                                      double* scratch, float* rinv) {
+    extern __shared__ double dynd[];
     const int z = blockIdx.x, tid = threadIdx.x;
     const double* p = partial + (int64_t)z * chunks * ell_pad * ell_pad;
-    double* R = scratch + (int64_t)z * 2 * ell_pad * ell_pad;
-    double* X = R + (int64_t)ell_pad * ell_pad;
+    const bool in_lds = ell <= kCholLdsMax;
+    const int ld = in_lds ? ell + 1 : ell_pad;
+    double* R = in_lds ? dynd : scratch + (int64_t)z * 2 * ell_pad * ell_pad;
+    double* tmp = in_lds ? dynd + ell * ld : R + (int64_t)ell_pad * ell_pad;
     float* out = rinv + (int64_t)z * ell_pad * ell_pad;
     __shared__ double diag0[384];
     __shared__ double inv_diag[384];
-    for (int q = tid; q < ell * ell; q += 256) {
+    for (int q = tid; q < ell * ell; q += NT) {
         const int c = q / ell, d = q - (q / ell) * ell;
-        R[c * ell_pad + d] = gram_at(p, chunks, ell_pad, c, d);
+        if (d >= c) R[c * ld + d] = gram_at(p, chunks, ell_pad, c, d);
     }
     __syncthreads();
-    for (int k = tid; k < ell; k += 256) diag0[k] = R[k * ell_pad + k];
+    for (int k = tid; k < ell; k += NT) diag0[k] = R[k * ld + k];
     __syncthreads();
     for (int k = 0; k < ell; ++k) {
         if (tid == 0) {
-            const double piv = R[k * ell_pad + k];
+            const double piv = R[k * ld + k];
             const bool keep = diag0[k] > 0.0 && piv > kDropTol * diag0[k];
             const double rkk = keep ? sqrt(piv) : 0.0;
-            R[k * ell_pad + k] = rkk;
+            R[k * ld + k] = rkk;
             inv_diag[k] = keep ? 1.0 / rkk : 0.0;
         }
         __syncthreads();
         const double ik = inv_diag[k];
-        for (int j = k + 1 + tid; j < ell; j += 256) R[k * ell_pad + j] *= ik;
+        for (int j = k + 1 + tid; j < ell; j += NT) R[k * ld + j] *= ik;
         __syncthreads();
         const int nrem = ell - k - 1;
-        for (int q = tid; q < nrem * nrem; q += 256) {
+        for (int q = tid; q < nrem * nrem; q += NT) {
             const int i = k + 1 + q / nrem, j = k + 1 + q % nrem;
-            if (j >= i) R[i * ell_pad + j] -= R[k * ell_pad + i] * R[k * ell_pad + j];
+            if (j >= i) R[i * ld + j] -= R[k * ld + i] * R[k * ld + j];
         }
         __syncthreads();
     }
-    // X = R^{-1} (upper), row by row from the bottom; rows of dropped pivots stay 0.
-    for (int q = tid; q < ell_pad * ell_pad; q += 256) X[q] = 0.0;
-    __syncthreads();
+    // X = R^{-1}: row i from R's row i and the finished rows below it.
     for (int i = ell - 1; i >= 0; --i) {
         const double ii = inv_diag[i];
-        for (int j = i + tid; j < ell; j += 256) {
-            double s;
+        for (int j = i + tid; j < ell; j += NT) {
+            double v;
             if (j == i) {
-                s = ii;
+                v = ii;
             } else {
-                s = 0.0;
-                for (int k = i + 1; k <= j; ++k) s += R[i * ell_pad + k] * X[k * ell_pad + j];
-                s = -s * ii;
+                double s = 0.0;
+                for (int k = i + 1; k <= j; ++k) s += R[i * ld + k] * R[k * ld + j];
+                v = -s * ii;
             }
-            X[i * ell_pad + j] = s;
+            tmp[j] = v;
         }
         __syncthreads();
+        for (int j = i + tid; j < ell; j += NT) R[i * ld + j] = tmp[j];
+        __syncthreads();
     }
-    for (int q = tid; q < ell_pad * ell_pad; q += 256) out[q] = (float)X[q];
+    for (int q = tid; q < ell_pad * ell_pad; q += NT) {
+        const int i = q / ell_pad, j = q - (q / ell_pad) * ell_pad;
+        out[q] = (i < ell && j < ell && j >= i) ? (float)R[i * ld + j] : 0.f;
+    }
 }
 
 // ------------------------------------------------------------- M^T V ----
@@ -256,7 +266,11 @@ __global__ void __launch_bounds__(256) small_mul_kernel(SmallMulArgs a) {
 }
 
 // ------------------------------------------------------ Jacobi + select --
-constexpr int kEigLdsMax = 84;   // A and Z in LDS when 2 l^2 floats fit
+// Two-sided cyclic Jacobi with the round-robin pairing: every round rotates
+// l/2 disjoint (p, q) pairs at once (rows p, q for all columns, then columns
+// p, q for all rows, and the same columns of Z).  A and Z live in LDS (row
+// stride l + 1) when they fit, else in a global scratch slice.
+constexpr int kEigLdsMax = 128;
 
 __device__ __forceinline__ void rr_pair(int round, int k, int n2, int& p, int& q) {
     const int n1 = n2 - 1;
@@ -265,56 +279,64 @@ __device__ __forceinline__ void rr_pair(int round, int k, int n2, int& p, int& q
     if (p > q) { const int t = p; p = q; q = t; }
 }
 
+template <int NT>
 __device__ __forceinline__ float block_sum_f(float v, float* red) {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
     __syncthreads();
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
     __syncthreads();
-    return red[0] + red[1] + red[2] + red[3];
+    float t = 0.f;
+#pragma unroll
+    for (int w = 0; w < NT / 64; ++w) t += red[w];
+    return t;
 }
 
-__global__ void __launch_bounds__(256) eig_select_kernel(EigArgs a) {
+template <int NT>
+__global__ void __launch_bounds__(NT) eig_select_kernel(EigArgs a) {
     extern __shared__ float dyn[];
     const int z = blockIdx.x, tid = threadIdx.x;
     const int n = a.ell, lp = a.ell_pad;
-    float* A = n <= kEigLdsMax ? dyn : a.scratch + (int64_t)z * 2 * lp * lp;
-    float* Z = A + n * n;
+    const bool in_lds = n <= kEigLdsMax;
+    const int ld = in_lds ? n + 1 : n;
+    float* A = in_lds ? dyn : a.scratch + (int64_t)z * 2 * lp * lp;
+    float* Z = A + n * ld;
     __shared__ float cs[192], sn[192];
     __shared__ int pp[192], qq[192];
-    __shared__ float red[4];
+    __shared__ float red[NT / 64];
     __shared__ float lam[384], fcoef[384];
     __shared__ int rnk[384];
     __shared__ int stop_flag;
     const double* part = a.partial + (int64_t)z * a.chunks * lp * lp;
-    for (int q = tid; q < n * n; q += 256) {
+    for (int q = tid; q < n * n; q += NT) {
         const int c = q / n, d = q - (q / n) * n;
-        A[q] = (float)gram_at(part, a.chunks, lp, c, d);
-        Z[q] = c == d ? 1.f : 0.f;
+        A[c * ld + d] = (float)gram_at(part, a.chunks, lp, c, d);
+        Z[c * ld + d] = c == d ? 1.f : 0.f;
     }
     __syncthreads();
     const int n2 = n + (n & 1);
     const int npairs = n2 / 2;
     for (int sweep = 0; sweep < a.max_sweeps; ++sweep) {
         float off = 0.f, tot = 0.f;
-        for (int q = tid; q < n * n; q += 256) {
-            const float v = A[q] * A[q];
+        for (int q = tid; q < n * n; q += NT) {
+            const int c = q / n, d = q - (q / n) * n;
+            const float v = A[c * ld + d] * A[c * ld + d];
             tot += v;
-            if (q / n != q % n) off += v;
+            if (c != d) off += v;
         }
-        off = block_sum_f(off, red);
-        tot = block_sum_f(tot, red);
+        off = block_sum_f<NT>(off, red);
+        tot = block_sum_f<NT>(tot, red);
         if (tid == 0) stop_flag = !(off > 1e-13f * tot);
         __syncthreads();
         if (stop_flag) break;
         for (int round = 0; round < n2 - 1; ++round) {
-            if (tid < npairs) {
+            for (int k = tid; k < npairs; k += NT) {
                 int p, q;
-                rr_pair(round, tid, n2, p, q);
+                rr_pair(round, k, n2, p, q);
                 float c = 1.f, s = 0.f;
                 if (q < n) {
-                    const float apq = A[p * n + q];
-                    const float app = A[p * n + p], aqq = A[q * n + q];
+                    const float apq = A[p * ld + q];
+                    const float app = A[p * ld + p], aqq = A[q * ld + q];
                     if (fabsf(apq) > 1e-30f && fabsf(apq) > 1e-9f * sqrtf(fabsf(app * aqq))) {
                         const float theta = (aqq - app) / (2.f * apq);
                         float t;
@@ -324,41 +346,43 @@ __global__ void __launch_bounds__(256) eig_select_kernel(EigArgs a) {
                         s = t * c;
                     }
                 }
-                cs[tid] = c; sn[tid] = s; pp[tid] = p; qq[tid] = q;
+                cs[k] = c; sn[k] = s; pp[k] = p; qq[k] = q;
             }
             __syncthreads();
-            // rows p, q <- J^T A
-            for (int w = tid; w < npairs * n; w += 256) {
-                const int k = w / n, j = w - (w / n) * n;
-                const int p = pp[k], q = qq[k];
-                if (q >= n) continue;
-                const float c = cs[k], s = sn[k];
-                const float ap = A[p * n + j], aq = A[q * n + j];
-                A[p * n + j] = c * ap - s * aq;
-                A[q * n + j] = s * ap + c * aq;
+            // rows p, q <- J^T A: each thread owns columns j.
+            for (int j = tid; j < n; j += NT) {
+                for (int k = 0; k < npairs; ++k) {
+                    const int p = pp[k], q = qq[k];
+                    if (q >= n) continue;
+                    const float c = cs[k], s = sn[k];
+                    const float ap = A[p * ld + j], aq = A[q * ld + j];
+                    A[p * ld + j] = c * ap - s * aq;
+                    A[q * ld + j] = s * ap + c * aq;
+                }
             }
             __syncthreads();
-            // columns p, q <- A J and Z J
-            for (int w = tid; w < npairs * n; w += 256) {
-                const int k = w / n, i = w - (w / n) * n;
-                const int p = pp[k], q = qq[k];
-                if (q >= n) continue;
-                const float c = cs[k], s = sn[k];
-                const float ap = A[i * n + p], aq = A[i * n + q];
-                A[i * n + p] = c * ap - s * aq;
-                A[i * n + q] = s * ap + c * aq;
-                const float zp = Z[i * n + p], zq = Z[i * n + q];
-                Z[i * n + p] = c * zp - s * zq;
-                Z[i * n + q] = s * zp + c * zq;
+            // columns p, q <- A J and Z J: each thread owns rows i.
+            for (int i = tid; i < n; i += NT) {
+                for (int k = 0; k < npairs; ++k) {
+                    const int p = pp[k], q = qq[k];
+                    if (q >= n) continue;
+                    const float c = cs[k], s = sn[k];
+                    const float ap = A[i * ld + p], aq = A[i * ld + q];
+                    A[i * ld + p] = c * ap - s * aq;
+                    A[i * ld + q] = s * ap + c * aq;
+                    const float zp = Z[i * ld + p], zq = Z[i * ld + q];
+                    Z[i * ld + p] = c * zp - s * zq;
+                    Z[i * ld + q] = s * zp + c * zq;
+                }
             }
             __syncthreads();
         }
     }
     // Ritz values, descending order with ties to the lower index.
-    for (int i = tid; i < n; i += 256) lam[i] = A[i * n + i];
+    for (int i = tid; i < n; i += NT) lam[i] = A[i * ld + i];
     __syncthreads();
     const int top = min(a.rank, n);
-    for (int i = tid; i < n; i += 256) {
+    for (int i = tid; i < n; i += NT) {
         const float li = lam[i];
         int r = 0;
         for (int j = 0; j < n; ++j) r += (lam[j] > li) || (lam[j] == li && j < i);
@@ -370,12 +394,12 @@ __global__ void __launch_bounds__(256) eig_select_kernel(EigArgs a) {
     __syncthreads();
     // K = Z diag(f) Z^T over the selected modes.
     float* K = a.kmat + (int64_t)z * lp * lp;
-    for (int q = tid; q < lp * lp; q += 256) {
+    for (int q = tid; q < lp * lp; q += NT) {
         const int c = q / lp, d = q - (q / lp) * lp;
         float s = 0.f;
         if (c < n && d < n)
             for (int i = 0; i < n; ++i)
-                if (fcoef[i] != 0.f) s = fmaf(Z[c * n + i] * fcoef[i], Z[d * n + i], s);
+                if (fcoef[i] != 0.f) s = fmaf(Z[c * ld + i] * fcoef[i], Z[d * ld + i], s);
         K[q] = s;
     }
     if (tid == 0) {
@@ -426,7 +450,13 @@ hipError_t launch_gram64(const float* v, int64_t ld, int64_t stride_v, int ell_p
 hipError_t launch_chol_inv(const double* partial, int chunks, int ell, int ell_pad, double* scratch, float* rinv,
                            int batch, hipStream_t s) {
     if (ell > 384 || ell_pad > 384) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(chol_inv_kernel, dim3(batch), dim3(256), 0, s, partial, chunks, ell, ell_pad, scratch, rinv);
+    const size_t lds = ell <= kCholLdsMax ? (size_t)(ell + 1) * (ell + 1) * sizeof(double) : 0;
+    if (ell <= 64)
+        hipLaunchKernelGGL((chol_inv_kernel<64>), dim3(batch), dim3(64), lds, s, partial, chunks, ell, ell_pad, scratch,
+                           rinv);
+    else
+        hipLaunchKernelGGL((chol_inv_kernel<256>), dim3(batch), dim3(256), lds, s, partial, chunks, ell, ell_pad,
+                           scratch, rinv);
     return hipGetLastError();
 }
 
@@ -438,8 +468,11 @@ hipError_t launch_small_mul(const SmallMulArgs& a, int batch, hipStream_t s) {
 
 hipError_t launch_eig_select(const EigArgs& a, int batch, hipStream_t s) {
     if (a.ell > 384 || a.ell_pad > 384) return hipErrorInvalidValue;
-    const size_t lds = a.ell <= kEigLdsMax ? (size_t)2 * a.ell * a.ell * sizeof(float) : 0;
-    hipLaunchKernelGGL(eig_select_kernel, dim3(batch), dim3(256), lds, s, a);
+    const size_t lds = a.ell <= kEigLdsMax ? (size_t)2 * a.ell * (a.ell + 1) * sizeof(float) : 0;
+    if (a.ell <= 64)
+        hipLaunchKernelGGL((eig_select_kernel<64>), dim3(batch), dim3(64), lds, s, a);
+    else
+        hipLaunchKernelGGL((eig_select_kernel<256>), dim3(batch), dim3(256), lds, s, a);
     return hipGetLastError();
 }
 
