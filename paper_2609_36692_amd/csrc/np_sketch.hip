@@ -147,17 +147,25 @@ __device__ __forceinline__ double gram_at(const double* p, int chunks, int ell_p
 // global scratch slice; R^{-1} overwrites R in place, bottom row first.
 constexpr double kDropTol = 1e-12;
 constexpr int kCholLdsMax = 128;
+constexpr int kSmallThreads = 512;
 
-template <int NT>
-__global__ void __launch_bounds__(NT) chol_inv_kernel(const double* partial, int chunks, int ell, int ell_pad,
-                                                      double* scratch, float* rinv) {
+template <bool IN_LDS>
+__global__ void __launch_bounds__(kSmallThreads) chol_inv_kernel(const double* partial, int chunks, int ell,
+                                                                 int ell_pad, double* scratch, float* rinv) {
+    constexpr int NT = kSmallThreads;
     extern __shared__ double dynd[];
     const int z = blockIdx.x, tid = threadIdx.x;
     const double* p = partial + (int64_t)z * chunks * ell_pad * ell_pad;
-    const bool in_lds = ell <= kCholLdsMax;
-    const int ld = in_lds ? ell + 1 : ell_pad;
-    double* R = in_lds ? dynd : scratch + (int64_t)z * 2 * ell_pad * ell_pad;
-    double* tmp = in_lds ? dynd + ell * ld : R + (int64_t)ell_pad * ell_pad;
+    const int ld = IN_LDS ? ell + 1 : ell_pad;
+    double* R;
+    double* tmp;
+    if constexpr (IN_LDS) {
+        R = dynd;
+        tmp = dynd + ell * ld;
+    } else {
+        R = scratch + (int64_t)z * 2 * ell_pad * ell_pad;
+        tmp = R + (int64_t)ell_pad * ell_pad;
+    }
     float* out = rinv + (int64_t)z * ell_pad * ell_pad;
     __shared__ double diag0[384];
     __shared__ double inv_diag[384];
@@ -267,9 +275,11 @@ __global__ void __launch_bounds__(256) small_mul_kernel(SmallMulArgs a) {
 
 // ------------------------------------------------------ Jacobi + select --
 // Two-sided cyclic Jacobi with the round-robin pairing: every round rotates
-// l/2 disjoint (p, q) pairs at once (rows p, q for all columns, then columns
-// p, q for all rows, and the same columns of Z).  A and Z live in LDS (row
-// stride l + 1) when they fit, else in a global scratch slice.
+// l/2 disjoint (p, q) pairs at once.  A round is one data-parallel phase: the
+// 2 x 2 block of A on rows (p1, q1) and columns (p2, q2) becomes
+// J1^T block J2 for every pair of pairs, and columns (p, q) of Z become Z J.
+// A and Z live in LDS (row stride l + 1) when they fit, else in a global
+// scratch slice.
 constexpr int kEigLdsMax = 128;
 
 __device__ __forceinline__ void rr_pair(int round, int k, int n2, int& p, int& q) {
@@ -292,14 +302,16 @@ __device__ __forceinline__ float block_sum_f(float v, float* red) {
     return t;
 }
 
-template <int NT>
-__global__ void __launch_bounds__(NT) eig_select_kernel(EigArgs a) {
+template <bool IN_LDS>
+__global__ void __launch_bounds__(kSmallThreads) eig_select_kernel(EigArgs a) {
+    constexpr int NT = kSmallThreads;
     extern __shared__ float dyn[];
     const int z = blockIdx.x, tid = threadIdx.x;
     const int n = a.ell, lp = a.ell_pad;
-    const bool in_lds = n <= kEigLdsMax;
-    const int ld = in_lds ? n + 1 : n;
-    float* A = in_lds ? dyn : a.scratch + (int64_t)z * 2 * lp * lp;
+    const int ld = IN_LDS ? n + 1 : n;
+    float* A;
+    if constexpr (IN_LDS) A = dyn;
+    else A = a.scratch + (int64_t)z * 2 * lp * lp;
     float* Z = A + n * ld;
     __shared__ float cs[192], sn[192];
     __shared__ int pp[192], qq[192];
@@ -316,6 +328,7 @@ __global__ void __launch_bounds__(NT) eig_select_kernel(EigArgs a) {
     __syncthreads();
     const int n2 = n + (n & 1);
     const int npairs = n2 / 2;
+    const int nblk = npairs * npairs;
     for (int sweep = 0; sweep < a.max_sweeps; ++sweep) {
         float off = 0.f, tot = 0.f;
         for (int q = tid; q < n * n; q += NT) {
@@ -349,31 +362,33 @@ __global__ void __launch_bounds__(NT) eig_select_kernel(EigArgs a) {
                 cs[k] = c; sn[k] = s; pp[k] = p; qq[k] = q;
             }
             __syncthreads();
-            // rows p, q <- J^T A: each thread owns columns j.
-            for (int j = tid; j < n; j += NT) {
-                for (int k = 0; k < npairs; ++k) {
-                    const int p = pp[k], q = qq[k];
-                    if (q >= n) continue;
-                    const float c = cs[k], s = sn[k];
-                    const float ap = A[p * ld + j], aq = A[q * ld + j];
-                    A[p * ld + j] = c * ap - s * aq;
-                    A[q * ld + j] = s * ap + c * aq;
-                }
+            // A <- J^T A J, one 2 x 2 block per work item.
+            for (int w = tid; w < nblk; w += NT) {
+                const int k1 = w / npairs, k2 = w - k1 * npairs;
+                const int p1 = pp[k1], q1 = qq[k1], p2 = pp[k2], q2 = qq[k2];
+                const float c1 = cs[k1], s1 = sn[k1], c2 = cs[k2], s2 = sn[k2];
+                const bool r1 = q1 < n, r2 = q2 < n;
+                const float a00 = A[p1 * ld + p2];
+                const float a01 = r2 ? A[p1 * ld + q2] : 0.f;
+                const float a10 = r1 ? A[q1 * ld + p2] : 0.f;
+                const float a11 = (r1 && r2) ? A[q1 * ld + q2] : 0.f;
+                // rows: J1^T
+                const float b00 = c1 * a00 - s1 * a10, b01 = c1 * a01 - s1 * a11;
+                const float b10 = s1 * a00 + c1 * a10, b11 = s1 * a01 + c1 * a11;
+                // columns: J2
+                A[p1 * ld + p2] = c2 * b00 - s2 * b01;
+                if (r2) A[p1 * ld + q2] = s2 * b00 + c2 * b01;
+                if (r1) A[q1 * ld + p2] = c2 * b10 - s2 * b11;
+                if (r1 && r2) A[q1 * ld + q2] = s2 * b10 + c2 * b11;
             }
-            __syncthreads();
-            // columns p, q <- A J and Z J: each thread owns rows i.
-            for (int i = tid; i < n; i += NT) {
-                for (int k = 0; k < npairs; ++k) {
-                    const int p = pp[k], q = qq[k];
-                    if (q >= n) continue;
-                    const float c = cs[k], s = sn[k];
-                    const float ap = A[i * ld + p], aq = A[i * ld + q];
-                    A[i * ld + p] = c * ap - s * aq;
-                    A[i * ld + q] = s * ap + c * aq;
-                    const float zp = Z[i * ld + p], zq = Z[i * ld + q];
-                    Z[i * ld + p] = c * zp - s * zq;
-                    Z[i * ld + q] = s * zp + c * zq;
-                }
+            for (int w = tid; w < npairs * n; w += NT) {
+                const int k = w / n, i = w - (w / n) * n;
+                const int p = pp[k], q = qq[k];
+                if (q >= n) continue;
+                const float c = cs[k], s = sn[k];
+                const float zp = Z[i * ld + p], zq = Z[i * ld + q];
+                Z[i * ld + p] = c * zp - s * zq;
+                Z[i * ld + q] = s * zp + c * zq;
             }
             __syncthreads();
         }
@@ -450,13 +465,14 @@ hipError_t launch_gram64(const float* v, int64_t ld, int64_t stride_v, int ell_p
 hipError_t launch_chol_inv(const double* partial, int chunks, int ell, int ell_pad, double* scratch, float* rinv,
                            int batch, hipStream_t s) {
     if (ell > 384 || ell_pad > 384) return hipErrorInvalidValue;
-    const size_t lds = ell <= kCholLdsMax ? (size_t)(ell + 1) * (ell + 1) * sizeof(double) : 0;
-    if (ell <= 64)
-        hipLaunchKernelGGL((chol_inv_kernel<64>), dim3(batch), dim3(64), lds, s, partial, chunks, ell, ell_pad, scratch,
-                           rinv);
-    else
-        hipLaunchKernelGGL((chol_inv_kernel<256>), dim3(batch), dim3(256), lds, s, partial, chunks, ell, ell_pad,
-                           scratch, rinv);
+    if (ell <= kCholLdsMax) {
+        const size_t lds = (size_t)(ell + 1) * (ell + 1) * sizeof(double);
+        hipLaunchKernelGGL((chol_inv_kernel<true>), dim3(batch), dim3(kSmallThreads), lds, s, partial, chunks, ell,
+                           ell_pad, scratch, rinv);
+    } else {
+        hipLaunchKernelGGL((chol_inv_kernel<false>), dim3(batch), dim3(kSmallThreads), 0, s, partial, chunks, ell,
+                           ell_pad, scratch, rinv);
+    }
     return hipGetLastError();
 }
 
@@ -468,11 +484,12 @@ hipError_t launch_small_mul(const SmallMulArgs& a, int batch, hipStream_t s) {
 
 hipError_t launch_eig_select(const EigArgs& a, int batch, hipStream_t s) {
     if (a.ell > 384 || a.ell_pad > 384) return hipErrorInvalidValue;
-    const size_t lds = a.ell <= kEigLdsMax ? (size_t)2 * a.ell * (a.ell + 1) * sizeof(float) : 0;
-    if (a.ell <= 64)
-        hipLaunchKernelGGL((eig_select_kernel<64>), dim3(batch), dim3(64), lds, s, a);
-    else
-        hipLaunchKernelGGL((eig_select_kernel<256>), dim3(batch), dim3(256), lds, s, a);
+    if (a.ell <= kEigLdsMax) {
+        const size_t lds = (size_t)2 * a.ell * (a.ell + 1) * sizeof(float);
+        hipLaunchKernelGGL((eig_select_kernel<true>), dim3(batch), dim3(kSmallThreads), lds, s, a);
+    } else {
+        hipLaunchKernelGGL((eig_select_kernel<false>), dim3(batch), dim3(kSmallThreads), 0, s, a);
+    }
     return hipGetLastError();
 }
 
