@@ -733,6 +733,7 @@ int run_group_l(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
         e.rows = (int)d.m; e.cols = (int)d.n;
         e.lr = hp.lr; e.wd = hp.weight_decay; e.target_rms = hp.target_rms;
         e.ptrs = make_chunk(sc, idx, first + c0, cnt);
+        e.vec_ok = (d.n % 4 == 0) && chunk_vec_ok(e.ptrs, cnt);
         NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_L_APPLY, 2.0 * d.ell * (double)d.m * d.n * cnt, 10.0 * d.m * d.n * cnt,
                      [&] { return launch_gemm_apply(A, B, sh, cnt, e, sc.s); }),
                "apply");

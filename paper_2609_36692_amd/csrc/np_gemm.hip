@@ -119,6 +119,22 @@ __device__ __forceinline__ float wave_sum(float v) {
     return v;
 }
 
+template <class E>
+__device__ __forceinline__ bool epi_has_sumsq(const E& e) {
+    if constexpr (E::kind == EpiKind::Affine || E::kind == EpiKind::ApplyNorm) return e.sumsq != nullptr;
+    else return false;
+}
+template <class E>
+__device__ __forceinline__ float* epi_sumsq_ptr(const E& e) {
+    if constexpr (E::kind == EpiKind::Affine || E::kind == EpiKind::ApplyNorm) return e.sumsq;
+    else return nullptr;
+}
+template <class E>
+__device__ __forceinline__ int epi_tiles(const E& e) {
+    if constexpr (E::kind == EpiKind::Affine || E::kind == EpiKind::ApplyNorm) return e.tiles_per_mat;
+    else return 0;
+}
+
 // Maps the hardware block order (dispatched round-robin over the 8 XCDs) to
 // a logical order in which each XCD owns one contiguous range of tiles, so
 // neighbouring tiles of a matrix share that XCD's L2.
@@ -139,10 +155,13 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     constexpr int NT = WM * WN * 64;
     constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 16, FN = TN / 16;
     // Two LDS stages: the MFMAs of stage i overlap the LDS stores of stage
-    // i + 1 and the global loads of stage i + 2.
-    __shared__ __attribute__((aligned(16))) half_t sA[2][BM * BK];
-    __shared__ __attribute__((aligned(16))) half_t sB[2][BN * BK];
+    // i + 1 and the global loads of stage i + 2.  The epilogue reuses the
+    // same LDS to stage one wave-row of fp32 results (row stride BN + 4).
+    constexpr int kStageBytes = 2 * (BM + BN) * BK * 2;
+    constexpr int kEpiBytes = (BM / WM) * (BN + 4) * 4;
+    __shared__ __attribute__((aligned(16))) unsigned char smem[kStageBytes > kEpiBytes ? kStageBytes : kEpiBytes];
     __shared__ float red[NT / 64];
+    half_t* const sbase = reinterpret_cast<half_t*>(smem);
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave - (wave / WN) * WN;
@@ -170,8 +189,8 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     if (kbeg < kend) {
         LA::load(ra, Ab, A.ld, m0, kbeg, tid);
         LB::load(rb, Bb, B.ld, n0, kbeg, tid);
-        LA::store(ra, sA[0], tid);
-        LB::store(rb, sB[0], tid);
+        LA::store(ra, sbase, tid);
+        LB::store(rb, sbase + BM * BK, tid);
         if (kbeg + BK < kend) {
             LA::load(ra, Ab, A.ld, m0, kbeg + BK, tid);
             LB::load(rb, Bb, B.ld, n0, kbeg + BK, tid);
@@ -179,8 +198,8 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
         int stage = 0;
         for (int k0 = kbeg; k0 < kend; k0 += BK, stage ^= 1) {
             __syncthreads();
-            const half_t* ca = sA[stage];
-            const half_t* cb = sB[stage];
+            const half_t* ca = sbase + stage * (BM + BN) * BK;
+            const half_t* cb = ca + BM * BK;
 #pragma unroll
             for (int s = 0; s < BK / 32; ++s) {
                 f16x8 af[FM], bf[FN];
@@ -198,8 +217,8 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
             }
             if (k0 + BK < kend) {
-                LA::store(ra, sA[stage ^ 1], tid);
-                LB::store(rb, sB[stage ^ 1], tid);
+                LA::store(ra, sbase + (stage ^ 1) * (BM + BN) * BK, tid);
+                LB::store(rb, sbase + (stage ^ 1) * (BM + BN) * BK + BM * BK, tid);
                 if (k0 + 2 * BK < kend) {
                     LA::load(ra, Ab, A.ld, m0, k0 + 2 * BK, tid);
                     LB::load(rb, Bb, B.ld, n0, k0 + 2 * BK, tid);
@@ -213,49 +232,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     const int rbase = m0 + wm * TM + 4 * (lane >> 4);
     const int cbase = n0 + wn * TN + (lane & 15);
 
-    if constexpr (Epi::kind == EpiKind::Affine) {
-        float mul = 1.f;
-        if (epi.mul && epi.mul_pow > 0) {
-            const float f = epi.mul[2 * z];
-            mul = epi.mul_pow == 1 ? f : f * f;
-        }
-        const float ca = epi.ca * mul, cs = epi.cs * mul;
-        half_t* out = epi.out + (int64_t)z * epi.stride_out;
-        const half_t* src = epi.src ? epi.src + (int64_t)z * epi.stride_src : nullptr;
-        const bool mirror = sh.sym && tm != tn;
-        float ss = 0.f;
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-            for (int j = 0; j < FN; ++j) {
-                const int col = cbase + j * 16;
-                half_t hv[4];
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int row = rbase + i * 16 + r;
-                    float v = ca * acc[i][j][r];
-                    if (src) v += cs * (float)src[(int64_t)row * epi.ld_src + col];
-                    hv[r] = (half_t)v;
-                    out[(int64_t)row * epi.ld_out + col] = hv[r];
-                    const float q = (float)hv[r];
-                    ss += q * q;
-                }
-                if (mirror) {
-                    half_t* dst = out + (int64_t)col * epi.ld_out + rbase + i * 16;
-                    *reinterpret_cast<uint2*>(dst) = *reinterpret_cast<const uint2*>(hv);
-                }
-            }
-        if (epi.sumsq) {
-            ss = wave_sum(ss);
-            if (lane == 0) red[wave] = ss;
-            __syncthreads();
-            if (tid == 0) {
-                float t = 0.f;
-                for (int w = 0; w < NT / 64; ++w) t += red[w];
-                epi.sumsq[(int64_t)z * epi.tiles_per_mat + bx] = t;
-            }
-        }
-    } else if constexpr (Epi::kind == EpiKind::Partial) {
+    if constexpr (Epi::kind == EpiKind::Partial) {
         float* out = epi.out + (int64_t)z * epi.stride_mat + (int64_t)split * epi.stride_split;
 #pragma unroll
         for (int i = 0; i < FM; ++i)
@@ -264,53 +241,139 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
                     out[(int64_t)(rbase + i * 16 + r) * epi.ld_out + cbase + j * 16] = acc[i][j][r];
-    } else if constexpr (Epi::kind == EpiKind::ApplyNorm) {
-        const half_t* psi = epi.psi + (int64_t)z * epi.stride_psi;
-        float ss = 0.f;
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-            for (int j = 0; j < FN; ++j) {
-                const int col = cbase + j * 16;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int row = rbase + i * 16 + r;
-                    if (row < epi.rows && col < epi.cols) {
-                        const float t = (float)psi[(int64_t)row * epi.ld_psi + col] + acc[i][j][r];
-                        ss = fmaf(t, t, ss);
-                    }
-                }
-            }
-        ss = wave_sum(ss);
-        if (lane == 0) red[wave] = ss;
-        __syncthreads();
-        if (tid == 0) {
-            float t = 0.f;
-            for (int w = 0; w < NT / 64; ++w) t += red[w];
-            epi.sumsq[(int64_t)z * epi.tiles_per_mat + bx] = t;
-        }
+        return;
     } else {
-        // NormPre-L apply + update.
-        const float t2 = epi.tnorm2[z];
-        const float scale = t2 > 0.f ? epi.target_rms * sqrtf((float)epi.rows * (float)epi.cols) / sqrtf(t2) : 0.f;
-        float* w = epi.ptrs.w[z];
-        const half_t* psi = epi.psi + (int64_t)z * epi.stride_psi;
+        // Per-epilogue set-up.
+        float ca = 1.f, cs = 0.f, scale = 0.f;
+        half_t* out = nullptr;
+        const half_t* src = nullptr;
+        const half_t* psi = nullptr;
+        float* w = nullptr;
+        if constexpr (Epi::kind == EpiKind::Affine) {
+            float mul = 1.f;
+            if (epi.mul && epi.mul_pow > 0) {
+                const float f = epi.mul[2 * z];
+                mul = epi.mul_pow == 1 ? f : f * f;
+            }
+            ca = epi.ca * mul;
+            cs = epi.cs * mul;
+            out = epi.out + (int64_t)z * epi.stride_out;
+            src = epi.src ? epi.src + (int64_t)z * epi.stride_src : nullptr;
+            if (sh.sym && tm != tn) {
+                // Transposed copy of an off-diagonal tile of a symmetric result,
+                // written from registers (4 consecutive halves per lane).
 #pragma unroll
-        for (int i = 0; i < FM; ++i)
+                for (int i = 0; i < FM; ++i)
 #pragma unroll
-            for (int j = 0; j < FN; ++j) {
-                const int col = cbase + j * 16;
+                    for (int j = 0; j < FN; ++j) {
+                        const int col = cbase + j * 16;
+                        half_t hv[4];
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int row = rbase + i * 16 + r;
-                    if (row < epi.rows && col < epi.cols) {
-                        const float t = (float)psi[(int64_t)row * epi.ld_psi + col] + acc[i][j][r];
-                        float* p = w + (int64_t)row * epi.cols + col;
-                        const float wv = *p;
-                        *p = wv - epi.lr * (scale * t + epi.wd * wv);
+                        for (int r = 0; r < 4; ++r) {
+                            const int row = rbase + i * 16 + r;
+                            float v = ca * acc[i][j][r];
+                            if (src) v += cs * (float)src[(int64_t)row * epi.ld_src + col];
+                            hv[r] = (half_t)v;
+                        }
+                        half_t* dst = out + (int64_t)col * epi.ld_out + rbase + i * 16;
+                        *reinterpret_cast<u32x2*>(dst) = *reinterpret_cast<const u32x2*>(hv);
+                    }
+            }
+        } else {
+            psi = epi.psi + (int64_t)z * epi.stride_psi;
+            if constexpr (Epi::kind == EpiKind::Apply) {
+                const float t2 = epi.tnorm2[z];
+                scale = t2 > 0.f ? epi.target_rms * sqrtf((float)epi.rows * (float)epi.cols) / sqrtf(t2) : 0.f;
+                w = epi.ptrs.w[z];
+            }
+        }
+        // Stage one wave-row (TM x BN fp32) at a time in LDS, then walk it
+        // row-contiguously: 8 columns per item (16-byte fp16 accesses).
+        constexpr int LDST = BN + 4;
+        constexpr int C8 = BN / 8;
+        float* stg = reinterpret_cast<float*>(smem);
+        float ss = 0.f;
+#pragma unroll 1
+        for (int pass = 0; pass < WM; ++pass) {
+            __syncthreads();
+            if (wm == pass) {
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < FN; ++j)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            stg[(i * 16 + 4 * (lane >> 4) + r) * LDST + wn * TN + j * 16 + (lane & 15)] = acc[i][j][r];
+            }
+            __syncthreads();
+            for (int c = tid; c < TM * C8; c += NT) {
+                const int r = c / C8, c8 = (c - r * C8) * 8;
+                const int grow = m0 + pass * TM + r, gcol = n0 + c8;
+                const f32x4 lo = *reinterpret_cast<const f32x4*>(stg + r * LDST + c8);
+                const f32x4 hi = *reinterpret_cast<const f32x4*>(stg + r * LDST + c8 + 4);
+                float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                if constexpr (Epi::kind == EpiKind::Affine) {
+                    half_t sv[8];
+                    if (src) *reinterpret_cast<u32x4*>(sv) = *reinterpret_cast<const u32x4*>(src + (int64_t)grow * epi.ld_src + gcol);
+                    half_t hv[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        float x = ca * v[e];
+                        if (src) x += cs * (float)sv[e];
+                        hv[e] = (half_t)x;
+                        const float q = (float)hv[e];
+                        ss += q * q;
+                    }
+                    *reinterpret_cast<u32x4*>(out + (int64_t)grow * epi.ld_out + gcol) = *reinterpret_cast<const u32x4*>(hv);
+                } else {
+                    if (grow >= epi.rows || gcol >= epi.cols) continue;
+                    half_t pv[8];
+                    *reinterpret_cast<u32x4*>(pv) = *reinterpret_cast<const u32x4*>(psi + (int64_t)grow * epi.ld_psi + gcol);
+                    float t[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) t[e] = (float)pv[e] + v[e];
+                    const bool full = gcol + 8 <= epi.cols;
+                    if constexpr (Epi::kind == EpiKind::ApplyNorm) {
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            if (full || gcol + e < epi.cols) ss = fmaf(t[e], t[e], ss);
+                    } else {
+                        float* wp = w + (int64_t)grow * epi.cols + gcol;
+                        if (full && epi.vec_ok) {
+                            f32x4 w0 = *reinterpret_cast<const f32x4*>(wp);
+                            f32x4 w1 = *reinterpret_cast<const f32x4*>(wp + 4);
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                w0[e] = w0[e] - epi.lr * (scale * t[e] + epi.wd * w0[e]);
+                                w1[e] = w1[e] - epi.lr * (scale * t[e + 4] + epi.wd * w1[e]);
+                            }
+                            *reinterpret_cast<f32x4*>(wp) = w0;
+                            *reinterpret_cast<f32x4*>(wp + 4) = w1;
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < 8; ++e)
+                                if (gcol + e < epi.cols) {
+                                    const float wv = wp[e];
+                                    wp[e] = wv - epi.lr * (scale * t[e] + epi.wd * wv);
+                                }
+                        }
                     }
                 }
             }
+        }
+        const bool want_sum = (Epi::kind == EpiKind::ApplyNorm) ||
+                              (Epi::kind == EpiKind::Affine && epi_has_sumsq(epi));
+        if (want_sum) {
+            ss = wave_sum(ss);
+            __syncthreads();
+            if (lane == 0) red[wave] = ss;
+            __syncthreads();
+            if (tid == 0) {
+                float t = 0.f;
+                for (int q = 0; q < NT / 64; ++q) t += red[q];
+                epi_sumsq_ptr(epi)[(int64_t)z * epi_tiles(epi) + bx] = t;
+            }
+        }
     }
 }
 

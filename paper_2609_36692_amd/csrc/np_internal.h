@@ -71,6 +71,7 @@ struct EpiApplyUpdate {
     const float* tnorm2;                // per matrix ||T||_F^2 (from the norm pass)
     int rows, cols;                     // real sizes of W
     float lr, wd, target_rms;
+    int vec_ok;                         // W rows 16-byte aligned (cols % 4 == 0)
     PtrChunk ptrs;                      // w[] used
 };
 
