@@ -290,6 +290,8 @@ int gram_chunk_len(int64_t len) {
 }
 
 int ns_tiles(const Dims& d) { return (int)((d.mp / 128) * (d.np_ / 128)); }
+// Tiles of the NormPre-L apply passes (64 x 128).
+int apply_tiles(const Dims& d) { return (int)((d.mp / 64) * (d.np_ / 128)); }
 int combine_tiles(const Dims& d, TileCfg cfg) {
     const int64_t t = cfg == TileCfg::Big256 ? 256 : 128;
     return (int)((d.mp / t) * (d.np_ / t));
@@ -310,7 +312,7 @@ GWork carve(Arena& ar, const Dims& d, int count, int variant) {
     w.psisq = ar.take<float>(count * d.lp_);
     w.scale = ar.take<float>(count * 2);
     w.colpart = ar.take<double>(count * normalize_cols_partials((int)d.m, (int)d.np_, kColRowChunk));
-    w.sumsq = ar.take<float>(count * ns_tiles(d));
+    w.sumsq = ar.take<float>(count * std::max(ns_tiles(d), apply_tiles(d)));
     w.tn2 = ar.take<float>(count);
     if (variant == NORMPRE_VARIANT_G) {
         w.xb = ar.take<half_t>(count * mn);
@@ -714,12 +716,12 @@ int run_group_l(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
         EpiApplyNorm e{};
         e.psi = w.psi; e.ld_psi = d.np_; e.stride_psi = mn;
         e.rows = (int)d.m; e.cols = (int)d.n;
-        e.sumsq = w.sumsq; e.tiles_per_mat = ns_tiles(d);
+        e.sumsq = w.sumsq; e.tiles_per_mat = apply_tiles(d);
         NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_L_APPLY, 2.0 * d.ell * (double)d.m * d.n * count, 2.0 * d.m * d.n * count,
                      [&] { return launch_gemm_apply_norm(A, B, sh, count, e, sc.s); }),
                "apply norm");
         NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
-                     [&] { return launch_sum_partials(w.sumsq, ns_tiles(d), w.tn2, count, sc.s); }),
+                     [&] { return launch_sum_partials(w.sumsq, apply_tiles(d), w.tn2, count, sc.s); }),
                "t norm");
     }
     for (int c0 = 0; c0 < count; c0 += kChunk) {

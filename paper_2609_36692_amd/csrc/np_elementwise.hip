@@ -119,82 +119,130 @@ __global__ void __launch_bounds__(NT) normalize_rows_kernel(NormArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Column-active orientation.  Block = 64 columns x 4 row lanes, over a chunk
-// of rows.  Pass 1 updates M and writes fp64 partial column sums; pass 2
-// combines the partials in a fixed order and writes Psi.
+// Column-active orientation.  Block = (64 * VW) columns x 4 row lanes over a
+// chunk of rows; each thread owns VW adjacent columns (one 16-byte access per
+// row when VW = 4).  Pass 1 updates M and writes fp64 partial column sums;
+// pass 2 combines the partials in a fixed order and writes Psi.
 constexpr int kColThreads = 256;
 
+template <int VW>
 __global__ void __launch_bounds__(kColThreads) normalize_cols_stats(NormArgs a, double* partials, int row_chunk) {
     const int z = blockIdx.z, chunk = blockIdx.y;
     const int cx = threadIdx.x & 63, ry = threadIdx.x >> 6;
-    const int col = blockIdx.x * 64 + cx;
+    const int col0 = (blockIdx.x * 64 + cx) * VW;
     const int r0 = chunk * row_chunk, r1 = min(a.rows, r0 + row_chunk);
-    double smm = 0.0, smw = 0.0, sww = 0.0;
-    if (col < a.cols) {
+    double smm[VW], smw[VW], sww[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) smm[e] = smw[e] = sww[e] = 0.0;
+    if (col0 < a.cols) {
         float* W = a.ptrs.w[z];
         float* M = a.ptrs.m[z];
         const float* G = a.ptrs.g[z];
         for (int i = r0 + ry; i < r1; i += 4) {
-            const int64_t o = (int64_t)i * a.cols + col;
-            const float m = fmaf(a.mu, M[o], G[o]);
-            M[o] = m;
-            const double md = m, wd = W[o];
-            smm = fma(md, md, smm);
-            smw = fma(md, wd, smw);
-            sww = fma(wd, wd, sww);
+            const int64_t o = (int64_t)i * a.cols + col0;
+            if constexpr (VW == 4) {
+                const float4 mp = *reinterpret_cast<const float4*>(M + o);
+                const float4 g = *reinterpret_cast<const float4*>(G + o);
+                const float4 w = *reinterpret_cast<const float4*>(W + o);
+                const float m[4] = {fmaf(a.mu, mp.x, g.x), fmaf(a.mu, mp.y, g.y), fmaf(a.mu, mp.z, g.z),
+                                    fmaf(a.mu, mp.w, g.w)};
+                *reinterpret_cast<float4*>(M + o) = make_float4(m[0], m[1], m[2], m[3]);
+                const float wv[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const double md = m[e], wd = wv[e];
+                    smm[e] = fma(md, md, smm[e]);
+                    smw[e] = fma(md, wd, smw[e]);
+                    sww[e] = fma(wd, wd, sww[e]);
+                }
+            } else {
+                const float m = fmaf(a.mu, M[o], G[o]);
+                M[o] = m;
+                const double md = m, wd = W[o];
+                smm[0] = fma(md, md, smm[0]);
+                smw[0] = fma(md, wd, smw[0]);
+                sww[0] = fma(wd, wd, sww[0]);
+            }
         }
     }
-    __shared__ double red[3][4][64];
-    red[0][ry][cx] = smm; red[1][ry][cx] = smw; red[2][ry][cx] = sww;
+    __shared__ double red[3][4][64 * VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) {
+        red[0][ry][cx * VW + e] = smm[e];
+        red[1][ry][cx * VW + e] = smw[e];
+        red[2][ry][cx * VW + e] = sww[e];
+    }
     __syncthreads();
-    if (ry == 0) {
-        const int64_t cols_pad = a.ld_psi;
-        const int nchunks = gridDim.y;
-        double* p = partials + ((int64_t)z * nchunks + chunk) * 3 * cols_pad;
-        if (col < cols_pad) {
-            for (int q = 0; q < 3; ++q)
-                p[q * cols_pad + col] = red[q][0][cx] + red[q][1][cx] + red[q][2][cx] + red[q][3][cx];
-        }
+    const int64_t cols_pad = a.ld_psi;
+    const int nchunks = gridDim.y;
+    double* p = partials + ((int64_t)z * nchunks + chunk) * 3 * cols_pad;
+    for (int c = threadIdx.x; c < 3 * 64 * VW; c += kColThreads) {
+        const int q = c / (64 * VW), cc = c - q * (64 * VW);
+        const int64_t col = (int64_t)blockIdx.x * 64 * VW + cc;
+        if (col < cols_pad) p[q * cols_pad + col] = red[q][0][cc] + red[q][1][cc] + red[q][2][cc] + red[q][3][cc];
     }
 }
 
-template <bool DBG>
+template <int VW, bool DBG>
 __global__ void __launch_bounds__(kColThreads) normalize_cols_apply(NormArgs a, const double* partials, int row_chunk) {
     const int z = blockIdx.z, chunk = blockIdx.y;
     const int cx = threadIdx.x & 63, ry = threadIdx.x >> 6;
-    const int col = blockIdx.x * 64 + cx;
+    const int col0 = (blockIdx.x * 64 + cx) * VW;
     const int64_t cols_pad = a.ld_psi;
     const int nchunks = (a.rows + row_chunk - 1) / row_chunk;
     half_t* P = a.psi + (int64_t)z * a.stride_psi;
     const int r0 = chunk * row_chunk, r1 = min((int)a.rows_pad, r0 + row_chunk);
-    if (col >= a.cols) {
-        if (col < cols_pad)
-            for (int i = r0 + ry; i < r1; i += 4) P[(int64_t)i * cols_pad + col] = (half_t)0.f;
-        return;
-    }
-    double smm = 0.0, smw = 0.0, sww = 0.0;
+    if (col0 >= cols_pad) return;
+    float df[VW], inv[VW];
     const double* p = partials + (int64_t)z * nchunks * 3 * cols_pad;
-    for (int c = 0; c < nchunks; ++c) {
-        smm += p[(c * 3 + 0) * cols_pad + col];
-        smw += p[(c * 3 + 1) * cols_pad + col];
-        sww += p[(c * 3 + 2) * cols_pad + col];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) {
+        const int col = col0 + e;
+        df[e] = 0.f;
+        inv[e] = 0.f;
+        if (col < a.cols) {
+            double smm = 0.0, smw = 0.0, sww = 0.0;
+            for (int c = 0; c < nchunks; ++c) {
+                smm += p[(c * 3 + 0) * cols_pad + col];
+                smw += p[(c * 3 + 1) * cols_pad + col];
+                sww += p[(c * 3 + 2) * cols_pad + col];
+            }
+            const double d = smw;
+            const double nrm2 = fmax(smm + d * d * (sww - 2.0), 0.0);
+            inv[e] = (float)(1.0 / fmax(sqrt(nrm2), (double)a.eps));
+            df[e] = (float)d;
+            if (chunk == 0 && ry == 0)
+                a.psisq[(int64_t)z * a.stride_psisq + col] = (float)(nrm2 * (double)inv[e] * (double)inv[e]);
+        }
     }
-    const double d = smw;
-    const double nrm2 = fmax(smm + d * d * (sww - 2.0), 0.0);
-    const float inv = (float)(1.0 / fmax(sqrt(nrm2), (double)a.eps));
-    const float df = (float)d;
-    if (chunk == 0 && ry == 0)
-        a.psisq[(int64_t)z * a.stride_psisq + col] = (float)(nrm2 * (double)inv * (double)inv);
     const float* W = a.ptrs.w[z];
     const float* M = a.ptrs.m[z];
     for (int i = r0 + ry; i < r1; i += 4) {
-        float v = 0.f;
-        if (i < a.rows) {
-            const int64_t o = (int64_t)i * a.cols + col;
-            v = (M[o] - df * W[o]) * inv;
-            if constexpr (DBG) a.psi32[(int64_t)z * a.stride_psi32 + o] = v;
+        half_t* prow = P + (int64_t)i * cols_pad + col0;
+        if constexpr (VW == 4) {
+            float v[4] = {0.f, 0.f, 0.f, 0.f};
+            if (i < a.rows && col0 < a.cols) {
+                const int64_t o = (int64_t)i * a.cols + col0;
+                const float4 m = *reinterpret_cast<const float4*>(M + o);
+                const float4 w = *reinterpret_cast<const float4*>(W + o);
+                v[0] = (m.x - df[0] * w.x) * inv[0];
+                v[1] = (m.y - df[1] * w.y) * inv[1];
+                v[2] = (m.z - df[2] * w.z) * inv[2];
+                v[3] = (m.w - df[3] * w.w) * inv[3];
+                if constexpr (DBG)
+                    *reinterpret_cast<float4*>(a.psi32 + (int64_t)z * a.stride_psi32 + o) = make_float4(v[0], v[1], v[2], v[3]);
+            }
+            half_t h[4] = {(half_t)v[0], (half_t)v[1], (half_t)v[2], (half_t)v[3]};
+            *reinterpret_cast<uint2*>(prow) = *reinterpret_cast<const uint2*>(h);
+        } else {
+            float v = 0.f;
+            if (i < a.rows && col0 < a.cols) {
+                const int64_t o = (int64_t)i * a.cols + col0;
+                v = (M[o] - df[0] * W[o]) * inv[0];
+                if constexpr (DBG) a.psi32[(int64_t)z * a.stride_psi32 + o] = v;
+            }
+            prow[0] = (half_t)v;
         }
-        P[(int64_t)i * cols_pad + col] = (half_t)v;
     }
 }
 
@@ -310,21 +358,30 @@ int64_t normalize_cols_partials(int rows, int cols_pad, int row_chunk) {
     return (int64_t)nchunks * 3 * cols_pad;
 }
 
-hipError_t launch_normalize_cols(const NormArgs& a, int batch, double* partials, int row_chunk, hipStream_t s) {
+template <int VW>
+hipError_t cols_launch(const NormArgs& a, int batch, double* partials, int row_chunk, hipStream_t s) {
     const int nchunks = (a.rows + row_chunk - 1) / row_chunk;
     const int pad_chunks = (int)((a.rows_pad + row_chunk - 1) / row_chunk);
-    const unsigned col_blocks = (unsigned)((a.ld_psi + 63) / 64);
-    hipLaunchKernelGGL(normalize_cols_stats, dim3(col_blocks, nchunks, batch), dim3(kColThreads), 0, s,
-                       a, partials, row_chunk);
+    const unsigned stat_blocks = (unsigned)((a.cols + 64 * VW - 1) / (64 * VW));
+    // The stats pass writes partials for every padded column block it covers;
+    // padded columns beyond the last real block are never read.
+    hipLaunchKernelGGL((normalize_cols_stats<VW>), dim3(stat_blocks, nchunks, batch), dim3(kColThreads), 0, s, a,
+                       partials, row_chunk);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    const unsigned app_blocks = (unsigned)((a.ld_psi + 64 * VW - 1) / (64 * VW));
     if (a.psi32)
-        hipLaunchKernelGGL((normalize_cols_apply<true>), dim3(col_blocks, pad_chunks, batch), dim3(kColThreads), 0, s,
-                           a, (const double*)partials, row_chunk);
+        hipLaunchKernelGGL((normalize_cols_apply<VW, true>), dim3(app_blocks, pad_chunks, batch), dim3(kColThreads), 0,
+                           s, a, (const double*)partials, row_chunk);
     else
-        hipLaunchKernelGGL((normalize_cols_apply<false>), dim3(col_blocks, pad_chunks, batch), dim3(kColThreads), 0, s,
-                           a, (const double*)partials, row_chunk);
+        hipLaunchKernelGGL((normalize_cols_apply<VW, false>), dim3(app_blocks, pad_chunks, batch), dim3(kColThreads), 0,
+                           s, a, (const double*)partials, row_chunk);
     return hipGetLastError();
+}
+
+hipError_t launch_normalize_cols(const NormArgs& a, int batch, double* partials, int row_chunk, hipStream_t s) {
+    if (a.vec_ok && a.cols % 4 == 0 && a.ld_psi % 4 == 0) return cols_launch<4>(a, batch, partials, row_chunk, s);
+    return cols_launch<1>(a, batch, partials, row_chunk, s);
 }
 
 hipError_t launch_psi_scale(const float* psisq, int64_t stride, int active_rows, float eps, float* out,

@@ -306,6 +306,69 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                             stg[(i * 16 + 4 * (lane >> 4) + r) * LDST + wn * TN + j * 16 + (lane & 15)] = acc[i][j][r];
             }
             __syncthreads();
+            constexpr int ITEMS = (TM * C8 + NT - 1) / NT;
+            if constexpr (Epi::kind == EpiKind::Apply || Epi::kind == EpiKind::ApplyNorm) {
+                // Issue every item's Psi (and W) loads before using any of them.
+                u32x4 pbuf[ITEMS];
+                f32x4 wbuf[ITEMS][2];
+                bool okv[ITEMS];
+#pragma unroll
+                for (int it = 0; it < ITEMS; ++it) {
+                    const int c = tid + it * NT;
+                    const int r = c / C8, c8 = (c - r * C8) * 8;
+                    const int grow = m0 + pass * TM + r, gcol = n0 + c8;
+                    okv[it] = c < TM * C8 && grow < epi.rows && gcol < epi.cols;
+                    if (okv[it]) {
+                        pbuf[it] = *reinterpret_cast<const u32x4*>(psi + (int64_t)grow * epi.ld_psi + gcol);
+                        if constexpr (Epi::kind == EpiKind::Apply) {
+                            if (gcol + 8 <= epi.cols && epi.vec_ok) {
+                                const float* wp = w + (int64_t)grow * epi.cols + gcol;
+                                wbuf[it][0] = *reinterpret_cast<const f32x4*>(wp);
+                                wbuf[it][1] = *reinterpret_cast<const f32x4*>(wp + 4);
+                            }
+                        }
+                    }
+                }
+#pragma unroll
+                for (int it = 0; it < ITEMS; ++it) {
+                    if (!okv[it]) continue;
+                    const int c = tid + it * NT;
+                    const int r = c / C8, c8 = (c - r * C8) * 8;
+                    const int grow = m0 + pass * TM + r, gcol = n0 + c8;
+                    const f32x4 lo = *reinterpret_cast<const f32x4*>(stg + r * LDST + c8);
+                    const f32x4 hi = *reinterpret_cast<const f32x4*>(stg + r * LDST + c8 + 4);
+                    const half_t* pv = reinterpret_cast<const half_t*>(&pbuf[it]);
+                    float t[8];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) { t[e] = (float)pv[e] + lo[e]; t[e + 4] = (float)pv[e + 4] + hi[e]; }
+                    const bool full = gcol + 8 <= epi.cols;
+                    if constexpr (Epi::kind == EpiKind::ApplyNorm) {
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            if (full || gcol + e < epi.cols) ss = fmaf(t[e], t[e], ss);
+                    } else {
+                        float* wp = w + (int64_t)grow * epi.cols + gcol;
+                        if (full && epi.vec_ok) {
+                            f32x4 w0 = wbuf[it][0], w1 = wbuf[it][1];
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                w0[e] = w0[e] - epi.lr * (scale * t[e] + epi.wd * w0[e]);
+                                w1[e] = w1[e] - epi.lr * (scale * t[e + 4] + epi.wd * w1[e]);
+                            }
+                            *reinterpret_cast<f32x4*>(wp) = w0;
+                            *reinterpret_cast<f32x4*>(wp + 4) = w1;
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < 8; ++e)
+                                if (gcol + e < epi.cols) {
+                                    const float wv = wp[e];
+                                    wp[e] = wv - epi.lr * (scale * t[e] + epi.wd * wv);
+                                }
+                        }
+                    }
+                }
+                continue;
+            }
             for (int c = tid; c < TM * C8; c += NT) {
                 const int r = c / C8, c8 = (c - r * C8) * 8;
                 const int grow = m0 + pass * TM + r, gcol = n0 + c8;
@@ -325,39 +388,6 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                         ss += q * q;
                     }
                     *reinterpret_cast<u32x4*>(out + (int64_t)grow * epi.ld_out + gcol) = *reinterpret_cast<const u32x4*>(hv);
-                } else {
-                    if (grow >= epi.rows || gcol >= epi.cols) continue;
-                    half_t pv[8];
-                    *reinterpret_cast<u32x4*>(pv) = *reinterpret_cast<const u32x4*>(psi + (int64_t)grow * epi.ld_psi + gcol);
-                    float t[8];
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) t[e] = (float)pv[e] + v[e];
-                    const bool full = gcol + 8 <= epi.cols;
-                    if constexpr (Epi::kind == EpiKind::ApplyNorm) {
-#pragma unroll
-                        for (int e = 0; e < 8; ++e)
-                            if (full || gcol + e < epi.cols) ss = fmaf(t[e], t[e], ss);
-                    } else {
-                        float* wp = w + (int64_t)grow * epi.cols + gcol;
-                        if (full && epi.vec_ok) {
-                            f32x4 w0 = *reinterpret_cast<const f32x4*>(wp);
-                            f32x4 w1 = *reinterpret_cast<const f32x4*>(wp + 4);
-#pragma unroll
-                            for (int e = 0; e < 4; ++e) {
-                                w0[e] = w0[e] - epi.lr * (scale * t[e] + epi.wd * w0[e]);
-                                w1[e] = w1[e] - epi.lr * (scale * t[e + 4] + epi.wd * w1[e]);
-                            }
-                            *reinterpret_cast<f32x4*>(wp) = w0;
-                            *reinterpret_cast<f32x4*>(wp + 4) = w1;
-                        } else {
-#pragma unroll
-                            for (int e = 0; e < 8; ++e)
-                                if (gcol + e < epi.cols) {
-                                    const float wv = wp[e];
-                                    wp[e] = wv - epi.lr * (scale * t[e] + epi.wd * wv);
-                                }
-                        }
-                    }
                 }
             }
         }
@@ -414,7 +444,7 @@ int gemm_tile_m(TileCfg cfg) {
         case TileCfg::Big256: return 256;
         case TileCfg::Skinny64: return 64;
         case TileCfg::Skinny128: return 128;
-        case TileCfg::Apply: return 128;
+        case TileCfg::Apply: return 64;
     }
     return 0;
 }
@@ -462,14 +492,14 @@ hipError_t launch_gemm_apply(Operand A, Operand B, GemmShape sh, int batch,
                              const EpiApplyUpdate& e, hipStream_t s) {
     EApp ee;
     static_cast<EpiApplyUpdate&>(ee) = e;
-    return run<128, 128, 2, 2, 0>(A, B, sh, batch, ee, s);
+    return run<64, 128, 1, 4, 0>(A, B, sh, batch, ee, s);
 }
 
 hipError_t launch_gemm_apply_norm(Operand A, Operand B, GemmShape sh, int batch,
                                   const EpiApplyNorm& e, hipStream_t s) {
     EAppN ee;
     static_cast<EpiApplyNorm&>(ee) = e;
-    return run<128, 128, 2, 2, 0>(A, B, sh, batch, ee, s);
+    return run<64, 128, 1, 4, 0>(A, B, sh, batch, ee, s);
 }
 
 }  // namespace np
