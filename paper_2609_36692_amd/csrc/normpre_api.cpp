@@ -26,7 +26,7 @@ constexpr int64_t kMaxDim = int64_t(1) << 20;
 constexpr int64_t kMaxElems = int64_t(1) << 31;
 constexpr int kMaxRowLen = 32768;   // row-active register kernel limit
 constexpr int kMaxEll = 384;
-constexpr int kColRowChunk = 64;    // rows per block in the column-active pass
+constexpr int kColRowChunk = 128;   // rows per block in the column-active pass
 constexpr int kGramMaxChunks = 32;  // at most this many length chunks in the fp64 Gram
 constexpr int kMaxSplits = 16;
 constexpr int kEigSweeps = 30;

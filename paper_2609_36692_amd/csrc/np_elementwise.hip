@@ -183,6 +183,28 @@ __global__ void __launch_bounds__(kColThreads) normalize_cols_stats(NormArgs a, 
     }
 }
 
+// Sums the row-chunk partials of each column once, in a fixed order, and
+// stores d = <m, w> and 1 / max(||x||, eps) in the chunk-0 slots.
+__global__ void __launch_bounds__(256) normalize_cols_finalize(NormArgs a, double* partials, int nchunks) {
+    const int z = blockIdx.y;
+    const int col = blockIdx.x * 256 + threadIdx.x;
+    if (col >= a.cols) return;
+    const int64_t cols_pad = a.ld_psi;
+    double* p = partials + (int64_t)z * nchunks * 3 * cols_pad;
+    double smm = 0.0, smw = 0.0, sww = 0.0;
+    for (int c = 0; c < nchunks; ++c) {
+        smm += p[(c * 3 + 0) * cols_pad + col];
+        smw += p[(c * 3 + 1) * cols_pad + col];
+        sww += p[(c * 3 + 2) * cols_pad + col];
+    }
+    const double d = smw;
+    const double nrm2 = fmax(smm + d * d * (sww - 2.0), 0.0);
+    const double inv = 1.0 / fmax(sqrt(nrm2), (double)a.eps);
+    p[col] = d;
+    p[cols_pad + col] = inv;
+    a.psisq[(int64_t)z * a.stride_psisq + col] = (float)(nrm2 * inv * inv);
+}
+
 template <int VW, bool DBG>
 __global__ void __launch_bounds__(kColThreads) normalize_cols_apply(NormArgs a, const double* partials, int row_chunk) {
     const int z = blockIdx.z, chunk = blockIdx.y;
@@ -198,22 +220,8 @@ __global__ void __launch_bounds__(kColThreads) normalize_cols_apply(NormArgs a, 
 #pragma unroll
     for (int e = 0; e < VW; ++e) {
         const int col = col0 + e;
-        df[e] = 0.f;
-        inv[e] = 0.f;
-        if (col < a.cols) {
-            double smm = 0.0, smw = 0.0, sww = 0.0;
-            for (int c = 0; c < nchunks; ++c) {
-                smm += p[(c * 3 + 0) * cols_pad + col];
-                smw += p[(c * 3 + 1) * cols_pad + col];
-                sww += p[(c * 3 + 2) * cols_pad + col];
-            }
-            const double d = smw;
-            const double nrm2 = fmax(smm + d * d * (sww - 2.0), 0.0);
-            inv[e] = (float)(1.0 / fmax(sqrt(nrm2), (double)a.eps));
-            df[e] = (float)d;
-            if (chunk == 0 && ry == 0)
-                a.psisq[(int64_t)z * a.stride_psisq + col] = (float)(nrm2 * (double)inv[e] * (double)inv[e]);
-        }
+        df[e] = col < a.cols ? (float)p[col] : 0.f;
+        inv[e] = col < a.cols ? (float)p[cols_pad + col] : 0.f;
     }
     const float* W = a.ptrs.w[z];
     const float* M = a.ptrs.m[z];
@@ -368,6 +376,10 @@ hipError_t cols_launch(const NormArgs& a, int batch, double* partials, int row_c
     hipLaunchKernelGGL((normalize_cols_stats<VW>), dim3(stat_blocks, nchunks, batch), dim3(kColThreads), 0, s, a,
                        partials, row_chunk);
     hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(normalize_cols_finalize, dim3((unsigned)((a.cols + 255) / 256), batch), dim3(256), 0, s, a,
+                       partials, nchunks);
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
     const unsigned app_blocks = (unsigned)((a.ld_psi + 64 * VW - 1) / (64 * VW));
     if (a.psi32)
