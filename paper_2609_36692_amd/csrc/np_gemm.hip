@@ -149,8 +149,10 @@ __device__ __forceinline__ void xcd_remap(int& bx, int& by, int& bz) {
     bz = lin / gy;
 }
 
+// At least two waves per SIMD: two 4-wave blocks (or one 8-wave block) per
+// CU, so one block's MFMAs overlap the other's LDS and barrier waits.
 template <int BM, int BN, int WM, int WN, int LAYOUT, class Epi>
-__global__ void __launch_bounds__(WM * WN * 64)
+__global__ void __launch_bounds__(WM * WN * 64, 2)
 gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     constexpr int NT = WM * WN * 64;
     constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 16, FN = TN / 16;
