@@ -27,10 +27,11 @@ constexpr int64_t kMaxElems = int64_t(1) << 31;
 constexpr int kMaxRowLen = 32768;   // row-active register kernel limit
 constexpr int kMaxEll = 384;
 constexpr int kColRowChunk = 128;   // rows per block in the column-active pass
-constexpr int kGramMaxChunks = 32;  // at most this many length chunks in the fp64 Gram
+constexpr int kGramChunks = 16;     // fixed chunk slots of the fp64 Gram (unused slots hold zeros)
 constexpr int kMaxSplits = 16;
 constexpr int kEigSweeps = 30;
-constexpr size_t kGroupBudget = size_t(24) << 30;  // workspace bytes per group
+constexpr size_t kGroupBudget = size_t(24) << 30;  // workspace bytes per item
+constexpr size_t kRoundBudget = size_t(48) << 30;  // workspace bytes per round
 
 struct Fail {
     int code;
@@ -283,10 +284,10 @@ Dims dims_of(int64_t m, int64_t n, int k, const normpre_hparams& hp) {
     return d;
 }
 
-// Length chunk of the fp64 Gram: >= 256 for parallel blocks, at most
-// kGramMaxChunks chunks so the consumers sum few partials.
+// Length chunk of the fp64 Gram: >= 256 for parallel blocks and at most
+// kGramChunks chunks (the consumers always sum kGramChunks slots).
 int gram_chunk_len(int64_t len) {
-    return (int)std::max<int64_t>(256, round_up((len + kGramMaxChunks - 1) / kGramMaxChunks, 64));
+    return (int)std::max<int64_t>(256, round_up((len + kGramChunks - 1) / kGramChunks, 64));
 }
 
 int ns_tiles(const Dims& d) { return (int)((d.mp / 128) * (d.np_ / 128)); }
@@ -305,8 +306,40 @@ int pick_splits(int64_t tiles_per_mat, int count, int64_t k_len) {
     return splits;
 }
 
-GWork carve(Arena& ar, const Dims& d, int count, int variant) {
+// One batch of equal-shape matrices (a sub-range of a shape group).
+struct Item {
+    int g = 0;            // shape group
+    int first = 0;        // first position in the group's list
+    int count = 0;
+    Dims d{};
     GWork w{};
+    int pool = -1;        // pool of its small matrices
+    int pool_off = 0;     // its first matrix inside the pool
+};
+
+// Small matrices shared by the items of a round that have the same width:
+// the s x s Newton-Schulz matrices (NormPre-G, keyed by s) or the l x l
+// sketch matrices (NormPre-L, keyed by l), so one launch covers all of them.
+struct Pool {
+    int64_t key = 0;
+    int count = 0;
+    int64_t sp = 0;
+    int ell = 0, ellp = 0, top = 0;
+    half_t* amat = nullptr;
+    half_t* bmat = nullptr;
+    double* gpart = nullptr;
+    double* chol = nullptr;
+    float* rinv = nullptr;
+    float* kmat = nullptr;
+    float* eigs = nullptr;
+    float* ritz = nullptr;
+    int* nsel = nullptr;
+};
+
+void carve_item(Arena& ar, Item& it, int variant) {
+    const Dims& d = it.d;
+    const int count = it.count;
+    GWork& w = it.w;
     const int64_t mn = d.mp * d.np_;
     w.psi = ar.take<half_t>(count * mn);
     w.psisq = ar.take<float>(count * d.lp_);
@@ -316,8 +349,6 @@ GWork carve(Arena& ar, const Dims& d, int count, int variant) {
     w.tn2 = ar.take<float>(count);
     if (variant == NORMPRE_VARIANT_G) {
         w.xb = ar.take<half_t>(count * mn);
-        w.amat = ar.take<half_t>(count * d.sp * d.sp);
-        w.bmat = ar.take<half_t>(count * d.sp * d.sp);
     } else {
         const int64_t lp = d.ellp, maxpad = d.lp_;
         // Every l-major skinny buffer (Omega^T included) has the per-matrix
@@ -328,23 +359,64 @@ GWork carve(Arena& ar, const Dims& d, int count, int variant) {
             w.v32[i] = ar.take<float>(count * lp * maxpad);
         }
         w.part = ar.take<float>(count * (int64_t)kMaxSplits * lp * maxpad);
-        w.gpart = ar.take<double>(count * (int64_t)(kGramMaxChunks + 1) * lp * lp);
-        w.chol = ar.take<double>(count * 2 * lp * lp);
-        w.rinv = ar.take<float>(count * lp * lp);
-        w.kmat = ar.take<float>(count * lp * lp);
         w.qlen = ar.take<half_t>(count * d.a_pad * lp);
         w.flen = ar.take<half_t>(count * d.b_pad * lp);
-        w.eigs = ar.take<float>(count * 2 * lp * lp);
-        w.ritz = ar.take<float>(count * (int64_t)d.top);
-        w.nsel = ar.take<int>(count);
     }
-    return w;
 }
 
-size_t group_bytes(const Dims& d, int count, int variant) {
-    Arena ar{nullptr, 0, 0};
-    carve(ar, d, count, variant);
+void carve_pool(Arena& ar, Pool& p, int variant) {
+    const int64_t c = p.count;
+    if (variant == NORMPRE_VARIANT_G) {
+        p.amat = ar.take<half_t>(c * p.sp * p.sp);
+        p.bmat = ar.take<half_t>(c * p.sp * p.sp);
+    } else {
+        const int64_t lp = p.ellp;
+        p.gpart = ar.take<double>(c * kGramChunks * lp * lp);
+        p.chol = ar.take<double>(c * 2 * lp * lp);
+        p.rinv = ar.take<float>(c * lp * lp);
+        p.kmat = ar.take<float>(c * lp * lp);
+        p.eigs = ar.take<float>(c * 2 * lp * lp);
+        p.ritz = ar.take<float>(c * (int64_t)p.top);
+        p.nsel = ar.take<int>(c);
+    }
+}
+
+// Assigns every item to the pool of its width; returns the pools.
+std::vector<Pool> make_pools(std::vector<Item>& items, int variant) {
+    std::vector<Pool> pools;
+    for (Item& it : items) {
+        const int64_t key = variant == NORMPRE_VARIANT_G ? it.d.sp : it.d.ell;
+        int pi = -1;
+        for (size_t q = 0; q < pools.size(); ++q)
+            if (pools[q].key == key) pi = (int)q;
+        if (pi < 0) {
+            Pool p;
+            p.key = key;
+            p.sp = it.d.sp;
+            p.ell = it.d.ell;
+            p.ellp = it.d.ellp;
+            p.top = it.d.top;
+            pools.push_back(p);
+            pi = (int)pools.size() - 1;
+        }
+        it.pool = pi;
+        it.pool_off = pools[pi].count;
+        pools[pi].count += it.count;
+    }
+    return pools;
+}
+
+// Carves a round's items and pools; with a null arena base it only measures.
+size_t carve_round(Arena& ar, std::vector<Item>& items, std::vector<Pool>& pools, int variant) {
+    for (Item& it : items) carve_item(ar, it, variant);
+    for (Pool& p : pools) carve_pool(ar, p, variant);
     return ar.off + 256;
+}
+
+size_t round_bytes(std::vector<Item> items, int variant) {
+    std::vector<Pool> pools = make_pools(items, variant);
+    Arena ar{nullptr, 0, 0};
+    return carve_round(ar, items, pools, variant);
 }
 
 struct StepCtx {
@@ -356,7 +428,9 @@ struct StepCtx {
     float* const* M;
     int variant;
     bool debug;
+    const std::vector<Group>* groups;
 };
+
 
 #define NP_TRY(expr, what)                                  \
     do {                                                    \
@@ -444,78 +518,85 @@ TileCfg ns_cfg(int64_t M, int64_t N, bool sym, int count) {
     return tiles * count >= 512 ? TileCfg::Big256 : TileCfg::Big;
 }
 
-int run_group_g(const StepCtx& sc, const Dims& d, const GWork& w, const std::vector<int>& idx, int first, int count,
-                DebugMat* dbg) {
-    int rc = run_normalize(sc, d, w, idx, first, count, dbg);
-    if (rc) return rc;
-    const normpre_hparams& hp = *sc.hp;
+int gram_launch(const StepCtx& sc, const Item& it, const Pool& pl, half_t* x, bool first_it) {
+    const Dims& d = it.d;
+    const int count = it.count;
     const int64_t mn = d.mp * d.np_, ss = d.sp * d.sp;
     const double s_ = (double)std::min(d.m, d.n), l_ = (double)std::max(d.m, d.n);
-    const int q = hp.ns_iters;
-    half_t* bufs[2] = {w.psi, w.xb};
-    for (int it = 0; it < q; ++it) {
-        half_t* x = bufs[it & 1];
-        half_t* xn = bufs[(it + 1) & 1];
-        const bool first_it = it == 0, last_it = it == q - 1;
-        // A = X X^T (wide) or Y^T Y (tall), times c^2 on the first iteration.
-        {
-            Operand A{x, d.np_, mn}, B{x, d.np_, mn};
-            GemmShape sh{(int)d.sp, (int)d.sp, (int)d.lp_, 1, (int)d.lp_, 1};
-            EpiAffine e{};
-            e.out = w.amat; e.ld_out = d.sp; e.stride_out = ss;
-            e.mul = first_it ? w.scale : nullptr; e.mul_pow = first_it ? 2 : 0;
-            e.ca = 1.f; e.cs = 0.f;
-            const int layout = d.tall ? 2 : 0;
-            const TileCfg cfg = ns_cfg(d.sp, d.sp, true, count);
-            NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_GRAM, 2.0 * s_ * s_ * l_ * count,
-                         2.0 * (s_ * l_ + s_ * s_) * count,
-                         [&] { return launch_gemm_affine(cfg, layout, A, B, sh, count, e, sc.s); }),
-                   "ns gram");
+    // A = X X^T (wide) or Y^T Y (tall), times c^2 on the first iteration.
+    Operand A{x, d.np_, mn}, B{x, d.np_, mn};
+    GemmShape sh{(int)d.sp, (int)d.sp, (int)d.lp_, 1, (int)d.lp_, 1};
+    EpiAffine e{};
+    e.out = pl.amat + (int64_t)it.pool_off * ss; e.ld_out = d.sp; e.stride_out = ss;
+    e.mul = first_it ? it.w.scale : nullptr; e.mul_pow = first_it ? 2 : 0;
+    e.ca = 1.f; e.cs = 0.f;
+    const int layout = d.tall ? 2 : 0;
+    const TileCfg cfg = ns_cfg(d.sp, d.sp, true, count);
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_GRAM, 2.0 * s_ * s_ * l_ * count, 2.0 * (s_ * l_ + s_ * s_) * count,
+                 [&] { return launch_gemm_affine(cfg, layout, A, B, sh, count, e, sc.s); }),
+           "ns gram");
+    return NORMPRE_OK;
+}
+
+int poly_launch(const StepCtx& sc, const Pool& pl, double nominal_flops) {
+    // B = b A + c A^2 for every matrix of the pool in one launch.
+    const int64_t sp = pl.sp, ss = sp * sp;
+    Operand A{pl.amat, sp, ss}, B{pl.amat, sp, ss};
+    GemmShape sh{(int)sp, (int)sp, (int)sp, 1, (int)sp, 1};
+    EpiAffine e{};
+    e.out = pl.bmat; e.ld_out = sp; e.stride_out = ss;
+    e.src = pl.amat; e.ld_src = sp; e.stride_src = ss;
+    e.ca = sc.hp->ns_coeffs[2]; e.cs = sc.hp->ns_coeffs[1];
+    const TileCfg cfg = ns_cfg(sp, sp, true, pl.count);
+    // Nominal FLOPs use the real s of each matrix (padding excluded).
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_POLY, nominal_flops, 6.0 * nominal_flops / (double)sp,
+                 [&] { return launch_gemm_affine(cfg, 0, A, B, sh, pl.count, e, sc.s); }),
+           "ns poly");
+    return NORMPRE_OK;
+}
+
+int combine_launch(const StepCtx& sc, const Item& it, const Pool& pl, half_t* x, half_t* xn, bool first_it,
+                   bool last_it) {
+    const Dims& d = it.d;
+    const int count = it.count;
+    const int64_t mn = d.mp * d.np_, ss = d.sp * d.sp;
+    const double s_ = (double)std::min(d.m, d.n), l_ = (double)std::max(d.m, d.n);
+    half_t* bmat = pl.bmat + (int64_t)it.pool_off * ss;
+    EpiAffine e{};
+    e.out = xn; e.ld_out = d.np_; e.stride_out = mn;
+    e.src = x; e.ld_src = d.np_; e.stride_src = mn;
+    e.mul = first_it ? it.w.scale : nullptr; e.mul_pow = first_it ? 1 : 0;
+    e.ca = 1.f; e.cs = sc.hp->ns_coeffs[0];
+    const TileCfg cfg = ns_cfg(d.mp, d.np_, false, count);
+    e.sumsq = last_it ? it.w.sumsq : nullptr;
+    e.tiles_per_mat = combine_tiles(d, cfg);
+    auto go = [&]() -> hipError_t {
+        if (!d.tall) {
+            // X <- a X + B X
+            Operand A{bmat, d.sp, ss}, B{x, d.np_, mn};
+            GemmShape sh{(int)d.sp, (int)d.lp_, (int)d.sp, 1, (int)d.sp, 0};
+            return launch_gemm_affine(cfg, 1, A, B, sh, count, e, sc.s);
         }
-        // B = b A + c A^2
-        {
-            Operand A{w.amat, d.sp, ss}, B{w.amat, d.sp, ss};
-            GemmShape sh{(int)d.sp, (int)d.sp, (int)d.sp, 1, (int)d.sp, 1};
-            EpiAffine e{};
-            e.out = w.bmat; e.ld_out = d.sp; e.stride_out = ss;
-            e.src = w.amat; e.ld_src = d.sp; e.stride_src = ss;
-            e.ca = hp.ns_coeffs[2]; e.cs = hp.ns_coeffs[1];
-            const TileCfg cfg = ns_cfg(d.sp, d.sp, true, count);
-            NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_POLY, 2.0 * s_ * s_ * s_ * count, 6.0 * s_ * s_ * count,
-                         [&] { return launch_gemm_affine(cfg, 0, A, B, sh, count, e, sc.s); }),
-                   "ns poly");
-        }
-        // X <- a X + B X (wide) or Y <- a Y + Y B (tall), times c on the first iteration.
-        {
-            EpiAffine e{};
-            e.out = xn; e.ld_out = d.np_; e.stride_out = mn;
-            e.src = x; e.ld_src = d.np_; e.stride_src = mn;
-            e.mul = first_it ? w.scale : nullptr; e.mul_pow = first_it ? 1 : 0;
-            e.ca = 1.f; e.cs = hp.ns_coeffs[0];
-            const TileCfg cfg = ns_cfg(d.mp, d.np_, false, count);
-            e.sumsq = last_it ? w.sumsq : nullptr;
-            e.tiles_per_mat = combine_tiles(d, cfg);
-            hipError_t (*fn)(TileCfg, int, Operand, Operand, GemmShape, int, const EpiAffine&, hipStream_t) =
-                launch_gemm_affine;
-            auto go = [&]() -> hipError_t {
-                if (!d.tall) {
-                    Operand A{w.bmat, d.sp, ss}, B{x, d.np_, mn};
-                    GemmShape sh{(int)d.sp, (int)d.lp_, (int)d.sp, 1, (int)d.sp, 0};
-                    return fn(cfg, 1, A, B, sh, count, e, sc.s);
-                }
-                Operand A{x, d.np_, mn}, B{w.bmat, d.sp, ss};
-                GemmShape sh{(int)d.lp_, (int)d.sp, (int)d.sp, 1, (int)d.sp, 0};
-                return fn(cfg, 0, A, B, sh, count, e, sc.s);
-            };
-            NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_COMBINE, 2.0 * s_ * s_ * l_ * count,
-                         2.0 * (2.0 * s_ * l_ + s_ * s_) * count, go),
-                   "ns combine");
-        }
-    }
-    const half_t* t = bufs[q & 1];
+        // Y <- a Y + Y B
+        Operand A{x, d.np_, mn}, B{bmat, d.sp, ss};
+        GemmShape sh{(int)d.lp_, (int)d.sp, (int)d.sp, 1, (int)d.sp, 0};
+        return launch_gemm_affine(cfg, 0, A, B, sh, count, e, sc.s);
+    };
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_COMBINE, 2.0 * s_ * s_ * l_ * count, 2.0 * (2.0 * s_ * l_ + s_ * s_) * count,
+                 go),
+           "ns combine");
+    return NORMPRE_OK;
+}
+
+int g_update_launch(const StepCtx& sc, const Item& it, const half_t* t, DebugMat* dbg) {
+    const Dims& d = it.d;
+    const normpre_hparams& hp = *sc.hp;
+    const std::vector<int>& idx = (*sc.groups)[it.g].idx;
+    const int first = it.first, count = it.count;
+    const int64_t mn = d.mp * d.np_;
     const int t_tiles = combine_tiles(d, ns_cfg(d.mp, d.np_, false, count));
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
-                 [&] { return launch_sum_partials(w.sumsq, t_tiles, w.tn2, count, sc.s); }),
+                 [&] { return launch_sum_partials(it.w.sumsq, t_tiles, it.w.tn2, count, sc.s); }),
            "t norm");
     for (int c0 = 0; c0 < count; c0 += kChunk) {
         const int cnt = std::min(kChunk, count - c0);
@@ -526,22 +607,17 @@ int run_group_g(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
         a.t = t + (int64_t)c0 * mn;
         a.ld_t = d.np_;
         a.stride_t = mn;
-        a.tnorm2 = w.tn2 + c0;
+        a.tnorm2 = it.w.tn2 + c0;
         a.lr = hp.lr;
         a.wd = hp.weight_decay;
         a.target_rms = hp.target_rms;
         a.vec_ok = chunk_vec_ok(a.ptrs, cnt);
         if (dbg) {
-            a.t32 = dbg[idx[first + c0]].t32;
-            a.stride_t32 = d.m * d.n;
-            for (int i = 0; i < cnt; ++i)
-                NP_TRY(hipMemcpyAsync(dbg[idx[first + c0 + i]].scalars, w.tn2 + c0 + i, sizeof(float),
+            for (int i = 0; i < cnt; ++i) {
+                NP_TRY(hipMemcpyAsync(dbg[idx[first + c0 + i]].scalars, it.w.tn2 + c0 + i, sizeof(float),
                                       hipMemcpyDeviceToDevice, sc.s),
                        "dbg");
-        }
-        if (dbg && cnt > 1) {
-            // one matrix per launch keeps the debug pointers simple
-            for (int i = 0; i < cnt; ++i) {
+                // one matrix per launch keeps the debug pointers simple
                 GUpdateArgs b = a;
                 PtrChunk pc{};
                 pc.w[0] = a.ptrs.w[i];
@@ -551,6 +627,7 @@ int run_group_g(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
                 b.t = a.t + (int64_t)i * mn;
                 b.tnorm2 = a.tnorm2 + i;
                 b.t32 = dbg[idx[first + c0 + i]].t32;
+                b.stride_t32 = d.m * d.n;
                 NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_G_UPDATE, 0.0, 10.0 * d.m * d.n,
                              [&] { return launch_g_update(b, 1, sc.s); }),
                        "g update");
@@ -560,6 +637,44 @@ int run_group_g(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
         NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_G_UPDATE, 0.0, 10.0 * d.m * d.n * cnt,
                      [&] { return launch_g_update(a, cnt, sc.s); }),
                "g update");
+    }
+    return NORMPRE_OK;
+}
+
+int run_round_g(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& pools, DebugMat* dbg) {
+    for (const Item& it : items) {
+        int rc = run_normalize(sc, it.d, it.w, (*sc.groups)[it.g].idx, it.first, it.count, dbg);
+        if (rc) return rc;
+    }
+    const int q = sc.hp->ns_iters;
+    for (int iter = 0; iter < q; ++iter) {
+        const bool first_it = iter == 0, last_it = iter == q - 1;
+        for (const Item& it : items) {
+            half_t* x = (iter & 1) ? it.w.xb : it.w.psi;
+            int rc = gram_launch(sc, it, pools[it.pool], x, first_it);
+            if (rc) return rc;
+        }
+        for (size_t pi = 0; pi < pools.size(); ++pi) {
+            double flops = 0.0;
+            for (const Item& it : items)
+                if (it.pool == (int)pi) {
+                    const double s_ = (double)std::min(it.d.m, it.d.n);
+                    flops += 2.0 * s_ * s_ * s_ * it.count;
+                }
+            int rc = poly_launch(sc, pools[pi], flops);
+            if (rc) return rc;
+        }
+        for (const Item& it : items) {
+            half_t* x = (iter & 1) ? it.w.xb : it.w.psi;
+            half_t* xn = (iter & 1) ? it.w.psi : it.w.xb;
+            int rc = combine_launch(sc, it, pools[it.pool], x, xn, first_it, last_it);
+            if (rc) return rc;
+        }
+    }
+    for (const Item& it : items) {
+        const half_t* t = (q & 1) ? it.w.xb : it.w.psi;
+        int rc = g_update_launch(sc, it, t, dbg);
+        if (rc) return rc;
     }
     return NORMPRE_OK;
 }
@@ -602,27 +717,53 @@ int sketch_product(const StepCtx& sc, const Dims& d, const GWork& w, int count, 
     return NORMPRE_OK;
 }
 
-// Cholesky-QR step: V (ell_pad x len fp32, l-major) -> Rinv -> M^T V outputs.
-int cholqr_step(const StepCtx& sc, const Dims& d, const GWork& w, int count, const float* v, int64_t len,
-                float* out32, half_t* out16, half_t* out16t) {
-    const int64_t lp = d.ellp, maxpad = d.lp_;
+// fp64 Gram of an item's l-major fp32 matrix V (ell_pad x len) into its slots
+// of the pool's partials (always kGramChunks chunk slots per matrix).
+int gram64_launch(const StepCtx& sc, const Item& it, const Pool& pl, const float* v, int64_t len) {
+    const int64_t lp = it.d.ellp, maxpad = it.d.lp_;
+    double* out = pl.gpart + (int64_t)it.pool_off * kGramChunks * lp * lp;
     const int chunk_len = gram_chunk_len(len);
-    const int chunks = gram64_chunks(len, chunk_len);
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
-                 [&] { return launch_gram64(v, len, lp * maxpad, (int)lp, len, chunk_len, w.gpart, count, sc.s); }),
+                 [&] {
+                     return launch_gram64(v, len, lp * maxpad, (int)lp, len, chunk_len, kGramChunks, out, it.count,
+                                          sc.s);
+                 }),
            "gram64");
-    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
-                 [&] { return launch_chol_inv(w.gpart, chunks, d.ell, (int)lp, w.chol, w.rinv, count, sc.s); }),
-           "cholesky");
-    SmallMulArgs a{};
-    a.mat = w.rinv; a.stride_mat = lp * lp;
-    a.v = v; a.ld_v = len; a.stride_v = lp * maxpad;
-    a.ell = d.ell; a.ell_pad = (int)lp; a.len = len; a.len_pad = len;
-    a.out32 = out32; a.stride_out32 = lp * maxpad;
-    a.out16 = out16; a.stride_out16 = lp * maxpad;
-    a.out16t = out16t; a.stride_out16t = len * lp;
-    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_small_mul(a, count, sc.s); }),
-           "q = y r^-1");
+    return NORMPRE_OK;
+}
+
+// One Cholesky-QR pass over every item of the round: Gram, Cholesky and
+// inverse (one launch per pool), then Q = Y R^-1 per item.
+int cholqr_round(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& pools, bool final_pass) {
+    for (const Item& it : items) {
+        const float* v = final_pass ? it.w.v32[1] : it.w.v32[0];
+        int rc = gram64_launch(sc, it, pools[it.pool], v, it.d.a_pad);
+        if (rc) return rc;
+    }
+    for (const Pool& pl : pools)
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+                     [&] {
+                         return launch_chol_inv(pl.gpart, kGramChunks, pl.ell, pl.ellp, pl.chol, pl.rinv, pl.count,
+                                                sc.s);
+                     }),
+               "cholesky");
+    for (const Item& it : items) {
+        const Dims& d = it.d;
+        const int64_t lp = d.ellp, maxpad = d.lp_, len = d.a_pad;
+        const Pool& pl = pools[it.pool];
+        SmallMulArgs a{};
+        a.mat = pl.rinv + (int64_t)it.pool_off * lp * lp; a.stride_mat = lp * lp;
+        a.v = final_pass ? it.w.v32[1] : it.w.v32[0]; a.ld_v = len; a.stride_v = lp * maxpad;
+        a.ell = d.ell; a.ell_pad = (int)lp; a.len = len; a.len_pad = len;
+        if (final_pass) {
+            a.out16 = it.w.v16[0]; a.stride_out16 = lp * maxpad;
+            a.out16t = it.w.qlen; a.stride_out16t = len * lp;
+        } else {
+            a.out32 = it.w.v32[1]; a.stride_out32 = lp * maxpad;
+        }
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_small_mul(a, it.count, sc.s); }),
+               "q = y r^-1");
+    }
     return NORMPRE_OK;
 }
 
@@ -633,12 +774,15 @@ float pow2_at_most_inv_sqrt(int64_t a) {
     return std::ldexp(1.f, -e);
 }
 
-int run_group_l(const StepCtx& sc, const Dims& d, const GWork& w, const std::vector<int>& idx, int first, int count,
-                DebugMat* dbg) {
+int sketch_front(const StepCtx& sc, const Item& it, DebugMat* dbg) {
+    const Dims& d = it.d;
+    const GWork& w = it.w;
+    const std::vector<int>& idx = (*sc.groups)[it.g].idx;
+    const int first = it.first, count = it.count;
     int rc = run_normalize(sc, d, w, idx, first, count, dbg);
     if (rc) return rc;
     const normpre_hparams& hp = *sc.hp;
-    const int64_t lp = d.ellp, maxpad = d.lp_, mn = d.mp * d.np_;
+    const int64_t lp = d.ellp, maxpad = d.lp_;
     // Omega^T (ell_pad x b_pad), one counter per matrix: its index in the list.
     for (int c0 = 0; c0 < count; c0 += kChunk) {
         const int cnt = std::min(kChunk, count - c0);
@@ -662,40 +806,26 @@ int run_group_l(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
     const int p = hp.power_iters;
     rc = sketch_product(sc, d, w, count, w.omega, true, w.v32[0], p > 0 ? w.v16[0] : nullptr, 1.f);
     if (rc) return rc;
-    for (int it = 0; it < p; ++it) {
+    for (int i = 0; i < p; ++i) {
         rc = sketch_product(sc, d, w, count, w.v16[0], false, nullptr, w.v16[1], sc_step);
         if (rc) return rc;
-        rc = sketch_product(sc, d, w, count, w.v16[1], true, w.v32[0], it + 1 < p ? w.v16[0] : nullptr, sc_step);
+        rc = sketch_product(sc, d, w, count, w.v16[1], true, w.v32[0], i + 1 < p ? w.v16[0] : nullptr, sc_step);
         if (rc) return rc;
     }
-    // Q = qr(Y) by two Cholesky-QR passes (fp64 Gram and factorization).
-    rc = cholqr_step(sc, d, w, count, w.v32[0], d.a_pad, w.v32[1], nullptr, nullptr);
-    if (rc) return rc;
-    rc = cholqr_step(sc, d, w, count, w.v32[1], d.a_pad, nullptr, w.v16[0], w.qlen);
-    if (rc) return rc;
-    // B = Q^T Psi (ell_pad x b_pad), Gamma_Q = B B^T, Ritz pairs and selection.
-    rc = sketch_product(sc, d, w, count, w.v16[0], false, w.v32[0], nullptr, 1.f);
-    if (rc) return rc;
-    const int b_chunk = gram_chunk_len(d.b_pad);
-    const int chunks = gram64_chunks(d.b_pad, b_chunk);
-    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
-                 [&] {
-                     return launch_gram64(w.v32[0], d.b_pad, lp * maxpad, (int)lp, d.b_pad, b_chunk, w.gpart, count,
-                                          sc.s);
-                 }),
-           "gram64 B");
-    EigArgs ea{};
-    ea.partial = w.gpart; ea.chunks = chunks;
-    ea.ell = d.ell; ea.ell_pad = (int)lp; ea.rank = hp.rank;
-    ea.scratch = w.eigs; ea.kmat = w.kmat;
-    ea.ritz = w.ritz; ea.ritz_stride = d.top; ea.nsel = w.nsel;
-    ea.max_sweeps = kEigSweeps;
-    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_eig_select(ea, count, sc.s); }),
-           "eigensolver");
+    return NORMPRE_OK;
+}
+
+int sketch_back(const StepCtx& sc, const Item& it, const Pool& pl, DebugMat* dbg) {
+    const Dims& d = it.d;
+    const GWork& w = it.w;
+    const std::vector<int>& idx = (*sc.groups)[it.g].idx;
+    const int first = it.first, count = it.count;
+    const normpre_hparams& hp = *sc.hp;
+    const int64_t lp = d.ellp, maxpad = d.lp_, mn = d.mp * d.np_;
     // F = B^T K (b_pad x ell_pad, fp16)
     {
         SmallMulArgs a{};
-        a.mat = w.kmat; a.stride_mat = lp * lp;
+        a.mat = pl.kmat + (int64_t)it.pool_off * lp * lp; a.stride_mat = lp * lp;
         a.v = w.v32[0]; a.ld_v = d.b_pad; a.stride_v = lp * maxpad;
         a.ell = d.ell; a.ell_pad = (int)lp; a.len = d.b_pad; a.len_pad = d.b_pad;
         a.out16t = w.flen; a.stride_out16t = d.b_pad * lp;
@@ -743,12 +873,48 @@ int run_group_l(const StepCtx& sc, const Dims& d, const GWork& w, const std::vec
     if (dbg) {
         for (int i = 0; i < count; ++i) {
             DebugMat& dm = dbg[idx[first + i]];
+            const int pz = it.pool_off + i;
             NP_TRY(hipMemcpyAsync(dm.scalars, w.tn2 + i, sizeof(float), hipMemcpyDeviceToDevice, sc.s), "dbg");
-            NP_TRY(hipMemcpyAsync(dm.scalars + 1, w.nsel + i, sizeof(int), hipMemcpyDeviceToDevice, sc.s), "dbg");
-            NP_TRY(hipMemcpyAsync(dm.scalars + 2, w.ritz + (int64_t)i * d.top, sizeof(float) * d.top,
+            NP_TRY(hipMemcpyAsync(dm.scalars + 1, pl.nsel + pz, sizeof(int), hipMemcpyDeviceToDevice, sc.s), "dbg");
+            NP_TRY(hipMemcpyAsync(dm.scalars + 2, pl.ritz + (int64_t)pz * d.top, sizeof(float) * d.top,
                                   hipMemcpyDeviceToDevice, sc.s),
                    "dbg");
         }
+    }
+    return NORMPRE_OK;
+}
+
+int run_round_l(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& pools, DebugMat* dbg) {
+    for (const Item& it : items) {
+        int rc = sketch_front(sc, it, dbg);
+        if (rc) return rc;
+    }
+    // Q = qr(Y) by two Cholesky-QR passes (fp64 Gram and factorization).
+    int rc = cholqr_round(sc, items, pools, false);
+    if (rc) return rc;
+    rc = cholqr_round(sc, items, pools, true);
+    if (rc) return rc;
+    // B = Q^T Psi (ell_pad x b_pad) and Gamma_Q = B B^T per item.
+    for (const Item& it : items) {
+        rc = sketch_product(sc, it.d, it.w, it.count, it.w.v16[0], false, it.w.v32[0], nullptr, 1.f);
+        if (rc) return rc;
+        rc = gram64_launch(sc, it, pools[it.pool], it.w.v32[0], it.d.b_pad);
+        if (rc) return rc;
+    }
+    // Ritz pairs and selection, one launch per pool.
+    for (const Pool& pl : pools) {
+        EigArgs ea{};
+        ea.partial = pl.gpart; ea.chunks = kGramChunks;
+        ea.ell = pl.ell; ea.ell_pad = pl.ellp; ea.rank = sc.hp->rank;
+        ea.scratch = pl.eigs; ea.kmat = pl.kmat;
+        ea.ritz = pl.ritz; ea.ritz_stride = pl.top; ea.nsel = pl.nsel;
+        ea.max_sweeps = kEigSweeps;
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_eig_select(ea, pl.count, sc.s); }),
+               "eigensolver");
+    }
+    for (const Item& it : items) {
+        rc = sketch_back(sc, it, pools[it.pool], dbg);
+        if (rc) return rc;
     }
     return NORMPRE_OK;
 }
@@ -958,17 +1124,43 @@ int normpre_step(normpre_ctx* ctx, int variant, int num_mats, float* const* para
             }
         }
     }
-    // Sub-batch size per group bounded by a workspace budget; the workspace
-    // is the maximum over sub-batches (they run one after the other).
-    size_t need = 0;
-    std::vector<int> batch_of(groups.size());
+    // Items: each shape group, split into sub-batches that fit kGroupBudget.
+    std::vector<Item> all;
     for (size_t g = 0; g < groups.size(); ++g) {
         const Dims d = dims_of(groups[g].m, groups[g].n, k, *hp);
         const int cnt = (int)groups[g].idx.size();
-        const size_t one = group_bytes(d, 1, variant);
-        int b = (int)std::max<size_t>(1, std::min<size_t>((size_t)cnt, kGroupBudget / std::max<size_t>(one, 1)));
-        batch_of[g] = b;
-        need = std::max(need, group_bytes(d, b, variant));
+        Item one;
+        one.g = (int)g;
+        one.count = 1;
+        one.d = d;
+        const size_t per = round_bytes({one}, variant);
+        const int b = (int)std::max<size_t>(1, std::min<size_t>((size_t)cnt, kGroupBudget / std::max<size_t>(per, 1)));
+        for (int first = 0; first < cnt; first += b) {
+            Item it;
+            it.g = (int)g;
+            it.first = first;
+            it.count = std::min(b, cnt - first);
+            it.d = d;
+            all.push_back(it);
+        }
+    }
+    // Rounds: consecutive items whose phases run interleaved, with their
+    // small matrices pooled; the workspace is the largest round.
+    std::vector<std::vector<Item>> rounds;
+    size_t need = 0;
+    for (const Item& it : all) {
+        if (!rounds.empty()) {
+            std::vector<Item> trial = rounds.back();
+            trial.push_back(it);
+            const size_t bytes = round_bytes(trial, variant);
+            if (bytes <= kRoundBudget) {
+                rounds.back().push_back(it);
+                need = std::max(need, bytes);
+                continue;
+            }
+        }
+        rounds.push_back({it});
+        need = std::max(need, round_bytes(rounds.back(), variant));
     }
     rc = ensure_workspace(ctx, need, s);
     if (rc) return rc;
@@ -981,19 +1173,14 @@ int normpre_step(normpre_ctx* ctx, int variant, int num_mats, float* const* para
     ctx->timing = (hp->flags & NORMPRE_FLAG_TIME_KERNELS) != 0;
     ctx->stream = s;
 
-    StepCtx sc{ctx, s, hp, params, grads, momentum, variant, debug};
-    for (size_t g = 0; g < groups.size(); ++g) {
-        const Dims d = dims_of(groups[g].m, groups[g].n, k, *hp);
-        const int cnt = (int)groups[g].idx.size();
-        for (int first = 0; first < cnt; first += batch_of[g]) {
-            const int count = std::min(batch_of[g], cnt - first);
-            Arena ar{static_cast<char*>(ctx->ws), 0, ctx->ws_bytes};
-            GWork w = carve(ar, d, count, variant);
-            DebugMat* dbg = debug ? ctx->dbg.data() : nullptr;
-            rc = variant == NORMPRE_VARIANT_G ? run_group_g(sc, d, w, groups[g].idx, first, count, dbg)
-                                              : run_group_l(sc, d, w, groups[g].idx, first, count, dbg);
-            if (rc) return rc;
-        }
+    StepCtx sc{ctx, s, hp, params, grads, momentum, variant, debug, &groups};
+    for (std::vector<Item>& items : rounds) {
+        std::vector<Pool> pools = make_pools(items, variant);
+        Arena ar{static_cast<char*>(ctx->ws), 0, ctx->ws_bytes};
+        carve_round(ar, items, pools, variant);
+        DebugMat* dbg = debug ? ctx->dbg.data() : nullptr;
+        rc = variant == NORMPRE_VARIANT_G ? run_round_g(sc, items, pools, dbg) : run_round_l(sc, items, pools, dbg);
+        if (rc) return rc;
     }
     ctx->last_stream = s;
     ctx->have_stream = true;

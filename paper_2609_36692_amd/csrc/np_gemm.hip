@@ -433,7 +433,7 @@ hipError_t dispatch_cfg(TileCfg cfg, Operand A, Operand B, GemmShape sh, int bat
     switch (cfg) {
         case TileCfg::Big:       return run<128, 128, 2, 2, LAYOUT>(A, B, sh, batch, e, s);
         case TileCfg::Skinny64:  return run<64, 256, 1, 4, LAYOUT>(A, B, sh, batch, e, s);
-        case TileCfg::Skinny128: return run<128, 256, 2, 2, LAYOUT>(A, B, sh, batch, e, s);
+        case TileCfg::Skinny128: return run<128, 256, 2, 4, LAYOUT>(A, B, sh, batch, e, s);
         default: return hipErrorInvalidValue;
     }
 }

@@ -162,8 +162,9 @@ hipError_t launch_reduce_splits(const float* part, int splits, int64_t stride_sp
 
 // fp64 Gram of the rows of an l-major fp32 matrix V (l_pad x len):
 // partial[z][chunk][c][d] = sum_{j in chunk} V[c][j] V[d][j], upper tiles.
+// Launches `chunks` length chunks of chunk_len (chunks past len write zeros).
 hipError_t launch_gram64(const float* v, int64_t ld, int64_t stride_v, int ell_pad,
-                         int64_t len, int chunk_len, double* partial, int batch,
+                         int64_t len, int chunk_len, int chunks, double* partial, int batch,
                          hipStream_t s);
 int gram64_chunks(int64_t len, int chunk_len);
 

@@ -454,10 +454,10 @@ hipError_t launch_reduce_splits(const float* part, int splits, int64_t stride_sp
 int gram64_chunks(int64_t len, int chunk_len) { return (int)((len + chunk_len - 1) / chunk_len); }
 
 hipError_t launch_gram64(const float* v, int64_t ld, int64_t stride_v, int ell_pad, int64_t len, int chunk_len,
-                         double* partial, int batch, hipStream_t s) {
-    if (ell_pad % 32 || chunk_len % 64) return hipErrorInvalidValue;
+                         int chunks, double* partial, int batch, hipStream_t s) {
+    if (ell_pad % 32 || chunk_len % 64 || gram64_chunks(len, chunk_len) > chunks) return hipErrorInvalidValue;
     const int tiles = ell_pad / 32;
-    dim3 grid(tiles * (tiles + 1) / 2, gram64_chunks(len, chunk_len), batch);
+    dim3 grid(tiles * (tiles + 1) / 2, chunks, batch);
     hipLaunchKernelGGL(gram64_kernel, grid, dim3(256), 0, s, v, ld, stride_v, ell_pad, len, chunk_len, partial);
     return hipGetLastError();
 }
