@@ -371,15 +371,36 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                 }
                 continue;
             }
-            for (int c = tid; c < TM * C8; c += NT) {
+            // Issue a batch of items' src loads before using any of them.
+            constexpr int SB = ITEMS > 4 ? 4 : ITEMS;
+#pragma unroll 1
+            for (int it0 = 0; it0 < ITEMS; it0 += SB) {
+            u32x4 sbuf[SB];
+            if constexpr (Epi::kind == EpiKind::Affine) {
+                if (src) {
+#pragma unroll
+                    for (int q = 0; q < SB; ++q) {
+                        const int c = tid + (it0 + q) * NT;
+                        if (c < TM * C8) {
+                            const int r = c / C8, c8 = (c - r * C8) * 8;
+                            sbuf[q] = *reinterpret_cast<const u32x4*>(src + (int64_t)(m0 + pass * TM + r) * epi.ld_src +
+                                                                      n0 + c8);
+                        }
+                    }
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < SB; ++q) {
+                const int it = it0 + q;
+                const int c = tid + it * NT;
+                if (c >= TM * C8) break;
                 const int r = c / C8, c8 = (c - r * C8) * 8;
                 const int grow = m0 + pass * TM + r, gcol = n0 + c8;
                 const f32x4 lo = *reinterpret_cast<const f32x4*>(stg + r * LDST + c8);
                 const f32x4 hi = *reinterpret_cast<const f32x4*>(stg + r * LDST + c8 + 4);
                 float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
                 if constexpr (Epi::kind == EpiKind::Affine) {
-                    half_t sv[8];
-                    if (src) *reinterpret_cast<u32x4*>(sv) = *reinterpret_cast<const u32x4*>(src + (int64_t)grow * epi.ld_src + gcol);
+                    const half_t* sv = reinterpret_cast<const half_t*>(&sbuf[q]);
                     half_t hv[8];
 #pragma unroll
                     for (int e = 0; e < 8; ++e) {
@@ -391,6 +412,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                     }
                     *reinterpret_cast<u32x4*>(out + (int64_t)grow * epi.ld_out + gcol) = *reinterpret_cast<const u32x4*>(hv);
                 }
+            }
             }
         }
         const bool want_sum = (Epi::kind == EpiKind::ApplyNorm) ||
