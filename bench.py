@@ -10,10 +10,17 @@ in `variants`.  The per-kernel roofline comes from a second timed region of
 the same K steps in which the library brackets every launch with HIP events
 on the step's stream (the clean region gives `value`).  The CPU baseline is
 the float64 oracle on a bounded sample of the same workload.
+
+`roofline.traffic` is the HBM traffic per launch of the roofline kernel,
+read from the committed rocprofv3 counter summary for the workload
+(FETCH_SIZE and WRITE_SIZE passes, each scaled by what the counter reads for
+a plain device copy of known size, `--copy-mib`); it is null when no summary
+exists or when the kernel sources changed since the counters were taken.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -38,7 +45,74 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-layers", type=int, default=1)
     p.add_argument("--json-out", default=None)
+    p.add_argument("--copy-mib", type=int, default=0,
+                   help="also run a plain device copy of this many MiB (reference kernel for "
+                        "calibrating the HBM byte counters) and report its bandwidth")
     return p.parse_args()
+
+
+CSRC = os.path.join(ROOT, "paper_2609_36692_amd", "csrc")
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def kernel_source_hash():
+    """SHA-256 over the HIP/C++ sources of the library (sorted by name)."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".hip", ".h", ".cpp")):
+            h.update(name.encode())
+            with open(os.path.join(CSRC, name), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload):
+    """Per-launch HBM bytes of each variant's roofline kernel from the counter
+    summary `profiles/hbm_traffic_<workload>.txt` ("key: value" lines), or {}
+    if it is missing or was taken on other kernel sources."""
+    path = os.path.join(PROFILES, f"hbm_traffic_{workload}.txt")
+    if not os.path.exists(path):
+        return {}
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith(("#", " ", "|", "`")):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("source_sha256") != kernel_source_hash():
+        return {}
+    out = {}
+    for v in ("G", "L"):
+        try:
+            fb = float(kv[f"{v}.fetch_bytes_per_launch"])
+            wb = float(kv[f"{v}.write_bytes_per_launch"])
+        except (KeyError, ValueError):
+            continue
+        out[v] = {"bytes_per_launch": fb + wb, "fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
+                  "source": os.path.relpath(path, ROOT)}
+    return out
+
+
+def copy_reference(torch, mib):
+    """Plain device-to-device copy of `mib` MiB: the reference kernel for the
+    byte counters, and a practical HBM ceiling."""
+    n = mib * (1 << 20) // 4
+    src = torch.randn(n, device="cuda:0")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 10
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"mib": mib, "bytes_read": mib << 20, "bytes_written": mib << 20, "launches": reps + 1,
+            "ms_per_copy": round(ms, 4), "gb_per_s": round(2.0 * (mib << 20) / (ms * 1e-3) / 1e9, 1)}
 
 
 def kclass_totals(N, ctx):
@@ -163,6 +237,7 @@ def main():
     wl = WL.WORKLOADS[a.workload]
     rank = a.rank or wl.rank
     variants = [v.strip().upper() for v in a.variants.split(",") if v.strip()]
+    traffic = measured_traffic(wl.name)
     res = {}
     for v in variants:
         r = time_variant(N, WL, torch, wl, v, a.steps, a.warmup, rank)
@@ -174,6 +249,9 @@ def main():
         else:
             roof = roofline_of(cls["sk_stream"], "hbm")
             roof["kernel"] = "sketch products streaming Psi (fp16 MFMA, split-K)"
+        if roof and v in traffic:
+            roof["traffic"] = round(traffic[v]["bytes_per_launch"], 1)
+            roof["traffic_detail"] = traffic[v]
         norm_roof = roofline_of(cls["normalize"], "hbm")
         if norm_roof:
             norm_roof["kernel"] = "momentum + tangent + normalization"
@@ -192,6 +270,8 @@ def main():
             res[v]["ns_tflops_step"] = round(ns["flops"] / a.steps / 1e12, 4)
             res[v]["ns_tflops_per_s_in_step"] = round(ns["flops"] / a.steps / 1e12 / (r["ms_per_step"] / 1e3), 2)
         print(f"[bench] NormPre-{v}: {res[v]['ms_per_step']:.3f} ms/step", file=sys.stderr, flush=True)
+
+    copy_ref = copy_reference(torch, a.copy_mib) if a.copy_mib > 0 else None
 
     cpu = None
     if not a.no_cpu_baseline:
@@ -222,6 +302,8 @@ def main():
         "cpu_baseline": cpu,
         "variants": res,
     }
+    if copy_ref:
+        line["copy_reference"] = copy_ref
     s = json.dumps(line)
     if a.json_out:
         with open(a.json_out, "w") as f:

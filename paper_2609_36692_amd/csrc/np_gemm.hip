@@ -142,7 +142,11 @@ __device__ __forceinline__ void xcd_remap(int& bx, int& by, int& bz) {
     const int gx = gridDim.x, gy = gridDim.y, gz = gridDim.z;
     const int total = gx * gy * gz;
     int lin = bx + gx * (by + gy * bz);
-    if ((total & 7) == 0) lin = (lin & 7) * (total >> 3) + (lin >> 3);
+    // Workgroup w runs on XCD w % 8.  The first 8 * floor(total / 8) ids are
+    // regrouped so each XCD takes one contiguous run of tiles (sharing
+    // operands in its own L2); the ragged tail keeps its order.
+    const int per = total >> 3;
+    if (lin < (per << 3)) lin = (lin & 7) * per + (lin >> 3);
     bx = lin % gx;
     lin /= gx;
     by = lin % gy;
@@ -151,11 +155,24 @@ __device__ __forceinline__ void xcd_remap(int& bx, int& by, int& bz) {
 
 // At least two waves per SIMD: two 4-wave blocks (or one 8-wave block) per
 // CU, so one block's MFMAs overlap the other's LDS and barrier waits.
-template <int BM, int BN, int WM, int WN, int LAYOUT, class Epi>
+// MF = 32: v_mfma_f32_32x32x16_f16 blocks (measured issue-bound ceiling on
+// gfx950 about 2.4 PFLOP/s); MF = 16: v_mfma_f32_16x16x32_f16 blocks (about
+// 1.45 PFLOP/s), kept for the 8-wave 256 x 256 tile, which is LDS-bound
+// either way and runs ~6% faster with the shorter instruction.
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+template <int MF> struct AccSel { using type = f32x4; };
+template <> struct AccSel<32> { using type = f32x16; };
+
+template <int BM, int BN, int WM, int WN, int LAYOUT, class Epi, int MF>
 __global__ void __launch_bounds__(WM * WN * 64, 2)
 gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     constexpr int NT = WM * WN * 64;
-    constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 16, FN = TN / 16;
+    constexpr int TM = BM / WM, TN = BN / WN, FM = TM / MF, FN = TN / MF;
+    // Accumulators as quads: 4 consecutive rows of one column per lane.
+    constexpr int QPB = MF == 16 ? 1 : 4;           // quads per MFMA block
+    static_assert((MF == 16 || MF == 32) && TM % MF == 0 && TN % MF == 0, "wave tile must hold whole MFMA blocks");
+    constexpr int NQ = FM * FN * QPB;
     // Two LDS stages: the MFMAs of stage i overlap the LDS stores of stage
     // i + 1 and the global loads of stage i + 2.  The epilogue reuses the
     // same LDS to stage one wave-row of fp32 results (row stride BN + 4).
@@ -182,11 +199,12 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     using LB = typename LoaderSel<(LAYOUT >= 1), BN, NT>::type;
     u32x4 ra[LA::N], rb[LB::N];
 
-    f32x4 acc[FM][FN];
+    using AccT = typename AccSel<MF>::type;
+    AccT acc[FM][FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < FN; ++j) acc[i][j] = AccT{};
 
     if (kbeg < kend) {
         LA::load(ra, Ab, A.ld, m0, kbeg, tid);
@@ -202,21 +220,50 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
             __syncthreads();
             const half_t* ca = sbase + stage * (BM + BN) * BK;
             const half_t* cb = ca + BM * BK;
+            if constexpr (MF == 16) {
 #pragma unroll
-            for (int s = 0; s < BK / 32; ++s) {
-                f16x8 af[FM], bf[FN];
-                const int chunk = s * 4 + (lane >> 4);
+                for (int s = 0; s < BK / 32; ++s) {
+                    f16x8 af[FM], bf[FN];
+                    const int chunk = s * 4 + (lane >> 4);
 #pragma unroll
-                for (int i = 0; i < FM; ++i)
-                    af[i] = *reinterpret_cast<const f16x8*>(ca + lds_idx(wm * TM + i * 16 + (lane & 15), chunk));
-#pragma unroll
-                for (int j = 0; j < FN; ++j)
-                    bf[j] = *reinterpret_cast<const f16x8*>(cb + lds_idx(wn * TN + j * 16 + (lane & 15), chunk));
-#pragma unroll
-                for (int i = 0; i < FM; ++i)
+                    for (int i = 0; i < FM; ++i)
+                        af[i] = *reinterpret_cast<const f16x8*>(ca + lds_idx(wm * TM + i * 16 + (lane & 15), chunk));
 #pragma unroll
                     for (int j = 0; j < FN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
+                        bf[j] = *reinterpret_cast<const f16x8*>(cb + lds_idx(wn * TN + j * 16 + (lane & 15), chunk));
+#pragma unroll
+                    for (int i = 0; i < FM; ++i)
+#pragma unroll
+                        for (int j = 0; j < FN; ++j)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
+                }
+            } else {
+                // Fragments of sub-step s + 1 are read while the MFMAs of
+                // sub-step s run; the scheduling barriers keep the compiler
+                // from hoisting every sub-step's reads (which would not fit
+                // beside 256 accumulator registers).
+                f16x8 af[2][FM], bf[2][FN];
+                auto read_frags = [&](int s, int buf) {
+                    const int chunk = s * 2 + (lane >> 5);
+#pragma unroll
+                    for (int i = 0; i < FM; ++i)
+                        af[buf][i] = *reinterpret_cast<const f16x8*>(ca + lds_idx(wm * TM + i * 32 + (lane & 31), chunk));
+#pragma unroll
+                    for (int j = 0; j < FN; ++j)
+                        bf[buf][j] = *reinterpret_cast<const f16x8*>(cb + lds_idx(wn * TN + j * 32 + (lane & 31), chunk));
+                };
+                read_frags(0, 0);
+#pragma unroll
+                for (int s = 0; s < BK / 16; ++s) {
+                    if (s + 1 < BK / 16) read_frags(s + 1, (s + 1) & 1);
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int i = 0; i < FM; ++i)
+#pragma unroll
+                        for (int j = 0; j < FN; ++j)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[s & 1][i], bf[s & 1][j], acc[i][j], 0, 0, 0);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
             }
             if (k0 + BK < kend) {
                 LA::store(ra, sbase + (stage ^ 1) * (BM + BN) * BK, tid);
@@ -229,20 +276,31 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
         }
     }
 
-    // Element (i, j, r) of this lane: row m0 + wm*TM + 16i + 4*(lane/16) + r,
-    // column n0 + wn*TN + 16j + lane%16.
-    const int rbase = m0 + wm * TM + 4 * (lane >> 4);
-    const int cbase = n0 + wn * TN + (lane & 15);
+    // Quad qi of this lane: rows quad_row(qi) + 0..3 (relative to the wave
+    // tile), column quad_col(qi).  16x16 blocks: row 16i + 4*(lane/16),
+    // column 16j + lane%16.  32x32 blocks: register r of block (i, j) is
+    // row 32i + 8*(r/4) + 4*(lane/32) + r%4, column 32j + lane%32.
+    auto quad_row = [&](int qi) -> int {
+        const int blk = qi / QPB, g = qi - blk * QPB, i = blk / FN;
+        return MF == 16 ? 16 * i + 4 * (lane >> 4) : 32 * i + 8 * g + 4 * (lane >> 5);
+    };
+    auto quad_col = [&](int qi) -> int {
+        const int blk = qi / QPB, j = blk - (blk / FN) * FN;
+        return MF == 16 ? 16 * j + (lane & 15) : 32 * j + (lane & 31);
+    };
+    auto quad_val = [&](int qi, int r) -> float {
+        const int blk = qi / QPB, g = qi - blk * QPB, i = blk / FN, j = blk - i * FN;
+        return acc[i][j][4 * g + r];
+    };
+    const int rw0 = m0 + wm * TM, cw0 = n0 + wn * TN;
 
     if constexpr (Epi::kind == EpiKind::Partial) {
         float* out = epi.out + (int64_t)z * epi.stride_mat + (int64_t)split * epi.stride_split;
 #pragma unroll
-        for (int i = 0; i < FM; ++i)
+        for (int qi = 0; qi < NQ; ++qi)
 #pragma unroll
-            for (int j = 0; j < FN; ++j)
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    out[(int64_t)(rbase + i * 16 + r) * epi.ld_out + cbase + j * 16] = acc[i][j][r];
+            for (int r = 0; r < 4; ++r)
+                out[(int64_t)(rw0 + quad_row(qi) + r) * epi.ld_out + cw0 + quad_col(qi)] = quad_val(qi, r);
         return;
     } else {
         // Per-epilogue set-up.
@@ -265,21 +323,18 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                 // Transposed copy of an off-diagonal tile of a symmetric result,
                 // written from registers (4 consecutive halves per lane).
 #pragma unroll
-                for (int i = 0; i < FM; ++i)
+                for (int qi = 0; qi < NQ; ++qi) {
+                    const int col = cw0 + quad_col(qi), row0 = rw0 + quad_row(qi);
+                    half_t hv[4];
 #pragma unroll
-                    for (int j = 0; j < FN; ++j) {
-                        const int col = cbase + j * 16;
-                        half_t hv[4];
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            const int row = rbase + i * 16 + r;
-                            float v = ca * acc[i][j][r];
-                            if (src) v += cs * (float)src[(int64_t)row * epi.ld_src + col];
-                            hv[r] = (half_t)v;
-                        }
-                        half_t* dst = out + (int64_t)col * epi.ld_out + rbase + i * 16;
-                        *reinterpret_cast<u32x2*>(dst) = *reinterpret_cast<const u32x2*>(hv);
+                    for (int r = 0; r < 4; ++r) {
+                        float v = ca * quad_val(qi, r);
+                        if (src) v += cs * (float)src[(int64_t)(row0 + r) * epi.ld_src + col];
+                        hv[r] = (half_t)v;
                     }
+                    half_t* dst = out + (int64_t)col * epi.ld_out + row0;
+                    *reinterpret_cast<u32x2*>(dst) = *reinterpret_cast<const u32x2*>(hv);
+                }
             }
         } else {
             psi = epi.psi + (int64_t)z * epi.stride_psi;
@@ -300,12 +355,10 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
             __syncthreads();
             if (wm == pass) {
 #pragma unroll
-                for (int i = 0; i < FM; ++i)
+                for (int qi = 0; qi < NQ; ++qi)
 #pragma unroll
-                    for (int j = 0; j < FN; ++j)
-#pragma unroll
-                        for (int r = 0; r < 4; ++r)
-                            stg[(i * 16 + 4 * (lane >> 4) + r) * LDST + wn * TN + j * 16 + (lane & 15)] = acc[i][j][r];
+                    for (int r = 0; r < 4; ++r)
+                        stg[(quad_row(qi) + r) * LDST + wn * TN + quad_col(qi)] = quad_val(qi, r);
             }
             __syncthreads();
             constexpr int ITEMS = (TM * C8 + NT - 1) / NT;
@@ -436,7 +489,7 @@ struct EPar : EpiPartial { static constexpr EpiKind kind = EpiKind::Partial; };
 struct EApp : EpiApplyUpdate { static constexpr EpiKind kind = EpiKind::Apply; };
 struct EAppN : EpiApplyNorm { static constexpr EpiKind kind = EpiKind::ApplyNorm; };
 
-template <int BM, int BN, int WM, int WN, int LAYOUT, class E>
+template <int BM, int BN, int WM, int WN, int LAYOUT, class E, int MF = 32>
 hipError_t run(Operand A, Operand B, GemmShape sh, int batch, const E& e, hipStream_t s) {
     if (sh.M % BM || sh.N % BN || sh.K % BK || sh.k_chunk % BK || batch < 1) return hipErrorInvalidValue;
     const int tm = sh.M / BM, tn = sh.N / BN;
@@ -446,7 +499,7 @@ hipError_t run(Operand A, Operand B, GemmShape sh, int batch, const E& e, hipStr
         tiles = tn * (tn + 1) / 2;
     }
     dim3 grid(tiles, sh.k_split, batch);
-    hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, LAYOUT, E>), grid, dim3(WM * WN * 64), 0, s, A, B, sh, e);
+    hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, LAYOUT, E, MF>), grid, dim3(WM * WN * 64), 0, s, A, B, sh, e);
     return hipGetLastError();
 }
 
@@ -492,9 +545,9 @@ hipError_t launch_gemm_affine(TileCfg cfg, int layout, Operand A, Operand B, Gem
         }
     } else if (cfg == TileCfg::Big256) {
         switch (layout) {
-            case 0: return run<256, 256, 2, 4, 0>(A, B, sh, batch, ee, s);
-            case 1: return run<256, 256, 2, 4, 1>(A, B, sh, batch, ee, s);
-            case 2: return run<256, 256, 2, 4, 2>(A, B, sh, batch, ee, s);
+            case 0: return run<256, 256, 2, 4, 0, EAff, 16>(A, B, sh, batch, ee, s);
+            case 1: return run<256, 256, 2, 4, 1, EAff, 16>(A, B, sh, batch, ee, s);
+            case 2: return run<256, 256, 2, 4, 2, EAff, 16>(A, B, sh, batch, ee, s);
         }
     }
     return hipErrorInvalidValue;
