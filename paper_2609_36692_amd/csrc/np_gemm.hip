@@ -113,6 +113,16 @@ __device__ __forceinline__ void decode_tile(int bid, int tiles_n, int sym, int& 
     tn = row + left;
 }
 
+// Block barrier that orders LDS only.  __syncthreads() is a workgroup fence
+// over all address spaces, which on gfx950 also waits for every outstanding
+// global load (vmcnt(0)) and so would drain the prefetch of the next K-stage
+// at each barrier; the kernel's cross-wave traffic is all in LDS.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -217,7 +227,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
         }
         int stage = 0;
         for (int k0 = kbeg; k0 < kend; k0 += BK, stage ^= 1) {
-            __syncthreads();
+            lds_barrier();
             const half_t* ca = sbase + stage * (BM + BN) * BK;
             const half_t* cb = ca + BM * BK;
             if constexpr (MF == 16) {
@@ -352,7 +362,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
         float ss = 0.f;
 #pragma unroll 1
         for (int pass = 0; pass < WM; ++pass) {
-            __syncthreads();
+            lds_barrier();
             if (wm == pass) {
 #pragma unroll
                 for (int qi = 0; qi < NQ; ++qi)
@@ -360,7 +370,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                     for (int r = 0; r < 4; ++r)
                         stg[(quad_row(qi) + r) * LDST + wn * TN + quad_col(qi)] = quad_val(qi, r);
             }
-            __syncthreads();
+            lds_barrier();
             constexpr int ITEMS = (TM * C8 + NT - 1) / NT;
             if constexpr (Epi::kind == EpiKind::Apply || Epi::kind == EpiKind::ApplyNorm) {
                 // Issue every item's Psi (and W) loads before using any of them.
@@ -472,9 +482,9 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                               (Epi::kind == EpiKind::Affine && epi_has_sumsq(epi));
         if (want_sum) {
             ss = wave_sum(ss);
-            __syncthreads();
+            lds_barrier();
             if (lane == 0) red[wave] = ss;
-            __syncthreads();
+            lds_barrier();
             if (tid == 0) {
                 float t = 0.f;
                 for (int q = 0; q < NT / 64; ++q) t += red[q];
