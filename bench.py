@@ -43,7 +43,8 @@ def parse():
     p.add_argument("--variants", default="G,L")
     p.add_argument("--rank", type=int, default=None, help="NormPre-L rank r (default: the workload's)")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-sample-layers", type=int, default=1)
+    p.add_argument("--cpu-seconds", type=float, default=12.0,
+                   help="time bound of the oracle CPU baseline sample")
     p.add_argument("--json-out", default=None)
     p.add_argument("--copy-mib", type=int, default=0,
                    help="also run a plain device copy of this many MiB (reference kernel for "
@@ -55,14 +56,18 @@ CSRC = os.path.join(ROOT, "paper_2609_36692_amd", "csrc")
 PROFILES = os.path.join(ROOT, "profiles")
 
 
+# Sources that decide what a roofline-kernel launch does: the GEMM kernels
+# and the host code that sizes and configures their launches.
+TRAFFIC_SOURCES = ("np_gemm.hip", "np_internal.h", "normpre_api.cpp")
+
+
 def kernel_source_hash():
-    """SHA-256 over the HIP/C++ sources of the library (sorted by name)."""
+    """SHA-256 over the GEMM kernel and launch-configuration sources."""
     h = hashlib.sha256()
-    for name in sorted(os.listdir(CSRC)):
-        if name.endswith((".hip", ".h", ".cpp")):
-            h.update(name.encode())
-            with open(os.path.join(CSRC, name), "rb") as f:
-                h.update(f.read())
+    for name in TRAFFIC_SOURCES:
+        h.update(name.encode())
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read())
     return h.hexdigest()
 
 
@@ -194,8 +199,11 @@ def merge_classes(classes, names):
     return out
 
 
-def cpu_baseline(wl, variant, layers, rank):
-    """Oracle (float64 NumPy) on the first `layers` layers of the stack."""
+def cpu_baseline(wl, variant, seconds, rank):
+    """Oracle (float64 NumPy) on a time-bounded sample of the workload: whole
+    steps of the stack in order (t = 0, 1, ...; both orientations) until
+    `seconds` have elapsed, at most two steps; the rate is scaled to steps of
+    the full stack."""
     import numpy as np
     from oracle import normpre_oracle as O
     from paper_2609_36692_amd import workloads as WL
@@ -204,20 +212,22 @@ def cpu_baseline(wl, variant, layers, rank):
         threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
     except Exception:
         threads = len(os.sched_getaffinity(0))
-    per_layer = {"gpt2_small": 4, "llama_1b": 7, "qwen3_1p7b": 7}.get(wl.name, len(wl.shapes))
-    n = min(len(wl.shapes), per_layer * layers)
     hp = O.HParams(lr=wl.lr, rank=rank, oversample=wl.oversample, power_iters=wl.power_iters)
-    mats = [WL.make_matrix(wl, i, "cpu") for i in range(n)]
+    n = len(wl.shapes)
+    done = 0
     t0 = time.perf_counter()
-    for i, (w, g, mp) in enumerate(mats):
-        O.normpre_step(w.numpy(), g.numpy(), mp.numpy(), i % 2, hp, variant, matrix_id=i)
+    while done < 2 * n:
+        i, t = done % n, done // n
+        w, g, mp = WL.make_matrix(wl, i, "cpu")
+        O.normpre_step(w.numpy(), g.numpy(), mp.numpy(), t, hp, variant, matrix_id=i)
+        done += 1
+        if time.perf_counter() - t0 >= seconds:
+            break
     dt = time.perf_counter() - t0
-    scale = len(wl.shapes) / n
-    sec_per_step = dt * scale
-    return {"value": round(1.0 / sec_per_step, 5), "unit": "steps/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"{n} of {len(wl.shapes)} matrices (first {layers} layer(s)), NormPre-{variant}, "
-                      f"{dt:.2f} s measured, scaled x{scale:g} to the full stack"}
+    steps = done / n
+    return {"value": round(steps / dt, 5), "unit": "steps/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{done} matrix updates ({steps:.3g} steps of the {n}-matrix stack, t = 0.."
+                      f"{(done - 1) // n}), NormPre-{variant}, {dt:.1f} s measured"}
 
 
 def main():
@@ -276,7 +286,7 @@ def main():
     cpu = None
     if not a.no_cpu_baseline:
         v0 = variants[0]
-        cpu = cpu_baseline(wl, v0, a.cpu_sample_layers, rank)
+        cpu = cpu_baseline(wl, v0, a.cpu_seconds, rank)
         print(f"[bench] cpu baseline: {cpu}", file=sys.stderr, flush=True)
 
     primary = variants[0]

@@ -172,7 +172,9 @@ hipEvent_t get_event(normpre_ctx* ctx) {
     return e;
 }
 
-// Runs one launch, bracketed by an event pair when kernel timing is on.
+// Runs one launch; with kernel timing on, times it with an event pair.  A
+// GEMM launch takes the pair itself (recorded at the kernel's own start and
+// end); any other launch is bracketed by stream-ordered records.
 template <class F>
 hipError_t timed(normpre_ctx* ctx, int kclass, double flops, double bytes, F&& launch) {
     if (!ctx->timing) return launch();
@@ -180,10 +182,14 @@ hipError_t timed(normpre_ctx* ctx, int kclass, double flops, double bytes, F&& l
     if (!a || !b) return hipErrorOutOfMemory;
     hipError_t e = hipEventRecord(a, ctx->stream);
     if (e != hipSuccess) return e;
+    np::arm_launch_events(a, b);
     e = launch();
+    const bool unused = np::disarm_launch_events();
     if (e != hipSuccess) return e;
-    e = hipEventRecord(b, ctx->stream);
-    if (e != hipSuccess) return e;
+    if (unused) {
+        e = hipEventRecord(b, ctx->stream);
+        if (e != hipSuccess) return e;
+    }
     ctx->pending.push_back({kclass, a, b, flops, bytes});
     return hipSuccess;
 }

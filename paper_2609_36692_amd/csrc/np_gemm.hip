@@ -17,6 +17,8 @@
 // All sizes are multiples of the tile sizes (the workspace is zero padded).
 #include "np_internal.h"
 
+#include <hip/hip_ext.h>
+
 namespace np {
 namespace {
 
@@ -499,6 +501,16 @@ struct EPar : EpiPartial { static constexpr EpiKind kind = EpiKind::Partial; };
 struct EApp : EpiApplyUpdate { static constexpr EpiKind kind = EpiKind::Apply; };
 struct EAppN : EpiApplyNorm { static constexpr EpiKind kind = EpiKind::ApplyNorm; };
 
+thread_local hipEvent_t t_ev_start = nullptr, t_ev_stop = nullptr;
+
+bool take_launch_events(hipEvent_t& start, hipEvent_t& stop) {
+    if (!t_ev_start) return false;
+    start = t_ev_start;
+    stop = t_ev_stop;
+    t_ev_start = t_ev_stop = nullptr;
+    return true;
+}
+
 template <int BM, int BN, int WM, int WN, int LAYOUT, class E, int MF = 32>
 hipError_t run(Operand A, Operand B, GemmShape sh, int batch, const E& e, hipStream_t s) {
     if (sh.M % BM || sh.N % BN || sh.K % BK || sh.k_chunk % BK || batch < 1) return hipErrorInvalidValue;
@@ -509,7 +521,12 @@ hipError_t run(Operand A, Operand B, GemmShape sh, int batch, const E& e, hipStr
         tiles = tn * (tn + 1) / 2;
     }
     dim3 grid(tiles, sh.k_split, batch);
-    hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, LAYOUT, E, MF>), grid, dim3(WM * WN * 64), 0, s, A, B, sh, e);
+    hipEvent_t ev0, ev1;
+    if (take_launch_events(ev0, ev1))
+        hipExtLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, LAYOUT, E, MF>), grid, dim3(WM * WN * 64), 0, s, ev0, ev1, 0,
+                              A, B, sh, e);
+    else
+        hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, LAYOUT, E, MF>), grid, dim3(WM * WN * 64), 0, s, A, B, sh, e);
     return hipGetLastError();
 }
 
@@ -524,6 +541,16 @@ hipError_t dispatch_cfg(TileCfg cfg, Operand A, Operand B, GemmShape sh, int bat
 }
 
 }  // namespace
+
+void arm_launch_events(hipEvent_t start, hipEvent_t stop) {
+    t_ev_start = start;
+    t_ev_stop = stop;
+}
+bool disarm_launch_events() {
+    const bool armed = t_ev_start != nullptr;
+    t_ev_start = t_ev_stop = nullptr;
+    return armed;
+}
 
 int gemm_tile_m(TileCfg cfg) {
     switch (cfg) {

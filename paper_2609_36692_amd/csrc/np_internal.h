@@ -99,6 +99,12 @@ hipError_t launch_gemm_apply(Operand A, Operand B, GemmShape sh, int batch,
 hipError_t launch_gemm_apply_norm(Operand A, Operand B, GemmShape sh, int batch,
                                   const EpiApplyNorm& e, hipStream_t s);
 int gemm_tile_m(TileCfg cfg);
+// Kernel timing hand-off (instrumented steps only): while a start/stop event
+// pair is armed on this thread, the next GEMM launch records it at its own
+// start and end (hipExtLaunchKernelGGL) and disarms it.
+void arm_launch_events(hipEvent_t start, hipEvent_t stop);
+bool disarm_launch_events();        // true if the pair was still armed
+
 int gemm_tile_n(TileCfg cfg);
 
 // ------------------------------------------------- elementwise kernels ---
