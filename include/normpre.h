@@ -55,6 +55,18 @@ extern "C" {
 /* ---- variants (Alg. 1: "optimizer variant") ----------------------------- */
 #define NORMPRE_VARIANT_G 0   /* global spectral preconditioning, Newton-Schulz */
 #define NORMPRE_VARIANT_L 1   /* localized preconditioning, randomized sketch   */
+/* Reference steps through the same kernels (for the latency comparisons of
+ * Sec. 4.2 and App. C.2, not optimizers of record):
+ *   MUON           Sec. 2.1 / App. A.1: M <- mu M + G; T = the same q-step
+ *                  Newton-Schulz iteration on M / (||M||_F + ns_eps) (short
+ *                  side, no tangent, no normalization); the RMS-matching
+ *                  convention the paper uses for Muon,
+ *                  U = target_rms * sqrt(max(m, n)) * T; no orientation.
+ *   NORMALIZE_ONLY Sec. 2.2: the NormPre step with P = I, T = Psi (momentum,
+ *                  orientation, tangent and diagonal-Gram normalization as
+ *                  for G and L, then the consistent update RMS). */
+#define NORMPRE_VARIANT_MUON            2
+#define NORMPRE_VARIANT_NORMALIZE_ONLY  3
 
 /* ---- orientation modes (Sec. 3.1, alternating row/column orientation) --- */
 #define NORMPRE_ORIENT_ALTERNATING 0   /* k = t mod 2 (the paper's rule) */
@@ -69,6 +81,15 @@ extern "C" {
 /* Record a HIP event pair around every kernel launch so that
  * normpre_kernel_stats() can report per-kernel-class device time. */
 #define NORMPRE_FLAG_TIME_KERNELS  2u
+/* Momentum-processing ablations (App. A.4, "Ablations on Marginally
+ * Normalized Update"; at most one of the two): the default is the relaxed
+ * tangent x_i = m_i - <m_i, w_i> w_i of Sec. 3.1.
+ *   TANGENT_NONE   x_i = m_i
+ *   TANGENT_STRICT x_i = m_i - (<m_i, w_i> / ||w_i||^2) w_i (the exact tangent
+ *                  projection; x_i = m_i where w_i = 0)
+ * Ignored by NORMPRE_VARIANT_MUON. */
+#define NORMPRE_FLAG_TANGENT_NONE   4u
+#define NORMPRE_FLAG_TANGENT_STRICT 8u
 
 /*
  * Hyper-parameters of one step.  Defaults (normpre_default_hparams) follow
@@ -121,7 +142,7 @@ const char* normpre_last_error(const normpre_ctx* ctx);
  * Errors: INVALID_ARG (variant, num_mats < 0, shapes null, a dimension < 1,
  * ns_iters outside 1..64, rank < 1, oversample < 0, power_iters outside
  * 0..8, a non-finite or negative lr/weight decay, a non-finite momentum,
- * norm_eps <= 0, unknown orientation or flags),
+ * norm_eps <= 0, unknown orientation or flags, both tangent flags),
  * UNSUPPORTED (a dimension above 1 << 20 or a matrix above 2^31 elements;
  * in the row-active orientation a row longer than 32768 elements; for
  * NormPre-L a sketch width l = min(active rows, r + o) above 384).
@@ -131,7 +152,7 @@ int normpre_validate(int variant, int num_mats, const int64_t* shapes,
 
 /*
  * One NormPre step (Alg. 1) on num_mats matrices.
- *   variant  : NORMPRE_VARIANT_G or NORMPRE_VARIANT_L
+ *   variant  : NORMPRE_VARIANT_G, _L, _MUON or _NORMALIZE_ONLY
  *   params   : host array of num_mats device pointers to W (updated in place)
  *   grads    : host array of num_mats device pointers to G (read only)
  *   momentum : host array of num_mats device pointers to M (updated in place;

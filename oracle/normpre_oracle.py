@@ -56,6 +56,7 @@ class HParams:
     norm_eps: float = 1e-12
     ns_eps: float = 1e-7
     orientation: str = "alternating"   # "alternating" | "row" | "col"
+    tangent: str = "relaxed"           # "relaxed" (Sec. 3.1) | "none" | "strict" (App. A.4)
 
 
 # --------------------------------------------------------------------------
@@ -96,6 +97,30 @@ def orient_inv(a: np.ndarray, k: int) -> np.ndarray:
 def relaxed_tangent(m_bar: np.ndarray, w_bar: np.ndarray) -> np.ndarray:
     d = np.sum(m_bar * w_bar, axis=1)
     return m_bar - d[:, None] * w_bar
+
+
+# --------------------------------------------------------------------------
+# Momentum-processing ablations (App. A.4, "Ablations on Marginally
+# Normalized Update"): "none" leaves the momentum unchanged; "strict" removes
+# the whole radial component, the orthogonal projection onto w_i^perp (the
+# relaxed form coincides with it when ||w_i|| = 1, Sec. 3.1).  A zero w_i has
+# no radial direction and leaves m_i unchanged.
+# --------------------------------------------------------------------------
+def strict_tangent(m_bar: np.ndarray, w_bar: np.ndarray) -> np.ndarray:
+    d = np.sum(m_bar * w_bar, axis=1)
+    ww = np.sum(w_bar * w_bar, axis=1)
+    coef = np.divide(d, ww, out=np.zeros_like(d), where=ww > 0)
+    return m_bar - coef[:, None] * w_bar
+
+
+def momentum_processing(m_bar: np.ndarray, w_bar: np.ndarray, mode: str = "relaxed") -> np.ndarray:
+    if mode == "relaxed":
+        return relaxed_tangent(m_bar, w_bar)
+    if mode == "strict":
+        return strict_tangent(m_bar, w_bar)
+    if mode == "none":
+        return m_bar.copy()
+    raise ValueError(f"unknown tangent mode {mode!r}")
 
 
 # --------------------------------------------------------------------------
@@ -301,18 +326,23 @@ def normpre_step(w, g, m_prev, t: int, hp: HParams, variant: str = "G",
     the RMS-matched update U, the new W and, for NormPre-L, sketch diagnostics.
 
     variant: "G" (Newton-Schulz msign) or "L" (localized; l_mode "sketch" per
-    Alg. 2 or "exact" per App. B).
+    Alg. 2 or "exact" per App. B); the reference steps "MUON" (``muon_step``)
+    and "NORM" (normalize-only: the step with P = I, T = Psi, Sec. 2.2).
     """
+    if variant == "MUON":
+        return muon_step(w, g, m_prev, hp)
     w = np.asarray(w, np.float64)
     g = np.asarray(g, np.float64)
     m_prev = np.asarray(m_prev, np.float64)
     m = momentum_update(m_prev, g, hp.momentum)
     k = orientation_of(t, hp.orientation)
     w_bar, m_bar = orient(w, k), orient(m, k)
-    x = relaxed_tangent(m_bar, w_bar)
+    x = momentum_processing(m_bar, w_bar, hp.tangent)
     psi = diagonal_gram_normalize(x, hp.norm_eps)
     out = {"k": k, "momentum": m, "psi": orient_inv(psi, k)}
-    if variant == "G":
+    if variant == "NORM":
+        t_act = psi
+    elif variant == "G":
         t_act = newton_schulz(psi, hp.ns_iters, hp.ns_coeffs, hp.ns_eps)
     elif variant == "L":
         a, b = psi.shape
@@ -336,6 +366,24 @@ def normpre_step(w, g, m_prev, t: int, hp: HParams, variant: str = "G",
     out["update"] = u
     out["w_new"] = parameter_update(w, u, hp.lr, hp.weight_decay)
     return out
+
+
+# --------------------------------------------------------------------------
+# Muon reference step (Sec. 2.1; configuration of App. A.1): heavy-ball
+# momentum, then the same q-step Newton-Schulz iteration applied to the
+# momentum itself (no tangent processing, no normalization, no orientation),
+# and the RMS-matching convention the paper uses for Muon on LLaMA / Qwen3:
+# U = 0.2 sqrt(max(m, n)) T.  Weight decay as in Alg. 1.
+# --------------------------------------------------------------------------
+def muon_step(w, g, m_prev, hp: HParams) -> dict:
+    w = np.asarray(w, np.float64)
+    g = np.asarray(g, np.float64)
+    m_prev = np.asarray(m_prev, np.float64)
+    m = momentum_update(m_prev, g, hp.momentum)
+    t_mat = newton_schulz(m, hp.ns_iters, hp.ns_coeffs, hp.ns_eps)
+    u = hp.target_rms * math.sqrt(max(m.shape)) * t_mat
+    return {"k": 0, "momentum": m, "psi": m / (np.linalg.norm(m) + hp.ns_eps), "t": t_mat,
+            "update": u, "w_new": parameter_update(w, u, hp.lr, hp.weight_decay)}
 
 
 # --------------------------------------------------------------------------

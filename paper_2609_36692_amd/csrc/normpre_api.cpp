@@ -57,9 +57,21 @@ int sketch_width(const normpre_hparams& hp, int64_t active_rows) {
     return (int)std::min<int64_t>(active_rows, (int64_t)hp.rank + hp.oversample);
 }
 
+// Active orientation of the step; the Muon reference step has none (it
+// works on the whole matrix in the W layout).
+int step_orientation(int variant, const normpre_hparams& hp) {
+    return variant == NORMPRE_VARIANT_MUON ? 0 : orientation_of(hp);
+}
+
+int tangent_mode(const normpre_hparams& hp) {
+    if (hp.flags & NORMPRE_FLAG_TANGENT_NONE) return np::kTangentNone;
+    if (hp.flags & NORMPRE_FLAG_TANGENT_STRICT) return np::kTangentStrict;
+    return np::kTangentRelaxed;
+}
+
 // Shared by normpre_validate() and normpre_step().
 Fail validate(int variant, int num_mats, const int64_t* shapes, const normpre_hparams* hp) {
-    if (variant != NORMPRE_VARIANT_G && variant != NORMPRE_VARIANT_L)
+    if (variant < NORMPRE_VARIANT_G || variant > NORMPRE_VARIANT_NORMALIZE_ONLY)
         return {NORMPRE_ERR_INVALID_ARG, fmt("unknown variant %d", variant)};
     if (num_mats < 0) return {NORMPRE_ERR_INVALID_ARG, "num_mats < 0"};
     if (!hp) return {NORMPRE_ERR_INVALID_ARG, "hparams is null"};
@@ -73,29 +85,32 @@ Fail validate(int variant, int num_mats, const int64_t* shapes, const normpre_hp
         return {NORMPRE_ERR_INVALID_ARG, "norm_eps must be finite and > 0"};
     if (hp->orientation < 0 || hp->orientation > 2)
         return {NORMPRE_ERR_INVALID_ARG, fmt("unknown orientation mode %d", hp->orientation)};
-    if (hp->flags & ~(NORMPRE_FLAG_DEBUG | NORMPRE_FLAG_TIME_KERNELS))
+    if (hp->flags & ~(NORMPRE_FLAG_DEBUG | NORMPRE_FLAG_TIME_KERNELS | NORMPRE_FLAG_TANGENT_NONE |
+                      NORMPRE_FLAG_TANGENT_STRICT))
         return {NORMPRE_ERR_INVALID_ARG, fmt("unknown flags 0x%x", hp->flags)};
-    if (variant == NORMPRE_VARIANT_G) {
+    if ((hp->flags & NORMPRE_FLAG_TANGENT_NONE) && (hp->flags & NORMPRE_FLAG_TANGENT_STRICT))
+        return {NORMPRE_ERR_INVALID_ARG, "at most one tangent mode flag"};
+    if (variant == NORMPRE_VARIANT_G || variant == NORMPRE_VARIANT_MUON) {
         if (hp->ns_iters < 1 || hp->ns_iters > 64)
             return {NORMPRE_ERR_INVALID_ARG, fmt("ns_iters %d outside 1..64", hp->ns_iters)};
         for (int i = 0; i < 3; ++i)
             if (!std::isfinite(hp->ns_coeffs[i])) return {NORMPRE_ERR_INVALID_ARG, "ns_coeffs must be finite"};
         if (!std::isfinite(hp->ns_eps) || hp->ns_eps < 0.f)
             return {NORMPRE_ERR_INVALID_ARG, "ns_eps must be finite and >= 0"};
-    } else {
+    } else if (variant == NORMPRE_VARIANT_L) {
         if (hp->rank < 1) return {NORMPRE_ERR_INVALID_ARG, fmt("rank %d < 1", hp->rank)};
         if (hp->oversample < 0) return {NORMPRE_ERR_INVALID_ARG, fmt("oversample %d < 0", hp->oversample)};
         if (hp->power_iters < 0 || hp->power_iters > 8)
             return {NORMPRE_ERR_INVALID_ARG, fmt("power_iters %d outside 0..8", hp->power_iters)};
     }
-    const int k = orientation_of(*hp);
+    const int k = step_orientation(variant, *hp);
     for (int i = 0; i < num_mats; ++i) {
         const int64_t m = shapes[2 * i], n = shapes[2 * i + 1];
         if (m < 1 || n < 1)
             return {NORMPRE_ERR_INVALID_ARG, fmt("matrix %d has shape %lld x %lld", i, (long long)m, (long long)n)};
         if (m > kMaxDim || n > kMaxDim || m * n > kMaxElems)
             return {NORMPRE_ERR_UNSUPPORTED, fmt("matrix %d (%lld x %lld) is too large", i, (long long)m, (long long)n)};
-        if (k == 0 && n > kMaxRowLen)
+        if (k == 0 && n > kMaxRowLen && variant != NORMPRE_VARIANT_MUON)
             return {NORMPRE_ERR_UNSUPPORTED,
                     fmt("matrix %d: row-active rows of %lld elements exceed %d", i, (long long)n, kMaxRowLen)};
         if (variant == NORMPRE_VARIANT_L) {
@@ -353,9 +368,9 @@ void carve_item(Arena& ar, Item& it, int variant) {
     w.colpart = ar.take<double>(count * normalize_cols_partials((int)d.m, (int)d.np_, kColRowChunk));
     w.sumsq = ar.take<float>(count * std::max(ns_tiles(d), apply_tiles(d)));
     w.tn2 = ar.take<float>(count);
-    if (variant == NORMPRE_VARIANT_G) {
+    if (variant == NORMPRE_VARIANT_G || variant == NORMPRE_VARIANT_MUON) {
         w.xb = ar.take<half_t>(count * mn);
-    } else {
+    } else if (variant == NORMPRE_VARIANT_L) {
         const int64_t lp = d.ellp, maxpad = d.lp_;
         // Every l-major skinny buffer (Omega^T included) has the per-matrix
         // stride lp * maxpad that the sketch products assume.
@@ -372,10 +387,10 @@ void carve_item(Arena& ar, Item& it, int variant) {
 
 void carve_pool(Arena& ar, Pool& p, int variant) {
     const int64_t c = p.count;
-    if (variant == NORMPRE_VARIANT_G) {
+    if (variant == NORMPRE_VARIANT_G || variant == NORMPRE_VARIANT_MUON) {
         p.amat = ar.take<half_t>(c * p.sp * p.sp);
         p.bmat = ar.take<half_t>(c * p.sp * p.sp);
-    } else {
+    } else if (variant == NORMPRE_VARIANT_L) {
         const int64_t lp = p.ellp;
         p.gpart = ar.take<double>(c * kGramChunks * lp * lp);
         p.chol = ar.take<double>(c * 2 * lp * lp);
@@ -391,7 +406,7 @@ void carve_pool(Arena& ar, Pool& p, int variant) {
 std::vector<Pool> make_pools(std::vector<Item>& items, int variant) {
     std::vector<Pool> pools;
     for (Item& it : items) {
-        const int64_t key = variant == NORMPRE_VARIANT_G ? it.d.sp : it.d.ell;
+        const int64_t key = variant == NORMPRE_VARIANT_L ? it.d.ell : it.d.sp;
         int pi = -1;
         for (size_t q = 0; q < pools.size(); ++q)
             if (pools[q].key == key) pi = (int)q;
@@ -484,6 +499,7 @@ int run_normalize(const StepCtx& sc, const Dims& d, const GWork& w, const std::v
         a.mu = sc.hp->momentum;
         a.eps = sc.hp->norm_eps;
         a.vec_ok = chunk_vec_ok(a.ptrs, cnt);
+        a.tangent = tangent_mode(*sc.hp);
         if (dbg) {
             // Debug copies are written chunk by chunk into per-matrix buffers
             // that are contiguous in the order of the caller's list.
@@ -518,6 +534,51 @@ int run_normalize(const StepCtx& sc, const Dims& d, const GWork& w, const std::v
 
 // 256 x 256 tiles (8 waves) when a launch has enough of them to fill the
 // 256 CUs, else 128 x 128 tiles.
+// Muon reference input (Sec. 2.1): M <- mu M + G, ||M||_F, X0 = M / (||M||_F +
+// ns_eps) in fp16 (W layout, zero padded).  The per-block sums of M^2 reuse
+// the row-statistics buffer.
+int run_muon_input(const StepCtx& sc, const Dims& d, const GWork& w, const std::vector<int>& idx, int first,
+                   int count, DebugMat* dbg) {
+    const int64_t mn = d.mp * d.np_;
+    const int nblk = momentum_sumsq_blocks(d.m * d.n);
+    if (nblk > d.lp_) return set_err(sc.ctx, NORMPRE_ERR_HIP, "internal: muon partial buffer too small");
+    std::vector<NormArgs> chunks;
+    for (int c0 = 0; c0 < count; c0 += kChunk) {
+        const int cnt = std::min(kChunk, count - c0);
+        NormArgs a{};
+        a.ptrs = make_chunk(sc, idx, first + c0, cnt);
+        a.rows = (int)d.m;
+        a.cols = (int)d.n;
+        a.ld_psi = d.np_;
+        a.rows_pad = d.mp;
+        a.psi = w.psi + (int64_t)c0 * mn;
+        a.stride_psi = mn;
+        a.mu = sc.hp->momentum;
+        a.vec_ok = chunk_vec_ok(a.ptrs, cnt);
+        if (dbg) {
+            a.psi32 = dbg[idx[first + c0]].psi32;
+            a.stride_psi32 = d.m * d.n;
+            for (int i = 1; i < cnt; ++i)
+                if (dbg[idx[first + c0 + i]].psi32 != a.psi32 + i * d.m * d.n) a.psi32 = nullptr;
+            if (!a.psi32) return set_err(sc.ctx, NORMPRE_ERR_HIP, "internal: debug buffers not contiguous");
+        }
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NORMALIZE, 0.0, 12.0 * (double)d.m * (double)d.n * cnt,
+                     [&] { return launch_momentum_sumsq(a, cnt, w.psisq + (int64_t)c0 * d.lp_, d.lp_, sc.s); }),
+               "muon momentum");
+        chunks.push_back(a);
+    }
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+                 [&] { return launch_psi_scale(w.psisq, d.lp_, nblk, sc.hp->ns_eps, w.scale, count, sc.s); }),
+           "muon scale");
+    for (size_t c = 0; c < chunks.size(); ++c) {
+        const int c0 = (int)c * kChunk, cnt = std::min(kChunk, count - c0);
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NORMALIZE, 0.0, (4.0 * d.m * d.n + 2.0 * mn) * cnt,
+                     [&] { return launch_scaled_cast(chunks[c], cnt, w.scale + 2 * c0, sc.s); }),
+               "muon cast");
+    }
+    return NORMPRE_OK;
+}
+
 TileCfg ns_cfg(int64_t M, int64_t N, bool sym, int count) {
     const int64_t tm = M / 256, tn = N / 256;
     const int64_t tiles = sym ? tm * (tm + 1) / 2 : tm * tn;
@@ -600,10 +661,22 @@ int g_update_launch(const StepCtx& sc, const Item& it, const half_t* t, DebugMat
     const std::vector<int>& idx = (*sc.groups)[it.g].idx;
     const int first = it.first, count = it.count;
     const int64_t mn = d.mp * d.np_;
-    const int t_tiles = combine_tiles(d, ns_cfg(d.mp, d.np_, false, count));
-    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
-                 [&] { return launch_sum_partials(it.w.sumsq, t_tiles, it.w.tn2, count, sc.s); }),
-           "t norm");
+    // ||T||_F^2: NormPre-G from the last combine's per-tile sums; normalize-only
+    // (T = Psi) from the normalization's row sums; Muon uses a fixed scale.
+    const float* tn2 = it.w.tn2;
+    int64_t tn2_stride = 1;
+    float fixed_scale = 0.f;
+    if (sc.variant == NORMPRE_VARIANT_G) {
+        const int t_tiles = combine_tiles(d, ns_cfg(d.mp, d.np_, false, count));
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+                     [&] { return launch_sum_partials(it.w.sumsq, t_tiles, it.w.tn2, count, sc.s); }),
+               "t norm");
+    } else if (sc.variant == NORMPRE_VARIANT_NORMALIZE_ONLY) {
+        tn2 = it.w.scale + 1;
+        tn2_stride = 2;
+    } else {
+        fixed_scale = hp.target_rms * std::sqrt((float)std::max(d.m, d.n));
+    }
     for (int c0 = 0; c0 < count; c0 += kChunk) {
         const int cnt = std::min(kChunk, count - c0);
         GUpdateArgs a{};
@@ -613,14 +686,16 @@ int g_update_launch(const StepCtx& sc, const Item& it, const half_t* t, DebugMat
         a.t = t + (int64_t)c0 * mn;
         a.ld_t = d.np_;
         a.stride_t = mn;
-        a.tnorm2 = it.w.tn2 + c0;
+        a.tnorm2 = tn2 + c0 * tn2_stride;
+        a.tnorm2_stride = tn2_stride;
+        a.fixed_scale = fixed_scale;
         a.lr = hp.lr;
         a.wd = hp.weight_decay;
         a.target_rms = hp.target_rms;
         a.vec_ok = chunk_vec_ok(a.ptrs, cnt);
         if (dbg) {
             for (int i = 0; i < cnt; ++i) {
-                NP_TRY(hipMemcpyAsync(dbg[idx[first + c0 + i]].scalars, it.w.tn2 + c0 + i, sizeof(float),
+                NP_TRY(hipMemcpyAsync(dbg[idx[first + c0 + i]].scalars, tn2 + (c0 + i) * tn2_stride, sizeof(float),
                                       hipMemcpyDeviceToDevice, sc.s),
                        "dbg");
                 // one matrix per launch keeps the debug pointers simple
@@ -631,7 +706,7 @@ int g_update_launch(const StepCtx& sc, const Item& it, const half_t* t, DebugMat
                 pc.g[0] = a.ptrs.g[i];
                 b.ptrs = pc;
                 b.t = a.t + (int64_t)i * mn;
-                b.tnorm2 = a.tnorm2 + i;
+                b.tnorm2 = a.tnorm2 + i * tn2_stride;
                 b.t32 = dbg[idx[first + c0 + i]].t32;
                 b.stride_t32 = d.m * d.n;
                 NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_G_UPDATE, 0.0, 10.0 * d.m * d.n,
@@ -647,14 +722,22 @@ int g_update_launch(const StepCtx& sc, const Item& it, const half_t* t, DebugMat
     return NORMPRE_OK;
 }
 
+// NormPre-G, and the Muon and normalize-only reference steps, which share
+// its stages: input (normalize, or Muon's momentum + Frobenius scaling),
+// q Newton-Schulz iterations (none for normalize-only), update.
 int run_round_g(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& pools, DebugMat* dbg) {
     for (const Item& it : items) {
-        int rc = run_normalize(sc, it.d, it.w, (*sc.groups)[it.g].idx, it.first, it.count, dbg);
+        int rc = sc.variant == NORMPRE_VARIANT_MUON
+                     ? run_muon_input(sc, it.d, it.w, (*sc.groups)[it.g].idx, it.first, it.count, dbg)
+                     : run_normalize(sc, it.d, it.w, (*sc.groups)[it.g].idx, it.first, it.count, dbg);
         if (rc) return rc;
     }
-    const int q = sc.hp->ns_iters;
+    // Muon's X0 is scaled when it is written; NormPre-G folds 1/||Psi||_F
+    // into the first iteration's epilogues.
+    const bool fold_scale = sc.variant == NORMPRE_VARIANT_G;
+    const int q = sc.variant == NORMPRE_VARIANT_NORMALIZE_ONLY ? 0 : sc.hp->ns_iters;
     for (int iter = 0; iter < q; ++iter) {
-        const bool first_it = iter == 0, last_it = iter == q - 1;
+        const bool first_it = iter == 0 && fold_scale, last_it = iter == q - 1;
         for (const Item& it : items) {
             half_t* x = (iter & 1) ? it.w.xb : it.w.psi;
             int rc = gram_launch(sc, it, pools[it.pool], x, first_it);
@@ -1114,7 +1197,7 @@ int normpre_step(normpre_ctx* ctx, int variant, int num_mats, float* const* para
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
     hipStream_t s = static_cast<hipStream_t>(stream);
 
-    const int k = orientation_of(*hp);
+    const int k = step_orientation(variant, *hp);
     // Group equal shapes (first-appearance order) so each group is one batch.
     std::vector<Group> groups;
     {
@@ -1185,7 +1268,7 @@ int normpre_step(normpre_ctx* ctx, int variant, int num_mats, float* const* para
         Arena ar{static_cast<char*>(ctx->ws), 0, ctx->ws_bytes};
         carve_round(ar, items, pools, variant);
         DebugMat* dbg = debug ? ctx->dbg.data() : nullptr;
-        rc = variant == NORMPRE_VARIANT_G ? run_round_g(sc, items, pools, dbg) : run_round_l(sc, items, pools, dbg);
+        rc = variant == NORMPRE_VARIANT_L ? run_round_l(sc, items, pools, dbg) : run_round_g(sc, items, pools, dbg);
         if (rc) return rc;
     }
     ctx->last_stream = s;
@@ -1210,16 +1293,16 @@ int normpre_debug_fetch(normpre_ctx* ctx, int index, int what, void* host_out, i
     switch (what) {
         case NORMPRE_DEBUG_PSI: src = d.psi32; bytes = d.rows * d.cols * 4; break;
         case NORMPRE_DEBUG_T:
-            if (d.variant != NORMPRE_VARIANT_G) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "T is kept for NormPre-G only");
+            if (d.variant == NORMPRE_VARIANT_L) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "T is not kept for NormPre-L");
             src = d.t32; bytes = d.rows * d.cols * 4; break;
         case NORMPRE_DEBUG_RITZ:
-            if (d.variant != NORMPRE_VARIANT_L) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "no Ritz values for NormPre-G");
+            if (d.variant != NORMPRE_VARIANT_L) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "Ritz values are NormPre-L only");
             src = d.scalars + 2; bytes = (int64_t)d.top * 4; break;
         case NORMPRE_DEBUG_NSEL:
-            if (d.variant != NORMPRE_VARIANT_L) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "no selection for NormPre-G");
+            if (d.variant != NORMPRE_VARIANT_L) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "the selection is NormPre-L only");
             src = d.scalars + 1; bytes = 4; break;
         case NORMPRE_DEBUG_ELL:
-            if (d.variant != NORMPRE_VARIANT_L) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "no sketch for NormPre-G");
+            if (d.variant != NORMPRE_VARIANT_L) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "the sketch is NormPre-L only");
             scalar = d.ell; bytes = 4; break;
         case NORMPRE_DEBUG_TNORM2: src = d.scalars; bytes = 4; break;
         case NORMPRE_DEBUG_ORIENT: scalar = d.k; bytes = 4; break;

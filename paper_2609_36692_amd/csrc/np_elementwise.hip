@@ -6,11 +6,16 @@
 //   * the NormPre-G RMS-matched weight update (Sec. 3.1, "Consistent
 //     Update RMS", and the last line of Alg. 1).
 //
-// Row statistics use one fp64 pass: with d = <m, w>,
-//   ||x||^2 = ||m - d w||^2 = ||m||^2 + d^2 (||w||^2 - 2),
+// Row statistics use one fp64 pass: with x = m - c w,
+//   ||x||^2 = ||m||^2 - 2 c <m, w> + c^2 ||w||^2,
 // so the row (or column) is read once for the three sums and Psi is written
 // from values still held in registers (row-active case) or from a second,
-// cache-friendly pass (column-active case).
+// cache-friendly pass (column-active case).  c = <m, w> is the relaxed
+// tangent of Sec. 3.1; the ablation modes of App. A.4 use c = 0 (no tangent)
+// or c = <m, w> / ||w||^2 (strict tangent projection).
+//
+// Also the input of the Muon reference step (Sec. 2.1): momentum update with
+// per-block sums of M^2, then X0 = M / (||M||_F + eps) cast to fp16.
 #include "np_internal.h"
 
 namespace np {
@@ -25,6 +30,13 @@ __device__ __forceinline__ float wave_sum_f(float v) {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
     return v;
+}
+
+// Coefficient c of x = m - c w for the momentum-processing mode.
+__device__ __forceinline__ double tangent_coef(int mode, double smw, double sww) {
+    if (mode == kTangentNone) return 0.0;
+    if (mode == kTangentStrict) return sww > 0.0 ? smw / sww : 0.0;
+    return smw;
 }
 
 // Block-wide sum of three doubles; result valid in every thread.
@@ -90,8 +102,8 @@ __global__ void __launch_bounds__(NT) normalize_rows_kernel(NormArgs a) {
         }
     }
     block_sum3<NT>(smm, smw, sww);
-    const double d = smw;
-    const double nrm2 = fmax(smm + d * d * (sww - 2.0), 0.0);
+    const double d = tangent_coef(a.tangent, smw, sww);
+    const double nrm2 = fmax(smm - 2.0 * d * smw + d * d * sww, 0.0);
     const double nrm = sqrt(nrm2);
     const float inv = (float)(1.0 / fmax(nrm, (double)a.eps));
     const float df = (float)d;
@@ -184,7 +196,8 @@ __global__ void __launch_bounds__(kColThreads) normalize_cols_stats(NormArgs a, 
 }
 
 // Sums the row-chunk partials of each column once, in a fixed order, and
-// stores d = <m, w> and 1 / max(||x||, eps) in the chunk-0 slots.
+// stores the tangent coefficient c and 1 / max(||x||, eps) in the chunk-0
+// slots.
 __global__ void __launch_bounds__(256) normalize_cols_finalize(NormArgs a, double* partials, int nchunks) {
     const int z = blockIdx.y;
     const int col = blockIdx.x * 256 + threadIdx.x;
@@ -197,8 +210,8 @@ __global__ void __launch_bounds__(256) normalize_cols_finalize(NormArgs a, doubl
         smw += p[(c * 3 + 1) * cols_pad + col];
         sww += p[(c * 3 + 2) * cols_pad + col];
     }
-    const double d = smw;
-    const double nrm2 = fmax(smm + d * d * (sww - 2.0), 0.0);
+    const double d = tangent_coef(a.tangent, smw, sww);
+    const double nrm2 = fmax(smm - 2.0 * d * smw + d * d * sww, 0.0);
     const double inv = 1.0 / fmax(sqrt(nrm2), (double)a.eps);
     p[col] = d;
     p[cols_pad + col] = inv;
@@ -255,6 +268,78 @@ __global__ void __launch_bounds__(kColThreads) normalize_cols_apply(NormArgs a, 
 }
 
 // ---------------------------------------------------------------------------
+// Muon input, pass 1: M <- mu M + G over the whole matrix, with the block's
+// sum of M^2 (fp64 in each thread, fixed-order block reduction) written to
+// part[z * stride_part + block].
+template <int VW>
+__global__ void __launch_bounds__(256) momentum_sumsq_kernel(NormArgs a, float* part, int64_t stride_part) {
+    const int z = blockIdx.y;
+    float* M = a.ptrs.m[z];
+    const float* G = a.ptrs.g[z];
+    const int64_t nv = (int64_t)a.rows * a.cols / VW;
+    double s = 0.0;
+    for (int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x; v < nv; v += (int64_t)gridDim.x * 256) {
+        if constexpr (VW == 4) {
+            const float4 mp = reinterpret_cast<const float4*>(M)[v];
+            const float4 g = reinterpret_cast<const float4*>(G)[v];
+            float4 m;
+            m.x = fmaf(a.mu, mp.x, g.x); m.y = fmaf(a.mu, mp.y, g.y);
+            m.z = fmaf(a.mu, mp.z, g.z); m.w = fmaf(a.mu, mp.w, g.w);
+            reinterpret_cast<float4*>(M)[v] = m;
+            s = fma((double)m.x, (double)m.x, s); s = fma((double)m.y, (double)m.y, s);
+            s = fma((double)m.z, (double)m.z, s); s = fma((double)m.w, (double)m.w, s);
+        } else {
+            const float m = fmaf(a.mu, M[v], G[v]);
+            M[v] = m;
+            s = fma((double)m, (double)m, s);
+        }
+    }
+    s = wave_sum_d(s);
+    __shared__ double red[4];
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) part[(int64_t)z * stride_part + blockIdx.x] = (float)(red[0] + red[1] + red[2] + red[3]);
+}
+
+// Muon input, pass 2: X0 = M * scale[2z] in fp16 over the whole zero-padded
+// W-layout workspace (rows_pad x ld_psi); optional fp32 copy of X0.
+template <int VW, bool DBG>
+__global__ void __launch_bounds__(256) scaled_cast_kernel(NormArgs a, const float* scale) {
+    const int z = blockIdx.y;
+    const float sc = scale[2 * z];
+    const float* M = a.ptrs.m[z];
+    half_t* P = a.psi + (int64_t)z * a.stride_psi;
+    const int64_t vpr = a.ld_psi / VW;
+    const int64_t nv = a.rows_pad * vpr;
+    for (int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x; v < nv; v += (int64_t)gridDim.x * 256) {
+        const int64_t row = v / vpr;
+        const int64_t col = (v - row * vpr) * VW;
+        float x[VW];
+#pragma unroll
+        for (int e = 0; e < VW; ++e) x[e] = 0.f;
+        if (row < a.rows && col < a.cols) {
+            const int64_t o = row * a.cols + col;
+            if constexpr (VW == 4) {
+                const float4 m = *reinterpret_cast<const float4*>(M + o);
+                x[0] = m.x * sc; x[1] = m.y * sc; x[2] = m.z * sc; x[3] = m.w * sc;
+                if constexpr (DBG)
+                    *reinterpret_cast<float4*>(a.psi32 + (int64_t)z * a.stride_psi32 + o) = make_float4(x[0], x[1], x[2], x[3]);
+            } else {
+                x[0] = M[o] * sc;
+                if constexpr (DBG) a.psi32[(int64_t)z * a.stride_psi32 + o] = x[0];
+            }
+        }
+        half_t* dst = P + row * a.ld_psi + col;
+        if constexpr (VW == 4) {
+            half_t h[4] = {(half_t)x[0], (half_t)x[1], (half_t)x[2], (half_t)x[3]};
+            *reinterpret_cast<uint2*>(dst) = *reinterpret_cast<const uint2*>(h);
+        } else {
+            dst[0] = (half_t)x[0];
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 __global__ void __launch_bounds__(256) psi_scale_kernel(const float* psisq, int64_t stride, int active_rows,
                                                         float eps, float* out) {
     const int z = blockIdx.x;
@@ -276,8 +361,11 @@ __global__ void __launch_bounds__(256) psi_scale_kernel(const float* psisq, int6
 template <int VW, bool DBG>
 __global__ void __launch_bounds__(256) g_update_kernel(GUpdateArgs a) {
     const int z = blockIdx.y;
-    const float t2 = a.tnorm2[z];
-    const float scale = t2 > 0.f ? a.target_rms * sqrtf((float)a.rows * (float)a.cols) / sqrtf(t2) : 0.f;
+    float scale = a.fixed_scale;
+    if (!(scale > 0.f)) {
+        const float t2 = a.tnorm2[(int64_t)z * a.tnorm2_stride];
+        scale = t2 > 0.f ? a.target_rms * sqrtf((float)a.rows * (float)a.cols) / sqrtf(t2) : 0.f;
+    }
 
     float* W = a.ptrs.w[z];
     const half_t* T = a.t + (int64_t)z * a.stride_t;
@@ -394,6 +482,34 @@ hipError_t cols_launch(const NormArgs& a, int batch, double* partials, int row_c
 hipError_t launch_normalize_cols(const NormArgs& a, int batch, double* partials, int row_chunk, hipStream_t s) {
     if (a.vec_ok && a.cols % 4 == 0 && a.ld_psi % 4 == 0) return cols_launch<4>(a, batch, partials, row_chunk, s);
     return cols_launch<1>(a, batch, partials, row_chunk, s);
+}
+
+int momentum_sumsq_blocks(int64_t elems) {
+    return (int)std::max<int64_t>(1, std::min<int64_t>(256, (elems + 4095) / 4096));
+}
+
+hipError_t launch_momentum_sumsq(const NormArgs& a, int batch, float* part, int64_t stride_part, hipStream_t s) {
+    const int64_t n = (int64_t)a.rows * a.cols;
+    const bool vec = a.vec_ok && n % 4 == 0;
+    dim3 grid((unsigned)momentum_sumsq_blocks(n), batch);
+    if (vec) hipLaunchKernelGGL((momentum_sumsq_kernel<4>), grid, dim3(256), 0, s, a, part, stride_part);
+    else hipLaunchKernelGGL((momentum_sumsq_kernel<1>), grid, dim3(256), 0, s, a, part, stride_part);
+    return hipGetLastError();
+}
+
+hipError_t launch_scaled_cast(const NormArgs& a, int batch, const float* scale, hipStream_t s) {
+    const bool vec = a.vec_ok && a.cols % 4 == 0 && a.ld_psi % 4 == 0;
+    const int64_t nv = a.rows_pad * a.ld_psi / (vec ? 4 : 1);
+    dim3 grid((unsigned)std::max<int64_t>(1, std::min<int64_t>((nv + 255) / 256, 2048)), batch);
+    const bool dbg = a.psi32 != nullptr;
+    if (vec) {
+        if (dbg) hipLaunchKernelGGL((scaled_cast_kernel<4, true>), grid, dim3(256), 0, s, a, scale);
+        else hipLaunchKernelGGL((scaled_cast_kernel<4, false>), grid, dim3(256), 0, s, a, scale);
+    } else {
+        if (dbg) hipLaunchKernelGGL((scaled_cast_kernel<1, true>), grid, dim3(256), 0, s, a, scale);
+        else hipLaunchKernelGGL((scaled_cast_kernel<1, false>), grid, dim3(256), 0, s, a, scale);
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch_psi_scale(const float* psisq, int64_t stride, int active_rows, float eps, float* out,

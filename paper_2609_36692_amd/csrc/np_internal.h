@@ -119,7 +119,9 @@ struct NormArgs {
     float* psisq; int64_t stride_psisq; // per active row ||psi_i||^2
     float mu, eps;
     int vec_ok;                     // 16-byte aligned W, M, G rows
+    int tangent;                    // kTangentRelaxed / kTangentNone / kTangentStrict
 };
+constexpr int kTangentRelaxed = 0, kTangentNone = 1, kTangentStrict = 2;
 hipError_t launch_normalize_rows(const NormArgs& a, int batch, hipStream_t s);
 // Column-active orientation: stats pass + normalize pass.
 hipError_t launch_normalize_cols(const NormArgs& a, int batch, double* partials,
@@ -141,12 +143,20 @@ struct GUpdateArgs {
     PtrChunk ptrs;
     int rows, cols;
     const half_t* t; int64_t ld_t; int64_t stride_t;
-    const float* tnorm2;            // per-matrix ||T||_F^2
+    const float* tnorm2;            // ||T||_F^2 of matrix z at tnorm2[z * tnorm2_stride]
+    int64_t tnorm2_stride;
+    float fixed_scale;              // > 0: U = fixed_scale * T instead of the RMS match
     float lr, wd, target_rms;
     float* t32; int64_t stride_t32; // optional fp32 copy of T (debug)
     int vec_ok;                     // 16-byte aligned W rows
 };
 hipError_t launch_g_update(const GUpdateArgs& a, int batch, hipStream_t s);
+// Muon input: momentum update with per-block sums of M^2 (part, one float per
+// block, momentum_sumsq_blocks(rows*cols) blocks), then X0 = M * scale[2z]
+// to fp16 in the zero-padded workspace.
+int momentum_sumsq_blocks(int64_t elems);
+hipError_t launch_momentum_sumsq(const NormArgs& a, int batch, float* part, int64_t stride_part, hipStream_t s);
+hipError_t launch_scaled_cast(const NormArgs& a, int batch, const float* scale, hipStream_t s);
 
 // ------------------------------------------------------ sketch kernels ---
 // Omega^T (l x b) in fp16, zero padded to (l_pad x b_pad), ld = b_pad.

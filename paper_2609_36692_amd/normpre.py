@@ -25,11 +25,17 @@ NORMPRE_ERR_NOT_INITIALIZED = -5
 
 NORMPRE_VARIANT_G = 0
 NORMPRE_VARIANT_L = 1
+NORMPRE_VARIANT_MUON = 2
+NORMPRE_VARIANT_NORMALIZE_ONLY = 3
+VARIANTS = {"G": NORMPRE_VARIANT_G, "L": NORMPRE_VARIANT_L, "MUON": NORMPRE_VARIANT_MUON,
+            "NORM": NORMPRE_VARIANT_NORMALIZE_ONLY}
 NORMPRE_ORIENT_ALTERNATING = 0
 NORMPRE_ORIENT_ROW = 1
 NORMPRE_ORIENT_COL = 2
 NORMPRE_FLAG_DEBUG = 1
 NORMPRE_FLAG_TIME_KERNELS = 2
+NORMPRE_FLAG_TANGENT_NONE = 4
+NORMPRE_FLAG_TANGENT_STRICT = 8
 
 NORMPRE_DEBUG_PSI = 0
 NORMPRE_DEBUG_T = 1
@@ -39,6 +45,15 @@ NORMPRE_DEBUG_ELL = 4
 NORMPRE_DEBUG_TNORM2 = 5
 NORMPRE_DEBUG_ORIENT = 6
 
+NORMPRE_KCLASS_NORMALIZE = 0
+NORMPRE_KCLASS_NS_GRAM = 1
+NORMPRE_KCLASS_NS_POLY = 2
+NORMPRE_KCLASS_NS_COMBINE = 3
+NORMPRE_KCLASS_G_UPDATE = 4
+NORMPRE_KCLASS_SK_STREAM = 5
+NORMPRE_KCLASS_SK_SMALL = 6
+NORMPRE_KCLASS_L_APPLY = 7
+NORMPRE_KCLASS_COUNT = 8
 KCLASS_NAMES = ["normalize", "ns_gram", "ns_poly", "ns_combine", "g_update",
                 "sk_stream", "sk_small", "l_apply"]
 
@@ -219,7 +234,7 @@ class NormPre:
     def __init__(self, params, variant: str = "G", device: int | None = None, **hparams):
         import torch
         self.params = list(params)
-        self.variant = NORMPRE_VARIANT_G if variant.upper() == "G" else NORMPRE_VARIANT_L
+        self.variant = VARIANTS[variant.upper()]
         dev = self.params[0].device.index if device is None else device
         self.ctx = normpre_init(0 if dev is None else dev)
         self.hp = normpre_default_hparams(**hparams)

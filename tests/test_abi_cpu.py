@@ -61,7 +61,13 @@ def test_version(N):
 @pytest.mark.parametrize("variant,shapes,over,code", [
     (0, [(768, 2304)], {}, 0),
     (1, [(768, 2304), (3072, 768)], {}, 0),
-    (2, [(8, 8)], {}, -1),
+    (2, [(8, 8)], {}, 0),                            # Muon reference step
+    (3, [(8, 8)], {}, 0),                            # normalize-only reference step
+    (4, [(8, 8)], {}, -1),
+    (-1, [(8, 8)], {}, -1),
+    (2, [(8, 8)], {"ns_iters": 0}, -1),
+    (2, [(8, 40000)], {}, 0),                        # Muon has no row-active pass
+    (3, [(8, 40000)], {}, -2),
     (0, [(0, 8)], {}, -1),
     (0, [(8, -1)], {}, -1),
     (0, [(8, 8)], {"ns_iters": 0}, -1),
@@ -74,7 +80,10 @@ def test_version(N):
     (0, [(8, 8)], {"weight_decay": float("inf")}, -1),
     (0, [(8, 8)], {"norm_eps": 0.0}, -1),
     (0, [(8, 8)], {"orientation": 3}, -1),
-    (0, [(8, 8)], {"flags": 8}, -1),
+    (0, [(8, 8)], {"flags": 16}, -1),
+    (0, [(8, 8)], {"flags": 4}, 0),                  # no tangent
+    (1, [(8, 8)], {"flags": 8}, 0),                  # strict tangent
+    (0, [(8, 8)], {"flags": 12}, -1),                # both tangent modes
     (0, [(8, 40000)], {}, -2),                       # row-active row too long
     (0, [(8, 40000)], {"orientation": 2}, 0),        # column-active is fine
     (0, [(8, 40000)], {"step": 1}, 0),               # t odd -> column-active
@@ -132,3 +141,16 @@ def test_binding_fails_loudly_without_library(tmp_path):
             normpre.load_library(str(tmp_path / "missing.so"))
         finally:
             normpre._lib = saved
+
+
+def test_header_constants_match_binding(N):
+    """Every NORMPRE_* integer constant of include/normpre.h has the same value
+    in the Python binding."""
+    import re
+    hdr = open(os.path.join(ROOT, "include", "normpre.h")).read()
+    consts = dict(re.findall(r"#define\s+(NORMPRE_[A-Z_0-9]+)\s+\(?(-?\d+)u?\)?", hdr))
+    assert consts, "no constants parsed"
+    missing = [k for k in consts if not hasattr(N, k)]
+    assert not missing, missing
+    for k, v in consts.items():
+        assert getattr(N, k) == int(v), (k, getattr(N, k), v)

@@ -67,10 +67,9 @@ def run_step(ctx, variant, mats, t, lr=1.0, wd=0.0, debug=True, **hp_over):
     Ws = [m[0].to(dev).clone() for m in mats]
     Gs = [m[1].to(dev).clone() for m in mats]
     Ms = [m[2].to(dev).clone() for m in mats]
-    flags = N.NORMPRE_FLAG_DEBUG if debug else 0
+    flags = hp_over.pop("flags", N.NORMPRE_FLAG_DEBUG if debug else 0)
     hp = N.normpre_default_hparams(lr=lr, weight_decay=wd, step=t, flags=flags, **hp_over)
-    v = N.NORMPRE_VARIANT_G if variant == "G" else N.NORMPRE_VARIANT_L
-    N.normpre_step(ctx, v, Ws, Gs, Ms, hp)
+    N.normpre_step(ctx, N.VARIANTS[variant], Ws, Gs, Ms, hp)
     torch.cuda.synchronize()
     out = []
     for (w, g, mp), W, M in zip(mats, Ws, Ms):
@@ -242,3 +241,62 @@ def test_invalid_args_leave_buffers_untouched(ctx):
         N.normpre_step(ctx, N.NORMPRE_VARIANT_G, [W], [G], [W], hp)   # W aliases M
     torch.cuda.synchronize()
     assert torch.equal(W.cpu(), mat[0]) and torch.equal(M.cpu(), mat[2])
+
+
+# ------------------------------------------- reference steps and ablations
+# Muon: the same fp16 Newton-Schulz path as NormPre-G (TOL_G).  Normalize-only:
+# U is the fp16 Psi rescaled, so fp16 rounding of Psi (u16 per element) bounds
+# it: 4 u16 relative Frobenius.
+TOL_NORM = 4.0 * U16
+REF_SHAPES = [(256, 256), (257, 513), (300, 1), (1, 300), (768, 2304), (3072, 768)]
+
+
+@pytest.mark.parametrize("variant", ["MUON", "NORM"])
+@pytest.mark.parametrize("shape", REF_SHAPES)
+@pytest.mark.parametrize("t", [0, 1])
+def test_reference_steps(ctx, variant, shape, t):
+    _say(f"reference step {variant} shape={shape} t={t}")
+    mat = _inputs(shape, "powerlaw" if min(shape) > 1 else "lowrank", seed=3)
+    res = run_step(ctx, variant, [mat], t)[0]
+    ref = oracle(mat, variant, t)
+    assert O.relative_fro(res["m"].numpy(), ref["momentum"]) < 1e-6
+    psi = N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_PSI, shape[0] * shape[1]).reshape(shape)
+    assert O.relative_fro(psi, ref["psi"]) < TOL_PSI
+    tol = TOL_G if variant == "MUON" else TOL_NORM
+    err = O.relative_fro(res["u"], ref["update"])
+    _say(f"  update err {err:.2e} (tol {tol:.1e})")
+    assert err < tol
+    if variant == "NORM":
+        assert math.isclose(np.linalg.norm(res["u"]), 0.2 * math.sqrt(shape[0] * shape[1]), rel_tol=2e-3)
+
+
+@pytest.mark.parametrize("variant", ["G", "L", "NORM"])
+@pytest.mark.parametrize("mode", ["none", "strict"])
+@pytest.mark.parametrize("t", [0, 1])
+def test_tangent_modes(ctx, variant, mode, t):
+    shape = (257, 513)
+    _say(f"tangent {mode} {variant} t={t}")
+    w, g, mp = _inputs(shape, "lowrank", seed=5)
+    w = w * 25.0   # rows of norm ~11: strict and relaxed differ visibly
+    mat = (w, g, mp)
+    flag = N.NORMPRE_FLAG_TANGENT_NONE if mode == "none" else N.NORMPRE_FLAG_TANGENT_STRICT
+    res = run_step(ctx, variant, [mat], t, flags=N.NORMPRE_FLAG_DEBUG | flag)[0]
+    ref = oracle(mat, variant, t, tangent=mode)
+    psi = N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_PSI, shape[0] * shape[1]).reshape(shape)
+    assert O.relative_fro(psi, ref["psi"]) < TOL_PSI
+    # the three modes give different Psi on these inputs (the flag took effect)
+    relaxed = oracle(mat, variant, t)
+    assert O.relative_fro(ref["psi"], relaxed["psi"]) > 10 * TOL_PSI
+    tol = {"G": TOL_G, "NORM": TOL_NORM}.get(variant) or tol_l(ref)
+    err = O.relative_fro(res["u"], ref["update"])
+    _say(f"  update err {err:.2e} (tol {tol:.1e})")
+    assert err < tol
+
+
+@pytest.mark.parametrize("variant", ["MUON", "NORM"])
+def test_reference_steps_zero_signal(ctx, variant):
+    shape = (300, 200)
+    w = torch.randn(shape) * 0.02
+    z = torch.zeros(shape)
+    res = run_step(ctx, variant, [(w, z, z)], 0, lr=0.5, wd=0.1)[0]
+    np.testing.assert_allclose(res["w"].numpy(), (w * (1 - 0.5 * 0.1)).numpy(), rtol=1e-6, atol=1e-9)

@@ -341,3 +341,88 @@ def test_orientation_alternates_with_t():
     # k = 1 normalises the columns of the W layout
     psi = O.normpre_step(w, g, mp, 1, hp, "G")["psi"]
     assert np.allclose(np.linalg.norm(psi, axis=0), 1.0)
+
+
+# ------------------------------------------------------------------ reference steps and ablations
+def test_strict_tangent_removes_the_radial_component():
+    # Exact tangent projection (App. A.4): <x_i, w_i> = 0 for any weight scale,
+    # equal to the relaxed form on unit rows (Sec. 3.1), identity on zero rows.
+    m, w = _rand(9, 14), _rand(9, 14, 3.0)
+    w[4] = 0.0
+    x = O.strict_tangent(m, w)
+    assert np.max(np.abs(np.sum(x * w, axis=1))) < 1e-12 * np.max(np.abs(m)) * np.max(np.abs(w)) * 14
+    np.testing.assert_allclose(x[4], m[4], rtol=0, atol=0)
+    wu = w / np.maximum(np.linalg.norm(w, axis=1, keepdims=True), 1e-300)
+    wu[4] = 0.0
+    np.testing.assert_allclose(O.strict_tangent(m, wu), O.relaxed_tangent(m, wu), rtol=1e-13, atol=1e-13)
+    # a plausible slip (dividing by ||w|| instead of ||w||^2) breaks orthogonality
+    d = np.sum(m * w, axis=1) / np.linalg.norm(w, axis=1).clip(1e-300)
+    bad = m - d[:, None] * w
+    assert np.max(np.abs(np.sum(bad * w, axis=1))) > 1e-3
+
+
+def test_tangent_none_normalizes_the_momentum_rows():
+    w, g, mp = _rand(6, 11), _rand(6, 11), _rand(6, 11)
+    hp = O.HParams(tangent="none", lr=1.0, weight_decay=0.0)
+    r = O.normpre_step(w, g, mp, 0, hp, "NORM")
+    m = hp.momentum * mp + g
+    np.testing.assert_allclose(r["psi"], m / np.linalg.norm(m, axis=1, keepdims=True), rtol=1e-13, atol=1e-14)
+
+
+def test_normalize_only_rows_and_rms():
+    # T = Psi: every active row of U has the same norm 0.2 sqrt(mn / a) and
+    # points along x_i (Sec. 2.2 with P = I, Sec. 3.1 RMS).
+    w, g, mp = _rand(12, 7), _rand(12, 7), _rand(12, 7)
+    hp = O.HParams(lr=1.0, weight_decay=0.0)
+    for t in (0, 1):
+        r = O.normpre_step(w, g, mp, t, hp, "NORM")
+        u_act = O.orient(r["update"], r["k"])
+        a = u_act.shape[0]
+        np.testing.assert_allclose(np.linalg.norm(u_act, axis=1), 0.2 * math.sqrt(w.size / a), rtol=1e-12)
+        x = O.relaxed_tangent(O.orient(hp.momentum * mp + g, r["k"]), O.orient(w, r["k"]))
+        cos = np.sum(u_act * x, axis=1) / (np.linalg.norm(u_act, axis=1) * np.linalg.norm(x, axis=1))
+        np.testing.assert_allclose(cos, 1.0, rtol=0, atol=1e-12)
+
+
+def test_normalize_only_equals_g_on_orthogonal_rows():
+    # Orthonormal Psi rows: the Newton-Schulz map scales Psi uniformly, so after
+    # the RMS match NormPre-G and the P = I step give the same update.
+    q, _ = np.linalg.qr(RNG.standard_normal((20, 6)))
+    g = (q.T * RNG.uniform(0.5, 3.0, 6)[:, None])   # 6 x 20, orthogonal rows
+    z = np.zeros_like(g)
+    hp = O.HParams(lr=1.0, weight_decay=0.0, orientation="row")
+    rg = O.normpre_step(z, g, z, 0, hp, "G")
+    rn = O.normpre_step(z, g, z, 0, hp, "NORM")
+    np.testing.assert_allclose(rg["update"], rn["update"], rtol=1e-10, atol=1e-12)
+
+
+def test_muon_with_cubic_iteration_is_scaled_polar_factor():
+    # Muon (Sec. 2.1): msign of the momentum; with Higham's cubic iterated to
+    # convergence U = 0.2 sqrt(max(m, n)) U_M V_M^T and ||U||_F = 0.2 sqrt(mn).
+    for shape in [(8, 21), (21, 8)]:
+        w, g, mp = _rand(*shape), _rand(*shape), _rand(*shape)
+        hp = O.HParams(lr=1.0, weight_decay=0.0, ns_iters=60, ns_coeffs=O.CUBIC_NS_COEFFS)
+        r = O.normpre_step(w, g, mp, 0, hp, "MUON")
+        m = hp.momentum * mp + g
+        np.testing.assert_allclose(r["update"], 0.2 * math.sqrt(max(shape)) * O.msign_svd(m), rtol=0, atol=1e-10)
+        assert math.isclose(np.linalg.norm(r["update"]), 0.2 * math.sqrt(w.size), rel_tol=1e-10)
+
+
+def test_muon_invariances():
+    w, g, mp = _rand(10, 16), _rand(10, 16), _rand(10, 16)
+    hp = O.HParams(lr=1.0, weight_decay=0.0, ns_eps=0.0)
+    r = O.normpre_step(w, g, mp, 0, hp, "MUON")
+    # scale of (G, M_prev) drops out (Frobenius pre-scaling, exact with no
+    # epsilon); t has no effect
+    r2 = O.normpre_step(w, 7.0 * g, 7.0 * mp, 1, hp, "MUON")
+    np.testing.assert_allclose(r2["update"], r["update"], rtol=1e-9, atol=1e-12)
+    # transposed inputs give the transposed update (odd polynomial in X X^T)
+    rt = O.normpre_step(w.T, g.T, mp.T, 0, hp, "MUON")
+    np.testing.assert_allclose(rt["update"], r["update"].T, rtol=1e-9, atol=1e-12)
+    # and, unlike NormPre, Muon does not equalize row scales: scaling one row
+    # of G and M_prev changes the update
+    g3, m3 = g.copy(), mp.copy()
+    g3[2] *= 10.0
+    m3[2] *= 10.0
+    r3 = O.normpre_step(w, g3, m3, 0, hp, "MUON")
+    assert O.relative_fro(r3["update"], r["update"]) > 1e-2
