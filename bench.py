@@ -145,7 +145,7 @@ def time_variant(N, WL, torch, wl, variant, steps, warmup, rank):
     ws, gs, ms = WL.make_stack(wl, dev)
     torch.cuda.synchronize()
     ctx = N.normpre_init(0)
-    v = N.NORMPRE_VARIANT_G if variant == "G" else N.NORMPRE_VARIANT_L
+    v = N.VARIANTS[variant]
     hp = N.normpre_default_hparams(lr=wl.lr, rank=rank, oversample=wl.oversample,
                                    power_iters=wl.power_iters)
     t = 0
@@ -308,10 +308,13 @@ def main():
     for v in variants:
         r = time_variant(N, WL, torch, wl, v, a.steps, a.warmup, rank)
         cls = r["classes"]
-        if v == "G":
+        if v in ("G", "MUON"):
             ns = merge_classes(cls, ["ns_gram", "ns_poly", "ns_combine"])
             roof = roofline_of(ns, "mfma")
             roof["kernel"] = "Newton-Schulz GEMMs (gram + poly + combine, fp16 MFMA)"
+        elif v == "NORM":
+            roof = roofline_of(cls["normalize"], "hbm")
+            roof["kernel"] = "momentum + tangent + normalization"
         else:
             roof = roofline_of(cls["sk_stream"], "hbm")
             roof["kernel"] = "sketch products streaming Psi (fp16 MFMA, split-K)"
@@ -332,11 +335,17 @@ def main():
             "kernel_ms_per_step": {k: round(c["ms"] / a.steps, 4) for k, c in cls.items() if c["launches"]},
             "kernel_share": {k: round(c["ms"] / total_dev, 4) for k, c in cls.items() if c["launches"]},
         }
-        if v == "G":
+        if v in ("G", "MUON"):
             res[v]["ns_tflops_step"] = round(ns["flops"] / a.steps / 1e12, 4)
             res[v]["ns_tflops_per_s_in_step"] = round(ns["flops"] / a.steps / 1e12 / (r["ms_per_step"] / 1e3), 2)
         print(f"[bench] NormPre-{v}: {res[v]['ms_per_step']:.3f} ms/step", file=sys.stderr, flush=True)
 
+    # Optimizer latency relative to the Muon reference step through the same
+    # kernels (the comparison of the paper's efficiency tables).
+    rel = None
+    if "MUON" in res:
+        rel = {f"{v}_vs_MUON": round(res[v]["ms_per_step"] / res["MUON"]["ms_per_step"] - 1.0, 4)
+               for v in res if v != "MUON"}
     copy_ref = copy_reference(torch, a.copy_mib) if a.copy_mib > 0 else None
 
     cpu = None
@@ -374,6 +383,8 @@ def main():
     }
     if copy_ref:
         line["copy_reference"] = copy_ref
+    if rel:
+        line["latency_vs_muon"] = rel
     s = json.dumps(line)
     if a.json_out:
         with open(a.json_out, "w") as f:
