@@ -146,7 +146,7 @@ __device__ __forceinline__ double gram_at(const double* p, int chunks, int ell_p
 // The matrix lives in LDS (fp64, row stride l + 1) when it fits, else in a
 // global scratch slice; R^{-1} overwrites R in place, bottom row first.
 constexpr double kDropTol = 1e-12;
-constexpr int kCholLdsMax = 128;
+constexpr int kCholLdsMax = 138;
 constexpr int kSmallThreads = 512;
 
 template <bool IN_LDS>
@@ -189,6 +189,9 @@ __global__ void __launch_bounds__(kSmallThreads) chol_inv_kernel(const double* p
         for (int j = k + 1 + tid; j < ell; j += NT) R[k * ld + j] *= ik;
         __syncthreads();
         const int nrem = ell - k - 1;
+        // Independent updates; unrolled so several global (scratch-mode)
+        // loads are in flight per thread.
+#pragma unroll 4
         for (int q = tid; q < nrem * nrem; q += NT) {
             const int i = k + 1 + q / nrem, j = k + 1 + q % nrem;
             if (j >= i) R[i * ld + j] -= R[k * ld + i] * R[k * ld + j];
@@ -203,9 +206,18 @@ __global__ void __launch_bounds__(kSmallThreads) chol_inv_kernel(const double* p
             if (j == i) {
                 v = ii;
             } else {
-                double s = 0.0;
-                for (int k = i + 1; k <= j; ++k) s += R[i * ld + k] * R[k * ld + j];
-                v = -s * ii;
+                // Four partial sums so consecutive loads do not wait on one
+                // accumulator chain.
+                double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+                int k = i + 1;
+                for (; k + 3 <= j; k += 4) {
+                    s0 += R[i * ld + k] * R[k * ld + j];
+                    s1 += R[i * ld + k + 1] * R[(k + 1) * ld + j];
+                    s2 += R[i * ld + k + 2] * R[(k + 2) * ld + j];
+                    s3 += R[i * ld + k + 3] * R[(k + 3) * ld + j];
+                }
+                for (; k <= j; ++k) s0 += R[i * ld + k] * R[k * ld + j];
+                v = -((s0 + s1) + (s2 + s3)) * ii;
             }
             tmp[j] = v;
         }
@@ -280,7 +292,10 @@ __global__ void __launch_bounds__(256) small_mul_kernel(SmallMulArgs a) {
 // J1^T block J2 for every pair of pairs, and columns (p, q) of Z become Z J.
 // A and Z live in LDS (row stride l + 1) when they fit, else in a global
 // scratch slice.
-constexpr int kEigLdsMax = 128;
+constexpr int kEigLdsMax = 138;
+// Packed mode: the upper triangle of A (rows packed) in LDS, Z^T in a global
+// scratch slice; used above kEigLdsMax while l (l + 1) / 2 floats fit.
+constexpr int kEigPackedMax = 278;
 
 __device__ __forceinline__ void rr_pair(int round, int k, int n2, int& p, int& q) {
     const int n1 = n2 - 1;
@@ -424,6 +439,167 @@ __global__ void __launch_bounds__(kSmallThreads) eig_select_kernel(EigArgs a) {
     }
 }
 
+// Index of (r, c) in the packed upper triangle of an n x n symmetric matrix.
+__device__ __forceinline__ int pk(int r, int c, int n) {
+    if (r > c) { const int t = r; r = c; c = t; }
+    return r * n - (r * (r - 1)) / 2 + (c - r);
+}
+
+// The same Jacobi sweep, selection and K as eig_select_kernel, with A packed
+// in LDS and Z stored transposed (row i = Ritz vector i) in global memory, so
+// the rotation of columns p, q of Z updates two contiguous rows.  Only the
+// pair-blocks (k1 <= k2) of the upper triangle are rotated; the diagonal
+// block keeps its three distinct entries.
+__global__ void __launch_bounds__(kSmallThreads) eig_select_packed_kernel(EigArgs a) {
+    constexpr int NT = kSmallThreads;
+    extern __shared__ float A[];
+    const int z = blockIdx.x, tid = threadIdx.x;
+    const int n = a.ell, lp = a.ell_pad;
+    float* Zt = a.scratch + (int64_t)z * 2 * lp * lp;
+    __shared__ float cs[192], sn[192];
+    __shared__ int pp[192], qq[192];
+    __shared__ float red[NT / 64];
+    __shared__ float lam[384], fcoef[384];
+    __shared__ int rnk[384];
+    __shared__ int stop_flag;
+    const double* part = a.partial + (int64_t)z * a.chunks * lp * lp;
+    for (int q = tid; q < n * n; q += NT) {
+        const int c = q / n, d = q - (q / n) * n;
+        if (c <= d) A[pk(c, d, n)] = (float)gram_at(part, a.chunks, lp, c, d);
+        Zt[(int64_t)c * lp + d] = c == d ? 1.f : 0.f;
+    }
+    __syncthreads();
+    const int n2 = n + (n & 1);
+    const int npairs = n2 / 2;
+    for (int sweep = 0; sweep < a.max_sweeps; ++sweep) {
+        float off = 0.f, tot = 0.f;
+        for (int q = tid; q < n * n; q += NT) {
+            const int c = q / n, d = q - (q / n) * n;
+            if (c > d) continue;
+            const float v = A[pk(c, d, n)] * A[pk(c, d, n)];
+            tot += c == d ? v : 2.f * v;
+            if (c != d) off += 2.f * v;
+        }
+        off = block_sum_f<NT>(off, red);
+        tot = block_sum_f<NT>(tot, red);
+        if (tid == 0) stop_flag = !(off > 1e-13f * tot);
+        __syncthreads();
+        if (stop_flag) break;
+        for (int round = 0; round < n2 - 1; ++round) {
+            for (int k = tid; k < npairs; k += NT) {
+                int p, q;
+                rr_pair(round, k, n2, p, q);
+                float c = 1.f, s = 0.f;
+                if (q < n) {
+                    const float apq = A[pk(p, q, n)];
+                    const float app = A[pk(p, p, n)], aqq = A[pk(q, q, n)];
+                    if (fabsf(apq) > 1e-30f && fabsf(apq) > 1e-9f * sqrtf(fabsf(app * aqq))) {
+                        const float theta = (aqq - app) / (2.f * apq);
+                        float t;
+                        if (fabsf(theta) > 1e15f) t = 0.5f / theta;
+                        else t = copysignf(1.f, theta) / (fabsf(theta) + sqrtf(theta * theta + 1.f));
+                        c = 1.f / sqrtf(t * t + 1.f);
+                        s = t * c;
+                    }
+                }
+                cs[k] = c; sn[k] = s; pp[k] = p; qq[k] = q;
+            }
+            __syncthreads();
+            for (int w = tid; w < npairs * npairs; w += NT) {
+                const int k1 = w / npairs, k2 = w - k1 * npairs;
+                if (k1 > k2) continue;
+                const int p1 = pp[k1], q1 = qq[k1], p2 = pp[k2], q2 = qq[k2];
+                const float c1 = cs[k1], s1 = sn[k1], c2 = cs[k2], s2 = sn[k2];
+                const bool r1 = q1 < n, r2 = q2 < n;
+                const float a00 = A[pk(p1, p2, n)];
+                const float a01 = r2 ? A[pk(p1, q2, n)] : 0.f;
+                const float a10 = r1 ? A[pk(q1, p2, n)] : 0.f;
+                const float a11 = (r1 && r2) ? A[pk(q1, q2, n)] : 0.f;
+                const float b00 = c1 * a00 - s1 * a10, b01 = c1 * a01 - s1 * a11;
+                const float b10 = s1 * a00 + c1 * a10, b11 = s1 * a01 + c1 * a11;
+                A[pk(p1, p2, n)] = c2 * b00 - s2 * b01;
+                if (r2) A[pk(p1, q2, n)] = s2 * b00 + c2 * b01;
+                // (q1, p2) is the same stored entry as (p1, q2) on the diagonal block
+                if (r1 && k1 != k2) A[pk(q1, p2, n)] = c2 * b10 - s2 * b11;
+                if (r1 && r2) A[pk(q1, q2, n)] = s2 * b10 + c2 * b11;
+            }
+            // Z^T rows p, q <- rotated; ZB items per thread per batch keep
+            // several global loads in flight.
+            constexpr int ZB = 8;
+            const int zitems = npairs * n;
+            for (int w0 = tid; w0 < zitems; w0 += NT * ZB) {
+                float vp[ZB], vq[ZB];
+                int64_t op[ZB], oq[ZB];
+                float cz[ZB], sz[ZB];
+#pragma unroll
+                for (int b = 0; b < ZB; ++b) {
+                    const int w = w0 + b * NT;
+                    op[b] = -1;
+                    if (w < zitems) {
+                        const int k = w / n, i = w - (w / n) * n;
+                        if (qq[k] < n) {
+                            op[b] = (int64_t)pp[k] * lp + i;
+                            oq[b] = (int64_t)qq[k] * lp + i;
+                            cz[b] = cs[k];
+                            sz[b] = sn[k];
+                            vp[b] = Zt[op[b]];
+                            vq[b] = Zt[oq[b]];
+                        }
+                    }
+                }
+#pragma unroll
+                for (int b = 0; b < ZB; ++b) {
+                    if (op[b] < 0) continue;
+                    Zt[op[b]] = cz[b] * vp[b] - sz[b] * vq[b];
+                    Zt[oq[b]] = sz[b] * vp[b] + cz[b] * vq[b];
+                }
+            }
+            __syncthreads();
+        }
+    }
+    for (int i = tid; i < n; i += NT) lam[i] = A[pk(i, i, n)];
+    __syncthreads();
+    const int top = min(a.rank, n);
+    for (int i = tid; i < n; i += NT) {
+        const float li = lam[i];
+        int r = 0;
+        for (int j = 0; j < n; ++j) r += (lam[j] > li) || (lam[j] == li && j < i);
+        rnk[i] = r;
+        const bool sel = r < top && li > 1.f;
+        fcoef[i] = sel ? (1.f / sqrtf(li) - 1.f) : 0.f;
+        if (r < top) a.ritz[(int64_t)z * a.ritz_stride + r] = li;
+    }
+    __syncthreads();
+    // K = sum_i f_i z_i z_i^T, with the rows of Z^T staged through the LDS that
+    // held A, CH rows at a time (K accumulated in place across chunks).
+    float* K = a.kmat + (int64_t)z * lp * lp;
+    const int CH = (n + 1) / 2;
+    for (int i0 = 0; i0 < n; i0 += CH) {
+        const int cnt = min(CH, n - i0);
+        for (int q = tid; q < cnt * n; q += NT) {
+            const int i = q / n, c = q - (q / n) * n;
+            A[q] = Zt[(int64_t)(i0 + i) * lp + c];
+        }
+        __syncthreads();
+        for (int q = tid; q < lp * lp; q += NT) {
+            const int c = q / lp, d = q - (q / lp) * lp;
+            float s = i0 == 0 ? 0.f : K[q];
+            if (c < n && d < n)
+                for (int i = 0; i < cnt; ++i) {
+                    const float f = fcoef[i0 + i];
+                    if (f != 0.f) s = fmaf(A[i * n + c] * f, A[i * n + d], s);
+                }
+            K[q] = s;
+        }
+        __syncthreads();
+    }
+    if (tid == 0) {
+        int cnt = 0;
+        for (int i = 0; i < n; ++i) cnt += (rnk[i] < top && lam[i] > 1.f);
+        a.nsel[z] = cnt;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_omega_f16(const OmegaArgs& a, int batch, hipStream_t s) {
@@ -487,6 +663,9 @@ hipError_t launch_eig_select(const EigArgs& a, int batch, hipStream_t s) {
     if (a.ell <= kEigLdsMax) {
         const size_t lds = (size_t)2 * a.ell * (a.ell + 1) * sizeof(float);
         hipLaunchKernelGGL((eig_select_kernel<true>), dim3(batch), dim3(kSmallThreads), lds, s, a);
+    } else if (a.ell <= kEigPackedMax) {
+        const size_t lds = (size_t)a.ell * (a.ell + 1) / 2 * sizeof(float);
+        hipLaunchKernelGGL(eig_select_packed_kernel, dim3(batch), dim3(kSmallThreads), lds, s, a);
     } else {
         hipLaunchKernelGGL((eig_select_kernel<false>), dim3(batch), dim3(kSmallThreads), 0, s, a);
     }
