@@ -90,6 +90,12 @@ extern "C" {
  * Ignored by NORMPRE_VARIANT_MUON. */
 #define NORMPRE_FLAG_TANGENT_NONE   4u
 #define NORMPRE_FLAG_TANGENT_STRICT 8u
+/* NormPre-L Exact (App. B): the leading interaction eigenpairs of the full
+ * Gamma = Psi Psi^T instead of a sketch.  Realized as Alg. 2 at full width,
+ * l = a (active rows) and no power iteration: the candidate subspace is then
+ * all of range(Psi), so the Rayleigh-Ritz pairs are the exact nonzero
+ * eigenpairs of Gamma.  Needs a <= 384 (else UNSUPPORTED); NormPre-L only. */
+#define NORMPRE_FLAG_L_EXACT       16u
 
 /*
  * Hyper-parameters of one step.  Defaults (normpre_default_hparams) follow
@@ -145,7 +151,8 @@ const char* normpre_last_error(const normpre_ctx* ctx);
  * norm_eps <= 0, unknown orientation or flags, both tangent flags),
  * UNSUPPORTED (a dimension above 1 << 20 or a matrix above 2^31 elements;
  * in the row-active orientation a row longer than 32768 elements; for
- * NormPre-L a sketch width l = min(active rows, r + o) above 384).
+ * NormPre-L a sketch width l = min(active rows, r + o) above 384, or with
+ * NORMPRE_FLAG_L_EXACT more than 384 active rows).
  */
 int normpre_validate(int variant, int num_mats, const int64_t* shapes,
                      const normpre_hparams* hp, char* msg, int msg_len);

@@ -53,8 +53,14 @@ int orientation_of(const normpre_hparams& hp) {
     return (int)(((hp.step % 2) + 2) % 2);
 }
 
+// l of Alg. 2; the exact variant spans all active rows.
 int sketch_width(const normpre_hparams& hp, int64_t active_rows) {
+    if (hp.flags & NORMPRE_FLAG_L_EXACT) return (int)std::min<int64_t>(active_rows, INT32_MAX);
     return (int)std::min<int64_t>(active_rows, (int64_t)hp.rank + hp.oversample);
+}
+
+int power_iterations(const normpre_hparams& hp) {
+    return (hp.flags & NORMPRE_FLAG_L_EXACT) ? 0 : hp.power_iters;
 }
 
 // Active orientation of the step; the Muon reference step has none (it
@@ -86,10 +92,12 @@ Fail validate(int variant, int num_mats, const int64_t* shapes, const normpre_hp
     if (hp->orientation < 0 || hp->orientation > 2)
         return {NORMPRE_ERR_INVALID_ARG, fmt("unknown orientation mode %d", hp->orientation)};
     if (hp->flags & ~(NORMPRE_FLAG_DEBUG | NORMPRE_FLAG_TIME_KERNELS | NORMPRE_FLAG_TANGENT_NONE |
-                      NORMPRE_FLAG_TANGENT_STRICT))
+                      NORMPRE_FLAG_TANGENT_STRICT | NORMPRE_FLAG_L_EXACT))
         return {NORMPRE_ERR_INVALID_ARG, fmt("unknown flags 0x%x", hp->flags)};
     if ((hp->flags & NORMPRE_FLAG_TANGENT_NONE) && (hp->flags & NORMPRE_FLAG_TANGENT_STRICT))
         return {NORMPRE_ERR_INVALID_ARG, "at most one tangent mode flag"};
+    if ((hp->flags & NORMPRE_FLAG_L_EXACT) && variant != NORMPRE_VARIANT_L)
+        return {NORMPRE_ERR_INVALID_ARG, "NORMPRE_FLAG_L_EXACT applies to NormPre-L only"};
     if (variant == NORMPRE_VARIANT_G || variant == NORMPRE_VARIANT_MUON) {
         if (hp->ns_iters < 1 || hp->ns_iters > 64)
             return {NORMPRE_ERR_INVALID_ARG, fmt("ns_iters %d outside 1..64", hp->ns_iters)};
@@ -116,7 +124,10 @@ Fail validate(int variant, int num_mats, const int64_t* shapes, const normpre_hp
         if (variant == NORMPRE_VARIANT_L) {
             const int64_t ell = sketch_width(*hp, k == 0 ? m : n);
             if (ell > kMaxEll)
-                return {NORMPRE_ERR_UNSUPPORTED, fmt("matrix %d: sketch width %lld exceeds %d", i, (long long)ell, kMaxEll)};
+                return {NORMPRE_ERR_UNSUPPORTED,
+                        fmt("matrix %d: %s %lld exceeds %d", i,
+                            (hp->flags & NORMPRE_FLAG_L_EXACT) ? "exact NormPre-L on active rows" : "sketch width",
+                            (long long)ell, kMaxEll)};
         }
     }
     return {NORMPRE_OK, ""};
@@ -892,7 +903,7 @@ int sketch_front(const StepCtx& sc, const Item& it, DebugMat* dbg) {
     // Z and Y are scaled by powers of two (lambda_max <= tr Gamma <= a bounds
     // each product), which only rescales the spanned subspace.
     const float sc_step = pow2_at_most_inv_sqrt(d.a);
-    const int p = hp.power_iters;
+    const int p = power_iterations(hp);
     rc = sketch_product(sc, d, w, count, w.omega, true, w.v32[0], p > 0 ? w.v16[0] : nullptr, 1.f);
     if (rc) return rc;
     for (int i = 0; i < p; ++i) {

@@ -80,7 +80,12 @@ def test_version(N):
     (0, [(8, 8)], {"weight_decay": float("inf")}, -1),
     (0, [(8, 8)], {"norm_eps": 0.0}, -1),
     (0, [(8, 8)], {"orientation": 3}, -1),
-    (0, [(8, 8)], {"flags": 16}, -1),
+    (0, [(8, 8)], {"flags": 32}, -1),
+    (1, [(100, 1000)], {"flags": 16}, 0),            # exact NormPre-L, a = 100
+    (1, [(400, 1000)], {"flags": 16}, -2),           # exact needs a <= 384
+    (1, [(400, 1000)], {"flags": 16, "step": 1}, -2),
+    (1, [(1000, 300)], {"flags": 16, "step": 1}, 0), # column-active: a = 300
+    (0, [(8, 8)], {"flags": 16}, -1),                # exact flag is NormPre-L only
     (0, [(8, 8)], {"flags": 4}, 0),                  # no tangent
     (1, [(8, 8)], {"flags": 8}, 0),                  # strict tangent
     (0, [(8, 8)], {"flags": 12}, -1),                # both tangent modes

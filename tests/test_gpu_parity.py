@@ -79,10 +79,10 @@ def run_step(ctx, variant, mats, t, lr=1.0, wd=0.0, debug=True, **hp_over):
     return out
 
 
-def oracle(mat, variant, t, lr=1.0, wd=0.0, matrix_id=0, **kw):
+def oracle(mat, variant, t, lr=1.0, wd=0.0, matrix_id=0, l_mode="sketch", **kw):
     w, g, mp = (x.numpy() for x in mat)
     hp = O.HParams(lr=lr, weight_decay=wd, **kw)
-    return O.normpre_step(w, g, mp, t, hp, variant, matrix_id=matrix_id)
+    return O.normpre_step(w, g, mp, t, hp, variant, matrix_id=matrix_id, l_mode=l_mode)
 
 
 # ----------------------------------------------------------------- Omega
@@ -300,3 +300,27 @@ def test_reference_steps_zero_signal(ctx, variant):
     z = torch.zeros(shape)
     res = run_step(ctx, variant, [(w, z, z)], 0, lr=0.5, wd=0.1)[0]
     np.testing.assert_allclose(res["w"].numpy(), (w * (1 - 0.5 * 0.1)).numpy(), rtol=1e-6, atol=1e-9)
+
+
+# ------------------------------------------------------ NormPre-L Exact
+@pytest.mark.parametrize("shape,t", [((256, 256), 0), ((256, 256), 1), ((300, 200), 0), ((100, 1000), 0),
+                                     ((1000, 300), 1), ((64, 64), 0)])
+def test_l_exact_matches_oracle(ctx, shape, t):
+    _say(f"L exact shape={shape} t={t}")
+    mat = _inputs(shape, "powerlaw", seed=7)
+    res = run_step(ctx, "L", [mat], t, flags=N.NORMPRE_FLAG_DEBUG | N.NORMPRE_FLAG_L_EXACT, rank=16)[0]
+    ref = oracle(mat, "L", t, rank=16, l_mode="exact")
+    a = shape[0] if t % 2 == 0 else shape[1]
+    assert int(N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_ELL, 1, np.int32)[0]) == a
+    lam_sel = ref["lam_sel"]
+    kappa = math.sqrt(float(np.sum(lam_sel))) / max(np.linalg.norm(ref["t"]), 1e-300)
+    tol = max(TOL_L, 8.0 * U16 * kappa)
+    err = O.relative_fro(res["u"], ref["update"])
+    _say(f"  update err {err:.2e} (tol {tol:.1e}), |C| = {len(lam_sel)}")
+    assert err < tol
+    # |C| against the exact spectrum (the lambda = 1 threshold is continuous,
+    # so modes within 1e-2 of it may fall either way)
+    psi_act = O.orient(ref["psi"], ref["k"])
+    ev = np.sort(np.linalg.eigvalsh(psi_act @ psi_act.T))[::-1][:16]
+    nsel = int(N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_NSEL, 1, np.int32)[0])
+    assert int(np.sum(ev > 1.01)) <= nsel <= int(np.sum(ev > 0.99))
