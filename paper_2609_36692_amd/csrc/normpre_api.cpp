@@ -590,10 +590,16 @@ int run_muon_input(const StepCtx& sc, const Dims& d, const GWork& w, const std::
     return NORMPRE_OK;
 }
 
+// 256 x 256 tiles (8 waves, 1 block per CU) once a launch has enough of them
+// to fill the chip about twice over (symmetric products count their
+// upper-triangle tiles); below that the 128 x 128 tile (2 blocks per CU)
+// keeps more CUs busy.  The combine switches a little earlier: measured on
+// 12-matrix launches, 432 large tiles ran faster than the small ones and 324
+// slower.
 TileCfg ns_cfg(int64_t M, int64_t N, bool sym, int count) {
     const int64_t tm = M / 256, tn = N / 256;
-    const int64_t tiles = sym ? tm * (tm + 1) / 2 : tm * tn;
-    return tiles * count >= 512 ? TileCfg::Big256 : TileCfg::Big;
+    const int64_t tiles = (sym ? tm * (tm + 1) / 2 : tm * tn) * count;
+    return tiles >= (sym ? 512 : 384) ? TileCfg::Big256 : TileCfg::Big;
 }
 
 int gram_launch(const StepCtx& sc, const Item& it, const Pool& pl, half_t* x, bool first_it) {

@@ -17,6 +17,8 @@
 // All sizes are multiples of the tile sizes (the workspace is zero padded).
 #include "np_internal.h"
 
+#include <type_traits>
+
 #include <hip/hip_ext.h>
 
 namespace np {
@@ -49,10 +51,18 @@ struct KMajorLoader {
     }
     static __device__ __forceinline__ void store(const u32x4 (&r)[N], half_t* lds, int tid) {
 #pragma unroll
-        for (int i = 0; i < N; ++i) {
-            const int row = (tid >> 3) + i * (NT / 8), ch = tid & 7;
-            *reinterpret_cast<u32x4*>(lds + lds_idx(row, ch)) = r[i];
-        }
+        for (int i = 0; i < N; ++i) store_item(r, lds, tid, i);
+    }
+    // Single items, so the stores and loads of one K-step can be spread over
+    // its MFMA sub-steps.
+    static __device__ __forceinline__ void load_item(u32x4 (&r)[N], const half_t* base, int64_t ld, int row0, int k0,
+                                                     int tid, int i) {
+        r[i] = *reinterpret_cast<const u32x4*>(base + (int64_t)(row0 + (tid >> 3) + i * (NT / 8)) * ld + k0 +
+                                               (tid & 7) * 8);
+    }
+    static __device__ __forceinline__ void store_item(const u32x4 (&r)[N], half_t* lds, int tid, int i) {
+        const int row = (tid >> 3) + i * (NT / 8), ch = tid & 7;
+        *reinterpret_cast<u32x4*>(lds + lds_idx(row, ch)) = r[i];
     }
 };
 
@@ -73,10 +83,16 @@ struct MNMajorLoader {
         for (int q = 0; q < KR; ++q) r[q] = *reinterpret_cast<const u32x4*>(p + q * ld);
     }
     static __device__ __forceinline__ void store(const u32x4 (&r)[N], half_t* lds, int tid) {
+        store_rows(r, lds, tid, 0, 8);
+    }
+    // LDS rows mm0 .. mm1-1 of this thread's 8 (each uses every staging
+    // register, so the next loads can only follow the last part).
+    static __device__ __forceinline__ void store_rows(const u32x4 (&r)[N], half_t* lds, int tid, int mm0, int mm1) {
         const int mblk = tid % MB, kblk = tid / MB;
         const int kofs = kblk * KR, chunk = kofs >> 3, within = kofs & 7;
 #pragma unroll
         for (int mm = 0; mm < 8; ++mm) {
+            if (mm < mm0 || mm >= mm1) continue;
             const int d = mm >> 1;
             uint32_t packed[KR / 2];
 #pragma unroll
@@ -99,6 +115,10 @@ struct MNMajorLoader {
 
 template <bool MN, int R, int NT>
 struct LoaderSel { using type = KMajorLoader<R, NT>; };
+template <class L>
+struct SplitOf { static constexpr bool value = false; };
+template <int R, int NT>
+struct SplitOf<KMajorLoader<R, NT>> { static constexpr bool value = true; };
 template <int R, int NT>
 struct LoaderSel<true, R, NT> { using type = MNMajorLoader<R, NT>; };
 
@@ -168,9 +188,8 @@ __device__ __forceinline__ void xcd_remap(int& bx, int& by, int& bz) {
 // At least two waves per SIMD: two 4-wave blocks (or one 8-wave block) per
 // CU, so one block's MFMAs overlap the other's LDS and barrier waits.
 // MF = 32: v_mfma_f32_32x32x16_f16 blocks (measured issue-bound ceiling on
-// gfx950 about 2.4 PFLOP/s); MF = 16: v_mfma_f32_16x16x32_f16 blocks (about
-// 1.45 PFLOP/s), kept for the 8-wave 256 x 256 tile, which is LDS-bound
-// either way and runs ~6% faster with the shorter instruction.
+// gfx950 about 2.4 PFLOP/s), used by every tile; MF = 16:
+// v_mfma_f32_16x16x32_f16 blocks (about 1.45 PFLOP/s), kept as an option.
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 template <int MF> struct AccSel { using type = f32x4; };
@@ -218,6 +237,92 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = AccT{};
 
+    // MFMAs over one LDS stage (16x16x32 blocks, BK / 32 sub-steps).
+    auto compute16 = [&](int stage) {
+      if constexpr (MF == 16) {
+        const half_t* ca = sbase + stage * (BM + BN) * BK;
+        const half_t* cb = ca + BM * BK;
+#pragma unroll
+        for (int s = 0; s < BK / 32; ++s) {
+            f16x8 af[FM], bf[FN];
+            const int chunk = s * 4 + (lane >> 4);
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+                af[i] = *reinterpret_cast<const f16x8*>(ca + lds_idx(wm * TM + i * 16 + (lane & 15), chunk));
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+                bf[j] = *reinterpret_cast<const f16x8*>(cb + lds_idx(wn * TN + j * 16 + (lane & 15), chunk));
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
+        }
+      }
+    };
+
+    // One K-step with 32x32x16 MFMAs (BK / 16 sub-steps).  With STORE the next
+    // stage's staging registers go to LDS and, with LOAD, the stage after
+    // that is fetched into them; K-major items are spread over the sub-steps
+    // (item i at sub-step i * NSUB / N) so the LDS stores and global loads
+    // are issued between MFMAs rather than after all of them.
+    constexpr int NSUB = BK / 16;
+    auto kstep32 = [&](auto store_tag, auto load_tag, int stage, int k_load) {
+        constexpr bool STORE = decltype(store_tag)::value, LOAD = decltype(load_tag)::value;
+      if constexpr (MF == 32) {
+        const half_t* ca = sbase + stage * (BM + BN) * BK;
+        const half_t* cb = ca + BM * BK;
+        half_t* sa = sbase + (stage ^ 1) * (BM + BN) * BK;
+        half_t* sb = sa + BM * BK;
+        f16x8 af[2][FM], bf[2][FN];
+        auto read_frags = [&](int s, int buf) {
+            const int chunk = s * 2 + (lane >> 5);
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+                af[buf][i] = *reinterpret_cast<const f16x8*>(ca + lds_idx(wm * TM + i * 32 + (lane & 31), chunk));
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+                bf[buf][j] = *reinterpret_cast<const f16x8*>(cb + lds_idx(wn * TN + j * 32 + (lane & 31), chunk));
+        };
+        read_frags(0, 0);
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s) {
+            if (s + 1 < NSUB) read_frags(s + 1, (s + 1) & 1);
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[s & 1][i], bf[s & 1][j], acc[i][j], 0, 0, 0);
+            if constexpr (STORE) {
+                if constexpr (SplitOf<LA>::value) {
+#pragma unroll
+                    for (int it = 0; it < LA::N; ++it)
+                        if (it * NSUB / LA::N == s) {
+                            LA::store_item(ra, sa, tid, it);
+                            if constexpr (LOAD) LA::load_item(ra, Ab, A.ld, m0, k_load, tid, it);
+                        }
+                } else {
+                    LA::store_rows(ra, sa, tid, s * 8 / NSUB, (s + 1) * 8 / NSUB);
+                    if constexpr (LOAD) if (s == NSUB - 1) LA::load(ra, Ab, A.ld, m0, k_load, tid);
+                }
+                if constexpr (SplitOf<LB>::value) {
+#pragma unroll
+                    for (int it = 0; it < LB::N; ++it)
+                        if (it * NSUB / LB::N == s) {
+                            LB::store_item(rb, sb, tid, it);
+                            if constexpr (LOAD) LB::load_item(rb, Bb, B.ld, n0, k_load, tid, it);
+                        }
+                } else {
+                    LB::store_rows(rb, sb, tid, s * 8 / NSUB, (s + 1) * 8 / NSUB);
+                    if constexpr (LOAD) if (s == NSUB - 1) LB::load(rb, Bb, B.ld, n0, k_load, tid);
+                }
+            }
+        }
+      }
+    };
+    using T_ = std::true_type;
+    using F_ = std::false_type;
+
     if (kbeg < kend) {
         LA::load(ra, Ab, A.ld, m0, kbeg, tid);
         LB::load(rb, Bb, B.ld, n0, kbeg, tid);
@@ -228,61 +333,36 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
             LB::load(rb, Bb, B.ld, n0, kbeg + BK, tid);
         }
         int stage = 0;
-        for (int k0 = kbeg; k0 < kend; k0 += BK, stage ^= 1) {
-            lds_barrier();
-            const half_t* ca = sbase + stage * (BM + BN) * BK;
-            const half_t* cb = ca + BM * BK;
-            if constexpr (MF == 16) {
-#pragma unroll
-                for (int s = 0; s < BK / 32; ++s) {
-                    f16x8 af[FM], bf[FN];
-                    const int chunk = s * 4 + (lane >> 4);
-#pragma unroll
-                    for (int i = 0; i < FM; ++i)
-                        af[i] = *reinterpret_cast<const f16x8*>(ca + lds_idx(wm * TM + i * 16 + (lane & 15), chunk));
-#pragma unroll
-                    for (int j = 0; j < FN; ++j)
-                        bf[j] = *reinterpret_cast<const f16x8*>(cb + lds_idx(wn * TN + j * 16 + (lane & 15), chunk));
-#pragma unroll
-                    for (int i = 0; i < FM; ++i)
-#pragma unroll
-                        for (int j = 0; j < FN; ++j)
-                            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
-                }
-            } else {
-                // Fragments of sub-step s + 1 are read while the MFMAs of
-                // sub-step s run; the scheduling barriers keep the compiler
-                // from hoisting every sub-step's reads (which would not fit
-                // beside 256 accumulator registers).
-                f16x8 af[2][FM], bf[2][FN];
-                auto read_frags = [&](int s, int buf) {
-                    const int chunk = s * 2 + (lane >> 5);
-#pragma unroll
-                    for (int i = 0; i < FM; ++i)
-                        af[buf][i] = *reinterpret_cast<const f16x8*>(ca + lds_idx(wm * TM + i * 32 + (lane & 31), chunk));
-#pragma unroll
-                    for (int j = 0; j < FN; ++j)
-                        bf[buf][j] = *reinterpret_cast<const f16x8*>(cb + lds_idx(wn * TN + j * 32 + (lane & 31), chunk));
-                };
-                read_frags(0, 0);
-#pragma unroll
-                for (int s = 0; s < BK / 16; ++s) {
-                    if (s + 1 < BK / 16) read_frags(s + 1, (s + 1) & 1);
-                    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                    for (int i = 0; i < FM; ++i)
-#pragma unroll
-                        for (int j = 0; j < FN; ++j)
-                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[s & 1][i], bf[s & 1][j], acc[i][j], 0, 0, 0);
-                    __builtin_amdgcn_sched_barrier(0);
-                }
+        if constexpr (MF == 32 && LAYOUT == 0) {
+            // Both operands K-major: branch-free steady state with the stores
+            // and loads spread over the MFMA sub-steps, the last two K-steps
+            // peeled.  (With a register-transposed MN-major operand the plain
+            // loop below measured faster.)
+            int k0 = kbeg;
+            for (; k0 + 2 * BK < kend; k0 += BK, stage ^= 1) {
+                lds_barrier();
+                kstep32(T_{}, T_{}, stage, k0 + 2 * BK);
             }
             if (k0 + BK < kend) {
-                LA::store(ra, sbase + (stage ^ 1) * (BM + BN) * BK, tid);
-                LB::store(rb, sbase + (stage ^ 1) * (BM + BN) * BK + BM * BK, tid);
-                if (k0 + 2 * BK < kend) {
-                    LA::load(ra, Ab, A.ld, m0, k0 + 2 * BK, tid);
-                    LB::load(rb, Bb, B.ld, n0, k0 + 2 * BK, tid);
+                lds_barrier();
+                kstep32(T_{}, F_{}, stage, 0);
+                k0 += BK;
+                stage ^= 1;
+            }
+            lds_barrier();
+            kstep32(F_{}, F_{}, stage, 0);
+        } else {
+            for (int k0 = kbeg; k0 < kend; k0 += BK, stage ^= 1) {
+                lds_barrier();
+                if constexpr (MF == 16) compute16(stage);
+                else kstep32(F_{}, F_{}, stage, 0);
+                if (k0 + BK < kend) {
+                    LA::store(ra, sbase + (stage ^ 1) * (BM + BN) * BK, tid);
+                    LB::store(rb, sbase + (stage ^ 1) * (BM + BN) * BK + BM * BK, tid);
+                    if (k0 + 2 * BK < kend) {
+                        LA::load(ra, Ab, A.ld, m0, k0 + 2 * BK, tid);
+                        LB::load(rb, Bb, B.ld, n0, k0 + 2 * BK, tid);
+                    }
                 }
             }
         }
@@ -582,9 +662,9 @@ hipError_t launch_gemm_affine(TileCfg cfg, int layout, Operand A, Operand B, Gem
         }
     } else if (cfg == TileCfg::Big256) {
         switch (layout) {
-            case 0: return run<256, 256, 2, 4, 0, EAff, 16>(A, B, sh, batch, ee, s);
-            case 1: return run<256, 256, 2, 4, 1, EAff, 16>(A, B, sh, batch, ee, s);
-            case 2: return run<256, 256, 2, 4, 2, EAff, 16>(A, B, sh, batch, ee, s);
+            case 0: return run<256, 256, 2, 4, 0, EAff, 32>(A, B, sh, batch, ee, s);
+            case 1: return run<256, 256, 2, 4, 1, EAff, 32>(A, B, sh, batch, ee, s);
+            case 2: return run<256, 256, 2, 4, 2, EAff, 32>(A, B, sh, batch, ee, s);
         }
     }
     return hipErrorInvalidValue;
