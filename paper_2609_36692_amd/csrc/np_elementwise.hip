@@ -131,6 +131,92 @@ __global__ void __launch_bounds__(NT) normalize_rows_kernel(NormArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Row-active orientation, rows of at most 64 * VW * NV elements: one wave per
+// row, four rows per block; the row stays in registers and the statistics are
+// reduced with wave shuffles only (no LDS, no block barrier).
+template <int VW, int NV, bool DBG>
+__global__ void __launch_bounds__(256) normalize_rows_wave_kernel(NormArgs a) {
+    const int z = blockIdx.y, lane = threadIdx.x & 63;
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= a.rows_pad) return;
+    half_t* prow = a.psi + (int64_t)z * a.stride_psi + (int64_t)row * a.ld_psi;
+    if (row >= a.rows) {
+        for (int64_t j = lane * 4; j < a.ld_psi; j += 256)
+            *reinterpret_cast<uint2*>(prow + j) = make_uint2(0u, 0u);
+        return;
+    }
+    const int64_t off = (int64_t)row * a.cols;
+    float* W = a.ptrs.w[z] + off;
+    float* M = a.ptrs.m[z] + off;
+    const float* G = a.ptrs.g[z] + off;
+    float mv[NV][VW], wv[NV][VW];
+    double smm = 0.0, smw = 0.0, sww = 0.0;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+        const int idx = (v * 64 + lane) * VW;
+        if (idx < a.cols) {
+            if constexpr (VW == 4) {
+                const float4 mp = *reinterpret_cast<const float4*>(M + idx);
+                const float4 g = *reinterpret_cast<const float4*>(G + idx);
+                const float4 w = *reinterpret_cast<const float4*>(W + idx);
+                float4 m;
+                m.x = fmaf(a.mu, mp.x, g.x); m.y = fmaf(a.mu, mp.y, g.y);
+                m.z = fmaf(a.mu, mp.z, g.z); m.w = fmaf(a.mu, mp.w, g.w);
+                *reinterpret_cast<float4*>(M + idx) = m;
+                mv[v][0] = m.x; mv[v][1] = m.y; mv[v][2] = m.z; mv[v][3] = m.w;
+                wv[v][0] = w.x; wv[v][1] = w.y; wv[v][2] = w.z; wv[v][3] = w.w;
+            } else {
+                const float m = fmaf(a.mu, M[idx], G[idx]);
+                M[idx] = m;
+                mv[v][0] = m;
+                wv[v][0] = W[idx];
+            }
+#pragma unroll
+            for (int e = 0; e < VW; ++e) {
+                const double md = mv[v][e], wd = wv[v][e];
+                smm = fma(md, md, smm);
+                smw = fma(md, wd, smw);
+                sww = fma(wd, wd, sww);
+            }
+        }
+    }
+    smm = wave_sum_d(smm);
+    smw = wave_sum_d(smw);
+    sww = wave_sum_d(sww);
+    const double d = tangent_coef(a.tangent, smw, sww);
+    const double nrm2 = fmax(smm - 2.0 * d * smw + d * d * sww, 0.0);
+    const float inv = (float)(1.0 / fmax(sqrt(nrm2), (double)a.eps));
+    const float df = (float)d;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+        const int idx = (v * 64 + lane) * VW;
+        if (idx < a.cols) {
+            float p[VW];
+#pragma unroll
+            for (int e = 0; e < VW; ++e) p[e] = (mv[v][e] - df * wv[v][e]) * inv;
+            if constexpr (VW == 4) {
+                half_t h[4] = {(half_t)p[0], (half_t)p[1], (half_t)p[2], (half_t)p[3]};
+                *reinterpret_cast<uint2*>(prow + idx) = *reinterpret_cast<const uint2*>(h);
+                if constexpr (DBG)
+                    *reinterpret_cast<float4*>(a.psi32 + (int64_t)z * a.stride_psi32 + off + idx) =
+                        make_float4(p[0], p[1], p[2], p[3]);
+            } else {
+                prow[idx] = (half_t)p[0];
+                if constexpr (DBG) a.psi32[(int64_t)z * a.stride_psi32 + off + idx] = p[0];
+            }
+        }
+    }
+    // zero padding of the row (ld_psi is a multiple of 256)
+    if constexpr (VW == 4) {
+        for (int64_t j = a.cols + lane * 4; j < a.ld_psi; j += 256)
+            *reinterpret_cast<uint2*>(prow + j) = make_uint2(0u, 0u);
+    } else {
+        for (int64_t j = a.cols + lane; j < a.ld_psi; j += 64) prow[j] = (half_t)0.f;
+    }
+    if (lane == 0) a.psisq[(int64_t)z * a.stride_psisq + row] = (float)(nrm2 * (double)inv * (double)inv);
+}
+
+// ---------------------------------------------------------------------------
 // Column-active orientation.  Block = (64 * VW) columns x 4 row lanes over a
 // chunk of rows; each thread owns VW adjacent columns (one 16-byte access per
 // row when VW = 4).  Pass 1 updates M and writes fp64 partial column sums;
@@ -436,9 +522,26 @@ hipError_t rows_pick_nv(const NormArgs& a, int batch, hipStream_t s, bool dbg) {
 
 }  // namespace
 
+template <int VW, int NV>
+hipError_t rows_wave_launch(const NormArgs& a, int batch, hipStream_t s, bool dbg) {
+    dim3 grid((unsigned)((a.rows_pad + 3) / 4), batch);
+    if (dbg) hipLaunchKernelGGL((normalize_rows_wave_kernel<VW, NV, true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((normalize_rows_wave_kernel<VW, NV, false>), grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
 hipError_t launch_normalize_rows(const NormArgs& a, int batch, hipStream_t s) {
     const bool dbg = a.psi32 != nullptr;
     const bool vec = a.vec_ok && (a.cols % 4) == 0;
+    // Rows up to 4096 elements (vectorized) or 1024 (scalar): a wave per row.
+    if (vec && a.cols <= 64 * 4 * 16) {
+        const int nv = (a.cols + 255) / 256;
+        if (nv <= 4) return rows_wave_launch<4, 4>(a, batch, s, dbg);
+        if (nv <= 8) return rows_wave_launch<4, 8>(a, batch, s, dbg);
+        if (nv <= 12) return rows_wave_launch<4, 12>(a, batch, s, dbg);
+        return rows_wave_launch<4, 16>(a, batch, s, dbg);
+    }
+    if (!vec && a.cols <= 64 * 16) return rows_wave_launch<1, 16>(a, batch, s, dbg);
     if (vec) {
         if (a.cols <= 256 * 4 * 8) return rows_pick_nv<256, 4>(a, batch, s, dbg);
         if (a.cols <= 1024 * 4 * 8) return rows_pick_nv<1024, 4>(a, batch, s, dbg);
