@@ -602,23 +602,62 @@ TileCfg ns_cfg(int64_t M, int64_t N, bool sym, int count) {
     return tiles >= (sym ? 512 : 384) ? TileCfg::Big256 : TileCfg::Big;
 }
 
-int gram_launch(const StepCtx& sc, const Item& it, const Pool& pl, half_t* x, bool first_it) {
-    const Dims& d = it.d;
-    const int count = it.count;
-    const int64_t mn = d.mp * d.np_, ss = d.sp * d.sp;
-    const double s_ = (double)std::min(d.m, d.n), l_ = (double)std::max(d.m, d.n);
-    // A = X X^T (wide) or Y^T Y (tall), times c^2 on the first iteration.
-    Operand A{x, d.np_, mn}, B{x, d.np_, mn};
-    GemmShape sh{(int)d.sp, (int)d.sp, (int)d.lp_, 1, (int)d.lp_, 1};
+// The Grams of every item of one pool with the same operand layout, in one
+// launch: small same-s batches (e.g. the three wide shapes of a transformer
+// block) fill the chip together where each alone would not.
+int gram_pool_launch(const StepCtx& sc, std::vector<const Item*> its, const Pool& pl, int iter, bool first_it) {
+    const int64_t ss = pl.sp * pl.sp;
+    // Longest K first: the costly matrices start in the first wave of blocks
+    // and the cheap ones fill the tail.
+    std::stable_sort(its.begin(), its.end(), [](const Item* a, const Item* b) { return a->d.lp_ > b->d.lp_; });
+    const int layout = its[0]->d.tall ? 2 : 0;
+    GramGroups gg{};
+    double flops = 0.0, bytes = 0.0;
+    int total = 0;
+    for (const Item* it : its) {
+        const Dims& d = it->d;
+        const int g = gg.n++;
+        gg.zbeg[g] = total;
+        gg.x[g] = (iter & 1) ? it->w.xb : it->w.psi;
+        gg.ld[g] = d.np_;
+        gg.stride[g] = d.mp * d.np_;
+        gg.K[g] = (int)d.lp_;
+        gg.mul[g] = first_it ? it->w.scale : nullptr;
+        gg.zout[g] = it->pool_off;
+        total += it->count;
+        const double s_ = (double)std::min(d.m, d.n), l_ = (double)std::max(d.m, d.n);
+        flops += 2.0 * s_ * s_ * l_ * it->count;
+        bytes += 2.0 * (s_ * l_ + s_ * s_) * it->count;
+    }
+    gg.zbeg[gg.n] = total;
     EpiAffine e{};
-    e.out = pl.amat + (int64_t)it.pool_off * ss; e.ld_out = d.sp; e.stride_out = ss;
-    e.mul = first_it ? it.w.scale : nullptr; e.mul_pow = first_it ? 2 : 0;
+    e.out = pl.amat; e.ld_out = pl.sp; e.stride_out = ss;
+    e.mul_pow = first_it ? 2 : 0;
     e.ca = 1.f; e.cs = 0.f;
-    const int layout = d.tall ? 2 : 0;
-    const TileCfg cfg = ns_cfg(d.sp, d.sp, true, count);
-    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_GRAM, 2.0 * s_ * s_ * l_ * count, 2.0 * (s_ * l_ + s_ * s_) * count,
-                 [&] { return launch_gemm_affine(cfg, layout, A, B, sh, count, e, sc.s); }),
+    const TileCfg cfg = ns_cfg(pl.sp, pl.sp, true, total);
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_GRAM, flops, bytes,
+                 [&] { return launch_gemm_gram_grouped(cfg, layout, gg, (int)pl.sp, e, sc.s); }),
            "ns gram");
+    return NORMPRE_OK;
+}
+
+int gram_launches(const StepCtx& sc, const std::vector<Item>& items, const std::vector<Pool>& pools, int iter,
+                  bool first_it) {
+    for (size_t pi = 0; pi < pools.size(); ++pi) {
+        for (int tall = 0; tall < 2; ++tall) {
+            std::vector<const Item*> its;
+            for (const Item& it : items)
+                if (it.pool == (int)pi && (int)it.d.tall == tall) {
+                    its.push_back(&it);
+                    if ((int)its.size() == kMaxGramGroups) {
+                        if (int rc = gram_pool_launch(sc, its, pools[pi], iter, first_it)) return rc;
+                        its.clear();
+                    }
+                }
+            if (!its.empty())
+                if (int rc = gram_pool_launch(sc, its, pools[pi], iter, first_it)) return rc;
+        }
+    }
     return NORMPRE_OK;
 }
 
@@ -755,11 +794,8 @@ int run_round_g(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& 
     const int q = sc.variant == NORMPRE_VARIANT_NORMALIZE_ONLY ? 0 : sc.hp->ns_iters;
     for (int iter = 0; iter < q; ++iter) {
         const bool first_it = iter == 0 && fold_scale, last_it = iter == q - 1;
-        for (const Item& it : items) {
-            half_t* x = (iter & 1) ? it.w.xb : it.w.psi;
-            int rc = gram_launch(sc, it, pools[it.pool], x, first_it);
-            if (rc) return rc;
-        }
+        int rc = gram_launches(sc, items, pools, iter, first_it);
+        if (rc) return rc;
         for (size_t pi = 0; pi < pools.size(); ++pi) {
             double flops = 0.0;
             for (const Item& it : items)

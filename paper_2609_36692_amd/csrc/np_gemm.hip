@@ -18,6 +18,7 @@
 #include "np_internal.h"
 
 #include <type_traits>
+#include <utility>
 
 #include <hip/hip_ext.h>
 
@@ -170,6 +171,7 @@ __device__ __forceinline__ int epi_tiles(const E& e) {
 // Maps the hardware block order (dispatched round-robin over the 8 XCDs) to
 // a logical order in which each XCD owns one contiguous range of tiles, so
 // neighbouring tiles of a matrix share that XCD's L2.
+template <bool STRIPED>
 __device__ __forceinline__ void xcd_remap(int& bx, int& by, int& bz) {
     const int gx = gridDim.x, gy = gridDim.y, gz = gridDim.z;
     const int total = gx * gy * gz;
@@ -177,8 +179,20 @@ __device__ __forceinline__ void xcd_remap(int& bx, int& by, int& bz) {
     // Workgroup w runs on XCD w % 8.  The first 8 * floor(total / 8) ids are
     // regrouped so each XCD takes one contiguous run of tiles (sharing
     // operands in its own L2); the ragged tail keeps its order.
-    const int per = total >> 3;
-    if (lin < (per << 3)) lin = (lin & 7) * per + (lin >> 3);
+    // STRIPED (launches whose matrices differ in cost): each XCD takes whole
+    // matrices in turn instead (matrix j of every eight on XCD j % 8), so
+    // every XCD gets the same mix of cheap and costly matrices in launch
+    // order; the ragged last round keeps its order.
+    if constexpr (STRIPED) {
+        const int st = gx * gy, full = (gz >> 3) * (st << 3);
+        if (lin < full) {
+            const int x = lin & 7, j = lin >> 3;
+            lin = (j / st) * (st << 3) + x * st + j % st;
+        }
+    } else {
+        const int per = total >> 3;
+        if (lin < (per << 3)) lin = (lin & 7) * per + (lin >> 3);
+    }
     bx = lin % gx;
     lin /= gx;
     by = lin % gy;
@@ -191,6 +205,12 @@ __device__ __forceinline__ void xcd_remap(int& bx, int& by, int& bz) {
 // gfx950 about 2.4 PFLOP/s), used by every tile; MF = 16:
 // v_mfma_f32_16x16x32_f16 blocks (about 1.45 PFLOP/s), kept as an option.
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// Epilogues that carry a GramGroups table (grouped Gram launches).
+template <class E, class = void>
+struct IsGrouped { static constexpr bool value = false; };
+template <class E>
+struct IsGrouped<E, std::void_t<decltype(std::declval<E>().gg)>> { static constexpr bool value = true; };
 
 template <int MF> struct AccSel { using type = f32x4; };
 template <> struct AccSel<32> { using type = f32x16; };
@@ -216,16 +236,32 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave - (wave / WN) * WN;
     int bx = blockIdx.x, split = blockIdx.y, z = blockIdx.z;
-    xcd_remap(bx, split, z);
+    xcd_remap<IsGrouped<Epi>::value>(bx, split, z);
     const int tiles_n = sh.N / BN;
     int tm, tn;
     decode_tile(bx, tiles_n, sh.sym, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
     const int kbeg = split * sh.k_chunk;
-    const int kend = min(sh.K, kbeg + sh.k_chunk);
+    int kend = min(sh.K, kbeg + sh.k_chunk);
 
     const half_t* Ab = A.ptr + (int64_t)z * A.batch_stride;
     const half_t* Bb = B.ptr + (int64_t)z * B.batch_stride;
+    int64_t lda = A.ld, ldb = B.ld;
+    int zo = z;                      // output matrix index
+    const float* mulz = nullptr;     // this matrix's scale pair, or null
+    if constexpr (IsGrouped<Epi>::value) {
+        int g = 0;
+        while (g + 1 < epi.gg.n && z >= epi.gg.zbeg[g + 1]) ++g;
+        const int lz = z - epi.gg.zbeg[g];
+        Ab = epi.gg.x[g] + (int64_t)lz * epi.gg.stride[g];
+        Bb = Ab;
+        lda = ldb = epi.gg.ld[g];
+        kend = epi.gg.K[g];
+        zo = epi.gg.zout[g] + lz;
+        mulz = epi.gg.mul[g] ? epi.gg.mul[g] + 2 * lz : nullptr;
+    } else if constexpr (Epi::kind == EpiKind::Affine) {
+        mulz = epi.mul ? epi.mul + 2 * z : nullptr;
+    }
     using LA = typename LoaderSel<(LAYOUT == 2), BM, NT>::type;
     using LB = typename LoaderSel<(LAYOUT >= 1), BN, NT>::type;
     u32x4 ra[LA::N], rb[LB::N];
@@ -299,22 +335,22 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                     for (int it = 0; it < LA::N; ++it)
                         if (it * NSUB / LA::N == s) {
                             LA::store_item(ra, sa, tid, it);
-                            if constexpr (LOAD) LA::load_item(ra, Ab, A.ld, m0, k_load, tid, it);
+                            if constexpr (LOAD) LA::load_item(ra, Ab, lda, m0, k_load, tid, it);
                         }
                 } else {
                     LA::store_rows(ra, sa, tid, s * 8 / NSUB, (s + 1) * 8 / NSUB);
-                    if constexpr (LOAD) if (s == NSUB - 1) LA::load(ra, Ab, A.ld, m0, k_load, tid);
+                    if constexpr (LOAD) if (s == NSUB - 1) LA::load(ra, Ab, lda, m0, k_load, tid);
                 }
                 if constexpr (SplitOf<LB>::value) {
 #pragma unroll
                     for (int it = 0; it < LB::N; ++it)
                         if (it * NSUB / LB::N == s) {
                             LB::store_item(rb, sb, tid, it);
-                            if constexpr (LOAD) LB::load_item(rb, Bb, B.ld, n0, k_load, tid, it);
+                            if constexpr (LOAD) LB::load_item(rb, Bb, ldb, n0, k_load, tid, it);
                         }
                 } else {
                     LB::store_rows(rb, sb, tid, s * 8 / NSUB, (s + 1) * 8 / NSUB);
-                    if constexpr (LOAD) if (s == NSUB - 1) LB::load(rb, Bb, B.ld, n0, k_load, tid);
+                    if constexpr (LOAD) if (s == NSUB - 1) LB::load(rb, Bb, ldb, n0, k_load, tid);
                 }
             }
         }
@@ -324,13 +360,13 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     using F_ = std::false_type;
 
     if (kbeg < kend) {
-        LA::load(ra, Ab, A.ld, m0, kbeg, tid);
-        LB::load(rb, Bb, B.ld, n0, kbeg, tid);
+        LA::load(ra, Ab, lda, m0, kbeg, tid);
+        LB::load(rb, Bb, ldb, n0, kbeg, tid);
         LA::store(ra, sbase, tid);
         LB::store(rb, sbase + BM * BK, tid);
         if (kbeg + BK < kend) {
-            LA::load(ra, Ab, A.ld, m0, kbeg + BK, tid);
-            LB::load(rb, Bb, B.ld, n0, kbeg + BK, tid);
+            LA::load(ra, Ab, lda, m0, kbeg + BK, tid);
+            LB::load(rb, Bb, ldb, n0, kbeg + BK, tid);
         }
         int stage = 0;
         if constexpr (MF == 32 && LAYOUT == 0) {
@@ -360,8 +396,8 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                     LA::store(ra, sbase + (stage ^ 1) * (BM + BN) * BK, tid);
                     LB::store(rb, sbase + (stage ^ 1) * (BM + BN) * BK + BM * BK, tid);
                     if (k0 + 2 * BK < kend) {
-                        LA::load(ra, Ab, A.ld, m0, k0 + 2 * BK, tid);
-                        LB::load(rb, Bb, B.ld, n0, k0 + 2 * BK, tid);
+                        LA::load(ra, Ab, lda, m0, k0 + 2 * BK, tid);
+                        LB::load(rb, Bb, ldb, n0, k0 + 2 * BK, tid);
                     }
                 }
             }
@@ -403,14 +439,14 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
         float* w = nullptr;
         if constexpr (Epi::kind == EpiKind::Affine) {
             float mul = 1.f;
-            if (epi.mul && epi.mul_pow > 0) {
-                const float f = epi.mul[2 * z];
+            if (mulz && epi.mul_pow > 0) {
+                const float f = mulz[0];
                 mul = epi.mul_pow == 1 ? f : f * f;
             }
             ca = epi.ca * mul;
             cs = epi.cs * mul;
-            out = epi.out + (int64_t)z * epi.stride_out;
-            src = epi.src ? epi.src + (int64_t)z * epi.stride_src : nullptr;
+            out = epi.out + (int64_t)zo * epi.stride_out;
+            src = epi.src ? epi.src + (int64_t)zo * epi.stride_src : nullptr;
             if (sh.sym && tm != tn) {
                 // Transposed copy of an off-diagonal tile of a symmetric result,
                 // written from registers (4 consecutive halves per lane).
@@ -570,13 +606,17 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
             if (tid == 0) {
                 float t = 0.f;
                 for (int q = 0; q < NT / 64; ++q) t += red[q];
-                epi_sumsq_ptr(epi)[(int64_t)z * epi_tiles(epi) + bx] = t;
+                epi_sumsq_ptr(epi)[(int64_t)zo * epi_tiles(epi) + bx] = t;
             }
         }
     }
 }
 
 struct EAff : EpiAffine { static constexpr EpiKind kind = EpiKind::Affine; };
+struct EAffG : EpiAffine {
+    static constexpr EpiKind kind = EpiKind::Affine;
+    GramGroups gg;
+};
 struct EPar : EpiPartial { static constexpr EpiKind kind = EpiKind::Partial; };
 struct EApp : EpiApplyUpdate { static constexpr EpiKind kind = EpiKind::Apply; };
 struct EAppN : EpiApplyNorm { static constexpr EpiKind kind = EpiKind::ApplyNorm; };
@@ -666,6 +706,32 @@ hipError_t launch_gemm_affine(TileCfg cfg, int layout, Operand A, Operand B, Gem
             case 1: return run<256, 256, 2, 4, 1, EAff, 32>(A, B, sh, batch, ee, s);
             case 2: return run<256, 256, 2, 4, 2, EAff, 32>(A, B, sh, batch, ee, s);
         }
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemm_gram_grouped(TileCfg cfg, int layout, const GramGroups& g, int sp, const EpiAffine& e,
+                                    hipStream_t s) {
+    if (g.n < 1 || g.n > kMaxGramGroups || (layout != 0 && layout != 2)) return hipErrorInvalidValue;
+    int kmax = 0;
+    for (int i = 0; i < g.n; ++i) {
+        if (g.K[i] < BK || g.K[i] % BK || g.zbeg[i + 1] <= g.zbeg[i]) return hipErrorInvalidValue;
+        kmax = std::max(kmax, g.K[i]);
+    }
+    EAffG ee;
+    static_cast<EpiAffine&>(ee) = e;
+    ee.mul = nullptr;
+    ee.gg = g;
+    Operand dummy{g.x[0], g.ld[0], 0};
+    GemmShape sh{sp, sp, kmax, 1, kmax, 1};
+    const int batch = g.zbeg[g.n] - g.zbeg[0];
+    if (g.zbeg[0] != 0) return hipErrorInvalidValue;
+    if (layout == 0) {
+        if (cfg == TileCfg::Big) return run<128, 128, 2, 2, 0, EAffG>(dummy, dummy, sh, batch, ee, s);
+        if (cfg == TileCfg::Big256) return run<256, 256, 2, 4, 0, EAffG>(dummy, dummy, sh, batch, ee, s);
+    } else {
+        if (cfg == TileCfg::Big) return run<128, 128, 2, 2, 2, EAffG>(dummy, dummy, sh, batch, ee, s);
+        if (cfg == TileCfg::Big256) return run<256, 256, 2, 4, 2, EAffG>(dummy, dummy, sh, batch, ee, s);
     }
     return hipErrorInvalidValue;
 }

@@ -98,6 +98,25 @@ hipError_t launch_gemm_apply(Operand A, Operand B, GemmShape sh, int batch,
                              const EpiApplyUpdate& e, hipStream_t s);
 hipError_t launch_gemm_apply_norm(Operand A, Operand B, GemmShape sh, int batch,
                                   const EpiApplyNorm& e, hipStream_t s);
+// Grouped symmetric Gram (X X^T with layout 0, Y^T Y with layout 2): shape
+// groups of one s (same padded s x s output) in one launch.  Group g covers
+// launch matrices [zbeg[g], zbeg[g + 1]) with its own operand (ld,
+// per-matrix stride), K and
+// first-iteration scale (mul[2 i], squared; null = 1); its matrices land at
+// output indices zout[g] + i.
+constexpr int kMaxGramGroups = 6;
+struct GramGroups {
+    int n;
+    int zbeg[kMaxGramGroups + 1];
+    const half_t* x[kMaxGramGroups];
+    int64_t ld[kMaxGramGroups];
+    int64_t stride[kMaxGramGroups];
+    int K[kMaxGramGroups];
+    const float* mul[kMaxGramGroups];
+    int zout[kMaxGramGroups];
+};
+hipError_t launch_gemm_gram_grouped(TileCfg cfg, int layout, const GramGroups& g, int sp, const EpiAffine& e,
+                                    hipStream_t s);
 int gemm_tile_m(TileCfg cfg);
 // Kernel timing hand-off (instrumented steps only): while a start/stop event
 // pair is armed on this thread, the next GEMM launch records it at its own
