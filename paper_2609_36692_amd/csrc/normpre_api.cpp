@@ -27,7 +27,6 @@ constexpr int64_t kMaxElems = int64_t(1) << 31;
 constexpr int kMaxRowLen = 32768;   // row-active register kernel limit
 constexpr int kMaxEll = 384;
 constexpr int kColRowChunk = 128;   // rows per block in the column-active pass
-constexpr int kGramChunks = 16;     // fixed chunk slots of the fp64 Gram (unused slots hold zeros)
 constexpr int kMaxSplits = 16;
 constexpr int kEigSweeps = 30;
 constexpr size_t kGroupBudget = size_t(24) << 30;  // workspace bytes per item
@@ -861,25 +860,79 @@ int sketch_product(const StepCtx& sc, const Dims& d, const GWork& w, int count, 
 
 // fp64 Gram of an item's l-major fp32 matrix V (ell_pad x len) into its slots
 // of the pool's partials (always kGramChunks chunk slots per matrix).
-int gram64_launch(const StepCtx& sc, const Item& it, const Pool& pl, const float* v, int64_t len) {
-    const int64_t lp = it.d.ellp, maxpad = it.d.lp_;
-    double* out = pl.gpart + (int64_t)it.pool_off * kGramChunks * lp * lp;
-    const int chunk_len = gram_chunk_len(len);
-    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
-                 [&] {
-                     return launch_gram64(v, len, lp * maxpad, (int)lp, len, chunk_len, kGramChunks, out, it.count,
-                                          sc.s);
-                 }),
+// The items of each pool in pool order, in runs of at most kMaxItems (one
+// grouped launch each); their matrices are contiguous in the pool buffers.
+std::vector<std::vector<const Item*>> pool_runs(const std::vector<Item>& items, const std::vector<Pool>& pools) {
+    std::vector<std::vector<const Item*>> runs;
+    for (size_t pi = 0; pi < pools.size(); ++pi) {
+        std::vector<const Item*> run;
+        for (const Item& it : items) {
+            if (it.pool != (int)pi) continue;
+            run.push_back(&it);
+            if ((int)run.size() == kMaxItems) {
+                runs.push_back(run);
+                run.clear();
+            }
+        }
+        if (!run.empty()) runs.push_back(run);
+    }
+    return runs;
+}
+
+// fp64 Gram partials of one l-major fp32 matrix per item (chosen by `pick`,
+// which returns the item's V and its length) for a run of one pool.
+template <class Pick>
+int gram64_run(const StepCtx& sc, const std::vector<const Item*>& run, const Pool& pl, Pick pick) {
+    const int64_t lp = pl.ellp, off0 = run[0]->pool_off;
+    Gram64Items t{};
+    for (const Item* it : run) {
+        const int g = t.n++;
+        int64_t len = 0;
+        t.v[g] = pick(*it, len);
+        t.zbeg[g] = it->pool_off - (int)off0;
+        t.ld[g] = len;
+        t.stride[g] = lp * it->d.lp_;
+        t.len[g] = len;
+        t.chunk_len[g] = gram_chunk_len(len);
+        t.zbeg[g + 1] = t.zbeg[g] + it->count;
+    }
+    double* out = pl.gpart + off0 * kGramChunks * lp * lp;
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_gram64(t, (int)lp, out, sc.s); }),
            "gram64");
     return NORMPRE_OK;
 }
 
-// One Cholesky-QR pass over every item of the round: Gram, Cholesky and
-// inverse (one launch per pool), then Q = Y R^-1 per item.
+// out = M^T V per item for a run of one pool (M from the pool's l x l
+// buffer `mats`); `fill` sets the item's V and outputs.
+template <class Fill>
+int small_mul_run(const StepCtx& sc, const std::vector<const Item*>& run, const Pool& pl, const float* mats,
+                  Fill fill, const char* what) {
+    const int64_t lp = pl.ellp, off0 = run[0]->pool_off;
+    SmallMulArgs a{};
+    a.ell = pl.ell;
+    a.ell_pad = (int)lp;
+    for (const Item* it : run) {
+        const int g = a.n++;
+        SmallMulItem& m = a.it[g];
+        m.mat = mats + (int64_t)it->pool_off * lp * lp;
+        fill(*it, m);
+        a.zbeg[g] = it->pool_off - (int)off0;
+        a.zbeg[g + 1] = a.zbeg[g] + it->count;
+    }
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_small_mul(a, sc.s); }), what);
+    return NORMPRE_OK;
+}
+
+// One Cholesky-QR pass over every item of the round: Gram (one launch per
+// pool), Cholesky and inverse (one launch per pool), then Q = Y R^-1 (one
+// launch per pool).
 int cholqr_round(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& pools, bool final_pass) {
-    for (const Item& it : items) {
-        const float* v = final_pass ? it.w.v32[1] : it.w.v32[0];
-        int rc = gram64_launch(sc, it, pools[it.pool], v, it.d.a_pad);
+    const auto runs = pool_runs(items, pools);
+    for (const auto& run : runs) {
+        int rc = gram64_run(sc, run, pools[run[0]->pool], [&](const Item& it, int64_t& len) -> const float* {
+            len = it.d.a_pad;
+            return final_pass ? it.w.v32[1] : it.w.v32[0];
+        });
         if (rc) return rc;
     }
     for (const Pool& pl : pools)
@@ -889,22 +942,26 @@ int cholqr_round(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>&
                                                 sc.s);
                      }),
                "cholesky");
-    for (const Item& it : items) {
-        const Dims& d = it.d;
-        const int64_t lp = d.ellp, maxpad = d.lp_, len = d.a_pad;
-        const Pool& pl = pools[it.pool];
-        SmallMulArgs a{};
-        a.mat = pl.rinv + (int64_t)it.pool_off * lp * lp; a.stride_mat = lp * lp;
-        a.v = final_pass ? it.w.v32[1] : it.w.v32[0]; a.ld_v = len; a.stride_v = lp * maxpad;
-        a.ell = d.ell; a.ell_pad = (int)lp; a.len = len; a.len_pad = len;
-        if (final_pass) {
-            a.out16 = it.w.v16[0]; a.stride_out16 = lp * maxpad;
-            a.out16t = it.w.qlen; a.stride_out16t = len * lp;
-        } else {
-            a.out32 = it.w.v32[1]; a.stride_out32 = lp * maxpad;
-        }
-        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_small_mul(a, it.count, sc.s); }),
-               "q = y r^-1");
+    for (const auto& run : runs) {
+        const Pool& pl = pools[run[0]->pool];
+        int rc = small_mul_run(
+            sc, run, pl, pl.rinv,
+            [&](const Item& it, SmallMulItem& m) {
+                const int64_t lp = it.d.ellp, maxpad = it.d.lp_, len = it.d.a_pad;
+                m.v = final_pass ? it.w.v32[1] : it.w.v32[0];
+                m.ld_v = len;
+                m.stride_v = lp * maxpad;
+                m.len = len;
+                m.len_pad = len;
+                if (final_pass) {
+                    m.out16 = it.w.v16[0]; m.stride_out16 = lp * maxpad;
+                    m.out16t = it.w.qlen; m.stride_out16t = len * lp;
+                } else {
+                    m.out32 = it.w.v32[1]; m.stride_out32 = lp * maxpad;
+                }
+            },
+            "q = y r^-1");
+        if (rc) return rc;
     }
     return NORMPRE_OK;
 }
@@ -963,17 +1020,7 @@ int sketch_back(const StepCtx& sc, const Item& it, const Pool& pl, DebugMat* dbg
     const std::vector<int>& idx = (*sc.groups)[it.g].idx;
     const int first = it.first, count = it.count;
     const normpre_hparams& hp = *sc.hp;
-    const int64_t lp = d.ellp, maxpad = d.lp_, mn = d.mp * d.np_;
-    // F = B^T K (b_pad x ell_pad, fp16)
-    {
-        SmallMulArgs a{};
-        a.mat = pl.kmat + (int64_t)it.pool_off * lp * lp; a.stride_mat = lp * lp;
-        a.v = w.v32[0]; a.ld_v = d.b_pad; a.stride_v = lp * maxpad;
-        a.ell = d.ell; a.ell_pad = (int)lp; a.len = d.b_pad; a.len_pad = d.b_pad;
-        a.out16t = w.flen; a.stride_out16t = d.b_pad * lp;
-        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_small_mul(a, count, sc.s); }),
-               "f = b^t k");
-    }
+    const int64_t lp = d.ellp, mn = d.mp * d.np_;
     // T = Psi + L R^T in the W layout, fused with the RMS-matched update.
     const half_t* L = d.k == 0 ? w.qlen : w.flen;
     const half_t* R = d.k == 0 ? w.flen : w.qlen;
@@ -1036,11 +1083,17 @@ int run_round_l(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& 
     if (rc) return rc;
     rc = cholqr_round(sc, items, pools, true);
     if (rc) return rc;
-    // B = Q^T Psi (ell_pad x b_pad) and Gamma_Q = B B^T per item.
+    // B = Q^T Psi (ell_pad x b_pad) per item, Gamma_Q = B B^T per pool.
     for (const Item& it : items) {
         rc = sketch_product(sc, it.d, it.w, it.count, it.w.v16[0], false, it.w.v32[0], nullptr, 1.f);
         if (rc) return rc;
-        rc = gram64_launch(sc, it, pools[it.pool], it.w.v32[0], it.d.b_pad);
+    }
+    const auto runs = pool_runs(items, pools);
+    for (const auto& run : runs) {
+        rc = gram64_run(sc, run, pools[run[0]->pool], [&](const Item& it, int64_t& len) -> const float* {
+            len = it.d.b_pad;
+            return it.w.v32[0];
+        });
         if (rc) return rc;
     }
     // Ritz pairs and selection, one launch per pool.
@@ -1053,6 +1106,20 @@ int run_round_l(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& 
         ea.max_sweeps = kEigSweeps;
         NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_eig_select(ea, pl.count, sc.s); }),
                "eigensolver");
+    }
+    // F = B^T K (b_pad x ell_pad, fp16), one launch per pool.
+    for (const auto& run : runs) {
+        const Pool& pl = pools[run[0]->pool];
+        rc = small_mul_run(
+            sc, run, pl, pl.kmat,
+            [&](const Item& it, SmallMulItem& m) {
+                const int64_t lp = it.d.ellp;
+                m.v = it.w.v32[0]; m.ld_v = it.d.b_pad; m.stride_v = lp * it.d.lp_;
+                m.len = it.d.b_pad; m.len_pad = it.d.b_pad;
+                m.out16t = it.w.flen; m.stride_out16t = it.d.b_pad * lp;
+            },
+            "f = b^t k");
+        if (rc) return rc;
     }
     for (const Item& it : items) {
         rc = sketch_back(sc, it, pools[it.pool], dbg);

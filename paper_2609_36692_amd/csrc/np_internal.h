@@ -195,12 +195,28 @@ hipError_t launch_reduce_splits(const float* part, int splits, int64_t stride_sp
                                 float* out32, half_t* out16, float scale16,
                                 int64_t stride_out, int batch, hipStream_t s);
 
-// fp64 Gram of the rows of an l-major fp32 matrix V (l_pad x len):
+// Fixed number of length-chunk slots of the fp64 Gram partial sums (unused
+// slots hold zeros); its consumers always add all of them.
+constexpr int kGramChunks = 16;
+// Grouped launches over the items of one pool (same l): item g covers the
+// launch's matrices [zbeg[g], zbeg[g + 1]), which are also its matrices'
+// indices in the pool's l x l buffers.
+constexpr int kMaxItems = 8;
+
+// fp64 Gram of the rows of l-major fp32 matrices V (l_pad x len each):
 // partial[z][chunk][c][d] = sum_{j in chunk} V[c][j] V[d][j], upper tiles.
-// Launches `chunks` length chunks of chunk_len (chunks past len write zeros).
-hipError_t launch_gram64(const float* v, int64_t ld, int64_t stride_v, int ell_pad,
-                         int64_t len, int chunk_len, int chunks, double* partial, int batch,
-                         hipStream_t s);
+// Every launch writes all kGramChunks chunk slots of chunk_len (slots past
+// len hold zeros).
+struct Gram64Items {
+    int n;
+    int zbeg[kMaxItems + 1];
+    const float* v[kMaxItems];
+    int64_t ld[kMaxItems];
+    int64_t stride[kMaxItems];
+    int64_t len[kMaxItems];
+    int chunk_len[kMaxItems];
+};
+hipError_t launch_gram64(const Gram64Items& t, int ell_pad, double* partial, hipStream_t s);
 int gram64_chunks(int64_t len, int chunk_len);
 
 // Cholesky (with dropping of numerically dependent columns) of the summed
@@ -210,15 +226,21 @@ hipError_t launch_chol_inv(const double* partial, int chunks, int ell, int ell_p
 
 // out = M^T V  (M: l_pad x l_pad fp32, V: l_pad x len fp32, l-major),
 // optional outputs: fp32 l-major, fp16 l-major, fp16 len-major (len x l_pad).
-struct SmallMulArgs {
-    const float* mat; int64_t stride_mat;
+struct SmallMulItem {
+    const float* mat;                            // first matrix's M; stride l_pad^2
     const float* v; int64_t ld_v; int64_t stride_v;
-    int ell, ell_pad; int64_t len, len_pad;
+    int64_t len, len_pad;
     float* out32; int64_t stride_out32;          // ld = ld_v
     half_t* out16; int64_t stride_out16;         // ld = ld_v
     half_t* out16t; int64_t stride_out16t;       // ld = ell_pad
 };
-hipError_t launch_small_mul(const SmallMulArgs& a, int batch, hipStream_t s);
+struct SmallMulArgs {
+    int ell, ell_pad;
+    int n;
+    int zbeg[kMaxItems + 1];
+    SmallMulItem it[kMaxItems];
+};
+hipError_t launch_small_mul(const SmallMulArgs& a, hipStream_t s);
 
 // Jacobi eigensolver of Gamma_Q (summed fp64 partials), selection of the
 // top-min(r, l) Ritz values > 1, K = Z_C diag(lambda^-1/2 - 1) Z_C^T (fp32,

@@ -13,6 +13,8 @@
 //     matrix K = Z_C diag(lambda_C^{-1/2} - 1) Z_C^T.
 #include "np_internal.h"
 
+#include <algorithm>
+
 namespace np {
 namespace {
 
@@ -89,17 +91,27 @@ __global__ void reduce_splits_kernel(const float* part, int splits, int64_t stri
 }
 
 // ------------------------------------------------------------ fp64 Gram ---
+// Item of launch matrix z in a grouped launch (few items: a linear scan).
+template <class T>
+__device__ __forceinline__ int item_of(const T& t, int z) {
+    int g = 0;
+    while (g + 1 < t.n && z >= t.zbeg[g + 1]) ++g;
+    return g;
+}
+
 // 32 x 32 output tile (tc <= td) over one chunk of the length dimension.
-__global__ void __launch_bounds__(256) gram64_kernel(const float* v, int64_t ld, int64_t stride_v, int ell_pad,
-                                                     int64_t len, int chunk_len, double* partial) {
+__global__ void __launch_bounds__(256) gram64_kernel(Gram64Items t, int ell_pad, double* partial) {
     const int z = blockIdx.z, chunk = blockIdx.y;
+    const int g = item_of(t, z);
+    const int64_t ld = t.ld[g], len = t.len[g];
+    const int chunk_len = t.chunk_len[g];
     const int tiles = ell_pad / 32;
     int tc = 0, left = blockIdx.x;
     while (left >= tiles - tc) { left -= tiles - tc; ++tc; }
     const int td = tc + left;
     __shared__ float sc[32][65], sd[32][65];
     const int tid = threadIdx.x, tr = tid >> 4, tcl = tid & 15;
-    const float* vz = v + (int64_t)z * stride_v;
+    const float* vz = t.v[g] + (int64_t)(z - t.zbeg[g]) * t.stride[g];
     double acc[2][2] = {{0.0, 0.0}, {0.0, 0.0}};
     const int64_t j0 = (int64_t)chunk * chunk_len, j1 = min(len, j0 + chunk_len);
     for (int64_t jb = j0; jb < j1; jb += 64) {
@@ -121,8 +133,7 @@ __global__ void __launch_bounds__(256) gram64_kernel(const float* v, int64_t ld,
         }
         __syncthreads();
     }
-    const int nchunks = gridDim.y;
-    double* out = partial + ((int64_t)z * nchunks + chunk) * ell_pad * ell_pad;
+    double* out = partial + ((int64_t)z * kGramChunks + chunk) * ell_pad * ell_pad;
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
@@ -130,11 +141,19 @@ __global__ void __launch_bounds__(256) gram64_kernel(const float* v, int64_t ld,
             out[(int64_t)(tc * 32 + 2 * tr + a) * ell_pad + td * 32 + 2 * tcl + b] = acc[a][b];
 }
 
-// Element (c, d) of the summed Gram (full symmetric view of upper tiles).
-__device__ __forceinline__ double gram_at(const double* p, int chunks, int ell_pad, int c, int d) {
+// Element (c, d) of the summed Gram (full symmetric view of upper tiles):
+// the kGramChunks partial sums are all requested before any is added, so
+// one memory latency covers the element; they are added in chunk order.
+__device__ __forceinline__ double gram_at(const double* p, int ell_pad, int c, int d) {
     if ((c >> 5) > (d >> 5)) { const int t = c; c = d; d = t; }
+    const double* q = p + (int64_t)c * ell_pad + d;
+    const int64_t cs = (int64_t)ell_pad * ell_pad;
+    double v[kGramChunks];
+#pragma unroll
+    for (int k = 0; k < kGramChunks; ++k) v[k] = q[k * cs];
     double s = 0.0;
-    for (int k = 0; k < chunks; ++k) s += p[((int64_t)k * ell_pad + c) * ell_pad + d];
+#pragma unroll
+    for (int k = 0; k < kGramChunks; ++k) s += v[k];
     return s;
 }
 
@@ -149,82 +168,116 @@ constexpr double kDropTol = 1e-12;
 constexpr int kCholLdsMax = 138;
 constexpr int kSmallThreads = 512;
 
+constexpr int kCholThreads = 1024;
+// Largest l whose inverse runs one column per thread.
+constexpr int kCholColInvMax = 96;
+// Upper-triangle entries (i <= j) owned per thread: l (l + 1) / 2 entries for
+// l <= kCholLdsMax over kCholThreads threads.
+constexpr int kCholOwn = (kCholLdsMax * (kCholLdsMax + 1) / 2 + kCholThreads - 1) / kCholThreads;
+
 template <bool IN_LDS>
-__global__ void __launch_bounds__(kSmallThreads) chol_inv_kernel(const double* partial, int chunks, int ell,
-                                                                 int ell_pad, double* scratch, float* rinv) {
-    constexpr int NT = kSmallThreads;
+__global__ void __launch_bounds__(kCholThreads) chol_inv_kernel(const double* partial, int chunks, int ell,
+                                                                int ell_pad, double* scratch, float* rinv) {
+    constexpr int NT = kCholThreads;
     extern __shared__ double dynd[];
     const int z = blockIdx.x, tid = threadIdx.x;
     const double* p = partial + (int64_t)z * chunks * ell_pad * ell_pad;
     const int ld = IN_LDS ? ell + 1 : ell_pad;
+    // One square buffer.  Step k reads the updated upper row k, leaves the
+    // finished row k of R in the lower triangle (R(k, j) at [j][k]) and
+    // updates the upper trailing block, so it never reads what it writes and
+    // one barrier per step suffices.  R^{-1} then fills the upper triangle,
+    // one column per thread, reading R from the lower triangle.
     double* R;
-    double* tmp;
-    if constexpr (IN_LDS) {
-        R = dynd;
-        tmp = dynd + ell * ld;
-    } else {
-        R = scratch + (int64_t)z * 2 * ell_pad * ell_pad;
-        tmp = R + (int64_t)ell_pad * ell_pad;
-    }
+    if constexpr (IN_LDS) R = dynd;
+    else R = scratch + (int64_t)z * 2 * ell_pad * ell_pad;
     float* out = rinv + (int64_t)z * ell_pad * ell_pad;
     __shared__ double diag0[384];
     __shared__ double inv_diag[384];
     for (int q = tid; q < ell * ell; q += NT) {
         const int c = q / ell, d = q - (q / ell) * ell;
-        if (d >= c) R[c * ld + d] = gram_at(p, chunks, ell_pad, c, d);
+        if (d >= c) {
+            const double g = gram_at(p, ell_pad, c, d);
+            R[c * ld + d] = g;
+            if (c == d) diag0[c] = g;
+        }
     }
     __syncthreads();
-    for (int k = tid; k < ell; k += NT) diag0[k] = R[k * ld + k];
-    __syncthreads();
-    for (int k = 0; k < ell; ++k) {
-        if (tid == 0) {
+    if (IN_LDS) {
+        // The trailing updates of this thread's fixed entries, no index
+        // arithmetic in the step loop.
+        int own[kCholOwn];
+        const int ne = ell * (ell + 1) / 2;
+#pragma unroll
+        for (int m = 0; m < kCholOwn; ++m) {
+            int e = tid + m * NT, i = 0;
+            if (e < ne) {
+                while (e >= ell - i) { e -= ell - i; ++i; }
+                own[m] = (i << 16) | (i + e);
+            } else {
+                own[m] = -1;
+            }
+        }
+        for (int k = 0; k < ell; ++k) {
             const double piv = R[k * ld + k];
             const bool keep = diag0[k] > 0.0 && piv > kDropTol * diag0[k];
-            const double rkk = keep ? sqrt(piv) : 0.0;
-            R[k * ld + k] = rkk;
-            inv_diag[k] = keep ? 1.0 / rkk : 0.0;
-        }
-        __syncthreads();
-        const double ik = inv_diag[k];
-        for (int j = k + 1 + tid; j < ell; j += NT) R[k * ld + j] *= ik;
-        __syncthreads();
-        const int nrem = ell - k - 1;
-        // Independent updates; unrolled so several global (scratch-mode)
-        // loads are in flight per thread.
-#pragma unroll 4
-        for (int q = tid; q < nrem * nrem; q += NT) {
-            const int i = k + 1 + q / nrem, j = k + 1 + q % nrem;
-            if (j >= i) R[i * ld + j] -= R[k * ld + i] * R[k * ld + j];
-        }
-        __syncthreads();
-    }
-    // X = R^{-1}: row i from R's row i and the finished rows below it.
-    for (int i = ell - 1; i >= 0; --i) {
-        const double ii = inv_diag[i];
-        for (int j = i + tid; j < ell; j += NT) {
-            double v;
-            if (j == i) {
-                v = ii;
-            } else {
-                // Four partial sums so consecutive loads do not wait on one
-                // accumulator chain.
-                double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-                int k = i + 1;
-                for (; k + 3 <= j; k += 4) {
-                    s0 += R[i * ld + k] * R[k * ld + j];
-                    s1 += R[i * ld + k + 1] * R[(k + 1) * ld + j];
-                    s2 += R[i * ld + k + 2] * R[(k + 2) * ld + j];
-                    s3 += R[i * ld + k + 3] * R[(k + 3) * ld + j];
-                }
-                for (; k <= j; ++k) s0 += R[i * ld + k] * R[k * ld + j];
-                v = -((s0 + s1) + (s2 + s3)) * ii;
+            const double ipiv = keep ? 1.0 / piv : 0.0;
+            const double irk = keep ? 1.0 / sqrt(piv) : 0.0;
+            if (tid == 0) inv_diag[k] = irk;
+            for (int j = k + 1 + tid; j < ell; j += NT) R[j * ld + k] = R[k * ld + j] * irk;
+#pragma unroll
+            for (int m = 0; m < kCholOwn; ++m) {
+                if (own[m] < 0) break;
+                const int i = own[m] >> 16, j = own[m] & 0xffff;
+                if (i > k) R[i * ld + j] -= R[k * ld + i] * R[k * ld + j] * ipiv;
             }
-            tmp[j] = v;
+            __syncthreads();
         }
-        __syncthreads();
-        for (int j = i + tid; j < ell; j += NT) R[i * ld + j] = tmp[j];
-        __syncthreads();
+    } else {
+        for (int k = 0; k < ell; ++k) {
+            const double piv = R[k * ld + k];
+            const bool keep = diag0[k] > 0.0 && piv > kDropTol * diag0[k];
+            const double ipiv = keep ? 1.0 / piv : 0.0;
+            const double irk = keep ? 1.0 / sqrt(piv) : 0.0;
+            if (tid == 0) inv_diag[k] = irk;
+            for (int j = k + 1 + tid; j < ell; j += NT) R[j * ld + k] = R[k * ld + j] * irk;
+            const int nrem = ell - k - 1;
+#pragma unroll 4
+            for (int q = tid; q < nrem * nrem; q += NT) {
+                const int i = k + 1 + q / nrem, j = k + 1 + q % nrem;
+                if (j >= i) R[i * ld + j] -= R[k * ld + i] * R[k * ld + j] * ipiv;
+            }
+            __syncthreads();
+        }
     }
+    // X = R^{-1}: X(i, j) = -(sum_{i < k <= j} R(i, k) X(k, j)) / R(i, i),
+    // X(i, i) = 1 / R(i, i); rows of dropped columns are zero.  Small l: one
+    // column per thread (no barriers); larger l: one row per step, bottom
+    // first, its entries in parallel.
+    auto x_entry = [&](int i, int j) {
+        double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+        int k = i + 1;
+        for (; k + 3 <= j; k += 4) {
+            s0 += R[k * ld + i] * R[k * ld + j];
+            s1 += R[(k + 1) * ld + i] * R[(k + 1) * ld + j];
+            s2 += R[(k + 2) * ld + i] * R[(k + 2) * ld + j];
+            s3 += R[(k + 3) * ld + i] * R[(k + 3) * ld + j];
+        }
+        for (; k <= j; ++k) s0 += R[k * ld + i] * R[k * ld + j];
+        return -((s0 + s1) + (s2 + s3)) * inv_diag[i];
+    };
+    if (IN_LDS && ell <= kCholColInvMax) {
+        for (int j = tid; j < ell; j += NT) {
+            R[j * ld + j] = inv_diag[j];
+            for (int i = j - 1; i >= 0; --i) R[i * ld + j] = x_entry(i, j);
+        }
+    } else {
+        for (int i = ell - 1; i >= 0; --i) {
+            for (int j = i + tid; j < ell; j += NT) R[i * ld + j] = j == i ? inv_diag[i] : x_entry(i, j);
+            __syncthreads();
+        }
+    }
+    __syncthreads();
     for (int q = tid; q < ell_pad * ell_pad; q += NT) {
         const int i = q / ell_pad, j = q - (q / ell_pad) * ell_pad;
         out[q] = (i < ell && j < ell && j >= i) ? (float)R[i * ld + j] : 0.f;
@@ -232,26 +285,31 @@ __global__ void __launch_bounds__(kSmallThreads) chol_inv_kernel(const double* p
 }
 
 // ------------------------------------------------------------- M^T V ----
-// Block: 64 columns of V, all l_pad outputs rows in groups of 64.
-__global__ void __launch_bounds__(256) small_mul_kernel(SmallMulArgs a) {
+// Block: 64 columns of V, all l_pad outputs rows in groups of 64.  The grid
+// spans the longest item; blocks past an item's length return at once.
+__global__ void __launch_bounds__(256) small_mul_kernel(SmallMulArgs args) {
     const int z = blockIdx.y;
+    const int g = item_of(args, z), lz = z - args.zbeg[g];
+    const SmallMulItem& a = args.it[g];
     const int64_t j0 = (int64_t)blockIdx.x * 64;
+    if (j0 >= a.len_pad) return;
+    const int ell = args.ell, ell_pad = args.ell_pad;
     const int tid = threadIdx.x, jx = tid & 63, cy = tid >> 6;
-    const float* M = a.mat + (int64_t)z * a.stride_mat;
-    const float* V = a.v + (int64_t)z * a.stride_v;
+    const float* M = a.mat + (int64_t)lz * ell_pad * ell_pad;
+    const float* V = a.v + (int64_t)lz * a.stride_v;
     __shared__ float sm[64][65];
     __shared__ float sv[64][65];
     __shared__ half_t st[64][72];
-    for (int c0 = 0; c0 < a.ell_pad; c0 += 64) {
+    for (int c0 = 0; c0 < ell_pad; c0 += 64) {
         float acc[16];
 #pragma unroll
         for (int q = 0; q < 16; ++q) acc[q] = 0.f;
-        for (int d0 = 0; d0 < a.ell; d0 += 64) {
+        for (int d0 = 0; d0 < ell; d0 += 64) {
             for (int q = tid; q < 64 * 64; q += 256) {
                 const int r = q >> 6, cc = q & 63;
                 const int d = d0 + r;
-                sm[r][cc] = (d < a.ell && c0 + cc < a.ell_pad) ? M[(int64_t)d * a.ell_pad + c0 + cc] : 0.f;
-                sv[r][cc] = (d < a.ell && j0 + cc < a.len_pad) ? V[(int64_t)d * a.ld_v + j0 + cc] : 0.f;
+                sm[r][cc] = (d < ell && c0 + cc < ell_pad) ? M[(int64_t)d * ell_pad + c0 + cc] : 0.f;
+                sv[r][cc] = (d < ell && j0 + cc < a.len_pad) ? V[(int64_t)d * a.ld_v + j0 + cc] : 0.f;
             }
             __syncthreads();
             for (int dd = 0; dd < 64; ++dd) {
@@ -265,9 +323,9 @@ __global__ void __launch_bounds__(256) small_mul_kernel(SmallMulArgs a) {
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
             const int c = c0 + cy + 4 * q;
-            if (c < a.ell_pad && j < a.len_pad) {
-                if (a.out32) a.out32[(int64_t)z * a.stride_out32 + (int64_t)c * a.ld_v + j] = acc[q];
-                if (a.out16) a.out16[(int64_t)z * a.stride_out16 + (int64_t)c * a.ld_v + j] = (half_t)acc[q];
+            if (c < ell_pad && j < a.len_pad) {
+                if (a.out32) a.out32[(int64_t)lz * a.stride_out32 + (int64_t)c * a.ld_v + j] = acc[q];
+                if (a.out16) a.out16[(int64_t)lz * a.stride_out16 + (int64_t)c * a.ld_v + j] = (half_t)acc[q];
             }
             st[jx][cy + 4 * q] = (half_t)acc[q];
         }
@@ -277,8 +335,8 @@ __global__ void __launch_bounds__(256) small_mul_kernel(SmallMulArgs a) {
             for (int q = tid; q < 64 * 64; q += 256) {
                 const int r = q >> 6, cc = q & 63;
                 const int64_t jr = j0 + r;
-                if (jr < a.len_pad && c0 + cc < a.ell_pad)
-                    a.out16t[(int64_t)z * a.stride_out16t + jr * a.ell_pad + c0 + cc] = st[r][cc];
+                if (jr < a.len_pad && c0 + cc < ell_pad)
+                    a.out16t[(int64_t)lz * a.stride_out16t + jr * ell_pad + c0 + cc] = st[r][cc];
             }
         }
         __syncthreads();
@@ -296,6 +354,15 @@ constexpr int kEigLdsMax = 138;
 // Packed mode: the upper triangle of A (rows packed) in LDS, Z^T in a global
 // scratch slice; used above kEigLdsMax while l (l + 1) / 2 floats fit.
 constexpr int kEigPackedMax = 278;
+
+// Stopping rule of every Jacobi kernel, tested on the squared off-diagonal
+// mass `off` against the squared Frobenius norm `tot`: converged below
+// 1e-13 relative, or stalled at the fp32 rounding floor (already below 1e-9
+// relative and less than a 4x drop over the last sweep; the quadratic phase
+// drops it far more per sweep until rounding dominates).
+__device__ __forceinline__ bool jacobi_done(float off, float tot, float prev_off) {
+    return !(off > 1e-13f * tot) || (off <= 1e-9f * tot && off >= 0.25f * prev_off);
+}
 
 __device__ __forceinline__ void rr_pair(int round, int k, int n2, int& p, int& q) {
     const int n1 = n2 - 1;
@@ -337,13 +404,14 @@ __global__ void __launch_bounds__(kSmallThreads) eig_select_kernel(EigArgs a) {
     const double* part = a.partial + (int64_t)z * a.chunks * lp * lp;
     for (int q = tid; q < n * n; q += NT) {
         const int c = q / n, d = q - (q / n) * n;
-        A[c * ld + d] = (float)gram_at(part, a.chunks, lp, c, d);
+        A[c * ld + d] = (float)gram_at(part, lp, c, d);
         Z[c * ld + d] = c == d ? 1.f : 0.f;
     }
     __syncthreads();
     const int n2 = n + (n & 1);
     const int npairs = n2 / 2;
     const int nblk = npairs * npairs;
+    float prev_off = INFINITY;
     for (int sweep = 0; sweep < a.max_sweeps; ++sweep) {
         float off = 0.f, tot = 0.f;
         for (int q = tid; q < n * n; q += NT) {
@@ -354,7 +422,8 @@ __global__ void __launch_bounds__(kSmallThreads) eig_select_kernel(EigArgs a) {
         }
         off = block_sum_f<NT>(off, red);
         tot = block_sum_f<NT>(tot, red);
-        if (tid == 0) stop_flag = !(off > 1e-13f * tot);
+        if (tid == 0) stop_flag = jacobi_done(off, tot, prev_off);
+        prev_off = off;
         __syncthreads();
         if (stop_flag) break;
         for (int round = 0; round < n2 - 1; ++round) {
@@ -465,12 +534,13 @@ __global__ void __launch_bounds__(kSmallThreads) eig_select_packed_kernel(EigArg
     const double* part = a.partial + (int64_t)z * a.chunks * lp * lp;
     for (int q = tid; q < n * n; q += NT) {
         const int c = q / n, d = q - (q / n) * n;
-        if (c <= d) A[pk(c, d, n)] = (float)gram_at(part, a.chunks, lp, c, d);
+        if (c <= d) A[pk(c, d, n)] = (float)gram_at(part, lp, c, d);
         Zt[(int64_t)c * lp + d] = c == d ? 1.f : 0.f;
     }
     __syncthreads();
     const int n2 = n + (n & 1);
     const int npairs = n2 / 2;
+    float prev_off = INFINITY;
     for (int sweep = 0; sweep < a.max_sweeps; ++sweep) {
         float off = 0.f, tot = 0.f;
         for (int q = tid; q < n * n; q += NT) {
@@ -482,7 +552,8 @@ __global__ void __launch_bounds__(kSmallThreads) eig_select_packed_kernel(EigArg
         }
         off = block_sum_f<NT>(off, red);
         tot = block_sum_f<NT>(tot, red);
-        if (tid == 0) stop_flag = !(off > 1e-13f * tot);
+        if (tid == 0) stop_flag = jacobi_done(off, tot, prev_off);
+        prev_off = off;
         __syncthreads();
         if (stop_flag) break;
         for (int round = 0; round < n2 - 1; ++round) {
@@ -600,6 +671,215 @@ __global__ void __launch_bounds__(kSmallThreads) eig_select_packed_kernel(EigArg
     }
 }
 
+// Round-robin Jacobi for l <= kEigRRMax with A double-buffered in LDS: a
+// round reads the current A and writes J^T A J into the other buffer, and
+// each thread derives the rotations of its own pair-blocks from the current
+// A with the same arithmetic the pair's diagonal block uses, so a round
+// needs one barrier instead of two.  The columns of Z take round r's
+// rotations during round r + 1 (published by the diagonal blocks, double
+// buffered by round parity).  The off-diagonal mass is summed while the last
+// round of a sweep is written, so the stopping test costs no extra pass.
+// Arithmetic per rotation, the stopping rule, selection and K are those of
+// eig_select_kernel.
+constexpr int kEigRRMax = 104;
+
+__device__ __forceinline__ void rr_pair_fast(int round, int k, int n1, int& p, int& q) {
+    if (k == 0) {
+        p = n1; q = round;
+    } else {
+        p = round + k;
+        if (p >= n1) p -= n1;
+        q = round - k;
+        if (q < 0) q += n1;
+    }
+    if (p > q) { const int t = p; p = q; q = t; }
+}
+
+// Rotation (c, s) that zeroes a_pq (Rutishauser's tangent form), or the
+// identity below the same threshold as the other Jacobi kernels.  Hardware
+// reciprocal / square-root approximations: the rotation only has to be
+// orthogonal to fp32 precision, which rsq keeps (c^2 + s^2 = 1 to ~1 ulp),
+// and every thread that needs a pair's rotation computes it with the same
+// instructions from the same operands.
+__device__ __forceinline__ void jacobi_rotation_fast(float app, float aqq, float apq, bool real, float& c, float& s) {
+    const float aa = fabsf(apq);
+    const bool rot = real && aa > 1e-30f && aa > 1e-9f * __builtin_amdgcn_sqrtf(fabsf(app * aqq));
+    const float theta = (aqq - app) * 0.5f * __builtin_amdgcn_rcpf(apq);
+    const float at = fabsf(theta);
+    const float t = copysignf(__builtin_amdgcn_rcpf(at + __builtin_amdgcn_sqrtf(fmaf(at, at, 1.f))), theta);
+    const float cc = __builtin_amdgcn_rsqf(fmaf(t, t, 1.f));
+    c = rot ? cc : 1.f;
+    s = rot ? t * cc : 0.f;
+}
+
+template <int NT, int NB, int NZ>
+__global__ void __launch_bounds__(NT) eig_select_rr_kernel(EigArgs a) {
+    extern __shared__ float dyn[];
+    const int z = blockIdx.x, tid = threadIdx.x;
+    const int n = a.ell, lp = a.ell_pad, ld = n + 1;
+    // Two n x (n + 1) buffers for A and one for Z; the padding column n
+    // absorbs the phantom index of odd n (reads there are masked, writes
+    // are identity rotations).
+    float* Ac = dyn;
+    float* An = dyn + n * ld;
+    float* Z = dyn + 2 * n * ld;
+    // Rotation of each pair, published by its diagonal block: (c, s, p, q).
+    __shared__ float4 rec[2][kEigRRMax / 2 + 1];
+    __shared__ float red[2][2][NT / 64];
+    __shared__ float lam[kEigRRMax], fcoef[kEigRRMax];
+    __shared__ int rnk[kEigRRMax];
+    const double* part = a.partial + (int64_t)z * a.chunks * lp * lp;
+    for (int q = tid; q < n * ld; q += NT) {
+        const int c = q / ld, d = q - (q / ld) * ld;
+        Ac[q] = d < n ? (float)gram_at(part, lp, c, d) : 0.f;
+        Z[q] = c == d ? 1.f : 0.f;
+    }
+    const int n2 = n + (n & 1), n1 = n2 - 1, npairs = n2 / 2;
+    const int ub = npairs * (npairs + 1) / 2;
+    // This thread's pair-blocks (k1 <= k2) and Z items (pair k, row i).
+    int bk1[NB], bk2[NB], zk[NZ], zi[NZ];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        int w = tid + j * NT, k1 = -1, k2 = -1;
+        if (w < ub) {
+            k1 = 0;
+            while (w >= npairs - k1) { w -= npairs - k1; ++k1; }
+            k2 = k1 + w;
+        }
+        bk1[j] = k1;
+        bk2[j] = k2;
+    }
+#pragma unroll
+    for (int j = 0; j < NZ; ++j) {
+        const int w = tid + j * NT;
+        zk[j] = w < npairs * n ? w / n : -1;
+        zi[j] = w < npairs * n ? w - (w / n) * n : 0;
+    }
+    __syncthreads();
+    int gr = 0;             // rounds done (parity of the published rotations)
+    const int lane = tid & 63, wave = tid >> 6;
+    // Columns p, q of Z take the rotations published in round gr - 1.
+    auto rotate_z = [&](int par) {
+#pragma unroll
+        for (int j = 0; j < NZ; ++j) {
+            if (zk[j] < 0) break;
+            const float4 r = rec[par][zk[j]];
+            const int p = __float_as_int(r.z), q = __float_as_int(r.w), i = zi[j];
+            const float za = Z[i * ld + p], zb = Z[i * ld + q];
+            Z[i * ld + p] = r.x * za - r.y * zb;
+            Z[i * ld + q] = r.y * za + r.x * zb;
+        }
+    };
+    float prev_off = INFINITY;
+    for (int sweep = 0; sweep < a.max_sweeps; ++sweep) {
+        float off = 0.f, tot = 0.f;
+        for (int round = 0; round < n1; ++round, ++gr) {
+            const bool last = round == n1 - 1;
+#pragma unroll
+            for (int j = 0; j < NB; ++j) {
+                const int k1 = bk1[j], k2 = bk2[j];
+                if (k1 < 0) break;
+                int p1, q1, p2, q2;
+                rr_pair_fast(round, k1, n1, p1, q1);
+                rr_pair_fast(round, k2, n1, p2, q2);
+                const bool r1 = q1 < n, r2 = q2 < n;
+                const int u1 = min(q1, n - 1), u2 = min(q2, n - 1);
+                // Every read of the block first, then the rotations.
+                const float x0 = Ac[p1 * ld + p1], x1 = Ac[u1 * ld + u1], x2 = Ac[p1 * ld + u1];
+                const float x3 = Ac[p2 * ld + p2], x4 = Ac[u2 * ld + u2], x5 = Ac[p2 * ld + u2];
+                const float x6 = Ac[p1 * ld + p2], x7 = Ac[p1 * ld + u2];
+                const float x8 = Ac[u1 * ld + p2], x9 = Ac[u1 * ld + u2];
+                if (j == 0 && gr > 0) rotate_z((gr - 1) & 1);
+                float c1, s1, c2, s2;
+                jacobi_rotation_fast(x0, x1, x2, r1, c1, s1);
+                jacobi_rotation_fast(x3, x4, x5, r2, c2, s2);
+                if (k2 == k1) rec[gr & 1][k1] = make_float4(c1, s1, __int_as_float(p1), __int_as_float(q1));
+                const float a00 = x6, a01 = r2 ? x7 : 0.f;
+                const float a10 = r1 ? x8 : 0.f, a11 = (r1 && r2) ? x9 : 0.f;
+                const float b00 = c1 * a00 - s1 * a10, b01 = c1 * a01 - s1 * a11;
+                const float b10 = s1 * a00 + c1 * a10, b11 = s1 * a01 + c1 * a11;
+                const float d00 = c2 * b00 - s2 * b01, d01 = s2 * b00 + c2 * b01;
+                const float d10 = c2 * b10 - s2 * b11, d11 = s2 * b10 + c2 * b11;
+                An[p1 * ld + p2] = d00;
+                if (r2) An[p1 * ld + q2] = d01;
+                if (r1) An[q1 * ld + p2] = d10;
+                if (r1 && r2) An[q1 * ld + q2] = d11;
+                if (k2 != k1) {
+                    An[p2 * ld + p1] = d00;
+                    if (r2) An[q2 * ld + p1] = d01;
+                    if (r1) An[p2 * ld + q1] = d10;
+                    if (r1 && r2) An[q2 * ld + q1] = d11;
+                }
+                if (last) {
+                    const float e00 = d00 * d00, e01 = r2 ? d01 * d01 : 0.f;
+                    const float e10 = r1 ? d10 * d10 : 0.f, e11 = (r1 && r2) ? d11 * d11 : 0.f;
+                    if (k2 != k1) {
+                        const float m = 2.f * (e00 + e01 + e10 + e11);
+                        off += m;
+                        tot += m;
+                    } else {
+                        off += e01 + e10;
+                        tot += e00 + e01 + e10 + e11;
+                    }
+                }
+            }
+            // Threads without a pair-block still rotate their Z items.
+            if (bk1[0] < 0 && gr > 0) rotate_z((gr - 1) & 1);
+            if (last) {
+#pragma unroll
+                for (int o = 32; o >= 1; o >>= 1) {
+                    off += __shfl_xor(off, o, 64);
+                    tot += __shfl_xor(tot, o, 64);
+                }
+                if (lane == 0) {
+                    red[sweep & 1][0][wave] = off;
+                    red[sweep & 1][1][wave] = tot;
+                }
+            }
+            __syncthreads();
+            float* t = Ac; Ac = An; An = t;
+        }
+        float so = 0.f, st = 0.f;
+#pragma unroll
+        for (int w = 0; w < NT / 64; ++w) {
+            so += red[sweep & 1][0][w];
+            st += red[sweep & 1][1][w];
+        }
+        if (jacobi_done(so, st, prev_off)) break;
+        prev_off = so;
+    }
+    if (gr > 0) rotate_z((gr - 1) & 1);
+    // Ritz values, descending order with ties to the lower index.
+    for (int i = tid; i < n; i += NT) lam[i] = Ac[i * ld + i];
+    __syncthreads();
+    const int top = min(a.rank, n);
+    for (int i = tid; i < n; i += NT) {
+        const float li = lam[i];
+        int r = 0;
+        for (int j = 0; j < n; ++j) r += (lam[j] > li) || (lam[j] == li && j < i);
+        rnk[i] = r;
+        const bool sel = r < top && li > 1.f;
+        fcoef[i] = sel ? (1.f / sqrtf(li) - 1.f) : 0.f;
+        if (r < top) a.ritz[(int64_t)z * a.ritz_stride + r] = li;
+    }
+    __syncthreads();
+    // K = Z diag(f) Z^T over the selected modes.
+    float* K = a.kmat + (int64_t)z * lp * lp;
+    for (int q = tid; q < lp * lp; q += NT) {
+        const int c = q / lp, d = q - (q / lp) * lp;
+        float s = 0.f;
+        if (c < n && d < n)
+            for (int i = 0; i < n; ++i)
+                if (fcoef[i] != 0.f) s = fmaf(Z[c * ld + i] * fcoef[i], Z[d * ld + i], s);
+        K[q] = s;
+    }
+    if (tid == 0) {
+        int cnt = 0;
+        for (int i = 0; i < n; ++i) cnt += (rnk[i] < top && lam[i] > 1.f);
+        a.nsel[z] = cnt;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_omega_f16(const OmegaArgs& a, int batch, hipStream_t s) {
@@ -629,38 +909,53 @@ hipError_t launch_reduce_splits(const float* part, int splits, int64_t stride_sp
 
 int gram64_chunks(int64_t len, int chunk_len) { return (int)((len + chunk_len - 1) / chunk_len); }
 
-hipError_t launch_gram64(const float* v, int64_t ld, int64_t stride_v, int ell_pad, int64_t len, int chunk_len,
-                         int chunks, double* partial, int batch, hipStream_t s) {
-    if (ell_pad % 32 || chunk_len % 64 || gram64_chunks(len, chunk_len) > chunks) return hipErrorInvalidValue;
+hipError_t launch_gram64(const Gram64Items& t, int ell_pad, double* partial, hipStream_t s) {
+    if (ell_pad % 32 || t.n < 1 || t.n > kMaxItems || t.zbeg[0] != 0) return hipErrorInvalidValue;
+    for (int g = 0; g < t.n; ++g)
+        if (t.chunk_len[g] % 64 || gram64_chunks(t.len[g], t.chunk_len[g]) > kGramChunks ||
+            t.zbeg[g + 1] <= t.zbeg[g])
+            return hipErrorInvalidValue;
     const int tiles = ell_pad / 32;
-    dim3 grid(tiles * (tiles + 1) / 2, chunks, batch);
-    hipLaunchKernelGGL(gram64_kernel, grid, dim3(256), 0, s, v, ld, stride_v, ell_pad, len, chunk_len, partial);
+    dim3 grid(tiles * (tiles + 1) / 2, kGramChunks, t.zbeg[t.n]);
+    hipLaunchKernelGGL(gram64_kernel, grid, dim3(256), 0, s, t, ell_pad, partial);
     return hipGetLastError();
 }
 
 hipError_t launch_chol_inv(const double* partial, int chunks, int ell, int ell_pad, double* scratch, float* rinv,
                            int batch, hipStream_t s) {
-    if (ell > 384 || ell_pad > 384) return hipErrorInvalidValue;
+    if (ell > 384 || ell_pad > 384 || chunks != kGramChunks) return hipErrorInvalidValue;
     if (ell <= kCholLdsMax) {
         const size_t lds = (size_t)(ell + 1) * (ell + 1) * sizeof(double);
-        hipLaunchKernelGGL((chol_inv_kernel<true>), dim3(batch), dim3(kSmallThreads), lds, s, partial, chunks, ell,
+        hipLaunchKernelGGL((chol_inv_kernel<true>), dim3(batch), dim3(kCholThreads), lds, s, partial, chunks, ell,
                            ell_pad, scratch, rinv);
     } else {
-        hipLaunchKernelGGL((chol_inv_kernel<false>), dim3(batch), dim3(kSmallThreads), 0, s, partial, chunks, ell,
+        hipLaunchKernelGGL((chol_inv_kernel<false>), dim3(batch), dim3(kCholThreads), 0, s, partial, chunks, ell,
                            ell_pad, scratch, rinv);
     }
     return hipGetLastError();
 }
 
-hipError_t launch_small_mul(const SmallMulArgs& a, int batch, hipStream_t s) {
-    dim3 grid((unsigned)((a.len_pad + 63) / 64), batch);
+hipError_t launch_small_mul(const SmallMulArgs& a, hipStream_t s) {
+    if (a.n < 1 || a.n > kMaxItems || a.zbeg[0] != 0) return hipErrorInvalidValue;
+    int64_t len_pad = 0;
+    for (int g = 0; g < a.n; ++g) {
+        if (a.zbeg[g + 1] <= a.zbeg[g]) return hipErrorInvalidValue;
+        len_pad = std::max(len_pad, a.it[g].len_pad);
+    }
+    dim3 grid((unsigned)((len_pad + 63) / 64), a.zbeg[a.n]);
     hipLaunchKernelGGL(small_mul_kernel, grid, dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
 hipError_t launch_eig_select(const EigArgs& a, int batch, hipStream_t s) {
-    if (a.ell > 384 || a.ell_pad > 384) return hipErrorInvalidValue;
-    if (a.ell <= kEigLdsMax) {
+    if (a.ell > 384 || a.ell_pad > 384 || a.chunks != kGramChunks) return hipErrorInvalidValue;
+    if (a.ell <= kEigRRMax) {
+        const size_t lds = (size_t)3 * a.ell * (a.ell + 1) * sizeof(float);
+        if (a.ell <= 64)
+            hipLaunchKernelGGL((eig_select_rr_kernel<1024, 1, 2>), dim3(batch), dim3(1024), lds, s, a);
+        else
+            hipLaunchKernelGGL((eig_select_rr_kernel<1024, 2, 6>), dim3(batch), dim3(1024), lds, s, a);
+    } else if (a.ell <= kEigLdsMax) {
         const size_t lds = (size_t)2 * a.ell * (a.ell + 1) * sizeof(float);
         hipLaunchKernelGGL((eig_select_kernel<true>), dim3(batch), dim3(kSmallThreads), lds, s, a);
     } else if (a.ell <= kEigPackedMax) {
