@@ -229,6 +229,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     // same LDS to stage one wave-row of fp32 results (row stride BN + 4).
     constexpr int kStageBytes = 2 * (BM + BN) * BK * 2;
     constexpr int kEpiBytes = (BM / WM) * (BN + 4) * 4;
+    constexpr bool kLdsMirror = BM * BN <= 128 * 128;
     __shared__ __attribute__((aligned(16))) unsigned char smem[kStageBytes > kEpiBytes ? kStageBytes : kEpiBytes];
     __shared__ float red[NT / 64];
     half_t* const sbase = reinterpret_cast<half_t*>(smem);
@@ -264,7 +265,12 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     }
     using LA = typename LoaderSel<(LAYOUT == 2), BM, NT>::type;
     using LB = typename LoaderSel<(LAYOUT >= 1), BN, NT>::type;
+    // DEEP: two staging sets, so each K-step's global loads have two
+    // K-steps to arrive (covers L2 misses served from the Infinity Cache);
+    // the 128 x 128 tile has the registers for it.
+    constexpr bool DEEP = MF == 32 && BM * BN <= 128 * 128;
     u32x4 ra[LA::N], rb[LB::N];
+    u32x4 ra2[LA::N], rb2[LB::N];
 
     using AccT = typename AccSel<MF>::type;
     AccT acc[FM][FN];
@@ -303,7 +309,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     // (item i at sub-step i * NSUB / N) so the LDS stores and global loads
     // are issued between MFMAs rather than after all of them.
     constexpr int NSUB = BK / 16;
-    auto kstep32 = [&](auto store_tag, auto load_tag, int stage, int k_load) {
+    auto kstep32 = [&](auto store_tag, auto load_tag, int stage, int k_load, auto& rA, auto& rB) {
         constexpr bool STORE = decltype(store_tag)::value, LOAD = decltype(load_tag)::value;
       if constexpr (MF == 32) {
         const half_t* ca = sbase + stage * (BM + BN) * BK;
@@ -334,23 +340,23 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
 #pragma unroll
                     for (int it = 0; it < LA::N; ++it)
                         if (it * NSUB / LA::N == s) {
-                            LA::store_item(ra, sa, tid, it);
-                            if constexpr (LOAD) LA::load_item(ra, Ab, lda, m0, k_load, tid, it);
+                            LA::store_item(rA, sa, tid, it);
+                            if constexpr (LOAD) LA::load_item(rA, Ab, lda, m0, k_load, tid, it);
                         }
                 } else {
-                    LA::store_rows(ra, sa, tid, s * 8 / NSUB, (s + 1) * 8 / NSUB);
-                    if constexpr (LOAD) if (s == NSUB - 1) LA::load(ra, Ab, lda, m0, k_load, tid);
+                    LA::store_rows(rA, sa, tid, s * 8 / NSUB, (s + 1) * 8 / NSUB);
+                    if constexpr (LOAD) if (s == NSUB - 1) LA::load(rA, Ab, lda, m0, k_load, tid);
                 }
                 if constexpr (SplitOf<LB>::value) {
 #pragma unroll
                     for (int it = 0; it < LB::N; ++it)
                         if (it * NSUB / LB::N == s) {
-                            LB::store_item(rb, sb, tid, it);
-                            if constexpr (LOAD) LB::load_item(rb, Bb, ldb, n0, k_load, tid, it);
+                            LB::store_item(rB, sb, tid, it);
+                            if constexpr (LOAD) LB::load_item(rB, Bb, ldb, n0, k_load, tid, it);
                         }
                 } else {
-                    LB::store_rows(rb, sb, tid, s * 8 / NSUB, (s + 1) * 8 / NSUB);
-                    if constexpr (LOAD) if (s == NSUB - 1) LB::load(rb, Bb, ldb, n0, k_load, tid);
+                    LB::store_rows(rB, sb, tid, s * 8 / NSUB, (s + 1) * 8 / NSUB);
+                    if constexpr (LOAD) if (s == NSUB - 1) LB::load(rB, Bb, ldb, n0, k_load, tid);
                 }
             }
         }
@@ -359,7 +365,57 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     using T_ = std::true_type;
     using F_ = std::false_type;
 
-    if (kbeg < kend) {
+    if (kbeg < kend && DEEP) {
+        // Step j computes LDS stage j & 1, stores staging set j & 1 (data of
+        // step j + 1) into the other stage and refills that set with the
+        // data of step j + 3 (clamped to the last K-step near the end: such
+        // loads are never stored).  Unrolled by two so the set is static.
+        const int nk = (kend - kbeg) / BK;
+        auto kat = [&](int j) { return kbeg + min(j, nk - 1) * BK; };
+        LA::load(ra, Ab, lda, m0, kbeg, tid);
+        LB::load(rb, Bb, ldb, n0, kbeg, tid);
+        LA::store(ra, sbase, tid);
+        LB::store(rb, sbase + BM * BK, tid);
+        LA::load(ra, Ab, lda, m0, kat(1), tid);
+        LB::load(rb, Bb, ldb, n0, kat(1), tid);
+        LA::load(ra2, Ab, lda, m0, kat(2), tid);
+        LB::load(rb2, Bb, ldb, n0, kat(2), tid);
+        auto step_plain = [&](int stage, int k_load, auto& rA, auto& rB, bool store, bool load) {
+            lds_barrier();
+            kstep32(F_{}, F_{}, stage, 0, rA, rB);
+            if (store) {
+                LA::store(rA, sbase + (stage ^ 1) * (BM + BN) * BK, tid);
+                LB::store(rB, sbase + (stage ^ 1) * (BM + BN) * BK + BM * BK, tid);
+                if (load) {
+                    LA::load(rA, Ab, lda, m0, k_load, tid);
+                    LB::load(rB, Bb, ldb, n0, k_load, tid);
+                }
+            }
+        };
+        int j = 0;
+        for (; j + 2 < nk; j += 2) {
+            if constexpr (LAYOUT == 0) {
+                lds_barrier();
+                kstep32(T_{}, T_{}, 0, kat(j + 3), ra, rb);
+                lds_barrier();
+                kstep32(T_{}, T_{}, 1, kat(j + 4), ra2, rb2);
+            } else {
+                step_plain(0, kat(j + 3), ra, rb, true, true);
+                step_plain(1, kat(j + 4), ra2, rb2, true, true);
+            }
+        }
+        if (j + 1 < nk) {
+            if constexpr (LAYOUT == 0) {
+                lds_barrier();
+                kstep32(T_{}, F_{}, 0, 0, ra, rb);
+            } else {
+                step_plain(0, 0, ra, rb, true, false);
+            }
+            ++j;
+        }
+        lds_barrier();
+        kstep32(F_{}, F_{}, j & 1, 0, ra, rb);
+    } else if (kbeg < kend) {
         LA::load(ra, Ab, lda, m0, kbeg, tid);
         LB::load(rb, Bb, ldb, n0, kbeg, tid);
         LA::store(ra, sbase, tid);
@@ -377,21 +433,21 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
             int k0 = kbeg;
             for (; k0 + 2 * BK < kend; k0 += BK, stage ^= 1) {
                 lds_barrier();
-                kstep32(T_{}, T_{}, stage, k0 + 2 * BK);
+                kstep32(T_{}, T_{}, stage, k0 + 2 * BK, ra, rb);
             }
             if (k0 + BK < kend) {
                 lds_barrier();
-                kstep32(T_{}, F_{}, stage, 0);
+                kstep32(T_{}, F_{}, stage, 0, ra, rb);
                 k0 += BK;
                 stage ^= 1;
             }
             lds_barrier();
-            kstep32(F_{}, F_{}, stage, 0);
+            kstep32(F_{}, F_{}, stage, 0, ra, rb);
         } else {
             for (int k0 = kbeg; k0 < kend; k0 += BK, stage ^= 1) {
                 lds_barrier();
                 if constexpr (MF == 16) compute16(stage);
-                else kstep32(F_{}, F_{}, stage, 0);
+                else kstep32(F_{}, F_{}, stage, 0, ra, rb);
                 if (k0 + BK < kend) {
                     LA::store(ra, sbase + (stage ^ 1) * (BM + BN) * BK, tid);
                     LB::store(rb, sbase + (stage ^ 1) * (BM + BN) * BK + BM * BK, tid);
@@ -437,6 +493,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
         const half_t* src = nullptr;
         const half_t* psi = nullptr;
         float* w = nullptr;
+        bool mirror = false;
         if constexpr (Epi::kind == EpiKind::Affine) {
             float mul = 1.f;
             if (mulz && epi.mul_pow > 0) {
@@ -447,21 +504,33 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
             cs = epi.cs * mul;
             out = epi.out + (int64_t)zo * epi.stride_out;
             src = epi.src ? epi.src + (int64_t)zo * epi.stride_src : nullptr;
-            if (sh.sym && tm != tn) {
-                // Transposed copy of an off-diagonal tile of a symmetric result,
-                // written from registers (4 consecutive halves per lane).
+            // Off-diagonal tiles of a symmetric result also write their
+            // transpose.  src is symmetric wherever the result is (A for
+            // B = b A + c A^2), so the transpose's src values are read from
+            // the transposed position too.  The 128 x 128 tile keeps its fp16
+            // results and transposes them through LDS after each pass; the
+            // 256 x 256 tile (no registers to spare) writes the transpose
+            // from its accumulators, 4 consecutive halves per lane.
+            mirror = sh.sym && tm != tn;
+            if constexpr (!kLdsMirror) {
+                if (mirror) {
 #pragma unroll
-                for (int qi = 0; qi < NQ; ++qi) {
-                    const int col = cw0 + quad_col(qi), row0 = rw0 + quad_row(qi);
-                    half_t hv[4];
+                    for (int qi = 0; qi < NQ; ++qi) {
+                        const int col = cw0 + quad_col(qi), row0 = rw0 + quad_row(qi);
+                        half_t sv[4] = {};
+                        if (src) *reinterpret_cast<u32x2*>(sv) =
+                                     *reinterpret_cast<const u32x2*>(src + (int64_t)col * epi.ld_src + row0);
+                        half_t hv[4];
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        float v = ca * quad_val(qi, r);
-                        if (src) v += cs * (float)src[(int64_t)(row0 + r) * epi.ld_src + col];
-                        hv[r] = (half_t)v;
+                        for (int r = 0; r < 4; ++r) {
+                            float v = ca * quad_val(qi, r);
+                            if (src) v += cs * (float)sv[r];
+                            hv[r] = (half_t)v;
+                        }
+                        // (A plain store: the 8-byte pieces merge in L2.)
+                        *reinterpret_cast<u32x2*>(out + (int64_t)col * epi.ld_out + row0) =
+                            *reinterpret_cast<const u32x2*>(hv);
                     }
-                    half_t* dst = out + (int64_t)col * epi.ld_out + row0;
-                    *reinterpret_cast<u32x2*>(dst) = *reinterpret_cast<const u32x2*>(hv);
                 }
             }
         } else {
@@ -554,7 +623,8 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
             }
             // Issue a batch of items' src loads before using any of them.
             constexpr int SB = ITEMS > 4 ? 4 : ITEMS;
-#pragma unroll 1
+            u32x4 hk[kLdsMirror ? ITEMS : 1];      // fp16 results, kept for the mirror
+#pragma unroll (kLdsMirror ? 8 : 1)
             for (int it0 = 0; it0 < ITEMS; it0 += SB) {
             u32x4 sbuf[SB];
             if constexpr (Epi::kind == EpiKind::Affine) {
@@ -591,9 +661,44 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                         const float q = (float)hv[e];
                         ss += q * q;
                     }
-                    *reinterpret_cast<u32x4*>(out + (int64_t)grow * epi.ld_out + gcol) = *reinterpret_cast<const u32x4*>(hv);
+                    // Streamed past L2 (nontemporal): the result is read by a
+                    // later launch, and keeping it out of L2 leaves the
+                    // operand panels resident.
+                    const u32x4 hq = *reinterpret_cast<const u32x4*>(hv);
+                    if constexpr (kLdsMirror) hk[it] = hq;
+                    __builtin_nontemporal_store(hq, reinterpret_cast<u32x4*>(out + (int64_t)grow * epi.ld_out + gcol));
                 }
             }
+            }
+            if constexpr (Epi::kind == EpiKind::Affine && kLdsMirror) {
+                if (mirror) {
+                    // T[c][r] = result[r][c] for this pass's TM rows: row c of
+                    // T holds TM halves in chunks of 8, chunk j stored at
+                    // j ^ (c / 8 mod TM / 8) so the 2-byte writes of one
+                    // wave spread over the banks; then 16-byte rows out.
+                    constexpr int R8 = TM / 8;
+                    half_t* tb = reinterpret_cast<half_t*>(smem);
+                    lds_barrier();
+#pragma unroll
+                    for (int it = 0; it < ITEMS; ++it) {
+                        const int c = tid + it * NT;
+                        if (c >= TM * C8) break;
+                        const int r = c / C8, c8 = (c - r * C8) * 8;
+                        const half_t* hv = reinterpret_cast<const half_t*>(&hk[it]);
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) {
+                            const int cc = c8 + e;
+                            tb[cc * TM + (((r >> 3) ^ ((cc >> 3) & (R8 - 1))) << 3) + (r & 7)] = hv[e];
+                        }
+                    }
+                    lds_barrier();
+                    for (int q = tid; q < BN * R8; q += NT) {
+                        const int cc = q / R8, j = q - cc * R8;
+                        const u32x4 v = *reinterpret_cast<const u32x4*>(tb + cc * TM + ((j ^ ((cc >> 3) & (R8 - 1))) << 3));
+                        __builtin_nontemporal_store(
+                            v, reinterpret_cast<u32x4*>(out + (int64_t)(n0 + cc) * epi.ld_out + m0 + pass * TM + 8 * j));
+                    }
+                }
             }
         }
         const bool want_sum = (Epi::kind == EpiKind::ApplyNorm) ||
