@@ -72,6 +72,13 @@ extern "C" {
 #define NORMPRE_ORIENT_ALTERNATING 0   /* k = t mod 2 (the paper's rule) */
 #define NORMPRE_ORIENT_ROW         1   /* always k = 0                  */
 #define NORMPRE_ORIENT_COL         2   /* always k = 1                  */
+/* Both axes every step (the "Row+Column/Step" orientation ablation, App. A.4,
+ * Table of ablations on the marginally normalized update, part (b)): the
+ * relaxed tangent and normalization act on the rows of W, then every column
+ * of the result is scaled to unit norm (zero columns stay zero); the
+ * preconditioner's active side is still k = t mod 2.  Rows must fit the
+ * row-active limit. */
+#define NORMPRE_ORIENT_BOTH        3
 
 /* ---- flags -------------------------------------------------------------- */
 /* Keep per-matrix intermediates of the last step for normpre_debug_fetch():
@@ -150,7 +157,8 @@ const char* normpre_last_error(const normpre_ctx* ctx);
  * 0..8, a non-finite or negative lr/weight decay, a non-finite momentum,
  * norm_eps <= 0, unknown orientation or flags, both tangent flags),
  * UNSUPPORTED (a dimension above 1 << 20 or a matrix above 2^31 elements;
- * in the row-active orientation a row longer than 32768 elements; for
+ * in the row-active or both-axes orientation a row longer than 32768
+ * elements; for
  * NormPre-L a sketch width l = min(active rows, r + o) above 384, or with
  * NORMPRE_FLAG_L_EXACT more than 384 active rows).
  */

@@ -55,7 +55,7 @@ class HParams:
     seed: int = 1337
     norm_eps: float = 1e-12
     ns_eps: float = 1e-7
-    orientation: str = "alternating"   # "alternating" | "row" | "col"
+    orientation: str = "alternating"   # "alternating" | "row" | "col" | "both" (App. A.4)
     tangent: str = "relaxed"           # "relaxed" (Sec. 3.1) | "none" | "strict" (App. A.4)
 
 
@@ -71,7 +71,10 @@ def momentum_update(m_prev: np.ndarray, g: np.ndarray, mu: float) -> np.ndarray:
 # Alg. 1 orientation: k_t = t mod 2, O_0(A) = A, O_1(A) = A^T  (Sec. 3.1)
 # --------------------------------------------------------------------------
 def orientation_of(t: int, mode: str = "alternating") -> int:
-    if mode == "alternating":
+    """Active side k of step t.  "both" normalizes rows and then columns every
+    step (the Row+Column/Step ablation of App. A.4); its preconditioner keeps
+    the alternating active side."""
+    if mode in ("alternating", "both"):
         return int(t) % 2
     if mode == "row":
         return 0
@@ -130,6 +133,16 @@ def momentum_processing(m_bar: np.ndarray, w_bar: np.ndarray, mode: str = "relax
 def diagonal_gram_normalize(x: np.ndarray, eps: float = 1e-12) -> np.ndarray:
     norms = np.sqrt(np.sum(x * x, axis=1))
     return x / np.maximum(norms, eps)[:, None]
+
+
+def both_axes_normalize(w: np.ndarray, m: np.ndarray, tangent: str = "relaxed",
+                        eps: float = 1e-12) -> np.ndarray:
+    """Row+Column/Step ablation (App. A.4, orientation table): the row-active
+    momentum processing and Eq. (2) on the rows of W, then Eq. (2) applied to
+    the columns of the result.  Reading: the second axis is a plain marginal
+    normalization (no second tangent step).  Returns Psi in the W layout."""
+    psi_rows = diagonal_gram_normalize(momentum_processing(m, w, tangent), eps)
+    return diagonal_gram_normalize(psi_rows.T, eps).T
 
 
 # --------------------------------------------------------------------------
@@ -336,9 +349,12 @@ def normpre_step(w, g, m_prev, t: int, hp: HParams, variant: str = "G",
     m_prev = np.asarray(m_prev, np.float64)
     m = momentum_update(m_prev, g, hp.momentum)
     k = orientation_of(t, hp.orientation)
-    w_bar, m_bar = orient(w, k), orient(m, k)
-    x = momentum_processing(m_bar, w_bar, hp.tangent)
-    psi = diagonal_gram_normalize(x, hp.norm_eps)
+    if hp.orientation == "both":
+        psi = orient(both_axes_normalize(w, m, hp.tangent, hp.norm_eps), k)
+    else:
+        w_bar, m_bar = orient(w, k), orient(m, k)
+        x = momentum_processing(m_bar, w_bar, hp.tangent)
+        psi = diagonal_gram_normalize(x, hp.norm_eps)
     out = {"k": k, "momentum": m, "psi": orient_inv(psi, k)}
     if variant == "NORM":
         t_act = psi

@@ -88,7 +88,7 @@ Fail validate(int variant, int num_mats, const int64_t* shapes, const normpre_hp
     if (!std::isfinite(hp->target_rms)) return {NORMPRE_ERR_INVALID_ARG, "target_rms must be finite"};
     if (!(hp->norm_eps > 0.f) || !std::isfinite(hp->norm_eps))
         return {NORMPRE_ERR_INVALID_ARG, "norm_eps must be finite and > 0"};
-    if (hp->orientation < 0 || hp->orientation > 2)
+    if (hp->orientation < NORMPRE_ORIENT_ALTERNATING || hp->orientation > NORMPRE_ORIENT_BOTH)
         return {NORMPRE_ERR_INVALID_ARG, fmt("unknown orientation mode %d", hp->orientation)};
     if (hp->flags & ~(NORMPRE_FLAG_DEBUG | NORMPRE_FLAG_TIME_KERNELS | NORMPRE_FLAG_TANGENT_NONE |
                       NORMPRE_FLAG_TANGENT_STRICT | NORMPRE_FLAG_L_EXACT))
@@ -117,7 +117,8 @@ Fail validate(int variant, int num_mats, const int64_t* shapes, const normpre_hp
             return {NORMPRE_ERR_INVALID_ARG, fmt("matrix %d has shape %lld x %lld", i, (long long)m, (long long)n)};
         if (m > kMaxDim || n > kMaxDim || m * n > kMaxElems)
             return {NORMPRE_ERR_UNSUPPORTED, fmt("matrix %d (%lld x %lld) is too large", i, (long long)m, (long long)n)};
-        if (k == 0 && n > kMaxRowLen && variant != NORMPRE_VARIANT_MUON)
+        const bool rows_pass = k == 0 || hp->orientation == NORMPRE_ORIENT_BOTH;
+        if (rows_pass && n > kMaxRowLen && variant != NORMPRE_VARIANT_MUON)
             return {NORMPRE_ERR_UNSUPPORTED,
                     fmt("matrix %d: row-active rows of %lld elements exceed %d", i, (long long)n, kMaxRowLen)};
         if (variant == NORMPRE_VARIANT_L) {
@@ -493,6 +494,9 @@ bool chunk_vec_ok(const PtrChunk& p, int cnt) {
 int run_normalize(const StepCtx& sc, const Dims& d, const GWork& w, const std::vector<int>& idx, int first,
                   int count, DebugMat* dbg) {
     const int64_t mn = d.mp * d.np_;
+    // Both axes: rows first, then the columns of the result (psisq then
+    // holds the squared column norms).
+    const bool both = sc.hp->orientation == NORMPRE_ORIENT_BOTH;
     const double bytes = 18.0 * (double)d.m * (double)d.n;
     for (int c0 = 0; c0 < count; c0 += kChunk) {
         const int cnt = std::min(kChunk, count - c0);
@@ -519,10 +523,22 @@ int run_normalize(const StepCtx& sc, const Dims& d, const GWork& w, const std::v
                 if (dbg[idx[first + c0 + i]].psi32 != a.psi32 + i * d.m * d.n) a.psi32 = nullptr;
             if (!a.psi32) return set_err(sc.ctx, NORMPRE_ERR_HIP, "internal: debug buffers not contiguous");
         }
-        if (d.k == 0) {
+        if (d.k == 0 || both) {
             NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NORMALIZE, 0.0, bytes * cnt,
                          [&] { return launch_normalize_rows(a, cnt, sc.s); }),
                    "normalize rows");
+            if (both)
+                NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NORMALIZE, 0.0, 6.0 * (double)d.m * (double)d.n * cnt,
+                             [&] {
+                                 return launch_psi_col_normalize(
+                                     a, cnt,
+                                     reinterpret_cast<float*>(
+                                         w.colpart +
+                                         (int64_t)c0 * normalize_cols_partials((int)d.m, (int)d.np_, kColRowChunk)),
+                                     2 * normalize_cols_partials((int)d.m, (int)d.np_, kColRowChunk), kColRowChunk,
+                                     sc.s);
+                             }),
+                       "normalize both axes");
         } else {
             NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NORMALIZE, 0.0, bytes * cnt,
                          [&] {
@@ -536,7 +552,8 @@ int run_normalize(const StepCtx& sc, const Dims& d, const GWork& w, const std::v
     }
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
                  [&] {
-                     return launch_psi_scale(w.psisq, d.lp_, (int)d.a, sc.hp->ns_eps, w.scale, count, sc.s);
+                     return launch_psi_scale(w.psisq, d.lp_, both ? (int)d.n : (int)d.a, sc.hp->ns_eps, w.scale,
+                                             count, sc.s);
                  }),
            "psi scale");
     return NORMPRE_OK;
@@ -1001,7 +1018,9 @@ int sketch_front(const StepCtx& sc, const Item& it, DebugMat* dbg) {
     // Alg. 2: Y = Psi Omega; p times Y <- Psi (Psi^T Y).  The fp16 copies of
     // Z and Y are scaled by powers of two (lambda_max <= tr Gamma <= a bounds
     // each product), which only rescales the spanned subspace.
-    const float sc_step = pow2_at_most_inv_sqrt(d.a);
+    // lambda_max(Gamma) <= tr Gamma = ||Psi||_F^2 <= a (n with both axes).
+    const float sc_step =
+        pow2_at_most_inv_sqrt(hp.orientation == NORMPRE_ORIENT_BOTH ? std::max(d.a, d.n) : d.a);
     const int p = power_iterations(hp);
     rc = sketch_product(sc, d, w, count, w.omega, true, w.v32[0], p > 0 ? w.v16[0] : nullptr, 1.f);
     if (rc) return rc;

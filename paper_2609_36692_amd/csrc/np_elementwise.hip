@@ -552,9 +552,75 @@ hipError_t launch_normalize_rows(const NormArgs& a, int batch, hipStream_t s) {
     return hipErrorInvalidValue;
 }
 
+// ------------------------------------- both axes: column pass over fp16 Psi --
+// Pass 1: partial sums of squares per (row chunk, column), fp32, fixed order.
+__global__ void __launch_bounds__(256) psi_colstats_kernel(const half_t* psi, int64_t ld, int64_t stride, int rows,
+                                                           int cols, int row_chunk, float* part, int64_t stride_part,
+                                                           int64_t cols_pad) {
+    const int z = blockIdx.z, chunk = blockIdx.y;
+    const int j = blockIdx.x * 256 + threadIdx.x;
+    if (j >= cols) return;
+    const half_t* p = psi + (int64_t)z * stride + j;
+    const int r0 = chunk * row_chunk, r1 = min(rows, r0 + row_chunk);
+    float s = 0.f;
+    for (int r = r0; r < r1; ++r) {
+        const float v = (float)p[(int64_t)r * ld];
+        s = fmaf(v, v, s);
+    }
+    part[(int64_t)z * stride_part + (int64_t)chunk * cols_pad + j] = s;
+}
+
+// Pass 2: per column f_j = 1 / max(||psi_j||, eps) and the new squared norm.
+__global__ void __launch_bounds__(256) psi_colfactor_kernel(float* part, int64_t stride_part, int nchunks, int cols,
+                                                            int64_t cols_pad, float eps, float* psisq,
+                                                            int64_t stride_psisq) {
+    const int z = blockIdx.y;
+    const int j = blockIdx.x * 256 + threadIdx.x;
+    if (j >= cols) return;
+    float* pz = part + (int64_t)z * stride_part;
+    float s = 0.f;
+    for (int c = 0; c < nchunks; ++c) s += pz[(int64_t)c * cols_pad + j];
+    const float f = 1.f / fmaxf(sqrtf(s), eps);
+    pz[(int64_t)nchunks * cols_pad + j] = f;
+    psisq[(int64_t)z * stride_psisq + j] = s * f * f;
+}
+
+// Pass 3: psi_ij *= f_j over the real region (fp16 and the fp32 debug copy).
+__global__ void __launch_bounds__(256) psi_colscale_kernel(half_t* psi, int64_t ld, int64_t stride, int rows,
+                                                           int cols, const float* part, int64_t stride_part,
+                                                           int nchunks, int64_t cols_pad, float* psi32,
+                                                           int64_t stride_psi32) {
+    const int z = blockIdx.y;
+    const float* f = part + (int64_t)z * stride_part + (int64_t)nchunks * cols_pad;
+    const int64_t total = (int64_t)rows * cols;
+    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
+        const int r = (int)(e / cols), j = (int)(e - (int64_t)r * cols);
+        half_t* q = psi + (int64_t)z * stride + (int64_t)r * ld + j;
+        *q = (half_t)((float)*q * f[j]);
+        if (psi32) psi32[(int64_t)z * stride_psi32 + e] *= f[j];
+    }
+}
+
 int64_t normalize_cols_partials(int rows, int cols_pad, int row_chunk) {
     const int nchunks = (rows + row_chunk - 1) / row_chunk;
     return (int64_t)nchunks * 3 * cols_pad;
+}
+
+hipError_t launch_psi_col_normalize(const NormArgs& a, int batch, float* part, int64_t part_floats, int row_chunk,
+                                    hipStream_t s) {
+    const int nchunks = (a.rows + row_chunk - 1) / row_chunk;
+    const int64_t cols_pad = a.ld_psi;
+    if ((int64_t)(nchunks + 1) * cols_pad > part_floats || a.cols > cols_pad) return hipErrorInvalidValue;
+    const unsigned cb = (unsigned)((a.cols + 255) / 256);
+    hipLaunchKernelGGL(psi_colstats_kernel, dim3(cb, nchunks, batch), dim3(256), 0, s, a.psi, a.ld_psi, a.stride_psi,
+                       a.rows, a.cols, row_chunk, part, part_floats, cols_pad);
+    hipLaunchKernelGGL(psi_colfactor_kernel, dim3(cb, batch), dim3(256), 0, s, part, part_floats, nchunks, a.cols,
+                       cols_pad, a.eps, a.psisq, a.stride_psisq);
+    const int64_t total = (int64_t)a.rows * a.cols;
+    const unsigned blocks = (unsigned)std::max<int64_t>(1, std::min<int64_t>((total + 255) / 256, 2048));
+    hipLaunchKernelGGL(psi_colscale_kernel, dim3(blocks, batch), dim3(256), 0, s, a.psi, a.ld_psi, a.stride_psi,
+                       a.rows, a.cols, part, part_floats, nchunks, cols_pad, a.psi32, a.stride_psi32);
+    return hipGetLastError();
 }
 
 template <int VW>

@@ -146,6 +146,12 @@ hipError_t launch_normalize_rows(const NormArgs& a, int batch, hipStream_t s);
 hipError_t launch_normalize_cols(const NormArgs& a, int batch, double* partials,
                                  int row_chunk, hipStream_t s);
 int64_t normalize_cols_partials(int rows, int cols_pad, int row_chunk);
+// Both-axes normalization, second half: every column of the fp16 Psi (and of
+// the fp32 debug copy) scaled to unit norm, zero columns kept at zero; the
+// squared column norms go to psisq.  `part` holds part_floats floats per
+// matrix (row-chunk partial sums, then the column factors).
+hipError_t launch_psi_col_normalize(const NormArgs& a, int batch, float* part, int64_t part_floats, int row_chunk,
+                                    hipStream_t s);
 
 // out[z] = sum_i in[z*n + i] in a fixed order (per-matrix ||T||_F^2 from
 // per-tile partial sums).

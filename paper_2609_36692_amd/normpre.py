@@ -32,6 +32,7 @@ VARIANTS = {"G": NORMPRE_VARIANT_G, "L": NORMPRE_VARIANT_L, "MUON": NORMPRE_VARI
 NORMPRE_ORIENT_ALTERNATING = 0
 NORMPRE_ORIENT_ROW = 1
 NORMPRE_ORIENT_COL = 2
+NORMPRE_ORIENT_BOTH = 3
 NORMPRE_FLAG_DEBUG = 1
 NORMPRE_FLAG_TIME_KERNELS = 2
 NORMPRE_FLAG_TANGENT_NONE = 4

@@ -293,6 +293,28 @@ def test_tangent_modes(ctx, variant, mode, t):
     assert err < tol
 
 
+@pytest.mark.parametrize("variant", ["G", "L", "NORM"])
+@pytest.mark.parametrize("shape", [(257, 513), (300, 200), (768, 2304), (3072, 768)])
+@pytest.mark.parametrize("t", [0, 1])
+def test_both_axes_orientation(ctx, variant, shape, t):
+    _say(f"both axes {variant} shape={shape} t={t}")
+    mat = _inputs(shape, "lowrank", seed=9)
+    res = run_step(ctx, variant, [mat], t, orientation=N.NORMPRE_ORIENT_BOTH)[0]
+    ref = oracle(mat, variant, t, orientation="both")
+    psi = N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_PSI, shape[0] * shape[1]).reshape(shape)
+    # The column norms come from the fp16 row-normalized Psi: each column
+    # scale carries about 2^-10 / sqrt(rows) relative error on top of the fp32
+    # normalization bound.
+    tol_psi = TOL_PSI + 2.0 ** -10 / math.sqrt(shape[0])
+    assert O.relative_fro(psi, ref["psi"]) < tol_psi
+    assert np.allclose(np.linalg.norm(psi.astype(np.float64), axis=0), 1.0, atol=2e-3)
+    assert int(N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_ORIENT, 1, np.int32)[0]) == t % 2
+    tol = {"G": TOL_G, "NORM": TOL_NORM}.get(variant) or tol_l(ref)
+    err = O.relative_fro(res["u"], ref["update"])
+    _say(f"  update err {err:.2e} (tol {tol:.1e})")
+    assert err < tol
+
+
 @pytest.mark.parametrize("variant", ["MUON", "NORM"])
 def test_reference_steps_zero_signal(ctx, variant):
     shape = (300, 200)

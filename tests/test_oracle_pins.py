@@ -333,6 +333,39 @@ def test_scale_and_row_permutation(variant):
     assert np.allclose(base[perm], permuted, atol=1e-11)
 
 
+def test_both_axes_rank_one_closed_form():
+    # W = 0 makes the relaxed tangent the identity (X = M).  For M = a b^T the
+    # row pass gives sign(a_i) b / ||b||, and the column pass then scales each
+    # column to unit norm: Psi_ij = sign(a_i) sign(b_j) / sqrt(m).
+    m, n = 7, 11
+    a = RNG.standard_normal(m)
+    b = RNG.standard_normal(n)
+    w = np.zeros((m, n))
+    g = np.outer(a, b)
+    hp = O.HParams(orientation="both")
+    for t in (0, 1):
+        out = O.normpre_step(w, g, np.zeros((m, n)), t, hp, "NORM")
+        assert out["k"] == t % 2
+        expect = np.outer(np.sign(a), np.sign(b)) / math.sqrt(m)
+        assert np.allclose(out["psi"], expect, atol=1e-14)
+
+
+def test_both_axes_unit_columns_and_preconditioner_side():
+    w, g, mp = _rand(9, 14), _rand(9, 14), _rand(9, 14)
+    hp = O.HParams(orientation="both", rank=3)
+    r0 = O.normpre_step(w, g, mp, 0, hp, "L")
+    r1 = O.normpre_step(w, g, mp, 1, hp, "L")
+    # the same Psi for both parities, every column of unit norm
+    assert np.allclose(r0["psi"], r1["psi"], atol=1e-15)
+    assert np.allclose(np.linalg.norm(r0["psi"], axis=0), 1.0)
+    # the localized preconditioner acts on rows for t even, on columns for t odd
+    assert r0["k"] == 0 and r1["k"] == 1
+    assert r0["ell"] == min(9, 3 + 8) and r1["ell"] == min(14, 3 + 8)
+    # it differs from row-only normalization (the column pass took effect)
+    row = O.normpre_step(w, g, mp, 0, O.HParams(orientation="row", rank=3), "L")
+    assert O.relative_fro(row["psi"], r0["psi"]) > 1e-3
+
+
 def test_orientation_alternates_with_t():
     hp = O.HParams()
     w, g, mp = _rand(5, 8), _rand(5, 8), _rand(5, 8)
