@@ -103,6 +103,14 @@ extern "C" {
  * all of range(Psi), so the Rayleigh-Ritz pairs are the exact nonzero
  * eigenpairs of Gamma.  Needs a <= 384 (else UNSUPPORTED); NormPre-L only. */
 #define NORMPRE_FLAG_L_EXACT       16u
+/* Interaction-source ablation (App. A.4, "Ablations on Interaction Geometry
+ * Source"): NormPre-L builds its preconditioner from the update before
+ * normalization, through the trace-matched Gram G_X = d X X^T / tr(X X^T)
+ * (d = active rows; App. A, spectral dynamics), and applies it to the same
+ * normalized Psi: T = Psi + U_C (Lambda_C^{-1/2} - I) U_C^T Psi with
+ * (U_C, Lambda_C) from G_X (sketched, or exact with NORMPRE_FLAG_L_EXACT).
+ * NormPre-L only, not with NORMPRE_ORIENT_BOTH (INVALID_ARG). */
+#define NORMPRE_FLAG_SOURCE_X      32u
 
 /*
  * Hyper-parameters of one step.  Defaults (normpre_default_hparams) follow

@@ -57,6 +57,7 @@ class HParams:
     ns_eps: float = 1e-7
     orientation: str = "alternating"   # "alternating" | "row" | "col" | "both" (App. A.4)
     tangent: str = "relaxed"           # "relaxed" (Sec. 3.1) | "none" | "strict" (App. A.4)
+    source: str = "psi"                # NormPre-L interaction source: "psi" | "x" (App. A.4)
 
 
 # --------------------------------------------------------------------------
@@ -133,6 +134,13 @@ def momentum_processing(m_bar: np.ndarray, w_bar: np.ndarray, mode: str = "relax
 def diagonal_gram_normalize(x: np.ndarray, eps: float = 1e-12) -> np.ndarray:
     norms = np.sqrt(np.sum(x * x, axis=1))
     return x / np.maximum(norms, eps)[:, None]
+
+
+def interaction_source_x(x: np.ndarray) -> np.ndarray:
+    """X_s = sqrt(d / tr(X X^T)) X, so that X_s X_s^T is the trace-matched Gram
+    G_X of App. A (d = active rows); zero X gives zero."""
+    tot = float(np.sum(x * x))
+    return x * math.sqrt(x.shape[0] / tot) if tot > 0 else np.zeros_like(x)
 
 
 def both_axes_normalize(w: np.ndarray, m: np.ndarray, tangent: str = "relaxed",
@@ -349,6 +357,7 @@ def normpre_step(w, g, m_prev, t: int, hp: HParams, variant: str = "G",
     m_prev = np.asarray(m_prev, np.float64)
     m = momentum_update(m_prev, g, hp.momentum)
     k = orientation_of(t, hp.orientation)
+    x = None
     if hp.orientation == "both":
         psi = orient(both_axes_normalize(w, m, hp.tangent, hp.norm_eps), k)
     else:
@@ -363,13 +372,22 @@ def normpre_step(w, g, m_prev, t: int, hp: HParams, variant: str = "G",
     elif variant == "L":
         a, b = psi.shape
         ell = min(a, hp.rank + hp.oversample)
+        # Interaction source (App. A.4): the eigenpairs come from Psi, or from
+        # the update before normalization through its trace-matched Gram
+        # G_X = a X X^T / tr(X X^T) (App. A); either way they act on Psi.
+        if hp.source == "psi":
+            src = psi
+        elif hp.source == "x" and x is not None:
+            src = interaction_source_x(x)
+        else:
+            raise ValueError(f"interaction source {hp.source!r} with orientation {hp.orientation!r}")
         if l_mode == "exact":
-            u_sel, lam_sel = localized_exact(psi, hp.rank)
+            u_sel, lam_sel = localized_exact(src, hp.rank)
             out["lam_sel"] = lam_sel
         else:
             if omega is None:
                 omega = sketch_omega(hp.seed, t, matrix_id, b, ell)
-            sk = interaction_sketch(psi, hp.rank, hp.oversample, hp.power_iters,
+            sk = interaction_sketch(src, hp.rank, hp.oversample, hp.power_iters,
                                     omega, force_count)
             u_sel, lam_sel = sk.u_sel, sk.lam_sel
             out.update(ell=sk.ell, ritz_values=sk.ritz_values,

@@ -91,12 +91,16 @@ Fail validate(int variant, int num_mats, const int64_t* shapes, const normpre_hp
     if (hp->orientation < NORMPRE_ORIENT_ALTERNATING || hp->orientation > NORMPRE_ORIENT_BOTH)
         return {NORMPRE_ERR_INVALID_ARG, fmt("unknown orientation mode %d", hp->orientation)};
     if (hp->flags & ~(NORMPRE_FLAG_DEBUG | NORMPRE_FLAG_TIME_KERNELS | NORMPRE_FLAG_TANGENT_NONE |
-                      NORMPRE_FLAG_TANGENT_STRICT | NORMPRE_FLAG_L_EXACT))
+                      NORMPRE_FLAG_TANGENT_STRICT | NORMPRE_FLAG_L_EXACT | NORMPRE_FLAG_SOURCE_X))
         return {NORMPRE_ERR_INVALID_ARG, fmt("unknown flags 0x%x", hp->flags)};
     if ((hp->flags & NORMPRE_FLAG_TANGENT_NONE) && (hp->flags & NORMPRE_FLAG_TANGENT_STRICT))
         return {NORMPRE_ERR_INVALID_ARG, "at most one tangent mode flag"};
     if ((hp->flags & NORMPRE_FLAG_L_EXACT) && variant != NORMPRE_VARIANT_L)
         return {NORMPRE_ERR_INVALID_ARG, "NORMPRE_FLAG_L_EXACT applies to NormPre-L only"};
+    if ((hp->flags & NORMPRE_FLAG_SOURCE_X) && variant != NORMPRE_VARIANT_L)
+        return {NORMPRE_ERR_INVALID_ARG, "NORMPRE_FLAG_SOURCE_X applies to NormPre-L only"};
+    if ((hp->flags & NORMPRE_FLAG_SOURCE_X) && hp->orientation == NORMPRE_ORIENT_BOTH)
+        return {NORMPRE_ERR_INVALID_ARG, "NORMPRE_FLAG_SOURCE_X needs a single active side"};
     if (variant == NORMPRE_VARIANT_G || variant == NORMPRE_VARIANT_MUON) {
         if (hp->ns_iters < 1 || hp->ns_iters > 64)
             return {NORMPRE_ERR_INVALID_ARG, fmt("ns_iters %d outside 1..64", hp->ns_iters)};
@@ -262,6 +266,11 @@ struct Group {
 struct GWork {
     // shared
     half_t* psi;
+    // L with the interaction source X: trace-matched X (fp16, W layout),
+    // the active rows' ||x_i||^2 and the per-matrix sum (2 floats).
+    half_t* xs;
+    float* xsq;
+    float* xtot;
     float* psisq;
     float* scale;
     double* colpart;
@@ -368,7 +377,7 @@ struct Pool {
     int* nsel = nullptr;
 };
 
-void carve_item(Arena& ar, Item& it, int variant) {
+void carve_item(Arena& ar, Item& it, int variant, bool source_x) {
     const Dims& d = it.d;
     const int count = it.count;
     GWork& w = it.w;
@@ -393,6 +402,11 @@ void carve_item(Arena& ar, Item& it, int variant) {
         w.part = ar.take<float>(count * (int64_t)kMaxSplits * lp * maxpad);
         w.qlen = ar.take<half_t>(count * d.a_pad * lp);
         w.flen = ar.take<half_t>(count * d.b_pad * lp);
+        if (source_x) {
+            w.xs = ar.take<half_t>(count * mn);
+            w.xsq = ar.take<float>(count * d.lp_);
+            w.xtot = ar.take<float>(count * 2);
+        }
     }
 }
 
@@ -439,16 +453,16 @@ std::vector<Pool> make_pools(std::vector<Item>& items, int variant) {
 }
 
 // Carves a round's items and pools; with a null arena base it only measures.
-size_t carve_round(Arena& ar, std::vector<Item>& items, std::vector<Pool>& pools, int variant) {
-    for (Item& it : items) carve_item(ar, it, variant);
+size_t carve_round(Arena& ar, std::vector<Item>& items, std::vector<Pool>& pools, int variant, bool source_x) {
+    for (Item& it : items) carve_item(ar, it, variant, source_x);
     for (Pool& p : pools) carve_pool(ar, p, variant);
     return ar.off + 256;
 }
 
-size_t round_bytes(std::vector<Item> items, int variant) {
+size_t round_bytes(std::vector<Item> items, int variant, bool source_x) {
     std::vector<Pool> pools = make_pools(items, variant);
     Arena ar{nullptr, 0, 0};
-    return carve_round(ar, items, pools, variant);
+    return carve_round(ar, items, pools, variant, source_x);
 }
 
 struct StepCtx {
@@ -514,6 +528,7 @@ int run_normalize(const StepCtx& sc, const Dims& d, const GWork& w, const std::v
         a.eps = sc.hp->norm_eps;
         a.vec_ok = chunk_vec_ok(a.ptrs, cnt);
         a.tangent = tangent_mode(*sc.hp);
+        if (w.xsq) a.xsq = w.xsq + (int64_t)c0 * d.lp_;
         if (dbg) {
             // Debug copies are written chunk by chunk into per-matrix buffers
             // that are contiguous in the order of the caller's list.
@@ -556,6 +571,19 @@ int run_normalize(const StepCtx& sc, const Dims& d, const GWork& w, const std::v
                                              count, sc.s);
                  }),
            "psi scale");
+    if (w.xs) {
+        // Interaction source X: X_s = sqrt(a / ||X||_F^2) D Psi, so that
+        // X_s X_s^T is the trace-matched Gram of the active rows.
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+                     [&] { return launch_psi_scale(w.xsq, d.lp_, (int)d.a, 0.f, w.xtot, count, sc.s); }),
+               "x norm");
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NORMALIZE, 0.0, 4.0 * (double)d.mp * (double)d.np_ * count,
+                     [&] {
+                         return launch_source_x(w.psi, d.np_, mn, (int)d.m, (int)d.n, (int)d.mp, d.k, (int)d.a,
+                                                w.xsq, d.lp_, w.xtot, w.xs, count, sc.s);
+                     }),
+               "source x");
+    }
     return NORMPRE_OK;
 }
 
@@ -841,7 +869,7 @@ int run_round_g(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& 
 // out_over_active = true gives (Psi V)^T (ell_pad x a_pad), false gives
 // (Psi^T V)^T (ell_pad x b_pad).  Writes fp32 and/or scaled fp16 results.
 int sketch_product(const StepCtx& sc, const Dims& d, const GWork& w, int count, const half_t* v16, bool over_active,
-                   float* out32, half_t* out16, float scale16) {
+                   float* out32, half_t* out16, float scale16, const half_t* src = nullptr) {
     const int64_t mn = d.mp * d.np_, lp = d.ellp, maxpad = d.lp_;
     // PV: out over the rows of the W-layout Psi; PtV: over its columns.
     const bool pv = over_active == (d.k == 0);
@@ -854,7 +882,7 @@ int sketch_product(const StepCtx& sc, const Dims& d, const GWork& w, int count, 
     const int64_t k_chunk = round_up((k_len + splits - 1) / splits, 64);
     const int real_splits = (int)((k_len + k_chunk - 1) / k_chunk);
     Operand A{v16, k_len, lp * maxpad};
-    Operand B{w.psi, d.np_, mn};
+    Operand B{src ? src : w.psi, d.np_, mn};
     GemmShape sh{(int)lp, (int)n_out, (int)k_len, real_splits, (int)k_chunk, 0};
     EpiPartial e{};
     e.out = w.part;
@@ -875,8 +903,6 @@ int sketch_product(const StepCtx& sc, const Dims& d, const GWork& w, int count, 
     return NORMPRE_OK;
 }
 
-// fp64 Gram of an item's l-major fp32 matrix V (ell_pad x len) into its slots
-// of the pool's partials (always kGramChunks chunk slots per matrix).
 // The items of each pool in pool order, in runs of at most kMaxItems (one
 // grouped launch each); their matrices are contiguous in the pool buffers.
 std::vector<std::vector<const Item*>> pool_runs(const std::vector<Item>& items, const std::vector<Pool>& pools) {
@@ -1022,12 +1048,15 @@ int sketch_front(const StepCtx& sc, const Item& it, DebugMat* dbg) {
     const float sc_step =
         pow2_at_most_inv_sqrt(hp.orientation == NORMPRE_ORIENT_BOTH ? std::max(d.a, d.n) : d.a);
     const int p = power_iterations(hp);
-    rc = sketch_product(sc, d, w, count, w.omega, true, w.v32[0], p > 0 ? w.v16[0] : nullptr, 1.f);
+    // The candidate subspace comes from the interaction source: Psi, or the
+    // trace-matched X (NORMPRE_FLAG_SOURCE_X).
+    const half_t* src = w.xs;
+    rc = sketch_product(sc, d, w, count, w.omega, true, w.v32[0], p > 0 ? w.v16[0] : nullptr, 1.f, src);
     if (rc) return rc;
     for (int i = 0; i < p; ++i) {
-        rc = sketch_product(sc, d, w, count, w.v16[0], false, nullptr, w.v16[1], sc_step);
+        rc = sketch_product(sc, d, w, count, w.v16[0], false, nullptr, w.v16[1], sc_step, src);
         if (rc) return rc;
-        rc = sketch_product(sc, d, w, count, w.v16[1], true, w.v32[0], i + 1 < p ? w.v16[0] : nullptr, sc_step);
+        rc = sketch_product(sc, d, w, count, w.v16[1], true, w.v32[0], i + 1 < p ? w.v16[0] : nullptr, sc_step, src);
         if (rc) return rc;
     }
     return NORMPRE_OK;
@@ -1102,9 +1131,10 @@ int run_round_l(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& 
     if (rc) return rc;
     rc = cholqr_round(sc, items, pools, true);
     if (rc) return rc;
-    // B = Q^T Psi (ell_pad x b_pad) per item, Gamma_Q = B B^T per pool.
+    // B = Q^T Psi (ell_pad x b_pad) per item, Gamma_Q = B B^T per pool
+    // (B = Q^T X_s with the interaction source X).
     for (const Item& it : items) {
-        rc = sketch_product(sc, it.d, it.w, it.count, it.w.v16[0], false, it.w.v32[0], nullptr, 1.f);
+        rc = sketch_product(sc, it.d, it.w, it.count, it.w.v16[0], false, it.w.v32[0], nullptr, 1.f, it.w.xs);
         if (rc) return rc;
     }
     const auto runs = pool_runs(items, pools);
@@ -1125,6 +1155,13 @@ int run_round_l(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& 
         ea.max_sweeps = kEigSweeps;
         NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_eig_select(ea, pl.count, sc.s); }),
                "eigensolver");
+    }
+    // With the interaction source X the preconditioner still acts on Psi:
+    // B = Q^T Psi for the apply.
+    for (const Item& it : items) {
+        if (!it.w.xs) continue;
+        rc = sketch_product(sc, it.d, it.w, it.count, it.w.v16[0], false, it.w.v32[0], nullptr, 1.f);
+        if (rc) return rc;
     }
     // F = B^T K (b_pad x ell_pad, fp16), one launch per pool.
     for (const auto& run : runs) {
@@ -1337,6 +1374,7 @@ int normpre_step(normpre_ctx* ctx, int variant, int num_mats, float* const* para
     hipStream_t s = static_cast<hipStream_t>(stream);
 
     const int k = step_orientation(variant, *hp);
+    const bool source_x = variant == NORMPRE_VARIANT_L && (hp->flags & NORMPRE_FLAG_SOURCE_X) != 0;
     // Group equal shapes (first-appearance order) so each group is one batch.
     std::vector<Group> groups;
     {
@@ -1361,7 +1399,7 @@ int normpre_step(normpre_ctx* ctx, int variant, int num_mats, float* const* para
         one.g = (int)g;
         one.count = 1;
         one.d = d;
-        const size_t per = round_bytes({one}, variant);
+        const size_t per = round_bytes({one}, variant, source_x);
         const int b = (int)std::max<size_t>(1, std::min<size_t>((size_t)cnt, kGroupBudget / std::max<size_t>(per, 1)));
         for (int first = 0; first < cnt; first += b) {
             Item it;
@@ -1380,7 +1418,7 @@ int normpre_step(normpre_ctx* ctx, int variant, int num_mats, float* const* para
         if (!rounds.empty()) {
             std::vector<Item> trial = rounds.back();
             trial.push_back(it);
-            const size_t bytes = round_bytes(trial, variant);
+            const size_t bytes = round_bytes(trial, variant, source_x);
             if (bytes <= kRoundBudget) {
                 rounds.back().push_back(it);
                 need = std::max(need, bytes);
@@ -1388,7 +1426,7 @@ int normpre_step(normpre_ctx* ctx, int variant, int num_mats, float* const* para
             }
         }
         rounds.push_back({it});
-        need = std::max(need, round_bytes(rounds.back(), variant));
+        need = std::max(need, round_bytes(rounds.back(), variant, source_x));
     }
     rc = ensure_workspace(ctx, need, s);
     if (rc) return rc;
@@ -1405,7 +1443,7 @@ int normpre_step(normpre_ctx* ctx, int variant, int num_mats, float* const* para
     for (std::vector<Item>& items : rounds) {
         std::vector<Pool> pools = make_pools(items, variant);
         Arena ar{static_cast<char*>(ctx->ws), 0, ctx->ws_bytes};
-        carve_round(ar, items, pools, variant);
+        carve_round(ar, items, pools, variant, source_x);
         DebugMat* dbg = debug ? ctx->dbg.data() : nullptr;
         rc = variant == NORMPRE_VARIANT_L ? run_round_l(sc, items, pools, dbg) : run_round_g(sc, items, pools, dbg);
         if (rc) return rc;

@@ -127,7 +127,10 @@ __global__ void __launch_bounds__(NT) normalize_rows_kernel(NormArgs a) {
         }
     }
     for (int64_t j = a.cols + tid; j < a.ld_psi; j += NT) prow[j] = (half_t)0.f;
-    if (tid == 0) a.psisq[(int64_t)z * a.stride_psisq + row] = (float)(nrm2 * (double)inv * (double)inv);
+    if (tid == 0) {
+        a.psisq[(int64_t)z * a.stride_psisq + row] = (float)(nrm2 * (double)inv * (double)inv);
+        if (a.xsq) a.xsq[(int64_t)z * a.stride_psisq + row] = (float)nrm2;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -213,7 +216,10 @@ __global__ void __launch_bounds__(256) normalize_rows_wave_kernel(NormArgs a) {
     } else {
         for (int64_t j = a.cols + lane; j < a.ld_psi; j += 64) prow[j] = (half_t)0.f;
     }
-    if (lane == 0) a.psisq[(int64_t)z * a.stride_psisq + row] = (float)(nrm2 * (double)inv * (double)inv);
+    if (lane == 0) {
+        a.psisq[(int64_t)z * a.stride_psisq + row] = (float)(nrm2 * (double)inv * (double)inv);
+        if (a.xsq) a.xsq[(int64_t)z * a.stride_psisq + row] = (float)nrm2;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -302,6 +308,7 @@ __global__ void __launch_bounds__(256) normalize_cols_finalize(NormArgs a, doubl
     p[col] = d;
     p[cols_pad + col] = inv;
     a.psisq[(int64_t)z * a.stride_psisq + col] = (float)(nrm2 * inv * inv);
+    if (a.xsq) a.xsq[(int64_t)z * a.stride_psisq + col] = (float)nrm2;
 }
 
 template <int VW, bool DBG>
@@ -552,6 +559,28 @@ hipError_t launch_normalize_rows(const NormArgs& a, int batch, hipStream_t s) {
     return hipErrorInvalidValue;
 }
 
+// ------------------------------------------ interaction source X (L only) --
+// X_s = c D Psi with c = sqrt(a / ||X||_F^2): recovers the update before
+// normalization from Psi and the active norms, trace-matched so that
+// X_s X_s^T has trace a.  Covers the padded W layout (zeros there).
+__global__ void __launch_bounds__(256) source_x_kernel(const half_t* psi, int64_t ld, int64_t stride, int rows,
+                                                       int cols, int rows_pad, int k, int active, const float* xsq,
+                                                       int64_t stride_xsq, const float* xtot, half_t* xs) {
+    const int z = blockIdx.y;
+    const float tot = xtot[2 * z + 1];
+    const float c = tot > 0.f ? sqrtf((float)active / tot) : 0.f;
+    const float* q = xsq + (int64_t)z * stride_xsq;
+    const int64_t total = (int64_t)rows_pad * ld;
+    const half_t* p = psi + (int64_t)z * stride;
+    half_t* o = xs + (int64_t)z * stride;
+    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
+        const int r = (int)(e / ld), j = (int)(e - (int64_t)r * ld);
+        float v = 0.f;
+        if (r < rows && j < cols) v = (float)p[e] * c * sqrtf(q[k == 0 ? r : j]);
+        o[e] = (half_t)v;
+    }
+}
+
 // ------------------------------------- both axes: column pass over fp16 Psi --
 // Pass 1: partial sums of squares per (row chunk, column), fp32, fixed order.
 __global__ void __launch_bounds__(256) psi_colstats_kernel(const half_t* psi, int64_t ld, int64_t stride, int rows,
@@ -604,6 +633,16 @@ __global__ void __launch_bounds__(256) psi_colscale_kernel(half_t* psi, int64_t 
 int64_t normalize_cols_partials(int rows, int cols_pad, int row_chunk) {
     const int nchunks = (rows + row_chunk - 1) / row_chunk;
     return (int64_t)nchunks * 3 * cols_pad;
+}
+
+hipError_t launch_source_x(const half_t* psi, int64_t ld, int64_t stride, int rows, int cols, int rows_pad, int k,
+                           int active, const float* xsq, int64_t stride_xsq, const float* xtot, half_t* xs,
+                           int batch, hipStream_t s) {
+    const int64_t total = (int64_t)rows_pad * ld;
+    const unsigned blocks = (unsigned)std::max<int64_t>(1, std::min<int64_t>((total + 255) / 256, 2048));
+    hipLaunchKernelGGL(source_x_kernel, dim3(blocks, batch), dim3(256), 0, s, psi, ld, stride, rows, cols, rows_pad,
+                       k, active, xsq, stride_xsq, xtot, xs);
+    return hipGetLastError();
 }
 
 hipError_t launch_psi_col_normalize(const NormArgs& a, int batch, float* part, int64_t part_floats, int row_chunk,

@@ -139,6 +139,7 @@ struct NormArgs {
     float mu, eps;
     int vec_ok;                     // 16-byte aligned W, M, G rows
     int tangent;                    // kTangentRelaxed / kTangentNone / kTangentStrict
+    float* xsq;                     // optional per active row ||x_i||^2 (stride_psisq)
 };
 constexpr int kTangentRelaxed = 0, kTangentNone = 1, kTangentStrict = 2;
 hipError_t launch_normalize_rows(const NormArgs& a, int batch, hipStream_t s);
@@ -150,6 +151,12 @@ int64_t normalize_cols_partials(int rows, int cols_pad, int row_chunk);
 // the fp32 debug copy) scaled to unit norm, zero columns kept at zero; the
 // squared column norms go to psisq.  `part` holds part_floats floats per
 // matrix (row-chunk partial sums, then the column factors).
+// X_s = sqrt(a / tot) D Psi over the padded W layout (zero padding kept):
+// D = diag(||x_i||) of the active rows (rows for k = 0, columns for k = 1),
+// tot = xtot[2 z + 1] = ||X||_F^2.
+hipError_t launch_source_x(const half_t* psi, int64_t ld, int64_t stride, int rows, int cols, int rows_pad, int k,
+                           int active, const float* xsq, int64_t stride_xsq, const float* xtot, half_t* xs,
+                           int batch, hipStream_t s);
 hipError_t launch_psi_col_normalize(const NormArgs& a, int batch, float* part, int64_t part_floats, int row_chunk,
                                     hipStream_t s);
 

@@ -38,6 +38,7 @@ NORMPRE_FLAG_TIME_KERNELS = 2
 NORMPRE_FLAG_TANGENT_NONE = 4
 NORMPRE_FLAG_TANGENT_STRICT = 8
 NORMPRE_FLAG_L_EXACT = 16
+NORMPRE_FLAG_SOURCE_X = 32
 
 NORMPRE_DEBUG_PSI = 0
 NORMPRE_DEBUG_T = 1

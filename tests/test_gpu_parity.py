@@ -315,6 +315,30 @@ def test_both_axes_orientation(ctx, variant, shape, t):
     assert err < tol
 
 
+@pytest.mark.parametrize("shape,t,exact", [((257, 513), 0, False), ((257, 513), 1, False), ((768, 2304), 0, False),
+                                           ((3072, 768), 1, False), ((300, 200), 0, True), ((1000, 300), 1, True)])
+def test_source_x_matches_oracle(ctx, shape, t, exact):
+    _say(f"source X shape={shape} t={t} exact={exact}")
+    w, g, mp = _inputs(shape, "lowrank", seed=11)
+    # unequal row and column scales so that X and Psi give different spectra
+    g = g * torch.linspace(0.2, 4.0, shape[0])[:, None] * torch.linspace(0.5, 2.0, shape[1])[None, :]
+    mat = (w, g, mp)
+    flags = N.NORMPRE_FLAG_DEBUG | N.NORMPRE_FLAG_SOURCE_X | (N.NORMPRE_FLAG_L_EXACT if exact else 0)
+    res = run_step(ctx, "L", [mat], t, flags=flags, rank=16)[0]
+    ref = oracle(mat, "L", t, rank=16, source="x", l_mode="exact" if exact else "sketch")
+    base = oracle(mat, "L", t, rank=16, l_mode="exact" if exact else "sketch")
+    assert O.relative_fro(ref["update"], base["update"]) > 1e-2   # the source matters here
+    if exact:
+        lam_sel = ref["lam_sel"]
+        kappa = math.sqrt(float(np.sum(lam_sel))) / max(np.linalg.norm(ref["t"]), 1e-300)
+        tol = max(TOL_L, 8.0 * U16 * kappa)
+    else:
+        tol = tol_l(ref)
+    err = O.relative_fro(res["u"], ref["update"])
+    _say(f"  update err {err:.2e} (tol {tol:.1e})")
+    assert err < tol
+
+
 @pytest.mark.parametrize("variant", ["MUON", "NORM"])
 def test_reference_steps_zero_signal(ctx, variant):
     shape = (300, 200)

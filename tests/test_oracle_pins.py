@@ -366,6 +366,47 @@ def test_both_axes_unit_columns_and_preconditioner_side():
     assert O.relative_fro(row["psi"], r0["psi"]) > 1e-3
 
 
+def test_source_x_orthogonal_rows_closed_form():
+    # App. A's worked example: mutually orthogonal rows with norms a_i have a
+    # diagonal trace-matched Gram with eigenvalues d a_i^2 / sum_j a_j^2.  With
+    # the interaction source X the exact localized step then scales each
+    # selected row of Psi (a unit row) by lambda_i^{-1/2} and leaves the rest.
+    d, n = 6, 10
+    q, _ = np.linalg.qr(RNG.standard_normal((n, d)))
+    norms = np.array([5.0, 0.5, 3.0, 1.0, 0.2, 2.5])
+    x = (q.T * norms[:, None])                       # orthogonal rows
+    w = np.zeros((d, n))
+    lam = d * norms ** 2 / np.sum(norms ** 2)
+    hp = O.HParams(rank=2, source="x", lr=1.0, weight_decay=0.0, orientation="row")
+    out = O.normpre_step(w, x, np.zeros((d, n)), 0, hp, "L", l_mode="exact")
+    top = np.sort(lam[lam > 1.0])[::-1][:2]
+    assert np.allclose(out["lam_sel"], top, rtol=1e-12)
+    psi = x / norms[:, None]
+    expect = psi.copy()
+    for v in top:
+        i = int(np.argmin(np.abs(lam - v)))
+        expect[i] *= v ** -0.5
+    assert np.allclose(out["t"], expect, atol=1e-12)
+
+
+@pytest.mark.parametrize("l_mode", ["exact", "sketch"])
+def test_source_x_equal_row_norms_reduces_to_psi(l_mode):
+    # Equal active-row norms make G_X = Gamma, so both sources coincide.
+    w = np.zeros((12, 20))
+    g = _rand(12, 20)
+    g = g / np.linalg.norm(g, axis=1, keepdims=True) * 3.0
+    zero = np.zeros((12, 20))
+    for t in (0,):
+        a = O.normpre_step(w, g, zero, t, O.HParams(rank=3, source="x", orientation="row"), "L", l_mode=l_mode)
+        b = O.normpre_step(w, g, zero, t, O.HParams(rank=3, source="psi", orientation="row"), "L", l_mode=l_mode)
+        assert np.allclose(a["update"], b["update"], atol=1e-10)
+    # unequal norms: the sources differ
+    g2 = g * np.linspace(0.2, 3.0, 12)[:, None]
+    a = O.normpre_step(w, g2, zero, 0, O.HParams(rank=3, source="x", orientation="row"), "L", l_mode=l_mode)
+    b = O.normpre_step(w, g2, zero, 0, O.HParams(rank=3, source="psi", orientation="row"), "L", l_mode=l_mode)
+    assert O.relative_fro(a["update"], b["update"]) > 1e-3
+
+
 def test_orientation_alternates_with_t():
     hp = O.HParams()
     w, g, mp = _rand(5, 8), _rand(5, 8), _rand(5, 8)
