@@ -1,4 +1,4 @@
-// Batched fp16 x fp16 -> fp32 MFMA GEMMs for gfx950 (v_mfma_f32_16x16x32_f16).
+// Batched fp16 x fp16 -> fp32 MFMA GEMMs for gfx950 (v_mfma_f32_32x32x16_f16).
 //
 // One kernel template serves every dense contraction of the NormPre step:
 //   * the Newton-Schulz products A = X X^T, B = bA + cA^2, X <- aX + BX
@@ -9,11 +9,11 @@
 //     fused with the RMS-matched weight update of Alg. 1.
 //
 // C(mm, nn) = sum_k Aop(mm, k) Bop(nn, k).  Each operand is either K-major
-// (op(r, k) = p[r*ld + k]) or MN-major (op(r, k) = p[k*ld + r]); MN-major
-// tiles are transposed in registers while they are staged into LDS, so the
-// MFMA fragment reads are always 16-byte K-contiguous.  LDS rows are 64
-// halves (128 B) with an XOR swizzle of the 16-byte chunk index, which keeps
-// both the fragment reads and the transposed stores free of bank conflicts.
+// (op(r, k) = p[r*ld + k]) or MN-major (op(r, k) = p[k*ld + r]).  Both are
+// staged into LDS in their memory orientation with 16-byte stores: K-major
+// tiles as rows of 64 halves (128 B) with an XOR swizzle of the 16-byte
+// chunk index, MN-major tiles as 64 k-rows of R halves, whose fragments the
+// transposing LDS read (ds_read_b64_tr_b16) returns K-contiguous.
 // All sizes are multiples of the tile sizes (the workspace is zero padded).
 #include "np_internal.h"
 
@@ -41,6 +41,7 @@ __device__ __forceinline__ int lds_idx(int row, int chunk) {
 // they stay in VGPRs.
 template <int R, int NT>
 struct KMajorLoader {
+    static constexpr bool kTrans = false;
     static constexpr int N = R * 8 / NT;
     static_assert(N >= 1 && R * 8 % NT == 0, "tile too small for the block");
     static __device__ __forceinline__ void load(u32x4 (&r)[N], const half_t* base, int64_t ld, int row0, int k0,
@@ -65,61 +66,67 @@ struct KMajorLoader {
         const int row = (tid >> 3) + i * (NT / 8), ch = tid & 7;
         *reinterpret_cast<u32x4*>(lds + lds_idx(row, ch)) = r[i];
     }
+    // 32 x 16 fragment of the 32x32x16 MFMA: lane l gets row mb + l % 32,
+    // k = 16 s + 8 (l / 32) .. + 7.
+    static __device__ __forceinline__ f16x8 frag(const half_t* lds, int mb, int s, int lane) {
+        return *reinterpret_cast<const f16x8*>(lds + lds_idx(mb + (lane & 31), s * 2 + (lane >> 5)));
+    }
 };
 
-// 64 x R MN-major tile (k rows, r contiguous): each thread loads KR rows of 8
-// consecutive r, transposes the KR x 8 block in registers and writes 8 LDS
-// rows of KR halves.
+// 64 x R MN-major tile (k rows, r contiguous), kept in that orientation in
+// LDS: row k holds R halves, its 16-byte chunk c stored at c ^ mswz(k), and
+// the MFMA fragments are read with ds_read_b64_tr_b16.  Within each 16-lane
+// group that instruction returns to lane j the j-th column of the 4 x 16
+// block the group addresses (lane p supplies row p / 4, halves 4 (p % 4) ..
+// 4 (p % 4) + 3), i.e. four consecutive k of one mn index; two such reads
+// make one K-contiguous 8-half fragment.  mswz spreads the four rows one
+// group reads over disjoint bank ranges.
 template <int R, int NT>
 struct MNMajorLoader {
-    static constexpr int KR = R * 8 / NT;
-    static_assert(KR == 2 || KR == 4 || KR == 8, "unsupported MN-major tile");
-    static constexpr int MB = R / 8;
-    static constexpr int N = KR;
+    static constexpr bool kTrans = true;
+    static constexpr int CH = R / 8;                 // 16-byte chunks per row
+    static constexpr int N = R * BK / 8 / NT;
+    static_assert(R >= 128 && N >= 1 && R * BK / 8 % NT == 0 && NT % CH == 0, "unsupported MN-major tile");
+    static __device__ __forceinline__ int mswz(int k) { return (4 * (k & 3)) & (CH - 1); }
+    static __device__ __forceinline__ void load_item(u32x4 (&r)[N], const half_t* base, int64_t ld, int row0, int k0,
+                                                     int tid, int i) {
+        const int k = tid / CH + i * (NT / CH), c = tid % CH;
+        r[i] = *reinterpret_cast<const u32x4*>(base + (int64_t)(k0 + k) * ld + row0 + c * 8);
+    }
+    static __device__ __forceinline__ void store_item(const u32x4 (&r)[N], half_t* lds, int tid, int i) {
+        const int k = tid / CH + i * (NT / CH), c = tid % CH;
+        *reinterpret_cast<u32x4*>(lds + k * R + ((c ^ mswz(k)) << 3)) = r[i];
+    }
     static __device__ __forceinline__ void load(u32x4 (&r)[N], const half_t* base, int64_t ld, int row0, int k0,
                                                 int tid) {
-        const int mblk = tid % MB, kblk = tid / MB;
-        const half_t* p = base + (int64_t)(k0 + kblk * KR) * ld + row0 + mblk * 8;
 #pragma unroll
-        for (int q = 0; q < KR; ++q) r[q] = *reinterpret_cast<const u32x4*>(p + q * ld);
+        for (int i = 0; i < N; ++i) load_item(r, base, ld, row0, k0, tid, i);
     }
     static __device__ __forceinline__ void store(const u32x4 (&r)[N], half_t* lds, int tid) {
-        store_rows(r, lds, tid, 0, 8);
+#pragma unroll
+        for (int i = 0; i < N; ++i) store_item(r, lds, tid, i);
     }
-    // LDS rows mm0 .. mm1-1 of this thread's 8 (each uses every staging
-    // register, so the next loads can only follow the last part).
-    static __device__ __forceinline__ void store_rows(const u32x4 (&r)[N], half_t* lds, int tid, int mm0, int mm1) {
-        const int mblk = tid % MB, kblk = tid / MB;
-        const int kofs = kblk * KR, chunk = kofs >> 3, within = kofs & 7;
-#pragma unroll
-        for (int mm = 0; mm < 8; ++mm) {
-            if (mm < mm0 || mm >= mm1) continue;
-            const int d = mm >> 1;
-            uint32_t packed[KR / 2];
-#pragma unroll
-            for (int e = 0; e < KR / 2; ++e) {
-                const uint32_t lo_src = r[2 * e][d], hi_src = r[2 * e + 1][d];
-                packed[e] = (mm & 1) ? ((lo_src >> 16) | (hi_src & 0xffff0000u))
-                                     : ((lo_src & 0xffffu) | (hi_src << 16));
-            }
-            half_t* dst = lds + lds_idx(mblk * 8 + mm, chunk) + within;
-            if constexpr (KR == 8) {
-                *reinterpret_cast<u32x4*>(dst) = u32x4{packed[0], packed[1], packed[2], packed[3]};
-            } else if constexpr (KR == 4) {
-                *reinterpret_cast<u32x2*>(dst) = u32x2{packed[0], packed[1]};
-            } else {
-                *reinterpret_cast<uint32_t*>(dst) = packed[0];
-            }
-        }
+    // 32 x 16 fragment of the 32x32x16 MFMA: lane l gets mn = mb + l % 32,
+    // k = 16 s + 8 (l / 32) .. + 7.
+    static __device__ __forceinline__ f16x8 frag(const half_t* lds, int mb, int s, int lane) {
+        const int g = lane >> 4, p = lane & 15;
+        const int c = (mb >> 3) + 2 * (g & 1) + ((p & 3) >> 1);
+        const int k = 16 * s + 8 * (g >> 1) + (p >> 2);
+        const int within = 4 * (p & 1);
+        typedef short s16x4 __attribute__((ext_vector_type(4)));
+        typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+        const half_t* a0 = lds + k * R + ((c ^ mswz(k)) << 3) + within;
+        const half_t* a1 = lds + (k + 4) * R + ((c ^ mswz(k + 4)) << 3) + within;
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(a0));
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(a1));
+        typedef short s16x8 __attribute__((ext_vector_type(8)));
+        const s16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        return __builtin_bit_cast(f16x8, v);
     }
 };
 
 template <bool MN, int R, int NT>
 struct LoaderSel { using type = KMajorLoader<R, NT>; };
-template <class L>
-struct SplitOf { static constexpr bool value = false; };
-template <int R, int NT>
-struct SplitOf<KMajorLoader<R, NT>> { static constexpr bool value = true; };
 template <int R, int NT>
 struct LoaderSel<true, R, NT> { using type = MNMajorLoader<R, NT>; };
 
@@ -202,8 +209,8 @@ __device__ __forceinline__ void xcd_remap(int& bx, int& by, int& bz) {
 // At least two waves per SIMD: two 4-wave blocks (or one 8-wave block) per
 // CU, so one block's MFMAs overlap the other's LDS and barrier waits.
 // MF = 32: v_mfma_f32_32x32x16_f16 blocks (measured issue-bound ceiling on
-// gfx950 about 2.4 PFLOP/s), used by every tile; MF = 16:
-// v_mfma_f32_16x16x32_f16 blocks (about 1.45 PFLOP/s), kept as an option.
+// gfx950 about 2.4 PFLOP/s, against about 1.45 PFLOP/s for the 16x16x32
+// form).
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 // Epilogues that carry a GramGroups table (grouped Gram launches).
@@ -221,8 +228,8 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     constexpr int NT = WM * WN * 64;
     constexpr int TM = BM / WM, TN = BN / WN, FM = TM / MF, FN = TN / MF;
     // Accumulators as quads: 4 consecutive rows of one column per lane.
-    constexpr int QPB = MF == 16 ? 1 : 4;           // quads per MFMA block
-    static_assert((MF == 16 || MF == 32) && TM % MF == 0 && TN % MF == 0, "wave tile must hold whole MFMA blocks");
+    constexpr int QPB = 4;                          // quads per MFMA block
+    static_assert(MF == 32 && TM % MF == 0 && TN % MF == 0, "wave tile must hold whole MFMA blocks");
     constexpr int NQ = FM * FN * QPB;
     // Two LDS stages: the MFMAs of stage i overlap the LDS stores of stage
     // i + 1 and the global loads of stage i + 2.  The epilogue reuses the
@@ -279,52 +286,25 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = AccT{};
 
-    // MFMAs over one LDS stage (16x16x32 blocks, BK / 32 sub-steps).
-    auto compute16 = [&](int stage) {
-      if constexpr (MF == 16) {
-        const half_t* ca = sbase + stage * (BM + BN) * BK;
-        const half_t* cb = ca + BM * BK;
-#pragma unroll
-        for (int s = 0; s < BK / 32; ++s) {
-            f16x8 af[FM], bf[FN];
-            const int chunk = s * 4 + (lane >> 4);
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
-                af[i] = *reinterpret_cast<const f16x8*>(ca + lds_idx(wm * TM + i * 16 + (lane & 15), chunk));
-#pragma unroll
-            for (int j = 0; j < FN; ++j)
-                bf[j] = *reinterpret_cast<const f16x8*>(cb + lds_idx(wn * TN + j * 16 + (lane & 15), chunk));
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
-#pragma unroll
-                for (int j = 0; j < FN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
-        }
-      }
-    };
-
     // One K-step with 32x32x16 MFMAs (BK / 16 sub-steps).  With STORE the next
     // stage's staging registers go to LDS and, with LOAD, the stage after
-    // that is fetched into them; K-major items are spread over the sub-steps
-    // (item i at sub-step i * NSUB / N) so the LDS stores and global loads
-    // are issued between MFMAs rather than after all of them.
+    // that is fetched into them; staging item i is stored (and refilled) at
+    // sub-step i * NSUB / N, and the scheduling groups below interleave one
+    // MFMA with one LDS or global access so the memory traffic of the step
+    // is issued between its MFMAs.
     constexpr int NSUB = BK / 16;
     auto kstep32 = [&](auto store_tag, auto load_tag, int stage, int k_load, auto& rA, auto& rB) {
         constexpr bool STORE = decltype(store_tag)::value, LOAD = decltype(load_tag)::value;
-      if constexpr (MF == 32) {
         const half_t* ca = sbase + stage * (BM + BN) * BK;
         const half_t* cb = ca + BM * BK;
         half_t* sa = sbase + (stage ^ 1) * (BM + BN) * BK;
         half_t* sb = sa + BM * BK;
         f16x8 af[2][FM], bf[2][FN];
         auto read_frags = [&](int s, int buf) {
-            const int chunk = s * 2 + (lane >> 5);
 #pragma unroll
-            for (int i = 0; i < FM; ++i)
-                af[buf][i] = *reinterpret_cast<const f16x8*>(ca + lds_idx(wm * TM + i * 32 + (lane & 31), chunk));
+            for (int i = 0; i < FM; ++i) af[buf][i] = LA::frag(ca, wm * TM + i * 32, s, lane);
 #pragma unroll
-            for (int j = 0; j < FN; ++j)
-                bf[buf][j] = *reinterpret_cast<const f16x8*>(cb + lds_idx(wn * TN + j * 32 + (lane & 31), chunk));
+            for (int j = 0; j < FN; ++j) bf[buf][j] = LB::frag(cb, wn * TN + j * 32, s, lane);
         };
         read_frags(0, 0);
 #pragma unroll
@@ -336,31 +316,59 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                 for (int j = 0; j < FN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[s & 1][i], bf[s & 1][j], acc[i][j], 0, 0, 0);
             if constexpr (STORE) {
-                if constexpr (SplitOf<LA>::value) {
 #pragma unroll
-                    for (int it = 0; it < LA::N; ++it)
-                        if (it * NSUB / LA::N == s) {
-                            LA::store_item(rA, sa, tid, it);
-                            if constexpr (LOAD) LA::load_item(rA, Ab, lda, m0, k_load, tid, it);
-                        }
-                } else {
-                    LA::store_rows(rA, sa, tid, s * 8 / NSUB, (s + 1) * 8 / NSUB);
-                    if constexpr (LOAD) if (s == NSUB - 1) LA::load(rA, Ab, lda, m0, k_load, tid);
-                }
-                if constexpr (SplitOf<LB>::value) {
+                for (int it = 0; it < LA::N; ++it)
+                    if (it * NSUB / LA::N == s) {
+                        LA::store_item(rA, sa, tid, it);
+                        if constexpr (LOAD) LA::load_item(rA, Ab, lda, m0, k_load, tid, it);
+                    }
 #pragma unroll
-                    for (int it = 0; it < LB::N; ++it)
-                        if (it * NSUB / LB::N == s) {
-                            LB::store_item(rB, sb, tid, it);
-                            if constexpr (LOAD) LB::load_item(rB, Bb, ldb, n0, k_load, tid, it);
-                        }
-                } else {
-                    LB::store_rows(rB, sb, tid, s * 8 / NSUB, (s + 1) * 8 / NSUB);
-                    if constexpr (LOAD) if (s == NSUB - 1) LB::load(rB, Bb, ldb, n0, k_load, tid);
-                }
+                for (int it = 0; it < LB::N; ++it)
+                    if (it * NSUB / LB::N == s) {
+                        LB::store_item(rB, sb, tid, it);
+                        if constexpr (LOAD) LB::load_item(rB, Bb, ldb, n0, k_load, tid, it);
+                    }
             }
         }
-      }
+        // Issue order: the fragments of sub-step 0, then per sub-step each
+        // MFMA followed by one fragment read of the next sub-step or, once
+        // those are out, one LDS store (and its refill load).  An MN-major
+        // fragment is two reads.
+        constexpr int RD = (LA::kTrans ? 2 : 1) * FM + (LB::kTrans ? 2 : 1) * FN;
+        __builtin_amdgcn_sched_group_barrier(0x100, RD, 0);
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s) {
+            int nw = 0;
+#pragma unroll
+            for (int it = 0; it < LA::N; ++it) nw += (it * NSUB / LA::N == s);
+#pragma unroll
+            for (int it = 0; it < LB::N; ++it) nw += (it * NSUB / LB::N == s);
+            if (!STORE) nw = 0;
+            const int nr = s + 1 < NSUB ? RD : 0;
+            const int per = (nr + FM * FN - 1) / (FM * FN);     // 0, 1 or 2
+            int r_left = nr, w_left = nw;
+#pragma unroll
+            for (int i = 0; i < FM * FN; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                if (r_left >= 2 && per == 2) {
+                    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+                    r_left -= 2;
+                } else if (r_left > 0) {
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                    --r_left;
+                } else if (w_left > 0) {
+                    __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+                    if (LOAD) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+                    --w_left;
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < LA::N + LB::N; ++q)
+                if (q < w_left) {
+                    __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+                    if (LOAD) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+                }
+        }
     };
     using T_ = std::true_type;
     using F_ = std::false_type;
@@ -380,37 +388,16 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
         LB::load(rb, Bb, ldb, n0, kat(1), tid);
         LA::load(ra2, Ab, lda, m0, kat(2), tid);
         LB::load(rb2, Bb, ldb, n0, kat(2), tid);
-        auto step_plain = [&](int stage, int k_load, auto& rA, auto& rB, bool store, bool load) {
-            lds_barrier();
-            kstep32(F_{}, F_{}, stage, 0, rA, rB);
-            if (store) {
-                LA::store(rA, sbase + (stage ^ 1) * (BM + BN) * BK, tid);
-                LB::store(rB, sbase + (stage ^ 1) * (BM + BN) * BK + BM * BK, tid);
-                if (load) {
-                    LA::load(rA, Ab, lda, m0, k_load, tid);
-                    LB::load(rB, Bb, ldb, n0, k_load, tid);
-                }
-            }
-        };
         int j = 0;
         for (; j + 2 < nk; j += 2) {
-            if constexpr (LAYOUT == 0) {
-                lds_barrier();
-                kstep32(T_{}, T_{}, 0, kat(j + 3), ra, rb);
-                lds_barrier();
-                kstep32(T_{}, T_{}, 1, kat(j + 4), ra2, rb2);
-            } else {
-                step_plain(0, kat(j + 3), ra, rb, true, true);
-                step_plain(1, kat(j + 4), ra2, rb2, true, true);
-            }
+            lds_barrier();
+            kstep32(T_{}, T_{}, 0, kat(j + 3), ra, rb);
+            lds_barrier();
+            kstep32(T_{}, T_{}, 1, kat(j + 4), ra2, rb2);
         }
         if (j + 1 < nk) {
-            if constexpr (LAYOUT == 0) {
-                lds_barrier();
-                kstep32(T_{}, F_{}, 0, 0, ra, rb);
-            } else {
-                step_plain(0, 0, ra, rb, true, false);
-            }
+            lds_barrier();
+            kstep32(T_{}, F_{}, 0, 0, ra, rb);
             ++j;
         }
         lds_barrier();
@@ -424,53 +411,33 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
             LA::load(ra, Ab, lda, m0, kbeg + BK, tid);
             LB::load(rb, Bb, ldb, n0, kbeg + BK, tid);
         }
+        // Branch-free steady state, the last two K-steps peeled.
         int stage = 0;
-        if constexpr (MF == 32 && LAYOUT == 0) {
-            // Both operands K-major: branch-free steady state with the stores
-            // and loads spread over the MFMA sub-steps, the last two K-steps
-            // peeled.  (With a register-transposed MN-major operand the plain
-            // loop below measured faster.)
-            int k0 = kbeg;
-            for (; k0 + 2 * BK < kend; k0 += BK, stage ^= 1) {
-                lds_barrier();
-                kstep32(T_{}, T_{}, stage, k0 + 2 * BK, ra, rb);
-            }
-            if (k0 + BK < kend) {
-                lds_barrier();
-                kstep32(T_{}, F_{}, stage, 0, ra, rb);
-                k0 += BK;
-                stage ^= 1;
-            }
+        int k0 = kbeg;
+        for (; k0 + 2 * BK < kend; k0 += BK, stage ^= 1) {
             lds_barrier();
-            kstep32(F_{}, F_{}, stage, 0, ra, rb);
-        } else {
-            for (int k0 = kbeg; k0 < kend; k0 += BK, stage ^= 1) {
-                lds_barrier();
-                if constexpr (MF == 16) compute16(stage);
-                else kstep32(F_{}, F_{}, stage, 0, ra, rb);
-                if (k0 + BK < kend) {
-                    LA::store(ra, sbase + (stage ^ 1) * (BM + BN) * BK, tid);
-                    LB::store(rb, sbase + (stage ^ 1) * (BM + BN) * BK + BM * BK, tid);
-                    if (k0 + 2 * BK < kend) {
-                        LA::load(ra, Ab, lda, m0, k0 + 2 * BK, tid);
-                        LB::load(rb, Bb, ldb, n0, k0 + 2 * BK, tid);
-                    }
-                }
-            }
+            kstep32(T_{}, T_{}, stage, k0 + 2 * BK, ra, rb);
         }
+        if (k0 + BK < kend) {
+            lds_barrier();
+            kstep32(T_{}, F_{}, stage, 0, ra, rb);
+            k0 += BK;
+            stage ^= 1;
+        }
+        lds_barrier();
+        kstep32(F_{}, F_{}, stage, 0, ra, rb);
     }
 
     // Quad qi of this lane: rows quad_row(qi) + 0..3 (relative to the wave
-    // tile), column quad_col(qi).  16x16 blocks: row 16i + 4*(lane/16),
-    // column 16j + lane%16.  32x32 blocks: register r of block (i, j) is
+    // tile), column quad_col(qi): register r of 32x32 block (i, j) is
     // row 32i + 8*(r/4) + 4*(lane/32) + r%4, column 32j + lane%32.
     auto quad_row = [&](int qi) -> int {
         const int blk = qi / QPB, g = qi - blk * QPB, i = blk / FN;
-        return MF == 16 ? 16 * i + 4 * (lane >> 4) : 32 * i + 8 * g + 4 * (lane >> 5);
+        return 32 * i + 8 * g + 4 * (lane >> 5);
     };
     auto quad_col = [&](int qi) -> int {
         const int blk = qi / QPB, j = blk - (blk / FN) * FN;
-        return MF == 16 ? 16 * j + (lane & 15) : 32 * j + (lane & 31);
+        return 32 * j + (lane & 31);
     };
     auto quad_val = [&](int qi, int r) -> float {
         const int blk = qi / QPB, g = qi - blk * QPB, i = blk / FN, j = blk - i * FN;
