@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 LIB_DIR = os.path.join(PKG, "lib")
 LIB = os.path.join(LIB_DIR, "libnormpre.so")
 OBJ_DIR = os.path.join(ROOT, "_build")
-SOURCES = ["np_gemm.hip", "np_elementwise.hip", "np_sketch.hip", "normpre_api.cpp"]
+SOURCES = ["np_gemm.hip", "np_elementwise.hip", "np_sketch.hip", "np_eigen.hip", "normpre_api.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -26,6 +26,10 @@ constexpr int64_t kMaxDim = int64_t(1) << 20;
 constexpr int64_t kMaxElems = int64_t(1) << 31;
 constexpr int kMaxRowLen = 32768;   // row-active register kernel limit
 constexpr int kMaxEll = 384;
+// Exact NormPre-L above kMaxEll active rows: dense fp64 eigensolver on the
+// a x a interaction matrix (tridiagonal reduction, bisection, inverse
+// iteration), up to this many active rows.
+constexpr int64_t kMaxExactRows = 8192;
 constexpr int kColRowChunk = 128;   // rows per block in the column-active pass
 constexpr int kMaxSplits = 16;
 constexpr int kEigSweeps = 30;
@@ -52,8 +56,16 @@ int orientation_of(const normpre_hparams& hp) {
     return (int)(((hp.step % 2) + 2) % 2);
 }
 
-// l of Alg. 2; the exact variant spans all active rows.
+// Exact NormPre-L through the dense eigensolver (more than kMaxEll active rows).
+bool exact_large(const normpre_hparams& hp, int64_t active_rows) {
+    return (hp.flags & NORMPRE_FLAG_L_EXACT) && active_rows > kMaxEll;
+}
+
+// l of Alg. 2.  The exact variant spans all active rows, or, above kMaxEll
+// of them, the leading min(r, a) eigenvectors of Gamma (all the selected
+// modes can come from).
 int sketch_width(const normpre_hparams& hp, int64_t active_rows) {
+    if (exact_large(hp, active_rows)) return (int)std::min<int64_t>(active_rows, hp.rank);
     if (hp.flags & NORMPRE_FLAG_L_EXACT) return (int)std::min<int64_t>(active_rows, INT32_MAX);
     return (int)std::min<int64_t>(active_rows, (int64_t)hp.rank + hp.oversample);
 }
@@ -126,11 +138,16 @@ Fail validate(int variant, int num_mats, const int64_t* shapes, const normpre_hp
             return {NORMPRE_ERR_UNSUPPORTED,
                     fmt("matrix %d: row-active rows of %lld elements exceed %d", i, (long long)n, kMaxRowLen)};
         if (variant == NORMPRE_VARIANT_L) {
-            const int64_t ell = sketch_width(*hp, k == 0 ? m : n);
+            const int64_t a = k == 0 ? m : n;
+            if (exact_large(*hp, a) && a > kMaxExactRows)
+                return {NORMPRE_ERR_UNSUPPORTED,
+                        fmt("matrix %d: exact NormPre-L on %lld active rows exceeds %lld", i, (long long)a,
+                            (long long)kMaxExactRows)};
+            const int64_t ell = sketch_width(*hp, a);
             if (ell > kMaxEll)
                 return {NORMPRE_ERR_UNSUPPORTED,
                         fmt("matrix %d: %s %lld exceeds %d", i,
-                            (hp->flags & NORMPRE_FLAG_L_EXACT) ? "exact NormPre-L on active rows" : "sketch width",
+                            (hp->flags & NORMPRE_FLAG_L_EXACT) ? "exact NormPre-L with rank" : "sketch width",
                             (long long)ell, kMaxEll)};
         }
     }
@@ -294,6 +311,10 @@ struct GWork {
     float* eigs;
     float* ritz;
     int* nsel;
+    // exact NormPre-L above kMaxEll active rows
+    float* gam32;           // Gamma, fp32 a_pad x a_pad
+    TriWork tw;             // eigensolver workspace (order a)
+    double* lam;            // leading ell eigenvalues
 };
 
 struct Dims {
@@ -303,6 +324,7 @@ struct Dims {
     // L
     int64_t a, b, a_pad, b_pad;
     int ell, ellp, top;
+    bool xl;                // exact NormPre-L through the dense eigensolver
 };
 
 Dims dims_of(int64_t m, int64_t n, int k, const normpre_hparams& hp) {
@@ -322,6 +344,7 @@ Dims dims_of(int64_t m, int64_t n, int k, const normpre_hparams& hp) {
     d.ell = sketch_width(hp, d.a);
     d.ellp = (int)round_up(d.ell, kEllPad);
     d.top = std::min(hp.rank, d.ell);
+    d.xl = exact_large(hp, d.a);
     return d;
 }
 
@@ -402,6 +425,18 @@ void carve_item(Arena& ar, Item& it, int variant, bool source_x) {
         w.part = ar.take<float>(count * (int64_t)kMaxSplits * lp * maxpad);
         w.qlen = ar.take<half_t>(count * d.a_pad * lp);
         w.flen = ar.take<half_t>(count * d.b_pad * lp);
+        if (d.xl) {
+            const int64_t a = d.a;
+            w.gam32 = ar.take<float>(count * d.a_pad * d.a_pad);
+            w.tw.A = ar.take<double>(count * a * a);
+            w.tw.vec = ar.take<double>(count * 4 * a);
+            w.tw.d = ar.take<double>(count * a);
+            w.tw.e = ar.take<double>(count * a);
+            w.tw.tau = ar.take<double>(count * a);
+            w.tw.lu = ar.take<double>(count * d.ell * 5 * a);
+            w.tw.y = ar.take<double>(count * d.ell * a);
+            w.lam = ar.take<double>(count * d.ell);
+        }
         if (source_x) {
             w.xs = ar.take<half_t>(count * mn);
             w.xsq = ar.take<float>(count * d.lp_);
@@ -1062,6 +1097,53 @@ int sketch_front(const StepCtx& sc, const Item& it, DebugMat* dbg) {
     return NORMPRE_OK;
 }
 
+// Exact NormPre-L above kMaxEll active rows (App. B, exact eigenspace
+// extraction): Gamma = Psi Psi^T of the active side (fp16 MFMA, fp32), its
+// leading ell = min(r, a) eigenvectors by the fp64 dense eigensolver, written
+// as Y^T in place of the sketch; the common tail (orthonormalization,
+// Rayleigh-Ritz, selection of lambda > 1, apply) then works on exactly the
+// modes C can come from.
+int exact_front(const StepCtx& sc, const Item& it, DebugMat* dbg) {
+    const Dims& d = it.d;
+    const GWork& w = it.w;
+    const std::vector<int>& idx = (*sc.groups)[it.g].idx;
+    const int count = it.count;
+    int rc = run_normalize(sc, d, w, idx, it.first, count, dbg);
+    if (rc) return rc;
+    const half_t* src = w.xs ? w.xs : w.psi;
+    const int64_t mn = d.mp * d.np_, ap = d.a_pad, a = d.a;
+    {
+        Operand A{src, d.np_, mn}, B{src, d.np_, mn};
+        GemmShape sh{(int)ap, (int)ap, (int)d.b_pad, 1, (int)d.b_pad, 0};
+        EpiPartial e{};
+        e.out = w.gam32;
+        e.ld_out = ap;
+        e.stride_split = 0;
+        e.stride_mat = ap * ap;
+        const double flops = 2.0 * (double)ap * (double)ap * (double)d.b_pad * count;
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_STREAM, flops, 2.0 * (double)d.m * (double)d.n * count,
+                     [&] { return launch_gemm_gram_f32(d.k == 0 ? 0 : 2, A, B, sh, count, e, sc.s); }),
+               "exact gamma");
+    }
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+                 [&] { return launch_gamma_to_f64(w.gam32, ap, ap * ap, (int)a, w.tw.A, count, sc.s); }),
+           "exact gamma f64");
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+                 [&] { return launch_tridiagonalize(w.tw, (int)a, count, sc.s); }),
+           "tridiagonalize");
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+                 [&] { return launch_tri_eigvals(w.tw, (int)a, 0, d.ell, w.lam, d.ell, count, sc.s); }),
+           "bisection");
+    const int64_t lp = d.ellp, maxpad = d.lp_;
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+                 [&] {
+                     return launch_tri_eigvecs(w.tw, (int)a, w.lam, d.ell, w.v32[0], ap, (int)lp, lp * maxpad, count,
+                                               sc.s);
+                 }),
+           "eigenvectors");
+    return NORMPRE_OK;
+}
+
 int sketch_back(const StepCtx& sc, const Item& it, const Pool& pl, DebugMat* dbg) {
     const Dims& d = it.d;
     const GWork& w = it.w;
@@ -1123,7 +1205,7 @@ int sketch_back(const StepCtx& sc, const Item& it, const Pool& pl, DebugMat* dbg
 
 int run_round_l(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& pools, DebugMat* dbg) {
     for (const Item& it : items) {
-        int rc = sketch_front(sc, it, dbg);
+        int rc = it.d.xl ? exact_front(sc, it, dbg) : sketch_front(sc, it, dbg);
         if (rc) return rc;
     }
     // Q = qr(Y) by two Cholesky-QR passes (fp64 Gram and factorization).

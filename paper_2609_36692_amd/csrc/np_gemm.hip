@@ -820,6 +820,15 @@ hipError_t launch_gemm_partial(TileCfg cfg, int layout, Operand A, Operand B, Ge
     return hipErrorInvalidValue;
 }
 
+hipError_t launch_gemm_gram_f32(int layout, Operand A, Operand B, GemmShape sh, int batch, const EpiPartial& e,
+                                hipStream_t s) {
+    EPar ee;
+    static_cast<EpiPartial&>(ee) = e;
+    if (layout == 0) return run<128, 128, 2, 2, 0>(A, B, sh, batch, ee, s);
+    if (layout == 2) return run<128, 128, 2, 2, 2>(A, B, sh, batch, ee, s);
+    return hipErrorInvalidValue;
+}
+
 hipError_t launch_gemm_apply(Operand A, Operand B, GemmShape sh, int batch,
                              const EpiApplyUpdate& e, hipStream_t s) {
     EApp ee;

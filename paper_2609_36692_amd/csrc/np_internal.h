@@ -271,4 +271,34 @@ hipError_t launch_eig_select(const EigArgs& a, int batch, hipStream_t s);
 
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t s);
 
+// ------------------------------------------ dense symmetric eigensolver ---
+// Workspace of one launch of matrices of equal order n (per matrix: A n x n,
+// vec 4 n, d / e / tau n each; per matrix and requested eigenvector: lu 5 n,
+// y n), all fp64.
+struct TriWork {
+    double* A;      // the matrix on entry; reflectors in its rows on exit
+    double* vec;
+    double* d;
+    double* e;
+    double* tau;
+    double* lu;
+    double* y;
+};
+// Symmetrized fp64 copy of an fp32 n x n matrix (leading block, ld ldg).
+hipError_t launch_gamma_to_f64(const float* g, int64_t ldg, int64_t strideg, int n, double* A, int batch,
+                               hipStream_t s);
+// Householder reduction of A to tridiagonal form (d, e), reflectors kept.
+hipError_t launch_tridiagonalize(const TriWork& w, int n, int batch, hipStream_t s);
+// Eigenvalues first .. first + nvals - 1 in descending order (0 = largest).
+hipError_t launch_tri_eigvals(const TriWork& w, int n, int first, int nvals, double* out, int64_t stride_out,
+                              int batch, hipStream_t s);
+// Unit eigenvectors of A for the given eigenvalues (nvals per matrix,
+// descending), as fp32 rows of out (ld_out >= n, zero padded; rows nvals ..
+// rows_out - 1 zero).
+hipError_t launch_tri_eigvecs(const TriWork& w, int n, const double* lam, int nvals, float* out, int64_t ld_out,
+                              int rows_out, int64_t stride_out, int batch, hipStream_t s);
+// Gamma = Psi Psi^T (layout 0) or Psi^T Psi (layout 2) in fp32, full tiles.
+hipError_t launch_gemm_gram_f32(int layout, Operand A, Operand B, GemmShape sh, int batch, const EpiPartial& e,
+                                hipStream_t s);
+
 }  // namespace np

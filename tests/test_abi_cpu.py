@@ -87,8 +87,10 @@ def test_version(N):
     (1, [(8, 40000)], {"orientation": 3, "step": 1}, -2),  # both axes: the row pass needs short rows
     (0, [(8, 8)], {"flags": 64}, -1),
     (1, [(100, 1000)], {"flags": 16}, 0),            # exact NormPre-L, a = 100
-    (1, [(400, 1000)], {"flags": 16}, -2),           # exact needs a <= 384
-    (1, [(400, 1000)], {"flags": 16, "step": 1}, -2),
+    (1, [(400, 1000)], {"flags": 16}, 0),            # exact above 384 rows: dense eigensolver
+    (1, [(400, 1000)], {"flags": 16, "step": 1}, 0),
+    (1, [(9000, 16)], {"flags": 16}, -2),            # exact needs a <= 8192
+    (1, [(1000, 1000)], {"flags": 16, "rank": 400}, -2),  # exact above 384 rows: rank <= 384
     (1, [(1000, 300)], {"flags": 16, "step": 1}, 0), # column-active: a = 300
     (0, [(8, 8)], {"flags": 16}, -1),                # exact flag is NormPre-L only
     (0, [(8, 8)], {"flags": 4}, 0),                  # no tangent
