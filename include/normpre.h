@@ -101,7 +101,12 @@ extern "C" {
  * Gamma = Psi Psi^T instead of a sketch.  Realized as Alg. 2 at full width,
  * l = a (active rows) and no power iteration: the candidate subspace is then
  * all of range(Psi), so the Rayleigh-Ritz pairs are the exact nonzero
- * eigenpairs of Gamma.  Needs a <= 384 (else UNSUPPORTED); NormPre-L only. */
+ * eigenpairs of Gamma.  Above 384 active rows the candidate subspace is
+ * instead spanned by the leading min(r, a) eigenvectors of Gamma, computed by
+ * a dense fp64 eigensolver on the GPU (Householder tridiagonalization,
+ * bisection, inverse iteration); the selected modes C are among them, so the
+ * result is again the exact one.  Needs a <= 8192 and r <= 384 (else
+ * UNSUPPORTED); NormPre-L only. */
 #define NORMPRE_FLAG_L_EXACT       16u
 /* Interaction-source ablation (App. A.4, "Ablations on Interaction Geometry
  * Source"): NormPre-L builds its preconditioner from the update before
@@ -168,7 +173,8 @@ const char* normpre_last_error(const normpre_ctx* ctx);
  * in the row-active or both-axes orientation a row longer than 32768
  * elements; for
  * NormPre-L a sketch width l = min(active rows, r + o) above 384, or with
- * NORMPRE_FLAG_L_EXACT more than 384 active rows).
+ * NORMPRE_FLAG_L_EXACT more than 8192 active rows, or more than 384 active
+ * rows with r above 384).
  */
 int normpre_validate(int variant, int num_mats, const int64_t* shapes,
                      const normpre_hparams* hp, char* msg, int msg_len);
@@ -194,6 +200,44 @@ int normpre_step(normpre_ctx* ctx, int variant, int num_mats,
                  float* const* params, const float* const* grads,
                  float* const* momentum, const int64_t* shapes,
                  const normpre_hparams* hp, void* stream);
+
+/* ---- spectral diagnostics (App. A, spectral dynamics) -------------------- */
+
+#define NORMPRE_SPECTRUM_GAMMA 0  /* Gamma = Psi Psi^T, after the normalization (Eq. 2) */
+#define NORMPRE_SPECTRUM_GX    1  /* trace-matched G_X = a X X^T / tr(X X^T), before it  */
+/*
+ * All eigenvalues of one matrix's interaction matrix in the active
+ * orientation, descending.  X is the update after momentum processing (the
+ * relaxed tangent of Sec. 3.1, or the mode hp->flags selects) formed from
+ * w (rows x cols, device fp32, read only) and m, the momentum M_t after the
+ * step's momentum update (device fp32, read only); Psi = D(X)^{-1} X.  The
+ * active orientation is hp's (orientation, step); NORMPRE_ORIENT_BOTH is
+ * INVALID_ARG.  Both matrices have trace a (active rows), so their spectra
+ * compare directly.
+ *   eigs : host array of a doubles (a = rows for k = 0, cols for k = 1)
+ * Works in the context's workspace on `stream` and synchronizes it before
+ * returning.  Gamma is formed from the fp16 Psi the step itself uses (fp32
+ * accumulation); the eigensolver is fp64.  At most 8192 active rows.
+ * Errors: NOT_INITIALIZED, INVALID_ARG (unknown `which`, null pointers, W and
+ * M overlapping, or the checks of normpre_validate), UNSUPPORTED, OOM,
+ * HIP_ERROR.
+ */
+int normpre_spectrum(normpre_ctx* ctx, int which, int64_t rows, int64_t cols, const float* w,
+                     const float* m, const normpre_hparams* hp, double* eigs, void* stream);
+
+/*
+ * Spectral transformation energy of global against localized
+ * preconditioning (App. A, spectral dynamics): with e_i = (sqrt(lambda_i) -
+ * 1)^2 over the positive eigenvalues among the first `count` of eigs (the
+ * nonzero spectrum of Gamma, descending), and C the first min(rank, |{lambda
+ * > 1}|) of them,
+ *   out[0] = E_top    = sum_{i in C} e_i
+ *   out[1] = E_remain = sum over lambda_i > 1 outside C
+ *   out[2] = E_sub    = sum over 0 < lambda_i < 1
+ *   out[3] = E_global = out[0] + out[1] + out[2].
+ * Host only.  Errors: INVALID_ARG (null pointers, count or rank < 0).
+ */
+int normpre_energy_split(const double* eigs, int64_t count, int32_t rank, double* out);
 
 /* ---- inspection (tests, benchmarks) -------------------------------------- */
 

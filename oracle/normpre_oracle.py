@@ -429,6 +429,31 @@ def trace_matched_gram(x: np.ndarray) -> np.ndarray:
     return x.shape[0] * gram / np.trace(gram)
 
 
+def interaction_spectrum(x_bar: np.ndarray, normalized: bool = True, eps: float = 1e-12) -> np.ndarray:
+    """Eigenvalues, descending, of Gamma = Psi Psi^T with Psi = D(X)^-1 X
+    (normalized) or of the trace-matched G_X (before normalization), for the
+    update X in its active orientation (App. A, spectral dynamics: both have
+    trace d, so their spectra are compared directly)."""
+    g = (lambda p: p @ p.T)(diagonal_gram_normalize(x_bar, eps)) if normalized else trace_matched_gram(x_bar)
+    return np.sort(np.linalg.eigvalsh(g))[::-1]
+
+
+def energy_split(eigs, count: int, rank: int) -> dict:
+    """Spectral transformation energy (App. A): e_i = (sqrt(lambda_i) - 1)^2
+    over the nonzero eigenvalues (the first `count`, descending, positive);
+    C = the largest at most `rank` eigenvalues above one.  E_top sums e_i
+    over C, E_remain over the other eigenvalues above one, E_sub over those
+    in (0, 1); E_global is the total."""
+    lam = [float(v) for v in list(eigs)[:count] if v > 0.0]
+    above = [v for v in lam if v > 1.0]
+    chosen = above[:rank]
+    e = lambda v: (math.sqrt(v) - 1.0) ** 2
+    top = sum(e(v) for v in chosen)
+    remain = sum(e(v) for v in above[len(chosen):])
+    sub = sum(e(v) for v in lam if v < 1.0)
+    return {"top": top, "remain": remain, "sub": sub, "global": top + remain + sub}
+
+
 def relative_fro(a, b) -> float:
     a = np.asarray(a, np.float64)
     b = np.asarray(b, np.float64)

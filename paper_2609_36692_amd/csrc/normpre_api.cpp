@@ -1539,6 +1539,121 @@ int normpre_step(normpre_ctx* ctx, int variant, int num_mats, float* const* para
     return NORMPRE_OK;
 }
 
+int normpre_spectrum(normpre_ctx* ctx, int which, int64_t rows, int64_t cols, const float* w, const float* m,
+                     const normpre_hparams* hp, double* eigs, void* stream) {
+    if (!ctx) return set_err(nullptr, NORMPRE_ERR_NOT_INITIALIZED, "context is null");
+    ctx->err.clear();
+    if (which != NORMPRE_SPECTRUM_GAMMA && which != NORMPRE_SPECTRUM_GX)
+        return set_err(ctx, NORMPRE_ERR_INVALID_ARG, fmt("unknown spectrum %d", which));
+    if (!w || !m || !eigs || !hp) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "null pointer argument");
+    if (hp->orientation == NORMPRE_ORIENT_BOTH)
+        return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "the spectrum needs a single active side");
+    // The momentum step is not repeated: M is taken as the update source
+    // (a zero previous momentum with M as the "gradient" at mu = 0).
+    normpre_hparams h = *hp;
+    h.momentum = 0.f;
+    h.flags &= NORMPRE_FLAG_TANGENT_NONE | NORMPRE_FLAG_TANGENT_STRICT;
+    const int64_t shape[2] = {rows, cols};
+    Fail f = validate(NORMPRE_VARIANT_NORMALIZE_ONLY, 1, shape, &h);
+    if (f.code) return set_err(ctx, f.code, f.msg);
+    const int k = orientation_of(h);
+    const Dims d = dims_of(rows, cols, k, h);
+    if (d.a > kMaxExactRows)
+        return set_err(ctx, NORMPRE_ERR_UNSUPPORTED,
+                       fmt("spectrum of %lld active rows exceeds %lld", (long long)d.a, (long long)kMaxExactRows));
+    const uintptr_t nbytes = (uintptr_t)(rows * cols) * 4u;
+    if ((uintptr_t)w < (uintptr_t)m + nbytes && (uintptr_t)m < (uintptr_t)w + nbytes)
+        return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "W and M overlap");
+    hipError_t e = hipSetDevice(ctx->device);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool gx = which == NORMPRE_SPECTRUM_GX;
+    const int64_t a = d.a, ap = d.a_pad;
+    Item it;
+    it.count = 1;
+    it.d = d;
+    auto carve = [&](Arena& ar, float*& mcopy) {
+        carve_item(ar, it, NORMPRE_VARIANT_NORMALIZE_ONLY, false);
+        GWork& g = it.w;
+        if (gx) {
+            g.xs = ar.take<half_t>(d.mp * d.np_);
+            g.xsq = ar.take<float>(d.lp_);
+            g.xtot = ar.take<float>(2);
+        }
+        g.gam32 = ar.take<float>(ap * ap);
+        g.tw.A = ar.take<double>(a * a);
+        g.tw.vec = ar.take<double>(4 * a);
+        g.tw.d = ar.take<double>(a);
+        g.tw.e = ar.take<double>(a);
+        g.tw.tau = ar.take<double>(a);
+        g.lam = ar.take<double>(a);
+        mcopy = ar.take<float>(rows * cols);
+        return ar.off + 256;
+    };
+    float* mcopy = nullptr;
+    Arena probe{nullptr, 0, 0};
+    int rc = ensure_workspace(ctx, carve(probe, mcopy), s);
+    if (rc) return rc;
+    Arena ar{static_cast<char*>(ctx->ws), 0, ctx->ws_bytes};
+    carve(ar, mcopy);
+    ctx->timing = false;
+    ctx->stream = s;
+    std::vector<Group> groups{{rows, cols, {0}}};
+    float* Wl[1] = {const_cast<float*>(w)};    // read only: the normalization reads W
+    const float* Gl[1] = {m};
+    float* Ml[1] = {mcopy};
+    StepCtx sc{ctx, s, &h, Wl, Gl, Ml, NORMPRE_VARIANT_NORMALIZE_ONLY, false, &groups};
+    NP_TRY(launch_fill_zero(mcopy, rows * cols * 4, s), "clear momentum copy");
+    rc = run_normalize(sc, d, it.w, groups[0].idx, 0, 1, nullptr);
+    if (rc) return rc;
+    const half_t* src = gx ? it.w.xs : it.w.psi;
+    {
+        const int64_t mn = d.mp * d.np_;
+        Operand A{src, d.np_, mn}, B{src, d.np_, mn};
+        GemmShape sh{(int)ap, (int)ap, (int)d.b_pad, 1, (int)d.b_pad, 0};
+        EpiPartial ep{};
+        ep.out = it.w.gam32;
+        ep.ld_out = ap;
+        ep.stride_mat = ap * ap;
+        NP_TRY(launch_gemm_gram_f32(k == 0 ? 0 : 2, A, B, sh, 1, ep, s), "spectrum gram");
+    }
+    NP_TRY(launch_gamma_to_f64(it.w.gam32, ap, ap * ap, (int)a, it.w.tw.A, 1, s), "spectrum gram f64");
+    NP_TRY(launch_tridiagonalize(it.w.tw, (int)a, 1, s), "tridiagonalize");
+    NP_TRY(launch_tri_eigvals(it.w.tw, (int)a, 0, (int)a, it.w.lam, a, 1, s), "bisection");
+    NP_TRY(hipMemcpyAsync(eigs, it.w.lam, (size_t)a * sizeof(double), hipMemcpyDeviceToHost, s), "copy eigenvalues");
+    NP_TRY(hipStreamSynchronize(s), "hipStreamSynchronize");
+    ctx->last_stream = s;
+    ctx->have_stream = true;
+    return NORMPRE_OK;
+}
+
+int normpre_energy_split(const double* eigs, int64_t count, int32_t rank, double* out) {
+    if (!eigs || !out || count < 0 || rank < 0)
+        return set_err(nullptr, NORMPRE_ERR_INVALID_ARG, "null pointer or negative count / rank");
+    double top = 0.0, remain = 0.0, sub = 0.0;
+    int32_t taken = 0;
+    for (int64_t i = 0; i < count; ++i) {
+        const double lam = eigs[i];
+        if (!(lam > 0.0)) continue;
+        const double r = std::sqrt(lam) - 1.0, e = r * r;
+        if (lam > 1.0) {
+            if (taken < rank) {
+                top += e;
+                ++taken;
+            } else {
+                remain += e;
+            }
+        } else if (lam < 1.0) {
+            sub += e;
+        }
+    }
+    out[0] = top;
+    out[1] = remain;
+    out[2] = sub;
+    out[3] = top + remain + sub;
+    return NORMPRE_OK;
+}
+
 int normpre_debug_fetch(normpre_ctx* ctx, int index, int what, void* host_out, int64_t capacity, int64_t* written) {
     if (!ctx) return set_err(nullptr, NORMPRE_ERR_NOT_INITIALIZED, "context is null");
     if (written) *written = 0;

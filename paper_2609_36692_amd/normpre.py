@@ -40,6 +40,9 @@ NORMPRE_FLAG_TANGENT_STRICT = 8
 NORMPRE_FLAG_L_EXACT = 16
 NORMPRE_FLAG_SOURCE_X = 32
 
+NORMPRE_SPECTRUM_GAMMA = 0
+NORMPRE_SPECTRUM_GX = 1
+
 NORMPRE_DEBUG_PSI = 0
 NORMPRE_DEBUG_T = 1
 NORMPRE_DEBUG_RITZ = 2
@@ -116,6 +119,10 @@ def load_library(path: str = LIB_PATH):
                                                 ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                                                 ctypes.c_int]),
         "normpre_version": (ctypes.c_char_p, []),
+        "normpre_spectrum": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int64, ctypes.c_int64, P, P, hpp,
+                                            ctypes.POINTER(ctypes.c_double), P]),
+        "normpre_energy_split": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.c_int64, ctypes.c_int32,
+                                                ctypes.POINTER(ctypes.c_double)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -228,6 +235,33 @@ def normpre_kernel_stats(ctx, kclass: int, reset: bool = False) -> dict:
                                                ctypes.byref(flops), ctypes.byref(nbytes), int(bool(reset)))
     _check(code, ctx)
     return {"launches": launches.value, "ms": ms.value, "flops": flops.value, "bytes": nbytes.value}
+
+
+def normpre_spectrum(ctx, which: int, w, m, hp: normpre_hparams, stream=None) -> np.ndarray:
+    """Eigenvalues (descending) of Gamma or of the trace-matched G_X of one
+    matrix in hp's active orientation; w, m: 2-D fp32 device tensors."""
+    rows, cols = (int(v) for v in w.shape)
+    a = rows if (hp.orientation == NORMPRE_ORIENT_ROW or
+                 (hp.orientation == NORMPRE_ORIENT_ALTERNATING and hp.step % 2 == 0)) else cols
+    out = np.empty(a, dtype=np.float64)
+    code = load_library().normpre_spectrum(ctx, int(which), rows, cols, ctypes.c_void_p(_ptr(w)),
+                                           ctypes.c_void_p(_ptr(m)), ctypes.byref(hp),
+                                           out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                                           _stream_handle(stream))
+    _check(code, ctx)
+    return out
+
+
+def normpre_energy_split(eigs, count: int, rank: int) -> np.ndarray:
+    """[E_top, E_remain, E_sub, E_global] of the first `count` eigenvalues."""
+    e = np.ascontiguousarray(np.asarray(eigs, dtype=np.float64))
+    if count > e.size:
+        raise ValueError("count exceeds the number of eigenvalues")
+    out = np.zeros(4, dtype=np.float64)
+    code = load_library().normpre_energy_split(e.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), int(count),
+                                               int(rank), out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    _check(code)
+    return out
 
 
 class NormPre:

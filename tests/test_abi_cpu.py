@@ -166,3 +166,18 @@ def test_header_constants_match_binding(N):
     assert not missing, missing
     for k, v in consts.items():
         assert getattr(N, k) == int(v), (k, getattr(N, k), v)
+
+
+def test_energy_split_host_matches_oracle(N):
+    # Host-only entry point: no GPU involved.
+    import numpy as np
+    from oracle import normpre_oracle as O
+    rng = np.random.default_rng(5)
+    lam = np.sort(np.concatenate([rng.uniform(1.0, 30.0, 40), rng.uniform(0.0, 1.0, 60), [1.0, 0.0, -1e-9]]))[::-1]
+    for count, r in [(len(lam), 32), (len(lam), 0), (50, 100), (0, 5)]:
+        got = N.normpre_energy_split(lam, count, r)
+        want = O.energy_split(lam, count, r)
+        np.testing.assert_allclose(got, [want["top"], want["remain"], want["sub"], want["global"]], rtol=1e-13,
+                                   atol=1e-13)
+    with pytest.raises(N.NormPreError):
+        N.normpre_energy_split(lam, -1, 3)

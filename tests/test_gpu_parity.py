@@ -374,3 +374,38 @@ def test_l_exact_matches_oracle(ctx, shape, t):
     ev = np.sort(np.linalg.eigvalsh(psi_act @ psi_act.T))[::-1][:16]
     nsel = int(N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_NSEL, 1, np.int32)[0])
     assert int(np.sum(ev > 1.01)) <= nsel <= int(np.sum(ev > 0.99))
+
+
+# ------------------------------------------------- spectral diagnostics (App. A)
+@pytest.mark.parametrize("shape,t,which", [((300, 200), 0, "gamma"), ((300, 200), 1, "gamma"), ((300, 200), 0, "gx"),
+                                           ((768, 2304), 0, "gamma"), ((768, 2304), 0, "gx"),
+                                           ((1000, 300), 0, "gamma"), ((1000, 300), 1, "gx")])
+def test_spectrum_matches_oracle(ctx, shape, t, which):
+    _say(f"spectrum {which} shape={shape} t={t}")
+    w, g, mp = _inputs(shape, "lowrank", seed=13)
+    # unequal row scales so that the spectra before and after normalization differ
+    m = (0.95 * mp + g) * torch.linspace(0.3, 3.0, shape[0])[:, None]
+    hp = N.normpre_default_hparams(step=t)
+    dev = torch.device("cuda:0")
+    eig = N.normpre_spectrum(ctx, N.NORMPRE_SPECTRUM_GAMMA if which == "gamma" else N.NORMPRE_SPECTRUM_GX,
+                             w.to(dev), m.to(dev), hp)
+    k = t % 2
+    x = O.momentum_processing(O.orient(m.double().numpy(), k), O.orient(w.double().numpy(), k))
+    ref = O.interaction_spectrum(x, normalized=(which == "gamma"))
+    a = x.shape[0]
+    assert eig.shape == (a,)
+    assert np.all(np.diff(eig) <= 1e-9 * ref[0])
+    # Weyl: the fp16 rounding of Psi (|delta| <= u |psi| elementwise, ||Psi||_F^2 = a)
+    # moves every eigenvalue by at most 2 u sqrt(lambda_max a); fp32 accumulation adds ~1e-6.
+    tol = 2.0 * U16 * math.sqrt(ref[0] * a) + 1e-6 * ref[0]
+    err = float(np.max(np.abs(eig - ref)))
+    _say(f"  max eigenvalue error {err:.2e} (tol {tol:.1e}), lambda_max {ref[0]:.3f}")
+    assert err < tol
+    assert abs(eig.sum() - a) < 1e-3 * a
+    count = min(shape)
+    got = N.normpre_energy_split(eig, count, 32)
+    want = O.energy_split(ref, count, 32)
+    _say(f"  E_top/E_remain/E_sub {got[0]:.4g}/{got[1]:.4g}/{got[2]:.4g} vs {want['top']:.4g}/{want['remain']:.4g}/{want['sub']:.4g}")
+    assert math.isclose(got[3], want["global"], rel_tol=1e-2)
+    assert math.isclose(got[0], want["top"], rel_tol=1e-2, abs_tol=1e-3 * want["global"])
+    assert math.isclose(got[2], want["sub"], rel_tol=2e-2, abs_tol=1e-3 * want["global"])

@@ -500,3 +500,42 @@ def test_muon_invariances():
     m3[2] *= 10.0
     r3 = O.normpre_step(w, g3, m3, 0, hp, "MUON")
     assert O.relative_fro(r3["update"], r["update"]) > 1e-2
+
+
+# ------------------------------------------------- spectral diagnostics (App. A)
+def test_interaction_spectrum_worked_example():
+    rows = [l.split() for l in open(os.path.join(GOLDEN, "orthogonal_rows_example.txt"))
+            if l.strip() and not l.startswith("#")]
+    a = np.array([float(r[0]) for r in rows])
+    q, _ = np.linalg.qr(_rand(6, 4))
+    x = a[:, None] * q.T
+    before = O.interaction_spectrum(x, normalized=False)
+    after = O.interaction_spectrum(x, normalized=True)
+    assert np.allclose(before, sorted((float(r[1]) for r in rows), reverse=True))
+    assert np.allclose(after, [float(r[2]) for r in rows])
+    assert abs(before.sum() - 4.0) < 1e-12 and abs(after.sum() - 4.0) < 1e-12   # both have trace d
+    split = O.energy_split(after, 4, 32)
+    assert split["global"] < 1e-24                        # Gamma = I: nothing to transform
+
+
+@pytest.mark.parametrize("shape,r", [((30, 70), 4), ((50, 20), 3), ((40, 40), 100)])
+def test_energy_split_closed_forms(shape, r):
+    # Low-rank-plus-noise rows: several singular values of Psi above one,
+    # the rest below.
+    x = _rand(shape[0], 5) @ _rand(5, shape[1]) + 0.3 * _rand(*shape)
+    psi = O.diagonal_gram_normalize(x)
+    lam = O.interaction_spectrum(x, normalized=True)
+    count = min(shape)
+    split = O.energy_split(lam, count, r)
+    # Global preconditioning sends every singular value to one: the total is
+    # the squared distance of Psi to its polar factor.
+    assert math.isclose(split["global"], np.linalg.norm(psi - O.msign_svd(psi)) ** 2, rel_tol=1e-9)
+    # Localized preconditioning changes exactly the modes of C: E_top is the
+    # squared distance of Psi to the exact NormPre-L output.
+    u_sel, lam_sel = O.localized_exact(psi, r)
+    t_loc = O.localized_apply(psi, u_sel, lam_sel)
+    assert math.isclose(split["top"], np.linalg.norm(psi - t_loc) ** 2, rel_tol=1e-9, abs_tol=1e-18)
+    # Brute force over the singular values.
+    sv = np.linalg.svd(psi, compute_uv=False)
+    assert math.isclose(split["sub"], float(np.sum((sv[(sv > 1e-9) & (sv < 1)] - 1) ** 2)), rel_tol=1e-9)
+    assert math.isclose(split["top"] + split["remain"], float(np.sum((sv[sv > 1] - 1) ** 2)), rel_tol=1e-9)
