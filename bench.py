@@ -145,7 +145,9 @@ def time_variant(N, WL, torch, wl, variant, steps, warmup, rank):
     ws, gs, ms = WL.make_stack(wl, dev)
     torch.cuda.synchronize()
     ctx = N.normpre_init(0)
-    v = N.VARIANTS[variant]
+    # LX: NormPre-L Exact (the leading eigenpairs of the full interaction matrix).
+    v = N.VARIANTS["L" if variant == "LX" else variant]
+    base_flags = N.NORMPRE_FLAG_L_EXACT if variant == "LX" else 0
     hp = N.normpre_default_hparams(lr=wl.lr, rank=rank, oversample=wl.oversample,
                                    power_iters=wl.power_iters)
     t = 0
@@ -154,7 +156,7 @@ def time_variant(N, WL, torch, wl, variant, steps, warmup, rank):
         nonlocal t
         for _ in range(n):
             hp.step = t
-            hp.flags = flags
+            hp.flags = flags | base_flags
             N.normpre_step(ctx, v, ws, gs, ms, hp)
             t += 1
 
@@ -315,6 +317,10 @@ def main():
         elif v == "NORM":
             roof = roofline_of(cls["normalize"], "hbm")
             roof["kernel"] = "momentum + tangent + normalization"
+        elif v == "LX":
+            roof = roofline_of(cls["eigen"], "hbm")
+            roof["kernel"] = ("dense eigensolver (fp64 tridiagonal reduction: one read + write of the trailing "
+                              "block per step; bisection, inverse iteration)")
         else:
             roof = roofline_of(cls["sk_stream"], "hbm")
             roof["kernel"] = "sketch products streaming Psi (fp16 MFMA, split-K)"

@@ -284,7 +284,8 @@ int normpre_sketch_omega(uint64_t seed, int64_t step, int32_t matrix_id,
 #define NORMPRE_KCLASS_SK_STREAM   5  /* sketch products streaming Psi               */
 #define NORMPRE_KCLASS_SK_SMALL    6  /* Omega, reductions, CholQR, eigensolver      */
 #define NORMPRE_KCLASS_L_APPLY     7  /* localized apply + RMS + weight update       */
-#define NORMPRE_KCLASS_COUNT       8
+#define NORMPRE_KCLASS_EIGEN       8  /* dense eigensolver of exact NormPre-L        */
+#define NORMPRE_KCLASS_COUNT       9
 
 /*
  * Per-kernel-class totals since the last reset, over steps made with

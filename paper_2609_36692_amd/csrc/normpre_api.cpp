@@ -1125,17 +1125,20 @@ int exact_front(const StepCtx& sc, const Item& it, DebugMat* dbg) {
                      [&] { return launch_gemm_gram_f32(d.k == 0 ? 0 : 2, A, B, sh, count, e, sc.s); }),
                "exact gamma");
     }
-    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_EIGEN, 0.0, 0.0,
                  [&] { return launch_gamma_to_f64(w.gam32, ap, ap * ap, (int)a, w.tw.A, count, sc.s); }),
            "exact gamma f64");
-    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+    // Algorithmic bytes of the reduction: step j reads and writes the
+    // (a - j - 1)^2 trailing fp64 block once.
+    const double tri_bytes = 16.0 * ((double)(a - 1) * a * (2 * a - 1) / 6.0) * count;
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_EIGEN, 0.0, tri_bytes,
                  [&] { return launch_tridiagonalize(w.tw, (int)a, count, sc.s); }),
            "tridiagonalize");
-    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_EIGEN, 0.0, 0.0,
                  [&] { return launch_tri_eigvals(w.tw, (int)a, 0, d.ell, w.lam, d.ell, count, sc.s); }),
            "bisection");
     const int64_t lp = d.ellp, maxpad = d.lp_;
-    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_EIGEN, 0.0, 0.0,
                  [&] {
                      return launch_tri_eigvecs(w.tw, (int)a, w.lam, d.ell, w.v32[0], ap, (int)lp, lp * maxpad, count,
                                                sc.s);

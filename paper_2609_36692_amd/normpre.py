@@ -59,9 +59,10 @@ NORMPRE_KCLASS_G_UPDATE = 4
 NORMPRE_KCLASS_SK_STREAM = 5
 NORMPRE_KCLASS_SK_SMALL = 6
 NORMPRE_KCLASS_L_APPLY = 7
-NORMPRE_KCLASS_COUNT = 8
+NORMPRE_KCLASS_EIGEN = 8
+NORMPRE_KCLASS_COUNT = 9
 KCLASS_NAMES = ["normalize", "ns_gram", "ns_poly", "ns_combine", "g_update",
-                "sk_stream", "sk_small", "l_apply"]
+                "sk_stream", "sk_small", "l_apply", "eigen"]
 
 
 class NormPreError(RuntimeError):
