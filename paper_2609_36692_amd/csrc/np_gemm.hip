@@ -235,7 +235,11 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     // i + 1 and the global loads of stage i + 2.  The epilogue reuses the
     // same LDS to stage one wave-row of fp32 results (row stride BN + 4).
     constexpr int kStageBytes = 2 * (BM + BN) * BK * 2;
-    constexpr int kEpiBytes = (BM / WM) * (BN + 4) * 4;
+    // Result rows staged per epilogue pass: the whole tile when its fp32
+    // staging adds little to the operand stages (up to 128 x 128), else one
+    // wave-row.
+    constexpr int kEpiRows = BM * BN <= 128 * 128 ? BM : BM / WM;
+    constexpr int kEpiBytes = kEpiRows * (BN + 4) * 4;
     constexpr bool kLdsMirror = BM * BN <= 128 * 128;
     __shared__ __attribute__((aligned(16))) unsigned char smem[kStageBytes > kEpiBytes ? kStageBytes : kEpiBytes];
     __shared__ float red[NT / 64];
@@ -508,24 +512,44 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                 w = epi.ptrs.w[z];
             }
         }
-        // Stage one wave-row (TM x BN fp32) at a time in LDS, then walk it
+        // Stage PR rows of fp32 results at a time in LDS (the whole tile at
+        // once when it fits, else one wave-row per pass), then walk them
         // row-contiguously: 8 columns per item (16-byte fp16 accesses).
         constexpr int LDST = BN + 4;
         constexpr int C8 = BN / 8;
+        constexpr int PR = kEpiRows;
+        constexpr int WPP = PR / TM;                // wave-rows per pass
         float* stg = reinterpret_cast<float*>(smem);
         float ss = 0.f;
 #pragma unroll 1
-        for (int pass = 0; pass < WM; ++pass) {
+        for (int pass = 0; pass < BM / PR; ++pass) {
+            constexpr int ITEMS = (PR * C8 + NT - 1) / NT;
+            // Affine: this pass's src rows are loaded before the staging
+            // barriers, so their latency overlaps the LDS traffic.
+            constexpr int SB = Epi::kind == EpiKind::Affine && !IsGrouped<Epi>::value ? ITEMS : 1;
+            u32x4 sbuf[SB];
+            if constexpr (Epi::kind == EpiKind::Affine) {
+                if (src) {
+#pragma unroll
+                    for (int q = 0; q < SB; ++q) {
+                        const int c = tid + q * NT;
+                        if (c < PR * C8) {
+                            const int r = c / C8, c8 = (c - r * C8) * 8;
+                            sbuf[q] = *reinterpret_cast<const u32x4*>(src + (int64_t)(m0 + pass * PR + r) * epi.ld_src +
+                                                                      n0 + c8);
+                        }
+                    }
+                }
+            }
             lds_barrier();
-            if (wm == pass) {
+            if (wm / WPP == pass) {
 #pragma unroll
                 for (int qi = 0; qi < NQ; ++qi)
 #pragma unroll
                     for (int r = 0; r < 4; ++r)
-                        stg[(quad_row(qi) + r) * LDST + wn * TN + quad_col(qi)] = quad_val(qi, r);
+                        stg[((wm % WPP) * TM + quad_row(qi) + r) * LDST + wn * TN + quad_col(qi)] = quad_val(qi, r);
             }
             lds_barrier();
-            constexpr int ITEMS = (TM * C8 + NT - 1) / NT;
             if constexpr (Epi::kind == EpiKind::Apply || Epi::kind == EpiKind::ApplyNorm) {
                 // Issue every item's Psi (and W) loads before using any of them.
                 u32x4 pbuf[ITEMS];
@@ -535,8 +559,8 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                 for (int it = 0; it < ITEMS; ++it) {
                     const int c = tid + it * NT;
                     const int r = c / C8, c8 = (c - r * C8) * 8;
-                    const int grow = m0 + pass * TM + r, gcol = n0 + c8;
-                    okv[it] = c < TM * C8 && grow < epi.rows && gcol < epi.cols;
+                    const int grow = m0 + pass * PR + r, gcol = n0 + c8;
+                    okv[it] = c < PR * C8 && grow < epi.rows && gcol < epi.cols;
                     if (okv[it]) {
                         pbuf[it] = *reinterpret_cast<const u32x4*>(psi + (int64_t)grow * epi.ld_psi + gcol);
                         if constexpr (Epi::kind == EpiKind::Apply) {
@@ -553,7 +577,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                     if (!okv[it]) continue;
                     const int c = tid + it * NT;
                     const int r = c / C8, c8 = (c - r * C8) * 8;
-                    const int grow = m0 + pass * TM + r, gcol = n0 + c8;
+                    const int grow = m0 + pass * PR + r, gcol = n0 + c8;
                     const f32x4 lo = *reinterpret_cast<const f32x4*>(stg + r * LDST + c8);
                     const f32x4 hi = *reinterpret_cast<const f32x4*>(stg + r * LDST + c8 + 4);
                     const half_t* pv = reinterpret_cast<const half_t*>(&pbuf[it]);
@@ -588,37 +612,18 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                 }
                 continue;
             }
-            // Issue a batch of items' src loads before using any of them.
-            constexpr int SB = ITEMS > 4 ? 4 : ITEMS;
             u32x4 hk[kLdsMirror ? ITEMS : 1];      // fp16 results, kept for the mirror
-#pragma unroll (kLdsMirror ? 8 : 1)
-            for (int it0 = 0; it0 < ITEMS; it0 += SB) {
-            u32x4 sbuf[SB];
-            if constexpr (Epi::kind == EpiKind::Affine) {
-                if (src) {
 #pragma unroll
-                    for (int q = 0; q < SB; ++q) {
-                        const int c = tid + (it0 + q) * NT;
-                        if (c < TM * C8) {
-                            const int r = c / C8, c8 = (c - r * C8) * 8;
-                            sbuf[q] = *reinterpret_cast<const u32x4*>(src + (int64_t)(m0 + pass * TM + r) * epi.ld_src +
-                                                                      n0 + c8);
-                        }
-                    }
-                }
-            }
-#pragma unroll
-            for (int q = 0; q < SB; ++q) {
-                const int it = it0 + q;
+            for (int it = 0; it < ITEMS; ++it) {
                 const int c = tid + it * NT;
-                if (c >= TM * C8) break;
+                if (c >= PR * C8) break;
                 const int r = c / C8, c8 = (c - r * C8) * 8;
-                const int grow = m0 + pass * TM + r, gcol = n0 + c8;
+                const int grow = m0 + pass * PR + r, gcol = n0 + c8;
                 const f32x4 lo = *reinterpret_cast<const f32x4*>(stg + r * LDST + c8);
                 const f32x4 hi = *reinterpret_cast<const f32x4*>(stg + r * LDST + c8 + 4);
                 float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
                 if constexpr (Epi::kind == EpiKind::Affine) {
-                    const half_t* sv = reinterpret_cast<const half_t*>(&sbuf[q]);
+                    const half_t* sv = reinterpret_cast<const half_t*>(&sbuf[it < SB ? it : 0]);
                     half_t hv[8];
 #pragma unroll
                     for (int e = 0; e < 8; ++e) {
@@ -636,34 +641,33 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                     __builtin_nontemporal_store(hq, reinterpret_cast<u32x4*>(out + (int64_t)grow * epi.ld_out + gcol));
                 }
             }
-            }
             if constexpr (Epi::kind == EpiKind::Affine && kLdsMirror) {
                 if (mirror) {
-                    // T[c][r] = result[r][c] for this pass's TM rows: row c of
-                    // T holds TM halves in chunks of 8, chunk j stored at
-                    // j ^ (c / 8 mod TM / 8) so the 2-byte writes of one
+                    // T[c][r] = result[r][c] for this pass's PR rows: row c of
+                    // T holds PR halves in chunks of 8, chunk j stored at
+                    // j ^ (c / 8 mod PR / 8) so the 2-byte writes of one
                     // wave spread over the banks; then 16-byte rows out.
-                    constexpr int R8 = TM / 8;
+                    constexpr int R8 = PR / 8;
                     half_t* tb = reinterpret_cast<half_t*>(smem);
                     lds_barrier();
 #pragma unroll
                     for (int it = 0; it < ITEMS; ++it) {
                         const int c = tid + it * NT;
-                        if (c >= TM * C8) break;
+                        if (c >= PR * C8) break;
                         const int r = c / C8, c8 = (c - r * C8) * 8;
                         const half_t* hv = reinterpret_cast<const half_t*>(&hk[it]);
 #pragma unroll
                         for (int e = 0; e < 8; ++e) {
                             const int cc = c8 + e;
-                            tb[cc * TM + (((r >> 3) ^ ((cc >> 3) & (R8 - 1))) << 3) + (r & 7)] = hv[e];
+                            tb[cc * PR + (((r >> 3) ^ ((cc >> 3) & (R8 - 1))) << 3) + (r & 7)] = hv[e];
                         }
                     }
                     lds_barrier();
                     for (int q = tid; q < BN * R8; q += NT) {
                         const int cc = q / R8, j = q - cc * R8;
-                        const u32x4 v = *reinterpret_cast<const u32x4*>(tb + cc * TM + ((j ^ ((cc >> 3) & (R8 - 1))) << 3));
+                        const u32x4 v = *reinterpret_cast<const u32x4*>(tb + cc * PR + ((j ^ ((cc >> 3) & (R8 - 1))) << 3));
                         __builtin_nontemporal_store(
-                            v, reinterpret_cast<u32x4*>(out + (int64_t)(n0 + cc) * epi.ld_out + m0 + pass * TM + 8 * j));
+                            v, reinterpret_cast<u32x4*>(out + (int64_t)(n0 + cc) * epi.ld_out + m0 + pass * PR + 8 * j));
                     }
                 }
             }
@@ -773,10 +777,10 @@ hipError_t launch_gemm_affine(TileCfg cfg, int layout, Operand A, Operand B, Gem
             case 2: return run<128, 128, 2, 2, 2>(A, B, sh, batch, ee, s);
         }
     } else if (cfg == TileCfg::Big256) {
+        // (Layout 2 on this tile serves the grouped Gram only.)
         switch (layout) {
             case 0: return run<256, 256, 2, 4, 0, EAff, 32>(A, B, sh, batch, ee, s);
             case 1: return run<256, 256, 2, 4, 1, EAff, 32>(A, B, sh, batch, ee, s);
-            case 2: return run<256, 256, 2, 4, 2, EAff, 32>(A, B, sh, batch, ee, s);
         }
     }
     return hipErrorInvalidValue;
