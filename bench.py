@@ -319,7 +319,7 @@ def main():
             roof["kernel"] = "momentum + tangent + normalization"
         elif v == "LX":
             roof = roofline_of(cls["eigen"], "hbm")
-            roof["kernel"] = ("dense eigensolver (fp64 tridiagonal reduction: one read + write of the trailing "
+            roof["kernel"] = ("dense eigensolver (tridiagonal reduction, fp32 storage / fp64 arithmetic: one read + write of the trailing "
                               "block per step; bisection, inverse iteration)")
         else:
             roof = roofline_of(cls["sk_stream"], "hbm")

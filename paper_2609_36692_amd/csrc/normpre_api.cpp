@@ -428,7 +428,7 @@ void carve_item(Arena& ar, Item& it, int variant, bool source_x) {
         if (d.xl) {
             const int64_t a = d.a;
             w.gam32 = ar.take<float>(count * d.a_pad * d.a_pad);
-            w.tw.A = ar.take<double>(count * a * a);
+            w.tw.A = ar.take<float>(count * a * a);
             w.tw.vec = ar.take<double>(count * 4 * a);
             w.tw.d = ar.take<double>(count * a);
             w.tw.e = ar.take<double>(count * a);
@@ -1126,11 +1126,11 @@ int exact_front(const StepCtx& sc, const Item& it, DebugMat* dbg) {
                "exact gamma");
     }
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_EIGEN, 0.0, 0.0,
-                 [&] { return launch_gamma_to_f64(w.gam32, ap, ap * ap, (int)a, w.tw.A, count, sc.s); }),
-           "exact gamma f64");
+                 [&] { return launch_gamma_sym(w.gam32, ap, ap * ap, (int)a, w.tw.A, count, sc.s); }),
+           "exact gamma");
     // Algorithmic bytes of the reduction: step j reads and writes the
-    // (a - j - 1)^2 trailing fp64 block once.
-    const double tri_bytes = 16.0 * ((double)(a - 1) * a * (2 * a - 1) / 6.0) * count;
+    // (a - j - 1)^2 trailing fp32 block once.
+    const double tri_bytes = 8.0 * ((double)(a - 1) * a * (2 * a - 1) / 6.0) * count;
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_EIGEN, 0.0, tri_bytes,
                  [&] { return launch_tridiagonalize(w.tw, (int)a, count, sc.s); }),
            "tridiagonalize");
@@ -1584,7 +1584,7 @@ int normpre_spectrum(normpre_ctx* ctx, int which, int64_t rows, int64_t cols, co
             g.xtot = ar.take<float>(2);
         }
         g.gam32 = ar.take<float>(ap * ap);
-        g.tw.A = ar.take<double>(a * a);
+        g.tw.A = ar.take<float>(a * a);
         g.tw.vec = ar.take<double>(4 * a);
         g.tw.d = ar.take<double>(a);
         g.tw.e = ar.take<double>(a);
@@ -1620,7 +1620,7 @@ int normpre_spectrum(normpre_ctx* ctx, int which, int64_t rows, int64_t cols, co
         ep.stride_mat = ap * ap;
         NP_TRY(launch_gemm_gram_f32(k == 0 ? 0 : 2, A, B, sh, 1, ep, s), "spectrum gram");
     }
-    NP_TRY(launch_gamma_to_f64(it.w.gam32, ap, ap * ap, (int)a, it.w.tw.A, 1, s), "spectrum gram f64");
+    NP_TRY(launch_gamma_sym(it.w.gam32, ap, ap * ap, (int)a, it.w.tw.A, 1, s), "spectrum gram");
     NP_TRY(launch_tridiagonalize(it.w.tw, (int)a, 1, s), "tridiagonalize");
     NP_TRY(launch_tri_eigvals(it.w.tw, (int)a, 0, (int)a, it.w.lam, a, 1, s), "bisection");
     NP_TRY(hipMemcpyAsync(eigs, it.w.lam, (size_t)a * sizeof(double), hipMemcpyDeviceToHost, s), "copy eigenvalues");

@@ -1,10 +1,11 @@
 // Dense symmetric eigensolver on the GPU, for the interaction matrix
 // Gamma = Psi Psi^T of one active orientation (n = active rows, up to a few
 // thousand):
-//   * Householder reduction to tridiagonal form, fp64, one reflector per
-//     step: a one-block kernel forms the reflector of column j, and one
-//     streaming pass over the trailing rows applies the previous step's
-//     rank-2 update and forms the next product p = tau A v in the same read;
+//   * Householder reduction to tridiagonal form (working matrix stored in
+//     fp32, all arithmetic and the vectors in fp64), one reflector per step:
+//     a one-block kernel forms the reflector of column j, and one streaming
+//     pass over the trailing rows applies the previous step's rank-2 update
+//     and forms the next product p = tau A v in the same read;
 //   * eigenvalues of the tridiagonal matrix by bisection on Sturm counts
 //     (one thread per eigenvalue, any subset of indices);
 //   * eigenvectors of the selected eigenvalues by inverse iteration with a
@@ -45,16 +46,16 @@ __device__ double block_sum_d(double v, double* red) {
     return t;
 }
 
-// Gamma fp32 (GEMM output, ld ldg) -> symmetrized fp64 n x n (ld n).
-__global__ void gamma_to_f64_kernel(const float* g, int64_t ldg, int64_t strideg, int n, double* A,
-                                    int64_t strideA) {
+// Gamma fp32 (GEMM output, ld ldg) -> symmetrized n x n (ld n).
+__global__ void gamma_sym_kernel(const float* g, int64_t ldg, int64_t strideg, int n, float* A,
+                                 int64_t strideA) {
     const int z = blockIdx.y;
     const float* gz = g + (int64_t)z * strideg;
-    double* Az = A + (int64_t)z * strideA;
+    float* Az = A + (int64_t)z * strideA;
     const int64_t nn = (int64_t)n * n;
     for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < nn; idx += (int64_t)gridDim.x * blockDim.x) {
         const int64_t i = idx / n, k = idx - i * n;
-        Az[idx] = 0.5 * ((double)gz[i * ldg + k] + (double)gz[k * ldg + i]);
+        Az[idx] = (float)(0.5 * ((double)gz[i * ldg + k] + (double)gz[k * ldg + i]));
     }
 }
 
@@ -64,18 +65,18 @@ __global__ void gamma_to_f64_kernel(const float* g, int64_t ldg, int64_t strideg
 // takes column j of the current matrix as row j of A (not yet updated by
 // step j - 1) minus that step's rank-2 term.  v_j (v_j[j + 1] = 1, zero at
 // indices <= j) is also stored in row j of A for the back-transformation.
-__global__ void __launch_bounds__(kHouseThreads) tri_house_kernel(double* A, int64_t strideA, int n, int j,
+__global__ void __launch_bounds__(kHouseThreads) tri_house_kernel(float* A, int64_t strideA, int n, int j,
                                                                   double* vec, int64_t stride_vec, double* dd,
                                                                   double* ee, double* tau, int64_t stride_n) {
     __shared__ double red[kHouseThreads / 64];
     const int z = blockIdx.x, tid = threadIdx.x;
-    double* Az = A + (int64_t)z * strideA;
+    float* Az = A + (int64_t)z * strideA;
     double* V = vec + (int64_t)z * stride_vec;
     double* vprev = V + (int64_t)((j + 1) & 1) * n;
     double* vcur = V + (int64_t)(j & 1) * n;
     double* W = V + 2 * (int64_t)n;
     const double* P = V + 3 * (int64_t)n;
-    double* row = Az + (int64_t)j * n;
+    float* row = Az + (int64_t)j * n;
     double wj = 0.0, vj = 0.0;
     if (j > 0) {
         const double tp = tau[(int64_t)z * stride_n + j - 1];
@@ -88,7 +89,10 @@ __global__ void __launch_bounds__(kHouseThreads) tri_house_kernel(double* A, int
         wj = W[j];
         vj = vprev[j];
     }
-    auto col = [&](int i) -> double { return j > 0 ? row[i] - vprev[i] * wj - W[i] * vj : row[i]; };
+    auto col = [&](int i) -> double {
+        const double r = row[i];
+        return j > 0 ? r - vprev[i] * wj - W[i] * vj : r;
+    };
     const double dj = col(j);
     const double alpha = j + 1 < n ? col(j + 1) : 0.0;
     double sig = 0.0;
@@ -106,7 +110,7 @@ __global__ void __launch_bounds__(kHouseThreads) tri_house_kernel(double* A, int
     for (int i = tid; i < n; i += kHouseThreads) {
         const double v = i <= j ? 0.0 : (i == j + 1 ? 1.0 : col(i) * scal);
         vcur[i] = v;
-        if (i > j) row[i] = v;
+        if (i > j) row[i] = (float)v;
     }
     if (tid == 0) {
         dd[(int64_t)z * stride_n + j] = dj;
@@ -118,7 +122,7 @@ __global__ void __launch_bounds__(kHouseThreads) tri_house_kernel(double* A, int
 // Rows i > j: A[i, k] -= v_{j-1}[i] w[k] + w[i] v_{j-1}[k] for k > j (step
 // j - 1's update, skipped for j = 0), then p[i] = tau_j sum_k A[i, k] v_j[k]
 // over the updated row.  One wave per row.
-__global__ void __launch_bounds__(kRowWaves * 64) tri_update_kernel(double* A, int64_t strideA, int n, int j,
+__global__ void __launch_bounds__(kRowWaves * 64) tri_update_kernel(float* A, int64_t strideA, int n, int j,
                                                                     double* vec, int64_t stride_vec,
                                                                     const double* tau, int64_t stride_n) {
     const int z = blockIdx.y, lane = threadIdx.x & 63;
@@ -129,7 +133,7 @@ __global__ void __launch_bounds__(kRowWaves * 64) tri_update_kernel(double* A, i
     const double* vcur = V + (int64_t)(j & 1) * n;
     const double* W = V + 2 * (int64_t)n;
     double* P = V + 3 * (int64_t)n;
-    double* Ar = A + (int64_t)z * strideA + (int64_t)i * n;
+    float* Ar = A + (int64_t)z * strideA + (int64_t)i * n;
     const bool upd = j > 0;
     const double vi = upd ? vprev[i] : 0.0, wi = upd ? W[i] : 0.0;
     double dot = 0.0;
@@ -137,7 +141,7 @@ __global__ void __launch_bounds__(kRowWaves * 64) tri_update_kernel(double* A, i
         double a = Ar[k];
         if (upd) {
             a -= vi * W[k] + wi * vprev[k];
-            Ar[k] = a;
+            Ar[k] = (float)a;
         }
         dot += a * vcur[k];
     }
@@ -299,7 +303,7 @@ __global__ void __launch_bounds__(kVecThreads) vec_cluster_mgs_kernel(const doub
 // u = H_0 H_1 ... H_{n-1} y_k (reflector j in row j of A, v_j[j + 1] = 1),
 // in place in y; then written as row k of the fp32 output (ld, zero padded
 // to ld), rows nvals .. rows_out - 1 zero.
-__global__ void __launch_bounds__(kVecThreads) tri_backtransform_kernel(const double* A, int64_t strideA, int n,
+__global__ void __launch_bounds__(kVecThreads) tri_backtransform_kernel(const float* A, int64_t strideA, int n,
                                                                        const double* tau, int64_t stride_n,
                                                                        double* y, int nvals, float* out,
                                                                        int64_t ld_out, int64_t stride_out) {
@@ -311,12 +315,12 @@ __global__ void __launch_bounds__(kVecThreads) tri_backtransform_kernel(const do
         return;
     }
     double* u = y + ((int64_t)z * nvals + k) * (int64_t)n;
-    const double* Az = A + (int64_t)z * strideA;
+    const float* Az = A + (int64_t)z * strideA;
     const double* tz = tau + (int64_t)z * stride_n;
     for (int j = n - 1; j >= 0; --j) {
         const double t = tz[j];
         if (t == 0.0) continue;
-        const double* v = Az + (int64_t)j * n;
+        const float* v = Az + (int64_t)j * n;
         double s = 0.0;
         for (int i = j + 1 + tid; i < n; i += kVecThreads) s += v[i] * u[i];
         s = block_sum_d<kVecThreads>(s, red);
@@ -329,11 +333,11 @@ __global__ void __launch_bounds__(kVecThreads) tri_backtransform_kernel(const do
 
 }  // namespace
 
-hipError_t launch_gamma_to_f64(const float* g, int64_t ldg, int64_t strideg, int n, double* A, int batch,
-                               hipStream_t s) {
+hipError_t launch_gamma_sym(const float* g, int64_t ldg, int64_t strideg, int n, float* A, int batch,
+                            hipStream_t s) {
     const int64_t nn = (int64_t)n * n;
     const unsigned blocks = (unsigned)std::min<int64_t>(4096, (nn + 255) / 256);
-    hipLaunchKernelGGL(gamma_to_f64_kernel, dim3(blocks, batch), dim3(256), 0, s, g, ldg, strideg, n, A, nn);
+    hipLaunchKernelGGL(gamma_sym_kernel, dim3(blocks, batch), dim3(256), 0, s, g, ldg, strideg, n, A, nn);
     return hipGetLastError();
 }
 

@@ -272,11 +272,11 @@ hipError_t launch_eig_select(const EigArgs& a, int batch, hipStream_t s);
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t s);
 
 // ------------------------------------------ dense symmetric eigensolver ---
-// Workspace of one launch of matrices of equal order n (per matrix: A n x n,
-// vec 4 n, d / e / tau n each; per matrix and requested eigenvector: lu 5 n,
-// y n), all fp64.
+// Workspace of one launch of matrices of equal order n (per matrix: A n x n
+// fp32, vec 4 n, d / e / tau n each; per matrix and requested eigenvector:
+// lu 5 n, y n; fp64 unless stated).
 struct TriWork {
-    double* A;      // the matrix on entry; reflectors in its rows on exit
+    float* A;       // the matrix on entry; reflectors in its rows on exit
     double* vec;
     double* d;
     double* e;
@@ -284,9 +284,9 @@ struct TriWork {
     double* lu;
     double* y;
 };
-// Symmetrized fp64 copy of an fp32 n x n matrix (leading block, ld ldg).
-hipError_t launch_gamma_to_f64(const float* g, int64_t ldg, int64_t strideg, int n, double* A, int batch,
-                               hipStream_t s);
+// Symmetrized copy of the leading n x n block of an fp32 matrix (ld ldg).
+hipError_t launch_gamma_sym(const float* g, int64_t ldg, int64_t strideg, int n, float* A, int batch,
+                            hipStream_t s);
 // Householder reduction of A to tridiagonal form (d, e), reflectors kept.
 hipError_t launch_tridiagonalize(const TriWork& w, int n, int batch, hipStream_t s);
 // Eigenvalues first .. first + nvals - 1 in descending order (0 = largest).
