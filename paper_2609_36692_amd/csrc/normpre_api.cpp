@@ -26,6 +26,9 @@ constexpr int64_t kMaxDim = int64_t(1) << 20;
 constexpr int64_t kMaxElems = int64_t(1) << 31;
 constexpr int kMaxRowLen = 32768;   // row-active register kernel limit
 constexpr int kMaxEll = 384;
+// Widths of Gamma_Q above this go to the dense eigensolver (tridiagonal
+// reduction, bisection, inverse iteration) instead of the Jacobi kernels.
+constexpr int kEigJacobiMax = 104;
 // Exact NormPre-L above kMaxEll active rows: dense fp64 eigensolver on the
 // a x a interaction matrix (tridiagonal reduction, bisection, inverse
 // iteration), up to this many active rows.
@@ -398,6 +401,10 @@ struct Pool {
     float* eigs = nullptr;
     float* ritz = nullptr;
     int* nsel = nullptr;
+    // Ritz pairs through the dense eigensolver (l > kEigJacobiMax)
+    TriWork tw{};
+    double* lam = nullptr;
+    float* zbuf = nullptr;
 };
 
 void carve_item(Arena& ar, Item& it, int variant, bool source_x) {
@@ -459,6 +466,18 @@ void carve_pool(Arena& ar, Pool& p, int variant) {
         p.eigs = ar.take<float>(c * 2 * lp * lp);
         p.ritz = ar.take<float>(c * (int64_t)p.top);
         p.nsel = ar.take<int>(c);
+        if (p.ell > kEigJacobiMax) {
+            const int64_t n = p.ell, top = p.top;
+            p.tw.A = ar.take<float>(c * n * n);
+            p.tw.vec = ar.take<double>(c * 4 * n);
+            p.tw.d = ar.take<double>(c * n);
+            p.tw.e = ar.take<double>(c * n);
+            p.tw.tau = ar.take<double>(c * n);
+            p.tw.lu = ar.take<double>(c * top * 5 * n);
+            p.tw.y = ar.take<double>(c * top * n);
+            p.lam = ar.take<double>(c * top);
+            p.zbuf = ar.take<float>(c * top * n);
+        }
     }
 }
 
@@ -1238,7 +1257,12 @@ int run_round_l(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& 
         ea.scratch = pl.eigs; ea.kmat = pl.kmat;
         ea.ritz = pl.ritz; ea.ritz_stride = pl.top; ea.nsel = pl.nsel;
         ea.max_sweeps = kEigSweeps;
-        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_eig_select(ea, pl.count, sc.s); }),
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+                     [&] {
+                         return pl.ell > kEigJacobiMax
+                                    ? launch_eig_select_dense(ea, pl.tw, pl.lam, pl.zbuf, pl.count, sc.s)
+                                    : launch_eig_select(ea, pl.count, sc.s);
+                     }),
                "eigensolver");
     }
     // With the interaction source X the preconditioner still acts on Psi:

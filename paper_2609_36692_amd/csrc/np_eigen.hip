@@ -271,14 +271,17 @@ __global__ void tri_inverse_kernel(const double* dd, const double* ee, int64_t s
 }
 
 // Modified Gram-Schmidt inside clusters (eigenvalues, descending, closer
-// than ortol = 1e-3 * max |lambda| to their neighbour), then unit norm.
+// than ortol = 1e-9 * max |lambda| to their neighbour), then unit norm.  With
+// shifts accurate to a few ulps, two solves leave a neighbour at gap g with a
+// weight of about (eps ||T|| / g)^2, so only near-degenerate eigenvalues (the
+// same shift from bisection) need the explicit orthogonalization.
 __global__ void __launch_bounds__(kVecThreads) vec_cluster_mgs_kernel(const double* lam, int64_t stride_lam, int n,
                                                                      int nvals, double* y) {
     __shared__ double red[kVecThreads / 64];
     const int z = blockIdx.x, tid = threadIdx.x;
     const double* lz = lam + (int64_t)z * stride_lam;
     double* yz = y + (int64_t)z * nvals * n;
-    const double ortol = 1e-3 * fmax(fabs(lz[0]), fabs(lz[nvals - 1]));
+    const double ortol = 1e-9 * fmax(fabs(lz[0]), fabs(lz[nvals - 1]));
     int cstart = 0;
     for (int k = 0; k < nvals; ++k) {
         if (k > 0 && lz[k - 1] - lz[k] > ortol) cstart = k;
@@ -329,6 +332,42 @@ __global__ void __launch_bounds__(kVecThreads) tri_backtransform_kernel(const fl
         __syncthreads();
     }
     for (int64_t i = tid; i < ld_out; i += kVecThreads) o[i] = i < n ? (float)u[i] : 0.f;
+}
+
+// Summed fp64 Gram partials (upper 32 x 32 tiles, chunks x l_pad x l_pad)
+// -> symmetric n x n fp32 matrix.
+__global__ void gram_to_mat_kernel(const double* partial, int chunks, int ell_pad, int n, float* A) {
+    const int z = blockIdx.y;
+    const double* part = partial + (int64_t)z * chunks * ell_pad * ell_pad;
+    float* Az = A + (int64_t)z * n * n;
+    for (int idx = blockIdx.x * blockDim.x + threadIdx.x; idx < n * n; idx += gridDim.x * blockDim.x) {
+        const int c = idx / n, d = idx - (idx / n) * n;
+        Az[idx] = (float)gram_at(part, ell_pad, c, d);
+    }
+}
+
+// Selection of the top eigenpairs (lam descending, z rows) above one, Ritz
+// values and |C|; K = Z_C diag(lambda^-1/2 - 1) Z_C^T (l_pad x l_pad, zero
+// outside n x n), 256 entries per block.
+__global__ void __launch_bounds__(256) select_k_kernel(const double* lam, int top, const float* zbuf, int n,
+                                                       int ell_pad, float* kmat, float* ritz, int ritz_stride,
+                                                       int* nsel) {
+    const int z = blockIdx.y;
+    const double* lz = lam + (int64_t)z * top;
+    const float* Z = zbuf + (int64_t)z * top * n;
+    int ns = 0;
+    while (ns < top && lz[ns] > 1.0) ++ns;      // descending: the selected ones lead
+    if (blockIdx.x == 0) {
+        for (int t = threadIdx.x; t < top; t += 256) ritz[(int64_t)z * ritz_stride + t] = (float)lz[t];
+        if (threadIdx.x == 0) nsel[z] = ns;
+    }
+    const int q = blockIdx.x * 256 + threadIdx.x;
+    if (q >= ell_pad * ell_pad) return;
+    const int c = q / ell_pad, d = q - (q / ell_pad) * ell_pad;
+    double sacc = 0.0;
+    if (c < n && d < n)
+        for (int t = 0; t < ns; ++t) sacc += (double)Z[t * n + c] * (1.0 / sqrt(lz[t]) - 1.0) * (double)Z[t * n + d];
+    kmat[(int64_t)z * ell_pad * ell_pad + q] = (float)sacc;
 }
 
 }  // namespace
@@ -389,6 +428,29 @@ hipError_t launch_tri_eigvecs(const TriWork& w, int n, const double* lam, int nv
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(tri_backtransform_kernel, dim3(rows_out, batch), dim3(kVecThreads), 0, s, w.A, (int64_t)n * n,
                        n, w.tau, (int64_t)n, w.y, nvals, out, ld_out, stride_out);
+    return hipGetLastError();
+}
+
+}  // namespace np
+
+namespace np {
+
+hipError_t launch_eig_select_dense(const EigArgs& a, const TriWork& w, double* lam, float* zbuf, int batch,
+                                   hipStream_t s) {
+    const int n = a.ell, lp = a.ell_pad, top = std::min(a.rank, n);
+    if (a.chunks != kGramChunks || n < 1 || n > lp) return hipErrorInvalidValue;
+    const unsigned gb = (unsigned)std::min<int64_t>(1024, ((int64_t)n * n + 255) / 256);
+    hipLaunchKernelGGL(gram_to_mat_kernel, dim3(gb, batch), dim3(256), 0, s, a.partial, a.chunks, lp, n, w.A);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = launch_tridiagonalize(w, n, batch, s);
+    if (e != hipSuccess) return e;
+    e = launch_tri_eigvals(w, n, 0, top, lam, top, batch, s);
+    if (e != hipSuccess) return e;
+    e = launch_tri_eigvecs(w, n, lam, top, zbuf, n, top, (int64_t)top * n, batch, s);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(select_k_kernel, dim3((unsigned)(((int64_t)lp * lp + 255) / 256), batch), dim3(256), 0, s,
+                       lam, top, zbuf, n, lp, a.kmat, a.ritz, a.ritz_stride, a.nsel);
     return hipGetLastError();
 }
 

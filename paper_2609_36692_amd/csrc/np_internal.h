@@ -230,6 +230,22 @@ struct Gram64Items {
     int chunk_len[kMaxItems];
 };
 hipError_t launch_gram64(const Gram64Items& t, int ell_pad, double* partial, hipStream_t s);
+// Element (c, d) of the summed Gram (full symmetric view of the upper 32 x 32
+// tiles gram64 writes): the kGramChunks partial sums are all requested
+// before any is added, so one memory latency covers the element; they are
+// added in chunk order.
+__device__ __forceinline__ double gram_at(const double* p, int ell_pad, int c, int d) {
+    if ((c >> 5) > (d >> 5)) { const int t = c; c = d; d = t; }
+    const double* q = p + (int64_t)c * ell_pad + d;
+    const int64_t cs = (int64_t)ell_pad * ell_pad;
+    double v[kGramChunks];
+#pragma unroll
+    for (int k = 0; k < kGramChunks; ++k) v[k] = q[k * cs];
+    double s = 0.0;
+#pragma unroll
+    for (int k = 0; k < kGramChunks; ++k) s += v[k];
+    return s;
+}
 int gram64_chunks(int64_t len, int chunk_len);
 
 // Cholesky (with dropping of numerically dependent columns) of the summed
@@ -297,6 +313,13 @@ hipError_t launch_tri_eigvals(const TriWork& w, int n, int first, int nvals, dou
 // rows_out - 1 zero).
 hipError_t launch_tri_eigvecs(const TriWork& w, int n, const double* lam, int nvals, float* out, int64_t ld_out,
                               int rows_out, int64_t stride_out, int batch, hipStream_t s);
+// Ritz pairs through the dense eigensolver (for l above the Jacobi kernels'
+// sweet spot): Gamma_Q from the summed fp64 Gram partials, its top
+// min(r, l) eigenpairs, the selection lambda > 1 and K = Z_C diag(lambda^-1/2
+// - 1) Z_C^T, with the outputs of launch_eig_select.  zbuf: top x l floats
+// per matrix; lam: top doubles per matrix.
+hipError_t launch_eig_select_dense(const EigArgs& a, const TriWork& w, double* lam, float* zbuf, int batch,
+                                   hipStream_t s);
 // Gamma = Psi Psi^T (layout 0) or Psi^T Psi (layout 2) in fp32, full tiles.
 hipError_t launch_gemm_gram_f32(int layout, Operand A, Operand B, GemmShape sh, int batch, const EpiPartial& e,
                                 hipStream_t s);

@@ -141,22 +141,6 @@ __global__ void __launch_bounds__(256) gram64_kernel(Gram64Items t, int ell_pad,
             out[(int64_t)(tc * 32 + 2 * tr + a) * ell_pad + td * 32 + 2 * tcl + b] = acc[a][b];
 }
 
-// Element (c, d) of the summed Gram (full symmetric view of upper tiles):
-// the kGramChunks partial sums are all requested before any is added, so
-// one memory latency covers the element; they are added in chunk order.
-__device__ __forceinline__ double gram_at(const double* p, int ell_pad, int c, int d) {
-    if ((c >> 5) > (d >> 5)) { const int t = c; c = d; d = t; }
-    const double* q = p + (int64_t)c * ell_pad + d;
-    const int64_t cs = (int64_t)ell_pad * ell_pad;
-    double v[kGramChunks];
-#pragma unroll
-    for (int k = 0; k < kGramChunks; ++k) v[k] = q[k * cs];
-    double s = 0.0;
-#pragma unroll
-    for (int k = 0; k < kGramChunks; ++k) s += v[k];
-    return s;
-}
-
 // -------------------------------------------------------- Cholesky + inverse
 // One block per matrix.  G = R^T R with R upper triangular; a pivot below
 // kDropTol * G_kk (relative to the column's own squared norm) marks the
