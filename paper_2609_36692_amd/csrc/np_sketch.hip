@@ -146,8 +146,6 @@ __global__ void __launch_bounds__(256) gram64_kernel(Gram64Items t, int ell_pad,
 // kDropTol * G_kk (relative to the column's own squared norm) marks the
 // column as numerically dependent: its row of R and of R^{-1} is zero, so the
 // matching column of Q = Y R^{-1} is zero and it never reaches the selection.
-// The matrix lives in LDS (fp64, row stride l + 1) when it fits, else in a
-// global scratch slice; R^{-1} overwrites R in place, bottom row first.
 constexpr double kDropTol = 1e-12;
 constexpr int kCholLdsMax = 138;
 constexpr int kSmallThreads = 512;
@@ -159,25 +157,24 @@ constexpr int kCholColInvMax = 96;
 // l <= kCholLdsMax over kCholThreads threads.
 constexpr int kCholOwn = (kCholLdsMax * (kCholLdsMax + 1) / 2 + kCholThreads - 1) / kCholThreads;
 
-template <bool IN_LDS>
+// l <= kCholLdsMax: the whole matrix lives in LDS (fp64, row stride l + 1);
+// R^{-1} overwrites R in place, bottom row first.
 __global__ void __launch_bounds__(kCholThreads) chol_inv_kernel(const double* partial, int chunks, int ell,
-                                                                int ell_pad, double* scratch, float* rinv) {
+                                                                int ell_pad, float* rinv) {
     constexpr int NT = kCholThreads;
     extern __shared__ double dynd[];
     const int z = blockIdx.x, tid = threadIdx.x;
     const double* p = partial + (int64_t)z * chunks * ell_pad * ell_pad;
-    const int ld = IN_LDS ? ell + 1 : ell_pad;
+    const int ld = ell + 1;
     // One square buffer.  Step k reads the updated upper row k, leaves the
     // finished row k of R in the lower triangle (R(k, j) at [j][k]) and
     // updates the upper trailing block, so it never reads what it writes and
     // one barrier per step suffices.  R^{-1} then fills the upper triangle,
     // one column per thread, reading R from the lower triangle.
-    double* R;
-    if constexpr (IN_LDS) R = dynd;
-    else R = scratch + (int64_t)z * 2 * ell_pad * ell_pad;
+    double* R = dynd;
     float* out = rinv + (int64_t)z * ell_pad * ell_pad;
-    __shared__ double diag0[384];
-    __shared__ double inv_diag[384];
+    __shared__ double diag0[kCholLdsMax];
+    __shared__ double inv_diag[kCholLdsMax];
     for (int q = tid; q < ell * ell; q += NT) {
         const int c = q / ell, d = q - (q / ell) * ell;
         if (d >= c) {
@@ -187,7 +184,7 @@ __global__ void __launch_bounds__(kCholThreads) chol_inv_kernel(const double* pa
         }
     }
     __syncthreads();
-    if (IN_LDS) {
+    {
         // The trailing updates of this thread's fixed entries, no index
         // arithmetic in the step loop.
         int own[kCholOwn];
@@ -217,22 +214,6 @@ __global__ void __launch_bounds__(kCholThreads) chol_inv_kernel(const double* pa
             }
             __syncthreads();
         }
-    } else {
-        for (int k = 0; k < ell; ++k) {
-            const double piv = R[k * ld + k];
-            const bool keep = diag0[k] > 0.0 && piv > kDropTol * diag0[k];
-            const double ipiv = keep ? 1.0 / piv : 0.0;
-            const double irk = keep ? 1.0 / sqrt(piv) : 0.0;
-            if (tid == 0) inv_diag[k] = irk;
-            for (int j = k + 1 + tid; j < ell; j += NT) R[j * ld + k] = R[k * ld + j] * irk;
-            const int nrem = ell - k - 1;
-#pragma unroll 4
-            for (int q = tid; q < nrem * nrem; q += NT) {
-                const int i = k + 1 + q / nrem, j = k + 1 + q % nrem;
-                if (j >= i) R[i * ld + j] -= R[k * ld + i] * R[k * ld + j] * ipiv;
-            }
-            __syncthreads();
-        }
     }
     // X = R^{-1}: X(i, j) = -(sum_{i < k <= j} R(i, k) X(k, j)) / R(i, i),
     // X(i, i) = 1 / R(i, i); rows of dropped columns are zero.  Small l: one
@@ -250,7 +231,7 @@ __global__ void __launch_bounds__(kCholThreads) chol_inv_kernel(const double* pa
         for (; k <= j; ++k) s0 += R[k * ld + i] * R[k * ld + j];
         return -((s0 + s1) + (s2 + s3)) * inv_diag[i];
     };
-    if (IN_LDS && ell <= kCholColInvMax) {
+    if (ell <= kCholColInvMax) {
         for (int j = tid; j < ell; j += NT) {
             R[j * ld + j] = inv_diag[j];
             for (int i = j - 1; i >= 0; --i) R[i * ld + j] = x_entry(i, j);
@@ -265,6 +246,155 @@ __global__ void __launch_bounds__(kCholThreads) chol_inv_kernel(const double* pa
     for (int q = tid; q < ell_pad * ell_pad; q += NT) {
         const int i = q / ell_pad, j = q - (q / ell_pad) * ell_pad;
         out[q] = (i < ell && j < ell && j >= i) ? (float)R[i * ld + j] : 0.f;
+    }
+}
+
+// l > kCholLdsMax: the matrix does not fit in LDS.  R and X = R^{-1} live in
+// a global scratch slice (two l_pad^2 fp64 squares, upper triangles only,
+// L2-resident at these sizes) and the work runs in row panels staged through
+// LDS, so the global traffic is one read and write of the trailing triangle
+// per panel rather than per pivot.
+//   Cholesky (right-looking), panel of kPanelC rows k0..: factor the panel
+//   rows in LDS (one barrier per pivot), scale them into rows of R, then
+//   subtract their outer products from the trailing upper triangle in 4x4
+//   register tiles.
+//   Inverse, row panels of kPanelI rows bottom up: with rows below the panel
+//   of X final, T = R(I, below) X(below, :) per column (a column and four
+//   panel rows per thread), then X(I, j) = R(I, I)^{-1} (e_j - T(:, j)) by
+//   back substitution, one column per thread in registers.
+constexpr int kPanelC = 32;
+constexpr int kPanelI = 16;
+
+__global__ void __launch_bounds__(kCholThreads) chol_inv_panel_kernel(const double* partial, int chunks, int ell,
+                                                                      int ell_pad, double* scratch, float* rinv) {
+    constexpr int NT = kCholThreads;
+    extern __shared__ double dynd[];
+    const int z = blockIdx.x, tid = threadIdx.x, lane = tid & 63, grp = tid >> 6;
+    constexpr int NG = NT / 64;
+    const double* p = partial + (int64_t)z * chunks * ell_pad * ell_pad;
+    const int ld = ell_pad, pst = ell + 1;
+    double* W = scratch + (int64_t)z * 2 * ell_pad * ell_pad;
+    double* X = W + (int64_t)ell_pad * ell_pad;
+    float* out = rinv + (int64_t)z * ell_pad * ell_pad;
+    __shared__ double diag0[384];
+    __shared__ double inv_diag[384];
+    for (int i = grp; i < ell; i += NG)
+        for (int j = i + lane; j < ell; j += 64) {
+            const double g = gram_at(p, ell_pad, i, j);
+            W[(int64_t)i * ld + j] = g;
+            if (i == j) diag0[i] = g;
+        }
+    __syncthreads();
+
+    double* P = dynd;  // kPanelC x pst
+    for (int k0 = 0; k0 < ell; k0 += kPanelC) {
+        const int kb = min(kPanelC, ell - k0), w = ell - k0;
+        for (int r = grp; r < kb; r += NG)
+            for (int c = r + lane; c < w; c += 64) P[r * pst + c] = W[(int64_t)(k0 + r) * ld + k0 + c];
+        __syncthreads();
+        for (int r = 0; r < kb; ++r) {
+            const int k = k0 + r;
+            const double piv = P[r * pst + r];
+            const bool keep = diag0[k] > 0.0 && piv > kDropTol * diag0[k];
+            const double ipiv = keep ? 1.0 / piv : 0.0;
+            if (tid == 0) inv_diag[k] = keep ? 1.0 / sqrt(piv) : 0.0;
+            const double* pr = P + r * pst;
+            for (int rr = r + 1 + grp; rr < kb; rr += NG) {
+                const double f = pr[rr] * ipiv;
+                double* prr = P + rr * pst;
+                for (int c = rr + lane; c < w; c += 64) prr[c] -= f * pr[c];
+            }
+            __syncthreads();
+        }
+        // Rows of R: the pivot rows scaled by 1 / sqrt(pivot) (zero when dropped).
+        for (int r = grp; r < kb; r += NG) {
+            const double s = inv_diag[k0 + r];
+            for (int c = r + lane; c < w; c += 64) {
+                const double v = P[r * pst + c] * s;
+                P[r * pst + c] = v;
+                W[(int64_t)(k0 + r) * ld + k0 + c] = v;
+            }
+        }
+        __syncthreads();
+        const int t0 = kb, t = w - kb, nbk = (t + 3) >> 2;
+        for (int b = tid; b < nbk * nbk; b += NT) {
+            const int bi = b / nbk, bj = b - bi * nbk;
+            if (bi > bj) continue;
+            const int ci = t0 + 4 * bi, cj = t0 + 4 * bj;
+            double acc[4][4];
+#pragma unroll
+            for (int a = 0; a < 4; ++a)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int i = ci + a, j = cj + e;
+                    acc[a][e] = (j < w && i <= j) ? W[(int64_t)(k0 + i) * ld + k0 + j] : 0.0;
+                }
+            for (int r = 0; r < kb; ++r) {
+                double vi[4], vj[4];
+#pragma unroll
+                for (int a = 0; a < 4; ++a) {
+                    vi[a] = ci + a < w ? P[r * pst + ci + a] : 0.0;
+                    vj[a] = cj + a < w ? P[r * pst + cj + a] : 0.0;
+                }
+#pragma unroll
+                for (int a = 0; a < 4; ++a)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) acc[a][e] -= vi[a] * vj[e];
+            }
+#pragma unroll
+            for (int a = 0; a < 4; ++a)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int i = ci + a, j = cj + e;
+                    if (j < w && i <= j) W[(int64_t)(k0 + i) * ld + k0 + j] = acc[a][e];
+                }
+        }
+        __syncthreads();
+    }
+
+    double* Rp = dynd;                  // kPanelI x pst: rows of R from column i0
+    double* T = dynd + kPanelI * pst;   // kPanelI x pst: R(I, below) X(below, :)
+    for (int i0 = ((ell - 1) / kPanelI) * kPanelI; i0 >= 0; i0 -= kPanelI) {
+        const int kb = min(kPanelI, ell - i0), w = ell - i0, nc = w - kb;
+        for (int r = grp; r < kPanelI; r += NG)
+            for (int c = lane; c < w; c += 64)
+                Rp[r * pst + c] = (r < kb && c >= r) ? W[(int64_t)(i0 + r) * ld + i0 + c] : 0.0;
+        __syncthreads();
+        for (int q = tid; q < (kPanelI / 4) * nc; q += NT) {
+            const int g = q / nc, jc = q - g * nc, j = i0 + kb + jc;
+            const double* r0 = Rp + 4 * g * pst;
+            double acc[4] = {0.0, 0.0, 0.0, 0.0};
+            for (int kk = kb; kk <= kb + jc; ++kk) {
+                const double x = X[(int64_t)(i0 + kk) * ld + j];
+#pragma unroll
+                for (int a = 0; a < 4; ++a) acc[a] += r0[a * pst + kk] * x;
+            }
+#pragma unroll
+            for (int a = 0; a < 4; ++a) T[(4 * g + a) * pst + jc] = acc[a];
+        }
+        __syncthreads();
+        for (int jc = tid; jc < w; jc += NT) {
+            double x[kPanelI];
+#pragma unroll
+            for (int r = kPanelI - 1; r >= 0; --r) {
+                double s = 0.0;
+                if (r < kb) {
+                    s = (jc == r ? 1.0 : 0.0) - (jc >= kb ? T[r * pst + jc - kb] : 0.0);
+#pragma unroll
+                    for (int r2 = r + 1; r2 < kPanelI; ++r2) s -= Rp[r * pst + r2] * x[r2];
+                    s *= inv_diag[i0 + r];
+                }
+                x[r] = s;
+            }
+#pragma unroll
+            for (int r = 0; r < kPanelI; ++r)
+                if (r < kb && r <= jc) X[(int64_t)(i0 + r) * ld + i0 + jc] = x[r];
+        }
+        __syncthreads();
+    }
+    for (int q = tid; q < ell_pad * ell_pad; q += NT) {
+        const int i = q / ell_pad, j = q - (q / ell_pad) * ell_pad;
+        out[q] = (i < ell && j < ell && j >= i) ? (float)X[(int64_t)i * ld + j] : 0.f;
     }
 }
 
@@ -907,13 +1037,14 @@ hipError_t launch_gram64(const Gram64Items& t, int ell_pad, double* partial, hip
 
 hipError_t launch_chol_inv(const double* partial, int chunks, int ell, int ell_pad, double* scratch, float* rinv,
                            int batch, hipStream_t s) {
-    if (ell > 384 || ell_pad > 384 || chunks != kGramChunks) return hipErrorInvalidValue;
+    if (ell < 1 || ell > 384 || ell_pad < ell || ell_pad > 384 || chunks != kGramChunks) return hipErrorInvalidValue;
     if (ell <= kCholLdsMax) {
         const size_t lds = (size_t)(ell + 1) * (ell + 1) * sizeof(double);
-        hipLaunchKernelGGL((chol_inv_kernel<true>), dim3(batch), dim3(kCholThreads), lds, s, partial, chunks, ell,
-                           ell_pad, scratch, rinv);
+        hipLaunchKernelGGL(chol_inv_kernel, dim3(batch), dim3(kCholThreads), lds, s, partial, chunks, ell, ell_pad,
+                           rinv);
     } else {
-        hipLaunchKernelGGL((chol_inv_kernel<false>), dim3(batch), dim3(kCholThreads), 0, s, partial, chunks, ell,
+        const size_t lds = (size_t)std::max(kPanelC, 2 * kPanelI) * (ell + 1) * sizeof(double);
+        hipLaunchKernelGGL(chol_inv_panel_kernel, dim3(batch), dim3(kCholThreads), lds, s, partial, chunks, ell,
                            ell_pad, scratch, rinv);
     }
     return hipGetLastError();
