@@ -264,6 +264,22 @@ __global__ void __launch_bounds__(kCholThreads) chol_inv_kernel(const double* pa
 //   back substitution, one column per thread in registers.
 constexpr int kPanelC = 32;
 constexpr int kPanelI = 16;
+// Widths above this take the panel kernel.
+constexpr int kCholPanelFrom = 96;
+static_assert(kCholPanelFrom <= kCholLdsMax, "the LDS kernel holds l <= kCholLdsMax");
+
+// Copies src[c] -> dst[c] for c in [c0, c1), lane-strided, with eight loads
+// in flight per lane before the first store (one L2 latency per 512 entries).
+__device__ __forceinline__ void row_to_lds(double* dst, const double* src, int c0, int c1, int lane) {
+    for (int c = c0 + lane; c < c1; c += 512) {
+        double v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = c + 64 * u < c1 ? src[c + 64 * u] : 0.0;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (c + 64 * u < c1) dst[c + 64 * u] = v[u];
+    }
+}
 
 __global__ void __launch_bounds__(kCholThreads) chol_inv_panel_kernel(const double* partial, int chunks, int ell,
                                                                       int ell_pad, double* scratch, float* rinv) {
@@ -277,38 +293,54 @@ __global__ void __launch_bounds__(kCholThreads) chol_inv_panel_kernel(const doub
     double* X = W + (int64_t)ell_pad * ell_pad;
     float* out = rinv + (int64_t)z * ell_pad * ell_pad;
     __shared__ double diag0[384];
+    __shared__ double pivot[384];
     __shared__ double inv_diag[384];
+    // Entries of the output outside the upper triangle of the l x l block
+    // are zero; the inverse writes the rest.
+    for (int i = grp; i < ell_pad; i += NG)
+        for (int j = lane; j < ell_pad; j += 64)
+            if (!(i < ell && j < ell && j >= i)) out[(int64_t)i * ell_pad + j] = 0.f;
     for (int i = grp; i < ell; i += NG)
-        for (int j = i + lane; j < ell; j += 64) {
-            const double g = gram_at(p, ell_pad, i, j);
-            W[(int64_t)i * ld + j] = g;
-            if (i == j) diag0[i] = g;
+        for (int j0 = i + lane; j0 < ell; j0 += 256) {
+            double g[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) g[u] = j0 + 64 * u < ell ? gram_at(p, ell_pad, i, j0 + 64 * u) : 0.0;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int j = j0 + 64 * u;
+                if (j < ell) {
+                    W[(int64_t)i * ld + j] = g[u];
+                    if (i == j) diag0[i] = g[u];
+                }
+            }
         }
     __syncthreads();
 
     double* P = dynd;  // kPanelC x pst
     for (int k0 = 0; k0 < ell; k0 += kPanelC) {
         const int kb = min(kPanelC, ell - k0), w = ell - k0;
-        for (int r = grp; r < kb; r += NG)
-            for (int c = r + lane; c < w; c += 64) P[r * pst + c] = W[(int64_t)(k0 + r) * ld + k0 + c];
+        for (int r = grp; r < kb; r += NG) row_to_lds(P + r * pst, W + (int64_t)(k0 + r) * ld + k0, r, w, lane);
         __syncthreads();
         for (int r = 0; r < kb; ++r) {
             const int k = k0 + r;
             const double piv = P[r * pst + r];
             const bool keep = diag0[k] > 0.0 && piv > kDropTol * diag0[k];
             const double ipiv = keep ? 1.0 / piv : 0.0;
-            if (tid == 0) inv_diag[k] = keep ? 1.0 / sqrt(piv) : 0.0;
+            if (tid == 0) pivot[k] = keep ? piv : 0.0;
             const double* pr = P + r * pst;
             for (int rr = r + 1 + grp; rr < kb; rr += NG) {
                 const double f = pr[rr] * ipiv;
                 double* prr = P + rr * pst;
+#pragma unroll 4
                 for (int c = rr + lane; c < w; c += 64) prr[c] -= f * pr[c];
             }
             __syncthreads();
         }
         // Rows of R: the pivot rows scaled by 1 / sqrt(pivot) (zero when dropped).
         for (int r = grp; r < kb; r += NG) {
-            const double s = inv_diag[k0 + r];
+            const double pv = pivot[k0 + r];
+            const double s = pv > 0.0 ? 1.0 / sqrt(pv) : 0.0;
+            if (lane == 0) inv_diag[k0 + r] = s;
             for (int c = r + lane; c < w; c += 64) {
                 const double v = P[r * pst + c] * s;
                 P[r * pst + c] = v;
@@ -329,6 +361,7 @@ __global__ void __launch_bounds__(kCholThreads) chol_inv_panel_kernel(const doub
                     const int i = ci + a, j = cj + e;
                     acc[a][e] = (j < w && i <= j) ? W[(int64_t)(k0 + i) * ld + k0 + j] : 0.0;
                 }
+#pragma unroll 4
             for (int r = 0; r < kb; ++r) {
                 double vi[4], vj[4];
 #pragma unroll
@@ -356,18 +389,34 @@ __global__ void __launch_bounds__(kCholThreads) chol_inv_panel_kernel(const doub
     double* T = dynd + kPanelI * pst;   // kPanelI x pst: R(I, below) X(below, :)
     for (int i0 = ((ell - 1) / kPanelI) * kPanelI; i0 >= 0; i0 -= kPanelI) {
         const int kb = min(kPanelI, ell - i0), w = ell - i0, nc = w - kb;
-        for (int r = grp; r < kPanelI; r += NG)
-            for (int c = lane; c < w; c += 64)
-                Rp[r * pst + c] = (r < kb && c >= r) ? W[(int64_t)(i0 + r) * ld + i0 + c] : 0.0;
+        for (int r = grp; r < kPanelI; r += NG) {
+            double* dst = Rp + r * pst;
+            const int c0 = r < kb ? r : w;
+            for (int c = lane; c < c0; c += 64) dst[c] = 0.0;
+            row_to_lds(dst, W + (int64_t)(i0 + r) * ld + i0, c0, w, lane);
+        }
         __syncthreads();
         for (int q = tid; q < (kPanelI / 4) * nc; q += NT) {
-            const int g = q / nc, jc = q - g * nc, j = i0 + kb + jc;
-            const double* r0 = Rp + 4 * g * pst;
+            const int g = q / nc, jc = q - g * nc;
+            const double* r0 = Rp + 4 * g * pst + kb;
+            const double* xc = X + (int64_t)(i0 + kb) * ld + i0 + kb + jc;  // X(i0 + kb + u, j) = xc[u ld]
             double acc[4] = {0.0, 0.0, 0.0, 0.0};
-            for (int kk = kb; kk <= kb + jc; ++kk) {
-                const double x = X[(int64_t)(i0 + kk) * ld + j];
+            // Eight independent loads in flight per thread: the column of X
+            // comes from L2, one latency per eight rows.
+            int u = 0;
+            for (; u + 8 <= jc + 1; u += 8) {
+                double xv[8];
 #pragma unroll
-                for (int a = 0; a < 4; ++a) acc[a] += r0[a * pst + kk] * x;
+                for (int e = 0; e < 8; ++e) xv[e] = xc[(int64_t)(u + e) * ld];
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+#pragma unroll
+                    for (int a = 0; a < 4; ++a) acc[a] += r0[a * pst + u + e] * xv[e];
+            }
+            for (; u <= jc; ++u) {
+                const double x = xc[(int64_t)u * ld];
+#pragma unroll
+                for (int a = 0; a < 4; ++a) acc[a] += r0[a * pst + u] * x;
             }
 #pragma unroll
             for (int a = 0; a < 4; ++a) T[(4 * g + a) * pst + jc] = acc[a];
@@ -388,13 +437,12 @@ __global__ void __launch_bounds__(kCholThreads) chol_inv_panel_kernel(const doub
             }
 #pragma unroll
             for (int r = 0; r < kPanelI; ++r)
-                if (r < kb && r <= jc) X[(int64_t)(i0 + r) * ld + i0 + jc] = x[r];
+                if (r < kb && r <= jc) {
+                    X[(int64_t)(i0 + r) * ld + i0 + jc] = x[r];
+                    out[(int64_t)(i0 + r) * ell_pad + i0 + jc] = (float)x[r];
+                }
         }
         __syncthreads();
-    }
-    for (int q = tid; q < ell_pad * ell_pad; q += NT) {
-        const int i = q / ell_pad, j = q - (q / ell_pad) * ell_pad;
-        out[q] = (i < ell && j < ell && j >= i) ? (float)X[(int64_t)i * ld + j] : 0.f;
     }
 }
 
@@ -1038,7 +1086,7 @@ hipError_t launch_gram64(const Gram64Items& t, int ell_pad, double* partial, hip
 hipError_t launch_chol_inv(const double* partial, int chunks, int ell, int ell_pad, double* scratch, float* rinv,
                            int batch, hipStream_t s) {
     if (ell < 1 || ell > 384 || ell_pad < ell || ell_pad > 384 || chunks != kGramChunks) return hipErrorInvalidValue;
-    if (ell <= kCholLdsMax) {
+    if (ell <= kCholPanelFrom) {
         const size_t lds = (size_t)(ell + 1) * (ell + 1) * sizeof(double);
         hipLaunchKernelGGL(chol_inv_kernel, dim3(batch), dim3(kCholThreads), lds, s, partial, chunks, ell, ell_pad,
                            rinv);

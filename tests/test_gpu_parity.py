@@ -136,8 +136,8 @@ def test_g_step_parity(ctx, shape, t):
 # ----------------------------------------------------------- NormPre-L
 L_CASES = [((256, 256), 16), ((257, 513), 8), ((300, 1), 4), ((3, 3), 2), ((768, 2304), 32),
            ((3072, 768), 32), ((640, 700), 64), ((40, 500), 64),
-           # l above 138: Cholesky-QR in LDS-staged panels out of global scratch
-           ((640, 700), 140), ((1000, 400), 300)]
+           # l above 96: Cholesky-QR in LDS-staged panels out of global scratch
+           ((640, 700), 100), ((640, 700), 140), ((1000, 400), 300)]
 
 
 @pytest.mark.parametrize("shape,rank", L_CASES)
