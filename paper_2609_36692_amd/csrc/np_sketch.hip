@@ -147,18 +147,16 @@ __global__ void __launch_bounds__(256) gram64_kernel(Gram64Items t, int ell_pad,
 // column as numerically dependent: its row of R and of R^{-1} is zero, so the
 // matching column of Q = Y R^{-1} is zero and it never reaches the selection.
 constexpr double kDropTol = 1e-12;
-constexpr int kCholLdsMax = 138;
+constexpr int kCholLdsMax = 96;
 constexpr int kSmallThreads = 512;
 
 constexpr int kCholThreads = 1024;
-// Largest l whose inverse runs one column per thread.
-constexpr int kCholColInvMax = 96;
 // Upper-triangle entries (i <= j) owned per thread: l (l + 1) / 2 entries for
 // l <= kCholLdsMax over kCholThreads threads.
 constexpr int kCholOwn = (kCholLdsMax * (kCholLdsMax + 1) / 2 + kCholThreads - 1) / kCholThreads;
 
 // l <= kCholLdsMax: the whole matrix lives in LDS (fp64, row stride l + 1);
-// R^{-1} overwrites R in place, bottom row first.
+// R^{-1} overwrites R in place.
 __global__ void __launch_bounds__(kCholThreads) chol_inv_kernel(const double* partial, int chunks, int ell,
                                                                 int ell_pad, float* rinv) {
     constexpr int NT = kCholThreads;
@@ -216,9 +214,8 @@ __global__ void __launch_bounds__(kCholThreads) chol_inv_kernel(const double* pa
         }
     }
     // X = R^{-1}: X(i, j) = -(sum_{i < k <= j} R(i, k) X(k, j)) / R(i, i),
-    // X(i, i) = 1 / R(i, i); rows of dropped columns are zero.  Small l: one
-    // column per thread (no barriers); larger l: one row per step, bottom
-    // first, its entries in parallel.
+    // X(i, i) = 1 / R(i, i); rows of dropped columns are zero.  One column per
+    // thread, bottom up, no barriers.
     auto x_entry = [&](int i, int j) {
         double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
         int k = i + 1;
@@ -231,16 +228,9 @@ __global__ void __launch_bounds__(kCholThreads) chol_inv_kernel(const double* pa
         for (; k <= j; ++k) s0 += R[k * ld + i] * R[k * ld + j];
         return -((s0 + s1) + (s2 + s3)) * inv_diag[i];
     };
-    if (ell <= kCholColInvMax) {
-        for (int j = tid; j < ell; j += NT) {
-            R[j * ld + j] = inv_diag[j];
-            for (int i = j - 1; i >= 0; --i) R[i * ld + j] = x_entry(i, j);
-        }
-    } else {
-        for (int i = ell - 1; i >= 0; --i) {
-            for (int j = i + tid; j < ell; j += NT) R[i * ld + j] = j == i ? inv_diag[i] : x_entry(i, j);
-            __syncthreads();
-        }
+    for (int j = tid; j < ell; j += NT) {
+        R[j * ld + j] = inv_diag[j];
+        for (int i = j - 1; i >= 0; --i) R[i * ld + j] = x_entry(i, j);
     }
     __syncthreads();
     for (int q = tid; q < ell_pad * ell_pad; q += NT) {
@@ -249,11 +239,12 @@ __global__ void __launch_bounds__(kCholThreads) chol_inv_kernel(const double* pa
     }
 }
 
-// l > kCholLdsMax: the matrix does not fit in LDS.  R and X = R^{-1} live in
-// a global scratch slice (two l_pad^2 fp64 squares, upper triangles only,
-// L2-resident at these sizes) and the work runs in row panels staged through
-// LDS, so the global traffic is one read and write of the trailing triangle
-// per panel rather than per pivot.
+// l > kCholLdsMax (the whole matrix fits in LDS up to l = 138, but one pivot
+// per barrier over the whole trailing matrix is slower from about l = 100 on):
+// R and X = R^{-1} live in a global scratch slice (two l_pad^2 fp64 squares,
+// upper triangles only, L2-resident at these sizes) and the work runs in row
+// panels staged through LDS, so the global traffic is one read and write of
+// the trailing triangle per panel rather than per pivot.
 //   Cholesky (right-looking), panel of kPanelC rows k0..: factor the panel
 //   rows in LDS (one barrier per pivot), scale them into rows of R, then
 //   subtract their outer products from the trailing upper triangle in 4x4
@@ -264,9 +255,6 @@ __global__ void __launch_bounds__(kCholThreads) chol_inv_kernel(const double* pa
 //   back substitution, one column per thread in registers.
 constexpr int kPanelC = 32;
 constexpr int kPanelI = 16;
-// Widths above this take the panel kernel.
-constexpr int kCholPanelFrom = 96;
-static_assert(kCholPanelFrom <= kCholLdsMax, "the LDS kernel holds l <= kCholLdsMax");
 
 // Copies src[c] -> dst[c] for c in [c0, c1), lane-strided, with eight loads
 // in flight per lane before the first store (one L2 latency per 512 entries).
@@ -447,61 +435,100 @@ __global__ void __launch_bounds__(kCholThreads) chol_inv_panel_kernel(const doub
 }
 
 // ------------------------------------------------------------- M^T V ----
-// Block: 64 columns of V, all l_pad outputs rows in groups of 64.  The grid
-// spans the longest item; blocks past an item's length return at once.
+// out(c, j) = sum_d M(d, c) V(d, j), d < l, c < l_pad, j < len.  Block: a
+// 64 (c) x 128 (j) output tile, 256 threads of 4 c x 8 j each (j in two runs
+// of four, 64 apart, so a row of the tile is 16 threads x 16 B contiguous).
+// The l dimension runs in chunks of 16 staged through LDS, the next chunk's
+// global loads in flight during the current chunk's FMAs.  Every d sums in
+// increasing order, one fp32 FMA per term.  len and the row strides of V and
+// the outputs are multiples of 128 (the 256-padded matrix sides), l_pad of 64.
+constexpr int kSmBM = 64, kSmBN = 128, kSmBK = 16;
+
 __global__ void __launch_bounds__(256) small_mul_kernel(SmallMulArgs args) {
-    const int z = blockIdx.y;
+    const int z = blockIdx.z;
     const int g = item_of(args, z), lz = z - args.zbeg[g];
     const SmallMulItem& a = args.it[g];
-    const int64_t j0 = (int64_t)blockIdx.x * 64;
+    const int64_t j0 = (int64_t)blockIdx.x * kSmBN;
     if (j0 >= a.len_pad) return;
+    const int c0 = blockIdx.y * kSmBM;
     const int ell = args.ell, ell_pad = args.ell_pad;
-    const int tid = threadIdx.x, jx = tid & 63, cy = tid >> 6;
+    const int tid = threadIdx.x, tc = tid >> 4, tj = tid & 15;
     const float* M = a.mat + (int64_t)lz * ell_pad * ell_pad;
     const float* V = a.v + (int64_t)lz * a.stride_v;
-    __shared__ float sm[64][65];
-    __shared__ float sv[64][65];
-    __shared__ half_t st[64][72];
-    for (int c0 = 0; c0 < ell_pad; c0 += 64) {
-        float acc[16];
+    __shared__ float4 sm[kSmBK][kSmBM / 4];
+    __shared__ float4 sv[kSmBK][kSmBN / 4];
+    // Global -> register staging: one float4 of M, two of V per thread.
+    const int mr = tid >> 4, mc = tid & 15;           // M: row, float4 column
+    const int vr = tid >> 5, vc = tid & 31;           // V: rows vr, vr + 8
+    float4 rm, rv0, rv1;
+    auto load = [&](int d0) {
+        const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+        const int dm = d0 + mr, dv0 = d0 + vr, dv1 = d0 + vr + 8;
+        rm = dm < ell ? *(const float4*)(M + (int64_t)dm * ell_pad + c0 + 4 * mc) : zero;
+        rv0 = dv0 < ell ? *(const float4*)(V + (int64_t)dv0 * a.ld_v + j0 + 4 * vc) : zero;
+        rv1 = dv1 < ell ? *(const float4*)(V + (int64_t)dv1 * a.ld_v + j0 + 4 * vc) : zero;
+    };
+    auto stage = [&]() {
+        sm[mr][mc] = rm;
+        sv[vr][vc] = rv0;
+        sv[vr + 8][vc] = rv1;
+    };
+    float acc[4][8];
 #pragma unroll
-        for (int q = 0; q < 16; ++q) acc[q] = 0.f;
-        for (int d0 = 0; d0 < ell; d0 += 64) {
-            for (int q = tid; q < 64 * 64; q += 256) {
-                const int r = q >> 6, cc = q & 63;
-                const int d = d0 + r;
-                sm[r][cc] = (d < ell && c0 + cc < ell_pad) ? M[(int64_t)d * ell_pad + c0 + cc] : 0.f;
-                sv[r][cc] = (d < ell && j0 + cc < a.len_pad) ? V[(int64_t)d * a.ld_v + j0 + cc] : 0.f;
-            }
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[u][e] = 0.f;
+    load(0);
+    stage();
+    __syncthreads();
+    for (int d0 = 0; d0 < ell; d0 += kSmBK) {
+        const bool more = d0 + kSmBK < ell;
+        if (more) load(d0 + kSmBK);
+#pragma unroll 4
+        for (int dd = 0; dd < kSmBK; ++dd) {
+            const float4 m4 = sm[dd][tc];
+            const float4 va = sv[dd][tj], vb = sv[dd][16 + tj];
+            const float mv[4] = {m4.x, m4.y, m4.z, m4.w};
+            const float vv[8] = {va.x, va.y, va.z, va.w, vb.x, vb.y, vb.z, vb.w};
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc[u][e] = fmaf(mv[u], vv[e], acc[u][e]);
+        }
+        if (more) {
             __syncthreads();
-            for (int dd = 0; dd < 64; ++dd) {
-                const float vv = sv[dd][jx];
-#pragma unroll
-                for (int q = 0; q < 16; ++q) acc[q] = fmaf(sm[dd][cy + 4 * q], vv, acc[q]);
-            }
+            stage();
             __syncthreads();
         }
-        const int64_t j = j0 + jx;
+    }
 #pragma unroll
-        for (int q = 0; q < 16; ++q) {
-            const int c = c0 + cy + 4 * q;
-            if (c < ell_pad && j < a.len_pad) {
-                if (a.out32) a.out32[(int64_t)lz * a.stride_out32 + (int64_t)c * a.ld_v + j] = acc[q];
-                if (a.out16) a.out16[(int64_t)lz * a.stride_out16 + (int64_t)c * a.ld_v + j] = (half_t)acc[q];
-            }
-            st[jx][cy + 4 * q] = (half_t)acc[q];
-        }
-        if (a.out16t) {
-            __syncthreads();
-            // Write rows j of the len-major output: 64 consecutive c per row.
-            for (int q = tid; q < 64 * 64; q += 256) {
-                const int r = q >> 6, cc = q & 63;
-                const int64_t jr = j0 + r;
-                if (jr < a.len_pad && c0 + cc < ell_pad)
-                    a.out16t[(int64_t)lz * a.stride_out16t + jr * ell_pad + c0 + cc] = st[r][cc];
+    for (int u = 0; u < 4; ++u) {
+        const int c = c0 + 4 * tc + u;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int64_t j = j0 + 64 * h + 4 * tj;
+            const float* q = acc[u] + 4 * h;
+            if (a.out32)
+                *(float4*)(a.out32 + (int64_t)lz * a.stride_out32 + (int64_t)c * a.ld_v + j) =
+                    make_float4(q[0], q[1], q[2], q[3]);
+            if (a.out16) {
+                half_t* o = a.out16 + (int64_t)lz * a.stride_out16 + (int64_t)c * a.ld_v + j;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o[e] = (half_t)q[e];
             }
         }
-        __syncthreads();
+    }
+    if (a.out16t) {
+        // len-major: row j holds l_pad consecutive c; four of them per store.
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int64_t j = j0 + 64 * h + 4 * tj + e;
+                half_t* o = a.out16t + (int64_t)lz * a.stride_out16t + j * ell_pad + c0 + 4 * tc;
+#pragma unroll
+                for (int u = 0; u < 4; ++u) o[u] = (half_t)acc[u][4 * h + e];
+            }
     }
 }
 
@@ -1086,7 +1113,7 @@ hipError_t launch_gram64(const Gram64Items& t, int ell_pad, double* partial, hip
 hipError_t launch_chol_inv(const double* partial, int chunks, int ell, int ell_pad, double* scratch, float* rinv,
                            int batch, hipStream_t s) {
     if (ell < 1 || ell > 384 || ell_pad < ell || ell_pad > 384 || chunks != kGramChunks) return hipErrorInvalidValue;
-    if (ell <= kCholPanelFrom) {
+    if (ell <= kCholLdsMax) {
         const size_t lds = (size_t)(ell + 1) * (ell + 1) * sizeof(double);
         hipLaunchKernelGGL(chol_inv_kernel, dim3(batch), dim3(kCholThreads), lds, s, partial, chunks, ell, ell_pad,
                            rinv);
@@ -1100,12 +1127,15 @@ hipError_t launch_chol_inv(const double* partial, int chunks, int ell, int ell_p
 
 hipError_t launch_small_mul(const SmallMulArgs& a, hipStream_t s) {
     if (a.n < 1 || a.n > kMaxItems || a.zbeg[0] != 0) return hipErrorInvalidValue;
+    if (a.ell < 1 || a.ell > a.ell_pad || a.ell_pad % kSmBM) return hipErrorInvalidValue;
     int64_t len_pad = 0;
     for (int g = 0; g < a.n; ++g) {
-        if (a.zbeg[g + 1] <= a.zbeg[g]) return hipErrorInvalidValue;
-        len_pad = std::max(len_pad, a.it[g].len_pad);
+        const SmallMulItem& m = a.it[g];
+        if (a.zbeg[g + 1] <= a.zbeg[g] || m.len_pad % kSmBN || m.ld_v % kSmBN || m.ld_v < m.len_pad)
+            return hipErrorInvalidValue;
+        len_pad = std::max(len_pad, m.len_pad);
     }
-    dim3 grid((unsigned)((len_pad + 63) / 64), a.zbeg[a.n]);
+    dim3 grid((unsigned)(len_pad / kSmBN), (unsigned)(a.ell_pad / kSmBM), a.zbeg[a.n]);
     hipLaunchKernelGGL(small_mul_kernel, grid, dim3(256), 0, s, a);
     return hipGetLastError();
 }
