@@ -440,7 +440,7 @@ void carve_item(Arena& ar, Item& it, int variant, bool source_x) {
             w.tw.d = ar.take<double>(count * a);
             w.tw.e = ar.take<double>(count * a);
             w.tw.tau = ar.take<double>(count * a);
-            w.tw.lu = ar.take<double>(count * d.ell * 5 * a);
+            w.tw.lu = ar.take<double>(count * d.ell * 6 * a);
             w.tw.y = ar.take<double>(count * d.ell * a);
             w.lam = ar.take<double>(count * d.ell);
         }
@@ -473,7 +473,7 @@ void carve_pool(Arena& ar, Pool& p, int variant) {
             p.tw.d = ar.take<double>(c * n);
             p.tw.e = ar.take<double>(c * n);
             p.tw.tau = ar.take<double>(c * n);
-            p.tw.lu = ar.take<double>(c * top * 5 * n);
+            p.tw.lu = ar.take<double>(c * top * 6 * n);
             p.tw.y = ar.take<double>(c * top * n);
             p.lam = ar.take<double>(c * top);
             p.zbuf = ar.take<float>(c * top * n);

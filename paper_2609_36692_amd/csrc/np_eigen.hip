@@ -151,123 +151,214 @@ __global__ void __launch_bounds__(kRowWaves * 64) tri_update_kernel(float* A, in
 
 // Number of eigenvalues of the tridiagonal (d, e) below x (Sturm count of
 // the LDL^T pivots; a pivot below pivmin in magnitude is set to -pivmin).
-__device__ int sturm_count(const double* d, const double* e, int n, double x, double pivmin) {
+// e^2 / q uses the hardware reciprocal refined by two Newton steps (within an
+// ulp or two of the quotient, a relative perturbation of each pivot that the
+// backward-stable count absorbs), keeping the dependent chain per step short.
+__device__ __forceinline__ double recip(double q) {
+    double r = __builtin_amdgcn_rcp(q);
+    r = fma(r, fma(-q, r, 1.0), r);
+    return fma(r, fma(-q, r, 1.0), r);
+}
+
+__device__ int sturm_count(const double* __restrict__ d, const double* __restrict__ e, int n, double x,
+                           double pivmin) {
     double q = d[0] - x;
     if (fabs(q) < pivmin) q = -pivmin;
     int c = q < 0.0;
+#pragma unroll 8
     for (int i = 1; i < n; ++i) {
-        q = d[i] - x - e[i - 1] * e[i - 1] / q;
+        const double ei = e[i - 1];
+        q = (d[i] - x) - ei * ei * recip(q);
         if (fabs(q) < pivmin) q = -pivmin;
         c += q < 0.0;
     }
     return c;
 }
 
-// Thread t finds the (first + t)-th largest eigenvalue.
-__global__ void tri_bisect_kernel(const double* dd, const double* ee, int64_t stride_n, int n, int first, int nvals,
-                                  double* out, int64_t stride_out) {
-    const int z = blockIdx.y, t = blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= nvals) return;
+// Multisection: kMsLanes lanes per eigenvalue, (first + t)-th largest for
+// group t.  Each round the lanes count at kMsLanes interior points of the
+// group's bracket [lo, hi] (splitting it into kMsLanes + 1 equal parts); the
+// bracket becomes the part where the count crosses the eigenvalue's index.
+// Stops at a width of 2 eps max(|lo|, |hi|) + pivmin, or when the points no
+// longer split the bracket.
+constexpr int kMsLanes = 16;
+
+__global__ void __launch_bounds__(64) tri_bisect_kernel(const double* dd, const double* ee, int64_t stride_n, int n,
+                                                        int first, int nvals, double* out, int64_t stride_out) {
+    const int z = blockIdx.y, lane = threadIdx.x, grp = lane / kMsLanes, sub = lane % kMsLanes;
+    const int t = blockIdx.x * (64 / kMsLanes) + grp;
     const double* d = dd + (int64_t)z * stride_n;
     const double* e = ee + (int64_t)z * stride_n;
+    // Gershgorin interval, the wave's lanes splitting the rows.
     double lo = DBL_MAX, hi = -DBL_MAX, emax = 0.0;
-    for (int i = 0; i < n; ++i) {
+    for (int i = lane; i < n; i += 64) {
         const double r = (i > 0 ? fabs(e[i - 1]) : 0.0) + (i + 1 < n ? fabs(e[i]) : 0.0);
         lo = fmin(lo, d[i] - r);
         hi = fmax(hi, d[i] + r);
         if (i + 1 < n) emax = fmax(emax, e[i] * e[i]);
     }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        lo = fmin(lo, __shfl_xor(lo, o, 64));
+        hi = fmax(hi, __shfl_xor(hi, o, 64));
+        emax = fmax(emax, __shfl_xor(emax, o, 64));
+    }
     const double pivmin = DBL_MIN * fmax(1.0, emax);
     const double span = fmax(fabs(lo), fabs(hi));
     lo -= 2.0 * DBL_EPSILON * span + pivmin;
     hi += 2.0 * DBL_EPSILON * span + pivmin;
+    if (t >= nvals) return;
     // smallest x with count(x) > idx, idx counted from the bottom
     const int idx = n - 1 - (first + t);
-    for (int it = 0; it < 200; ++it) {
-        const double mid = 0.5 * (lo + hi);
-        if (hi - lo <= 2.0 * DBL_EPSILON * fmax(fabs(lo), fabs(hi)) + pivmin || mid <= lo || mid >= hi) break;
-        if (sturm_count(d, e, n, mid, pivmin) > idx) hi = mid;
-        else lo = mid;
+    constexpr double kInv = 1.0 / (kMsLanes + 1);
+    for (int it = 0; it < 100; ++it) {
+        const double w = hi - lo;
+        if (w <= 2.0 * DBL_EPSILON * fmax(fabs(lo), fabs(hi)) + pivmin) break;
+        auto pt = [&](int k) { return lo + (w * (double)k) * kInv; };
+        const bool above = sturm_count(d, e, n, pt(sub + 1), pivmin) > idx;
+        const unsigned mask =
+            (unsigned)(__ballot(above) >> (grp * kMsLanes)) & ((1u << kMsLanes) - 1u);
+        // First point whose count exceeds idx (kMsLanes: none does).
+        const int s = mask ? __builtin_ctz(mask) : kMsLanes;
+        const double nlo = s > 0 ? pt(s) : lo;
+        const double nhi = s < kMsLanes ? pt(s + 1) : hi;
+        if (!(nlo > lo) && !(nhi < hi)) break;
+        lo = nlo;
+        hi = nhi;
     }
-    out[(int64_t)z * stride_out + t] = 0.5 * (lo + hi);
+    if (sub == 0) out[(int64_t)z * stride_out + t] = 0.5 * (lo + hi);
 }
 
-// Partially pivoted LU of T - lambda I (per matrix z, eigenvalue k), stored
-// as 5 arrays of n doubles [dl | d | du | du2 | piv], then `solves`
-// inverse-iteration solves of y (start: a fixed pseudo-random vector when
-// init is set), each followed by scaling to max |y_i| = 1.
-__global__ void tri_inverse_kernel(const double* dd, const double* ee, int64_t stride_n, int n, const double* lam,
-                                   int64_t stride_lam, int nvals, double* lu, double* y, int solves, int init) {
+// Inverse iteration, one thread per eigenvalue k of matrix z: partially
+// pivoted LU of T - lambda_k I, then `solves` solves of y (start: a fixed
+// pseudo-random vector when init is set, else y as left by the previous
+// launch), each followed by scaling to max |y_i| = 1.  The factors
+// [dl | 1/d | du | du2 | pivot flag] and the working vector live in `lu`,
+// interleaved across the eigenvalues of a matrix (entry i of vector k at
+// [i nvals + k]) so each load and store of a wave is contiguous; the values
+// a step carries to the next stay in registers.  y (one contiguous row per
+// vector) is read at the start when init is clear and written at the end.
+__global__ void __launch_bounds__(64) tri_inverse_kernel(const double* dd, const double* ee, int64_t stride_n, int n,
+                                                         const double* lam, int64_t stride_lam, int nvals, double* lu,
+                                                         double* y, int solves, int init) {
     const int z = blockIdx.y, k = blockIdx.x * blockDim.x + threadIdx.x;
     if (k >= nvals) return;
-    const double* d0 = dd + (int64_t)z * stride_n;
-    const double* e0 = ee + (int64_t)z * stride_n;
-    double* L = lu + ((int64_t)z * nvals + k) * 5 * (int64_t)n;
-    double* dl = L;
-    double* dg = L + n;
-    double* du = L + 2 * (int64_t)n;
-    double* du2 = L + 3 * (int64_t)n;
-    double* pv = L + 4 * (int64_t)n;
-    double* yk = y + ((int64_t)z * nvals + k) * (int64_t)n;
+    const double* __restrict__ d0 = dd + (int64_t)z * stride_n;
+    const double* __restrict__ e0 = ee + (int64_t)z * stride_n;
+    const int64_t nv = nvals, an = (int64_t)n * nv;
+    double* base = lu + (int64_t)z * 6 * an + k;
+    double* __restrict__ dl = base;
+    double* __restrict__ ig = base + an;
+    double* __restrict__ du = base + 2 * an;
+    double* __restrict__ du2 = base + 3 * an;
+    double* __restrict__ pv = base + 4 * an;
+    double* __restrict__ yw = base + 5 * an;
+    double* __restrict__ yk = y + ((int64_t)z * nvals + k) * (int64_t)n;
     const double lk = lam[(int64_t)z * stride_lam + k];
-    // Scale of T for the pivot floor.
-    double tn = 0.0;
-    for (int i = 0; i < n; ++i)
-        tn = fmax(tn, fabs(d0[i]) + (i > 0 ? fabs(e0[i - 1]) : 0.0) + (i + 1 < n ? fabs(e0[i]) : 0.0));
-    const double floor_piv = fmax(tn, DBL_MIN) * DBL_EPSILON;
     if (init) {
-        for (int i = 0; i < n; ++i) {
-            dg[i] = d0[i] - lk;
-            if (i + 1 < n) { dl[i] = e0[i]; du[i] = e0[i]; }
-        }
+        // Scale of T for the pivot floor.
+        double tn = 0.0;
+        for (int i = 0; i < n; ++i)
+            tn = fmax(tn, fabs(d0[i]) + (i > 0 ? fabs(e0[i - 1]) : 0.0) + (i + 1 < n ? fabs(e0[i]) : 0.0));
+        const double floor_piv = fmax(tn, DBL_MIN) * DBL_EPSILON;
+        auto floored = [&](double g) { return fabs(g) < floor_piv ? (g < 0.0 ? -floor_piv : floor_piv) : g; };
+        // g, u: the current diagonal and superdiagonal entries of row i (row
+        // i + 1 of the matrix is still untouched when step i starts).
+        double g = d0[0] - lk, u = n > 1 ? e0[0] : 0.0;
+#pragma unroll 4
         for (int i = 0; i + 1 < n; ++i) {
-            if (fabs(dg[i]) >= fabs(dl[i])) {
-                const double f = dg[i] != 0.0 ? dl[i] / dg[i] : 0.0;
-                dl[i] = f;
-                dg[i + 1] -= f * du[i];
-                if (i + 2 < n) du2[i] = 0.0;
-                pv[i] = 0.0;
+            const double l = e0[i], gn = d0[i + 1] - lk, un = i + 2 < n ? e0[i + 1] : 0.0;
+            const int64_t o = (int64_t)i * nv;
+            if (fabs(g) >= fabs(l)) {
+                const double f = g != 0.0 ? l / g : 0.0;
+                dl[o] = f;
+                ig[o] = 1.0 / floored(g);
+                du[o] = u;
+                du2[o] = 0.0;
+                pv[o] = 0.0;
+                g = gn - f * u;
+                u = un;
             } else {
-                const double f = dg[i] / dl[i];
-                dg[i] = dl[i];
-                dl[i] = f;
-                const double tmp = du[i];
-                du[i] = dg[i + 1];
-                dg[i + 1] = tmp - f * dg[i + 1];
-                if (i + 2 < n) {
-                    du2[i] = du[i + 1];
-                    du[i + 1] = -f * du[i + 1];
-                }
-                pv[i] = 1.0;
+                const double f = g / l;
+                dl[o] = f;
+                ig[o] = 1.0 / floored(l);
+                du[o] = gn;
+                du2[o] = un;
+                pv[o] = 1.0;
+                g = u - f * gn;
+                u = -f * un;
             }
         }
-        for (int i = 0; i < n; ++i)
-            if (fabs(dg[i]) < floor_piv) dg[i] = dg[i] < 0.0 ? -floor_piv : floor_piv;
+        ig[(int64_t)(n - 1) * nv] = 1.0 / floored(g);
         // Start vector: a fixed pseudo-random sequence in [-1, 1], distinct per k.
         uint32_t h = 0x9e3779b9u * (uint32_t)(k + 1);
         for (int i = 0; i < n; ++i) {
             h ^= h << 13; h ^= h >> 17; h ^= h << 5;
-            yk[i] = ((double)(h >> 8) * (1.0 / 8388608.0)) - 1.0;
+            yw[(int64_t)i * nv] = ((double)(h >> 8) * (1.0 / 8388608.0)) - 1.0;
         }
+    } else {
+#pragma unroll 8
+        for (int i = 0; i < n; ++i) yw[(int64_t)i * nv] = yk[i];
     }
+    // Both sweeps load eight steps' operands before the first of their stores
+    // (the loads of the working vector would otherwise wait on the stores).
+    constexpr int B = 8;
+    double scale = 1.0;
     for (int sv = 0; sv < solves; ++sv) {
-        for (int i = 0; i + 1 < n; ++i) {
-            if (pv[i] == 0.0) {
-                yk[i + 1] -= dl[i] * yk[i];
-            } else {
-                const double tmp = yk[i];
-                yk[i] = yk[i + 1];
-                yk[i + 1] = tmp - dl[i] * yk[i];
+        // Forward: P L, the running entry c = y[i] in a register.
+        double c = yw[0] * scale;
+        for (int i0 = 0; i0 + 1 < n; i0 += B) {
+            double nx[B], fl[B], pf[B];
+#pragma unroll
+            for (int j = 0; j < B; ++j) {
+                const int64_t o = (int64_t)(i0 + j) * nv;
+                const bool in = i0 + j + 1 < n;
+                nx[j] = in ? yw[o + nv] * scale : 0.0;
+                fl[j] = in ? dl[o] : 0.0;
+                pf[j] = in ? pv[o] : 0.0;
+            }
+#pragma unroll
+            for (int j = 0; j < B; ++j) {
+                if (i0 + j + 1 >= n) break;
+                const int64_t o = (int64_t)(i0 + j) * nv;
+                if (pf[j] == 0.0) {
+                    yw[o] = c;
+                    c = nx[j] - fl[j] * c;
+                } else {
+                    yw[o] = nx[j];
+                    c = c - fl[j] * nx[j];
+                }
             }
         }
-        yk[n - 1] /= dg[n - 1];
-        if (n > 1) yk[n - 2] = (yk[n - 2] - du[n - 2] * yk[n - 1]) / dg[n - 2];
-        for (int i = n - 3; i >= 0; --i) yk[i] = (yk[i] - du[i] * yk[i + 1] - du2[i] * yk[i + 2]) / dg[i];
-        double mx = 0.0;
-        for (int i = 0; i < n; ++i) mx = fmax(mx, fabs(yk[i]));
-        const double inv = mx > 0.0 ? 1.0 / mx : 1.0;
-        for (int i = 0; i < n; ++i) yk[i] *= inv;
+        // Backward: U with two superdiagonals, y[i + 1] and y[i + 2] carried.
+        double y1 = c * ig[(int64_t)(n - 1) * nv], y2 = 0.0, mx = fabs(y1);
+        yw[(int64_t)(n - 1) * nv] = y1;
+        for (int i0 = n - 2; i0 >= 0; i0 -= B) {
+            double yv[B], uu[B], u2[B], gi[B];
+#pragma unroll
+            for (int j = 0; j < B; ++j) {
+                const int i = i0 - j;
+                const int64_t o = (int64_t)(i < 0 ? 0 : i) * nv;
+                yv[j] = i >= 0 ? yw[o] : 0.0;
+                uu[j] = i >= 0 ? du[o] : 0.0;
+                u2[j] = i >= 0 && i + 2 < n ? du2[o] : 0.0;
+                gi[j] = i >= 0 ? ig[o] : 0.0;
+            }
+#pragma unroll
+            for (int j = 0; j < B; ++j) {
+                const int i = i0 - j;
+                if (i < 0) break;
+                const double y0 = (yv[j] - uu[j] * y1 - u2[j] * y2) * gi[j];
+                yw[(int64_t)i * nv] = y0;
+                mx = fmax(mx, fabs(y0));
+                y2 = y1;
+                y1 = y0;
+            }
+        }
+        scale = mx > 0.0 ? 1.0 / mx : 1.0;
     }
+#pragma unroll 8
+    for (int i = 0; i < n; ++i) yk[i] = yw[(int64_t)i * nv] * scale;
 }
 
 // Modified Gram-Schmidt inside clusters (eigenvalues, descending, closer
@@ -401,8 +492,9 @@ hipError_t launch_tridiagonalize(const TriWork& w, int n, int batch, hipStream_t
 hipError_t launch_tri_eigvals(const TriWork& w, int n, int first, int nvals, double* out, int64_t stride_out,
                               int batch, hipStream_t s) {
     if (nvals < 1) return hipSuccess;
-    hipLaunchKernelGGL(tri_bisect_kernel, dim3((nvals + 63) / 64, batch), dim3(64), 0, s, w.d, w.e, (int64_t)n, n,
-                       first, nvals, out, stride_out);
+    constexpr int per_block = 64 / kMsLanes;
+    hipLaunchKernelGGL(tri_bisect_kernel, dim3((nvals + per_block - 1) / per_block, batch), dim3(64), 0, s, w.d,
+                       w.e, (int64_t)n, n, first, nvals, out, stride_out);
     return hipGetLastError();
 }
 

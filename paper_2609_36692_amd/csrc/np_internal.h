@@ -297,7 +297,7 @@ struct TriWork {
     double* d;
     double* e;
     double* tau;
-    double* lu;
+    double* lu;     // inverse iteration: 6 n doubles per eigenvector
     double* y;
 };
 // Symmetrized copy of the leading n x n block of an fp32 matrix (ld ldg).
