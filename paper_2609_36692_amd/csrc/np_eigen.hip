@@ -149,6 +149,78 @@ __global__ void __launch_bounds__(kRowWaves * 64) tri_update_kernel(float* A, in
     if (lane == 0) P[i] = tau[(int64_t)z * stride_n + j] * dot;
 }
 
+// Householder tridiagonalization of one matrix per block for n <= kTriLdsMax,
+// the whole reduction in one launch with the working matrix in LDS: per
+// column j the reflector from the current column (two block sums), p = tau M v
+// over the trailing rows (one wave per row), w = p - (tau/2)(p^T v) v, and the
+// eager rank-2 update M -= v w^T + w v^T of the trailing block.  fp32 storage
+// with fp64 arithmetic, as in the multi-launch reduction, whose outputs (d, e,
+// tau and the reflectors in rows of A) it reproduces.  Larger n take the
+// multi-launch reduction: one CU's LDS holds neither the square nor, from
+// about n = 200 on, beats the many-CU launches with the packed triangle.
+constexpr int kTriLdsMax = 192;
+constexpr int kTriThreads = 1024;
+
+__global__ void __launch_bounds__(kTriThreads) tri_small_kernel(float* A, int64_t strideA, int n, double* dd,
+                                                                double* ee, double* tau, int64_t stride_n) {
+    extern __shared__ float M[];
+    __shared__ double v[kTriLdsMax], w[kTriLdsMax], red[kTriThreads / 64];
+    constexpr int NW = kTriThreads / 64;
+    const int z = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    float* Ag = A + (int64_t)z * strideA;
+    for (int q = tid; q < n * n; q += kTriThreads) M[q] = Ag[q];
+    __syncthreads();
+    for (int j = 0; j < n; ++j) {
+        const float* row = M + j * n;   // column j by symmetry
+        const double dj = row[j];
+        const double alpha = j + 1 < n ? (double)row[j + 1] : 0.0;
+        double sig = 0.0;
+        for (int i = j + 2 + tid; i < n; i += kTriThreads) {
+            const double c = row[i];
+            sig += c * c;
+        }
+        sig = block_sum_d<kTriThreads>(sig, red);
+        double beta = alpha, t = 0.0, scal = 0.0;
+        if (sig > 0.0) {
+            beta = -copysign(sqrt(alpha * alpha + sig), alpha);
+            t = (beta - alpha) / beta;
+            scal = 1.0 / (alpha - beta);
+        }
+        if (tid == 0) {
+            dd[(int64_t)z * stride_n + j] = dj;
+            ee[(int64_t)z * stride_n + j] = beta;
+            tau[(int64_t)z * stride_n + j] = t;
+        }
+        if (t == 0.0) continue;   // H_j = I (uniform across the block)
+        for (int i = j + 1 + tid; i < n; i += kTriThreads) {
+            const double vi = i == j + 1 ? 1.0 : (double)row[i] * scal;
+            v[i] = vi;
+            Ag[(int64_t)j * n + i] = (float)vi;
+        }
+        __syncthreads();
+        // p = t M v, rows i > j, one wave per row.
+        for (int i = j + 1 + wave; i < n; i += NW) {
+            const float* mi = M + i * n;
+            double dot = 0.0;
+            for (int k = j + 1 + lane; k < n; k += 64) dot += (double)mi[k] * v[k];
+            dot = wave_sum_d(dot);
+            if (lane == 0) w[i] = t * dot;
+        }
+        __syncthreads();
+        double pv = 0.0;
+        for (int i = j + 1 + tid; i < n; i += kTriThreads) pv += w[i] * v[i];
+        const double K = 0.5 * t * block_sum_d<kTriThreads>(pv, red);
+        for (int i = j + 1 + tid; i < n; i += kTriThreads) w[i] -= K * v[i];
+        __syncthreads();
+        for (int i = j + 1 + wave; i < n; i += NW) {
+            float* mi = M + i * n;
+            const double vi = v[i], wi = w[i];
+            for (int k = j + 1 + lane; k < n; k += 64) mi[k] = (float)((double)mi[k] - vi * w[k] - wi * v[k]);
+        }
+        __syncthreads();
+    }
+}
+
 // Number of eigenvalues of the tridiagonal (d, e) below x (Sturm count of
 // the LDL^T pivots; a pivot below pivmin in magnitude is set to -pivmin).
 // e^2 / q uses the hardware reciprocal refined by two Newton steps (within an
@@ -365,19 +437,22 @@ __global__ void __launch_bounds__(64) tri_inverse_kernel(const double* dd, const
 // than ortol = 1e-9 * max |lambda| to their neighbour), then unit norm.  With
 // shifts accurate to a few ulps, two solves leave a neighbour at gap g with a
 // weight of about (eps ||T|| / g)^2, so only near-degenerate eigenvalues (the
-// same shift from bisection) need the explicit orthogonalization.
+// same shift from bisection) need the explicit orthogonalization.  Block k
+// owns the cluster that starts at eigenvalue k (other blocks return), so
+// clusters, mostly single vectors, run in parallel.
 __global__ void __launch_bounds__(kVecThreads) vec_cluster_mgs_kernel(const double* lam, int64_t stride_lam, int n,
                                                                      int nvals, double* y) {
     __shared__ double red[kVecThreads / 64];
-    const int z = blockIdx.x, tid = threadIdx.x;
+    const int z = blockIdx.y, k0 = blockIdx.x, tid = threadIdx.x;
     const double* lz = lam + (int64_t)z * stride_lam;
-    double* yz = y + (int64_t)z * nvals * n;
     const double ortol = 1e-9 * fmax(fabs(lz[0]), fabs(lz[nvals - 1]));
-    int cstart = 0;
-    for (int k = 0; k < nvals; ++k) {
-        if (k > 0 && lz[k - 1] - lz[k] > ortol) cstart = k;
+    if (k0 > 0 && !(lz[k0 - 1] - lz[k0] > ortol)) return;
+    int k1 = k0 + 1;
+    while (k1 < nvals && !(lz[k1 - 1] - lz[k1] > ortol)) ++k1;
+    double* yz = y + (int64_t)z * nvals * n;
+    for (int k = k0; k < k1; ++k) {
         double* yk = yz + (int64_t)k * n;
-        for (int q = cstart; q < k; ++q) {
+        for (int q = k0; q < k; ++q) {
             const double* yq = yz + (int64_t)q * n;
             double s = 0.0;
             for (int i = tid; i < n; i += kVecThreads) s += yk[i] * yq[i];
@@ -472,6 +547,12 @@ hipError_t launch_gamma_sym(const float* g, int64_t ldg, int64_t strideg, int n,
 }
 
 hipError_t launch_tridiagonalize(const TriWork& w, int n, int batch, hipStream_t s) {
+    if (n < 1) return hipErrorInvalidValue;
+    if (n <= kTriLdsMax) {
+        hipLaunchKernelGGL(tri_small_kernel, dim3(batch), dim3(kTriThreads), (size_t)n * n * sizeof(float), s, w.A,
+                           (int64_t)n * n, n, w.d, w.e, w.tau, (int64_t)n);
+        return hipGetLastError();
+    }
     for (int j = 0; j < n; ++j) {
         hipLaunchKernelGGL(tri_house_kernel, dim3(batch), dim3(kHouseThreads), 0, s, w.A, (int64_t)n * n, n, j,
                            w.vec, 4 * (int64_t)n, w.d, w.e, w.tau, (int64_t)n);
@@ -506,16 +587,16 @@ hipError_t launch_tri_eigvecs(const TriWork& w, int n, const double* lam, int nv
                        w.lu, w.y, 2, 1);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(vec_cluster_mgs_kernel, dim3(batch), dim3(kVecThreads), 0, s, lam, (int64_t)nvals, n, nvals,
-                       w.y);
+    hipLaunchKernelGGL(vec_cluster_mgs_kernel, dim3(nvals, batch), dim3(kVecThreads), 0, s, lam, (int64_t)nvals, n,
+                       nvals, w.y);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(tri_inverse_kernel, g, dim3(64), 0, s, w.d, w.e, (int64_t)n, n, lam, (int64_t)nvals, nvals,
                        w.lu, w.y, 1, 0);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(vec_cluster_mgs_kernel, dim3(batch), dim3(kVecThreads), 0, s, lam, (int64_t)nvals, n, nvals,
-                       w.y);
+    hipLaunchKernelGGL(vec_cluster_mgs_kernel, dim3(nvals, batch), dim3(kVecThreads), 0, s, lam, (int64_t)nvals, n,
+                       nvals, w.y);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(tri_backtransform_kernel, dim3(rows_out, batch), dim3(kVecThreads), 0, s, w.A, (int64_t)n * n,
