@@ -982,6 +982,7 @@ template <class Pick>
 int gram64_run(const StepCtx& sc, const std::vector<const Item*>& run, const Pool& pl, Pick pick) {
     const int64_t lp = pl.ellp, off0 = run[0]->pool_off;
     Gram64Items t{};
+    t.ell = pl.ell;
     for (const Item* it : run) {
         const int g = t.n++;
         int64_t len = 0;

@@ -222,6 +222,7 @@ constexpr int kMaxItems = 8;
 // len hold zeros).
 struct Gram64Items {
     int n;
+    int ell;                                     // rows of each matrix that enter the Gram
     int zbeg[kMaxItems + 1];
     const float* v[kMaxItems];
     int64_t ld[kMaxItems];
@@ -230,12 +231,12 @@ struct Gram64Items {
     int chunk_len[kMaxItems];
 };
 hipError_t launch_gram64(const Gram64Items& t, int ell_pad, double* partial, hipStream_t s);
-// Element (c, d) of the summed Gram (full symmetric view of the upper 32 x 32
+// Element (c, d) of the summed Gram (full symmetric view of the upper 64 x 64
 // tiles gram64 writes): the kGramChunks partial sums are all requested
 // before any is added, so one memory latency covers the element; they are
 // added in chunk order.
 __device__ __forceinline__ double gram_at(const double* p, int ell_pad, int c, int d) {
-    if ((c >> 5) > (d >> 5)) { const int t = c; c = d; d = t; }
+    if ((c >> 6) > (d >> 6)) { const int t = c; c = d; d = t; }
     const double* q = p + (int64_t)c * ell_pad + d;
     const int64_t cs = (int64_t)ell_pad * ell_pad;
     double v[kGramChunks];

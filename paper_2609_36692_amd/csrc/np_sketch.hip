@@ -99,46 +99,98 @@ __device__ __forceinline__ int item_of(const T& t, int z) {
     return g;
 }
 
-// 32 x 32 output tile (tc <= td) over one chunk of the length dimension.
+// 64 x 64 output tile (tc <= td) over one chunk of the length dimension, in
+// 4 x 4 register blocks, one per thread, only those with rows and columns
+// below l, and on a diagonal tile only the upper ones (written to both
+// triangles): waves without a block skip the products, so padding and
+// symmetry cost no fp64 FMAs.  The tile's rows stream through LDS 64 columns
+// at a time (columns major, so a thread reads its four rows as one float4).
+// Every entry sums in increasing column order; chunks past the item's length
+// write zeros.  Lengths and chunk lengths are multiples of 64.
 __global__ void __launch_bounds__(256) gram64_kernel(Gram64Items t, int ell_pad, double* partial) {
     const int z = blockIdx.z, chunk = blockIdx.y;
     const int g = item_of(t, z);
     const int64_t ld = t.ld[g], len = t.len[g];
-    const int chunk_len = t.chunk_len[g];
-    const int tiles = ell_pad / 32;
+    const int chunk_len = t.chunk_len[g], ell = t.ell;
+    const int tiles = ell_pad / 64;
     int tc = 0, left = blockIdx.x;
     while (left >= tiles - tc) { left -= tiles - tc; ++tc; }
     const int td = tc + left;
-    __shared__ float sc[32][65], sd[32][65];
-    const int tid = threadIdx.x, tr = tid >> 4, tcl = tid & 15;
+    const bool diag = tc == td;
+    __shared__ float sc[64][68], sd[64][68];
+    float (*sb)[68] = diag ? sc : sd;
+    const int tid = threadIdx.x;
+    // This thread's block (bi, bj): row blocks of 4 below l in each tile.
+    const int nbc = min(16, (ell - 64 * tc + 3) / 4), nbd = min(16, (ell - 64 * td + 3) / 4);
+    int bi = -1, bj = -1;
+    if (diag) {
+        int w = tid, r = 0;
+        while (r < nbc && w >= nbc - r) { w -= nbc - r; ++r; }
+        if (r < nbc) { bi = r; bj = r + w; }
+    } else if (tid < nbc * nbd) {
+        bi = tid / nbd;
+        bj = tid - bi * nbd;
+    }
     const float* vz = t.v[g] + (int64_t)(z - t.zbeg[g]) * t.stride[g];
-    double acc[2][2] = {{0.0, 0.0}, {0.0, 0.0}};
+    double acc[4][4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[u][e] = 0.0;
     const int64_t j0 = (int64_t)chunk * chunk_len, j1 = min(len, j0 + chunk_len);
+    const int lr = tid >> 2, lc = (tid & 3) * 16;
+    const bool rc = 64 * tc + lr < ell, rd = 64 * td + lr < ell;
+    // The next slab's global loads are in flight during this slab's FMAs.
+    float4 a[4], b[4];
+    auto gload = [&](int64_t jb) {
+        const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            a[u] = rc ? *(const float4*)(vz + (int64_t)(64 * tc + lr) * ld + jb + lc + 4 * u) : zero;
+            b[u] = !diag && rd ? *(const float4*)(vz + (int64_t)(64 * td + lr) * ld + jb + lc + 4 * u) : zero;
+        }
+    };
+    if (j0 < j1) gload(j0);
     for (int64_t jb = j0; jb < j1; jb += 64) {
-        for (int q = tid; q < 32 * 64; q += 256) {
-            const int r = q >> 6, cc = q & 63;
-            const int64_t j = jb + cc;
-            sc[r][cc] = j < j1 ? vz[(int64_t)(tc * 32 + r) * ld + j] : 0.f;
-            sd[r][cc] = j < j1 ? vz[(int64_t)(td * 32 + r) * ld + j] : 0.f;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            sc[lc + 4 * u][lr] = a[u].x;
+            sc[lc + 4 * u + 1][lr] = a[u].y;
+            sc[lc + 4 * u + 2][lr] = a[u].z;
+            sc[lc + 4 * u + 3][lr] = a[u].w;
+            if (!diag) {
+                sd[lc + 4 * u][lr] = b[u].x;
+                sd[lc + 4 * u + 1][lr] = b[u].y;
+                sd[lc + 4 * u + 2][lr] = b[u].z;
+                sd[lc + 4 * u + 3][lr] = b[u].w;
+            }
         }
         __syncthreads();
-#pragma unroll 8
-        for (int jj = 0; jj < 64; ++jj) {
-            const double a0 = sc[2 * tr][jj], a1 = sc[2 * tr + 1][jj];
-            const double b0 = sd[2 * tcl][jj], b1 = sd[2 * tcl + 1][jj];
-            acc[0][0] = fma(a0, b0, acc[0][0]);
-            acc[0][1] = fma(a0, b1, acc[0][1]);
-            acc[1][0] = fma(a1, b0, acc[1][0]);
-            acc[1][1] = fma(a1, b1, acc[1][1]);
+        if (jb + 64 < j1) gload(jb + 64);
+        if (bi >= 0) {
+#pragma unroll 4
+            for (int jj = 0; jj < 64; ++jj) {
+                const float4 xa = *(const float4*)&sc[jj][4 * bi];
+                const float4 xb = *(const float4*)&sb[jj][4 * bj];
+                const double av[4] = {xa.x, xa.y, xa.z, xa.w}, bv[4] = {xb.x, xb.y, xb.z, xb.w};
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) acc[u][e] = fma(av[u], bv[e], acc[u][e]);
+            }
         }
         __syncthreads();
     }
+    if (bi < 0) return;
     double* out = partial + ((int64_t)z * kGramChunks + chunk) * ell_pad * ell_pad;
+    const int r0 = 64 * tc + 4 * bi, c0 = 64 * td + 4 * bj;
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int u = 0; u < 4; ++u)
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
-            out[(int64_t)(tc * 32 + 2 * tr + a) * ell_pad + td * 32 + 2 * tcl + b] = acc[a][b];
+        for (int e = 0; e < 4; ++e) {
+            out[(int64_t)(r0 + u) * ell_pad + c0 + e] = acc[u][e];
+            if (diag) out[(int64_t)(c0 + e) * ell_pad + r0 + u] = acc[u][e];
+        }
 }
 
 // -------------------------------------------------------- Cholesky + inverse
@@ -1099,12 +1151,13 @@ hipError_t launch_reduce_splits(const float* part, int splits, int64_t stride_sp
 int gram64_chunks(int64_t len, int chunk_len) { return (int)((len + chunk_len - 1) / chunk_len); }
 
 hipError_t launch_gram64(const Gram64Items& t, int ell_pad, double* partial, hipStream_t s) {
-    if (ell_pad % 32 || t.n < 1 || t.n > kMaxItems || t.zbeg[0] != 0) return hipErrorInvalidValue;
+    if (ell_pad % 64 || t.ell < 1 || t.ell > ell_pad || t.n < 1 || t.n > kMaxItems || t.zbeg[0] != 0)
+        return hipErrorInvalidValue;
     for (int g = 0; g < t.n; ++g)
-        if (t.chunk_len[g] % 64 || gram64_chunks(t.len[g], t.chunk_len[g]) > kGramChunks ||
-            t.zbeg[g + 1] <= t.zbeg[g])
+        if (t.chunk_len[g] % 64 || t.len[g] % 64 || t.ld[g] % 4 ||
+            gram64_chunks(t.len[g], t.chunk_len[g]) > kGramChunks || t.zbeg[g + 1] <= t.zbeg[g])
             return hipErrorInvalidValue;
-    const int tiles = ell_pad / 32;
+    const int tiles = ell_pad / 64;
     dim3 grid(tiles * (tiles + 1) / 2, kGramChunks, t.zbeg[t.n]);
     hipLaunchKernelGGL(gram64_kernel, grid, dim3(256), 0, s, t, ell_pad, partial);
     return hipGetLastError();
