@@ -957,6 +957,71 @@ int sketch_product(const StepCtx& sc, const Dims& d, const GWork& w, int count, 
     return NORMPRE_OK;
 }
 
+// One sketch-product stage for the items of a pool run: one grouped split-K
+// launch and one grouped split reduction (the per-item arithmetic of
+// sketch_product).  `pick` gives an item's l-major operand, outputs, fp16
+// scale and source (null: Psi).
+struct SkIO {
+    const half_t* v16;
+    float* out32;
+    half_t* out16;
+    float scale16;
+    const half_t* src;
+};
+
+template <class Pick>
+int sketch_product_run(const StepCtx& sc, const std::vector<const Item*>& its, bool over_active, Pick pick) {
+    SketchGroups g{};
+    ReduceGroups r{};
+    TileCfg cfg = TileCfg::Skinny64;
+    int layout = -1, total = 0;
+    int64_t lp0 = 0;
+    double flops = 0.0, bytes = 0.0;
+    for (const Item* it : its) {
+        const Dims& d = it->d;
+        const GWork& w = it->w;
+        const SkIO io = pick(*it);
+        const int64_t mn = d.mp * d.np_, lp = d.ellp, maxpad = d.lp_;
+        const bool pv = over_active == (d.k == 0);
+        const int64_t n_out = pv ? d.mp : d.np_;
+        const int64_t k_len = pv ? d.np_ : d.mp;
+        const TileCfg c = lp == 128 ? TileCfg::Skinny128 : TileCfg::Skinny64;
+        if (layout < 0) {
+            cfg = c;
+            layout = pv ? 0 : 1;
+            lp0 = lp;
+        } else if (c != cfg || layout != (pv ? 0 : 1) || lp != lp0) {
+            return set_err(sc.ctx, NORMPRE_ERR_HIP, "internal: sketch products of one launch differ in l or side");
+        }
+        const int64_t tiles = (lp / gemm_tile_m(cfg)) * (n_out / gemm_tile_n(cfg));
+        const int splits = pick_splits(tiles, it->count, k_len);
+        const int64_t k_chunk = round_up((k_len + splits - 1) / splits, 64);
+        const int real_splits = (int)((k_len + k_chunk - 1) / k_chunk);
+        const int i = g.n++;
+        g.zbeg[i] = r.zbeg[i] = total;
+        g.a[i] = io.v16; g.lda[i] = k_len; g.a_stride[i] = lp * maxpad;
+        g.b[i] = io.src ? io.src : w.psi; g.ldb[i] = d.np_; g.b_stride[i] = mn;
+        g.N[i] = (int)n_out; g.K[i] = (int)k_len; g.k_chunk[i] = (int)k_chunk; g.splits[i] = real_splits;
+        g.out[i] = w.part; g.stride_split[i] = lp * n_out; g.stride_mat[i] = (int64_t)kMaxSplits * lp * maxpad;
+        r.part[i] = w.part; r.splits[i] = real_splits;
+        r.stride_split[i] = lp * n_out; r.stride_mat[i] = (int64_t)kMaxSplits * lp * maxpad;
+        r.n4[i] = lp * n_out / 4;
+        r.out32[i] = io.out32; r.out16[i] = io.out16; r.scale16[i] = io.scale16; r.stride_out[i] = lp * maxpad;
+        flops += 2.0 * d.ell * (double)d.m * (double)d.n * it->count;
+        bytes += 2.0 * (double)d.m * (double)d.n * it->count;
+        total += it->count;
+    }
+    if (g.n == 0) return NORMPRE_OK;
+    g.zbeg[g.n] = r.zbeg[g.n] = total;
+    r.n = g.n;
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_STREAM, flops, bytes,
+                 [&] { return launch_gemm_partial_grouped(cfg, layout, (int)lp0, g, sc.s); }),
+           "sketch product");
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_reduce_splits_grouped(r, sc.s); }),
+           "reduce splits");
+    return NORMPRE_OK;
+}
+
 // The items of each pool in pool order, in runs of at most kMaxItems (one
 // grouped launch each); their matrices are contiguous in the pool buffers.
 std::vector<std::vector<const Item*>> pool_runs(const std::vector<Item>& items, const std::vector<Pool>& pools) {
@@ -1096,22 +1161,34 @@ int sketch_front(const StepCtx& sc, const Item& it, DebugMat* dbg) {
         NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_omega_f16(o, cnt, sc.s); }),
                "omega");
     }
-    // Alg. 2: Y = Psi Omega; p times Y <- Psi (Psi^T Y).  The fp16 copies of
-    // Z and Y are scaled by powers of two (lambda_max <= tr Gamma <= a bounds
-    // each product), which only rescales the spanned subspace.
-    // lambda_max(Gamma) <= tr Gamma = ||Psi||_F^2 <= a (n with both axes).
-    const float sc_step =
-        pow2_at_most_inv_sqrt(hp.orientation == NORMPRE_ORIENT_BOTH ? std::max(d.a, d.n) : d.a);
+    return NORMPRE_OK;
+}
+
+// Alg. 2: Y = Psi Omega; p times Y <- Psi (Psi^T Y), each product one grouped
+// launch over the sketched items of a pool run.  The fp16 copies of Z and Y
+// are scaled by powers of two (lambda_max <= tr Gamma <= a bounds each
+// product), which only rescales the spanned subspace.  The candidate
+// subspace comes from the interaction source: Psi, or the trace-matched X
+// (NORMPRE_FLAG_SOURCE_X).
+int sketch_power_run(const StepCtx& sc, const std::vector<const Item*>& its) {
+    const normpre_hparams& hp = *sc.hp;
     const int p = power_iterations(hp);
-    // The candidate subspace comes from the interaction source: Psi, or the
-    // trace-matched X (NORMPRE_FLAG_SOURCE_X).
-    const half_t* src = w.xs;
-    rc = sketch_product(sc, d, w, count, w.omega, true, w.v32[0], p > 0 ? w.v16[0] : nullptr, 1.f, src);
+    // lambda_max(Gamma) <= tr Gamma = ||Psi||_F^2 <= a (n with both axes).
+    auto step_scale = [&](const Item& it) {
+        return pow2_at_most_inv_sqrt(hp.orientation == NORMPRE_ORIENT_BOTH ? std::max(it.d.a, it.d.n) : it.d.a);
+    };
+    int rc = sketch_product_run(sc, its, true, [&](const Item& it) {
+        return SkIO{it.w.omega, it.w.v32[0], p > 0 ? it.w.v16[0] : nullptr, 1.f, it.w.xs};
+    });
     if (rc) return rc;
     for (int i = 0; i < p; ++i) {
-        rc = sketch_product(sc, d, w, count, w.v16[0], false, nullptr, w.v16[1], sc_step, src);
+        rc = sketch_product_run(sc, its, false, [&](const Item& it) {
+            return SkIO{it.w.v16[0], nullptr, it.w.v16[1], step_scale(it), it.w.xs};
+        });
         if (rc) return rc;
-        rc = sketch_product(sc, d, w, count, w.v16[1], true, w.v32[0], i + 1 < p ? w.v16[0] : nullptr, sc_step, src);
+        rc = sketch_product_run(sc, its, true, [&](const Item& it) {
+            return SkIO{it.w.v16[1], it.w.v32[0], i + 1 < p ? it.w.v16[0] : nullptr, step_scale(it), it.w.xs};
+        });
         if (rc) return rc;
     }
     return NORMPRE_OK;
@@ -1231,18 +1308,26 @@ int run_round_l(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& 
         int rc = it.d.xl ? exact_front(sc, it, dbg) : sketch_front(sc, it, dbg);
         if (rc) return rc;
     }
+    const auto runs = pool_runs(items, pools);
+    for (const auto& run : runs) {
+        std::vector<const Item*> sketched;
+        for (const Item* it : run)
+            if (!it->d.xl) sketched.push_back(it);
+        if (int rc = sketch_power_run(sc, sketched)) return rc;
+    }
     // Q = qr(Y) by two Cholesky-QR passes (fp64 Gram and factorization).
     int rc = cholqr_round(sc, items, pools, false);
     if (rc) return rc;
     rc = cholqr_round(sc, items, pools, true);
     if (rc) return rc;
-    // B = Q^T Psi (ell_pad x b_pad) per item, Gamma_Q = B B^T per pool
+    // B = Q^T Psi (ell_pad x b_pad) per pool run, Gamma_Q = B B^T per pool
     // (B = Q^T X_s with the interaction source X).
-    for (const Item& it : items) {
-        rc = sketch_product(sc, it.d, it.w, it.count, it.w.v16[0], false, it.w.v32[0], nullptr, 1.f, it.w.xs);
+    for (const auto& run : runs) {
+        rc = sketch_product_run(sc, run, false, [&](const Item& it) {
+            return SkIO{it.w.v16[0], it.w.v32[0], nullptr, 1.f, it.w.xs};
+        });
         if (rc) return rc;
     }
-    const auto runs = pool_runs(items, pools);
     for (const auto& run : runs) {
         rc = gram64_run(sc, run, pools[run[0]->pool], [&](const Item& it, int64_t& len) -> const float* {
             len = it.d.b_pad;

@@ -17,6 +17,7 @@
 // All sizes are multiples of the tile sizes (the workspace is zero padded).
 #include "np_internal.h"
 
+#include <algorithm>
 #include <type_traits>
 #include <utility>
 
@@ -218,6 +219,11 @@ template <class E, class = void>
 struct IsGrouped { static constexpr bool value = false; };
 template <class E>
 struct IsGrouped<E, std::void_t<decltype(std::declval<E>().gg)>> { static constexpr bool value = true; };
+// Epilogues that carry a SketchGroups table (grouped split-K sketch products).
+template <class E, class = void>
+struct IsSkGrouped { static constexpr bool value = false; };
+template <class E>
+struct IsSkGrouped<E, std::void_t<decltype(std::declval<E>().sg)>> { static constexpr bool value = true; };
 
 template <int MF> struct AccSel { using type = f32x4; };
 template <> struct AccSel<32> { using type = f32x16; };
@@ -248,13 +254,24 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave - (wave / WN) * WN;
     int bx = blockIdx.x, split = blockIdx.y, z = blockIdx.z;
-    xcd_remap<IsGrouped<Epi>::value>(bx, split, z);
-    const int tiles_n = sh.N / BN;
+    xcd_remap<IsGrouped<Epi>::value || IsSkGrouped<Epi>::value>(bx, split, z);
+    int tiles_n = sh.N / BN, K = sh.K, k_chunk = sh.k_chunk;
+    int sgi = 0, slz = 0;           // sketch group and matrix within it
+    if constexpr (IsSkGrouped<Epi>::value) {
+        while (sgi + 1 < epi.sg.n && z >= epi.sg.zbeg[sgi + 1]) ++sgi;
+        slz = z - epi.sg.zbeg[sgi];
+        tiles_n = epi.sg.N[sgi] / BN;
+        // The grid spans the largest group; the whole block leaves before
+        // its first barrier when its tile or split is past this group's.
+        if (bx >= (sh.M / BM) * tiles_n || split >= epi.sg.splits[sgi]) return;
+        K = epi.sg.K[sgi];
+        k_chunk = epi.sg.k_chunk[sgi];
+    }
     int tm, tn;
     decode_tile(bx, tiles_n, sh.sym, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
-    const int kbeg = split * sh.k_chunk;
-    int kend = min(sh.K, kbeg + sh.k_chunk);
+    const int kbeg = split * k_chunk;
+    int kend = min(K, kbeg + k_chunk);
 
     const half_t* Ab = A.ptr + (int64_t)z * A.batch_stride;
     const half_t* Bb = B.ptr + (int64_t)z * B.batch_stride;
@@ -271,6 +288,11 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
         kend = epi.gg.K[g];
         zo = epi.gg.zout[g] + lz;
         mulz = epi.gg.mul[g] ? epi.gg.mul[g] + 2 * lz : nullptr;
+    } else if constexpr (IsSkGrouped<Epi>::value) {
+        Ab = epi.sg.a[sgi] + (int64_t)slz * epi.sg.a_stride[sgi];
+        Bb = epi.sg.b[sgi] + (int64_t)slz * epi.sg.b_stride[sgi];
+        lda = epi.sg.lda[sgi];
+        ldb = epi.sg.ldb[sgi];
     } else if constexpr (Epi::kind == EpiKind::Affine) {
         mulz = epi.mul ? epi.mul + 2 * z : nullptr;
     }
@@ -450,12 +472,20 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     const int rw0 = m0 + wm * TM, cw0 = n0 + wn * TN;
 
     if constexpr (Epi::kind == EpiKind::Partial) {
-        float* out = epi.out + (int64_t)z * epi.stride_mat + (int64_t)split * epi.stride_split;
+        float* out;
+        int64_t ldo;
+        if constexpr (IsSkGrouped<Epi>::value) {
+            out = epi.sg.out[sgi] + (int64_t)slz * epi.sg.stride_mat[sgi] + (int64_t)split * epi.sg.stride_split[sgi];
+            ldo = epi.sg.N[sgi];
+        } else {
+            out = epi.out + (int64_t)z * epi.stride_mat + (int64_t)split * epi.stride_split;
+            ldo = epi.ld_out;
+        }
 #pragma unroll
         for (int qi = 0; qi < NQ; ++qi)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-                out[(int64_t)(rw0 + quad_row(qi) + r) * epi.ld_out + cw0 + quad_col(qi)] = quad_val(qi, r);
+                out[(int64_t)(rw0 + quad_row(qi) + r) * ldo + cw0 + quad_col(qi)] = quad_val(qi, r);
         return;
     } else {
         // Per-epilogue set-up.
@@ -694,6 +724,10 @@ struct EAffG : EpiAffine {
     GramGroups gg;
 };
 struct EPar : EpiPartial { static constexpr EpiKind kind = EpiKind::Partial; };
+struct EParG : EpiPartial {
+    static constexpr EpiKind kind = EpiKind::Partial;
+    SketchGroups sg;
+};
 struct EApp : EpiApplyUpdate { static constexpr EpiKind kind = EpiKind::Apply; };
 struct EAppN : EpiApplyNorm { static constexpr EpiKind kind = EpiKind::ApplyNorm; };
 
@@ -820,6 +854,33 @@ hipError_t launch_gemm_partial(TileCfg cfg, int layout, Operand A, Operand B, Ge
     switch (layout) {
         case 0: return dispatch_cfg<EPar, 0>(cfg, A, B, sh, batch, ee, s);
         case 1: return dispatch_cfg<EPar, 1>(cfg, A, B, sh, batch, ee, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemm_partial_grouped(TileCfg cfg, int layout, int M, const SketchGroups& g, hipStream_t s) {
+    if (cfg != TileCfg::Skinny64 && cfg != TileCfg::Skinny128) return hipErrorInvalidValue;
+    if (g.n < 1 || g.n > kMaxItems || g.zbeg[0] != 0 || (layout != 0 && layout != 1)) return hipErrorInvalidValue;
+    const int bm = gemm_tile_m(cfg), bn = gemm_tile_n(cfg);
+    if (M < bm || M % bm) return hipErrorInvalidValue;
+    int maxN = 0, maxS = 0;
+    for (int i = 0; i < g.n; ++i) {
+        if (g.zbeg[i + 1] <= g.zbeg[i] || g.N[i] < bn || g.N[i] % bn || g.K[i] < BK || g.K[i] % BK ||
+            g.k_chunk[i] < BK || g.k_chunk[i] % BK || g.splits[i] < 1 ||
+            (int64_t)(g.splits[i] - 1) * g.k_chunk[i] >= g.K[i] || (int64_t)g.splits[i] * g.k_chunk[i] < g.K[i])
+            return hipErrorInvalidValue;
+        maxN = std::max(maxN, g.N[i]);
+        maxS = std::max(maxS, g.splits[i]);
+    }
+    EParG ee{};
+    ee.sg = g;
+    // The grid spans the largest group (its tiles, its splits); operands
+    // and strides come from the table.
+    Operand dummy{nullptr, 0, 0};
+    GemmShape sh{M, maxN, BK, maxS, BK, 0};
+    switch (layout) {
+        case 0: return dispatch_cfg<EParG, 0>(cfg, dummy, dummy, sh, g.zbeg[g.n], ee, s);
+        case 1: return dispatch_cfg<EParG, 1>(cfg, dummy, dummy, sh, g.zbeg[g.n], ee, s);
     }
     return hipErrorInvalidValue;
 }

@@ -18,6 +18,10 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int kPad = 256;
 // The sketch width l is padded to a multiple of this (MFMA K granule).
 constexpr int kEllPad = 64;
+// Grouped launches over the items of one pool (same l): item g covers the
+// launch's matrices [zbeg[g], zbeg[g + 1]), which are also its matrices'
+// indices in the pool's l x l buffers.
+constexpr int kMaxItems = 8;
 
 inline int64_t round_up(int64_t x, int64_t g) { return (x + g - 1) / g * g; }
 
@@ -94,6 +98,21 @@ hipError_t launch_gemm_affine(TileCfg cfg, int layout, Operand A, Operand B,
 hipError_t launch_gemm_partial(TileCfg cfg, int layout, Operand A, Operand B,
                                GemmShape sh, int batch, const EpiPartial& e,
                                hipStream_t s);
+// Split-K sketch products of several shape groups with one padded width l
+// (M) in one launch.  Group g covers launch matrices [zbeg[g], zbeg[g + 1]):
+// operands a (M x K, K-major) and b (the W-layout Psi, per-matrix strides),
+// output length N, reduction length K in `splits` chunks of k_chunk, fp32
+// partials out[i][split][mm][nn] (ld N).  N, K and k_chunk are multiples of
+// the tile sizes and of 64; chunk `splits - 1` is the last non-empty one.
+struct SketchGroups {
+    int n;
+    int zbeg[kMaxItems + 1];
+    const half_t* a[kMaxItems]; int64_t lda[kMaxItems]; int64_t a_stride[kMaxItems];
+    const half_t* b[kMaxItems]; int64_t ldb[kMaxItems]; int64_t b_stride[kMaxItems];
+    int N[kMaxItems], K[kMaxItems], k_chunk[kMaxItems], splits[kMaxItems];
+    float* out[kMaxItems]; int64_t stride_split[kMaxItems]; int64_t stride_mat[kMaxItems];
+};
+hipError_t launch_gemm_partial_grouped(TileCfg cfg, int layout, int M, const SketchGroups& g, hipStream_t s);
 hipError_t launch_gemm_apply(Operand A, Operand B, GemmShape sh, int batch,
                              const EpiApplyUpdate& e, hipStream_t s);
 hipError_t launch_gemm_apply_norm(Operand A, Operand B, GemmShape sh, int batch,
@@ -207,14 +226,26 @@ hipError_t launch_reduce_splits(const float* part, int splits, int64_t stride_sp
                                 int64_t stride_mat, int rows, int64_t len,
                                 float* out32, half_t* out16, float scale16,
                                 int64_t stride_out, int batch, hipStream_t s);
+// The split sums of several sketch products in one launch: group g covers
+// launch matrices [zbeg[g], zbeg[g + 1]) with its own partials and outputs
+// (arguments as in launch_reduce_splits; rows x len per matrix).
+struct ReduceGroups {
+    int n;
+    int zbeg[kMaxItems + 1];
+    const float* part[kMaxItems];
+    int splits[kMaxItems];
+    int64_t stride_split[kMaxItems], stride_mat[kMaxItems];
+    int64_t n4[kMaxItems];                       // rows * len / 4
+    float* out32[kMaxItems];
+    half_t* out16[kMaxItems];
+    float scale16[kMaxItems];
+    int64_t stride_out[kMaxItems];
+};
+hipError_t launch_reduce_splits_grouped(const ReduceGroups& g, hipStream_t s);
 
 // Fixed number of length-chunk slots of the fp64 Gram partial sums (unused
 // slots hold zeros); its consumers always add all of them.
 constexpr int kGramChunks = 16;
-// Grouped launches over the items of one pool (same l): item g covers the
-// launch's matrices [zbeg[g], zbeg[g + 1]), which are also its matrices'
-// indices in the pool's l x l buffers.
-constexpr int kMaxItems = 8;
 
 // fp64 Gram of the rows of l-major fp32 matrices V (l_pad x len each):
 // partial[z][chunk][c][d] = sum_{j in chunk} V[c][j] V[d][j], upper tiles.

@@ -71,23 +71,46 @@ __global__ void omega_f32_kernel(uint64_t seed, int64_t step, uint32_t id, int64
 }
 
 // ------------------------------------------------------ split reduction ---
+// Partial sums of one split-K product: out = sum over splits in split order
+// (fp32), to fp32 and/or fp16 (times scale16).
+__device__ __forceinline__ void reduce_splits_one(const float4* p, int splits, int64_t split4, int64_t i,
+                                                  float* out32, half_t* out16, float scale16) {
+    float4 s = p[i];
+    for (int k = 1; k < splits; ++k) {
+        const float4 q = p[i + k * split4];
+        s.x += q.x; s.y += q.y; s.z += q.z; s.w += q.w;
+    }
+    if (out32) reinterpret_cast<float4*>(out32)[i] = s;
+    if (out16) {
+        half_t h[4] = {(half_t)(s.x * scale16), (half_t)(s.y * scale16), (half_t)(s.z * scale16),
+                       (half_t)(s.w * scale16)};
+        reinterpret_cast<uint2*>(out16)[i] = *reinterpret_cast<const uint2*>(h);
+    }
+}
+
 __global__ void reduce_splits_kernel(const float* part, int splits, int64_t stride_split, int64_t stride_mat,
                                      int64_t n4, float* out32, half_t* out16, float scale16, int64_t stride_out) {
     const int z = blockIdx.y;
     const float4* p = reinterpret_cast<const float4*>(part + (int64_t)z * stride_mat);
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
-        float4 s = p[i];
-        for (int k = 1; k < splits; ++k) {
-            const float4 q = p[i + k * (stride_split / 4)];
-            s.x += q.x; s.y += q.y; s.z += q.z; s.w += q.w;
-        }
-        if (out32) reinterpret_cast<float4*>(out32 + (int64_t)z * stride_out)[i] = s;
-        if (out16) {
-            half_t h[4] = {(half_t)(s.x * scale16), (half_t)(s.y * scale16), (half_t)(s.z * scale16),
-                           (half_t)(s.w * scale16)};
-            reinterpret_cast<uint2*>(out16 + (int64_t)z * stride_out)[i] = *reinterpret_cast<const uint2*>(h);
-        }
-    }
+    float* o32 = out32 ? out32 + (int64_t)z * stride_out : nullptr;
+    half_t* o16 = out16 ? out16 + (int64_t)z * stride_out : nullptr;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x)
+        reduce_splits_one(p, splits, stride_split / 4, i, o32, o16, scale16);
+}
+
+// The split sums of several sketch products, matrix z of the launch in the
+// group whose range holds it.
+__global__ void reduce_splits_grouped_kernel(ReduceGroups g) {
+    const int z = blockIdx.y;
+    int gi = 0;
+    while (gi + 1 < g.n && z >= g.zbeg[gi + 1]) ++gi;
+    const int lz = z - g.zbeg[gi];
+    const float4* p = reinterpret_cast<const float4*>(g.part[gi] + (int64_t)lz * g.stride_mat[gi]);
+    float* o32 = g.out32[gi] ? g.out32[gi] + (int64_t)lz * g.stride_out[gi] : nullptr;
+    half_t* o16 = g.out16[gi] ? g.out16[gi] + (int64_t)lz * g.stride_out[gi] : nullptr;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < g.n4[gi];
+         i += (int64_t)gridDim.x * blockDim.x)
+        reduce_splits_one(p, g.splits[gi], g.stride_split[gi] / 4, i, o32, o16, g.scale16[gi]);
 }
 
 // ------------------------------------------------------------ fp64 Gram ---
@@ -1145,6 +1168,19 @@ hipError_t launch_reduce_splits(const float* part, int splits, int64_t stride_sp
     const unsigned blocks = (unsigned)std::min<int64_t>((n4 + 255) / 256, 2048);
     hipLaunchKernelGGL(reduce_splits_kernel, dim3(blocks, batch), dim3(256), 0, s, part, splits, stride_split,
                        stride_mat, n4, out32, out16, scale16, stride_out);
+    return hipGetLastError();
+}
+
+hipError_t launch_reduce_splits_grouped(const ReduceGroups& g, hipStream_t s) {
+    if (g.n < 1 || g.n > kMaxItems || g.zbeg[0] != 0) return hipErrorInvalidValue;
+    int64_t n4 = 0;
+    for (int i = 0; i < g.n; ++i) {
+        if (g.zbeg[i + 1] <= g.zbeg[i] || g.splits[i] < 1 || g.stride_split[i] % 4 || g.n4[i] < 1)
+            return hipErrorInvalidValue;
+        n4 = std::max(n4, g.n4[i]);
+    }
+    const unsigned blocks = (unsigned)std::min<int64_t>((n4 + 255) / 256, 2048);
+    hipLaunchKernelGGL(reduce_splits_grouped_kernel, dim3(blocks, g.zbeg[g.n]), dim3(256), 0, s, g);
     return hipGetLastError();
 }
 
