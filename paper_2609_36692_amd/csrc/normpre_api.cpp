@@ -382,6 +382,7 @@ struct Item {
     GWork w{};
     int pool = -1;        // pool of its small matrices
     int pool_off = 0;     // its first matrix inside the pool
+    TileCfg ccfg = TileCfg::Big;   // tile of its Newton-Schulz combines
 };
 
 // Small matrices shared by the items of a round that have the same width:
@@ -788,7 +789,7 @@ int combine_launch(const StepCtx& sc, const Item& it, const Pool& pl, half_t* x,
     e.src = x; e.ld_src = d.np_; e.stride_src = mn;
     e.mul = first_it ? it.w.scale : nullptr; e.mul_pow = first_it ? 1 : 0;
     e.ca = 1.f; e.cs = sc.hp->ns_coeffs[0];
-    const TileCfg cfg = ns_cfg(d.mp, d.np_, false, count);
+    const TileCfg cfg = it.ccfg;
     e.sumsq = last_it ? it.w.sumsq : nullptr;
     e.tiles_per_mat = combine_tiles(d, cfg);
     auto go = [&]() -> hipError_t {
@@ -809,6 +810,72 @@ int combine_launch(const StepCtx& sc, const Item& it, const Pool& pl, half_t* x,
     return NORMPRE_OK;
 }
 
+// The combines of the wide items (m <= n) of one pool, in chunks of up to
+// kMaxItems: one launch each, one tile for the chunk from its total tile
+// count (ns_cfg's rule), so small shape groups fill the chip together.
+std::vector<std::vector<Item*>> wide_combine_chunks(std::vector<Item>& items, size_t npools) {
+    std::vector<std::vector<Item*>> chunks;
+    for (size_t pi = 0; pi < npools; ++pi) {
+        std::vector<Item*> cur;
+        for (Item& it : items) {
+            if (it.pool != (int)pi || it.d.tall) continue;
+            cur.push_back(&it);
+            if ((int)cur.size() == kMaxItems) {
+                chunks.push_back(cur);
+                cur.clear();
+            }
+        }
+        if (!cur.empty()) chunks.push_back(cur);
+    }
+    for (auto& ch : chunks) {
+        int64_t tiles = 0;
+        for (const Item* it : ch) tiles += (it->d.mp / 256) * (it->d.np_ / 256) * it->count;
+        const TileCfg cfg = tiles >= 384 ? TileCfg::Big256 : TileCfg::Big;
+        for (Item* it : ch) it->ccfg = cfg;
+    }
+    return chunks;
+}
+
+int combine_grouped_launch(const StepCtx& sc, const std::vector<Item*>& ch, const Pool& pl, int iter, bool first_it,
+                           bool last_it) {
+    CombineGroups g{};
+    int total = 0;
+    double flops = 0.0, bytes = 0.0;
+    const TileCfg cfg = ch[0]->ccfg;
+    const int64_t sp = ch[0]->d.sp;
+    for (const Item* it : ch) {
+        const Dims& d = it->d;
+        const int64_t mn = d.mp * d.np_, ss = d.sp * d.sp;
+        if (d.sp != sp || it->ccfg != cfg || d.tall)
+            return set_err(sc.ctx, NORMPRE_ERR_HIP, "internal: combines of one launch differ in s or tile");
+        half_t* x = (iter & 1) ? it->w.xb : it->w.psi;
+        half_t* xn = (iter & 1) ? it->w.psi : it->w.xb;
+        const int i = g.n++;
+        g.zbeg[i] = total;
+        g.a[i] = pl.bmat + (int64_t)it->pool_off * ss; g.lda[i] = d.sp; g.a_stride[i] = ss;
+        g.b[i] = x; g.ldb[i] = d.np_; g.b_stride[i] = mn;
+        g.N[i] = (int)d.lp_;
+        g.out[i] = xn; g.ld_out[i] = d.np_; g.stride_out[i] = mn;
+        g.src[i] = x; g.ld_src[i] = d.np_; g.stride_src[i] = mn;
+        g.mul[i] = first_it ? it->w.scale : nullptr;
+        g.sumsq[i] = last_it ? it->w.sumsq : nullptr;
+        g.tiles[i] = combine_tiles(d, cfg);
+        const double s_ = (double)std::min(d.m, d.n), l_ = (double)std::max(d.m, d.n);
+        flops += 2.0 * s_ * s_ * l_ * it->count;
+        bytes += 2.0 * (2.0 * s_ * l_ + s_ * s_) * it->count;
+        total += it->count;
+    }
+    g.zbeg[g.n] = total;
+    EpiAffine e{};
+    e.mul_pow = first_it ? 1 : 0;
+    e.ca = 1.f;
+    e.cs = sc.hp->ns_coeffs[0];
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_COMBINE, flops, bytes,
+                 [&] { return launch_gemm_combine_grouped(cfg, (int)sp, g, e, sc.s); }),
+           "ns combine");
+    return NORMPRE_OK;
+}
+
 int g_update_launch(const StepCtx& sc, const Item& it, const half_t* t, DebugMat* dbg) {
     const Dims& d = it.d;
     const normpre_hparams& hp = *sc.hp;
@@ -821,7 +888,7 @@ int g_update_launch(const StepCtx& sc, const Item& it, const half_t* t, DebugMat
     int64_t tn2_stride = 1;
     float fixed_scale = 0.f;
     if (sc.variant == NORMPRE_VARIANT_G) {
-        const int t_tiles = combine_tiles(d, ns_cfg(d.mp, d.np_, false, count));
+        const int t_tiles = combine_tiles(d, it.ccfg);
         NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
                      [&] { return launch_sum_partials(it.w.sumsq, t_tiles, it.w.tn2, count, sc.s); }),
                "t norm");
@@ -890,6 +957,11 @@ int run_round_g(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& 
     // into the first iteration's epilogues.
     const bool fold_scale = sc.variant == NORMPRE_VARIANT_G;
     const int q = sc.variant == NORMPRE_VARIANT_NORMALIZE_ONLY ? 0 : sc.hp->ns_iters;
+    // Combine tiles: the wide items of a pool share launches; tall ones run
+    // per item.
+    for (Item& it : items)
+        if (it.d.tall) it.ccfg = ns_cfg(it.d.mp, it.d.np_, false, it.count);
+    const auto wide = wide_combine_chunks(items, pools.size());
     for (int iter = 0; iter < q; ++iter) {
         const bool first_it = iter == 0 && fold_scale, last_it = iter == q - 1;
         int rc = gram_launches(sc, items, pools, iter, first_it);
@@ -904,7 +976,17 @@ int run_round_g(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& 
             int rc = poly_launch(sc, pools[pi], flops);
             if (rc) return rc;
         }
+        for (const auto& ch : wide) {
+            const Item& it0 = *ch[0];
+            half_t* x = (iter & 1) ? it0.w.xb : it0.w.psi;
+            half_t* xn = (iter & 1) ? it0.w.psi : it0.w.xb;
+            // A lone item takes the plain launch (no table to walk).
+            int rc = ch.size() == 1 ? combine_launch(sc, it0, pools[it0.pool], x, xn, first_it, last_it)
+                                    : combine_grouped_launch(sc, ch, pools[it0.pool], iter, first_it, last_it);
+            if (rc) return rc;
+        }
         for (const Item& it : items) {
+            if (!it.d.tall) continue;
             half_t* x = (iter & 1) ? it.w.xb : it.w.psi;
             half_t* xn = (iter & 1) ? it.w.psi : it.w.xb;
             int rc = combine_launch(sc, it, pools[it.pool], x, xn, first_it, last_it);

@@ -160,22 +160,6 @@ __device__ __forceinline__ float wave_sum(float v) {
     return v;
 }
 
-template <class E>
-__device__ __forceinline__ bool epi_has_sumsq(const E& e) {
-    if constexpr (E::kind == EpiKind::Affine || E::kind == EpiKind::ApplyNorm) return e.sumsq != nullptr;
-    else return false;
-}
-template <class E>
-__device__ __forceinline__ float* epi_sumsq_ptr(const E& e) {
-    if constexpr (E::kind == EpiKind::Affine || E::kind == EpiKind::ApplyNorm) return e.sumsq;
-    else return nullptr;
-}
-template <class E>
-__device__ __forceinline__ int epi_tiles(const E& e) {
-    if constexpr (E::kind == EpiKind::Affine || E::kind == EpiKind::ApplyNorm) return e.tiles_per_mat;
-    else return 0;
-}
-
 // Maps the hardware block order (dispatched round-robin over the 8 XCDs) to
 // a logical order in which each XCD owns one contiguous range of tiles, so
 // neighbouring tiles of a matrix share that XCD's L2.
@@ -219,6 +203,11 @@ template <class E, class = void>
 struct IsGrouped { static constexpr bool value = false; };
 template <class E>
 struct IsGrouped<E, std::void_t<decltype(std::declval<E>().gg)>> { static constexpr bool value = true; };
+// Epilogues that carry a CombineGroups table (grouped Newton-Schulz combines).
+template <class E, class = void>
+struct IsCmbGrouped { static constexpr bool value = false; };
+template <class E>
+struct IsCmbGrouped<E, std::void_t<decltype(std::declval<E>().cg)>> { static constexpr bool value = true; };
 // Epilogues that carry a SketchGroups table (grouped split-K sketch products).
 template <class E, class = void>
 struct IsSkGrouped { static constexpr bool value = false; };
@@ -254,7 +243,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave - (wave / WN) * WN;
     int bx = blockIdx.x, split = blockIdx.y, z = blockIdx.z;
-    xcd_remap<IsGrouped<Epi>::value || IsSkGrouped<Epi>::value>(bx, split, z);
+    xcd_remap<IsGrouped<Epi>::value || IsSkGrouped<Epi>::value || IsCmbGrouped<Epi>::value>(bx, split, z);
     int tiles_n = sh.N / BN, K = sh.K, k_chunk = sh.k_chunk;
     int sgi = 0, slz = 0;           // sketch group and matrix within it
     if constexpr (IsSkGrouped<Epi>::value) {
@@ -266,6 +255,13 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
         if (bx >= (sh.M / BM) * tiles_n || split >= epi.sg.splits[sgi]) return;
         K = epi.sg.K[sgi];
         k_chunk = epi.sg.k_chunk[sgi];
+    }
+    int cgi = 0, clz = 0;           // combine group and matrix within it
+    if constexpr (IsCmbGrouped<Epi>::value) {
+        while (cgi + 1 < epi.cg.n && z >= epi.cg.zbeg[cgi + 1]) ++cgi;
+        clz = z - epi.cg.zbeg[cgi];
+        tiles_n = epi.cg.N[cgi] / BN;
+        if (bx >= (sh.M / BM) * tiles_n) return;   // whole block, before any barrier
     }
     int tm, tn;
     decode_tile(bx, tiles_n, sh.sym, tm, tn);
@@ -288,6 +284,13 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
         kend = epi.gg.K[g];
         zo = epi.gg.zout[g] + lz;
         mulz = epi.gg.mul[g] ? epi.gg.mul[g] + 2 * lz : nullptr;
+    } else if constexpr (IsCmbGrouped<Epi>::value) {
+        Ab = epi.cg.a[cgi] + (int64_t)clz * epi.cg.a_stride[cgi];
+        Bb = epi.cg.b[cgi] + (int64_t)clz * epi.cg.b_stride[cgi];
+        lda = epi.cg.lda[cgi];
+        ldb = epi.cg.ldb[cgi];
+        zo = clz;
+        mulz = epi.cg.mul[cgi] ? epi.cg.mul[cgi] + 2 * clz : nullptr;
     } else if constexpr (IsSkGrouped<Epi>::value) {
         Ab = epi.sg.a[sgi] + (int64_t)slz * epi.sg.a_stride[sgi];
         Bb = epi.sg.b[sgi] + (int64_t)slz * epi.sg.b_stride[sgi];
@@ -295,6 +298,35 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
         ldb = epi.sg.ldb[sgi];
     } else if constexpr (Epi::kind == EpiKind::Affine) {
         mulz = epi.mul ? epi.mul + 2 * z : nullptr;
+    }
+    // Per-matrix operands of the Affine and ApplyNorm epilogues (the grouped
+    // combine takes them from its table).
+    half_t* e_out = nullptr;
+    const half_t* e_src = nullptr;
+    int64_t e_ld_out = 0, e_stride_out = 0, e_ld_src = 0, e_stride_src = 0;
+    float* e_sumsq = nullptr;
+    int e_tiles = 0;
+    if constexpr (IsCmbGrouped<Epi>::value) {
+        e_out = epi.cg.out[cgi];
+        e_ld_out = epi.cg.ld_out[cgi];
+        e_stride_out = epi.cg.stride_out[cgi];
+        e_src = epi.cg.src[cgi];
+        e_ld_src = epi.cg.ld_src[cgi];
+        e_stride_src = epi.cg.stride_src[cgi];
+        e_sumsq = epi.cg.sumsq[cgi];
+        e_tiles = epi.cg.tiles[cgi];
+    } else if constexpr (Epi::kind == EpiKind::Affine) {
+        e_out = epi.out;
+        e_ld_out = epi.ld_out;
+        e_stride_out = epi.stride_out;
+        e_src = epi.src;
+        e_ld_src = epi.ld_src;
+        e_stride_src = epi.stride_src;
+        e_sumsq = epi.sumsq;
+        e_tiles = epi.tiles_per_mat;
+    } else if constexpr (Epi::kind == EpiKind::ApplyNorm) {
+        e_sumsq = epi.sumsq;
+        e_tiles = epi.tiles_per_mat;
     }
     using LA = typename LoaderSel<(LAYOUT == 2), BM, NT>::type;
     using LB = typename LoaderSel<(LAYOUT >= 1), BN, NT>::type;
@@ -503,8 +535,8 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
             }
             ca = epi.ca * mul;
             cs = epi.cs * mul;
-            out = epi.out + (int64_t)zo * epi.stride_out;
-            src = epi.src ? epi.src + (int64_t)zo * epi.stride_src : nullptr;
+            out = e_out + (int64_t)zo * e_stride_out;
+            src = e_src ? e_src + (int64_t)zo * e_stride_src : nullptr;
             // Off-diagonal tiles of a symmetric result also write their
             // transpose.  src is symmetric wherever the result is (A for
             // B = b A + c A^2), so the transpose's src values are read from
@@ -520,7 +552,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                         const int col = cw0 + quad_col(qi), row0 = rw0 + quad_row(qi);
                         half_t sv[4] = {};
                         if (src) *reinterpret_cast<u32x2*>(sv) =
-                                     *reinterpret_cast<const u32x2*>(src + (int64_t)col * epi.ld_src + row0);
+                                     *reinterpret_cast<const u32x2*>(src + (int64_t)col * e_ld_src + row0);
                         half_t hv[4];
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
@@ -529,7 +561,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                             hv[r] = (half_t)v;
                         }
                         // (A plain store: the 8-byte pieces merge in L2.)
-                        *reinterpret_cast<u32x2*>(out + (int64_t)col * epi.ld_out + row0) =
+                        *reinterpret_cast<u32x2*>(out + (int64_t)col * e_ld_out + row0) =
                             *reinterpret_cast<const u32x2*>(hv);
                     }
                 }
@@ -565,7 +597,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                         const int c = tid + q * NT;
                         if (c < PR * C8) {
                             const int r = c / C8, c8 = (c - r * C8) * 8;
-                            sbuf[q] = *reinterpret_cast<const u32x4*>(src + (int64_t)(m0 + pass * PR + r) * epi.ld_src +
+                            sbuf[q] = *reinterpret_cast<const u32x4*>(src + (int64_t)(m0 + pass * PR + r) * e_ld_src +
                                                                       n0 + c8);
                         }
                     }
@@ -668,7 +700,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                     // operand panels resident.
                     const u32x4 hq = *reinterpret_cast<const u32x4*>(hv);
                     if constexpr (kLdsMirror) hk[it] = hq;
-                    __builtin_nontemporal_store(hq, reinterpret_cast<u32x4*>(out + (int64_t)grow * epi.ld_out + gcol));
+                    __builtin_nontemporal_store(hq, reinterpret_cast<u32x4*>(out + (int64_t)grow * e_ld_out + gcol));
                 }
             }
             if constexpr (Epi::kind == EpiKind::Affine && kLdsMirror) {
@@ -697,13 +729,13 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                         const int cc = q / R8, j = q - cc * R8;
                         const u32x4 v = *reinterpret_cast<const u32x4*>(tb + cc * PR + ((j ^ ((cc >> 3) & (R8 - 1))) << 3));
                         __builtin_nontemporal_store(
-                            v, reinterpret_cast<u32x4*>(out + (int64_t)(n0 + cc) * epi.ld_out + m0 + pass * PR + 8 * j));
+                            v, reinterpret_cast<u32x4*>(out + (int64_t)(n0 + cc) * e_ld_out + m0 + pass * PR + 8 * j));
                     }
                 }
             }
         }
         const bool want_sum = (Epi::kind == EpiKind::ApplyNorm) ||
-                              (Epi::kind == EpiKind::Affine && epi_has_sumsq(epi));
+                              (Epi::kind == EpiKind::Affine && e_sumsq != nullptr);
         if (want_sum) {
             ss = wave_sum(ss);
             lds_barrier();
@@ -712,7 +744,7 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
             if (tid == 0) {
                 float t = 0.f;
                 for (int q = 0; q < NT / 64; ++q) t += red[q];
-                epi_sumsq_ptr(epi)[(int64_t)zo * epi_tiles(epi) + bx] = t;
+                e_sumsq[(int64_t)zo * e_tiles + bx] = t;
             }
         }
     }
@@ -724,6 +756,10 @@ struct EAffG : EpiAffine {
     GramGroups gg;
 };
 struct EPar : EpiPartial { static constexpr EpiKind kind = EpiKind::Partial; };
+struct EAffC : EpiAffine {
+    static constexpr EpiKind kind = EpiKind::Affine;
+    CombineGroups cg;
+};
 struct EParG : EpiPartial {
     static constexpr EpiKind kind = EpiKind::Partial;
     SketchGroups sg;
@@ -883,6 +919,29 @@ hipError_t launch_gemm_partial_grouped(TileCfg cfg, int layout, int M, const Ske
         case 1: return dispatch_cfg<EParG, 1>(cfg, dummy, dummy, sh, g.zbeg[g.n], ee, s);
     }
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemm_combine_grouped(TileCfg cfg, int s_dim, const CombineGroups& g, const EpiAffine& e,
+                                       hipStream_t s) {
+    if (cfg != TileCfg::Big && cfg != TileCfg::Big256) return hipErrorInvalidValue;
+    if (g.n < 1 || g.n > kMaxItems || g.zbeg[0] != 0) return hipErrorInvalidValue;
+    const int t = cfg == TileCfg::Big256 ? 256 : 128;
+    if (s_dim < t || s_dim % t) return hipErrorInvalidValue;
+    int maxN = 0;
+    for (int i = 0; i < g.n; ++i) {
+        if (g.zbeg[i + 1] <= g.zbeg[i] || g.N[i] < t || g.N[i] % t) return hipErrorInvalidValue;
+        if (g.sumsq[i] && g.tiles[i] != (s_dim / t) * (g.N[i] / t)) return hipErrorInvalidValue;
+        maxN = std::max(maxN, g.N[i]);
+    }
+    EAffC ee{};
+    static_cast<EpiAffine&>(ee) = e;
+    ee.cg = g;
+    // The grid spans the widest group; operands, outputs and scales come
+    // from the table.
+    Operand dummy{nullptr, 0, 0};
+    GemmShape sh{s_dim, maxN, s_dim, 1, s_dim, 0};
+    if (cfg == TileCfg::Big) return run<128, 128, 2, 2, 1>(dummy, dummy, sh, g.zbeg[g.n], ee, s);
+    return run<256, 256, 2, 4, 1, EAffC, 32>(dummy, dummy, sh, g.zbeg[g.n], ee, s);
 }
 
 hipError_t launch_gemm_gram_f32(int layout, Operand A, Operand B, GemmShape sh, int batch, const EpiPartial& e,

@@ -113,6 +113,25 @@ struct SketchGroups {
     float* out[kMaxItems]; int64_t stride_split[kMaxItems]; int64_t stride_mat[kMaxItems];
 };
 hipError_t launch_gemm_partial_grouped(TileCfg cfg, int layout, int M, const SketchGroups& g, hipStream_t s);
+// Newton-Schulz combines X <- a X + B X of the wide shape groups of one s in
+// one launch (B MN-major: the layout-1 combine).  Group g covers launch
+// matrices [zbeg[g], zbeg[g + 1]) with its own B (s x s), X (s x N), output,
+// source, first-iteration scale (mul[2 i]; null = 1) and per-tile sums of
+// squares (sumsq, tiles per matrix; null = none).  ca, cs and mul_pow come
+// from the EpiAffine argument.
+struct CombineGroups {
+    int n;
+    int zbeg[kMaxItems + 1];
+    const half_t* a[kMaxItems]; int64_t lda[kMaxItems]; int64_t a_stride[kMaxItems];
+    const half_t* b[kMaxItems]; int64_t ldb[kMaxItems]; int64_t b_stride[kMaxItems];
+    int N[kMaxItems];
+    half_t* out[kMaxItems]; int64_t ld_out[kMaxItems]; int64_t stride_out[kMaxItems];
+    const half_t* src[kMaxItems]; int64_t ld_src[kMaxItems]; int64_t stride_src[kMaxItems];
+    const float* mul[kMaxItems];
+    float* sumsq[kMaxItems]; int tiles[kMaxItems];
+};
+hipError_t launch_gemm_combine_grouped(TileCfg cfg, int s_dim, const CombineGroups& g, const EpiAffine& e,
+                                       hipStream_t s);
 hipError_t launch_gemm_apply(Operand A, Operand B, GemmShape sh, int batch,
                              const EpiApplyUpdate& e, hipStream_t s);
 hipError_t launch_gemm_apply_norm(Operand A, Operand B, GemmShape sh, int batch,
