@@ -1059,6 +1059,15 @@ int sketch_product_run(const StepCtx& sc, const std::vector<const Item*>& its, b
     int layout = -1, total = 0;
     int64_t lp0 = 0;
     double flops = 0.0, bytes = 0.0;
+    // The split count comes from the launch's total tile count: every item's
+    // split chunks fill the chip together.
+    int64_t all_tiles = 0;
+    for (const Item* it : its) {
+        const Dims& d = it->d;
+        const bool pv = over_active == (d.k == 0);
+        const TileCfg c = d.ellp == 128 ? TileCfg::Skinny128 : TileCfg::Skinny64;
+        all_tiles += (d.ellp / gemm_tile_m(c)) * ((pv ? d.mp : d.np_) / gemm_tile_n(c)) * it->count;
+    }
     for (const Item* it : its) {
         const Dims& d = it->d;
         const GWork& w = it->w;
@@ -1075,8 +1084,7 @@ int sketch_product_run(const StepCtx& sc, const std::vector<const Item*>& its, b
         } else if (c != cfg || layout != (pv ? 0 : 1) || lp != lp0) {
             return set_err(sc.ctx, NORMPRE_ERR_HIP, "internal: sketch products of one launch differ in l or side");
         }
-        const int64_t tiles = (lp / gemm_tile_m(cfg)) * (n_out / gemm_tile_n(cfg));
-        const int splits = pick_splits(tiles, it->count, k_len);
+        const int splits = pick_splits(all_tiles, 1, k_len);
         const int64_t k_chunk = round_up((k_len + splits - 1) / splits, 64);
         const int real_splits = (int)((k_len + k_chunk - 1) / k_chunk);
         const int i = g.n++;
