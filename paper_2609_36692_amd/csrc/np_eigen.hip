@@ -2,18 +2,20 @@
 // Gamma = Psi Psi^T of one active orientation (n = active rows, up to a few
 // thousand):
 //   * Householder reduction to tridiagonal form (working matrix stored in
-//     fp32, all arithmetic and the vectors in fp64), one reflector per step:
-//     a one-block kernel forms the reflector of column j, and one streaming
+//     fp32, all arithmetic and the vectors in fp64): up to n = 192 one
+//     launch with the matrix in LDS; above, one reflector per step: a
+//     one-block kernel forms the reflector of column j, and one streaming
 //     pass over the trailing rows applies the previous step's rank-2 update
 //     and forms the next product p = tau A v in the same read;
-//   * eigenvalues of the tridiagonal matrix by bisection on Sturm counts
-//     (one thread per eigenvalue, any subset of indices);
+//   * eigenvalues of the tridiagonal matrix by multisection on Sturm counts
+//     (16 lanes per eigenvalue, any subset of indices);
 //   * eigenvectors of the selected eigenvalues by inverse iteration with a
 //     partially pivoted tridiagonal LU, Gram-Schmidt inside clusters of
 //     close eigenvalues, and back-transformation through the reflectors.
 // Used by the exact variant of NormPre-L (App. B, exact eigenspace
-// extraction: the leading eigenvectors of Gamma span the selected modes) and
-// by the spectral diagnostics of the normalized and unnormalized Grams
+// extraction: the leading eigenvectors of Gamma span the selected modes), by
+// the Rayleigh-Ritz problems of the sketch wider than the Jacobi's limit,
+// and by the spectral diagnostics of the normalized and unnormalized Grams
 // (App. A, spectral dynamics).  Matrices of one launch share n (grid y).
 #include "np_internal.h"
 
