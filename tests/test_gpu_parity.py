@@ -137,7 +137,12 @@ def test_g_step_parity(ctx, shape, t):
 L_CASES = [((256, 256), 16), ((257, 513), 8), ((300, 1), 4), ((3, 3), 2), ((768, 2304), 32),
            ((3072, 768), 32), ((640, 700), 64), ((40, 500), 64),
            # l above 96: Cholesky-QR in LDS-staged panels out of global scratch
-           ((640, 700), 100), ((640, 700), 140), ((1000, 400), 300)]
+           ((640, 700), 100), ((640, 700), 140), ((1000, 400), 300),
+           # both sides of each width switch (l = r + 8): LDS / panel Cholesky
+           # at 96 / 97, Jacobi / dense Ritz solver at 104 / 105, one-launch /
+           # per-column tridiagonal reduction at 192 / 193
+           ((640, 700), 88), ((640, 700), 89), ((640, 700), 96), ((640, 700), 97),
+           ((640, 700), 184), ((640, 700), 185)]
 
 
 @pytest.mark.parametrize("shape,rank", L_CASES)
