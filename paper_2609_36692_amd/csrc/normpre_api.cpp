@@ -1790,7 +1790,7 @@ int normpre_spectrum(normpre_ctx* ctx, int which, int64_t rows, int64_t cols, co
         g.tw.e = ar.take<double>(a);
         g.tw.tau = ar.take<double>(a);
         g.lam = ar.take<double>(a);
-        mcopy = ar.take<float>(rows * cols);
+        mcopy = ar.take<float>(round_up(rows * cols, 4));   // whole 16-byte blocks for the clear
         return ar.off + 256;
     };
     float* mcopy = nullptr;
@@ -1806,7 +1806,7 @@ int normpre_spectrum(normpre_ctx* ctx, int which, int64_t rows, int64_t cols, co
     const float* Gl[1] = {m};
     float* Ml[1] = {mcopy};
     StepCtx sc{ctx, s, &h, Wl, Gl, Ml, NORMPRE_VARIANT_NORMALIZE_ONLY, false, &groups};
-    NP_TRY(launch_fill_zero(mcopy, rows * cols * 4, s), "clear momentum copy");
+    NP_TRY(launch_fill_zero(mcopy, round_up(rows * cols, 4) * 4, s), "clear momentum copy");
     rc = run_normalize(sc, d, it.w, groups[0].idx, 0, 1, nullptr);
     if (rc) return rc;
     const half_t* src = gx ? it.w.xs : it.w.psi;

@@ -386,7 +386,10 @@ def test_l_exact_matches_oracle(ctx, shape, t):
 # ------------------------------------------------- spectral diagnostics (App. A)
 @pytest.mark.parametrize("shape,t,which", [((300, 200), 0, "gamma"), ((300, 200), 1, "gamma"), ((300, 200), 0, "gx"),
                                            ((768, 2304), 0, "gamma"), ((768, 2304), 0, "gx"),
-                                           ((1000, 300), 0, "gamma"), ((1000, 300), 1, "gx")])
+                                           ((1000, 300), 0, "gamma"), ((1000, 300), 1, "gx"),
+                                           # one-launch / per-column tridiagonal reduction
+                                           ((192, 150), 0, "gamma"), ((193, 150), 0, "gamma"),
+                                           ((40, 500), 0, "gx")])
 def test_spectrum_matches_oracle(ctx, shape, t, which):
     _say(f"spectrum {which} shape={shape} t={t}")
     w, g, mp = _inputs(shape, "lowrank", seed=13)
