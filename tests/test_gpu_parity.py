@@ -180,6 +180,19 @@ def test_batched_equals_single_g(ctx):
         assert torch.equal(alone["w"], together[i]["w"])
 
 
+def test_mixed_shapes_g(ctx):
+    # wide shapes of one s share grouped Gram and combine launches; the tall
+    # one and a lone other s take their own
+    _say("mixed shapes (G)")
+    shapes = [(256, 256), (200, 512), (256, 1024), (512, 256), (100, 700)]
+    mats = [_inputs(sh, seed=20 + i) for i, sh in enumerate(shapes)]
+    for t in (0, 1):
+        res = run_step(ctx, "G", mats, t, debug=False)
+        for i, mat in enumerate(mats):
+            ref = oracle(mat, "G", t, matrix_id=i)
+            assert O.relative_fro(res[i]["u"], ref["update"]) < TOL_G
+
+
 def test_mixed_shapes_and_ids_l(ctx):
     _say("mixed shapes (L), matrix ids")
     mats = [_inputs((200, 300), seed=1), _inputs((128, 64), seed=2), _inputs((200, 300), seed=3)]
