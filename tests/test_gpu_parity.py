@@ -371,7 +371,7 @@ def test_reference_steps_zero_signal(ctx, variant):
 
 # ------------------------------------------------------ NormPre-L Exact
 @pytest.mark.parametrize("shape,t", [((256, 256), 0), ((256, 256), 1), ((300, 200), 0), ((100, 1000), 0),
-                                     ((1000, 300), 1), ((64, 64), 0),
+                                     ((1000, 300), 1), ((64, 64), 0), ((150, 400), 0),
                                      # above 384 active rows: the dense eigensolver
                                      ((512, 700), 0), ((512, 700), 1), ((1000, 300), 0), ((768, 2304), 1)])
 def test_l_exact_matches_oracle(ctx, shape, t):
