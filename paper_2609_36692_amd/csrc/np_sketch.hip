@@ -227,14 +227,18 @@ constexpr int kSmallThreads = 512;
 
 constexpr int kCholThreads = 1024;
 // Upper-triangle entries (i <= j) owned per thread: l (l + 1) / 2 entries for
-// l <= kCholLdsMax over kCholThreads threads.
-constexpr int kCholOwn = (kCholLdsMax * (kCholLdsMax + 1) / 2 + kCholThreads - 1) / kCholThreads;
+// l <= kCholLdsMax over NT threads.
+template <int NT>
+constexpr int chol_own() { return (kCholLdsMax * (kCholLdsMax + 1) / 2 + NT - 1) / NT; }
+// Threads of the LDS kernel (measured: 512 a little ahead of 256 and 1024).
+constexpr int kCholLdsThreads = 512;
 
 // l <= kCholLdsMax: the whole matrix lives in LDS (fp64, row stride l + 1);
 // R^{-1} overwrites R in place.
-__global__ void __launch_bounds__(kCholThreads) chol_inv_kernel(const double* partial, int chunks, int ell,
-                                                                int ell_pad, float* rinv) {
-    constexpr int NT = kCholThreads;
+template <int NT>
+__global__ void __launch_bounds__(NT) chol_inv_kernel(const double* partial, int chunks, int ell, int ell_pad,
+                                                      float* rinv) {
+    constexpr int kCholOwn = chol_own<NT>();
     extern __shared__ double dynd[];
     const int z = blockIdx.x, tid = threadIdx.x;
     const double* p = partial + (int64_t)z * chunks * ell_pad * ell_pad;
@@ -1204,8 +1208,8 @@ hipError_t launch_chol_inv(const double* partial, int chunks, int ell, int ell_p
     if (ell < 1 || ell > 384 || ell_pad < ell || ell_pad > 384 || chunks != kGramChunks) return hipErrorInvalidValue;
     if (ell <= kCholLdsMax) {
         const size_t lds = (size_t)(ell + 1) * (ell + 1) * sizeof(double);
-        hipLaunchKernelGGL(chol_inv_kernel, dim3(batch), dim3(kCholThreads), lds, s, partial, chunks, ell, ell_pad,
-                           rinv);
+        hipLaunchKernelGGL(chol_inv_kernel<kCholLdsThreads>, dim3(batch), dim3(kCholLdsThreads), lds, s, partial,
+                           chunks, ell, ell_pad, rinv);
     } else {
         const size_t lds = (size_t)std::max(kPanelC, 2 * kPanelI) * (ell + 1) * sizeof(double);
         hipLaunchKernelGGL(chol_inv_panel_kernel, dim3(batch), dim3(kCholThreads), lds, s, partial, chunks, ell,
