@@ -151,33 +151,59 @@ __global__ void __launch_bounds__(kRowWaves * 64) tri_update_kernel(float* A, in
     if (lane == 0) P[i] = tau[(int64_t)z * stride_n + j] * dot;
 }
 
-// Householder tridiagonalization of one matrix per block for n <= kTriLdsMax,
-// the whole reduction in one launch with the working matrix in LDS: per
-// column j the reflector from the current column (two block sums), p = tau M v
-// over the trailing rows (one wave per row), w = p - (tau/2)(p^T v) v, and the
-// eager rank-2 update M -= v w^T + w v^T of the trailing block.  fp32 storage
-// with fp64 arithmetic, as in the multi-launch reduction, whose outputs (d, e,
-// tau and the reflectors in rows of A) it reproduces.  Larger n take the
-// multi-launch reduction: one CU's LDS holds neither the square nor, from
-// about n = 200 on, beats the many-CU launches with the packed triangle.
+// Householder tridiagonalization of the trailing m x m block (m = n - j0 <=
+// kTriLdsMax) of one matrix per block, in one launch with the block in LDS:
+// per column the reflector from the current column (two block sums),
+// p = tau M v over the trailing rows (one wave per row),
+// w = p - (tau/2)(p^T v) v, and the eager rank-2 update M -= v w^T + w v^T.
+// fp32 storage with fp64 arithmetic, as in the multi-launch reduction, whose
+// outputs (d, e, tau and the reflectors in rows of A) it reproduces.  With
+// j0 > 0 the multi-launch reduction has done columns 0 .. j0 - 1 and left the
+// rank-2 update of column j0 - 1 pending (its reflector and p = tau A v in
+// `vec`): the block is loaded with that update applied.  Larger trailing
+// blocks stay with the multi-launch reduction: one CU's LDS holds neither the
+// square nor, from about m = 200 on, beats the many-CU launches with the
+// packed triangle.
 constexpr int kTriLdsMax = 192;
 constexpr int kTriThreads = 1024;
 
-__global__ void __launch_bounds__(kTriThreads) tri_small_kernel(float* A, int64_t strideA, int n, double* dd,
+__global__ void __launch_bounds__(kTriThreads) tri_small_kernel(float* A, int64_t strideA, int n, int j0,
+                                                                const double* vec, int64_t stride_vec, double* dd,
                                                                 double* ee, double* tau, int64_t stride_n) {
     extern __shared__ float M[];
     __shared__ double v[kTriLdsMax], w[kTriLdsMax], red[kTriThreads / 64];
     constexpr int NW = kTriThreads / 64;
     const int z = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int m = n - j0;
     float* Ag = A + (int64_t)z * strideA;
-    for (int q = tid; q < n * n; q += kTriThreads) M[q] = Ag[q];
+    if (j0 == 0) {
+        for (int q = tid; q < m * m; q += kTriThreads) M[q] = Ag[q];
+    } else {
+        const double* V = vec + (int64_t)z * stride_vec;
+        const double* vp = V + (int64_t)((j0 - 1) & 1) * n;
+        const double* P = V + 3 * (int64_t)n;
+        const double tp = tau[(int64_t)z * stride_n + j0 - 1];
+        double s = 0.0;
+        for (int i = j0 + tid; i < n; i += kTriThreads) s += P[i] * vp[i];
+        const double K = 0.5 * tp * block_sum_d<kTriThreads>(s, red);
+        for (int i = tid; i < m; i += kTriThreads) {
+            v[i] = vp[j0 + i];
+            w[i] = P[j0 + i] - K * vp[j0 + i];
+        }
+        __syncthreads();
+        for (int q = tid; q < m * m; q += kTriThreads) {
+            const int ii = q / m, kk = q - (q / m) * m;
+            M[q] = (float)((double)Ag[(int64_t)(j0 + ii) * n + j0 + kk] - v[ii] * w[kk] - w[ii] * v[kk]);
+        }
+    }
     __syncthreads();
-    for (int j = 0; j < n; ++j) {
-        const float* row = M + j * n;   // column j by symmetry
-        const double dj = row[j];
-        const double alpha = j + 1 < n ? (double)row[j + 1] : 0.0;
+    for (int jj = 0; jj < m; ++jj) {
+        const int j = j0 + jj;
+        const float* row = M + jj * m;   // column jj by symmetry
+        const double dj = row[jj];
+        const double alpha = jj + 1 < m ? (double)row[jj + 1] : 0.0;
         double sig = 0.0;
-        for (int i = j + 2 + tid; i < n; i += kTriThreads) {
+        for (int i = jj + 2 + tid; i < m; i += kTriThreads) {
             const double c = row[i];
             sig += c * c;
         }
@@ -194,30 +220,30 @@ __global__ void __launch_bounds__(kTriThreads) tri_small_kernel(float* A, int64_
             tau[(int64_t)z * stride_n + j] = t;
         }
         if (t == 0.0) continue;   // H_j = I (uniform across the block)
-        for (int i = j + 1 + tid; i < n; i += kTriThreads) {
-            const double vi = i == j + 1 ? 1.0 : (double)row[i] * scal;
+        for (int i = jj + 1 + tid; i < m; i += kTriThreads) {
+            const double vi = i == jj + 1 ? 1.0 : (double)row[i] * scal;
             v[i] = vi;
-            Ag[(int64_t)j * n + i] = (float)vi;
+            Ag[(int64_t)j * n + j0 + i] = (float)vi;
         }
         __syncthreads();
-        // p = t M v, rows i > j, one wave per row.
-        for (int i = j + 1 + wave; i < n; i += NW) {
-            const float* mi = M + i * n;
+        // p = t M v, rows i > jj, one wave per row.
+        for (int i = jj + 1 + wave; i < m; i += NW) {
+            const float* mi = M + i * m;
             double dot = 0.0;
-            for (int k = j + 1 + lane; k < n; k += 64) dot += (double)mi[k] * v[k];
+            for (int k = jj + 1 + lane; k < m; k += 64) dot += (double)mi[k] * v[k];
             dot = wave_sum_d(dot);
             if (lane == 0) w[i] = t * dot;
         }
         __syncthreads();
         double pv = 0.0;
-        for (int i = j + 1 + tid; i < n; i += kTriThreads) pv += w[i] * v[i];
+        for (int i = jj + 1 + tid; i < m; i += kTriThreads) pv += w[i] * v[i];
         const double K = 0.5 * t * block_sum_d<kTriThreads>(pv, red);
-        for (int i = j + 1 + tid; i < n; i += kTriThreads) w[i] -= K * v[i];
+        for (int i = jj + 1 + tid; i < m; i += kTriThreads) w[i] -= K * v[i];
         __syncthreads();
-        for (int i = j + 1 + wave; i < n; i += NW) {
-            float* mi = M + i * n;
+        for (int i = jj + 1 + wave; i < m; i += NW) {
+            float* mi = M + i * m;
             const double vi = v[i], wi = w[i];
-            for (int k = j + 1 + lane; k < n; k += 64) mi[k] = (float)((double)mi[k] - vi * w[k] - wi * v[k]);
+            for (int k = jj + 1 + lane; k < m; k += 64) mi[k] = (float)((double)mi[k] - vi * w[k] - wi * v[k]);
         }
         __syncthreads();
     }
@@ -550,26 +576,25 @@ hipError_t launch_gamma_sym(const float* g, int64_t ldg, int64_t strideg, int n,
 
 hipError_t launch_tridiagonalize(const TriWork& w, int n, int batch, hipStream_t s) {
     if (n < 1) return hipErrorInvalidValue;
-    if (n <= kTriLdsMax) {
-        hipLaunchKernelGGL(tri_small_kernel, dim3(batch), dim3(kTriThreads), (size_t)n * n * sizeof(float), s, w.A,
-                           (int64_t)n * n, n, w.d, w.e, w.tau, (int64_t)n);
-        return hipGetLastError();
-    }
-    for (int j = 0; j < n; ++j) {
+    // Columns 0 .. j0 - 1 two launches each, then the trailing block of at
+    // most kTriLdsMax in one launch.
+    const int j0 = std::max(0, n - kTriLdsMax);
+    for (int j = 0; j < j0; ++j) {
         hipLaunchKernelGGL(tri_house_kernel, dim3(batch), dim3(kHouseThreads), 0, s, w.A, (int64_t)n * n, n, j,
                            w.vec, 4 * (int64_t)n, w.d, w.e, w.tau, (int64_t)n);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        if (j + 1 < n) {
-            const int rows = n - j - 1;
-            hipLaunchKernelGGL(tri_update_kernel, dim3((rows + kRowWaves - 1) / kRowWaves, batch),
-                               dim3(kRowWaves * 64), 0, s, w.A, (int64_t)n * n, n, j, w.vec, 4 * (int64_t)n, w.tau,
-                               (int64_t)n);
-            e = hipGetLastError();
-            if (e != hipSuccess) return e;
-        }
+        const int rows = n - j - 1;
+        hipLaunchKernelGGL(tri_update_kernel, dim3((rows + kRowWaves - 1) / kRowWaves, batch),
+                           dim3(kRowWaves * 64), 0, s, w.A, (int64_t)n * n, n, j, w.vec, 4 * (int64_t)n, w.tau,
+                           (int64_t)n);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
-    return hipSuccess;
+    const int m = n - j0;
+    hipLaunchKernelGGL(tri_small_kernel, dim3(batch), dim3(kTriThreads), (size_t)m * m * sizeof(float), s, w.A,
+                       (int64_t)n * n, n, j0, w.vec, 4 * (int64_t)n, w.d, w.e, w.tau, (int64_t)n);
+    return hipGetLastError();
 }
 
 hipError_t launch_tri_eigvals(const TriWork& w, int n, int first, int nvals, double* out, int64_t stride_out,
