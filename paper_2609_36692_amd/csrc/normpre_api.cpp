@@ -351,6 +351,24 @@ Dims dims_of(int64_t m, int64_t n, int k, const normpre_hparams& hp) {
     return d;
 }
 
+// Newton-Schulz in Gram space (NormPre-G and the Muon reference step).  Every
+// iterate is X_k = Q_k X_0 with Q_k a polynomial in A_0 = X_0 X_0^T, and with
+// P_k = a I + b A_k + c A_k^2 the recurrences Q_{k+1} = P_k Q_k and
+// A_{k+1} = X_{k+1} X_{k+1}^T = P_k A_k P_k hold exactly (the P_k commute with
+// A_k).  The iterations then run on s x s matrices and X is formed only at
+// segment ends: X_3 = Q_3 X_0 (with a fresh Gram A_3, which bounds the fp16
+// error growth of the s x s recurrences) and T = X_5 = Q_5 X_3.  Nominal
+// FLOPs per matrix 8 s^2 L + 28 s^3 against 20 s^2 L + 10 s^3 for the plain
+// iteration; used for the quintic's five iterations when L >= 2 s.
+constexpr int kGnsIters = 5;
+constexpr int kGnsRestart = 3;
+
+bool gram_space_ns(int variant, const Dims& d, const normpre_hparams& hp) {
+    if (variant != NORMPRE_VARIANT_G && variant != NORMPRE_VARIANT_MUON) return false;
+    if (hp.ns_iters != kGnsIters) return false;
+    return std::max(d.m, d.n) >= 2 * std::min(d.m, d.n);
+}
+
 // Length chunk of the fp64 Gram: >= 256 for parallel blocks and at most
 // kGramChunks chunks (the consumers always sum kGramChunks slots).
 int gram_chunk_len(int64_t len) {
@@ -383,6 +401,7 @@ struct Item {
     int pool = -1;        // pool of its small matrices
     int pool_off = 0;     // its first matrix inside the pool
     TileCfg ccfg = TileCfg::Big;   // tile of its Newton-Schulz combines
+    bool gns = false;     // Newton-Schulz iterations carried in Gram space
 };
 
 // Small matrices shared by the items of a round that have the same width:
@@ -395,6 +414,12 @@ struct Pool {
     int ell = 0, ellp = 0, top = 0;
     half_t* amat = nullptr;
     half_t* bmat = nullptr;
+    // Gram-space Newton-Schulz: its items hold pool slots [0, gns_count);
+    // Q (double buffered, qcur the current one) and the product R.
+    int gns_count = 0;
+    half_t* qmat[2] = {nullptr, nullptr};
+    half_t* rmat = nullptr;
+    int qcur = 0;
     double* gpart = nullptr;
     double* chol = nullptr;
     float* rinv = nullptr;
@@ -458,6 +483,12 @@ void carve_pool(Arena& ar, Pool& p, int variant) {
     if (variant == NORMPRE_VARIANT_G || variant == NORMPRE_VARIANT_MUON) {
         p.amat = ar.take<half_t>(c * p.sp * p.sp);
         p.bmat = ar.take<half_t>(c * p.sp * p.sp);
+        if (p.gns_count > 0) {
+            const int64_t gc = p.gns_count;
+            p.qmat[0] = ar.take<half_t>(gc * p.sp * p.sp);
+            p.qmat[1] = ar.take<half_t>(gc * p.sp * p.sp);
+            p.rmat = ar.take<half_t>(gc * p.sp * p.sp);
+        }
     } else if (variant == NORMPRE_VARIANT_L) {
         const int64_t lp = p.ellp;
         p.gpart = ar.take<double>(c * kGramChunks * lp * lp);
@@ -501,9 +532,17 @@ std::vector<Pool> make_pools(std::vector<Item>& items, int variant) {
             pi = (int)pools.size() - 1;
         }
         it.pool = pi;
-        it.pool_off = pools[pi].count;
-        pools[pi].count += it.count;
     }
+    // Gram-space items take the first slots of their pool, so their s x s
+    // matrices form one contiguous range (one launch per Gram-space product).
+    for (int pass = 0; pass < 2; ++pass)
+        for (Item& it : items) {
+            if (it.gns != (pass == 0)) continue;
+            Pool& p = pools[it.pool];
+            it.pool_off = p.count;
+            p.count += it.count;
+            if (it.gns) p.gns_count += it.count;
+        }
     return pools;
 }
 
@@ -746,7 +785,8 @@ int gram_launches(const StepCtx& sc, const std::vector<Item>& items, const std::
         for (int tall = 0; tall < 2; ++tall) {
             std::vector<const Item*> its;
             for (const Item& it : items)
-                if (it.pool == (int)pi && (int)it.d.tall == tall) {
+                if (it.pool == (int)pi && (int)it.d.tall == tall &&
+                    (!it.gns || iter == 0 || iter == kGnsRestart)) {
                     its.push_back(&it);
                     if ((int)its.size() == kMaxGramGroups) {
                         if (int rc = gram_pool_launch(sc, its, pools[pi], iter, first_it)) return rc;
@@ -777,18 +817,21 @@ int poly_launch(const StepCtx& sc, const Pool& pl, double nominal_flops) {
     return NORMPRE_OK;
 }
 
-int combine_launch(const StepCtx& sc, const Item& it, const Pool& pl, half_t* x, half_t* xn, bool first_it,
-                   bool last_it) {
+// X <- cs X + S X (wide) or X <- cs X + X S (tall) with S the item's slots of
+// the pool's s x s matrices `smat` (B for the plain iteration, Q at a
+// Gram-space segment end with cs = 0).
+int combine_launch(const StepCtx& sc, const Item& it, const half_t* smat, half_t* x, half_t* xn, bool first_it,
+                   bool last_it, float cs) {
     const Dims& d = it.d;
     const int count = it.count;
     const int64_t mn = d.mp * d.np_, ss = d.sp * d.sp;
     const double s_ = (double)std::min(d.m, d.n), l_ = (double)std::max(d.m, d.n);
-    half_t* bmat = pl.bmat + (int64_t)it.pool_off * ss;
+    const half_t* bmat = smat + (int64_t)it.pool_off * ss;
     EpiAffine e{};
     e.out = xn; e.ld_out = d.np_; e.stride_out = mn;
-    e.src = x; e.ld_src = d.np_; e.stride_src = mn;
+    e.src = cs != 0.f ? x : nullptr; e.ld_src = d.np_; e.stride_src = mn;
     e.mul = first_it ? it.w.scale : nullptr; e.mul_pow = first_it ? 1 : 0;
-    e.ca = 1.f; e.cs = sc.hp->ns_coeffs[0];
+    e.ca = 1.f; e.cs = cs;
     const TileCfg cfg = it.ccfg;
     e.sumsq = last_it ? it.w.sumsq : nullptr;
     e.tiles_per_mat = combine_tiles(d, cfg);
@@ -818,7 +861,7 @@ std::vector<std::vector<Item*>> wide_combine_chunks(std::vector<Item>& items, si
     for (size_t pi = 0; pi < npools; ++pi) {
         std::vector<Item*> cur;
         for (Item& it : items) {
-            if (it.pool != (int)pi || it.d.tall) continue;
+            if (it.pool != (int)pi || it.d.tall || it.gns) continue;
             cur.push_back(&it);
             if ((int)cur.size() == kMaxItems) {
                 chunks.push_back(cur);
@@ -873,6 +916,63 @@ int combine_grouped_launch(const StepCtx& sc, const std::vector<Item*>& ch, cons
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_COMBINE, flops, bytes,
                  [&] { return launch_gemm_combine_grouped(cfg, (int)sp, g, e, sc.s); }),
            "ns combine");
+    return NORMPRE_OK;
+}
+
+// out = S R + cs R for the pool's Gram-space slots (symmetric results: S and R
+// are polynomials in the same A_0, so only upper tiles are computed).
+int gns_product(const StepCtx& sc, const Pool& pl, const half_t* smat, const half_t* r, half_t* out, float cs,
+                double flops) {
+    const int64_t sp = pl.sp, ss = sp * sp;
+    Operand A{smat, sp, ss}, B{r, sp, ss};
+    GemmShape sh{(int)sp, (int)sp, (int)sp, 1, (int)sp, 1};
+    EpiAffine e{};
+    e.out = out; e.ld_out = sp; e.stride_out = ss;
+    e.src = r; e.ld_src = sp; e.stride_src = ss;
+    e.ca = 1.f; e.cs = cs;
+    const TileCfg cfg = ns_cfg(sp, sp, true, pl.gns_count);
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_POLY, flops, 6.0 * flops / (double)sp,
+                 [&] { return launch_gemm_affine(cfg, 0, A, B, sh, pl.gns_count, e, sc.s); }),
+           "ns gram-space product");
+    return NORMPRE_OK;
+}
+
+// One Gram-space iteration of a pool's Gram-space items, after the pool's
+// B_k = b A_k + c A_k^2: Q_{k+1} = a Q_k + B_k Q_k (Q = B + a I at a segment
+// start), then either A_{k+1} = P_k (P_k A_k) or, at a segment end, the
+// items' X = Q X_base (X_0 in psi -> xb, then X_3 in xb -> T in psi).
+int gns_iteration(const StepCtx& sc, const std::vector<Item>& items, Pool& pl, int pi, int iter, int q,
+                  bool fold_scale) {
+    const float a = sc.hp->ns_coeffs[0];
+    const bool seg_start = iter == 0 || iter == kGnsRestart;
+    const bool seg_end = iter == kGnsRestart - 1 || iter == q - 1;
+    double flops = 0.0;
+    for (const Item& it : items)
+        if (it.pool == pi && it.gns) {
+            const double s_ = (double)std::min(it.d.m, it.d.n);
+            flops += 2.0 * s_ * s_ * s_ * it.count;
+        }
+    if (seg_start) {
+        pl.qcur = 0;
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 4.0 * (double)pl.gns_count * pl.sp * pl.sp,
+                     [&] { return launch_add_identity(pl.bmat, pl.qmat[0], pl.sp, pl.gns_count, a, sc.s); }),
+               "ns gram-space identity");
+    } else {
+        if (int rc = gns_product(sc, pl, pl.bmat, pl.qmat[pl.qcur], pl.qmat[1 - pl.qcur], a, flops)) return rc;
+        pl.qcur = 1 - pl.qcur;
+    }
+    if (!seg_end) {
+        if (int rc = gns_product(sc, pl, pl.bmat, pl.amat, pl.rmat, a, flops)) return rc;
+        return gns_product(sc, pl, pl.bmat, pl.rmat, pl.amat, a, flops);
+    }
+    const bool first_seg = iter < kGnsRestart;
+    for (const Item& it : items) {
+        if (it.pool != pi || !it.gns) continue;
+        half_t* x = first_seg ? it.w.psi : it.w.xb;
+        half_t* xn = first_seg ? it.w.xb : it.w.psi;
+        if (int rc = combine_launch(sc, it, pl.qmat[pl.qcur], x, xn, first_seg && fold_scale, iter == q - 1, 0.f))
+            return rc;
+    }
     return NORMPRE_OK;
 }
 
@@ -960,7 +1060,7 @@ int run_round_g(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& 
     // Combine tiles: the wide items of a pool share launches; tall ones run
     // per item.
     for (Item& it : items)
-        if (it.d.tall) it.ccfg = ns_cfg(it.d.mp, it.d.np_, false, it.count);
+        if (it.d.tall || it.gns) it.ccfg = ns_cfg(it.d.mp, it.d.np_, false, it.count);
     const auto wide = wide_combine_chunks(items, pools.size());
     for (int iter = 0; iter < q; ++iter) {
         const bool first_it = iter == 0 && fold_scale, last_it = iter == q - 1;
@@ -981,20 +1081,26 @@ int run_round_g(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& 
             half_t* x = (iter & 1) ? it0.w.xb : it0.w.psi;
             half_t* xn = (iter & 1) ? it0.w.psi : it0.w.xb;
             // A lone item takes the plain launch (no table to walk).
-            int rc = ch.size() == 1 ? combine_launch(sc, it0, pools[it0.pool], x, xn, first_it, last_it)
+            int rc = ch.size() == 1 ? combine_launch(sc, it0, pools[it0.pool].bmat, x, xn, first_it, last_it,
+                                                     sc.hp->ns_coeffs[0])
                                     : combine_grouped_launch(sc, ch, pools[it0.pool], iter, first_it, last_it);
             if (rc) return rc;
         }
         for (const Item& it : items) {
-            if (!it.d.tall) continue;
+            if (!it.d.tall || it.gns) continue;
             half_t* x = (iter & 1) ? it.w.xb : it.w.psi;
             half_t* xn = (iter & 1) ? it.w.psi : it.w.xb;
-            int rc = combine_launch(sc, it, pools[it.pool], x, xn, first_it, last_it);
+            int rc = combine_launch(sc, it, pools[it.pool].bmat, x, xn, first_it, last_it, sc.hp->ns_coeffs[0]);
             if (rc) return rc;
+        }
+        for (size_t pi = 0; pi < pools.size(); ++pi) {
+            if (pools[pi].gns_count == 0) continue;
+            if (int rc = gns_iteration(sc, items, pools[pi], (int)pi, iter, q, fold_scale)) return rc;
         }
     }
     for (const Item& it : items) {
-        const half_t* t = (q & 1) ? it.w.xb : it.w.psi;
+        // Gram-space items end with T in psi (their second segment writes it).
+        const half_t* t = it.gns ? it.w.psi : (q & 1) ? it.w.xb : it.w.psi;
         int rc = g_update_launch(sc, it, t, dbg);
         if (rc) return rc;
     }
@@ -1684,6 +1790,7 @@ int normpre_step(normpre_ctx* ctx, int variant, int num_mats, float* const* para
         one.g = (int)g;
         one.count = 1;
         one.d = d;
+        one.gns = gram_space_ns(variant, d, *hp);
         const size_t per = round_bytes({one}, variant, source_x);
         const int b = (int)std::max<size_t>(1, std::min<size_t>((size_t)cnt, kGroupBudget / std::max<size_t>(per, 1)));
         for (int first = 0; first < cnt; first += b) {
@@ -1692,6 +1799,7 @@ int normpre_step(normpre_ctx* ctx, int variant, int num_mats, float* const* para
             it.first = first;
             it.count = std::min(b, cnt - first);
             it.d = d;
+            it.gns = one.gns;
             all.push_back(it);
         }
     }

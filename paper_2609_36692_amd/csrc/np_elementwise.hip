@@ -228,6 +228,7 @@ __global__ void __launch_bounds__(256) normalize_rows_wave_kernel(NormArgs a) {
 // row when VW = 4).  Pass 1 updates M and writes fp64 partial column sums;
 // pass 2 combines the partials in a fixed order and writes Psi.
 constexpr int kColThreads = 256;
+constexpr int kColBatch = 4;   // rows whose loads a stats-pass thread issues together
 
 template <int VW>
 __global__ void __launch_bounds__(kColThreads) normalize_cols_stats(NormArgs a, double* partials, int row_chunk) {
@@ -242,7 +243,38 @@ __global__ void __launch_bounds__(kColThreads) normalize_cols_stats(NormArgs a, 
         float* W = a.ptrs.w[z];
         float* M = a.ptrs.m[z];
         const float* G = a.ptrs.g[z];
-        for (int i = r0 + ry; i < r1; i += 4) {
+        int i = r0 + ry;
+        if constexpr (VW == 4) {
+            // kColBatch rows per step: every load of the batch is issued before
+            // the first M store, so a wave keeps 12 16-byte loads per lane in
+            // flight.  Rows are still accumulated in ascending order.
+            for (; i + 4 * (kColBatch - 1) < r1; i += 4 * kColBatch) {
+                float4 mp[kColBatch], g[kColBatch], w[kColBatch];
+#pragma unroll
+                for (int u = 0; u < kColBatch; ++u) {
+                    const int64_t o = (int64_t)(i + 4 * u) * a.cols + col0;
+                    mp[u] = *reinterpret_cast<const float4*>(M + o);
+                    g[u] = *reinterpret_cast<const float4*>(G + o);
+                    w[u] = *reinterpret_cast<const float4*>(W + o);
+                }
+#pragma unroll
+                for (int u = 0; u < kColBatch; ++u) {
+                    const int64_t o = (int64_t)(i + 4 * u) * a.cols + col0;
+                    const float m[4] = {fmaf(a.mu, mp[u].x, g[u].x), fmaf(a.mu, mp[u].y, g[u].y),
+                                        fmaf(a.mu, mp[u].z, g[u].z), fmaf(a.mu, mp[u].w, g[u].w)};
+                    *reinterpret_cast<float4*>(M + o) = make_float4(m[0], m[1], m[2], m[3]);
+                    const float wv[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const double md = m[e], wd = wv[e];
+                        smm[e] = fma(md, md, smm[e]);
+                        smw[e] = fma(md, wd, smw[e]);
+                        sww[e] = fma(wd, wd, sww[e]);
+                    }
+                }
+            }
+        }
+        for (; i < r1; i += 4) {
             const int64_t o = (int64_t)i * a.cols + col0;
             if constexpr (VW == 4) {
                 const float4 mp = *reinterpret_cast<const float4*>(M + o);
@@ -504,6 +536,24 @@ __global__ void __launch_bounds__(256) sum_partials_kernel(const float* in, int 
     if (threadIdx.x == 0) out[z] = red[0] + red[1] + red[2] + red[3];
 }
 
+// Q = B + a I for a batch of sp x sp fp16 matrices (8 halves per thread
+// and grid-stride step; sp is a multiple of 8, so a chunk never straddles
+// two rows).
+__global__ void __launch_bounds__(256) add_identity_kernel(const uint4* b, uint4* q, int64_t sp, int64_t n8,
+                                                           float a) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n8; i += (int64_t)gridDim.x * blockDim.x) {
+        uint4 v = b[i];
+        const int64_t e = (i * 8) % (sp * sp);           // element index inside its matrix
+        const int64_t row = e / sp, c0 = e - row * sp;
+        if (row >= c0 && row < c0 + 8) {
+            half_t* h = reinterpret_cast<half_t*>(&v);
+            const int j = (int)(row - c0);
+            h[j] = (half_t)((float)h[j] + a);
+        }
+        q[i] = v;
+    }
+}
+
 __global__ void fill_zero_kernel(uint4* p, int64_t n16) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (int64_t)gridDim.x * blockDim.x)
         p[i] = make_uint4(0, 0, 0, 0);
@@ -746,6 +796,17 @@ hipError_t launch_g_update(const GUpdateArgs& a, int batch, hipStream_t s) {
 
 hipError_t launch_sum_partials(const float* in, int n, float* out, int batch, hipStream_t s) {
     hipLaunchKernelGGL(sum_partials_kernel, dim3(batch), dim3(256), 0, s, in, n, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_add_identity(const half_t* b, half_t* q, int64_t sp, int count, float a, hipStream_t s) {
+    if (count < 1 || sp < 8 || sp % 8 || b == q || (reinterpret_cast<uintptr_t>(b) & 15) ||
+        (reinterpret_cast<uintptr_t>(q) & 15))
+        return hipErrorInvalidValue;
+    const int64_t n8 = (int64_t)count * sp * sp / 8;
+    const unsigned blocks = (unsigned)std::min<int64_t>((n8 + 255) / 256, 4096);
+    hipLaunchKernelGGL(add_identity_kernel, dim3(blocks), dim3(256), 0, s, reinterpret_cast<const uint4*>(b),
+                       reinterpret_cast<uint4*>(q), sp, n8, a);
     return hipGetLastError();
 }
 
