@@ -800,19 +800,21 @@ int gram_launches(const StepCtx& sc, const std::vector<Item>& items, const std::
     return NORMPRE_OK;
 }
 
-int poly_launch(const StepCtx& sc, const Pool& pl, double nominal_flops) {
-    // B = b A + c A^2 for every matrix of the pool in one launch.
+// B = b A + c A^2 for the pool's slots [first, first + cnt) in one launch,
+// written to `out` (slot `first` at out[0]).
+int poly_launch(const StepCtx& sc, const Pool& pl, int first, int cnt, half_t* out, double nominal_flops) {
     const int64_t sp = pl.sp, ss = sp * sp;
-    Operand A{pl.amat, sp, ss}, B{pl.amat, sp, ss};
+    const half_t* a0 = pl.amat + (int64_t)first * ss;
+    Operand A{a0, sp, ss}, B{a0, sp, ss};
     GemmShape sh{(int)sp, (int)sp, (int)sp, 1, (int)sp, 1};
     EpiAffine e{};
-    e.out = pl.bmat; e.ld_out = sp; e.stride_out = ss;
-    e.src = pl.amat; e.ld_src = sp; e.stride_src = ss;
+    e.out = out; e.ld_out = sp; e.stride_out = ss;
+    e.src = a0; e.ld_src = sp; e.stride_src = ss;
     e.ca = sc.hp->ns_coeffs[2]; e.cs = sc.hp->ns_coeffs[1];
-    const TileCfg cfg = ns_cfg(sp, sp, true, pl.count);
+    const TileCfg cfg = ns_cfg(sp, sp, true, cnt);
     // Nominal FLOPs use the real s of each matrix (padding excluded).
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_POLY, nominal_flops, 6.0 * nominal_flops / (double)sp,
-                 [&] { return launch_gemm_affine(cfg, 0, A, B, sh, pl.count, e, sc.s); }),
+                 [&] { return launch_gemm_affine(cfg, 0, A, B, sh, cnt, e, sc.s); }),
            "ns poly");
     return NORMPRE_OK;
 }
@@ -938,9 +940,11 @@ int gns_product(const StepCtx& sc, const Pool& pl, const half_t* smat, const hal
 }
 
 // One Gram-space iteration of a pool's Gram-space items, after the pool's
-// B_k = b A_k + c A_k^2: Q_{k+1} = a Q_k + B_k Q_k (Q = B + a I at a segment
-// start), then either A_{k+1} = P_k (P_k A_k) or, at a segment end, the
-// items' X = Q X_base (X_0 in psi -> xb, then X_3 in xb -> T in psi).
+// B_k = b A_k + c A_k^2 (written into Q's first buffer at a segment start,
+// else into the pool's B): Q_{k+1} = P_k at a segment start (a I added in
+// place), else a Q_k + B_k Q_k; then either A_{k+1} = P_k (P_k A_k) or, at a
+// segment end, the items' X = Q X_base (X_0 in psi -> xb, then X_3 in xb ->
+// T in psi).
 int gns_iteration(const StepCtx& sc, const std::vector<Item>& items, Pool& pl, int pi, int iter, int q,
                   bool fold_scale) {
     const float a = sc.hp->ns_coeffs[0];
@@ -954,16 +958,19 @@ int gns_iteration(const StepCtx& sc, const std::vector<Item>& items, Pool& pl, i
         }
     if (seg_start) {
         pl.qcur = 0;
-        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 4.0 * (double)pl.gns_count * pl.sp * pl.sp,
-                     [&] { return launch_add_identity(pl.bmat, pl.qmat[0], pl.sp, pl.gns_count, a, sc.s); }),
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 4.0 * (double)pl.gns_count * pl.sp,
+                     [&] { return launch_add_diag(pl.qmat[0], pl.sp, pl.gns_count, a, sc.s); }),
                "ns gram-space identity");
     } else {
         if (int rc = gns_product(sc, pl, pl.bmat, pl.qmat[pl.qcur], pl.qmat[1 - pl.qcur], a, flops)) return rc;
         pl.qcur = 1 - pl.qcur;
     }
     if (!seg_end) {
-        if (int rc = gns_product(sc, pl, pl.bmat, pl.amat, pl.rmat, a, flops)) return rc;
-        return gns_product(sc, pl, pl.bmat, pl.rmat, pl.amat, a, flops);
+        // P_k is Q's first buffer at a segment start (no src term), else B_k + a I.
+        const half_t* left = seg_start ? pl.qmat[0] : pl.bmat;
+        const float cs = seg_start ? 0.f : a;
+        if (int rc = gns_product(sc, pl, left, pl.amat, pl.rmat, cs, flops)) return rc;
+        return gns_product(sc, pl, left, pl.rmat, pl.amat, cs, flops);
     }
     const bool first_seg = iter < kGnsRestart;
     for (const Item& it : items) {
@@ -1067,13 +1074,21 @@ int run_round_g(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& 
         int rc = gram_launches(sc, items, pools, iter, first_it);
         if (rc) return rc;
         for (size_t pi = 0; pi < pools.size(); ++pi) {
-            double flops = 0.0;
+            Pool& pl = pools[pi];
+            double fg = 0.0, fs = 0.0;
             for (const Item& it : items)
                 if (it.pool == (int)pi) {
                     const double s_ = (double)std::min(it.d.m, it.d.n);
-                    flops += 2.0 * s_ * s_ * s_ * it.count;
+                    (it.gns ? fg : fs) += 2.0 * s_ * s_ * s_ * it.count;
                 }
-            int rc = poly_launch(sc, pools[pi], flops);
+            // At a Gram-space segment start the Gram-space slots' B goes
+            // straight into Q's first buffer (Q_{k+1} = B_k + a I).
+            const bool split = pl.gns_count > 0 && (iter == 0 || iter == kGnsRestart);
+            int rc = split ? poly_launch(sc, pl, 0, pl.gns_count, pl.qmat[0], fg)
+                           : poly_launch(sc, pl, 0, pl.count, pl.bmat, fg + fs);
+            if (!rc && split && pl.count > pl.gns_count)
+                rc = poly_launch(sc, pl, pl.gns_count, pl.count - pl.gns_count,
+                                 pl.bmat + (int64_t)pl.gns_count * pl.sp * pl.sp, fs);
             if (rc) return rc;
         }
         for (const auto& ch : wide) {

@@ -536,22 +536,14 @@ __global__ void __launch_bounds__(256) sum_partials_kernel(const float* in, int 
     if (threadIdx.x == 0) out[z] = red[0] + red[1] + red[2] + red[3];
 }
 
-// Q = B + a I for a batch of sp x sp fp16 matrices (8 halves per thread
-// and grid-stride step; sp is a multiple of 8, so a chunk never straddles
-// two rows).
-__global__ void __launch_bounds__(256) add_identity_kernel(const uint4* b, uint4* q, int64_t sp, int64_t n8,
-                                                           float a) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n8; i += (int64_t)gridDim.x * blockDim.x) {
-        uint4 v = b[i];
-        const int64_t e = (i * 8) % (sp * sp);           // element index inside its matrix
-        const int64_t row = e / sp, c0 = e - row * sp;
-        if (row >= c0 && row < c0 + 8) {
-            half_t* h = reinterpret_cast<half_t*>(&v);
-            const int j = (int)(row - c0);
-            h[j] = (half_t)((float)h[j] + a);
-        }
-        q[i] = v;
-    }
+// Q <- Q + a I in place for a batch of sp x sp fp16 matrices: one thread per
+// diagonal entry.
+__global__ void __launch_bounds__(256) add_diag_kernel(half_t* q, int64_t sp, int64_t n, float a) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const int64_t z = i / sp, d = i - z * sp;
+    half_t* e = q + z * sp * sp + d * (sp + 1);
+    *e = (half_t)((float)*e + a);
 }
 
 __global__ void fill_zero_kernel(uint4* p, int64_t n16) {
@@ -799,14 +791,10 @@ hipError_t launch_sum_partials(const float* in, int n, float* out, int batch, hi
     return hipGetLastError();
 }
 
-hipError_t launch_add_identity(const half_t* b, half_t* q, int64_t sp, int count, float a, hipStream_t s) {
-    if (count < 1 || sp < 8 || sp % 8 || b == q || (reinterpret_cast<uintptr_t>(b) & 15) ||
-        (reinterpret_cast<uintptr_t>(q) & 15))
-        return hipErrorInvalidValue;
-    const int64_t n8 = (int64_t)count * sp * sp / 8;
-    const unsigned blocks = (unsigned)std::min<int64_t>((n8 + 255) / 256, 4096);
-    hipLaunchKernelGGL(add_identity_kernel, dim3(blocks), dim3(256), 0, s, reinterpret_cast<const uint4*>(b),
-                       reinterpret_cast<uint4*>(q), sp, n8, a);
+hipError_t launch_add_diag(half_t* q, int64_t sp, int count, float a, hipStream_t s) {
+    if (count < 1 || sp < 1) return hipErrorInvalidValue;
+    const int64_t n = (int64_t)count * sp;
+    hipLaunchKernelGGL(add_diag_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, q, sp, n, a);
     return hipGetLastError();
 }
 

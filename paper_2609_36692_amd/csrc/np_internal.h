@@ -337,9 +337,8 @@ struct EigArgs {
 hipError_t launch_eig_select(const EigArgs& a, int batch, hipStream_t s);
 
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t s);
-// Q = B + a I for `count` contiguous sp x sp fp16 matrices (B and Q distinct,
-// 16-byte aligned; sp a multiple of 8).
-hipError_t launch_add_identity(const half_t* b, half_t* q, int64_t sp, int count, float a, hipStream_t s);
+// Q <- Q + a I in place for `count` contiguous sp x sp fp16 matrices.
+hipError_t launch_add_diag(half_t* q, int64_t sp, int count, float a, hipStream_t s);
 
 // ------------------------------------------ dense symmetric eigensolver ---
 // Workspace of one launch of matrices of equal order n (per matrix: A n x n
