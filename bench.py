@@ -201,7 +201,8 @@ def roofline_of(cls, bound):
         peak, unit = PEAK_HBM_GBS, "GB/s"
     return {"bound": bound, "achieved": round(ach, 2), "peak": peak, "unit": unit,
             "frac": round(ach / peak, 4), "traffic": None,
-            "launches": cls["launches"], "avg_launch_us": round(1e3 * cls["ms"] / cls["launches"], 2)}
+            "launches": cls["launches"], "avg_launch_us": round(1e3 * cls["ms"] / cls["launches"], 2),
+            "algorithmic_bytes_per_launch": round(cls["bytes"] / cls["launches"])}
 
 
 def merge_classes(classes, names):
@@ -313,7 +314,7 @@ def main():
         if v in ("G", "MUON"):
             ns = merge_classes(cls, ["ns_gram", "ns_poly", "ns_combine"])
             roof = roofline_of(ns, "mfma")
-            roof["kernel"] = "Newton-Schulz GEMMs (gram + poly + combine, fp16 MFMA)"
+            roof["kernel"] = "Newton-Schulz GEMMs (gram + poly + Gram-space products + combine, fp16 MFMA)"
         elif v == "NORM":
             roof = roofline_of(cls["normalize"], "hbm")
             roof["kernel"] = "momentum + tangent + normalization"

@@ -812,8 +812,9 @@ int poly_launch(const StepCtx& sc, const Pool& pl, int first, int cnt, half_t* o
     e.src = a0; e.ld_src = sp; e.stride_src = ss;
     e.ca = sc.hp->ns_coeffs[2]; e.cs = sc.hp->ns_coeffs[1];
     const TileCfg cfg = ns_cfg(sp, sp, true, cnt);
-    // Nominal FLOPs use the real s of each matrix (padding excluded).
-    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_POLY, nominal_flops, 6.0 * nominal_flops / (double)sp,
+    // Nominal FLOPs use the real s of each matrix (padding excluded); bytes
+    // are A read once and B written once (4 s^2 per matrix).
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_POLY, nominal_flops, 2.0 * nominal_flops / (double)sp,
                  [&] { return launch_gemm_affine(cfg, 0, A, B, sh, cnt, e, sc.s); }),
            "ns poly");
     return NORMPRE_OK;
@@ -933,7 +934,8 @@ int gns_product(const StepCtx& sc, const Pool& pl, const half_t* smat, const hal
     e.src = r; e.ld_src = sp; e.stride_src = ss;
     e.ca = 1.f; e.cs = cs;
     const TileCfg cfg = ns_cfg(sp, sp, true, pl.gns_count);
-    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_POLY, flops, 6.0 * flops / (double)sp,
+    // Bytes: S and R read once, the result written once (6 s^2 per matrix).
+    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_POLY, flops, 3.0 * flops / (double)sp,
                  [&] { return launch_gemm_affine(cfg, 0, A, B, sh, pl.gns_count, e, sc.s); }),
            "ns gram-space product");
     return NORMPRE_OK;
