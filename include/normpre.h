@@ -278,8 +278,11 @@ int normpre_sketch_omega(uint64_t seed, int64_t step, int32_t matrix_id,
 /* Kernel classes reported by normpre_kernel_stats(). */
 #define NORMPRE_KCLASS_NORMALIZE   0  /* momentum + tangent + row/col normalization */
 #define NORMPRE_KCLASS_NS_GRAM     1  /* Newton-Schulz A = X X^T                     */
-#define NORMPRE_KCLASS_NS_POLY     2  /* Newton-Schulz B = bA + cA^2                 */
-#define NORMPRE_KCLASS_NS_COMBINE  3  /* Newton-Schulz X <- aX + BX                  */
+#define NORMPRE_KCLASS_NS_POLY     2  /* Newton-Schulz B = bA + cA^2, and the s x s  */
+                                      /* products of the Gram-space schedule        */
+                                      /* (Q <- P Q, A <- P A P; matrices with L >= 2s) */
+#define NORMPRE_KCLASS_NS_COMBINE  3  /* Newton-Schulz X <- aX + BX (X = Q X_base at  */
+                                      /* the Gram-space segment ends)               */
 #define NORMPRE_KCLASS_G_UPDATE    4  /* RMS scaling + weight update (NormPre-G)     */
 #define NORMPRE_KCLASS_SK_STREAM   5  /* sketch products streaming Psi               */
 #define NORMPRE_KCLASS_SK_SMALL    6  /* Omega, reductions, CholQR, eigensolver      */
