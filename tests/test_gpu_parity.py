@@ -133,6 +133,25 @@ def test_g_step_parity(ctx, shape, t):
     assert math.isclose(np.linalg.norm(res["u"]), 0.2 * math.sqrt(shape[0] * shape[1]), rel_tol=1e-3)
 
 
+# Both sides of the switch to the Gram-space Newton-Schulz schedule (L >= 2s),
+# wide and tall, and a ragged s whose padding (513 -> 768) the s x s
+# recurrences carry.
+GNS_SHAPES = [(200, 400), (201, 400), (400, 200), (400, 201), (513, 1100)]
+
+
+@pytest.mark.parametrize("shape", GNS_SHAPES)
+@pytest.mark.parametrize("t", [0, 1])
+def test_g_step_parity_gram_space_switch(ctx, shape, t):
+    _say(f"G step (Gram-space switch) shape={shape} t={t}")
+    mat = _inputs(shape, seed=5)
+    res = run_step(ctx, "G", [mat], t)[0]
+    ref = oracle(mat, "G", t)
+    err = O.relative_fro(res["u"], ref["update"])
+    _say(f"   update err {err:.3e}")
+    assert err < TOL_G
+    assert math.isclose(np.linalg.norm(res["u"]), 0.2 * math.sqrt(shape[0] * shape[1]), rel_tol=1e-3)
+
+
 # ----------------------------------------------------------- NormPre-L
 L_CASES = [((256, 256), 16), ((257, 513), 8), ((300, 1), 4), ((3, 3), 2), ((768, 2304), 32),
            ((3072, 768), 32), ((640, 700), 64), ((40, 500), 64),
