@@ -1066,8 +1066,8 @@ int run_round_g(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& 
     // into the first iteration's epilogues.
     const bool fold_scale = sc.variant == NORMPRE_VARIANT_G;
     const int q = sc.variant == NORMPRE_VARIANT_NORMALIZE_ONLY ? 0 : sc.hp->ns_iters;
-    // Combine tiles: the wide items of a pool share launches; tall ones run
-    // per item.
+    // Combine tiles: the plain-iteration wide items of a pool share launches;
+    // tall and Gram-space items run per item.
     for (Item& it : items)
         if (it.d.tall || it.gns) it.ccfg = ns_cfg(it.d.mp, it.d.np_, false, it.count);
     const auto wide = wide_combine_chunks(items, pools.size());
