@@ -7,11 +7,14 @@ table or helper with the HIP library; the only thing both sides consume is
 the seeded input data handed to them by the callers.
 
 Everything here is written out from the paper "Normalize-Then-Precondition"
-(arXiv 2609.36692) in the order and notation of its Algorithm 1 (the NormPre
-optimizer, Sec. 3.1) and Algorithm 2 (randomized interaction sketch, App. B).
-Library routines used as single steps: ``@`` (matmul), ``np.linalg.qr``
-(the ``qr`` step of Alg. 2), ``np.linalg.eigh`` (the eigen-steps of Alg. 2
-and of the exact variant in App. B).
+(arXiv 2609.36692): the step of Algorithm 1 (the NormPre optimizer, Sec. 3.1)
+in its order, and the randomized interaction sketch of Algorithm 2 (App. B)
+from what it computes: an orthonormal basis of the power-iterated sketch of
+range(Psi), the Rayleigh-Ritz pairs of Gamma = Psi Psi^T on it, and the
+selection of the over-amplified modes.  Library routines used as single
+steps: ``@`` (matmul), ``np.linalg.qr`` (an orthonormal basis),
+``np.linalg.svd`` (the eigenpairs of Gamma_Q = B B^T from the singular pairs
+of B) and ``np.linalg.eigh`` (the exact variant of App. B).
 
 Conventions the paper leaves open (each one is also listed among the
 readings in the design notes):
@@ -265,38 +268,65 @@ def _desc_order(vals: np.ndarray) -> np.ndarray:
     return np.argsort(-vals, kind="stable")
 
 
+def candidate_subspace(psi: np.ndarray, omega: np.ndarray, power_iters: int) -> np.ndarray:
+    """Orthonormal basis Q (a x l) of the candidate subspace of Alg. 2:
+    range((Psi Psi^T)^p Psi Omega), the Gaussian sketch of the column space of
+    Psi sharpened by p power iterations (each one multiplies by Psi^T, then by
+    Psi, so the leading directions of Gamma = Psi Psi^T gain weight lambda per
+    pass).  ``np.linalg.qr`` supplies the orthonormal basis."""
+    y = psi @ omega
+    for _ in range(power_iters):
+        y = psi @ (psi.T @ y)
+    basis, _ = np.linalg.qr(y, mode="reduced")
+    return basis
+
+
+def rayleigh_ritz(psi: np.ndarray, basis: np.ndarray):
+    """Ritz pairs of Gamma = Psi Psi^T on range(Q) (Alg. 2, Ritz pairs; App. B):
+    with B = Q^T Psi the projected matrix is Gamma_Q = B B^T, whose eigenpairs
+    are the squared singular values of B and its left singular vectors.
+    Returns (B, Gamma_Q, values descending, l x l eigenvector matrix)."""
+    b_mat = basis.T @ psi
+    ell = basis.shape[1]
+    z, sv, _ = np.linalg.svd(b_mat, full_matrices=True)
+    vals = np.zeros(ell)
+    vals[: sv.size] = sv ** 2
+    return b_mat, b_mat @ b_mat.T, vals, z
+
+
+def select_modes(vals_desc: np.ndarray, rank: int, force_count: int | None = None) -> np.ndarray:
+    """Spectral budget and threshold of Alg. 2 / Eq. (P^L): of the leading
+    min(r, l) Ritz values keep those strictly above one (the modes that the
+    normalized geometry over-amplifies).  Returns a mask over the leading
+    min(r, l) values."""
+    top = min(rank, vals_desc.size)
+    if force_count is None:
+        return vals_desc[:top] > 1.0
+    sel = np.zeros(top, bool)
+    sel[:force_count] = True
+    return sel
+
+
 def interaction_sketch(psi: np.ndarray, rank: int, oversample: int,
                        power_iters: int, omega: np.ndarray,
                        force_count: int | None = None) -> SketchResult:
-    """Alg. 2: l = min(m, r + o); Y = Psi Omega; p times Y <- Psi (Psi^T Y);
-    Q = qr(Y); Gamma_Q = (Q^T Psi)(Q^T Psi)^T; top-r eigenpairs (Z, Lambda);
-    U = Q Z; C = {i : lambda_i > 1}.
+    """Randomized interaction sketch (Alg. 2, App. B): sketch width
+    l = min(a, r + o) for a active rows, the candidate subspace, its Ritz
+    pairs, the leading min(r, l) of them, and the selected set C.
 
     ``force_count`` (tests only) selects exactly that many leading Ritz pairs
     instead of applying the threshold, to compare against a run whose
     r-th boundary fell inside a near-tie.
     """
-    a = psi.shape[0]
-    ell = min(a, rank + oversample)
-    y = psi @ omega[:, :ell]
-    for _ in range(power_iters):
-        y = psi @ (psi.T @ y)
-    q, _ = np.linalg.qr(y, mode="reduced")
-    b_mat = q.T @ psi
-    gamma_q = b_mat @ b_mat.T
-    evals, evecs = np.linalg.eigh(gamma_q)
-    order = _desc_order(evals)
-    top = order[: min(rank, ell)]
-    lam = evals[top]
-    z = evecs[:, top]
-    if force_count is None:
-        sel = lam > 1.0
-    else:
-        sel = np.zeros(lam.shape, bool)
-        sel[:force_count] = True
-    u_hat = q @ z
-    return SketchResult(ell=ell, q=q, b_mat=b_mat, gamma_q=gamma_q,
-                        ritz_values=lam, ritz_vectors=z, selected=sel,
+    ell = min(psi.shape[0], rank + oversample)
+    basis = candidate_subspace(psi, omega[:, :ell], power_iters)
+    b_mat, gamma_q, vals, z = rayleigh_ritz(psi, basis)
+    top = min(rank, ell)
+    sel = select_modes(vals, rank, force_count)
+    lam, z_top = vals[:top], z[:, :top]
+    u_hat = basis @ z_top
+    return SketchResult(ell=ell, q=basis, b_mat=b_mat, gamma_q=gamma_q,
+                        ritz_values=lam, ritz_vectors=z_top, selected=sel,
                         u_sel=u_hat[:, sel], lam_sel=lam[sel])
 
 

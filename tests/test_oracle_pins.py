@@ -278,6 +278,65 @@ def test_sketch_basis_invariance():
     assert np.allclose(t2, O.localized_apply(psi, sk.u_sel, sk.lam_sel), atol=1e-11)
 
 
+def _psi_from_factors(a, b, sig, seed):
+    """Psi = U diag(sig) V^T with Haar-like orthonormal U (a x k), V (b x k)."""
+    rng = np.random.default_rng(seed)
+    k = len(sig)
+    u, _ = np.linalg.qr(rng.standard_normal((a, k)))
+    v, _ = np.linalg.qr(rng.standard_normal((b, k)))
+    return u, np.asarray(sig, float), v, (u * np.asarray(sig, float)) @ v.T
+
+
+def _projector(basis):
+    return basis @ basis.T
+
+
+@pytest.mark.parametrize("p", [0, 1, 2])
+def test_candidate_subspace_is_the_power_iterated_range(p):
+    # Alg. 2: range(Y) = range((Psi Psi^T)^p Psi Omega).  With Psi = U S V^T
+    # that is range(U S^(2p+1) V^T Omega), formed here from the factors alone.
+    # Each p gives a different l-dimensional subspace (rank 30 > l = 8), so a
+    # dropped, repeated or skipped power iteration fails the projector match.
+    sig = np.linspace(2.0, 0.5, 30)
+    u, s, v, psi = _psi_from_factors(40, 60, sig, 100 + p)
+    omega = O.sketch_omega(21, 3, 1, 60, 8)
+    q = O.candidate_subspace(psi, omega, p)
+    assert np.allclose(q.T @ q, np.eye(8), atol=1e-12)
+    expect = {}
+    for pp in range(4):
+        y = u @ (s[:, None] ** (2 * pp + 1) * (v.T @ omega))
+        expect[pp], _ = np.linalg.qr(y)
+    assert np.linalg.norm(_projector(q) - _projector(expect[p]), 2) < 1e-9
+    for pp in range(4):
+        if pp != p:
+            assert np.linalg.norm(_projector(q) - _projector(expect[pp]), 2) > 1e-2
+    # and the whole sketch uses exactly hp.power_iters of them
+    sk = O.interaction_sketch(psi, 4, 4, p, omega)
+    assert np.linalg.norm(_projector(sk.q) - _projector(expect[p]), 2) < 1e-9
+
+
+def test_power_iteration_converges_to_the_leading_eigenpairs():
+    # Spectral gap after r = 4: sigma = (3, 2.8, 2.6, 2.4 | 0.5 ...).  Subspace
+    # iteration contracts the error by (sigma_5 / sigma_4)^2 per pass, so with
+    # p = 30 the top-r Ritz values are the top-r eigenvalues of Gamma to
+    # rounding; with p = 0 a 6-dimensional random subspace of a 50-dimensional
+    # range misses them by a wide margin, and each extra pass gets closer.
+    sig = np.concatenate([[3.0, 2.8, 2.6, 2.4], np.linspace(0.5, 0.05, 46)])
+    u, s, v, psi = _psi_from_factors(50, 80, sig, 7)
+    omega = O.sketch_omega(5, 0, 0, 80, 6)
+    lam_true = s[:4] ** 2
+    err = []
+    for p in range(6):
+        sk = O.interaction_sketch(psi, 4, 2, p, omega)
+        err.append(np.max(np.abs(sk.ritz_values - lam_true) / lam_true))
+    sk30 = O.interaction_sketch(psi, 4, 2, 30, omega)
+    assert np.allclose(sk30.ritz_values, lam_true, rtol=1e-10, atol=0)
+    # the selected eigenvectors are the leading left singular vectors
+    assert np.linalg.norm(_projector(sk30.u_sel) - _projector(u[:, :4]), 2) < 1e-9
+    assert err[0] > 0.05
+    assert all(err[i + 1] < err[i] for i in range(5)), err
+
+
 def test_topr_then_threshold_equals_threshold_then_topr():
     psi = _correlated_psi(30, 45, rank=10, noise=0.2)
     om = O.sketch_omega(2, 2, 2, 45, 13)
