@@ -1,15 +1,24 @@
 """Benchmark of the NormPre optimizer step on one MI355X.
 
 A step is one NormPre-G (or NormPre-L) optimizer step over a whole synthetic
-layer stack (default: the 48 hidden matrices of GPT-2 Small), with t
-incrementing so both orientations are timed, inputs resident in HBM.
+layer stack (default: the 196 hidden matrices of Qwen3-1.7B, the largest
+single-GPU stack of the workload list), with t incrementing so both
+orientations are timed, inputs resident in HBM.
 
-Prints ONE JSON line.  `value` is NormPre-G steps/s of the stack (the metric
-also reports NS GEMM TFLOP/s and roofline fractions); NormPre-L is reported
-in `variants`.  The per-kernel roofline comes from a second timed region of
-the same K steps in which the library brackets every launch with HIP events
-on the step's stream (the clean region gives `value`).  The CPU baseline is
-the float64 oracle on a bounded sample of the same workload.
+Prints ONE JSON line.  `value` is NormPre-G steps/s of the stack; NormPre-L is
+reported in `variants`, and the GPT-2 Small stack (the paper's other
+optimizer-latency workload) under `gpt2_small`.  The per-kernel roofline
+comes from a second timed region of the same K steps in which the library
+brackets every launch with HIP events on the step's stream (the clean region
+gives `value`).  For NormPre-G the roofline kernel is the Newton-Schulz GEMM
+class: `achieved` is the nominal Newton-Schulz work of the plain iteration,
+q (4 s^2 L + 2 s^3) per matrix (s, L the short and long side), over the
+class's device time, and `mfma_util_executed` is the MFMA work the launches
+actually issue (tiles x tile FLOPs; symmetric products compute only upper
+tiles, and the Gram-space schedule does less work than the plain iteration)
+over the same time, as a fraction of peak.  The CPU baseline is the float64
+oracle timed on one matrix of every shape group of the stack (both
+orientations), scaled by the group sizes to whole-stack steps/s.
 
 `roofline.traffic` is the HBM traffic per launch of the roofline kernel,
 read from the committed rocprofv3 counter summary for the workload
@@ -47,12 +56,14 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", default="gpt2_small")
+    p.add_argument("--workload", default="qwen3_1p7b")
+    p.add_argument("--no-gpt2", action="store_true",
+                   help="skip the GPT-2 Small stack reported next to the headline workload")
     p.add_argument("--variants", default="G,L")
     p.add_argument("--rank", type=int, default=None, help="NormPre-L rank r (default: the workload's)")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-seconds", type=float, default=12.0,
-                   help="time bound of the oracle CPU baseline sample")
+    p.add_argument("--cpu-seconds", type=float, default=20.0,
+                   help="time bound of the oracle CPU baseline sample (per variant)")
     p.add_argument("--json-out", default=None)
     p.add_argument("--crossover", action="store_true",
                    help="time NormPre-G against NormPre-L at every rank of the large single-matrix "
@@ -205,8 +216,40 @@ def roofline_of(cls, bound):
             "algorithmic_bytes_per_launch": round(cls["bytes"] / cls["launches"])}
 
 
+def ns_nominal_flops(shapes, q=5):
+    """Nominal Newton-Schulz FLOPs of one step of the plain iteration:
+    q (4 s^2 L + 2 s^3) per matrix (Gram 2 s^2 L, A^2 2 s^3, combine 2 s^2 L)."""
+    tot = 0.0
+    for m, n in shapes:
+        sm, lg = float(min(m, n)), float(max(m, n))
+        tot += 4.0 * sm * sm * lg + 2.0 * sm ** 3
+    return q * tot
+
+
+def ns_roofline(ns, shapes, steps):
+    """Roofline of the Newton-Schulz GEMM class: nominal work (plain
+    iteration) per launch over the average launch duration, and the issued
+    MFMA work over the same time."""
+    if not ns or ns["launches"] == 0 or ns["ms"] <= 0:
+        return None
+    sec = ns["ms"] / 1e3
+    nominal = ns_nominal_flops(shapes) * steps
+    ach = nominal / sec / 1e12
+    executed = ns["exec_flops"] / sec / 1e12
+    return {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_FP16_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(ach / PEAK_FP16_TFLOPS, 4), "traffic": None,
+            "mfma_util_executed": round(executed / PEAK_FP16_TFLOPS, 4),
+            "executed_tflops_per_s": round(executed, 2),
+            "schedule_tflops_per_s": round(ns["flops"] / sec / 1e12, 2),
+            "launches": ns["launches"], "avg_launch_us": round(1e3 * ns["ms"] / ns["launches"], 2),
+            "nominal_flops_per_launch": round(nominal / ns["launches"]),
+            "executed_flops_per_launch": round(ns["exec_flops"] / ns["launches"]),
+            "nominal_flops_per_step": ns_nominal_flops(shapes),
+            "algorithmic_bytes_per_launch": round(ns["bytes"] / ns["launches"])}
+
+
 def merge_classes(classes, names):
-    out = {"launches": 0, "ms": 0.0, "flops": 0.0, "bytes": 0.0}
+    out = {"launches": 0, "ms": 0.0, "flops": 0.0, "exec_flops": 0.0, "bytes": 0.0}
     for n in names:
         c = classes.get(n)
         if c:
@@ -215,35 +258,58 @@ def merge_classes(classes, names):
     return out
 
 
-def cpu_baseline(wl, variant, seconds, rank):
-    """Oracle (float64 NumPy) on a time-bounded sample of the workload: whole
-    steps of the stack in order (t = 0, 1, ...; both orientations) until
-    `seconds` have elapsed, at most two steps; the rate is scaled to steps of
-    the full stack."""
-    import numpy as np
-    from oracle import normpre_oracle as O
-    from paper_2609_36692_amd import workloads as WL
+def blas_info():
+    """BLAS library numpy calls and its thread count (threadpoolctl)."""
     try:
         from threadpoolctl import threadpool_info
-        threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+        infos = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if infos:
+            i = infos[0]
+            return {"library": f"{i.get('internal_api')} {i.get('version')}", "threads": int(i.get("num_threads", 1)),
+                    "arch": i.get("architecture")}
     except Exception:
-        threads = len(os.sched_getaffinity(0))
+        pass
+    return {"library": "unknown", "threads": len(os.sched_getaffinity(0)), "arch": None}
+
+
+def cpu_baseline(wl, variant, seconds, rank):
+    """Oracle (float64 NumPy) on a bounded sample of the workload: one matrix
+    of every shape group of the stack, at t = 0 and t = 1 (both orientations),
+    timed per matrix update; the stack step time is the group-size-weighted
+    sum, and the rate is reported in whole-stack steps/s.  Stops early (and
+    scales what it measured) if `seconds` run out."""
+    from oracle import normpre_oracle as O
+    from paper_2609_36692_amd import workloads as WL
+    blas = blas_info()
     hp = O.HParams(lr=wl.lr, rank=rank, oversample=wl.oversample, power_iters=wl.power_iters)
-    n = len(wl.shapes)
-    done = 0
+    groups = {}
+    for i, sh in enumerate(wl.shapes):
+        groups.setdefault(tuple(sh), []).append(i)
+    per_matrix, done = {}, 0
     t0 = time.perf_counter()
-    while done < 2 * n:
-        i, t = done % n, done // n
-        w, g, mp = WL.make_matrix(wl, i, "cpu")
-        O.normpre_step(w.numpy(), g.numpy(), mp.numpy(), t, hp, variant, matrix_id=i)
-        done += 1
+    for sh, idx in groups.items():
+        times = []
+        for t in (0, 1):
+            if time.perf_counter() - t0 >= seconds and times:
+                break
+            w, g, mp = WL.make_matrix(wl, idx[0], "cpu")
+            a = time.perf_counter()
+            O.normpre_step(w.numpy(), g.numpy(), mp.numpy(), t, hp, variant, matrix_id=idx[0])
+            times.append(time.perf_counter() - a)
+            done += 1
+        per_matrix[sh] = sum(times) / len(times)
         if time.perf_counter() - t0 >= seconds:
             break
+    measured = [sh for sh in groups if sh in per_matrix]
+    covered = sum(len(groups[sh]) for sh in measured)
+    est = sum(len(groups[sh]) * per_matrix[sh] for sh in measured) * len(wl.shapes) / covered
     dt = time.perf_counter() - t0
-    steps = done / n
-    return {"value": round(steps / dt, 5), "unit": "steps/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{done} matrix updates ({steps:.3g} steps of the {n}-matrix stack, t = 0.."
-                      f"{(done - 1) // n}), NormPre-{variant}, {dt:.1f} s measured"}
+    detail = ", ".join(f"{sh[0]}x{sh[1]} x{len(groups[sh])}: {per_matrix[sh]:.2f} s" for sh in measured)
+    return {"value": round(1.0 / est, 6), "unit": "steps/s", "cores": blas["threads"], "kind": "oracle",
+            "sample": f"NormPre-{variant}: one matrix per shape group at t = 0 and 1 ({done} matrix updates, "
+                      f"{dt:.1f} s; per matrix {detail}), weighted by group size to the {len(wl.shapes)}-matrix "
+                      f"stack ({covered} of {len(wl.shapes)} matrices' groups measured)",
+            "blas": blas}
 
 
 def crossover(N, WL, torch, steps, warmup):
@@ -313,7 +379,7 @@ def main():
         cls = r["classes"]
         if v in ("G", "MUON"):
             ns = merge_classes(cls, ["ns_gram", "ns_poly", "ns_combine"])
-            roof = roofline_of(ns, "mfma")
+            roof = ns_roofline(ns, wl.shapes, a.steps)
             roof["kernel"] = "Newton-Schulz GEMMs (gram + poly + Gram-space products + combine, fp16 MFMA)"
         elif v == "NORM":
             roof = roofline_of(cls["normalize"], "hbm")
@@ -343,8 +409,9 @@ def main():
             "kernel_share": {k: round(c["ms"] / total_dev, 4) for k, c in cls.items() if c["launches"]},
         }
         if v in ("G", "MUON"):
-            res[v]["ns_tflops_step"] = round(ns["flops"] / a.steps / 1e12, 4)
-            res[v]["ns_tflops_per_s_in_step"] = round(ns["flops"] / a.steps / 1e12 / (r["ms_per_step"] / 1e3), 2)
+            nominal = ns_nominal_flops(wl.shapes)
+            res[v]["ns_nominal_tflop_per_step"] = round(nominal / 1e12, 4)
+            res[v]["ns_nominal_tflops_per_s_whole_step"] = round(nominal / 1e12 / (r["ms_per_step"] / 1e3), 2)
         print(f"[bench] NormPre-{v}: {res[v]['ms_per_step']:.3f} ms/step", file=sys.stderr, flush=True)
 
     # Optimizer latency relative to the Muon reference step through the same
@@ -357,9 +424,31 @@ def main():
 
     cpu = None
     if not a.no_cpu_baseline:
-        v0 = variants[0]
-        cpu = cpu_baseline(wl, v0, a.cpu_seconds, rank)
-        print(f"[bench] cpu baseline: {cpu}", file=sys.stderr, flush=True)
+        for v in variants:
+            if v not in ("G", "L"):
+                continue
+            cb = cpu_baseline(wl, v, a.cpu_seconds, rank)
+            res[v]["cpu_baseline"] = cb
+            print(f"[bench] cpu baseline NormPre-{v}: {cb['value']} steps/s ({cb['sample']})", file=sys.stderr,
+                  flush=True)
+        cpu = res[variants[0]].get("cpu_baseline")
+
+    # The paper's other optimizer-latency workload, for the comparison of its
+    # efficiency tables (context).
+    gpt2 = None
+    if not a.no_gpt2 and wl.name != "gpt2_small":
+        g2 = WL.WORKLOADS["gpt2_small"]
+        gpt2 = {}
+        for v in ("G", "L"):
+            r = time_variant(N, WL, torch, g2, v, a.steps, a.warmup, g2.rank)
+            entry = {"steps_per_s": round(1e3 / r["ms_per_step"], 3), "ms_per_step": round(r["ms_per_step"], 4)}
+            if (g2.name, v) in PAPER_STEPS_PER_S:
+                entry["vs_paper_a100"] = round(entry["steps_per_s"] / PAPER_STEPS_PER_S[(g2.name, v)], 2)
+            if v == "G":
+                ns = merge_classes(r["classes"], ["ns_gram", "ns_poly", "ns_combine"])
+                entry["ns_roofline"] = ns_roofline(ns, g2.shapes, a.steps)
+            gpt2[v] = entry
+            print(f"[bench] gpt2_small NormPre-{v}: {entry['ms_per_step']:.3f} ms/step", file=sys.stderr, flush=True)
 
     primary = variants[0]
     p = res[primary]
@@ -388,6 +477,8 @@ def main():
         "cpu_baseline": cpu,
         "variants": res,
     }
+    if gpt2:
+        line["gpt2_small"] = gpt2
     if copy_ref:
         line["copy_reference"] = copy_ref
     if rel:

@@ -22,18 +22,24 @@
  *   - The caller owns W, G and M.  W and M are updated in place, G is read
  *     only.  Distinct matrices must not overlap; W, G and M of one matrix
  *     must be three distinct buffers.
- *   - The library owns only its workspace (grown on demand, released by
- *     normpre_destroy).  The step counter t and the seed are caller state:
- *     restoring (W, M, t, seed) reproduces the next step exactly.
+ *   - The library owns only its workspace (released by normpre_destroy).
+ *     It is grown on demand by normpre_step(), which then waits for the
+ *     context's earlier work and reallocates (see normpre_step), or sized up
+ *     front by normpre_reserve(), after which steps never grow it.  The step
+ *     counter t and the seed are caller state: restoring (W, M, t, seed)
+ *     reproduces the next step exactly.
  *   - Errors: every int-returning entry point returns NORMPRE_OK (0) or a
  *     negative NORMPRE_ERR_* code; nothing throws or aborts across the ABI.
  *     Argument validation happens on the host before any launch, so on an
  *     error no device memory has been written.  The message of the last
  *     error on a context is available from normpre_last_error().
- *   - normpre_step() only enqueues work on the given stream and never
- *     synchronizes; device faults surface at the caller's next
- *     synchronization.  A context must be used by one host thread and one
- *     stream at a time.
+ *   - normpre_step() only enqueues work on the given stream; it
+ *     synchronizes only when it has to grow the workspace (never after
+ *     normpre_reserve) or the debug buffers (NORMPRE_FLAG_DEBUG).  Device
+ *     faults surface at the caller's next synchronization.  A context must
+ *     be used by one host thread at a time; consecutive calls may use
+ *     different streams (a call on a new stream is ordered after the work
+ *     the previous call enqueued, through an event).
  */
 #ifndef NORMPRE_H
 #define NORMPRE_H
@@ -192,14 +198,46 @@ int normpre_validate(int variant, int num_mats, const int64_t* shapes,
  * The sketch of matrix i uses the counter (seed, t, i): its index in this list.
  * Matrices of equal shape are processed by shared batched launches.
  * num_mats == 0 is a successful no-op.
+ * Workspace: when the step needs more than the context holds (and no
+ * normpre_reserve was made) the call waits for the context's previous stream
+ * and `stream`, frees the old workspace and hipMallocs a larger one.
  * Errors: NOT_INITIALIZED, INVALID_ARG (as normpre_validate, plus null
- * pointer arrays or entries, or W/G/M of one matrix aliasing), UNSUPPORTED,
+ * pointer arrays or entries, or W/G/M of one matrix aliasing), UNSUPPORTED
+ * (as normpre_validate, or more workspace than normpre_reserve reserved),
  * OOM (workspace growth), HIP_ERROR (a launch or runtime call failed).
  */
 int normpre_step(normpre_ctx* ctx, int variant, int num_mats,
                  float* const* params, const float* const* grads,
                  float* const* momentum, const int64_t* shapes,
                  const normpre_hparams* hp, void* stream);
+
+/*
+ * Workspace bytes that normpre_step() needs for this argument list at every
+ * step t (both orientations of the alternating rule).  Host only; the
+ * arguments are checked as in normpre_validate.  *bytes = 0 for num_mats = 0.
+ * (The Alg. 1 Require list: the optimizer state is W, M and t; the library's
+ * own memory is this workspace.)
+ * Errors: INVALID_ARG (null bytes, or the checks of normpre_validate),
+ * UNSUPPORTED.
+ */
+int normpre_workspace_size(int variant, int num_mats, const int64_t* shapes,
+                           const normpre_hparams* hp, int64_t* bytes);
+
+/*
+ * Sizes the context's workspace for this argument list (normpre_workspace_size
+ * bytes) so that later normpre_step() calls never synchronize or allocate.
+ * May itself synchronize the context's last stream and `stream` and
+ * reallocate.  After it, a step that needs more workspace fails with
+ * UNSUPPORTED instead of growing it; a new normpre_reserve raises the size.
+ * Errors: NOT_INITIALIZED, INVALID_ARG, UNSUPPORTED (the checks of
+ * normpre_validate), OOM, HIP_ERROR.
+ */
+int normpre_reserve(normpre_ctx* ctx, int variant, int num_mats, const int64_t* shapes,
+                    const normpre_hparams* hp, void* stream);
+
+/* Bytes of workspace the context currently holds.
+ * Errors: NOT_INITIALIZED, INVALID_ARG (null bytes). */
+int normpre_workspace_bytes(const normpre_ctx* ctx, int64_t* bytes);
 
 /* ---- spectral diagnostics (App. A, spectral dynamics) -------------------- */
 
@@ -238,6 +276,27 @@ int normpre_spectrum(normpre_ctx* ctx, int which, int64_t rows, int64_t cols, co
  * Host only.  Errors: INVALID_ARG (null pointers, count or rank < 0).
  */
 int normpre_energy_split(const double* eigs, int64_t count, int32_t rank, double* out);
+
+/*
+ * Descent alignment (App. A, training dynamics): for matrices i = 0..num_mats-1
+ * with gradient G_i and weights W_i before and after an optimizer step of
+ * learning rate lr and decoupled weight decay weight_decay, the update
+ * direction before learning-rate scaling with the decay excluded is
+ *   Phi_i = (W_before_i - W_after_i) / lr - weight_decay * W_before_i
+ * (for normpre_step: the RMS-matched update U of Alg. 1), and
+ *   cosines[i] = <G_i, Phi_i>_F / (||G_i||_F ||Phi_i||_F)   (0 if either is 0),
+ *   *mean      = the average of cosines[] (Align_t).
+ * grads, w_before, w_after: host arrays of device pointers to row-major fp32
+ * rows x cols matrices (shapes as in normpre_step), read only; cosines: host
+ * array of num_mats doubles.  fp64 accumulation, fixed summation order.
+ * Uses the context's workspace on `stream` and synchronizes it.
+ * Errors: NOT_INITIALIZED, INVALID_ARG (null pointers, num_mats < 0, a bad
+ * shape, lr not > 0 or not finite), OOM, HIP_ERROR.
+ */
+int normpre_descent_alignment(normpre_ctx* ctx, int num_mats, const float* const* grads,
+                              const float* const* w_before, const float* const* w_after,
+                              const int64_t* shapes, float lr, float weight_decay,
+                              double* cosines, double* mean, void* stream);
 
 /* ---- inspection (tests, benchmarks) -------------------------------------- */
 
@@ -293,15 +352,20 @@ int normpre_sketch_omega(uint64_t seed, int64_t step, int32_t matrix_id,
 /*
  * Per-kernel-class totals since the last reset, over steps made with
  * NORMPRE_FLAG_TIME_KERNELS: launches, device milliseconds (HIP events on the
- * step's stream around each launch), algorithmic flops and algorithmic HBM
- * bytes (the minimum the operation must move; formulas in the design notes).
- * Synchronizes the last step's stream.  reset != 0 clears the totals after
- * reading them.  Any output pointer may be null.
+ * step's stream around each launch), the algorithmic flops of the operations
+ * the launches perform (a Newton-Schulz Gram 2 s^2 L, an s x s product
+ * 2 s^3, a combine 2 s^2 L, real sizes), the MFMA flops the launches issue
+ * (tiles computed x 2 x tile rows x tile columns x padded reduction length;
+ * symmetric products compute their upper-triangular tiles only; 0 for
+ * classes that are not matrix products) and the algorithmic HBM bytes (the
+ * minimum the operation must move).  Synchronizes the last step's stream.
+ * reset != 0 clears the totals after reading them.  Any output pointer may
+ * be null.
  * Errors: NOT_INITIALIZED, INVALID_ARG (kclass out of range), HIP_ERROR.
  */
 int normpre_kernel_stats(normpre_ctx* ctx, int kclass, int64_t* launches,
-                         double* device_ms, double* flops, double* bytes,
-                         int reset);
+                         double* device_ms, double* flops, double* exec_flops,
+                         double* bytes, int reset);
 
 /* Library version string (static storage). */
 const char* normpre_version(void);

@@ -484,6 +484,21 @@ def energy_split(eigs, count: int, rank: int) -> dict:
     return {"top": top, "remain": remain, "sub": sub, "global": top + remain + sub}
 
 
+def descent_alignment(grads, updates):
+    """Descent alignment (App. A, training dynamics): for each matrix the
+    cosine of its gradient G and its update direction Phi before
+    learning-rate scaling, decoupled weight decay excluded (for NormPre the
+    RMS-matched update U of Alg. 1); Align_t is their plain mean.  A zero G or
+    Phi gives cosine 0.  Returns (cosines, mean)."""
+    cos = []
+    for g, phi in zip(grads, updates):
+        g = np.asarray(g, np.float64)
+        phi = np.asarray(phi, np.float64)
+        den = np.linalg.norm(g) * np.linalg.norm(phi)
+        cos.append(float(np.sum(g * phi) / den) if den > 0 else 0.0)
+    return cos, (sum(cos) / len(cos) if cos else 0.0)
+
+
 def relative_fro(a, b) -> float:
     a = np.asarray(a, np.float64)
     b = np.asarray(b, np.float64)

@@ -160,12 +160,12 @@ Fail validate(int variant, int num_mats, const int64_t* shapes, const normpre_hp
 // -------------------------------------------------------------- timing ---
 struct KStat {
     int64_t launches = 0;
-    double ms = 0, flops = 0, bytes = 0;
+    double ms = 0, flops = 0, bytes = 0, exec_flops = 0;
 };
 struct PendingEvent {
     int kclass;
     hipEvent_t start, stop;
-    double flops, bytes;
+    double flops, bytes, exec_flops;
 };
 
 struct DebugMat {
@@ -197,6 +197,11 @@ struct normpre_ctx {
     std::vector<hipEvent_t> event_pool;
     bool timing = false;
     hipStream_t stream = nullptr;
+    // Orders a step after the previous step's work when the caller switches
+    // streams (created by normpre_init, so no step allocates it).
+    hipEvent_t order_ev = nullptr;
+    // Workspace reserved by normpre_reserve(): steps then never grow it.
+    bool reserved = false;
 };
 
 namespace {
@@ -225,8 +230,10 @@ hipEvent_t get_event(normpre_ctx* ctx) {
 // Runs one launch; with kernel timing on, times it with an event pair.  A
 // GEMM launch takes the pair itself (recorded at the kernel's own start and
 // end); any other launch is bracketed by stream-ordered records.
+// `exec_flops`: MFMA work the launch issues (tiles x tile FLOPs, zero padding
+// included); negative for launches that are not matrix products.
 template <class F>
-hipError_t timed(normpre_ctx* ctx, int kclass, double flops, double bytes, F&& launch) {
+hipError_t timed(normpre_ctx* ctx, int kclass, double flops, double bytes, F&& launch, double exec_flops = -1.0) {
     if (!ctx->timing) return launch();
     hipEvent_t a = get_event(ctx), b = get_event(ctx);
     if (!a || !b) return hipErrorOutOfMemory;
@@ -240,7 +247,7 @@ hipError_t timed(normpre_ctx* ctx, int kclass, double flops, double bytes, F&& l
         e = hipEventRecord(b, ctx->stream);
         if (e != hipSuccess) return e;
     }
-    ctx->pending.push_back({kclass, a, b, flops, bytes});
+    ctx->pending.push_back({kclass, a, b, flops, bytes, exec_flops < 0.0 ? 0.0 : exec_flops});
     return hipSuccess;
 }
 
@@ -256,6 +263,7 @@ int collect_events(normpre_ctx* ctx) {
         s.ms += ms;
         s.flops += p.flops;
         s.bytes += p.bytes;
+        s.exec_flops += p.exec_flops;
         ctx->event_pool.push_back(p.start);
         ctx->event_pool.push_back(p.stop);
     }
@@ -740,6 +748,15 @@ TileCfg ns_cfg(int64_t M, int64_t N, bool sym, int count) {
     return tiles >= (sym ? 512 : 384) ? TileCfg::Big256 : TileCfg::Big;
 }
 
+// MFMA FLOPs a product launch issues for `count` matrices of M x N x K with
+// tile `cfg`: symmetric products compute the upper-triangular tiles only.
+double issued_flops(TileCfg cfg, int64_t M, int64_t N, int64_t K, bool sym, int64_t count) {
+    const int64_t bm = gemm_tile_m(cfg), bn = gemm_tile_n(cfg);
+    const int64_t tm = M / bm, tn = N / bn;
+    const int64_t tiles = sym ? tm * (tm + 1) / 2 : tm * tn;
+    return 2.0 * (double)tiles * (double)(bm * bn) * (double)K * (double)count;
+}
+
 // The Grams of every item of one pool with the same operand layout, in one
 // launch: small same-s batches (e.g. the three wide shapes of a transformer
 // block) fill the chip together where each alone would not.
@@ -773,8 +790,10 @@ int gram_pool_launch(const StepCtx& sc, std::vector<const Item*> its, const Pool
     e.mul_pow = first_it ? 2 : 0;
     e.ca = 1.f; e.cs = 0.f;
     const TileCfg cfg = ns_cfg(pl.sp, pl.sp, true, total);
+    double issued = 0.0;
+    for (const Item* it : its) issued += issued_flops(cfg, pl.sp, pl.sp, it->d.lp_, true, it->count);
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_GRAM, flops, bytes,
-                 [&] { return launch_gemm_gram_grouped(cfg, layout, gg, (int)pl.sp, e, sc.s); }),
+                 [&] { return launch_gemm_gram_grouped(cfg, layout, gg, (int)pl.sp, e, sc.s); }, issued),
            "ns gram");
     return NORMPRE_OK;
 }
@@ -815,7 +834,8 @@ int poly_launch(const StepCtx& sc, const Pool& pl, int first, int cnt, half_t* o
     // Nominal FLOPs use the real s of each matrix (padding excluded); bytes
     // are A read once and B written once (4 s^2 per matrix).
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_POLY, nominal_flops, 2.0 * nominal_flops / (double)sp,
-                 [&] { return launch_gemm_affine(cfg, 0, A, B, sh, cnt, e, sc.s); }),
+                 [&] { return launch_gemm_affine(cfg, 0, A, B, sh, cnt, e, sc.s); },
+                 issued_flops(cfg, sp, sp, sp, true, cnt)),
            "ns poly");
     return NORMPRE_OK;
 }
@@ -851,7 +871,7 @@ int combine_launch(const StepCtx& sc, const Item& it, const half_t* smat, half_t
         return launch_gemm_affine(cfg, 0, A, B, sh, count, e, sc.s);
     };
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_COMBINE, 2.0 * s_ * s_ * l_ * count, 2.0 * (2.0 * s_ * l_ + s_ * s_) * count,
-                 go),
+                 go, issued_flops(cfg, d.sp, d.lp_, d.sp, false, count)),
            "ns combine");
     return NORMPRE_OK;
 }
@@ -916,8 +936,10 @@ int combine_grouped_launch(const StepCtx& sc, const std::vector<Item*>& ch, cons
     e.mul_pow = first_it ? 1 : 0;
     e.ca = 1.f;
     e.cs = sc.hp->ns_coeffs[0];
+    double issued = 0.0;
+    for (const Item* it : ch) issued += issued_flops(cfg, sp, it->d.lp_, sp, false, it->count);
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_COMBINE, flops, bytes,
-                 [&] { return launch_gemm_combine_grouped(cfg, (int)sp, g, e, sc.s); }),
+                 [&] { return launch_gemm_combine_grouped(cfg, (int)sp, g, e, sc.s); }, issued),
            "ns combine");
     return NORMPRE_OK;
 }
@@ -936,7 +958,8 @@ int gns_product(const StepCtx& sc, const Pool& pl, const half_t* smat, const hal
     const TileCfg cfg = ns_cfg(sp, sp, true, pl.gns_count);
     // Bytes: S and R read once, the result written once (6 s^2 per matrix).
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_POLY, flops, 3.0 * flops / (double)sp,
-                 [&] { return launch_gemm_affine(cfg, 0, A, B, sh, pl.gns_count, e, sc.s); }),
+                 [&] { return launch_gemm_affine(cfg, 0, A, B, sh, pl.gns_count, e, sc.s); },
+                 issued_flops(cfg, sp, sp, sp, true, pl.gns_count)),
            "ns gram-space product");
     return NORMPRE_OK;
 }
@@ -1692,6 +1715,138 @@ int check_aliasing(normpre_ctx* ctx, int num_mats, float* const* W, const float*
     return NORMPRE_OK;
 }
 
+// The launch plan of one step: equal shapes grouped (first-appearance order),
+// groups cut into items of at most item_budget workspace bytes, items packed
+// into rounds of at most round_budget bytes; `need` is the largest round.
+struct Plan {
+    std::vector<Group> groups;
+    std::vector<std::vector<Item>> rounds;
+    size_t need = 0;
+    size_t one_matrix = 0;   // the largest single-matrix item of the step
+};
+
+Plan plan_step(int variant, int num_mats, const int64_t* shapes, const normpre_hparams& hp, int k,
+               size_t item_budget, size_t round_budget) {
+    Plan pl;
+    const bool source_x = variant == NORMPRE_VARIANT_L && (hp.flags & NORMPRE_FLAG_SOURCE_X) != 0;
+    {
+        std::map<std::pair<int64_t, int64_t>, int> where;
+        for (int i = 0; i < num_mats; ++i) {
+            auto key = std::make_pair(shapes[2 * i], shapes[2 * i + 1]);
+            auto it = where.find(key);
+            if (it == where.end()) {
+                where[key] = (int)pl.groups.size();
+                pl.groups.push_back({key.first, key.second, {i}});
+            } else {
+                pl.groups[it->second].idx.push_back(i);
+            }
+        }
+    }
+    std::vector<Item> all;
+    for (size_t g = 0; g < pl.groups.size(); ++g) {
+        const Dims d = dims_of(pl.groups[g].m, pl.groups[g].n, k, hp);
+        const int cnt = (int)pl.groups[g].idx.size();
+        Item one;
+        one.g = (int)g;
+        one.count = 1;
+        one.d = d;
+        one.gns = gram_space_ns(variant, d, hp);
+        const size_t per = round_bytes({one}, variant, source_x);
+        pl.one_matrix = std::max(pl.one_matrix, per);
+        const int b = (int)std::max<size_t>(1, std::min<size_t>((size_t)cnt, item_budget / std::max<size_t>(per, 1)));
+        for (int first = 0; first < cnt; first += b) {
+            Item it;
+            it.g = (int)g;
+            it.first = first;
+            it.count = std::min(b, cnt - first);
+            it.d = d;
+            it.gns = one.gns;
+            all.push_back(it);
+        }
+    }
+    // Rounds: consecutive items whose phases run interleaved, with their
+    // small matrices pooled.
+    for (const Item& it : all) {
+        if (!pl.rounds.empty()) {
+            std::vector<Item> trial = pl.rounds.back();
+            trial.push_back(it);
+            const size_t bytes = round_bytes(trial, variant, source_x);
+            if (bytes <= round_budget) {
+                pl.rounds.back().push_back(it);
+                pl.need = std::max(pl.need, bytes);
+                continue;
+            }
+        }
+        pl.rounds.push_back({it});
+        pl.need = std::max(pl.need, round_bytes(pl.rounds.back(), variant, source_x));
+    }
+    return pl;
+}
+
+// Workspace bytes that cover every step of this argument list: both
+// orientations under the alternating rule.
+size_t workspace_need(int variant, int num_mats, const int64_t* shapes, const normpre_hparams& hp) {
+    normpre_hparams h = hp;
+    size_t need = 0;
+    for (int t = 0; t < 2; ++t) {
+        h.step = hp.step + t;
+        const int k = step_orientation(variant, h);
+        need = std::max(need, plan_step(variant, num_mats, shapes, h, k, kGroupBudget, kRoundBudget).need);
+    }
+    return need;
+}
+
+// Makes stream s wait for the work the context enqueued on another stream
+// (the workspace is shared by consecutive steps).
+int order_after_last(normpre_ctx* ctx, hipStream_t s) {
+    if (!ctx->have_stream || ctx->last_stream == s) return NORMPRE_OK;
+    hipError_t e = hipEventRecord(ctx->order_ev, ctx->last_stream);
+    if (e == hipSuccess) e = hipStreamWaitEvent(s, ctx->order_ev, 0);
+    if (e != hipSuccess) return hip_fail(ctx, e, "ordering after the previous stream");
+    return NORMPRE_OK;
+}
+
+// Enqueues every round of a plan on s, with the workspace at ws (ws_bytes).
+int run_plan(normpre_ctx* ctx, int variant, Plan& plan, float* const* params, const float* const* grads,
+             float* const* momentum, const normpre_hparams* hp, hipStream_t s, void* ws, size_t ws_bytes,
+             bool debug) {
+    const bool source_x = variant == NORMPRE_VARIANT_L && (hp->flags & NORMPRE_FLAG_SOURCE_X) != 0;
+    ctx->dbg_valid = false;
+    ctx->timing = (hp->flags & NORMPRE_FLAG_TIME_KERNELS) != 0;
+    ctx->stream = s;
+    StepCtx sc{ctx, s, hp, params, grads, momentum, variant, debug, &plan.groups};
+    for (std::vector<Item>& items : plan.rounds) {
+        std::vector<Pool> pools = make_pools(items, variant);
+        Arena ar{static_cast<char*>(ws), 0, ws_bytes};
+        carve_round(ar, items, pools, variant, source_x);
+        if (ar.off > ws_bytes) return set_err(ctx, NORMPRE_ERR_HIP, "internal: round exceeds the workspace");
+        DebugMat* dbg = debug ? ctx->dbg.data() : nullptr;
+        int rc = variant == NORMPRE_VARIANT_L ? run_round_l(sc, items, pools, dbg) : run_round_g(sc, items, pools, dbg);
+        if (rc) return rc;
+    }
+    ctx->last_stream = s;
+    ctx->have_stream = true;
+    if (debug) {
+        ctx->dbg_valid = true;
+        ctx->dbg_stream = s;
+    }
+    return NORMPRE_OK;
+}
+
+// Common entry checks of the step entry points; on success *s is the stream.
+int step_prologue(normpre_ctx* ctx, int variant, int num_mats, float* const* params, const float* const* grads,
+                  float* const* momentum, const int64_t* shapes, const normpre_hparams* hp) {
+    Fail f = validate(variant, num_mats, shapes, hp);
+    if (f.code) return set_err(ctx, f.code, f.msg);
+    if (num_mats == 0) return NORMPRE_OK;
+    if (!params || !grads || !momentum) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "pointer array is null");
+    int rc = check_aliasing(ctx, num_mats, params, grads, momentum, shapes);
+    if (rc) return rc;
+    hipError_t e = hipSetDevice(ctx->device);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+    return NORMPRE_OK;
+}
+
 }  // namespace
 
 // =========================================================== C ABI ========
@@ -1732,6 +1887,16 @@ int normpre_init(normpre_ctx** ctx, int device) {
     normpre_ctx* c = new (std::nothrow) normpre_ctx();
     if (!c) return set_err(nullptr, NORMPRE_ERR_OOM, "context allocation failed");
     c->device = device;
+    int prev = 0;
+    (void)hipGetDevice(&prev);
+    e = hipSetDevice(device);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&c->order_ev, hipEventDisableTiming);
+    (void)hipSetDevice(prev);
+    if (e != hipSuccess) {
+        if (c->order_ev) (void)hipEventDestroy(c->order_ev);
+        delete c;
+        return set_err(nullptr, NORMPRE_ERR_HIP, fmt("context set-up on device %d: %s", device, hipGetErrorString(e)));
+    }
     *ctx = c;
     return NORMPRE_OK;
 }
@@ -1747,6 +1912,7 @@ void normpre_destroy(normpre_ctx* ctx) {
         (void)hipEventDestroy(p.stop);
     }
     for (hipEvent_t e : ctx->event_pool) (void)hipEventDestroy(e);
+    if (ctx->order_ev) (void)hipEventDestroy(ctx->order_ev);
     if (ctx->ws) (void)hipFree(ctx->ws);
     if (ctx->dbg_mem) (void)hipFree(ctx->dbg_mem);
     (void)hipSetDevice(prev);
@@ -1771,99 +1937,58 @@ int normpre_step(normpre_ctx* ctx, int variant, int num_mats, float* const* para
                  float* const* momentum, const int64_t* shapes, const normpre_hparams* hp, void* stream) {
     if (!ctx) return set_err(nullptr, NORMPRE_ERR_NOT_INITIALIZED, "context is null");
     ctx->err.clear();
-    Fail f = validate(variant, num_mats, shapes, hp);
-    if (f.code) return set_err(ctx, f.code, f.msg);
-    if (num_mats == 0) return NORMPRE_OK;
-    if (!params || !grads || !momentum) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "pointer array is null");
-    int rc = check_aliasing(ctx, num_mats, params, grads, momentum, shapes);
-    if (rc) return rc;
-    hipError_t e = hipSetDevice(ctx->device);
-    if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+    int rc = step_prologue(ctx, variant, num_mats, params, grads, momentum, shapes, hp);
+    if (rc || num_mats == 0) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
-
     const int k = step_orientation(variant, *hp);
-    const bool source_x = variant == NORMPRE_VARIANT_L && (hp->flags & NORMPRE_FLAG_SOURCE_X) != 0;
-    // Group equal shapes (first-appearance order) so each group is one batch.
-    std::vector<Group> groups;
-    {
-        std::map<std::pair<int64_t, int64_t>, int> where;
-        for (int i = 0; i < num_mats; ++i) {
-            auto key = std::make_pair(shapes[2 * i], shapes[2 * i + 1]);
-            auto it = where.find(key);
-            if (it == where.end()) {
-                where[key] = (int)groups.size();
-                groups.push_back({key.first, key.second, {i}});
-            } else {
-                groups[it->second].idx.push_back(i);
-            }
-        }
-    }
-    // Items: each shape group, split into sub-batches that fit kGroupBudget.
-    std::vector<Item> all;
-    for (size_t g = 0; g < groups.size(); ++g) {
-        const Dims d = dims_of(groups[g].m, groups[g].n, k, *hp);
-        const int cnt = (int)groups[g].idx.size();
-        Item one;
-        one.g = (int)g;
-        one.count = 1;
-        one.d = d;
-        one.gns = gram_space_ns(variant, d, *hp);
-        const size_t per = round_bytes({one}, variant, source_x);
-        const int b = (int)std::max<size_t>(1, std::min<size_t>((size_t)cnt, kGroupBudget / std::max<size_t>(per, 1)));
-        for (int first = 0; first < cnt; first += b) {
-            Item it;
-            it.g = (int)g;
-            it.first = first;
-            it.count = std::min(b, cnt - first);
-            it.d = d;
-            it.gns = one.gns;
-            all.push_back(it);
-        }
-    }
-    // Rounds: consecutive items whose phases run interleaved, with their
-    // small matrices pooled; the workspace is the largest round.
-    std::vector<std::vector<Item>> rounds;
-    size_t need = 0;
-    for (const Item& it : all) {
-        if (!rounds.empty()) {
-            std::vector<Item> trial = rounds.back();
-            trial.push_back(it);
-            const size_t bytes = round_bytes(trial, variant, source_x);
-            if (bytes <= kRoundBudget) {
-                rounds.back().push_back(it);
-                need = std::max(need, bytes);
-                continue;
-            }
-        }
-        rounds.push_back({it});
-        need = std::max(need, round_bytes(rounds.back(), variant, source_x));
-    }
-    rc = ensure_workspace(ctx, need, s);
+    Plan plan = plan_step(variant, num_mats, shapes, *hp, k, kGroupBudget, kRoundBudget);
+    if (plan.need > ctx->ws_bytes && ctx->reserved)
+        return set_err(ctx, NORMPRE_ERR_UNSUPPORTED,
+                       fmt("the step needs %zu workspace bytes, %zu are reserved (normpre_reserve)", plan.need,
+                           ctx->ws_bytes));
+    rc = ensure_workspace(ctx, plan.need, s);
     if (rc) return rc;
     const bool debug = (hp->flags & NORMPRE_FLAG_DEBUG) != 0;
     if (debug) {
         rc = prepare_debug(ctx, num_mats, shapes, variant, k, *hp, s);
         if (rc) return rc;
     }
-    ctx->dbg_valid = false;
-    ctx->timing = (hp->flags & NORMPRE_FLAG_TIME_KERNELS) != 0;
-    ctx->stream = s;
+    rc = order_after_last(ctx, s);
+    if (rc) return rc;
+    return run_plan(ctx, variant, plan, params, grads, momentum, hp, s, ctx->ws, ctx->ws_bytes, debug);
+}
 
-    StepCtx sc{ctx, s, hp, params, grads, momentum, variant, debug, &groups};
-    for (std::vector<Item>& items : rounds) {
-        std::vector<Pool> pools = make_pools(items, variant);
-        Arena ar{static_cast<char*>(ctx->ws), 0, ctx->ws_bytes};
-        carve_round(ar, items, pools, variant, source_x);
-        DebugMat* dbg = debug ? ctx->dbg.data() : nullptr;
-        rc = variant == NORMPRE_VARIANT_L ? run_round_l(sc, items, pools, dbg) : run_round_g(sc, items, pools, dbg);
+int normpre_workspace_size(int variant, int num_mats, const int64_t* shapes, const normpre_hparams* hp,
+                           int64_t* bytes) {
+    if (!bytes) return set_err(nullptr, NORMPRE_ERR_INVALID_ARG, "bytes is null");
+    *bytes = 0;
+    Fail f = validate(variant, num_mats, shapes, hp);
+    if (f.code) return set_err(nullptr, f.code, f.msg);
+    if (num_mats > 0) *bytes = (int64_t)workspace_need(variant, num_mats, shapes, *hp);
+    return NORMPRE_OK;
+}
+
+int normpre_reserve(normpre_ctx* ctx, int variant, int num_mats, const int64_t* shapes, const normpre_hparams* hp,
+                    void* stream) {
+    if (!ctx) return set_err(nullptr, NORMPRE_ERR_NOT_INITIALIZED, "context is null");
+    ctx->err.clear();
+    Fail f = validate(variant, num_mats, shapes, hp);
+    if (f.code) return set_err(ctx, f.code, f.msg);
+    hipError_t e = hipSetDevice(ctx->device);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+    const size_t need = num_mats > 0 ? workspace_need(variant, num_mats, shapes, *hp) : 0;
+    if (need > ctx->ws_bytes) {
+        int rc = ensure_workspace(ctx, need, static_cast<hipStream_t>(stream));
         if (rc) return rc;
     }
-    ctx->last_stream = s;
-    ctx->have_stream = true;
-    if (debug) {
-        ctx->dbg_valid = true;
-        ctx->dbg_stream = s;
-    }
+    ctx->reserved = true;
+    return NORMPRE_OK;
+}
+
+int normpre_workspace_bytes(const normpre_ctx* ctx, int64_t* bytes) {
+    if (!ctx) return set_err(nullptr, NORMPRE_ERR_NOT_INITIALIZED, "context is null");
+    if (!bytes) return NORMPRE_ERR_INVALID_ARG;
+    *bytes = (int64_t)ctx->ws_bytes;
     return NORMPRE_OK;
 }
 
@@ -1922,6 +2047,8 @@ int normpre_spectrum(normpre_ctx* ctx, int which, int64_t rows, int64_t cols, co
     Arena probe{nullptr, 0, 0};
     int rc = ensure_workspace(ctx, carve(probe, mcopy), s);
     if (rc) return rc;
+    rc = order_after_last(ctx, s);
+    if (rc) return rc;
     Arena ar{static_cast<char*>(ctx->ws), 0, ctx->ws_bytes};
     carve(ar, mcopy);
     ctx->timing = false;
@@ -1950,6 +2077,61 @@ int normpre_spectrum(normpre_ctx* ctx, int which, int64_t rows, int64_t cols, co
     NP_TRY(launch_tri_eigvals(it.w.tw, (int)a, 0, (int)a, it.w.lam, a, 1, s), "bisection");
     NP_TRY(hipMemcpyAsync(eigs, it.w.lam, (size_t)a * sizeof(double), hipMemcpyDeviceToHost, s), "copy eigenvalues");
     NP_TRY(hipStreamSynchronize(s), "hipStreamSynchronize");
+    ctx->last_stream = s;
+    ctx->have_stream = true;
+    return NORMPRE_OK;
+}
+
+int normpre_descent_alignment(normpre_ctx* ctx, int num_mats, const float* const* grads,
+                              const float* const* w_before, const float* const* w_after, const int64_t* shapes,
+                              float lr, float weight_decay, double* cosines, double* mean, void* stream) {
+    if (!ctx) return set_err(nullptr, NORMPRE_ERR_NOT_INITIALIZED, "context is null");
+    ctx->err.clear();
+    if (num_mats < 0) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "num_mats < 0");
+    if (!mean) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "mean is null");
+    if (!(lr > 0.f) || !std::isfinite(lr) || !std::isfinite(weight_decay))
+        return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "lr must be finite and > 0, weight_decay finite");
+    *mean = 0.0;
+    if (num_mats == 0) return NORMPRE_OK;
+    if (!grads || !w_before || !w_after || !shapes || !cosines)
+        return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "null pointer argument");
+    for (int i = 0; i < num_mats; ++i) {
+        if (!grads[i] || !w_before[i] || !w_after[i])
+            return set_err(ctx, NORMPRE_ERR_INVALID_ARG, fmt("matrix %d has a null pointer", i));
+        if (shapes[2 * i] < 1 || shapes[2 * i + 1] < 1 || shapes[2 * i] > kMaxDim || shapes[2 * i + 1] > kMaxDim)
+            return set_err(ctx, NORMPRE_ERR_INVALID_ARG, fmt("matrix %d has a bad shape", i));
+    }
+    hipError_t e = hipSetDevice(ctx->device);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const size_t part_n = (size_t)num_mats * kAlignBlocks * 3;
+    const size_t need = (part_n + num_mats + 1) * sizeof(double) + 256;
+    int rc = ensure_workspace(ctx, need, s);
+    if (rc) return rc;
+    rc = order_after_last(ctx, s);
+    if (rc) return rc;
+    double* part = static_cast<double*>(ctx->ws);
+    double* cos_dev = part + part_n;
+    double* mean_dev = cos_dev + num_mats;
+    for (int c0 = 0; c0 < num_mats; c0 += kChunk) {
+        const int cnt = std::min(kChunk, num_mats - c0);
+        AlignChunk ch{};
+        for (int i = 0; i < cnt; ++i) {
+            ch.g[i] = grads[c0 + i];
+            ch.wb[i] = w_before[c0 + i];
+            ch.wa[i] = w_after[c0 + i];
+            ch.n[i] = shapes[2 * (c0 + i)] * shapes[2 * (c0 + i) + 1];
+        }
+        e = launch_alignment_partials(ch, cnt, (double)lr, (double)weight_decay,
+                                      part + (size_t)c0 * kAlignBlocks * 3, s);
+        if (e != hipSuccess) return hip_fail(ctx, e, "alignment partials");
+    }
+    e = launch_alignment_finalize(part, num_mats, cos_dev, mean_dev, s);
+    if (e != hipSuccess) return hip_fail(ctx, e, "alignment finalize");
+    e = hipMemcpyAsync(cosines, cos_dev, sizeof(double) * num_mats, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(mean, mean_dev, sizeof(double), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(ctx, e, "alignment copy");
     ctx->last_stream = s;
     ctx->have_stream = true;
     return NORMPRE_OK;
@@ -2032,7 +2214,7 @@ int normpre_sketch_omega(uint64_t seed, int64_t step, int32_t matrix_id, int64_t
 }
 
 int normpre_kernel_stats(normpre_ctx* ctx, int kclass, int64_t* launches, double* device_ms, double* flops,
-                         double* bytes, int reset) {
+                         double* exec_flops, double* bytes, int reset) {
     if (!ctx) return set_err(nullptr, NORMPRE_ERR_NOT_INITIALIZED, "context is null");
     if (kclass < 0 || kclass >= NORMPRE_KCLASS_COUNT) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "kclass out of range");
     int rc = collect_events(ctx);
@@ -2041,6 +2223,7 @@ int normpre_kernel_stats(normpre_ctx* ctx, int kclass, int64_t* launches, double
     if (launches) *launches = s.launches;
     if (device_ms) *device_ms = s.ms;
     if (flops) *flops = s.flops;
+    if (exec_flops) *exec_flops = s.exec_flops;
     if (bytes) *bytes = s.bytes;
     if (reset) ctx->stats[kclass] = KStat{};
     return NORMPRE_OK;

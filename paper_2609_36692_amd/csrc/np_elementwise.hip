@@ -6,13 +6,18 @@
 //   * the NormPre-G RMS-matched weight update (Sec. 3.1, "Consistent
 //     Update RMS", and the last line of Alg. 1).
 //
-// Row statistics use one fp64 pass: with x = m - c w,
-//   ||x||^2 = ||m||^2 - 2 c <m, w> + c^2 ||w||^2,
-// so the row (or column) is read once for the three sums and Psi is written
-// from values still held in registers (row-active case) or from a second,
-// cache-friendly pass (column-active case).  c = <m, w> is the relaxed
-// tangent of Sec. 3.1; the ablation modes of App. A.4 use c = 0 (no tangent)
-// or c = <m, w> / ||w||^2 (strict tangent projection).
+// x = m - c w with c = <m, w> (the relaxed tangent of Sec. 3.1; the ablation
+// modes of App. A.4 use c = 0, no tangent, or c = <m, w> / ||w||^2, the strict
+// tangent projection) is formed in fp64 from the fp32 values, so a nearly
+// radial momentum (m close to a multiple of w) loses no accuracy beyond the
+// fp32 rounding of the stored M.  Row-active: the row stays in registers;
+// one pass gives <m, w> and ||w||^2, a second one ||x||^2 from the formed x,
+// a third writes Psi.  Column-active: one streaming pass gives ||m||^2,
+// <m, w>, ||w||^2 per column (fp64), ||x||^2 follows from
+//   ||x||^2 = ||m||^2 - 2 c <m, w> + c^2 ||w||^2
+// (relative error about u64 K ||m||^2 / ||x||^2 for K summed terms, far
+// below the fp32 rounding of M unless ||x|| < 1e-6 ||m||), and a second,
+// cache-friendly pass writes Psi.
 //
 // Also the input of the Muon reference step (Sec. 2.1): momentum update with
 // per-block sums of M^2, then X0 = M / (||M||_F + eps) cast to fp16.
@@ -39,20 +44,35 @@ __device__ __forceinline__ double tangent_coef(int mode, double smw, double sww)
     return smw;
 }
 
-// Block-wide sum of three doubles; result valid in every thread.
+// Block-wide sums (fixed order); results valid in every thread.  The two
+// helpers own separate LDS arrays, so one may follow the other without a
+// barrier in between.
 template <int NT>
-__device__ __forceinline__ void block_sum3(double& a, double& b, double& c) {
-    __shared__ double red[3][NT / 64];
+__device__ __forceinline__ void block_sum2(double& a, double& b) {
+    __shared__ double red2[2][NT / 64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     a = wave_sum_d(a);
     b = wave_sum_d(b);
-    c = wave_sum_d(c);
-    if (lane == 0) { red[0][wave] = a; red[1][wave] = b; red[2][wave] = c; }
+    if (lane == 0) { red2[0][wave] = a; red2[1][wave] = b; }
     __syncthreads();
-    a = b = c = 0.0;
+    a = b = 0.0;
 #pragma unroll
-    for (int w = 0; w < NT / 64; ++w) { a += red[0][w]; b += red[1][w]; c += red[2][w]; }
+    for (int w = 0; w < NT / 64; ++w) { a += red2[0][w]; b += red2[1][w]; }
 }
+template <int NT>
+__device__ __forceinline__ void block_sum1(double& a) {
+    __shared__ double red1[NT / 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    a = wave_sum_d(a);
+    if (lane == 0) red1[wave] = a;
+    __syncthreads();
+    a = 0.0;
+#pragma unroll
+    for (int w = 0; w < NT / 64; ++w) a += red1[w];
+}
+
+// x = m - c w in fp64.
+__device__ __forceinline__ double tangent_x(float m, float w, double c) { return fma(-c, (double)w, (double)m); }
 
 // ---------------------------------------------------------------------------
 // Row-active orientation: one block per row of W; the row of M and W stays in
@@ -71,7 +91,7 @@ __global__ void __launch_bounds__(NT) normalize_rows_kernel(NormArgs a) {
     float* M = a.ptrs.m[z] + off;
     const float* G = a.ptrs.g[z] + off;
     float mv[NV][VW], wv[NV][VW];
-    double smm = 0.0, smw = 0.0, sww = 0.0;
+    double smw = 0.0, sww = 0.0;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
         const int idx = (v * NT + tid) * VW;
@@ -95,25 +115,36 @@ __global__ void __launch_bounds__(NT) normalize_rows_kernel(NormArgs a) {
 #pragma unroll
             for (int e = 0; e < VW; ++e) {
                 const double md = mv[v][e], wd = wv[v][e];
-                smm = fma(md, md, smm);
                 smw = fma(md, wd, smw);
                 sww = fma(wd, wd, sww);
             }
         }
     }
-    block_sum3<NT>(smm, smw, sww);
+    block_sum2<NT>(smw, sww);
     const double d = tangent_coef(a.tangent, smw, sww);
-    const double nrm2 = fmax(smm - 2.0 * d * smw + d * d * sww, 0.0);
-    const double nrm = sqrt(nrm2);
-    const float inv = (float)(1.0 / fmax(nrm, (double)a.eps));
-    const float df = (float)d;
+    // x replaces m in the registers (rounded to fp32 after it is formed, so
+    // its relative error is u32 whatever the cancellation was).
+    double nrm2 = 0.0;
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+        if ((v * NT + tid) * VW < a.cols) {
+#pragma unroll
+            for (int e = 0; e < VW; ++e) {
+                const double x = tangent_x(mv[v][e], wv[v][e], d);
+                nrm2 = fma(x, x, nrm2);
+                mv[v][e] = (float)x;
+            }
+        }
+    block_sum1<NT>(nrm2);
+    const double inv = 1.0 / fmax(sqrt(nrm2), (double)a.eps);
+    const float invf = (float)inv;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
         const int idx = (v * NT + tid) * VW;
         if (idx < a.cols) {
             float p[VW];
 #pragma unroll
-            for (int e = 0; e < VW; ++e) p[e] = (mv[v][e] - df * wv[v][e]) * inv;
+            for (int e = 0; e < VW; ++e) p[e] = mv[v][e] * invf;
             if constexpr (VW == 4) {
                 half_t h[4] = {(half_t)p[0], (half_t)p[1], (half_t)p[2], (half_t)p[3]};
                 *reinterpret_cast<uint2*>(prow + idx) = *reinterpret_cast<const uint2*>(h);
@@ -128,7 +159,7 @@ __global__ void __launch_bounds__(NT) normalize_rows_kernel(NormArgs a) {
     }
     for (int64_t j = a.cols + tid; j < a.ld_psi; j += NT) prow[j] = (half_t)0.f;
     if (tid == 0) {
-        a.psisq[(int64_t)z * a.stride_psisq + row] = (float)(nrm2 * (double)inv * (double)inv);
+        a.psisq[(int64_t)z * a.stride_psisq + row] = (float)(nrm2 * inv * inv);
         if (a.xsq) a.xsq[(int64_t)z * a.stride_psisq + row] = (float)nrm2;
     }
 }
@@ -153,7 +184,7 @@ __global__ void __launch_bounds__(256) normalize_rows_wave_kernel(NormArgs a) {
     float* M = a.ptrs.m[z] + off;
     const float* G = a.ptrs.g[z] + off;
     float mv[NV][VW], wv[NV][VW];
-    double smm = 0.0, smw = 0.0, sww = 0.0;
+    double smw = 0.0, sww = 0.0;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
         const int idx = (v * 64 + lane) * VW;
@@ -177,26 +208,37 @@ __global__ void __launch_bounds__(256) normalize_rows_wave_kernel(NormArgs a) {
 #pragma unroll
             for (int e = 0; e < VW; ++e) {
                 const double md = mv[v][e], wd = wv[v][e];
-                smm = fma(md, md, smm);
                 smw = fma(md, wd, smw);
                 sww = fma(wd, wd, sww);
             }
         }
     }
-    smm = wave_sum_d(smm);
     smw = wave_sum_d(smw);
     sww = wave_sum_d(sww);
     const double d = tangent_coef(a.tangent, smw, sww);
-    const double nrm2 = fmax(smm - 2.0 * d * smw + d * d * sww, 0.0);
-    const float inv = (float)(1.0 / fmax(sqrt(nrm2), (double)a.eps));
-    const float df = (float)d;
+    // x replaces m in the registers (rounded to fp32 after it is formed, so
+    // its relative error is u32 whatever the cancellation was).
+    double nrm2 = 0.0;
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+        if ((v * 64 + lane) * VW < a.cols) {
+#pragma unroll
+            for (int e = 0; e < VW; ++e) {
+                const double x = tangent_x(mv[v][e], wv[v][e], d);
+                nrm2 = fma(x, x, nrm2);
+                mv[v][e] = (float)x;
+            }
+        }
+    nrm2 = wave_sum_d(nrm2);
+    const double inv = 1.0 / fmax(sqrt(nrm2), (double)a.eps);
+    const float invf = (float)inv;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
         const int idx = (v * 64 + lane) * VW;
         if (idx < a.cols) {
             float p[VW];
 #pragma unroll
-            for (int e = 0; e < VW; ++e) p[e] = (mv[v][e] - df * wv[v][e]) * inv;
+            for (int e = 0; e < VW; ++e) p[e] = mv[v][e] * invf;
             if constexpr (VW == 4) {
                 half_t h[4] = {(half_t)p[0], (half_t)p[1], (half_t)p[2], (half_t)p[3]};
                 *reinterpret_cast<uint2*>(prow + idx) = *reinterpret_cast<const uint2*>(h);
@@ -217,7 +259,7 @@ __global__ void __launch_bounds__(256) normalize_rows_wave_kernel(NormArgs a) {
         for (int64_t j = a.cols + lane; j < a.ld_psi; j += 64) prow[j] = (half_t)0.f;
     }
     if (lane == 0) {
-        a.psisq[(int64_t)z * a.stride_psisq + row] = (float)(nrm2 * (double)inv * (double)inv);
+        a.psisq[(int64_t)z * a.stride_psisq + row] = (float)(nrm2 * inv * inv);
         if (a.xsq) a.xsq[(int64_t)z * a.stride_psisq + row] = (float)nrm2;
     }
 }
@@ -353,13 +395,13 @@ __global__ void __launch_bounds__(kColThreads) normalize_cols_apply(NormArgs a, 
     half_t* P = a.psi + (int64_t)z * a.stride_psi;
     const int r0 = chunk * row_chunk, r1 = min((int)a.rows_pad, r0 + row_chunk);
     if (col0 >= cols_pad) return;
-    float df[VW], inv[VW];
+    double df[VW], inv[VW];
     const double* p = partials + (int64_t)z * nchunks * 3 * cols_pad;
 #pragma unroll
     for (int e = 0; e < VW; ++e) {
         const int col = col0 + e;
-        df[e] = col < a.cols ? (float)p[col] : 0.f;
-        inv[e] = col < a.cols ? (float)p[cols_pad + col] : 0.f;
+        df[e] = col < a.cols ? p[col] : 0.0;
+        inv[e] = col < a.cols ? p[cols_pad + col] : 0.0;
     }
     const float* W = a.ptrs.w[z];
     const float* M = a.ptrs.m[z];
@@ -371,10 +413,10 @@ __global__ void __launch_bounds__(kColThreads) normalize_cols_apply(NormArgs a, 
                 const int64_t o = (int64_t)i * a.cols + col0;
                 const float4 m = *reinterpret_cast<const float4*>(M + o);
                 const float4 w = *reinterpret_cast<const float4*>(W + o);
-                v[0] = (m.x - df[0] * w.x) * inv[0];
-                v[1] = (m.y - df[1] * w.y) * inv[1];
-                v[2] = (m.z - df[2] * w.z) * inv[2];
-                v[3] = (m.w - df[3] * w.w) * inv[3];
+                v[0] = (float)(tangent_x(m.x, w.x, df[0]) * inv[0]);
+                v[1] = (float)(tangent_x(m.y, w.y, df[1]) * inv[1]);
+                v[2] = (float)(tangent_x(m.z, w.z, df[2]) * inv[2]);
+                v[3] = (float)(tangent_x(m.w, w.w, df[3]) * inv[3]);
                 if constexpr (DBG)
                     *reinterpret_cast<float4*>(a.psi32 + (int64_t)z * a.stride_psi32 + o) = make_float4(v[0], v[1], v[2], v[3]);
             }
@@ -384,7 +426,7 @@ __global__ void __launch_bounds__(kColThreads) normalize_cols_apply(NormArgs a, 
             float v = 0.f;
             if (i < a.rows && col0 < a.cols) {
                 const int64_t o = (int64_t)i * a.cols + col0;
-                v = (M[o] - df[0] * W[o]) * inv[0];
+                v = (float)(tangent_x(M[o], W[o], df[0]) * inv[0]);
                 if constexpr (DBG) a.psi32[(int64_t)z * a.stride_psi32 + o] = v;
             }
             prow[0] = (half_t)v;
@@ -549,6 +591,59 @@ __global__ void __launch_bounds__(256) add_diag_kernel(half_t* q, int64_t sp, in
 __global__ void fill_zero_kernel(uint4* p, int64_t n16) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (int64_t)gridDim.x * blockDim.x)
         p[i] = make_uint4(0, 0, 0, 0);
+}
+
+// Descent alignment, pass 1: block b of matrix z sums g phi, g^2 and phi^2
+// over a grid-stride slice (fp64), phi = (wb - wa) / lr - wd wb.
+__global__ void __launch_bounds__(256) alignment_partials_kernel(AlignChunk c, double inv_lr, double wd,
+                                                                 double* part) {
+    const int z = blockIdx.y;
+    const float* g = c.g[z];
+    const float* wb = c.wb[z];
+    const float* wa = c.wa[z];
+    const int64_t n = c.n[z];
+    double sgp = 0.0, sgg = 0.0, spp = 0.0;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+        const double b = wb[i], gv = g[i];
+        const double phi = (b - (double)wa[i]) * inv_lr - wd * b;
+        sgp = fma(gv, phi, sgp);
+        sgg = fma(gv, gv, sgg);
+        spp = fma(phi, phi, spp);
+    }
+    sgp = wave_sum_d(sgp);
+    sgg = wave_sum_d(sgg);
+    spp = wave_sum_d(spp);
+    __shared__ double red[3][4];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) { red[0][wave] = sgp; red[1][wave] = sgg; red[2][wave] = spp; }
+    __syncthreads();
+    if (threadIdx.x < 3) {
+        const int q = threadIdx.x;
+        part[((int64_t)z * kAlignBlocks + blockIdx.x) * 3 + q] = red[q][0] + red[q][1] + red[q][2] + red[q][3];
+    }
+}
+
+// Pass 2 (one block): cos[z] from the partials of matrix z in block order;
+// the mean of the cosines in matrix order.
+__global__ void __launch_bounds__(256) alignment_finalize_kernel(const double* part, int num_mats, double* cos_out,
+                                                                 double* mean_out) {
+    for (int z = threadIdx.x; z < num_mats; z += 256) {
+        double sgp = 0.0, sgg = 0.0, spp = 0.0;
+        for (int b = 0; b < kAlignBlocks; ++b) {
+            const double* p = part + ((int64_t)z * kAlignBlocks + b) * 3;
+            sgp += p[0];
+            sgg += p[1];
+            spp += p[2];
+        }
+        const double den = sqrt(sgg) * sqrt(spp);
+        cos_out[z] = den > 0.0 ? sgp / den : 0.0;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double m = 0.0;
+        for (int z = 0; z < num_mats; ++z) m += cos_out[z];
+        *mean_out = num_mats > 0 ? m / num_mats : 0.0;
+    }
 }
 
 template <int NT, int VW, int NV>
@@ -795,6 +890,19 @@ hipError_t launch_add_diag(half_t* q, int64_t sp, int count, float a, hipStream_
     if (count < 1 || sp < 1) return hipErrorInvalidValue;
     const int64_t n = (int64_t)count * sp;
     hipLaunchKernelGGL(add_diag_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, q, sp, n, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_alignment_partials(const AlignChunk& c, int cnt, double lr, double wd, double* part,
+                                     hipStream_t s) {
+    if (cnt < 1 || cnt > kChunk || !(lr > 0.0)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(alignment_partials_kernel, dim3(kAlignBlocks, cnt), dim3(256), 0, s, c, 1.0 / lr, wd, part);
+    return hipGetLastError();
+}
+
+hipError_t launch_alignment_finalize(const double* part, int num_mats, double* cos_out, double* mean_out,
+                                     hipStream_t s) {
+    hipLaunchKernelGGL(alignment_finalize_kernel, dim3(1), dim3(256), 0, s, part, num_mats, cos_out, mean_out);
     return hipGetLastError();
 }
 

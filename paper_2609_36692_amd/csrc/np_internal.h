@@ -337,6 +337,23 @@ struct EigArgs {
 hipError_t launch_eig_select(const EigArgs& a, int batch, hipStream_t s);
 
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t s);
+
+// Descent alignment (App. A, training dynamics): per matrix the cosine of the
+// gradient G and the update direction Phi = (W_before - W_after) / lr -
+// wd W_before (the update before learning-rate scaling, weight decay
+// excluded).  Partial sums per block (fp64), then one block reduces them in
+// a fixed order to cos[z] and their mean.
+struct AlignChunk {
+    const float* g[kChunk];
+    const float* wb[kChunk];
+    const float* wa[kChunk];
+    int64_t n[kChunk];
+};
+constexpr int kAlignBlocks = 128;
+hipError_t launch_alignment_partials(const AlignChunk& c, int cnt, double lr, double wd, double* part,
+                                     hipStream_t s);
+hipError_t launch_alignment_finalize(const double* part, int num_mats, double* cos_out, double* mean_out,
+                                     hipStream_t s);
 // Q <- Q + a I in place for `count` contiguous sp x sp fp16 matrices.
 hipError_t launch_add_diag(half_t* q, int64_t sp, int count, float a, hipStream_t s);
 

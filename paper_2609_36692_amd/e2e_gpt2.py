@@ -80,11 +80,14 @@ def main(argv=None):
         torch.cuda.synchronize()
         t2 = time.perf_counter()
         if last:
-            cos = []
-            for p, (w0, g) in zip(hidden, before):
-                phi = (w0 - p.detach()) / a.lr - a.weight_decay * w0
-                cos.append(float(torch.sum(g * phi) / (torch.linalg.norm(g) * torch.linalg.norm(phi) + 1e-30)))
-            align = sum(cos) / len(cos)
+            # App. A descent alignment, computed by the library's kernels.
+            from . import normpre as N
+            actx = N.normpre_init(dev.index or 0)
+            try:
+                _, align = N.normpre_descent_alignment(actx, [b[1] for b in before], [b[0] for b in before],
+                                                       [p.detach() for p in hidden], a.lr, a.weight_decay)
+            finally:
+                N.normpre_destroy(actx)
         opt.zero_grad(set_to_none=True)
         if it >= a.warmup:
             fb_ms.append(1e3 * (t1 - t0))

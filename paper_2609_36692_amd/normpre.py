@@ -118,12 +118,19 @@ def load_library(path: str = LIB_PATH):
                                                 ctypes.c_int32, P, P]),
         "normpre_kernel_stats": (ctypes.c_int, [P, ctypes.c_int, i64p, ctypes.POINTER(ctypes.c_double),
                                                 ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
-                                                ctypes.c_int]),
+                                                ctypes.POINTER(ctypes.c_double), ctypes.c_int]),
         "normpre_version": (ctypes.c_char_p, []),
         "normpre_spectrum": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int64, ctypes.c_int64, P, P, hpp,
                                             ctypes.POINTER(ctypes.c_double), P]),
         "normpre_energy_split": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.c_int64, ctypes.c_int32,
                                                 ctypes.POINTER(ctypes.c_double)]),
+        "normpre_descent_alignment": (ctypes.c_int, [P, ctypes.c_int, ctypes.POINTER(P), ctypes.POINTER(P),
+                                                     ctypes.POINTER(P), i64p, ctypes.c_float, ctypes.c_float,
+                                                     ctypes.POINTER(ctypes.c_double),
+                                                     ctypes.POINTER(ctypes.c_double), P]),
+        "normpre_workspace_size": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, i64p, hpp, i64p]),
+        "normpre_reserve": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int, i64p, hpp, P]),
+        "normpre_workspace_bytes": (ctypes.c_int, [P, i64p]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -199,9 +206,7 @@ def normpre_validate(variant: int, shapes, hp: normpre_hparams):
     return code, buf.value.decode()
 
 
-def normpre_step(ctx, variant: int, params, grads, momentum, hp: normpre_hparams, stream=None,
-                 shapes=None) -> None:
-    """One NormPre step on lists of fp32 device tensors (or raw pointers + shapes)."""
+def _step_args(params, grads, momentum, shapes):
     n = len(params)
     if shapes is None:
         shapes = [tuple(p.shape) for p in params]
@@ -209,9 +214,35 @@ def normpre_step(ctx, variant: int, params, grads, momentum, hp: normpre_hparams
     pw = (P * max(1, n))(*[_ptr(x) for x in params])
     pg = (P * max(1, n))(*[_ptr(x) for x in grads])
     pm = (P * max(1, n))(*[_ptr(x) for x in momentum])
-    code = load_library().normpre_step(ctx, int(variant), n, pw, pg, pm, _shapes_array(shapes),
-                                       ctypes.byref(hp), _stream_handle(stream))
+    return n, pw, pg, pm, _shapes_array(shapes)
+
+
+def normpre_step(ctx, variant: int, params, grads, momentum, hp: normpre_hparams, stream=None,
+                 shapes=None) -> None:
+    """One NormPre step on lists of fp32 device tensors (or raw pointers + shapes)."""
+    n, pw, pg, pm, sh = _step_args(params, grads, momentum, shapes)
+    code = load_library().normpre_step(ctx, int(variant), n, pw, pg, pm, sh, ctypes.byref(hp),
+                                       _stream_handle(stream))
     _check(code, ctx)
+
+
+def normpre_workspace_size(variant: int, shapes, hp: normpre_hparams) -> int:
+    out = ctypes.c_int64()
+    _check(load_library().normpre_workspace_size(int(variant), len(shapes), _shapes_array(shapes),
+                                                 ctypes.byref(hp), ctypes.byref(out)))
+    return out.value
+
+
+def normpre_reserve(ctx, variant: int, shapes, hp: normpre_hparams, stream=None) -> None:
+    code = load_library().normpre_reserve(ctx, int(variant), len(shapes), _shapes_array(shapes), ctypes.byref(hp),
+                                          _stream_handle(stream))
+    _check(code, ctx)
+
+
+def normpre_workspace_bytes(ctx) -> int:
+    out = ctypes.c_int64()
+    _check(load_library().normpre_workspace_bytes(ctx, ctypes.byref(out)), ctx)
+    return out.value
 
 
 def normpre_debug_fetch(ctx, index: int, what: int, count: int, dtype=np.float32) -> np.ndarray:
@@ -231,11 +262,13 @@ def normpre_sketch_omega(seed: int, step: int, matrix_id: int, b: int, ell: int,
 
 def normpre_kernel_stats(ctx, kclass: int, reset: bool = False) -> dict:
     launches = ctypes.c_int64()
-    ms, flops, nbytes = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    ms, flops, xflops, nbytes = ctypes.c_double(), ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
     code = load_library().normpre_kernel_stats(ctx, int(kclass), ctypes.byref(launches), ctypes.byref(ms),
-                                               ctypes.byref(flops), ctypes.byref(nbytes), int(bool(reset)))
+                                               ctypes.byref(flops), ctypes.byref(xflops), ctypes.byref(nbytes),
+                                               int(bool(reset)))
     _check(code, ctx)
-    return {"launches": launches.value, "ms": ms.value, "flops": flops.value, "bytes": nbytes.value}
+    return {"launches": launches.value, "ms": ms.value, "flops": flops.value, "exec_flops": xflops.value,
+            "bytes": nbytes.value}
 
 
 def normpre_spectrum(ctx, which: int, w, m, hp: normpre_hparams, stream=None) -> np.ndarray:
@@ -251,6 +284,25 @@ def normpre_spectrum(ctx, which: int, w, m, hp: normpre_hparams, stream=None) ->
                                            _stream_handle(stream))
     _check(code, ctx)
     return out
+
+
+def normpre_descent_alignment(ctx, grads, w_before, w_after, lr: float, weight_decay: float, stream=None):
+    """(per-matrix cosines, mean) of App. A's descent alignment; lists of 2-D
+    fp32 device tensors (gradients, weights before and after the step)."""
+    n = len(grads)
+    P = ctypes.c_void_p
+    shapes = [tuple(g.shape) for g in grads]
+    pg = (P * max(1, n))(*[_ptr(x) for x in grads])
+    pb = (P * max(1, n))(*[_ptr(x) for x in w_before])
+    pa = (P * max(1, n))(*[_ptr(x) for x in w_after])
+    cos = np.zeros(max(1, n), dtype=np.float64)
+    mean = ctypes.c_double()
+    code = load_library().normpre_descent_alignment(ctx, n, pg, pb, pa, _shapes_array(shapes), float(lr),
+                                                    float(weight_decay),
+                                                    cos.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                                                    ctypes.byref(mean), _stream_handle(stream))
+    _check(code, ctx)
+    return cos[:n], mean.value
 
 
 def normpre_energy_split(eigs, count: int, rank: int) -> np.ndarray:

@@ -127,7 +127,7 @@ def test_entry_points_reject_null_context(N):
         N.NORMPRE_ERR_NOT_INITIALIZED
     assert "null" in N.normpre_last_error(None)
     assert lib.normpre_debug_fetch(None, 0, 0, None, 0, None) == N.NORMPRE_ERR_NOT_INITIALIZED
-    assert lib.normpre_kernel_stats(None, 0, None, None, None, None, 0) == N.NORMPRE_ERR_NOT_INITIALIZED
+    assert lib.normpre_kernel_stats(None, 0, None, None, None, None, None, 0) == N.NORMPRE_ERR_NOT_INITIALIZED
     assert lib.normpre_init(None, 0) == N.NORMPRE_ERR_INVALID_ARG
     lib.normpre_destroy(None)   # no-op
     assert lib.normpre_sketch_omega(1, 0, 0, 10, 4, None, None) == N.NORMPRE_ERR_INVALID_ARG
@@ -181,3 +181,20 @@ def test_energy_split_host_matches_oracle(N):
                                    atol=1e-13)
     with pytest.raises(N.NormPreError):
         N.normpre_energy_split(lam, -1, 3)
+
+
+def test_workspace_size_is_host_only_and_covers_both_orientations(N):
+    hp = N.normpre_default_hparams()
+    shapes = [(768, 2304), (3072, 768), (768, 768)]
+    g = N.normpre_workspace_size(N.NORMPRE_VARIANT_G, shapes, hp)
+    lv = N.normpre_workspace_size(N.NORMPRE_VARIANT_L, shapes, hp)
+    assert g > 0 and lv > 0
+    # the requirement covers t and t + 1, so it does not depend on t's parity
+    hp.step = 1
+    assert N.normpre_workspace_size(N.NORMPRE_VARIANT_G, shapes, hp) == g
+    # more matrices never need less
+    assert N.normpre_workspace_size(N.NORMPRE_VARIANT_G, shapes * 2, hp) >= g
+    assert N.normpre_workspace_size(N.NORMPRE_VARIANT_G, [], hp) == 0
+    with pytest.raises(N.NormPreError) as ei:
+        N.normpre_workspace_size(N.NORMPRE_VARIANT_G, [(0, 5)], hp)
+    assert ei.value.code == N.NORMPRE_ERR_INVALID_ARG

@@ -21,6 +21,7 @@ torch = pytest.importorskip("torch")
 from oracle import normpre_oracle as O  # noqa: E402
 from paper_2609_36692_amd import normpre as N  # noqa: E402
 from paper_2609_36692_amd import workloads as WL  # noqa: E402
+from parity_util import check_update, record  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -111,7 +112,9 @@ def test_momentum_and_psi(ctx, shape, t):
     ref = oracle(mat, "G", t)
     assert O.relative_fro(res["m"].numpy(), ref["momentum"]) < 1e-6
     psi = N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_PSI, shape[0] * shape[1]).reshape(shape)
-    assert O.relative_fro(psi, ref["psi"]) < TOL_PSI
+    err = O.relative_fro(psi, ref["psi"])
+    record(f"normalize {shape} t={t}", "Psi rel-Frobenius", err, TOL_PSI)
+    assert err < TOL_PSI
     # every active row has unit norm
     axis = 1 if t % 2 == 0 else 0
     assert np.allclose(np.linalg.norm(psi.astype(np.float64), axis=axis), 1.0, atol=1e-5)
@@ -125,9 +128,8 @@ def test_g_step_parity(ctx, shape, t):
     mat = _inputs(shape)
     res = run_step(ctx, "G", [mat], t)[0]
     ref = oracle(mat, "G", t)
-    err = O.relative_fro(res["u"], ref["update"])
+    err = check_update(f"G {shape} t={t}", res["u"], ref["update"], TOL_G)
     _say(f"   update err {err:.3e}")
-    assert err < TOL_G
     tg = N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_T, shape[0] * shape[1]).reshape(shape)
     assert O.relative_fro(tg, ref["t"] / np.linalg.norm(ref["t"]) * np.linalg.norm(tg)) < TOL_G
     assert math.isclose(np.linalg.norm(res["u"]), 0.2 * math.sqrt(shape[0] * shape[1]), rel_tol=1e-3)
@@ -146,9 +148,8 @@ def test_g_step_parity_gram_space_switch(ctx, shape, t):
     mat = _inputs(shape, seed=5)
     res = run_step(ctx, "G", [mat], t)[0]
     ref = oracle(mat, "G", t)
-    err = O.relative_fro(res["u"], ref["update"])
+    err = check_update(f"G Gram-space switch {shape} t={t}", res["u"], ref["update"], TOL_G)
     _say(f"   update err {err:.3e}")
-    assert err < TOL_G
     assert math.isclose(np.linalg.norm(res["u"]), 0.2 * math.sqrt(shape[0] * shape[1]), rel_tol=1e-3)
 
 
@@ -185,7 +186,8 @@ def test_l_step_parity(ctx, shape, rank, t):
     # The lambda > 1 threshold is continuous (the factor lambda^-1/2 -> 1), so a
     # Ritz value within the Ritz tolerance of 1 may fall on either side.
     assert int(np.sum(lam > 1 + delta)) <= nsel <= int(np.sum(lam > 1 - delta))
-    assert err < tol
+    record(f"L {shape} r={rank} t={t}", "Ritz values (abs)", float(np.max(np.abs(ritz - lam))), delta)
+    check_update(f"L {shape} r={rank} t={t}", res["u"], ref["update"], tol, kappa_tol=tol)
     assert math.isclose(np.linalg.norm(res["u"]), 0.2 * math.sqrt(shape[0] * shape[1]), rel_tol=2e-3)
 
 
@@ -209,7 +211,7 @@ def test_mixed_shapes_g(ctx):
         res = run_step(ctx, "G", mats, t, debug=False)
         for i, mat in enumerate(mats):
             ref = oracle(mat, "G", t, matrix_id=i)
-            assert O.relative_fro(res[i]["u"], ref["update"]) < TOL_G
+            check_update(f"G mixed shapes #{i} {shapes[i]} t={t}", res[i]["u"], ref["update"], TOL_G)
 
 
 def test_mixed_shapes_and_ids_l(ctx):
@@ -218,7 +220,7 @@ def test_mixed_shapes_and_ids_l(ctx):
     res = run_step(ctx, "L", mats, 1, rank=8)
     for i, mat in enumerate(mats):
         ref = oracle(mat, "L", 1, rank=8, matrix_id=i)
-        assert O.relative_fro(res[i]["u"], ref["update"]) < tol_l(ref)
+        check_update(f"L mixed shapes #{i} t=1", res[i]["u"], ref["update"], tol_l(ref))
 
 
 @pytest.mark.parametrize("variant", ["G", "L"])
@@ -302,9 +304,8 @@ def test_reference_steps(ctx, variant, shape, t):
     psi = N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_PSI, shape[0] * shape[1]).reshape(shape)
     assert O.relative_fro(psi, ref["psi"]) < TOL_PSI
     tol = TOL_G if variant == "MUON" else TOL_NORM
-    err = O.relative_fro(res["u"], ref["update"])
+    err = check_update(f"{variant} {shape} t={t}", res["u"], ref["update"], tol)
     _say(f"  update err {err:.2e} (tol {tol:.1e})")
-    assert err < tol
     if variant == "NORM":
         assert math.isclose(np.linalg.norm(res["u"]), 0.2 * math.sqrt(shape[0] * shape[1]), rel_tol=2e-3)
 
@@ -327,9 +328,8 @@ def test_tangent_modes(ctx, variant, mode, t):
     relaxed = oracle(mat, variant, t)
     assert O.relative_fro(ref["psi"], relaxed["psi"]) > 10 * TOL_PSI
     tol = {"G": TOL_G, "NORM": TOL_NORM}.get(variant) or tol_l(ref)
-    err = O.relative_fro(res["u"], ref["update"])
+    err = check_update(f"{variant} tangent {mode} t={t}", res["u"], ref["update"], tol)
     _say(f"  update err {err:.2e} (tol {tol:.1e})")
-    assert err < tol
 
 
 @pytest.mark.parametrize("variant", ["G", "L", "NORM"])
@@ -349,9 +349,8 @@ def test_both_axes_orientation(ctx, variant, shape, t):
     assert np.allclose(np.linalg.norm(psi.astype(np.float64), axis=0), 1.0, atol=2e-3)
     assert int(N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_ORIENT, 1, np.int32)[0]) == t % 2
     tol = {"G": TOL_G, "NORM": TOL_NORM}.get(variant) or tol_l(ref)
-    err = O.relative_fro(res["u"], ref["update"])
+    err = check_update(f"{variant} both axes {shape} t={t}", res["u"], ref["update"], tol)
     _say(f"  update err {err:.2e} (tol {tol:.1e})")
-    assert err < tol
 
 
 @pytest.mark.parametrize("shape,t,exact", [((257, 513), 0, False), ((257, 513), 1, False), ((768, 2304), 0, False),
@@ -374,9 +373,8 @@ def test_source_x_matches_oracle(ctx, shape, t, exact):
         tol = max(TOL_L, 8.0 * U16 * kappa)
     else:
         tol = tol_l(ref)
-    err = O.relative_fro(res["u"], ref["update"])
+    err = check_update(f"L source X {shape} t={t} exact={exact}", res["u"], ref["update"], tol)
     _say(f"  update err {err:.2e} (tol {tol:.1e})")
-    assert err < tol
 
 
 @pytest.mark.parametrize("variant", ["MUON", "NORM"])
@@ -404,9 +402,8 @@ def test_l_exact_matches_oracle(ctx, shape, t):
     lam_sel = ref["lam_sel"]
     kappa = math.sqrt(float(np.sum(lam_sel))) / max(np.linalg.norm(ref["t"]), 1e-300)
     tol = max(TOL_L, 8.0 * U16 * kappa)
-    err = O.relative_fro(res["u"], ref["update"])
+    err = check_update(f"L exact {shape} t={t}", res["u"], ref["update"], tol, kappa=kappa)
     _say(f"  update err {err:.2e} (tol {tol:.1e}), |C| = {len(lam_sel)}")
-    assert err < tol
     # |C| against the exact spectrum (the lambda = 1 threshold is continuous,
     # so modes within 1e-2 of it may fall either way)
     psi_act = O.orient(ref["psi"], ref["k"])
@@ -451,3 +448,162 @@ def test_spectrum_matches_oracle(ctx, shape, t, which):
     assert math.isclose(got[3], want["global"], rel_tol=1e-2)
     assert math.isclose(got[0], want["top"], rel_tol=1e-2, abs_tol=1e-3 * want["global"])
     assert math.isclose(got[2], want["sub"], rel_tol=2e-2, abs_tol=1e-3 * want["global"])
+
+
+# ------------------------------------------------ nearly radial momentum
+# The relaxed tangent of Sec. 3.1 is built around momentum that is mostly
+# radial: m_i = c w_i + (small tangent part), with ||w_i|| = 1.  Inputs: unit
+# active rows of W, G = 3 W + eps N with N's active rows unit vectors, and
+# M_prev either zero (then M = G exactly in fp32) or another draw of the same
+# form.  The library stores M in fp32 (rounding delta, ||delta|| <= u32 ||m||
+# per row) and forms x = m - <m, w> w from it in fp64, so x carries the
+# projection of delta: relative error up to u32 ||m_i|| / ||x_i||, while the
+# oracle works on the unrounded fp64 M.  Bound per active row of Psi:
+#   1e-4 + 8 u32 ||m_i|| / ||x_i||
+# (with M_prev = 0 the second term has nothing to cover, and the error stays
+# at the fp32 output rounding on the row-active side; the column-active side
+# takes ||x||^2 from fp64 sums, whose cancellation adds about
+# u64 K ||m||^2 / ||x||^2).  The oracle runs with the fp32 value of mu, the
+# one the library receives.
+U32 = 2.0 ** -24
+
+
+def _radial_inputs(shape, k, eps, mprev_kind, seed):
+    g = torch.Generator().manual_seed(seed)
+
+    def unit_active(x):
+        return x / torch.linalg.vector_norm(x, dim=1 if k == 0 else 0, keepdim=True)
+
+    w = unit_active(torch.randn(shape, generator=g))
+    gr = 3.0 * w + eps * unit_active(torch.randn(shape, generator=g))
+    if mprev_kind == "zero":
+        mp = torch.zeros(shape)
+    else:
+        mp = 2.0 * w + eps * unit_active(torch.randn(shape, generator=g))
+    return w.contiguous(), gr.contiguous(), mp.contiguous()
+
+
+RADIAL_SHAPES = [(256, 1024), (257, 513), (64, 5000)]
+
+
+@pytest.mark.parametrize("shape", RADIAL_SHAPES)
+@pytest.mark.parametrize("t", [0, 1])
+@pytest.mark.parametrize("mprev_kind", ["zero", "radial"])
+def test_nearly_radial_momentum(ctx, shape, t, mprev_kind):
+    k = t % 2
+    mu32 = float(np.float32(0.95))
+    for eps in (1e-2, 1e-3, 1e-4, 1e-5):
+        _say(f"radial momentum shape={shape} t={t} M_prev={mprev_kind} eps={eps:g}")
+        mat = _radial_inputs(shape, k, eps, mprev_kind, seed=31 + t)
+        res = run_step(ctx, "G", [mat], t)[0]
+        ref = oracle(mat, "G", t, momentum=mu32)
+        psi = N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_PSI, shape[0] * shape[1]).reshape(shape)
+        p_act = O.orient(psi.astype(np.float64), k)
+        r_act = O.orient(ref["psi"], k)
+        m_act = O.orient(ref["momentum"], k)
+        x_act = O.momentum_processing(m_act, O.orient(mat[0].double().numpy(), k))
+        ratio = np.linalg.norm(m_act, axis=1) / np.linalg.norm(x_act, axis=1)
+        row_err = np.linalg.norm(p_act - r_act, axis=1)
+        bound = 1e-4 + 8.0 * U32 * ratio
+        worst = int(np.argmax(row_err / bound))
+        case = f"radial {shape} t={t} M_prev={mprev_kind} eps={eps:g}"
+        record(case, "Psi worst row", float(row_err[worst]), float(bound[worst]),
+               m_over_x=float(ratio[worst]))
+        _say(f"  worst Psi row error {row_err[worst]:.2e} (bound {bound[worst]:.2e}, ||m||/||x|| {ratio[worst]:.3g})")
+        assert np.all(row_err < bound)
+        check_update(case, res["u"], ref["update"], TOL_G)
+
+
+# ------------------------------------------------ fixed orientation modes
+@pytest.mark.parametrize("variant", ["G", "L"])
+@pytest.mark.parametrize("mode", ["row", "col"])
+@pytest.mark.parametrize("t", [0, 1])
+def test_fixed_orientation(ctx, variant, mode, t):
+    shape = (257, 513)
+    _say(f"orientation {mode} {variant} t={t}")
+    mat = _inputs(shape, "lowrank", seed=17)
+    orient = N.NORMPRE_ORIENT_ROW if mode == "row" else N.NORMPRE_ORIENT_COL
+    res = run_step(ctx, variant, [mat], t, orientation=orient, rank=16)[0]
+    k = 0 if mode == "row" else 1
+    assert int(N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_ORIENT, 1, np.int32)[0]) == k
+    ref = oracle(mat, variant, t, orientation=mode, rank=16)
+    assert ref["k"] == k
+    psi = N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_PSI, shape[0] * shape[1]).reshape(shape)
+    assert O.relative_fro(psi, ref["psi"]) < TOL_PSI
+    assert np.allclose(np.linalg.norm(psi.astype(np.float64), axis=1 - k), 1.0, atol=1e-5)
+    tol = TOL_G if variant == "G" else tol_l(ref)
+    err = check_update(f"{variant} orientation {mode} t={t}", res["u"], ref["update"], tol)
+    _say(f"  update err {err:.2e} (tol {tol:.1e})")
+
+
+# ------------------------------------------------ workspace and streams
+def test_reserve_then_steps_never_grow(ctx):
+    _say("normpre_reserve: steps keep the reserved workspace")
+    c = N.normpre_init(0)
+    try:
+        shapes = [(300, 500), (300, 500), (700, 256), (128, 1100)]
+        mats = [_inputs(sh, seed=40 + i) for i, sh in enumerate(shapes)]
+        hp = N.normpre_default_hparams(lr=1.0, weight_decay=0.0)
+        need = N.normpre_workspace_size(N.NORMPRE_VARIANT_G, shapes, hp)
+        assert N.normpre_workspace_bytes(c) == 0
+        N.normpre_reserve(c, N.NORMPRE_VARIANT_G, shapes, hp)
+        held = N.normpre_workspace_bytes(c)
+        assert held >= need
+        dev = torch.device("cuda:0")
+        Ws = [m[0].to(dev).clone() for m in mats]
+        Gs = [m[1].to(dev).clone() for m in mats]
+        Ms = [m[2].to(dev).clone() for m in mats]
+        for t in range(3):
+            hp.step = t
+            w_before = [w.cpu() for w in Ws]
+            m_before = [m.cpu() for m in Ms]
+            N.normpre_step(c, N.NORMPRE_VARIANT_G, Ws, Gs, Ms, hp)
+            assert N.normpre_workspace_bytes(c) == held
+            torch.cuda.synchronize()
+            for i in range(len(shapes)):
+                w0 = w_before[i].double().numpy()
+                ref = O.normpre_step(w0, mats[i][1].numpy(), m_before[i].numpy(), t,
+                                     O.HParams(lr=1.0, weight_decay=0.0), "G", matrix_id=i)
+                check_update(f"G reserved step t={t} #{i}", w0 - Ws[i].cpu().double().numpy(), ref["update"], TOL_G)
+        # a larger step than reserved is refused and writes nothing
+        big = _inputs((2048, 2048), seed=50)
+        W, G, M = (x.to(dev).clone() for x in big)
+        with pytest.raises(N.NormPreError) as ei:
+            N.normpre_step(c, N.NORMPRE_VARIANT_G, [W], [G], [M], hp)
+        assert ei.value.code == N.NORMPRE_ERR_UNSUPPORTED
+        torch.cuda.synchronize()
+        assert torch.equal(W.cpu(), big[0]) and torch.equal(M.cpu(), big[2])
+        assert N.normpre_workspace_bytes(c) == held
+    finally:
+        N.normpre_destroy(c)
+
+
+@pytest.mark.parametrize("variant", ["G", "L"])
+def test_steps_alternating_streams_match_one_stream(ctx, variant):
+    # Consecutive steps on two streams share the workspace; the library
+    # orders each one after the previous stream's work.
+    _say(f"alternating streams {variant}")
+    mats = [_inputs((640, 900), seed=60 + i) for i in range(3)]
+    dev = torch.device("cuda:0")
+
+    def run(streams):
+        c = N.normpre_init(0)
+        try:
+            Ws = [m[0].to(dev).clone() for m in mats]
+            Gs = [m[1].to(dev).clone() for m in mats]
+            Ms = [m[2].to(dev).clone() for m in mats]
+            torch.cuda.synchronize()
+            for t, s in enumerate(streams):
+                hp = N.normpre_default_hparams(lr=0.5, step=t, rank=16)
+                with torch.cuda.stream(s):
+                    N.normpre_step(c, N.VARIANTS[variant], Ws, Gs, Ms, hp, stream=s)
+            torch.cuda.synchronize()
+            return [w.cpu() for w in Ws]
+        finally:
+            N.normpre_destroy(c)
+
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    one = run([s1] * 4)
+    two = run([s1, s2, s1, s2])
+    for a, b in zip(one, two):
+        assert torch.equal(a, b)

@@ -598,3 +598,29 @@ def test_energy_split_closed_forms(shape, r):
     sv = np.linalg.svd(psi, compute_uv=False)
     assert math.isclose(split["sub"], float(np.sum((sv[(sv > 1e-9) & (sv < 1)] - 1) ** 2)), rel_tol=1e-9)
     assert math.isclose(split["top"] + split["remain"], float(np.sum((sv[sv > 1] - 1) ** 2)), rel_tol=1e-9)
+
+
+# ------------------------------------------------- descent alignment (App. A)
+def test_descent_alignment_closed_forms():
+    g = _rand(20, 30)
+    q = _rand(20, 30)
+    q -= np.sum(q * g) / np.sum(g * g) * g          # orthogonal to g
+    cos, mean = O.descent_alignment([g, g, g, g], [3.0 * g, -0.5 * g, q, np.zeros_like(g)])
+    assert np.allclose(cos, [1.0, -1.0, 0.0, 0.0], atol=1e-14)
+    assert math.isclose(mean, 0.0, abs_tol=1e-14)
+
+
+def test_descent_alignment_of_normalize_only_step():
+    # W = 0 and M_prev = 0: x_i = g_i, Psi = D(G)^-1 G and U = c Psi (c > 0),
+    # so <G, U> / (||G|| ||U||) = sum_i ||g_i|| / (sqrt(m) ||G||_F): the
+    # Cauchy-Schwarz ratio of the row norms (1 exactly when they are equal).
+    rng = np.random.default_rng(3)
+    g = rng.standard_normal((12, 40)) * rng.uniform(0.1, 5.0, (12, 1))
+    z = np.zeros_like(g)
+    out = O.normpre_step(z, g, z, 0, O.HParams(lr=1.0, weight_decay=0.0), "NORM")
+    cos, _ = O.descent_alignment([g], [out["update"]])
+    rn = np.linalg.norm(g, axis=1)
+    assert math.isclose(cos[0], rn.sum() / (math.sqrt(12) * np.linalg.norm(g)), rel_tol=1e-13)
+    g_eq = g / rn[:, None]
+    out = O.normpre_step(z, g_eq, z, 0, O.HParams(lr=1.0, weight_decay=0.0), "NORM")
+    assert math.isclose(O.descent_alignment([g_eq], [out["update"]])[0][0], 1.0, rel_tol=1e-13)
