@@ -239,6 +239,28 @@ int normpre_reserve(normpre_ctx* ctx, int variant, int num_mats, const int64_t* 
  * Errors: NOT_INITIALIZED, INVALID_ARG (null bytes). */
 int normpre_workspace_bytes(const normpre_ctx* ctx, int64_t* bytes);
 
+/*
+ * normpre_step() for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * same arguments and results, but the workspace is a static device array of
+ * NORMPRE_NOALLOC_SCRATCH_BYTES bytes that every device loading the library
+ * holds for the life of the process, and the call makes no hipMalloc,
+ * hipFree or synchronization.  A step larger than the array runs in several
+ * rounds through it; a single matrix that needs more than the whole array is
+ * rejected (UNSUPPORTED).  Every call on one device shares that device's
+ * array: calls that overlap on one device (other streams, other contexts,
+ * other threads) race; calls in sequence on one stream are safe (the
+ * array's earlier contents are never read before being written).
+ * NORMPRE_FLAG_DEBUG and NORMPRE_FLAG_TIME_KERNELS are rejected
+ * (INVALID_ARG): they allocate.
+ * Errors: as normpre_step, and UNSUPPORTED when a matrix does not fit.
+ */
+#define NORMPRE_NOALLOC_SCRATCH_BYTES 268435456ll   /* 256 MiB */
+int normpre_step_noalloc(normpre_ctx* ctx, int variant, int num_mats,
+                         float* const* params, const float* const* grads,
+                         float* const* momentum, const int64_t* shapes,
+                         const normpre_hparams* hp, void* stream);
+
 /* ---- spectral diagnostics (App. A, spectral dynamics) -------------------- */
 
 #define NORMPRE_SPECTRUM_GAMMA 0  /* Gamma = Psi Psi^T, after the normalization (Eq. 2) */

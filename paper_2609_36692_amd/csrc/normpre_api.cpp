@@ -38,6 +38,12 @@ constexpr int kMaxSplits = 16;
 constexpr int kEigSweeps = 30;
 constexpr size_t kGroupBudget = size_t(24) << 30;  // workspace bytes per item
 constexpr size_t kRoundBudget = size_t(48) << 30;  // workspace bytes per round
+// Static scratch of normpre_step_noalloc(): the whole workspace of that entry
+// point (items and rounds are cut to fit it).  Every device that loads the
+// library holds one copy for the life of the process.
+constexpr size_t kScratchBytes = size_t(256) << 20;
+static __device__ __align__(256) char scratch[kScratchBytes];
+static_assert(kScratchBytes == (size_t)NORMPRE_NOALLOC_SCRATCH_BYTES, "scratch size differs from the header");
 
 struct Fail {
     int code;
@@ -202,6 +208,9 @@ struct normpre_ctx {
     hipEvent_t order_ev = nullptr;
     // Workspace reserved by normpre_reserve(): steps then never grow it.
     bool reserved = false;
+    // Device address of the static scratch array of normpre_step_noalloc()
+    // on this context's device (from hipGetSymbolAddress at init).
+    void* scratch = nullptr;
 };
 
 namespace {
@@ -1891,6 +1900,9 @@ int normpre_init(normpre_ctx** ctx, int device) {
     (void)hipGetDevice(&prev);
     e = hipSetDevice(device);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&c->order_ev, hipEventDisableTiming);
+    // The static scratch array of normpre_step_noalloc: its address on this
+    // device (each device holds its own copy of the array).
+    if (e == hipSuccess) e = hipGetSymbolAddress(&c->scratch, HIP_SYMBOL(scratch));
     (void)hipSetDevice(prev);
     if (e != hipSuccess) {
         if (c->order_ev) (void)hipEventDestroy(c->order_ev);
@@ -1990,6 +2002,29 @@ int normpre_workspace_bytes(const normpre_ctx* ctx, int64_t* bytes) {
     if (!bytes) return NORMPRE_ERR_INVALID_ARG;
     *bytes = (int64_t)ctx->ws_bytes;
     return NORMPRE_OK;
+}
+
+int normpre_step_noalloc(normpre_ctx* ctx, int variant, int num_mats, float* const* params,
+                         const float* const* grads, float* const* momentum, const int64_t* shapes,
+                         const normpre_hparams* hp, void* stream) {
+    if (!ctx) return set_err(nullptr, NORMPRE_ERR_NOT_INITIALIZED, "context is null");
+    ctx->err.clear();
+    if (hp && (hp->flags & (NORMPRE_FLAG_DEBUG | NORMPRE_FLAG_TIME_KERNELS)))
+        return set_err(ctx, NORMPRE_ERR_INVALID_ARG,
+                       "NORMPRE_FLAG_DEBUG and NORMPRE_FLAG_TIME_KERNELS need allocations; not with normpre_step_noalloc");
+    int rc = step_prologue(ctx, variant, num_mats, params, grads, momentum, shapes, hp);
+    if (rc || num_mats == 0) return rc;
+    if (!ctx->scratch) return set_err(ctx, NORMPRE_ERR_HIP, "the scratch array has no device address");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int k = step_orientation(variant, *hp);
+    Plan plan = plan_step(variant, num_mats, shapes, *hp, k, kScratchBytes, kScratchBytes);
+    if (plan.one_matrix > kScratchBytes || plan.need > kScratchBytes)
+        return set_err(ctx, NORMPRE_ERR_UNSUPPORTED,
+                       fmt("a matrix of this step needs %zu workspace bytes; the static scratch holds %zu",
+                           std::max(plan.one_matrix, plan.need), kScratchBytes));
+    rc = order_after_last(ctx, s);
+    if (rc) return rc;
+    return run_plan(ctx, variant, plan, params, grads, momentum, hp, s, ctx->scratch, kScratchBytes, false);
 }
 
 int normpre_spectrum(normpre_ctx* ctx, int which, int64_t rows, int64_t cols, const float* w, const float* m,

@@ -40,6 +40,8 @@ NORMPRE_FLAG_TANGENT_STRICT = 8
 NORMPRE_FLAG_L_EXACT = 16
 NORMPRE_FLAG_SOURCE_X = 32
 
+NORMPRE_NOALLOC_SCRATCH_BYTES = 256 << 20
+
 NORMPRE_SPECTRUM_GAMMA = 0
 NORMPRE_SPECTRUM_GX = 1
 
@@ -131,6 +133,8 @@ def load_library(path: str = LIB_PATH):
         "normpre_workspace_size": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, i64p, hpp, i64p]),
         "normpre_reserve": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int, i64p, hpp, P]),
         "normpre_workspace_bytes": (ctypes.c_int, [P, i64p]),
+        "normpre_step_noalloc": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int, ctypes.POINTER(P), ctypes.POINTER(P),
+                                                ctypes.POINTER(P), i64p, hpp, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -223,6 +227,15 @@ def normpre_step(ctx, variant: int, params, grads, momentum, hp: normpre_hparams
     n, pw, pg, pm, sh = _step_args(params, grads, momentum, shapes)
     code = load_library().normpre_step(ctx, int(variant), n, pw, pg, pm, sh, ctypes.byref(hp),
                                        _stream_handle(stream))
+    _check(code, ctx)
+
+
+def normpre_step_noalloc(ctx, variant: int, params, grads, momentum, hp: normpre_hparams, stream=None,
+                         shapes=None) -> None:
+    """normpre_step through the library's static scratch array (no allocation)."""
+    n, pw, pg, pm, sh = _step_args(params, grads, momentum, shapes)
+    code = load_library().normpre_step_noalloc(ctx, int(variant), n, pw, pg, pm, sh, ctypes.byref(hp),
+                                               _stream_handle(stream))
     _check(code, ctx)
 
 
