@@ -231,11 +231,18 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     // same LDS to stage one wave-row of fp32 results (row stride BN + 4).
     constexpr int kStageBytes = 2 * (BM + BN) * BK * 2;
     // Result rows staged per epilogue pass: the whole tile when its fp32
-    // staging adds little to the operand stages (up to 128 x 128), else one
-    // wave-row.
-    constexpr int kEpiRows = BM * BN <= 128 * 128 ? BM : BM / WM;
+    // staging adds little to the operand stages (up to 128 x 128), else 64
+    // rows, so that the fp32 staging and the fp16 transpose of the mirror
+    // (BN x 64 halves, after it in LDS) fit next to each other.
+    constexpr int kEpiRows = BM * BN <= 128 * 128 ? BM : 64;
     constexpr int kEpiBytes = kEpiRows * (BN + 4) * 4;
-    constexpr bool kLdsMirror = BM * BN <= 128 * 128;
+    // Symmetric results write their mirror from an LDS transpose of the fp16
+    // tile: src is symmetric wherever the result is (A for B = b A + c A^2,
+    // the right factor of a Gram-space product), so the mirrored values are
+    // exactly the transposed results.
+    constexpr bool kSepMirror = Epi::kind == EpiKind::Affine && BM * BN > 128 * 128;  // buffer after the staging
+    constexpr int kMirrorOff = (kEpiBytes + 15) / 16 * 16;
+    static_assert(!kSepMirror || kMirrorOff + BN * kEpiRows * 2 <= kStageBytes, "mirror buffer does not fit");
     __shared__ __attribute__((aligned(16))) unsigned char smem[kStageBytes > kEpiBytes ? kStageBytes : kEpiBytes];
     __shared__ float red[NT / 64];
     half_t* const sbase = reinterpret_cast<half_t*>(smem);
@@ -538,34 +545,8 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
             out = e_out + (int64_t)zo * e_stride_out;
             src = e_src ? e_src + (int64_t)zo * e_stride_src : nullptr;
             // Off-diagonal tiles of a symmetric result also write their
-            // transpose.  src is symmetric wherever the result is (A for
-            // B = b A + c A^2), so the transpose's src values are read from
-            // the transposed position too.  The 128 x 128 tile keeps its fp16
-            // results and transposes them through LDS after each pass; the
-            // 256 x 256 tile (no registers to spare) writes the transpose
-            // from its accumulators, 4 consecutive halves per lane.
+            // transpose (through LDS, after each pass's row stores).
             mirror = sh.sym && tm != tn;
-            if constexpr (!kLdsMirror) {
-                if (mirror) {
-#pragma unroll
-                    for (int qi = 0; qi < NQ; ++qi) {
-                        const int col = cw0 + quad_col(qi), row0 = rw0 + quad_row(qi);
-                        half_t sv[4] = {};
-                        if (src) *reinterpret_cast<u32x2*>(sv) =
-                                     *reinterpret_cast<const u32x2*>(src + (int64_t)col * e_ld_src + row0);
-                        half_t hv[4];
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            float v = ca * quad_val(qi, r);
-                            if (src) v += cs * (float)sv[r];
-                            hv[r] = (half_t)v;
-                        }
-                        // (A plain store: the 8-byte pieces merge in L2.)
-                        *reinterpret_cast<u32x2*>(out + (int64_t)col * e_ld_out + row0) =
-                            *reinterpret_cast<const u32x2*>(hv);
-                    }
-                }
-            }
         } else {
             psi = epi.psi + (int64_t)z * epi.stride_psi;
             if constexpr (Epi::kind == EpiKind::Apply) {
@@ -580,7 +561,6 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
         constexpr int LDST = BN + 4;
         constexpr int C8 = BN / 8;
         constexpr int PR = kEpiRows;
-        constexpr int WPP = PR / TM;                // wave-rows per pass
         float* stg = reinterpret_cast<float*>(smem);
         float ss = 0.f;
 #pragma unroll 1
@@ -604,12 +584,15 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                 }
             }
             lds_barrier();
-            if (wm / WPP == pass) {
+            // This pass's rows [pass * PR, pass * PR + PR) of the tile (a
+            // quad's four rows never straddle a pass).
 #pragma unroll
-                for (int qi = 0; qi < NQ; ++qi)
+            for (int qi = 0; qi < NQ; ++qi) {
+                const int qrow = wm * TM + quad_row(qi) - pass * PR;
+                if (qrow >= 0 && qrow < PR) {
 #pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        stg[((wm % WPP) * TM + quad_row(qi) + r) * LDST + wn * TN + quad_col(qi)] = quad_val(qi, r);
+                    for (int r = 0; r < 4; ++r) stg[(qrow + r) * LDST + wn * TN + quad_col(qi)] = quad_val(qi, r);
+                }
             }
             lds_barrier();
             if constexpr (Epi::kind == EpiKind::Apply || Epi::kind == EpiKind::ApplyNorm) {
@@ -674,7 +657,9 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                 }
                 continue;
             }
-            u32x4 hk[kLdsMirror ? ITEMS : 1];      // fp16 results, kept for the mirror
+            u32x4 hk[kSepMirror ? 1 : ITEMS];      // fp16 results, kept for the mirror
+            half_t* const tb = reinterpret_cast<half_t*>(smem + (kSepMirror ? kMirrorOff : 0));
+            constexpr int R8 = PR / 8;
 #pragma unroll
             for (int it = 0; it < ITEMS; ++it) {
                 const int c = tid + it * NT;
@@ -699,21 +684,33 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
                     // later launch, and keeping it out of L2 leaves the
                     // operand panels resident.
                     const u32x4 hq = *reinterpret_cast<const u32x4*>(hv);
-                    if constexpr (kLdsMirror) hk[it] = hq;
+                    if constexpr (kSepMirror) {
+                        // Transposed copy straight into its own LDS buffer.
+                        if (mirror) {
+#pragma unroll
+                            for (int e = 0; e < 8; ++e) {
+                                const int cc = c8 + e;
+                                tb[cc * PR + (((r >> 3) ^ ((cc >> 3) & (R8 - 1))) << 3) + (r & 7)] = hv[e];
+                            }
+                        }
+                    } else {
+                        hk[it] = hq;
+                    }
                     __builtin_nontemporal_store(hq, reinterpret_cast<u32x4*>(out + (int64_t)grow * e_ld_out + gcol));
                 }
             }
-            if constexpr (Epi::kind == EpiKind::Affine && kLdsMirror) {
+            if constexpr (Epi::kind == EpiKind::Affine) {
                 if (mirror) {
                     // T[c][r] = result[r][c] for this pass's PR rows: row c of
                     // T holds PR halves in chunks of 8, chunk j stored at
                     // j ^ (c / 8 mod PR / 8) so the 2-byte writes of one
-                    // wave spread over the banks; then 16-byte rows out.
-                    constexpr int R8 = PR / 8;
-                    half_t* tb = reinterpret_cast<half_t*>(smem);
+                    // wave spread over the banks; then 16-byte rows out.  The
+                    // whole-tile pass (128 x 128) transposes its fp16 results
+                    // from registers into the freed staging LDS; the 64-row
+                    // passes of the larger tile wrote theirs above.
                     lds_barrier();
 #pragma unroll
-                    for (int it = 0; it < ITEMS; ++it) {
+                    for (int it = 0; it < (kSepMirror ? 0 : ITEMS); ++it) {
                         const int c = tid + it * NT;
                         if (c >= PR * C8) break;
                         const int r = c / C8, c8 = (c - r * C8) * 8;
