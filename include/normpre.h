@@ -122,6 +122,14 @@ extern "C" {
  * (U_C, Lambda_C) from G_X (sketched, or exact with NORMPRE_FLAG_L_EXACT).
  * NormPre-L only, not with NORMPRE_ORIENT_BOTH (INVALID_ARG). */
 #define NORMPRE_FLAG_SOURCE_X      32u
+/* Finite check (a defined outcome for overflowed or corrupted inputs): every
+ * non-finite entry of G, M_prev and W is counted per matrix; non-finite G and
+ * M_prev entries count as zero when M is formed (so the stored M is finite),
+ * non-finite W entries count as zero in the tangent projection (so Psi, T and
+ * the other entries of the update stay finite; those entries of W stay
+ * non-finite).  The counts of the step are read with
+ * normpre_nonfinite_counts().  Not for NORMPRE_VARIANT_MUON (INVALID_ARG). */
+#define NORMPRE_FLAG_CHECK_FINITE  64u
 
 /*
  * Hyper-parameters of one step.  Defaults (normpre_default_hparams) follow
@@ -174,7 +182,8 @@ const char* normpre_last_error(const normpre_ctx* ctx);
  * Errors: INVALID_ARG (variant, num_mats < 0, shapes null, a dimension < 1,
  * ns_iters outside 1..64, rank < 1, oversample < 0, power_iters outside
  * 0..8, a non-finite or negative lr/weight decay, a non-finite momentum,
- * norm_eps <= 0, unknown orientation or flags, both tangent flags),
+ * norm_eps <= 0, unknown orientation or flags, both tangent flags,
+ * NORMPRE_FLAG_CHECK_FINITE with the Muon step),
  * UNSUPPORTED (a dimension above 1 << 20 or a matrix above 2^31 elements;
  * in the row-active or both-axes orientation a row longer than 32768
  * elements; for
@@ -319,6 +328,17 @@ int normpre_descent_alignment(normpre_ctx* ctx, int num_mats, const float* const
                               const float* const* w_before, const float* const* w_after,
                               const int64_t* shapes, float lr, float weight_decay,
                               double* cosines, double* mean, void* stream);
+
+/*
+ * Non-finite entry counts (G, M_prev and W together) per matrix, in the
+ * caller's order, of the last normpre_step() or normpre_step_noalloc() made
+ * with NORMPRE_FLAG_CHECK_FINITE on this context; valid until the next call
+ * that uses the context's workspace.  counts: host array of num_mats int64.
+ * Synchronizes that step's stream.
+ * Errors: NOT_INITIALIZED, INVALID_ARG (null counts, no such step, num_mats
+ * different from that step's), HIP_ERROR.
+ */
+int normpre_nonfinite_counts(normpre_ctx* ctx, int64_t* counts, int num_mats);
 
 /* ---- inspection (tests, benchmarks) -------------------------------------- */
 

@@ -112,8 +112,11 @@ Fail validate(int variant, int num_mats, const int64_t* shapes, const normpre_hp
     if (hp->orientation < NORMPRE_ORIENT_ALTERNATING || hp->orientation > NORMPRE_ORIENT_BOTH)
         return {NORMPRE_ERR_INVALID_ARG, fmt("unknown orientation mode %d", hp->orientation)};
     if (hp->flags & ~(NORMPRE_FLAG_DEBUG | NORMPRE_FLAG_TIME_KERNELS | NORMPRE_FLAG_TANGENT_NONE |
-                      NORMPRE_FLAG_TANGENT_STRICT | NORMPRE_FLAG_L_EXACT | NORMPRE_FLAG_SOURCE_X))
+                      NORMPRE_FLAG_TANGENT_STRICT | NORMPRE_FLAG_L_EXACT | NORMPRE_FLAG_SOURCE_X |
+                      NORMPRE_FLAG_CHECK_FINITE))
         return {NORMPRE_ERR_INVALID_ARG, fmt("unknown flags 0x%x", hp->flags)};
+    if ((hp->flags & NORMPRE_FLAG_CHECK_FINITE) && variant == NORMPRE_VARIANT_MUON)
+        return {NORMPRE_ERR_INVALID_ARG, "NORMPRE_FLAG_CHECK_FINITE applies to the normalized variants"};
     if ((hp->flags & NORMPRE_FLAG_TANGENT_NONE) && (hp->flags & NORMPRE_FLAG_TANGENT_STRICT))
         return {NORMPRE_ERR_INVALID_ARG, "at most one tangent mode flag"};
     if ((hp->flags & NORMPRE_FLAG_L_EXACT) && variant != NORMPRE_VARIANT_L)
@@ -208,6 +211,11 @@ struct normpre_ctx {
     hipEvent_t order_ev = nullptr;
     // Workspace reserved by normpre_reserve(): steps then never grow it.
     bool reserved = false;
+    // Non-finite counts of the last step made with NORMPRE_FLAG_CHECK_FINITE
+    // (device, in that step's workspace; null after any other step).
+    long long* status = nullptr;
+    int status_count = 0;
+    hipStream_t status_stream = nullptr;
     // Device address of the static scratch array of normpre_step_noalloc()
     // on this context's device (from hipGetSymbolAddress at init).
     void* scratch = nullptr;
@@ -316,6 +324,7 @@ struct GWork {
     half_t* amat;
     half_t* bmat;
     float* sumsq;           // per-tile partial sums of T^2 (both variants)
+    int* nfin;              // finite check: non-finite count slots
     float* tn2;             // per-matrix ||T||_F^2
     // L
     half_t* omega;
@@ -450,7 +459,24 @@ struct Pool {
     float* zbuf = nullptr;
 };
 
-void carve_item(Arena& ar, Item& it, int variant, bool source_x) {
+// Workspace options of a step: the interaction-source-X buffers and the
+// non-finite count slots of the finite check.
+constexpr int kOptSourceX = 1, kOptCheck = 2;
+int step_opts(int variant, const normpre_hparams& hp) {
+    int o = 0;
+    if (variant == NORMPRE_VARIANT_L && (hp.flags & NORMPRE_FLAG_SOURCE_X)) o |= kOptSourceX;
+    if (hp.flags & NORMPRE_FLAG_CHECK_FINITE) o |= kOptCheck;
+    return o;
+}
+
+// Count slots per matrix of the finite check (an upper bound for both
+// orientations: one per row, or one per 128-row chunk and 64-column block).
+int64_t nfin_stride(const Dims& d) {
+    return std::max<int64_t>(d.m, ((d.m + kColRowChunk - 1) / kColRowChunk) * ((d.n + 63) / 64));
+}
+
+void carve_item(Arena& ar, Item& it, int variant, int opts) {
+    const bool source_x = (opts & kOptSourceX) != 0;
     const Dims& d = it.d;
     const int count = it.count;
     GWork& w = it.w;
@@ -461,6 +487,7 @@ void carve_item(Arena& ar, Item& it, int variant, bool source_x) {
     w.colpart = ar.take<double>(count * normalize_cols_partials((int)d.m, (int)d.np_, kColRowChunk));
     w.sumsq = ar.take<float>(count * std::max(ns_tiles(d), apply_tiles(d)));
     w.tn2 = ar.take<float>(count);
+    if (opts & kOptCheck) w.nfin = ar.take<int>(count * nfin_stride(d));
     if (variant == NORMPRE_VARIANT_G || variant == NORMPRE_VARIANT_MUON) {
         w.xb = ar.take<half_t>(count * mn);
     } else if (variant == NORMPRE_VARIANT_L) {
@@ -564,16 +591,16 @@ std::vector<Pool> make_pools(std::vector<Item>& items, int variant) {
 }
 
 // Carves a round's items and pools; with a null arena base it only measures.
-size_t carve_round(Arena& ar, std::vector<Item>& items, std::vector<Pool>& pools, int variant, bool source_x) {
-    for (Item& it : items) carve_item(ar, it, variant, source_x);
+size_t carve_round(Arena& ar, std::vector<Item>& items, std::vector<Pool>& pools, int variant, int opts) {
+    for (Item& it : items) carve_item(ar, it, variant, opts);
     for (Pool& p : pools) carve_pool(ar, p, variant);
     return ar.off + 256;
 }
 
-size_t round_bytes(std::vector<Item> items, int variant, bool source_x) {
+size_t round_bytes(std::vector<Item> items, int variant, int opts) {
     std::vector<Pool> pools = make_pools(items, variant);
     Arena ar{nullptr, 0, 0};
-    return carve_round(ar, items, pools, variant, source_x);
+    return carve_round(ar, items, pools, variant, opts);
 }
 
 struct StepCtx {
@@ -586,6 +613,7 @@ struct StepCtx {
     int variant;
     bool debug;
     const std::vector<Group>* groups;
+    long long* status = nullptr;    // finite check: per-matrix counts, caller order
 };
 
 
@@ -640,6 +668,10 @@ int run_normalize(const StepCtx& sc, const Dims& d, const GWork& w, const std::v
         a.vec_ok = chunk_vec_ok(a.ptrs, cnt);
         a.tangent = tangent_mode(*sc.hp);
         if (w.xsq) a.xsq = w.xsq + (int64_t)c0 * d.lp_;
+        if (w.nfin) {
+            a.stride_nfin = nfin_stride(d);
+            a.nfin = w.nfin + (int64_t)c0 * a.stride_nfin;
+        }
         if (dbg) {
             // Debug copies are written chunk by chunk into per-matrix buffers
             // that are contiguous in the order of the caller's list.
@@ -674,6 +706,14 @@ int run_normalize(const StepCtx& sc, const Dims& d, const GWork& w, const std::v
                                  kColRowChunk, sc.s);
                          }),
                    "normalize cols");
+        }
+        if (a.nfin && sc.status) {
+            IdxChunk ic{};
+            for (int i = 0; i < cnt; ++i) ic.idx[i] = idx[first + c0 + i];
+            const int64_t slots = nonfinite_slots(a, d.k == 0 || both, kColRowChunk);
+            NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
+                         [&] { return launch_count_reduce(a.nfin, slots, a.stride_nfin, ic, cnt, sc.status, sc.s); }),
+                   "non-finite counts");
         }
     }
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
@@ -746,15 +786,17 @@ int run_muon_input(const StepCtx& sc, const Dims& d, const GWork& w, const std::
 }
 
 // 256 x 256 tiles (8 waves, 1 block per CU) once a launch has enough of them
-// to fill the chip about twice over (symmetric products count their
+// to fill the chip several times over (symmetric products count their
 // upper-triangle tiles); below that the 128 x 128 tile (2 blocks per CU)
-// keeps more CUs busy.  The combine switches a little earlier: measured on
-// 12-matrix launches, 432 large tiles ran faster than the small ones and 324
-// slower.
+// keeps more CUs busy.  Measured on random data: symmetric 1024^3 products
+// x56 (560 large tiles) ran 648 TFLOP/s on the small tile against 584 on the
+// large one, 2048^3 x84 (3024 large tiles) 717 against 740; the combine
+// switches earlier (12-matrix launches: 432 large tiles faster than the
+// small ones, 324 slower).
 TileCfg ns_cfg(int64_t M, int64_t N, bool sym, int count) {
     const int64_t tm = M / 256, tn = N / 256;
     const int64_t tiles = (sym ? tm * (tm + 1) / 2 : tm * tn) * count;
-    return tiles >= (sym ? 512 : 384) ? TileCfg::Big256 : TileCfg::Big;
+    return tiles >= (sym ? 1024 : 384) ? TileCfg::Big256 : TileCfg::Big;
 }
 
 // MFMA FLOPs a product launch issues for `count` matrices of M x N x K with
@@ -1728,16 +1770,21 @@ int check_aliasing(normpre_ctx* ctx, int num_mats, float* const* W, const float*
 // groups cut into items of at most item_budget workspace bytes, items packed
 // into rounds of at most round_budget bytes; `need` is the largest round.
 struct Plan {
+    int num_mats = 0;
     std::vector<Group> groups;
     std::vector<std::vector<Item>> rounds;
     size_t need = 0;
     size_t one_matrix = 0;   // the largest single-matrix item of the step
 };
 
+// Bytes of the per-matrix non-finite counts at the front of the workspace.
+size_t status_bytes(int num_mats) { return ((size_t)num_mats * sizeof(long long) + 255) & ~size_t(255); }
+
 Plan plan_step(int variant, int num_mats, const int64_t* shapes, const normpre_hparams& hp, int k,
                size_t item_budget, size_t round_budget) {
     Plan pl;
-    const bool source_x = variant == NORMPRE_VARIANT_L && (hp.flags & NORMPRE_FLAG_SOURCE_X) != 0;
+    pl.num_mats = num_mats;
+    const int opts = step_opts(variant, hp);
     {
         std::map<std::pair<int64_t, int64_t>, int> where;
         for (int i = 0; i < num_mats; ++i) {
@@ -1760,7 +1807,7 @@ Plan plan_step(int variant, int num_mats, const int64_t* shapes, const normpre_h
         one.count = 1;
         one.d = d;
         one.gns = gram_space_ns(variant, d, hp);
-        const size_t per = round_bytes({one}, variant, source_x);
+        const size_t per = round_bytes({one}, variant, opts);
         pl.one_matrix = std::max(pl.one_matrix, per);
         const int b = (int)std::max<size_t>(1, std::min<size_t>((size_t)cnt, item_budget / std::max<size_t>(per, 1)));
         for (int first = 0; first < cnt; first += b) {
@@ -1779,7 +1826,7 @@ Plan plan_step(int variant, int num_mats, const int64_t* shapes, const normpre_h
         if (!pl.rounds.empty()) {
             std::vector<Item> trial = pl.rounds.back();
             trial.push_back(it);
-            const size_t bytes = round_bytes(trial, variant, source_x);
+            const size_t bytes = round_bytes(trial, variant, opts);
             if (bytes <= round_budget) {
                 pl.rounds.back().push_back(it);
                 pl.need = std::max(pl.need, bytes);
@@ -1787,8 +1834,9 @@ Plan plan_step(int variant, int num_mats, const int64_t* shapes, const normpre_h
             }
         }
         pl.rounds.push_back({it});
-        pl.need = std::max(pl.need, round_bytes(pl.rounds.back(), variant, source_x));
+        pl.need = std::max(pl.need, round_bytes(pl.rounds.back(), variant, opts));
     }
+    if (opts & kOptCheck) pl.need += status_bytes(num_mats);
     return pl;
 }
 
@@ -1819,16 +1867,27 @@ int order_after_last(normpre_ctx* ctx, hipStream_t s) {
 int run_plan(normpre_ctx* ctx, int variant, Plan& plan, float* const* params, const float* const* grads,
              float* const* momentum, const normpre_hparams* hp, hipStream_t s, void* ws, size_t ws_bytes,
              bool debug) {
-    const bool source_x = variant == NORMPRE_VARIANT_L && (hp->flags & NORMPRE_FLAG_SOURCE_X) != 0;
+    const int opts = step_opts(variant, *hp);
     ctx->dbg_valid = false;
+    // Finite check: the per-matrix counts (caller order) at the front of the
+    // workspace, the rounds after them.
+    long long* status = nullptr;
+    size_t front = 0;
+    if (opts & kOptCheck) {
+        status = static_cast<long long*>(ws);
+        front = status_bytes(plan.num_mats);
+    }
+    ctx->status = status;
+    ctx->status_count = status ? plan.num_mats : 0;
+    ctx->status_stream = s;
     ctx->timing = (hp->flags & NORMPRE_FLAG_TIME_KERNELS) != 0;
     ctx->stream = s;
-    StepCtx sc{ctx, s, hp, params, grads, momentum, variant, debug, &plan.groups};
+    StepCtx sc{ctx, s, hp, params, grads, momentum, variant, debug, &plan.groups, status};
     for (std::vector<Item>& items : plan.rounds) {
         std::vector<Pool> pools = make_pools(items, variant);
-        Arena ar{static_cast<char*>(ws), 0, ws_bytes};
-        carve_round(ar, items, pools, variant, source_x);
-        if (ar.off > ws_bytes) return set_err(ctx, NORMPRE_ERR_HIP, "internal: round exceeds the workspace");
+        Arena ar{static_cast<char*>(ws) + front, 0, ws_bytes - front};
+        carve_round(ar, items, pools, variant, opts);
+        if (front + ar.off > ws_bytes) return set_err(ctx, NORMPRE_ERR_HIP, "internal: round exceeds the workspace");
         DebugMat* dbg = debug ? ctx->dbg.data() : nullptr;
         int rc = variant == NORMPRE_VARIANT_L ? run_round_l(sc, items, pools, dbg) : run_round_g(sc, items, pools, dbg);
         if (rc) return rc;
@@ -2017,8 +2076,10 @@ int normpre_step_noalloc(normpre_ctx* ctx, int variant, int num_mats, float* con
     if (!ctx->scratch) return set_err(ctx, NORMPRE_ERR_HIP, "the scratch array has no device address");
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int k = step_orientation(variant, *hp);
-    Plan plan = plan_step(variant, num_mats, shapes, *hp, k, kScratchBytes, kScratchBytes);
-    if (plan.one_matrix > kScratchBytes || plan.need > kScratchBytes)
+    const size_t front = (hp->flags & NORMPRE_FLAG_CHECK_FINITE) ? status_bytes(num_mats) : 0;
+    if (front >= kScratchBytes) return set_err(ctx, NORMPRE_ERR_UNSUPPORTED, "too many matrices for the static scratch");
+    Plan plan = plan_step(variant, num_mats, shapes, *hp, k, kScratchBytes - front, kScratchBytes - front);
+    if (plan.one_matrix + front > kScratchBytes || plan.need > kScratchBytes)
         return set_err(ctx, NORMPRE_ERR_UNSUPPORTED,
                        fmt("a matrix of this step needs %zu workspace bytes; the static scratch holds %zu",
                            std::max(plan.one_matrix, plan.need), kScratchBytes));
@@ -2088,6 +2149,7 @@ int normpre_spectrum(normpre_ctx* ctx, int which, int64_t rows, int64_t cols, co
     carve(ar, mcopy);
     ctx->timing = false;
     ctx->stream = s;
+    ctx->status = nullptr;
     std::vector<Group> groups{{rows, cols, {0}}};
     float* Wl[1] = {const_cast<float*>(w)};    // read only: the normalization reads W
     const float* Gl[1] = {m};
@@ -2145,6 +2207,7 @@ int normpre_descent_alignment(normpre_ctx* ctx, int num_mats, const float* const
     if (rc) return rc;
     rc = order_after_last(ctx, s);
     if (rc) return rc;
+    ctx->status = nullptr;
     double* part = static_cast<double*>(ctx->ws);
     double* cos_dev = part + part_n;
     double* mean_dev = cos_dev + num_mats;
@@ -2169,6 +2232,21 @@ int normpre_descent_alignment(normpre_ctx* ctx, int num_mats, const float* const
     if (e != hipSuccess) return hip_fail(ctx, e, "alignment copy");
     ctx->last_stream = s;
     ctx->have_stream = true;
+    return NORMPRE_OK;
+}
+
+int normpre_nonfinite_counts(normpre_ctx* ctx, int64_t* counts, int num_mats) {
+    if (!ctx) return set_err(nullptr, NORMPRE_ERR_NOT_INITIALIZED, "context is null");
+    if (!counts) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "counts is null");
+    if (!ctx->status) return set_err(ctx, NORMPRE_ERR_INVALID_ARG, "no step with NORMPRE_FLAG_CHECK_FINITE recorded");
+    if (num_mats != ctx->status_count)
+        return set_err(ctx, NORMPRE_ERR_INVALID_ARG,
+                       fmt("num_mats %d differs from the %d matrices of the checked step", num_mats, ctx->status_count));
+    hipError_t e = hipSetDevice(ctx->device);
+    if (e == hipSuccess) e = hipStreamSynchronize(ctx->status_stream);
+    if (e == hipSuccess)
+        e = hipMemcpy(counts, ctx->status, sizeof(long long) * (size_t)num_mats, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(ctx, e, "non-finite counts");
     return NORMPRE_OK;
 }
 

@@ -74,6 +74,53 @@ __device__ __forceinline__ void block_sum1(double& a) {
 // x = m - c w in fp64.
 __device__ __forceinline__ double tangent_x(float m, float w, double c) { return fma(-c, (double)w, (double)m); }
 
+// Finite check: a non-finite value counts as zero, and is counted.
+__device__ __forceinline__ float finite_or_zero(float v, int& bad) {
+    const bool ok = __builtin_isfinite(v);
+    bad += ok ? 0 : 1;
+    return ok ? v : 0.f;
+}
+
+// One VW-wide piece of a row: M <- mu M_prev + G (stored), the new m and w
+// kept for the statistics.  With the finite check, non-finite M_prev and G
+// entries count as zero (and the stored M is finite), non-finite W entries
+// count as zero in the tangent; `bad` counts all three.
+template <int VW>
+__device__ __forceinline__ void load_row_piece(const NormArgs& a, float* M, const float* G, const float* W, int idx,
+                                               float (&mv)[VW], float (&wv)[VW], int& bad, int64_t base = 0) {
+    M += base;
+    G += base;
+    W += base;
+    float mp[VW], g[VW], w[VW];
+    if constexpr (VW == 4) {
+        const float4 mp4 = *reinterpret_cast<const float4*>(M + idx);
+        const float4 g4 = *reinterpret_cast<const float4*>(G + idx);
+        const float4 w4 = *reinterpret_cast<const float4*>(W + idx);
+        mp[0] = mp4.x; mp[1] = mp4.y; mp[2] = mp4.z; mp[3] = mp4.w;
+        g[0] = g4.x; g[1] = g4.y; g[2] = g4.z; g[3] = g4.w;
+        w[0] = w4.x; w[1] = w4.y; w[2] = w4.z; w[3] = w4.w;
+    } else {
+        mp[0] = M[idx];
+        g[0] = G[idx];
+        w[0] = W[idx];
+    }
+    if (a.nfin) {
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+            mp[e] = finite_or_zero(mp[e], bad);
+            g[e] = finite_or_zero(g[e], bad);
+            w[e] = finite_or_zero(w[e], bad);
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < VW; ++e) {
+        mv[e] = fmaf(a.mu, mp[e], g[e]);
+        wv[e] = w[e];
+    }
+    if constexpr (VW == 4) *reinterpret_cast<float4*>(M + idx) = make_float4(mv[0], mv[1], mv[2], mv[3]);
+    else M[idx] = mv[0];
+}
+
 // ---------------------------------------------------------------------------
 // Row-active orientation: one block per row of W; the row of M and W stays in
 // registers between the statistics and the Psi store.  VW = vector width
@@ -92,26 +139,12 @@ __global__ void __launch_bounds__(NT) normalize_rows_kernel(NormArgs a) {
     const float* G = a.ptrs.g[z] + off;
     float mv[NV][VW], wv[NV][VW];
     double smw = 0.0, sww = 0.0;
+    int bad = 0;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
         const int idx = (v * NT + tid) * VW;
         if (idx < a.cols) {
-            if constexpr (VW == 4) {
-                const float4 mp = *reinterpret_cast<const float4*>(M + idx);
-                const float4 g = *reinterpret_cast<const float4*>(G + idx);
-                const float4 w = *reinterpret_cast<const float4*>(W + idx);
-                float4 m;
-                m.x = fmaf(a.mu, mp.x, g.x); m.y = fmaf(a.mu, mp.y, g.y);
-                m.z = fmaf(a.mu, mp.z, g.z); m.w = fmaf(a.mu, mp.w, g.w);
-                *reinterpret_cast<float4*>(M + idx) = m;
-                mv[v][0] = m.x; mv[v][1] = m.y; mv[v][2] = m.z; mv[v][3] = m.w;
-                wv[v][0] = w.x; wv[v][1] = w.y; wv[v][2] = w.z; wv[v][3] = w.w;
-            } else {
-                const float m = fmaf(a.mu, M[idx], G[idx]);
-                M[idx] = m;
-                mv[v][0] = m;
-                wv[v][0] = W[idx];
-            }
+            load_row_piece<VW>(a, M, G, W, idx, mv[v], wv[v], bad);
 #pragma unroll
             for (int e = 0; e < VW; ++e) {
                 const double md = mv[v][e], wd = wv[v][e];
@@ -119,6 +152,12 @@ __global__ void __launch_bounds__(NT) normalize_rows_kernel(NormArgs a) {
                 sww = fma(wd, wd, sww);
             }
         }
+    }
+    if (a.nfin) {
+        double b = bad;
+        block_sum1<NT>(b);
+        if (tid == 0) a.nfin[(int64_t)z * a.stride_nfin + row] = (int)b;
+        __syncthreads();   // the second block_sum1 below reuses its LDS
     }
     block_sum2<NT>(smw, sww);
     const double d = tangent_coef(a.tangent, smw, sww);
@@ -185,26 +224,12 @@ __global__ void __launch_bounds__(256) normalize_rows_wave_kernel(NormArgs a) {
     const float* G = a.ptrs.g[z] + off;
     float mv[NV][VW], wv[NV][VW];
     double smw = 0.0, sww = 0.0;
+    int bad = 0;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
         const int idx = (v * 64 + lane) * VW;
         if (idx < a.cols) {
-            if constexpr (VW == 4) {
-                const float4 mp = *reinterpret_cast<const float4*>(M + idx);
-                const float4 g = *reinterpret_cast<const float4*>(G + idx);
-                const float4 w = *reinterpret_cast<const float4*>(W + idx);
-                float4 m;
-                m.x = fmaf(a.mu, mp.x, g.x); m.y = fmaf(a.mu, mp.y, g.y);
-                m.z = fmaf(a.mu, mp.z, g.z); m.w = fmaf(a.mu, mp.w, g.w);
-                *reinterpret_cast<float4*>(M + idx) = m;
-                mv[v][0] = m.x; mv[v][1] = m.y; mv[v][2] = m.z; mv[v][3] = m.w;
-                wv[v][0] = w.x; wv[v][1] = w.y; wv[v][2] = w.z; wv[v][3] = w.w;
-            } else {
-                const float m = fmaf(a.mu, M[idx], G[idx]);
-                M[idx] = m;
-                mv[v][0] = m;
-                wv[v][0] = W[idx];
-            }
+            load_row_piece<VW>(a, M, G, W, idx, mv[v], wv[v], bad);
 #pragma unroll
             for (int e = 0; e < VW; ++e) {
                 const double md = mv[v][e], wd = wv[v][e];
@@ -212,6 +237,10 @@ __global__ void __launch_bounds__(256) normalize_rows_wave_kernel(NormArgs a) {
                 sww = fma(wd, wd, sww);
             }
         }
+    }
+    if (a.nfin) {
+        const double b = wave_sum_d((double)bad);
+        if (lane == 0) a.nfin[(int64_t)z * a.stride_nfin + row] = (int)b;
     }
     smw = wave_sum_d(smw);
     sww = wave_sum_d(sww);
@@ -281,6 +310,7 @@ __global__ void __launch_bounds__(kColThreads) normalize_cols_stats(NormArgs a, 
     double smm[VW], smw[VW], sww[VW];
 #pragma unroll
     for (int e = 0; e < VW; ++e) smm[e] = smw[e] = sww[e] = 0.0;
+    int bad = 0;
     if (col0 < a.cols) {
         float* W = a.ptrs.w[z];
         float* M = a.ptrs.m[z];
@@ -302,10 +332,19 @@ __global__ void __launch_bounds__(kColThreads) normalize_cols_stats(NormArgs a, 
 #pragma unroll
                 for (int u = 0; u < kColBatch; ++u) {
                     const int64_t o = (int64_t)(i + 4 * u) * a.cols + col0;
-                    const float m[4] = {fmaf(a.mu, mp[u].x, g[u].x), fmaf(a.mu, mp[u].y, g[u].y),
-                                        fmaf(a.mu, mp[u].z, g[u].z), fmaf(a.mu, mp[u].w, g[u].w)};
+                    float pv[4] = {mp[u].x, mp[u].y, mp[u].z, mp[u].w}, gv[4] = {g[u].x, g[u].y, g[u].z, g[u].w};
+                    float wv[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
+                    if (a.nfin) {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            pv[e] = finite_or_zero(pv[e], bad);
+                            gv[e] = finite_or_zero(gv[e], bad);
+                            wv[e] = finite_or_zero(wv[e], bad);
+                        }
+                    }
+                    const float m[4] = {fmaf(a.mu, pv[0], gv[0]), fmaf(a.mu, pv[1], gv[1]), fmaf(a.mu, pv[2], gv[2]),
+                                        fmaf(a.mu, pv[3], gv[3])};
                     *reinterpret_cast<float4*>(M + o) = make_float4(m[0], m[1], m[2], m[3]);
-                    const float wv[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         const double md = m[e], wd = wv[e];
@@ -318,14 +357,9 @@ __global__ void __launch_bounds__(kColThreads) normalize_cols_stats(NormArgs a, 
         }
         for (; i < r1; i += 4) {
             const int64_t o = (int64_t)i * a.cols + col0;
+            float m[VW], wv[VW];
+            load_row_piece<VW>(a, M, G, W, (int)0, m, wv, bad, o);
             if constexpr (VW == 4) {
-                const float4 mp = *reinterpret_cast<const float4*>(M + o);
-                const float4 g = *reinterpret_cast<const float4*>(G + o);
-                const float4 w = *reinterpret_cast<const float4*>(W + o);
-                const float m[4] = {fmaf(a.mu, mp.x, g.x), fmaf(a.mu, mp.y, g.y), fmaf(a.mu, mp.z, g.z),
-                                    fmaf(a.mu, mp.w, g.w)};
-                *reinterpret_cast<float4*>(M + o) = make_float4(m[0], m[1], m[2], m[3]);
-                const float wv[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const double md = m[e], wd = wv[e];
@@ -334,9 +368,7 @@ __global__ void __launch_bounds__(kColThreads) normalize_cols_stats(NormArgs a, 
                     sww[e] = fma(wd, wd, sww[e]);
                 }
             } else {
-                const float m = fmaf(a.mu, M[o], G[o]);
-                M[o] = m;
-                const double md = m, wd = W[o];
+                const double md = m[0], wd = wv[0];
                 smm[0] = fma(md, md, smm[0]);
                 smw[0] = fma(md, wd, smw[0]);
                 sww[0] = fma(wd, wd, sww[0]);
@@ -344,13 +376,24 @@ __global__ void __launch_bounds__(kColThreads) normalize_cols_stats(NormArgs a, 
         }
     }
     __shared__ double red[3][4][64 * VW];
+    __shared__ int redbad[kColThreads / 64];
 #pragma unroll
     for (int e = 0; e < VW; ++e) {
         red[0][ry][cx * VW + e] = smm[e];
         red[1][ry][cx * VW + e] = smw[e];
         red[2][ry][cx * VW + e] = sww[e];
     }
+    if (a.nfin) {
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) bad += __shfl_xor(bad, o, 64);
+        if ((threadIdx.x & 63) == 0) redbad[threadIdx.x >> 6] = bad;
+    }
     __syncthreads();
+    if (a.nfin && threadIdx.x == 0) {
+        int t = 0;
+        for (int q = 0; q < kColThreads / 64; ++q) t += redbad[q];
+        a.nfin[(int64_t)z * a.stride_nfin + (int64_t)chunk * gridDim.x + blockIdx.x] = t;
+    }
     const int64_t cols_pad = a.ld_psi;
     const int nchunks = gridDim.y;
     double* p = partials + ((int64_t)z * nchunks + chunk) * 3 * cols_pad;
@@ -412,7 +455,12 @@ __global__ void __launch_bounds__(kColThreads) normalize_cols_apply(NormArgs a, 
             if (i < a.rows && col0 < a.cols) {
                 const int64_t o = (int64_t)i * a.cols + col0;
                 const float4 m = *reinterpret_cast<const float4*>(M + o);
-                const float4 w = *reinterpret_cast<const float4*>(W + o);
+                float4 w = *reinterpret_cast<const float4*>(W + o);
+                if (a.nfin) {
+                    int unused = 0;
+                    w.x = finite_or_zero(w.x, unused); w.y = finite_or_zero(w.y, unused);
+                    w.z = finite_or_zero(w.z, unused); w.w = finite_or_zero(w.w, unused);
+                }
                 v[0] = (float)(tangent_x(m.x, w.x, df[0]) * inv[0]);
                 v[1] = (float)(tangent_x(m.y, w.y, df[1]) * inv[1]);
                 v[2] = (float)(tangent_x(m.z, w.z, df[2]) * inv[2]);
@@ -426,7 +474,9 @@ __global__ void __launch_bounds__(kColThreads) normalize_cols_apply(NormArgs a, 
             float v = 0.f;
             if (i < a.rows && col0 < a.cols) {
                 const int64_t o = (int64_t)i * a.cols + col0;
-                v = (float)(tangent_x(M[o], W[o], df[0]) * inv[0]);
+                int unused = 0;
+                const float wo = a.nfin ? finite_or_zero(W[o], unused) : W[o];
+                v = (float)(tangent_x(M[o], wo, df[0]) * inv[0]);
                 if constexpr (DBG) a.psi32[(int64_t)z * a.stride_psi32 + o] = v;
             }
             prow[0] = (half_t)v;
@@ -765,6 +815,38 @@ __global__ void __launch_bounds__(256) psi_colscale_kernel(half_t* psi, int64_t 
         *q = (half_t)((float)*q * f[j]);
         if (psi32) psi32[(int64_t)z * stride_psi32 + e] *= f[j];
     }
+}
+
+// Count slots per matrix, as the launches write them: one per real row in the
+// row-active kernels, one per stats block (row chunk x column block) in the
+// column-active stats pass (its vector width as launch_normalize_cols picks).
+int64_t nonfinite_slots(const NormArgs& a, bool row_active, int row_chunk) {
+    if (row_active) return a.rows;
+    const int nchunks = (a.rows + row_chunk - 1) / row_chunk;
+    const int vw = (a.vec_ok && a.cols % 4 == 0 && a.ld_psi % 4 == 0) ? 4 : 1;
+    return (int64_t)nchunks * ((a.cols + 64 * vw - 1) / (64 * vw));
+}
+
+// One block per matrix: the sum of its count slots, written to the caller's
+// position of the matrix.
+__global__ void __launch_bounds__(256) count_reduce_kernel(const int* nfin, int64_t slots, int64_t stride,
+                                                           IdxChunk idx, long long* status) {
+    const int z = blockIdx.x;
+    long long t = 0;
+    for (int64_t i = threadIdx.x; i < slots; i += 256) t += nfin[(int64_t)z * stride + i];
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) t += __shfl_xor(t, o, 64);
+    __shared__ long long red[4];
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = t;
+    __syncthreads();
+    if (threadIdx.x == 0) status[idx.idx[z]] = red[0] + red[1] + red[2] + red[3];
+}
+
+hipError_t launch_count_reduce(const int* nfin, int64_t slots, int64_t stride, const IdxChunk& idx, int count,
+                               long long* status, hipStream_t s) {
+    if (count < 1 || count > kChunk) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(count_reduce_kernel, dim3(count), dim3(256), 0, s, nfin, slots, stride, idx, status);
+    return hipGetLastError();
 }
 
 int64_t normalize_cols_partials(int rows, int cols_pad, int row_chunk) {

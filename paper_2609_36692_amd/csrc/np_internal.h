@@ -178,8 +178,19 @@ struct NormArgs {
     int vec_ok;                     // 16-byte aligned W, M, G rows
     int tangent;                    // kTangentRelaxed / kTangentNone / kTangentStrict
     float* xsq;                     // optional per active row ||x_i||^2 (stride_psisq)
+    // Finite check: non-finite G and M_prev entries count as zero in M,
+    // non-finite W entries as zero in the tangent; the number of non-finite
+    // G, M_prev and W entries per row (row-active) or per stats block
+    // (column-active) goes to nfin[z * stride_nfin + slot].
+    int* nfin; int64_t stride_nfin;
 };
 constexpr int kTangentRelaxed = 0, kTangentNone = 1, kTangentStrict = 2;
+// Slots of non-finite counts a normalization launch writes per matrix.
+int64_t nonfinite_slots(const NormArgs& a, bool row_active, int row_chunk);
+// status[idx[i]] = sum of the matrix's count slots (i < count <= kChunk).
+struct IdxChunk { int idx[kChunk]; };
+hipError_t launch_count_reduce(const int* nfin, int64_t slots, int64_t stride, const IdxChunk& idx, int count,
+                               long long* status, hipStream_t s);
 hipError_t launch_normalize_rows(const NormArgs& a, int batch, hipStream_t s);
 // Column-active orientation: stats pass + normalize pass.
 hipError_t launch_normalize_cols(const NormArgs& a, int batch, double* partials,

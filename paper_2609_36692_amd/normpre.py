@@ -39,6 +39,7 @@ NORMPRE_FLAG_TANGENT_NONE = 4
 NORMPRE_FLAG_TANGENT_STRICT = 8
 NORMPRE_FLAG_L_EXACT = 16
 NORMPRE_FLAG_SOURCE_X = 32
+NORMPRE_FLAG_CHECK_FINITE = 64
 
 NORMPRE_NOALLOC_SCRATCH_BYTES = 256 << 20
 
@@ -130,6 +131,7 @@ def load_library(path: str = LIB_PATH):
                                                      ctypes.POINTER(P), i64p, ctypes.c_float, ctypes.c_float,
                                                      ctypes.POINTER(ctypes.c_double),
                                                      ctypes.POINTER(ctypes.c_double), P]),
+        "normpre_nonfinite_counts": (ctypes.c_int, [P, i64p, ctypes.c_int]),
         "normpre_workspace_size": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, i64p, hpp, i64p]),
         "normpre_reserve": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int, i64p, hpp, P]),
         "normpre_workspace_bytes": (ctypes.c_int, [P, i64p]),
@@ -237,6 +239,15 @@ def normpre_step_noalloc(ctx, variant: int, params, grads, momentum, hp: normpre
     code = load_library().normpre_step_noalloc(ctx, int(variant), n, pw, pg, pm, sh, ctypes.byref(hp),
                                                _stream_handle(stream))
     _check(code, ctx)
+
+
+def normpre_nonfinite_counts(ctx, num_mats: int) -> np.ndarray:
+    """Per-matrix non-finite entry counts of the last step made with
+    NORMPRE_FLAG_CHECK_FINITE."""
+    out = np.zeros(max(1, num_mats), dtype=np.int64)
+    _check(load_library().normpre_nonfinite_counts(ctx, out.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                                                    int(num_mats)), ctx)
+    return out[:num_mats]
 
 
 def normpre_workspace_size(variant: int, shapes, hp: normpre_hparams) -> int:

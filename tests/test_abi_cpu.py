@@ -78,6 +78,10 @@ def test_version(N):
     (0, [(8, 8)], {"lr": float("nan")}, -1),
     (0, [(8, 8)], {"lr": -1.0}, -1),
     (0, [(8, 8)], {"weight_decay": float("inf")}, -1),
+    (0, [(8, 8)], {"flags": 64}, 0),                 # finite check
+    (1, [(8, 8)], {"flags": 64}, 0),
+    (2, [(8, 8)], {"flags": 64}, -1),                # not for the Muon step
+    (0, [(8, 8)], {"flags": 128}, -1),               # unknown flag
     (0, [(8, 8)], {"norm_eps": 0.0}, -1),
     (0, [(8, 8)], {"orientation": 4}, -1),
     (1, [(8, 8)], {"flags": 32}, 0),                 # interaction source X
@@ -85,7 +89,7 @@ def test_version(N):
     (1, [(8, 8)], {"flags": 32, "orientation": 3}, -1),
     (0, [(8, 8)], {"orientation": 3}, 0),            # both axes
     (1, [(8, 40000)], {"orientation": 3, "step": 1}, -2),  # both axes: the row pass needs short rows
-    (0, [(8, 8)], {"flags": 64}, -1),
+    (0, [(8, 8)], {"flags": 256}, -1),               # unknown flag
     (1, [(100, 1000)], {"flags": 16}, 0),            # exact NormPre-L, a = 100
     (1, [(400, 1000)], {"flags": 16}, 0),            # exact above 384 rows: dense eigensolver
     (1, [(400, 1000)], {"flags": 16, "step": 1}, 0),

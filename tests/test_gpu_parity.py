@@ -607,3 +607,60 @@ def test_steps_alternating_streams_match_one_stream(ctx, variant):
     two = run([s1, s2, s1, s2])
     for a, b in zip(one, two):
         assert torch.equal(a, b)
+
+
+# ------------------------------------------------ finite check
+# NORMPRE_FLAG_CHECK_FINITE: non-finite G and M_prev entries count as zero in
+# M, non-finite W entries count as zero in the tangent (and stay non-finite in
+# W); the per-matrix counts come back in caller order.  Expected values: the
+# oracle step on the inputs with those entries set to zero.
+def _poison(mat, seed, n_g, n_m, n_w):
+    w, g, mp = (x.clone() for x in mat)
+    rng = np.random.default_rng(seed)
+    bad = [float("nan"), float("inf"), float("-inf")]
+    pos = {}
+    for name, x, n in (("g", g, n_g), ("m", mp, n_m), ("w", w, n_w)):
+        flat = x.view(-1)
+        idx = rng.choice(flat.numel(), size=n, replace=False)
+        for j, i in enumerate(idx):
+            flat[int(i)] = bad[j % 3]
+        pos[name] = idx
+    return (w, g, mp), pos
+
+
+def _sanitized(mat):
+    return tuple(torch.where(torch.isfinite(x), x, torch.zeros_like(x)) for x in mat)
+
+
+@pytest.mark.parametrize("variant", ["G", "L", "NORM"])
+@pytest.mark.parametrize("t", [0, 1])
+def test_check_finite(ctx, variant, t):
+    _say(f"finite check {variant} t={t}")
+    shapes = [(257, 513), (256, 1024), (300, 200)]
+    clean = [_inputs(sh, "lowrank", seed=70 + i) for i, sh in enumerate(shapes)]
+    plan = [(5, 3, 1), (0, 0, 0), (1, 7, 2)]
+    mats, where = [], []
+    for i, (m, (ng, nm, nw)) in enumerate(zip(clean, plan)):
+        pm, pos = _poison(m, 80 + i, ng, nm, nw)
+        mats.append(pm)
+        where.append(pos)
+    flags = N.NORMPRE_FLAG_DEBUG | N.NORMPRE_FLAG_CHECK_FINITE
+    res = run_step(ctx, variant, mats, t, flags=flags, rank=16)
+    counts = N.normpre_nonfinite_counts(ctx, len(mats))
+    assert list(counts) == [sum(p) for p in plan]
+    for i, (mat, r) in enumerate(zip(mats, res)):
+        assert torch.isfinite(r["m"]).all()
+        ref = oracle(_sanitized(mat), variant, t, matrix_id=i, rank=16)
+        assert O.relative_fro(r["m"].numpy(), ref["momentum"]) < 1e-6
+        finite_w = torch.isfinite(mat[0]).numpy()
+        # entries of W that were not finite stay so; every other entry moved by U
+        assert not torch.isfinite(r["w"]).numpy()[~finite_w].any()
+        u = np.where(finite_w, r["u"], 0.0)
+        u_ref = np.where(finite_w, ref["update"], 0.0)
+        tol = {"G": TOL_G, "NORM": TOL_NORM}.get(variant) or tol_l(ref)
+        err = check_update(f"finite check {variant} t={t} #{i}", u, u_ref, tol)
+        _say(f"  #{i}: {counts[i]} non-finite entries, update err {err:.2e} (tol {tol:.1e})")
+    # a step without the flag leaves no counts to read
+    run_step(ctx, variant, clean, t, debug=False, rank=16)
+    with pytest.raises(N.NormPreError):
+        N.normpre_nonfinite_counts(ctx, len(mats))
