@@ -68,6 +68,8 @@ def parse():
     p.add_argument("--crossover", action="store_true",
                    help="time NormPre-G against NormPre-L at every rank of the large single-matrix "
                         "sweep (one matrix per step) and report the cost crossover instead")
+    p.add_argument("--ceiling-mib", type=int, default=256,
+                   help="MiB per fp32 array of the streaming-ceiling reference kernels (0: skip)")
     p.add_argument("--copy-mib", type=int, default=0,
                    help="also run a plain device copy of this many MiB (reference kernel for "
                         "calibrating the HBM byte counters) and report its bandwidth")
@@ -142,6 +144,69 @@ def copy_reference(torch, mib):
     torch.cuda.empty_cache()
     return {"mib": mib, "bytes_read": mib << 20, "bytes_written": mib << 20, "launches": reps + 1,
             "ms_per_copy_min": round(ms, 4), "gb_per_s": round(2.0 * (mib << 20) / (ms * 1e-3) / 1e9, 1)}
+
+
+# Byte mixes of the normalization passes (normpre_stream_ceiling): bytes per
+# element and what they stand for.
+STREAM_MIXES = {0: (18, "row-active normalize: read 3 fp32, write fp32 + fp16"),
+                1: (16, "column-active statistics: read 3 fp32, write fp32"),
+                2: (10, "column-active apply: read 2 fp32, write fp16"),
+                3: (8, "copy: read fp32, write fp32")}
+
+
+def stream_ceiling(N, torch, mib):
+    """Attainable streaming bandwidth with each normalization byte mix: the
+    library's reference kernels over `mib` MiB per fp32 array, best of 10."""
+    n = (mib << 20) // 4
+    dev = torch.device("cuda:0")
+    a, b, c = (torch.randn(n, device=dev) for _ in range(3))
+    o32 = torch.empty(n, device=dev)
+    o16 = torch.empty(n, device=dev, dtype=torch.float16)
+    out = {}
+    for mix, (bpe, what) in STREAM_MIXES.items():
+        N.normpre_stream_ceiling(mix, a, b, c, o32, o16)
+        torch.cuda.synchronize()
+        best = None
+        for _ in range(10):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            N.normpre_stream_ceiling(mix, a, b, c, o32, o16)
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1)
+            best = ms if best is None else min(best, ms)
+        out[str(mix)] = {"gb_per_s": round(bpe * n / (best * 1e-3) / 1e9, 1), "bytes_per_element": bpe,
+                         "mix": what}
+    del a, b, c, o32, o16
+    torch.cuda.empty_cache()
+    return out
+
+
+def normalize_rooflines(cls, ceiling):
+    """Normalization rooflines per orientation on the algorithmic 18 B per
+    element (read G, M_prev, W; write M and fp16 Psi), with the fraction of
+    the measured ceiling of the same byte mix; the column-active pass also
+    on the 26 B it moves (statistics 16 B + apply 10 B) against the ceiling
+    of those two mixes."""
+    out = {}
+    for name, label in (("normalize", "row-active"), ("normalize_col", "column-active")):
+        r = roofline_of(cls.get(name), "hbm")
+        if not r:
+            continue
+        r["kernel"] = f"momentum + tangent + normalization, {label}"
+        if ceiling:
+            c0 = ceiling["0"]["gb_per_s"]
+            r["ceiling_gbs_same_mix"] = c0
+            r["frac_of_ceiling"] = round(r["achieved"] / c0, 4)
+            if name == "normalize_col":
+                sec = cls[name]["ms"] / 1e3
+                moved = cls[name]["bytes"] * 26.0 / 18.0
+                t_ceil = cls[name]["bytes"] / 18.0 * (16.0 / (ceiling["1"]["gb_per_s"] * 1e9) +
+                                                      10.0 / (ceiling["2"]["gb_per_s"] * 1e9))
+                r["moved_gbs"] = round(moved / sec / 1e9, 1)
+                r["moved_frac_of_ceiling"] = round(t_ceil / sec, 4)
+        out[name] = r
+    return out
 
 
 def kclass_totals(N, ctx):
@@ -373,6 +438,7 @@ def main():
     rank = a.rank or wl.rank
     variants = [v.strip().upper() for v in a.variants.split(",") if v.strip()]
     traffic = measured_traffic(wl.name)
+    ceiling = stream_ceiling(N, torch, a.ceiling_mib) if a.ceiling_mib > 0 else None
     res = {}
     for v in variants:
         r = time_variant(N, WL, torch, wl, v, a.steps, a.warmup, rank)
@@ -382,7 +448,7 @@ def main():
             roof = ns_roofline(ns, wl.shapes, a.steps)
             roof["kernel"] = "Newton-Schulz GEMMs (gram + poly + Gram-space products + combine, fp16 MFMA)"
         elif v == "NORM":
-            roof = roofline_of(cls["normalize"], "hbm")
+            roof = roofline_of(merge_classes(cls, ["normalize", "normalize_col"]), "hbm")
             roof["kernel"] = "momentum + tangent + normalization"
         elif v == "LX":
             roof = roofline_of(cls["eigen"], "hbm")
@@ -394,9 +460,7 @@ def main():
         if roof and v in traffic:
             roof["traffic"] = round(traffic[v]["bytes_per_launch"], 1)
             roof["traffic_detail"] = traffic[v]
-        norm_roof = roofline_of(cls["normalize"], "hbm")
-        if norm_roof:
-            norm_roof["kernel"] = "momentum + tangent + normalization"
+        norm_roof = normalize_rooflines(cls, ceiling)
         total_dev = sum(c["ms"] for c in cls.values())
         res[v] = {
             "steps_per_s": round(1e3 / r["ms_per_step"], 3),
@@ -479,6 +543,8 @@ def main():
     }
     if gpt2:
         line["gpt2_small"] = gpt2
+    if ceiling:
+        line["stream_ceiling"] = ceiling
     if copy_ref:
         line["copy_reference"] = copy_ref
     if rel:

@@ -377,7 +377,8 @@ int normpre_sketch_omega(uint64_t seed, int64_t step, int32_t matrix_id,
                          int64_t b, int32_t l, float* dev_out, void* stream);
 
 /* Kernel classes reported by normpre_kernel_stats(). */
-#define NORMPRE_KCLASS_NORMALIZE   0  /* momentum + tangent + row/col normalization */
+#define NORMPRE_KCLASS_NORMALIZE   0  /* momentum + tangent + normalization, row-active */
+                                      /* (and the both-axes column pass)           */
 #define NORMPRE_KCLASS_NS_GRAM     1  /* Newton-Schulz A = X X^T                     */
 #define NORMPRE_KCLASS_NS_POLY     2  /* Newton-Schulz B = bA + cA^2, and the s x s  */
                                       /* products of the Gram-space schedule        */
@@ -389,7 +390,9 @@ int normpre_sketch_omega(uint64_t seed, int64_t step, int32_t matrix_id,
 #define NORMPRE_KCLASS_SK_SMALL    6  /* Omega, reductions, CholQR, eigensolver      */
 #define NORMPRE_KCLASS_L_APPLY     7  /* localized apply + RMS + weight update       */
 #define NORMPRE_KCLASS_EIGEN       8  /* dense eigensolver of exact NormPre-L        */
-#define NORMPRE_KCLASS_COUNT       9
+#define NORMPRE_KCLASS_NORMALIZE_COL 9 /* momentum + tangent + normalization,         */
+                                      /* column-active (statistics, finalize, apply) */
+#define NORMPRE_KCLASS_COUNT      10
 
 /*
  * Per-kernel-class totals since the last reset, over steps made with
@@ -408,6 +411,24 @@ int normpre_sketch_omega(uint64_t seed, int64_t step, int32_t matrix_id,
 int normpre_kernel_stats(normpre_ctx* ctx, int kclass, int64_t* launches,
                          double* device_ms, double* flops, double* exec_flops,
                          double* bytes, int reset);
+
+/*
+ * Streaming-bandwidth reference kernels with the byte mixes of the
+ * normalization passes, for measuring the attainable HBM ceiling those
+ * passes are held to (n elements, n % 4 == 0, 16-byte aligned device
+ * buffers; the result values are of no interest):
+ *   mix 0: read a, b, c (fp32); write out32 (fp32) and out16 (fp16)  18 B/element
+ *          (the row-active momentum + tangent + normalization pass)
+ *   mix 1: read a, b, c; write out32                                 16 B/element
+ *          (the column-active statistics pass)
+ *   mix 2: read a, b; write out16                                    10 B/element
+ *          (the column-active normalization pass)
+ *   mix 3: read a; write out32 (a plain copy)                          8 B/element
+ * Buffers a mix does not use may be null.  Enqueued on `stream`.
+ * Errors: INVALID_ARG (mix, n, null or misaligned buffers), HIP_ERROR.
+ */
+int normpre_stream_ceiling(int mix, int64_t n, const float* a, const float* b, const float* c,
+                           float* out32, void* out16, void* stream);
 
 /* Library version string (static storage). */
 const char* normpre_version(void);

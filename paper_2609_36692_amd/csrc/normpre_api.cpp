@@ -698,7 +698,7 @@ int run_normalize(const StepCtx& sc, const Dims& d, const GWork& w, const std::v
                              }),
                        "normalize both axes");
         } else {
-            NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NORMALIZE, 0.0, bytes * cnt,
+            NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NORMALIZE_COL, 0.0, bytes * cnt,
                          [&] {
                              return launch_normalize_cols(
                                  a, cnt,
@@ -2247,6 +2247,19 @@ int normpre_nonfinite_counts(normpre_ctx* ctx, int64_t* counts, int num_mats) {
     if (e == hipSuccess)
         e = hipMemcpy(counts, ctx->status, sizeof(long long) * (size_t)num_mats, hipMemcpyDeviceToHost);
     if (e != hipSuccess) return hip_fail(ctx, e, "non-finite counts");
+    return NORMPRE_OK;
+}
+
+int normpre_stream_ceiling(int mix, int64_t n, const float* a, const float* b, const float* c, float* out32,
+                           void* out16, void* stream) {
+    if (mix < 0 || mix > 3 || n < 4 || n % 4 || !a) return set_err(nullptr, NORMPRE_ERR_INVALID_ARG, "bad stream probe");
+    if ((mix <= 1 && (!b || !c)) || (mix == 2 && !b) || (mix != 2 && !out32) || ((mix == 0 || mix == 2) && !out16))
+        return set_err(nullptr, NORMPRE_ERR_INVALID_ARG, "null buffer for this mix");
+    const void* ptrs[] = {a, b, c, out32, out16};
+    for (const void* q : ptrs)
+        if (reinterpret_cast<uintptr_t>(q) & 15) return set_err(nullptr, NORMPRE_ERR_INVALID_ARG, "buffers must be 16-byte aligned");
+    hipError_t e = launch_stream_probe(mix, n, a, b, c, out32, static_cast<half_t*>(out16), static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return set_err(nullptr, NORMPRE_ERR_HIP, fmt("stream probe: %s", hipGetErrorString(e)));
     return NORMPRE_OK;
 }
 

@@ -988,6 +988,70 @@ hipError_t launch_alignment_finalize(const double* part, int num_mats, double* c
     return hipGetLastError();
 }
 
+// Each thread moves kProbeU 16-byte vectors per iteration, every load of the
+// iteration issued before the first store.
+constexpr int kProbeU = 4;
+template <int MIX>
+__global__ void __launch_bounds__(256) stream_probe_kernel(const float4* a, const float4* b, const float4* c,
+                                                           float4* o32, uint2* o16, int64_t n4) {
+    const int64_t step = (int64_t)gridDim.x * 256 * kProbeU;
+    for (int64_t base = (int64_t)blockIdx.x * 256 * kProbeU + threadIdx.x; base < n4; base += step) {
+        float4 x[kProbeU], y[kProbeU], z[kProbeU];
+#pragma unroll
+        for (int u = 0; u < kProbeU; ++u) {
+            const int64_t i = base + u * 256;
+            if (i < n4) {
+                x[u] = a[i];
+                if constexpr (MIX != 3) y[u] = b[i];
+                if constexpr (MIX <= 1) z[u] = c[i];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kProbeU; ++u) {
+            const int64_t i = base + u * 256;
+            if (i >= n4) break;
+            if constexpr (MIX == 3) {
+                o32[i] = x[u];
+            } else if constexpr (MIX == 2) {
+                half_t h[4] = {(half_t)(x[u].x - y[u].x), (half_t)(x[u].y - y[u].y), (half_t)(x[u].z - y[u].z),
+                               (half_t)(x[u].w - y[u].w)};
+                o16[i] = *reinterpret_cast<const uint2*>(h);
+            } else {
+                float4 m;
+                m.x = fmaf(0.95f, x[u].x, y[u].x); m.y = fmaf(0.95f, x[u].y, y[u].y);
+                m.z = fmaf(0.95f, x[u].z, y[u].z); m.w = fmaf(0.95f, x[u].w, y[u].w);
+                if constexpr (MIX == 1) {
+                    m.x += z[u].x; m.y += z[u].y; m.z += z[u].z; m.w += z[u].w;
+                    o32[i] = m;
+                } else {
+                    o32[i] = m;
+                    half_t h[4] = {(half_t)z[u].x, (half_t)z[u].y, (half_t)z[u].z, (half_t)z[u].w};
+                    o16[i] = *reinterpret_cast<const uint2*>(h);
+                }
+            }
+        }
+    }
+}
+
+hipError_t launch_stream_probe(int mix, int64_t n, const float* a, const float* b, const float* c, float* o32,
+                               half_t* o16, hipStream_t s) {
+    if (n < 4 || n % 4 || mix < 0 || mix > 3) return hipErrorInvalidValue;
+    const int64_t n4 = n / 4;
+    const unsigned blocks = (unsigned)std::min<int64_t>((n4 + 256 * kProbeU - 1) / (256 * kProbeU), 4096);
+    auto A = reinterpret_cast<const float4*>(a);
+    auto B = reinterpret_cast<const float4*>(b);
+    auto C = reinterpret_cast<const float4*>(c);
+    auto O = reinterpret_cast<float4*>(o32);
+    auto H = reinterpret_cast<uint2*>(o16);
+    switch (mix) {
+        case 0: hipLaunchKernelGGL(stream_probe_kernel<0>, dim3(blocks), dim3(256), 0, s, A, B, C, O, H, n4); break;
+        case 1: hipLaunchKernelGGL(stream_probe_kernel<1>, dim3(blocks), dim3(256), 0, s, A, B, C, O, H, n4); break;
+        case 2: hipLaunchKernelGGL(stream_probe_kernel<2>, dim3(blocks), dim3(256), 0, s, A, B, C, O, H, n4); break;
+        default: hipLaunchKernelGGL(stream_probe_kernel<3>, dim3(blocks), dim3(256), 0, s, A, B, C, O, H, n4); break;
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t s) {
     if (bytes <= 0) return hipSuccess;
     if (bytes % 16 || (reinterpret_cast<uintptr_t>(p) & 15)) return hipErrorInvalidValue;

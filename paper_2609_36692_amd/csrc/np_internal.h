@@ -349,6 +349,15 @@ hipError_t launch_eig_select(const EigArgs& a, int batch, hipStream_t s);
 
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t s);
 
+// Streaming ceilings with the byte mixes of the normalization passes (n
+// elements, a multiple of 4; 16-byte aligned buffers):
+//   0: read a, b, c, write o32 = 0.95 a + b and o16 = fp16(c)   18 B/element
+//   1: read a, b, c, write o32 = 0.95 a + b + c                16 B/element
+//   2: read a, b, write o16 = fp16(a - b)                     10 B/element
+//   3: read a, write o32 = a                                    8 B/element
+hipError_t launch_stream_probe(int mix, int64_t n, const float* a, const float* b, const float* c, float* o32,
+                               half_t* o16, hipStream_t s);
+
 // Descent alignment (App. A, training dynamics): per matrix the cosine of the
 // gradient G and the update direction Phi = (W_before - W_after) / lr -
 // wd W_before (the update before learning-rate scaling, weight decay

@@ -63,9 +63,10 @@ NORMPRE_KCLASS_SK_STREAM = 5
 NORMPRE_KCLASS_SK_SMALL = 6
 NORMPRE_KCLASS_L_APPLY = 7
 NORMPRE_KCLASS_EIGEN = 8
-NORMPRE_KCLASS_COUNT = 9
+NORMPRE_KCLASS_NORMALIZE_COL = 9
+NORMPRE_KCLASS_COUNT = 10
 KCLASS_NAMES = ["normalize", "ns_gram", "ns_poly", "ns_combine", "g_update",
-                "sk_stream", "sk_small", "l_apply", "eigen"]
+                "sk_stream", "sk_small", "l_apply", "eigen", "normalize_col"]
 
 
 class NormPreError(RuntimeError):
@@ -132,6 +133,7 @@ def load_library(path: str = LIB_PATH):
                                                      ctypes.POINTER(ctypes.c_double),
                                                      ctypes.POINTER(ctypes.c_double), P]),
         "normpre_nonfinite_counts": (ctypes.c_int, [P, i64p, ctypes.c_int]),
+        "normpre_stream_ceiling": (ctypes.c_int, [ctypes.c_int, ctypes.c_int64, P, P, P, P, P, P]),
         "normpre_workspace_size": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, i64p, hpp, i64p]),
         "normpre_reserve": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int, i64p, hpp, P]),
         "normpre_workspace_bytes": (ctypes.c_int, [P, i64p]),
@@ -248,6 +250,15 @@ def normpre_nonfinite_counts(ctx, num_mats: int) -> np.ndarray:
     _check(load_library().normpre_nonfinite_counts(ctx, out.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
                                                     int(num_mats)), ctx)
     return out[:num_mats]
+
+
+def normpre_stream_ceiling(mix: int, a, b, c, out32, out16, stream=None) -> None:
+    """Streaming reference kernel with a normalization pass's byte mix
+    (fp32 tensors a, b, c, out32 and an fp16 out16 of the same length)."""
+    n = a.numel()
+    vp = lambda x: ctypes.c_void_p(_ptr(x)) if x is not None else None  # noqa: E731
+    _check(load_library().normpre_stream_ceiling(int(mix), n, vp(a), vp(b), vp(c), vp(out32), vp(out16),
+                                                 _stream_handle(stream)))
 
 
 def normpre_workspace_size(variant: int, shapes, hp: normpre_hparams) -> int:
