@@ -792,11 +792,15 @@ int run_muon_input(const StepCtx& sc, const Dims& d, const GWork& w, const std::
 // x56 (560 large tiles) ran 648 TFLOP/s on the small tile against 584 on the
 // large one, 2048^3 x84 (3024 large tiles) 717 against 740; the combine
 // switches earlier (12-matrix launches: 432 large tiles faster than the
-// small ones, 324 slower).
-TileCfg ns_cfg(int64_t M, int64_t N, bool sym, int count) {
+// small ones, 324 slower).  A long reduction (K >= 4096) amortizes the
+// large tile's multi-pass epilogue, and there 512 tiles suffice: a single
+// symmetric 8192^3 product (528 large tiles) runs ~15% faster on the large
+// tile than on the small one.  `K` is the shortest reduction of the launch.
+TileCfg ns_cfg(int64_t M, int64_t N, int64_t K, bool sym, int count) {
     const int64_t tm = M / 256, tn = N / 256;
     const int64_t tiles = (sym ? tm * (tm + 1) / 2 : tm * tn) * count;
-    return tiles >= (sym ? 1024 : 384) ? TileCfg::Big256 : TileCfg::Big;
+    const int64_t sym_min = K >= 4096 ? 512 : 1024;
+    return tiles >= (sym ? sym_min : 384) ? TileCfg::Big256 : TileCfg::Big;
 }
 
 // MFMA FLOPs a product launch issues for `count` matrices of M x N x K with
@@ -840,7 +844,9 @@ int gram_pool_launch(const StepCtx& sc, std::vector<const Item*> its, const Pool
     e.out = pl.amat; e.ld_out = pl.sp; e.stride_out = ss;
     e.mul_pow = first_it ? 2 : 0;
     e.ca = 1.f; e.cs = 0.f;
-    const TileCfg cfg = ns_cfg(pl.sp, pl.sp, true, total);
+    int64_t kmin = its[0]->d.lp_;
+    for (const Item* it : its) kmin = std::min(kmin, it->d.lp_);
+    const TileCfg cfg = ns_cfg(pl.sp, pl.sp, kmin, true, total);
     double issued = 0.0;
     for (const Item* it : its) issued += issued_flops(cfg, pl.sp, pl.sp, it->d.lp_, true, it->count);
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_GRAM, flops, bytes,
@@ -881,7 +887,7 @@ int poly_launch(const StepCtx& sc, const Pool& pl, int first, int cnt, half_t* o
     e.out = out; e.ld_out = sp; e.stride_out = ss;
     e.src = a0; e.ld_src = sp; e.stride_src = ss;
     e.ca = sc.hp->ns_coeffs[2]; e.cs = sc.hp->ns_coeffs[1];
-    const TileCfg cfg = ns_cfg(sp, sp, true, cnt);
+    const TileCfg cfg = ns_cfg(sp, sp, sp, true, cnt);
     // Nominal FLOPs use the real s of each matrix (padding excluded); bytes
     // are A read once and B written once (4 s^2 per matrix).
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_POLY, nominal_flops, 2.0 * nominal_flops / (double)sp,
@@ -1006,7 +1012,7 @@ int gns_product(const StepCtx& sc, const Pool& pl, const half_t* smat, const hal
     e.out = out; e.ld_out = sp; e.stride_out = ss;
     e.src = r; e.ld_src = sp; e.stride_src = ss;
     e.ca = 1.f; e.cs = cs;
-    const TileCfg cfg = ns_cfg(sp, sp, true, pl.gns_count);
+    const TileCfg cfg = ns_cfg(sp, sp, sp, true, pl.gns_count);
     // Bytes: S and R read once, the result written once (6 s^2 per matrix).
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_NS_POLY, flops, 3.0 * flops / (double)sp,
                  [&] { return launch_gemm_affine(cfg, 0, A, B, sh, pl.gns_count, e, sc.s); },
@@ -1143,7 +1149,7 @@ int run_round_g(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& 
     // Combine tiles: the plain-iteration wide items of a pool share launches;
     // tall and Gram-space items run per item.
     for (Item& it : items)
-        if (it.d.tall || it.gns) it.ccfg = ns_cfg(it.d.mp, it.d.np_, false, it.count);
+        if (it.d.tall || it.gns) it.ccfg = ns_cfg(it.d.mp, it.d.np_, it.d.sp, false, it.count);
     const auto wide = wide_combine_chunks(items, pools.size());
     for (int iter = 0; iter < q; ++iter) {
         const bool first_it = iter == 0 && fold_scale, last_it = iter == q - 1;
