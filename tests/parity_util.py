@@ -10,10 +10,14 @@
   independent rounding errors deviates from the mean error by O(1/sqrt(b)),
   and single-element rows by a chi(1) factor, below 4 for a few hundred rows).
 * ``record``: per-case error, tolerance and margin.  When the environment
-  variable NORMPRE_PARITY_LOG names a file, the session writes every record
-  there as a Markdown table at its end (see conftest.py).
+  variable NORMPRE_PARITY_LOG names a file, the session writes a Markdown
+  summary there at its end (see conftest.py): per test function the number
+  of checks and the smallest and median margin, then the tightest checks.
 """
 from __future__ import annotations
+
+import os
+import sys
 
 import numpy as np
 
@@ -35,9 +39,14 @@ def localized_error(u, ref) -> float:
     return worst
 
 
+def _test_family() -> str:
+    node = os.environ.get("PYTEST_CURRENT_TEST", "?").split(" ")[0]
+    return node.split("[")[0]
+
+
 def record(case: str, quantity: str, err: float, tol: float, **extra) -> None:
-    RECORDS.append({"case": case, "quantity": quantity, "err": float(err), "tol": float(tol),
-                    "margin": float(tol) / max(float(err), 1e-300), **extra})
+    RECORDS.append({"test": _test_family(), "case": case, "quantity": quantity, "err": float(err),
+                    "tol": float(tol), "margin": float(tol) / float(err) if err > 0 else float("inf"), **extra})
 
 
 def check_update(case: str, u, ref_u, tol: float, **extra) -> float:
@@ -53,15 +62,36 @@ def check_update(case: str, u, ref_u, tol: float, **extra) -> float:
     return err
 
 
-def write_markdown(path: str) -> None:
-    lines = ["| case | quantity | error | tolerance | tol / err | notes |", "|---|---|---|---|---|---|"]
+def _row(r: dict) -> str:
+    notes = ", ".join(f"{k} {v:.3g}" if isinstance(v, float) else f"{k} {v}" for k, v in r.items()
+                      if k not in ("test", "case", "quantity", "err", "tol", "margin"))
+    return f"| {_md(r['case'])} | {_md(r['quantity'])} | {r['err']:.3e} | {r['tol']:.3e} | {r['margin']:.1f} | {notes} |"
+
+
+def _md(text: str) -> str:
+    return str(text).replace("|", "\\|")
+
+
+def write_markdown(path: str, tightest: int = 40) -> None:
+    """Per test function: checks, smallest and median tol/err; then the
+    `tightest` checks with the smallest margins in full."""
+    fams: dict[str, list[dict]] = {}
     for r in RECORDS:
-        notes = ", ".join(f"{k} {v:.3g}" if isinstance(v, float) else f"{k} {v}" for k, v in r.items()
-                          if k not in ("case", "quantity", "err", "tol", "margin"))
-        lines.append(f"| {r['case']} | {r['quantity']} | {r['err']:.3e} | {r['tol']:.3e} | {r['margin']:.1f} | {notes} |")
-    worst = min(RECORDS, key=lambda r: r["margin"]) if RECORDS else None
-    head = [f"{len(RECORDS)} checks."]
-    if worst:
-        head.append(f"Smallest margin: {worst['margin']:.2f} ({worst['case']}, {worst['quantity']}).")
+        fams.setdefault(r["test"], []).append(r)
+    cmd = "NORMPRE_PARITY_LOG=<file> python -m pytest " + " ".join(sys.argv[1:])
+    out = ["# Parity margins of the GPU tests against the oracle", "",
+           f"Written at the end of `{cmd}` (repository root).  tol / err > 1 passes; "
+           "`U worst row/col` is the largest row or column error relative to the RMS row (column) norm; "
+           "inf marks a bit-identical result.", "",
+           f"{len(RECORDS)} checks in {len(fams)} test functions.", "",
+           "| test | checks | quantities | smallest tol/err (case) | median tol/err |", "|---|---|---|---|---|"]
+    for name, rs in sorted(fams.items()):
+        w = min(rs, key=lambda r: r["margin"])
+        qs = ", ".join(sorted({_md(r["quantity"]) for r in rs}))
+        med = float(np.median([r["margin"] for r in rs]))
+        out.append(f"| {name} | {len(rs)} | {qs} | {w['margin']:.2f} ({_md(w['case'])}, {_md(w['quantity'])}) | {med:.1f} |")
+    out += ["", f"The {min(tightest, len(RECORDS))} checks with the smallest margins:", "",
+            "| case | quantity | error | tolerance | tol / err | notes |", "|---|---|---|---|---|---|"]
+    out += [_row(r) for r in sorted(RECORDS, key=lambda r: r["margin"])[:tightest]]
     with open(path, "w") as f:
-        f.write(" ".join(head) + "\n\n" + "\n".join(lines) + "\n")
+        f.write("\n".join(out) + "\n")
