@@ -409,10 +409,14 @@ int combine_tiles(const Dims& d, TileCfg cfg) {
     return (int)((d.mp / t) * (d.np_ / t));
 }
 
-// Split count for a skinny product with output length n_out and reduction length k_len.
+// Split count for a skinny product with output length n_out and reduction
+// length k_len: doubled until the launch has one block per CU (256) or the
+// chunks get short.  More splits stream Psi with more blocks but cost a
+// reduction launch; one split writes the result directly (on GPT-2 Small's
+// NormPre-L step a 1024-block target measured 2.7% slower).
 int pick_splits(int64_t tiles_per_mat, int count, int64_t k_len) {
     int splits = 1;
-    while (splits < kMaxSplits && tiles_per_mat * count * splits < 1024 && k_len / (64 * splits * 2) >= 4)
+    while (splits < kMaxSplits && tiles_per_mat * count * splits < 256 && k_len / (64 * splits * 2) >= 4)
         splits *= 2;
     return splits;
 }
@@ -1259,7 +1263,7 @@ int sketch_product_run(const StepCtx& sc, const std::vector<const Item*>& its, b
     SketchGroups g{};
     ReduceGroups r{};
     TileCfg cfg = TileCfg::Skinny64;
-    int layout = -1, total = 0;
+    int layout = -1, total = 0, rtotal = 0;
     int64_t lp0 = 0;
     double flops = 0.0, bytes = 0.0;
     // The split count comes from the launch's total tile count: every item's
@@ -1291,27 +1295,35 @@ int sketch_product_run(const StepCtx& sc, const std::vector<const Item*>& its, b
         const int64_t k_chunk = round_up((k_len + splits - 1) / splits, 64);
         const int real_splits = (int)((k_len + k_chunk - 1) / k_chunk);
         const int i = g.n++;
-        g.zbeg[i] = r.zbeg[i] = total;
+        g.zbeg[i] = total;
         g.a[i] = io.v16; g.lda[i] = k_len; g.a_stride[i] = lp * maxpad;
         g.b[i] = io.src ? io.src : w.psi; g.ldb[i] = d.np_; g.b_stride[i] = mn;
         g.N[i] = (int)n_out; g.K[i] = (int)k_len; g.k_chunk[i] = (int)k_chunk; g.splits[i] = real_splits;
         g.out[i] = w.part; g.stride_split[i] = lp * n_out; g.stride_mat[i] = (int64_t)kMaxSplits * lp * maxpad;
-        r.part[i] = w.part; r.splits[i] = real_splits;
-        r.stride_split[i] = lp * n_out; r.stride_mat[i] = (int64_t)kMaxSplits * lp * maxpad;
-        r.n4[i] = lp * n_out / 4;
-        r.out32[i] = io.out32; r.out16[i] = io.out16; r.scale16[i] = io.scale16; r.stride_out[i] = lp * maxpad;
+        g.out32[i] = io.out32; g.out16[i] = io.out16; g.scale16[i] = io.scale16; g.stride_out[i] = lp * maxpad;
+        // One split: the product launch writes the outputs itself.
+        if (real_splits > 1 && (io.out32 || io.out16)) {
+            const int j = r.n++;
+            r.zbeg[j] = rtotal;
+            r.part[j] = w.part; r.splits[j] = real_splits;
+            r.stride_split[j] = lp * n_out; r.stride_mat[j] = (int64_t)kMaxSplits * lp * maxpad;
+            r.n4[j] = lp * n_out / 4;
+            r.out32[j] = io.out32; r.out16[j] = io.out16; r.scale16[j] = io.scale16; r.stride_out[j] = lp * maxpad;
+            rtotal += it->count;
+        }
         flops += 2.0 * d.ell * (double)d.m * (double)d.n * it->count;
         bytes += 2.0 * (double)d.m * (double)d.n * it->count;
         total += it->count;
     }
     if (g.n == 0) return NORMPRE_OK;
-    g.zbeg[g.n] = r.zbeg[g.n] = total;
-    r.n = g.n;
+    g.zbeg[g.n] = total;
+    r.zbeg[r.n] = rtotal;
     NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_STREAM, flops, bytes,
                  [&] { return launch_gemm_partial_grouped(cfg, layout, (int)lp0, g, sc.s); }),
            "sketch product");
-    NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_reduce_splits_grouped(r, sc.s); }),
-           "reduce splits");
+    if (r.n > 0)
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_reduce_splits_grouped(r, sc.s); }),
+               "reduce splits");
     return NORMPRE_OK;
 }
 

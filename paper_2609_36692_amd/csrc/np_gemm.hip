@@ -514,8 +514,26 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
         float* out;
         int64_t ldo;
         if constexpr (IsSkGrouped<Epi>::value) {
-            out = epi.sg.out[sgi] + (int64_t)slz * epi.sg.stride_mat[sgi] + (int64_t)split * epi.sg.stride_split[sgi];
             ldo = epi.sg.N[sgi];
+            float* const o32 = epi.sg.out32[sgi];
+            half_t* const o16 = epi.sg.out16[sgi];
+            if (epi.sg.splits[sgi] == 1 && (o32 || o16)) {
+                // One split: the final product, as the split reduction
+                // would write it.
+                const int64_t zoff = (int64_t)slz * epi.sg.stride_out[sgi];
+                const float sc16 = epi.sg.scale16[sgi];
+#pragma unroll
+                for (int qi = 0; qi < NQ; ++qi)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int64_t idx = zoff + (int64_t)(rw0 + quad_row(qi) + r) * ldo + cw0 + quad_col(qi);
+                        const float v = quad_val(qi, r);
+                        if (o32) o32[idx] = v;
+                        if (o16) o16[idx] = (half_t)(v * sc16);
+                    }
+                return;
+            }
+            out = epi.sg.out[sgi] + (int64_t)slz * epi.sg.stride_mat[sgi] + (int64_t)split * epi.sg.stride_split[sgi];
         } else {
             out = epi.out + (int64_t)z * epi.stride_mat + (int64_t)split * epi.stride_split;
             ldo = epi.ld_out;

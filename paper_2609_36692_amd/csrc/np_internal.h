@@ -104,6 +104,10 @@ hipError_t launch_gemm_partial(TileCfg cfg, int layout, Operand A, Operand B,
 // output length N, reduction length K in `splits` chunks of k_chunk, fp32
 // partials out[i][split][mm][nn] (ld N).  N, K and k_chunk are multiples of
 // the tile sizes and of 64; chunk `splits - 1` is the last non-empty one.
+// A group with one split and a final output (out32 and/or out16 set) gets
+// the product itself instead of a partial: fp32 into out32 and fp16 of
+// scale16 times it into out16 (ld N, matrix stride stride_out), the values a
+// one-split reduction would write.
 struct SketchGroups {
     int n;
     int zbeg[kMaxItems + 1];
@@ -111,6 +115,7 @@ struct SketchGroups {
     const half_t* b[kMaxItems]; int64_t ldb[kMaxItems]; int64_t b_stride[kMaxItems];
     int N[kMaxItems], K[kMaxItems], k_chunk[kMaxItems], splits[kMaxItems];
     float* out[kMaxItems]; int64_t stride_split[kMaxItems]; int64_t stride_mat[kMaxItems];
+    float* out32[kMaxItems]; half_t* out16[kMaxItems]; float scale16[kMaxItems]; int64_t stride_out[kMaxItems];
 };
 hipError_t launch_gemm_partial_grouped(TileCfg cfg, int layout, int M, const SketchGroups& g, hipStream_t s);
 // Newton-Schulz combines X <- a X + B X of the wide shape groups of one s in
