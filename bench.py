@@ -54,8 +54,8 @@ PAPER_STEPS_PER_S = {
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=20)
-    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", default="qwen3_1p7b")
     p.add_argument("--no-gpt2", action="store_true",
                    help="skip the GPT-2 Small stack reported next to the headline workload")
