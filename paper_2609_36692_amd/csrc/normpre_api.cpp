@@ -1266,13 +1266,24 @@ int sketch_product_run(const StepCtx& sc, const std::vector<const Item*>& its, b
     int layout = -1, total = 0, rtotal = 0;
     int64_t lp0 = 0;
     double flops = 0.0, bytes = 0.0;
+    // l_pad = 64 takes 512-wide output tiles when every product's output
+    // length allows it (half the re-reads of the l-major operand per byte of
+    // Psi streamed), else 256-wide ones.
+    bool wide = true;
+    for (const Item* it : its) {
+        const bool pv = over_active == (it->d.k == 0);
+        wide = wide && ((pv ? it->d.mp : it->d.np_) % 512 == 0);
+    }
+    auto tile_of = [&](int64_t lp) {
+        return lp == 128 ? TileCfg::Skinny128 : wide ? TileCfg::Skinny64W : TileCfg::Skinny64;
+    };
     // The split count comes from the launch's total tile count: every item's
     // split chunks fill the chip together.
     int64_t all_tiles = 0;
     for (const Item* it : its) {
         const Dims& d = it->d;
         const bool pv = over_active == (d.k == 0);
-        const TileCfg c = d.ellp == 128 ? TileCfg::Skinny128 : TileCfg::Skinny64;
+        const TileCfg c = tile_of(d.ellp);
         all_tiles += (d.ellp / gemm_tile_m(c)) * ((pv ? d.mp : d.np_) / gemm_tile_n(c)) * it->count;
     }
     for (const Item* it : its) {
@@ -1283,7 +1294,7 @@ int sketch_product_run(const StepCtx& sc, const std::vector<const Item*>& its, b
         const bool pv = over_active == (d.k == 0);
         const int64_t n_out = pv ? d.mp : d.np_;
         const int64_t k_len = pv ? d.np_ : d.mp;
-        const TileCfg c = lp == 128 ? TileCfg::Skinny128 : TileCfg::Skinny64;
+        const TileCfg c = tile_of(lp);
         if (layout < 0) {
             cfg = c;
             layout = pv ? 0 : 1;

@@ -339,8 +339,9 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     using LB = typename LoaderSel<(LAYOUT >= 1), BN, NT>::type;
     // DEEP: two staging sets, so each K-step's global loads have two
     // K-steps to arrive (covers L2 misses served from the Infinity Cache);
-    // the 128 x 128 tile has the registers for it.
-    constexpr bool DEEP = MF == 32 && BM * BN <= 128 * 128;
+    // the tiles up to 128 x 128 have the registers for it, and so has the
+    // 64 x 512 one (eight waves: the same loads per thread as 64 x 256).
+    constexpr bool DEEP = MF == 32 && (BM * BN <= 128 * 128 || (BM == 64 && BN == 512));
     u32x4 ra[LA::N], rb[LB::N];
     u32x4 ra2[LA::N], rb2[LB::N];
 
@@ -816,6 +817,7 @@ hipError_t dispatch_cfg(TileCfg cfg, Operand A, Operand B, GemmShape sh, int bat
     switch (cfg) {
         case TileCfg::Big:       return run<128, 128, 2, 2, LAYOUT>(A, B, sh, batch, e, s);
         case TileCfg::Skinny64:  return run<64, 256, 1, 4, LAYOUT>(A, B, sh, batch, e, s);
+        case TileCfg::Skinny64W: return run<64, 512, 1, 8, LAYOUT>(A, B, sh, batch, e, s);
         case TileCfg::Skinny128: return run<128, 256, 2, 4, LAYOUT>(A, B, sh, batch, e, s);
         default: return hipErrorInvalidValue;
     }
@@ -838,6 +840,7 @@ int gemm_tile_m(TileCfg cfg) {
         case TileCfg::Big: return 128;
         case TileCfg::Big256: return 256;
         case TileCfg::Skinny64: return 64;
+        case TileCfg::Skinny64W: return 64;
         case TileCfg::Skinny128: return 128;
         case TileCfg::Apply: return 64;
     }
@@ -845,6 +848,7 @@ int gemm_tile_m(TileCfg cfg) {
 }
 int gemm_tile_n(TileCfg cfg) {
     switch (cfg) {
+        case TileCfg::Skinny64W: return 512;
         case TileCfg::Big: return 128;
         case TileCfg::Apply: return 128;
         default: return 256;
@@ -901,7 +905,8 @@ hipError_t launch_gemm_partial(TileCfg cfg, int layout, Operand A, Operand B, Ge
                                int batch, const EpiPartial& e, hipStream_t s) {
     EPar ee;
     static_cast<EpiPartial&>(ee) = e;
-    if (cfg != TileCfg::Skinny64 && cfg != TileCfg::Skinny128) return hipErrorInvalidValue;
+    if (cfg != TileCfg::Skinny64 && cfg != TileCfg::Skinny64W && cfg != TileCfg::Skinny128)
+        return hipErrorInvalidValue;
     switch (layout) {
         case 0: return dispatch_cfg<EPar, 0>(cfg, A, B, sh, batch, ee, s);
         case 1: return dispatch_cfg<EPar, 1>(cfg, A, B, sh, batch, ee, s);
@@ -910,7 +915,8 @@ hipError_t launch_gemm_partial(TileCfg cfg, int layout, Operand A, Operand B, Ge
 }
 
 hipError_t launch_gemm_partial_grouped(TileCfg cfg, int layout, int M, const SketchGroups& g, hipStream_t s) {
-    if (cfg != TileCfg::Skinny64 && cfg != TileCfg::Skinny128) return hipErrorInvalidValue;
+    if (cfg != TileCfg::Skinny64 && cfg != TileCfg::Skinny64W && cfg != TileCfg::Skinny128)
+        return hipErrorInvalidValue;
     if (g.n < 1 || g.n > kMaxItems || g.zbeg[0] != 0 || (layout != 0 && layout != 1)) return hipErrorInvalidValue;
     const int bm = gemm_tile_m(cfg), bn = gemm_tile_n(cfg);
     if (M < bm || M % bm) return hipErrorInvalidValue;

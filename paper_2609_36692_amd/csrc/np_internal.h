@@ -91,7 +91,9 @@ enum class EpiKind { Affine, Partial, Apply, ApplyNorm };
 
 // Launchers (gemm kernels, np_gemm.hip).  `layout` selects which operands
 // are MN-major: 0 = both K-major, 1 = B MN-major, 2 = both MN-major.
-enum class TileCfg { Big, Big256, Skinny64, Skinny128, Apply };
+// Skinny64 / Skinny64W / Skinny128: split-K sketch products, l-major rows
+// of 64 (or 128) by 256 (or 512) output columns.
+enum class TileCfg { Big, Big256, Skinny64, Skinny64W, Skinny128, Apply };
 hipError_t launch_gemm_affine(TileCfg cfg, int layout, Operand A, Operand B,
                               GemmShape sh, int batch, const EpiAffine& e,
                               hipStream_t s);
