@@ -91,8 +91,11 @@ struct MNMajorLoader {
     static __device__ __forceinline__ int mswz(int k) { return (4 * (k & 3)) & (CH - 1); }
     static __device__ __forceinline__ void load_item(u32x4 (&r)[N], const half_t* base, int64_t ld, int row0, int k0,
                                                      int tid, int i) {
+        // The per-thread part of the address does not depend on the K-step
+        // (hoisted out of the loop); k0 * ld is wave-uniform (scalar).
         const int k = tid / CH + i * (NT / CH), c = tid % CH;
-        r[i] = *reinterpret_cast<const u32x4*>(base + (int64_t)(k0 + k) * ld + row0 + c * 8);
+        const half_t* p = base + (int64_t)k * ld + row0 + c * 8;
+        r[i] = *reinterpret_cast<const u32x4*>(p + (int64_t)k0 * ld);
     }
     static __device__ __forceinline__ void store_item(const u32x4 (&r)[N], half_t* lds, int tid, int i) {
         const int k = tid / CH + i * (NT / CH), c = tid % CH;
