@@ -191,6 +191,35 @@ def test_l_step_parity(ctx, shape, rank, t):
     assert math.isclose(np.linalg.norm(res["u"]), 0.2 * math.sqrt(shape[0] * shape[1]), rel_tol=2e-3)
 
 
+# Zero active rows (columns): x_i = 0, so psi_i = 0 through the epsilon guard
+# of the normalization, and T, hence U, keep that row (column) exactly zero in
+# both variants (Newton-Schulz and the sketch both act through Psi's rows).
+# The other orientation sees the same zeros inside its active rows.
+ZERO_CASES = [((300, 420), "G"), ((200, 450), "G"), ((420, 300), "L"), ((300, 420), "L")]
+
+
+@pytest.mark.parametrize("shape,variant", ZERO_CASES)
+@pytest.mark.parametrize("t", [0, 1])
+def test_zero_rows_and_columns(ctx, shape, variant, t):
+    _say(f"zero rows/columns {variant} {shape} t={t}")
+    w, g, mp = (x.clone() for x in _inputs(shape, seed=3))
+    zr, zc = [0, 7, 31, shape[0] - 1], [2, 64, shape[1] - 1]
+    for x in (w, g, mp):
+        x[zr, :] = 0.0
+        x[:, zc] = 0.0
+    mat = (w, g, mp)
+    kw = {"rank": 8} if variant == "L" else {}
+    res = run_step(ctx, variant, [mat], t, debug=False, **kw)[0]
+    ref = oracle(mat, variant, t, **kw)
+    tol = TOL_G if variant == "G" else tol_l(ref)
+    check_update(f"zero rows/cols {variant} {shape} t={t}", res["u"], ref["update"], tol)
+    zero = zr if t == 0 else zc
+    u = res["u"]
+    assert np.all((u[zero, :] if t == 0 else u[:, zero]) == 0.0)
+    assert np.isfinite(u).all()
+    assert math.isclose(np.linalg.norm(u), 0.2 * math.sqrt(shape[0] * shape[1]), rel_tol=2e-3)
+
+
 # ----------------------------------------------------------- batching etc.
 def test_batched_equals_single_g(ctx):
     _say("batched vs single (G)")
