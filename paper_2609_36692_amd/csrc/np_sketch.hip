@@ -222,6 +222,22 @@ __global__ void __launch_bounds__(256) gram64_kernel(Gram64Items t, int ell_pad,
 // column as numerically dependent: its row of R and of R^{-1} is zero, so the
 // matching column of Q = Y R^{-1} is zero and it never reaches the selection.
 constexpr double kDropTol = 1e-12;
+// fp64 1/sqrt(x) and 1/x for x > 0: the hardware estimates refined by two
+// Newton steps, accurate to fp64 rounding with a much shorter dependent chain
+// than the IEEE square-root and division sequences (which sit on the
+// per-pivot critical path of the factorizations below).
+__device__ __forceinline__ double rsqrt_f64(double x) {
+    double y = __builtin_amdgcn_rsq(x);
+    const double h = 0.5 * x;
+    y = y * fma(-h * y, y, 1.5);
+    return y * fma(-h * y, y, 1.5);
+}
+__device__ __forceinline__ double rcp_f64(double x) {
+    double y = __builtin_amdgcn_rcp(x);
+    y = fma(y, fma(-x, y, 1.0), y);
+    return fma(y, fma(-x, y, 1.0), y);
+}
+
 constexpr int kCholLdsMax = 96;
 constexpr int kSmallThreads = 512;
 
@@ -279,8 +295,8 @@ __global__ void __launch_bounds__(NT) chol_inv_kernel(const double* partial, int
         for (int k = 0; k < ell; ++k) {
             const double piv = R[k * ld + k];
             const bool keep = diag0[k] > 0.0 && piv > kDropTol * diag0[k];
-            const double ipiv = keep ? 1.0 / piv : 0.0;
-            const double irk = keep ? 1.0 / sqrt(piv) : 0.0;
+            const double irk = keep ? rsqrt_f64(piv) : 0.0;
+            const double ipiv = irk * irk;
             if (tid == 0) inv_diag[k] = irk;
             for (int j = k + 1 + tid; j < ell; j += NT) R[j * ld + k] = R[k * ld + j] * irk;
 #pragma unroll
@@ -392,7 +408,7 @@ __global__ void __launch_bounds__(kCholThreads) chol_inv_panel_kernel(const doub
             const int k = k0 + r;
             const double piv = P[r * pst + r];
             const bool keep = diag0[k] > 0.0 && piv > kDropTol * diag0[k];
-            const double ipiv = keep ? 1.0 / piv : 0.0;
+            const double ipiv = keep ? rcp_f64(piv) : 0.0;
             if (tid == 0) pivot[k] = keep ? piv : 0.0;
             const double* pr = P + r * pst;
             for (int rr = r + 1 + grp; rr < kb; rr += NG) {
@@ -406,7 +422,7 @@ __global__ void __launch_bounds__(kCholThreads) chol_inv_panel_kernel(const doub
         // Rows of R: the pivot rows scaled by 1 / sqrt(pivot) (zero when dropped).
         for (int r = grp; r < kb; r += NG) {
             const double pv = pivot[k0 + r];
-            const double s = pv > 0.0 ? 1.0 / sqrt(pv) : 0.0;
+            const double s = pv > 0.0 ? rsqrt_f64(pv) : 0.0;
             if (lane == 0) inv_diag[k0 + r] = s;
             for (int c = r + lane; c < w; c += 64) {
                 const double v = P[r * pst + c] * s;
