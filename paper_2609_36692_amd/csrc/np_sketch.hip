@@ -128,8 +128,8 @@ __device__ __forceinline__ int item_of(const T& t, int z) {
 // triangles): waves without a block skip the products, so padding and
 // symmetry cost no fp64 FMAs.  The tile's rows stream through LDS 64 columns
 // at a time (columns major, so a thread reads its four rows as one float4).
-// Every entry sums in increasing column order; chunks past the item's length
-// write zeros.  Lengths and chunk lengths are multiples of 64.
+// Every entry sums in a fixed order; chunks past the item's length write
+// zeros.  Lengths and chunk lengths are multiples of 64.
 __global__ void __launch_bounds__(256) gram64_kernel(Gram64Items t, int ell_pad, double* partial) {
     const int z = blockIdx.z, chunk = blockIdx.y;
     const int g = item_of(t, z);
@@ -144,15 +144,22 @@ __global__ void __launch_bounds__(256) gram64_kernel(Gram64Items t, int ell_pad,
     float (*sb)[68] = diag ? sc : sd;
     const int tid = threadIdx.x;
     // This thread's block (bi, bj): row blocks of 4 below l in each tile.
+    // When the tile has few blocks (small l), `split` adjacent lanes share a
+    // block, each taking every split-th column of a slab, and their sums are
+    // combined by shuffles at the end (a fixed order).
     const int nbc = min(16, (ell - 64 * tc + 3) / 4), nbd = min(16, (ell - 64 * td + 3) / 4);
+    const int nact = diag ? nbc * (nbc + 1) / 2 : nbc * nbd;
+    int split = 1;
+    while (split < 8 && nact * split * 2 <= 256) split *= 2;
+    const int blk = tid / split, part = tid - blk * split;
     int bi = -1, bj = -1;
     if (diag) {
-        int w = tid, r = 0;
+        int w = blk, r = 0;
         while (r < nbc && w >= nbc - r) { w -= nbc - r; ++r; }
         if (r < nbc) { bi = r; bj = r + w; }
-    } else if (tid < nbc * nbd) {
-        bi = tid / nbd;
-        bj = tid - bi * nbd;
+    } else if (blk < nact) {
+        bi = blk / nbd;
+        bj = blk - bi * nbd;
     }
     const float* vz = t.v[g] + (int64_t)(z - t.zbeg[g]) * t.stride[g];
     double acc[4][4];
@@ -192,7 +199,7 @@ __global__ void __launch_bounds__(256) gram64_kernel(Gram64Items t, int ell_pad,
         if (jb + 64 < j1) gload(jb + 64);
         if (bi >= 0) {
 #pragma unroll 4
-            for (int jj = 0; jj < 64; ++jj) {
+            for (int jj = part; jj < 64; jj += split) {
                 const float4 xa = *(const float4*)&sc[jj][4 * bi];
                 const float4 xb = *(const float4*)&sb[jj][4 * bj];
                 const double av[4] = {xa.x, xa.y, xa.z, xa.w}, bv[4] = {xb.x, xb.y, xb.z, xb.w};
@@ -204,7 +211,13 @@ __global__ void __launch_bounds__(256) gram64_kernel(Gram64Items t, int ell_pad,
         }
         __syncthreads();
     }
-    if (bi < 0) return;
+    // The split lanes of a block are adjacent in one wave (split divides 64).
+    for (int o = 1; o < split; o <<= 1)
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[u][e] += __shfl_xor(acc[u][e], o, 64);
+    if (bi < 0 || part != 0) return;
     double* out = partial + ((int64_t)z * kGramChunks + chunk) * ell_pad * ell_pad;
     const int r0 = 64 * tc + 4 * bi, c0 = 64 * td + 4 * bj;
 #pragma unroll
