@@ -443,7 +443,7 @@ def main():
         rows = crossover(N, WL, torch, a.steps, a.warmup)
         line = {"metric": "NormPre-G vs NormPre-L step time on large single matrices (cost crossover in r)",
                 "unit": "ms/step", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup, "higher_is_better": False,
-                "dtype": "fp16 MFMA operands, fp32 accumulate and state", "data": "synthetic",
+                "dtype": "fp16", "precision": "fp16 MFMA operands, fp32 accumulate and state", "data": "synthetic",
                 "config": {"workload": "large_sweep: 4096^2, 4096x16384, 8192^2, 8192x28672, power-law spectrum",
                            "ranks": WL.WORKLOADS["large_sweep"].extra["ranks"], "oversample": 8, "power_iters": 1},
                 "rows": rows}
@@ -550,7 +550,8 @@ def main():
         "vs_baseline_ref": ({"value": round(PAPER_STEPS_PER_S[(wl.name, primary)], 3), "unit": "steps/s",
                              "source": "paper's optimizer latency, NVIDIA A100 80GB (context, not a target)"}
                             if (wl.name, primary) in PAPER_STEPS_PER_S else None),
-        "dtype": "fp16 MFMA operands, fp32 accumulate and state",
+        "dtype": "fp16",
+        "precision": "fp16 MFMA operands, fp32 accumulate; fp32 normalization, update and state",
         "data": "synthetic",
         "config": {"workload": f"{wl.name}: {wl.description}", "matrices": len(wl.shapes),
                    "elements": wl.elements, "variant": f"NormPre-{primary}",
