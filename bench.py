@@ -428,8 +428,8 @@ def crossover(N, WL, torch, steps, warmup):
 def main():
     a = parse()
     if a.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; --gpus above 1 is not supported "
-                                   "(the step shards by matrix ownership; see the design notes)"}))
+        print(json.dumps({"error": "this library runs on one GPU; --gpus above 1 is not supported "
+                                   "(across GPUs the step would shard by matrix ownership)"}))
         sys.exit(2)
     import torch
     from paper_2609_36692_amd import normpre as N

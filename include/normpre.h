@@ -53,7 +53,7 @@ extern "C" {
 /* ---- return codes ------------------------------------------------------ */
 #define NORMPRE_OK                   0
 #define NORMPRE_ERR_INVALID_ARG     (-1)  /* null pointer, bad size or value  */
-#define NORMPRE_ERR_UNSUPPORTED     (-2)  /* valid but outside this build     */
+#define NORMPRE_ERR_UNSUPPORTED     (-2)  /* valid but outside this library   */
 #define NORMPRE_ERR_OOM             (-3)  /* workspace allocation failed      */
 #define NORMPRE_ERR_HIP             (-4)  /* a HIP runtime call failed        */
 #define NORMPRE_ERR_NOT_INITIALIZED (-5)  /* null or destroyed context        */

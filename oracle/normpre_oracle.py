@@ -16,11 +16,10 @@ steps: ``@`` (matmul), ``np.linalg.qr`` (an orthonormal basis),
 ``np.linalg.svd`` (the eigenpairs of Gamma_Q = B B^T from the singular pairs
 of B) and ``np.linalg.eigh`` (the exact variant of App. B).
 
-Conventions the paper leaves open (each one is also listed among the
-readings in the design notes):
+Conventions the paper leaves open:
   * Newton-Schulz polynomial: the quintic used by Muon, coefficients
     (3.4445, -4.7750, 2.0315), Frobenius pre-scaling with +1e-7 (Sec. 3.2
-    only says "the Newton-Schulz iteration adopted by Muon").
+    names Muon's iteration without giving its coefficients).
   * Orientation: k = t mod 2 with k = 0 acting on rows of W (Alg. 1).
   * Zero rows: psi_i = x_i / max(||x_i||, eps), eps = 1e-12 (Eq. 2 needs
     non-zero rows; this keeps a zero row at zero).
