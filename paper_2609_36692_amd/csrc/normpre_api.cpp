@@ -36,6 +36,9 @@ constexpr int64_t kMaxExactRows = 8192;
 constexpr int kColRowChunk = 128;   // rows per block in the column-active pass
 constexpr int kMaxSplits = 16;
 constexpr int kEigSweeps = 30;
+// NormPre-L: largest share of ||Psi||_F^2 in the selected modes for which
+// ||T||_F^2 is taken in closed form (see sketch_back).
+constexpr float kClosedNormFrac = 0.25f;
 constexpr size_t kGroupBudget = size_t(24) << 30;  // workspace bytes per item
 constexpr size_t kRoundBudget = size_t(48) << 30;  // workspace bytes per round
 // Static scratch of normpre_step_noalloc(): the whole workspace of that entry
@@ -340,6 +343,7 @@ struct GWork {
     float* eigs;
     float* ritz;
     int* nsel;
+    int* lneed;             // NormPre-L: 1 where ||T||_F needs the norm pass
     // exact NormPre-L above kMaxEll active rows
     float* gam32;           // Gamma, fp32 a_pad x a_pad
     TriWork tw;             // eigensolver workspace (order a)
@@ -506,6 +510,7 @@ void carve_item(Arena& ar, Item& it, int variant, int opts) {
         w.part = ar.take<float>(count * (int64_t)kMaxSplits * lp * maxpad);
         w.qlen = ar.take<half_t>(count * d.a_pad * lp);
         w.flen = ar.take<half_t>(count * d.b_pad * lp);
+        w.lneed = ar.take<int>(count);
         if (d.xl) {
             const int64_t a = d.a;
             w.gam32 = ar.take<float>(count * d.a_pad * d.a_pad);
@@ -1572,8 +1577,26 @@ int sketch_back(const StepCtx& sc, const Item& it, const Pool& pl, DebugMat* dbg
     const half_t* R = d.k == 0 ? w.flen : w.qlen;
     const int64_t l_stride = (d.k == 0 ? d.a_pad : d.b_pad) * lp;
     const int64_t r_stride = (d.k == 0 ? d.b_pad : d.a_pad) * lp;
-    // ||T||_F^2 directly from the same product (a closed form through the
-    // Ritz values cancels when Psi lies almost entirely in the selected modes).
+    // ||T||_F^2: in closed form, ||Psi||_F^2 - sum_C (lambda_i - 1), where the
+    // selected modes hold at most a quarter of ||Psi||_F^2; there its error
+    // is a few 1e-4 of ||T||^2 (fp16 Q and B) while a norm pass over T would
+    // stream Psi once more.  Where they hold more, the subtraction cancels,
+    // and those matrices take the norm pass: the same product as the update,
+    // reduced to per-tile sums of T^2.  (The closed form needs the Ritz
+    // values of Psi itself: not with the interaction source X, nor for the
+    // dense eigensolver's exact variant.)
+    const bool closed = !d.xl && !w.xs;
+    if (closed) {
+        LNormArgs a{};
+        a.psi2 = w.scale + 1; a.psi2_stride = 2;
+        a.ritz = pl.ritz + (int64_t)it.pool_off * pl.top; a.ritz_stride = pl.top;
+        a.nsel = pl.nsel + it.pool_off;
+        a.tn2 = w.tn2;
+        a.need = w.lneed;
+        a.frac = kClosedNormFrac;
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_l_norm_closed(a, count, sc.s); }),
+               "t norm (closed form)");
+    }
     {
         Operand A{L, lp, l_stride};
         Operand B{R, lp, r_stride};
@@ -1582,11 +1605,15 @@ int sketch_back(const StepCtx& sc, const Item& it, const Pool& pl, DebugMat* dbg
         e.psi = w.psi; e.ld_psi = d.np_; e.stride_psi = mn;
         e.rows = (int)d.m; e.cols = (int)d.n;
         e.sumsq = w.sumsq; e.tiles_per_mat = apply_tiles(d);
+        e.need = closed ? w.lneed : nullptr;
         NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_L_APPLY, 2.0 * d.ell * (double)d.m * d.n * count, 2.0 * d.m * d.n * count,
                      [&] { return launch_gemm_apply_norm(A, B, sh, count, e, sc.s); }),
                "apply norm");
         NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0,
-                     [&] { return launch_sum_partials(w.sumsq, apply_tiles(d), w.tn2, count, sc.s); }),
+                     [&] {
+                         return launch_sum_partials(w.sumsq, apply_tiles(d), w.tn2, count, sc.s,
+                                                    closed ? w.lneed : nullptr);
+                     }),
                "t norm");
     }
     for (int c0 = 0; c0 < count; c0 += kChunk) {

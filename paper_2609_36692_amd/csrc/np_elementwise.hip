@@ -616,8 +616,9 @@ __global__ void __launch_bounds__(256) g_update_kernel(GUpdateArgs a) {
 }
 
 // One block per matrix; fixed-order (deterministic) sum of n partials.
-__global__ void __launch_bounds__(256) sum_partials_kernel(const float* in, int n, float* out) {
+__global__ void __launch_bounds__(256) sum_partials_kernel(const float* in, int n, float* out, const int* need) {
     const int z = blockIdx.x;
+    if (need && need[z] == 0) return;   // the whole block
     const float* p = in + (int64_t)z * n;
     float s = 0.f;
     for (int i = threadIdx.x; i < n; i += 256) s += p[i];
@@ -626,6 +627,32 @@ __global__ void __launch_bounds__(256) sum_partials_kernel(const float* in, int 
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
     __syncthreads();
     if (threadIdx.x == 0) out[z] = red[0] + red[1] + red[2] + red[3];
+}
+
+// One wave per matrix: the closed-form ||T||_F^2 of NormPre-L and whether it
+// cancels (see LNormArgs).  The sums over the selected modes are in fp64.
+__global__ void __launch_bounds__(64) l_norm_closed_kernel(LNormArgs a) {
+    const int z = blockIdx.x, lane = threadIdx.x;
+    const int n = a.nsel[z];
+    const float* r = a.ritz + (int64_t)z * a.ritz_stride;
+    double sl = 0.0, sc = 0.0;
+    for (int i = lane; i < n; i += 64) {
+        const double l = r[i];
+        sl += l;
+        sc += l - 1.0;
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        sl += __shfl_xor(sl, o, 64);
+        sc += __shfl_xor(sc, o, 64);
+    }
+    if (lane == 0) {
+        const double p2 = a.psi2[(int64_t)z * a.psi2_stride];
+        const double t2 = p2 - sc;
+        const bool need = !(sl <= (double)a.frac * p2) || !(t2 > 0.0);
+        a.need[z] = need ? 1 : 0;
+        if (!need) a.tn2[z] = (float)t2;
+    }
 }
 
 // Q <- Q + a I in place for a batch of sp x sp fp16 matrices: one thread per
@@ -963,8 +990,14 @@ hipError_t launch_g_update(const GUpdateArgs& a, int batch, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_sum_partials(const float* in, int n, float* out, int batch, hipStream_t s) {
-    hipLaunchKernelGGL(sum_partials_kernel, dim3(batch), dim3(256), 0, s, in, n, out);
+hipError_t launch_sum_partials(const float* in, int n, float* out, int batch, hipStream_t s, const int* need) {
+    hipLaunchKernelGGL(sum_partials_kernel, dim3(batch), dim3(256), 0, s, in, n, out, need);
+    return hipGetLastError();
+}
+
+hipError_t launch_l_norm_closed(const LNormArgs& a, int batch, hipStream_t s) {
+    if (batch < 1 || !a.psi2 || !a.ritz || !a.nsel || !a.tn2 || !a.need) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(l_norm_closed_kernel, dim3(batch), dim3(64), 0, s, a);
     return hipGetLastError();
 }
 

@@ -254,6 +254,9 @@ gemm_kernel(Operand A, Operand B, GemmShape sh, Epi epi) {
     const int wm = wave / WN, wn = wave - (wave / WN) * WN;
     int bx = blockIdx.x, split = blockIdx.y, z = blockIdx.z;
     xcd_remap<IsGrouped<Epi>::value || IsSkGrouped<Epi>::value || IsCmbGrouped<Epi>::value>(bx, split, z);
+    if constexpr (Epi::kind == EpiKind::ApplyNorm) {
+        if (epi.need && epi.need[z] == 0) return;   // whole block, before any barrier
+    }
     int tiles_n = sh.N / BN, K = sh.K, k_chunk = sh.k_chunk;
     int sgi = 0, slz = 0;           // sketch group and matrix within it
     if constexpr (IsSkGrouped<Epi>::value) {

@@ -85,6 +85,7 @@ struct EpiApplyNorm {
     const half_t* psi; int64_t ld_psi; int64_t stride_psi;
     int rows, cols;
     float* sumsq; int tiles_per_mat;
+    const int* need;                    // if set: only matrices with need[z] != 0
 };
 
 enum class EpiKind { Affine, Partial, Apply, ApplyNorm };
@@ -217,8 +218,25 @@ hipError_t launch_psi_col_normalize(const NormArgs& a, int batch, float* part, i
                                     hipStream_t s);
 
 // out[z] = sum_i in[z*n + i] in a fixed order (per-matrix ||T||_F^2 from
-// per-tile partial sums).
-hipError_t launch_sum_partials(const float* in, int n, float* out, int batch, hipStream_t s);
+// per-tile partial sums); with `need`, only for the matrices with
+// need[z] != 0.
+hipError_t launch_sum_partials(const float* in, int n, float* out, int batch, hipStream_t s,
+                               const int* need = nullptr);
+// NormPre-L ||T||_F^2 in closed form (App. B): with the selected Ritz values
+// the first nsel[z] of the descending list ritz[z], ||T||_F^2 =
+// ||Psi||_F^2 - sum_C (lambda_i - 1).  It is written to tn2[z] unless the
+// selected modes hold more than `frac` of ||Psi||_F^2 (or the result is not
+// positive); need[z] = 1 marks those matrices, whose norm the norm pass over
+// T supplies instead.  psi2[z * psi2_stride] is ||Psi||_F^2.
+struct LNormArgs {
+    const float* psi2; int64_t psi2_stride;
+    const float* ritz; int64_t ritz_stride;
+    const int* nsel;
+    float* tn2;
+    int* need;
+    float frac;
+};
+hipError_t launch_l_norm_closed(const LNormArgs& a, int batch, hipStream_t s);
 
 // Per-matrix Newton-Schulz pre-scale c = 1 / (sqrt(sum psisq) + eps) and
 // ||Psi||_F^2: out[z*2] = c, out[z*2+1] = ||Psi||^2.

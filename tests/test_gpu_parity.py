@@ -220,6 +220,25 @@ def test_zero_rows_and_columns(ctx, shape, variant, t):
     assert math.isclose(np.linalg.norm(u), 0.2 * math.sqrt(shape[0] * shape[1]), rel_tol=2e-3)
 
 
+# ||T||_F of NormPre-L in closed form: on noise-like (Student-t) inputs the
+# selected modes hold a small share of ||Psi||_F^2, so the library takes
+# ||Psi||^2 - sum_C (lambda - 1) instead of a norm pass over T; the update
+# must still match the oracle (which takes the norm of its T) and have the
+# consistent RMS.  The low-rank cases above take the norm pass.
+@pytest.mark.parametrize("shape", [(512, 1536), (1536, 512), (640, 640)])
+@pytest.mark.parametrize("t", [0, 1])
+def test_l_closed_form_norm(ctx, shape, t):
+    _say(f"L closed-form norm {shape} t={t}")
+    mat = _inputs(shape, kind="student_t", seed=4)
+    res = run_step(ctx, "L", [mat], t, debug=False, rank=32)[0]
+    ref = oracle(mat, "L", t, rank=32)
+    lam = ref["ritz_values"][: ref["n_selected"]]
+    share = float(np.sum(lam)) / float(np.sum(ref["psi"].astype(np.float64) ** 2))
+    assert share <= 0.25, share        # the input is in the closed-form regime
+    check_update(f"L closed-form norm {shape} t={t}", res["u"], ref["update"], tol_l(ref), share=share)
+    assert math.isclose(np.linalg.norm(res["u"]), 0.2 * math.sqrt(shape[0] * shape[1]), rel_tol=2e-3)
+
+
 # ----------------------------------------------------------- batching etc.
 def test_batched_equals_single_g(ctx):
     _say("batched vs single (G)")
