@@ -1565,6 +1565,44 @@ int exact_front(const StepCtx& sc, const Item& it, DebugMat* dbg) {
     return NORMPRE_OK;
 }
 
+// NormPre-L items whose ||T||_F^2 may come in closed form: the Ritz values
+// are those of Psi itself (not with the interaction source X, not the dense
+// eigensolver's exact variant).
+bool closed_norm(const Item& it) { return !it.d.xl && !it.w.xs; }
+
+// The closed-form ||T||_F^2 of every such item of the round, kMaxItems shape
+// groups per launch (see LNormGroups).
+int closed_norm_launches(const StepCtx& sc, const std::vector<Item>& items, const std::vector<Pool>& pools) {
+    LNormGroups g{};
+    g.frac = kClosedNormFrac;
+    int total = 0;
+    auto flush = [&]() -> int {
+        if (g.n == 0) return NORMPRE_OK;
+        g.zbeg[g.n] = total;
+        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_l_norm_closed(g, sc.s); }),
+               "t norm (closed form)");
+        g.n = 0;
+        total = 0;
+        return NORMPRE_OK;
+    };
+    for (const Item& it : items) {
+        if (!closed_norm(it)) continue;
+        const Pool& pl = pools[it.pool];
+        const int i = g.n++;
+        g.zbeg[i] = total;
+        g.psi2[i] = it.w.scale + 1;
+        g.ritz[i] = pl.ritz + (int64_t)it.pool_off * pl.top;
+        g.ritz_stride[i] = pl.top;
+        g.nsel[i] = pl.nsel + it.pool_off;
+        g.tn2[i] = it.w.tn2;
+        g.need[i] = it.w.lneed;
+        total += it.count;
+        if (g.n == kMaxItems)
+            if (int rc = flush()) return rc;
+    }
+    return flush();
+}
+
 int sketch_back(const StepCtx& sc, const Item& it, const Pool& pl, DebugMat* dbg) {
     const Dims& d = it.d;
     const GWork& w = it.w;
@@ -1585,18 +1623,8 @@ int sketch_back(const StepCtx& sc, const Item& it, const Pool& pl, DebugMat* dbg
     // reduced to per-tile sums of T^2.  (The closed form needs the Ritz
     // values of Psi itself: not with the interaction source X, nor for the
     // dense eigensolver's exact variant.)
-    const bool closed = !d.xl && !w.xs;
-    if (closed) {
-        LNormArgs a{};
-        a.psi2 = w.scale + 1; a.psi2_stride = 2;
-        a.ritz = pl.ritz + (int64_t)it.pool_off * pl.top; a.ritz_stride = pl.top;
-        a.nsel = pl.nsel + it.pool_off;
-        a.tn2 = w.tn2;
-        a.need = w.lneed;
-        a.frac = kClosedNormFrac;
-        NP_TRY(timed(sc.ctx, NORMPRE_KCLASS_SK_SMALL, 0.0, 0.0, [&] { return launch_l_norm_closed(a, count, sc.s); }),
-               "t norm (closed form)");
-    }
+    // (closed_norm_launches ran the closed form for these matrices.)
+    const bool closed = closed_norm(it);
     {
         Operand A{L, lp, l_stride};
         Operand B{R, lp, r_stride};
@@ -1715,6 +1743,8 @@ int run_round_l(const StepCtx& sc, std::vector<Item>& items, std::vector<Pool>& 
             "f = b^t k");
         if (rc) return rc;
     }
+    rc = closed_norm_launches(sc, items, pools);
+    if (rc) return rc;
     for (const Item& it : items) {
         rc = sketch_back(sc, it, pools[it.pool], dbg);
         if (rc) return rc;

@@ -630,11 +630,14 @@ __global__ void __launch_bounds__(256) sum_partials_kernel(const float* in, int 
 }
 
 // One wave per matrix: the closed-form ||T||_F^2 of NormPre-L and whether it
-// cancels (see LNormArgs).  The sums over the selected modes are in fp64.
-__global__ void __launch_bounds__(64) l_norm_closed_kernel(LNormArgs a) {
-    const int z = blockIdx.x, lane = threadIdx.x;
-    const int n = a.nsel[z];
-    const float* r = a.ritz + (int64_t)z * a.ritz_stride;
+// cancels (see LNormGroups).  The sums over the selected modes are in fp64.
+__global__ void __launch_bounds__(64) l_norm_closed_kernel(LNormGroups g) {
+    const int zl = blockIdx.x, lane = threadIdx.x;
+    int gi = 0;
+    while (gi + 1 < g.n && zl >= g.zbeg[gi + 1]) ++gi;
+    const int z = zl - g.zbeg[gi];
+    const int n = g.nsel[gi][z];
+    const float* r = g.ritz[gi] + (int64_t)z * g.ritz_stride[gi];
     double sl = 0.0, sc = 0.0;
     for (int i = lane; i < n; i += 64) {
         const double l = r[i];
@@ -647,11 +650,11 @@ __global__ void __launch_bounds__(64) l_norm_closed_kernel(LNormArgs a) {
         sc += __shfl_xor(sc, o, 64);
     }
     if (lane == 0) {
-        const double p2 = a.psi2[(int64_t)z * a.psi2_stride];
+        const double p2 = g.psi2[gi][2 * (int64_t)z];
         const double t2 = p2 - sc;
-        const bool need = !(sl <= (double)a.frac * p2) || !(t2 > 0.0);
-        a.need[z] = need ? 1 : 0;
-        if (!need) a.tn2[z] = (float)t2;
+        const bool need = !(sl <= (double)g.frac * p2) || !(t2 > 0.0);
+        g.need[gi][z] = need ? 1 : 0;
+        if (!need) g.tn2[gi][z] = (float)t2;
     }
 }
 
@@ -995,9 +998,12 @@ hipError_t launch_sum_partials(const float* in, int n, float* out, int batch, hi
     return hipGetLastError();
 }
 
-hipError_t launch_l_norm_closed(const LNormArgs& a, int batch, hipStream_t s) {
-    if (batch < 1 || !a.psi2 || !a.ritz || !a.nsel || !a.tn2 || !a.need) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(l_norm_closed_kernel, dim3(batch), dim3(64), 0, s, a);
+hipError_t launch_l_norm_closed(const LNormGroups& g, hipStream_t s) {
+    if (g.n < 1 || g.n > kMaxItems || g.zbeg[0] != 0) return hipErrorInvalidValue;
+    for (int i = 0; i < g.n; ++i)
+        if (g.zbeg[i + 1] <= g.zbeg[i] || !g.psi2[i] || !g.ritz[i] || !g.nsel[i] || !g.tn2[i] || !g.need[i])
+            return hipErrorInvalidValue;
+    hipLaunchKernelGGL(l_norm_closed_kernel, dim3(g.zbeg[g.n]), dim3(64), 0, s, g);
     return hipGetLastError();
 }
 

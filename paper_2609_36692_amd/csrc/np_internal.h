@@ -222,21 +222,25 @@ hipError_t launch_psi_col_normalize(const NormArgs& a, int batch, float* part, i
 // need[z] != 0.
 hipError_t launch_sum_partials(const float* in, int n, float* out, int batch, hipStream_t s,
                                const int* need = nullptr);
-// NormPre-L ||T||_F^2 in closed form (App. B): with the selected Ritz values
-// the first nsel[z] of the descending list ritz[z], ||T||_F^2 =
-// ||Psi||_F^2 - sum_C (lambda_i - 1).  It is written to tn2[z] unless the
-// selected modes hold more than `frac` of ||Psi||_F^2 (or the result is not
-// positive); need[z] = 1 marks those matrices, whose norm the norm pass over
-// T supplies instead.  psi2[z * psi2_stride] is ||Psi||_F^2.
-struct LNormArgs {
-    const float* psi2; int64_t psi2_stride;
-    const float* ritz; int64_t ritz_stride;
-    const int* nsel;
-    float* tn2;
-    int* need;
+// NormPre-L ||T||_F^2 in closed form (App. B), for several shape groups in
+// one launch: matrix z of the launch is matrix z - zbeg[g] of group g.  With
+// the selected Ritz values the first nsel[i] of the descending list ritz[i]
+// (stride ritz_stride), ||T||_F^2 = ||Psi||_F^2 - sum_C (lambda_i - 1),
+// psi2[i * 2] being ||Psi||_F^2.  It is written to tn2[i] unless the selected
+// modes hold more than `frac` of ||Psi||_F^2 (or the result is not
+// positive); need[i] = 1 marks those matrices, whose norm the norm pass over
+// T supplies instead.
+struct LNormGroups {
+    int n;
+    int zbeg[kMaxItems + 1];
+    const float* psi2[kMaxItems];
+    const float* ritz[kMaxItems]; int64_t ritz_stride[kMaxItems];
+    const int* nsel[kMaxItems];
+    float* tn2[kMaxItems];
+    int* need[kMaxItems];
     float frac;
 };
-hipError_t launch_l_norm_closed(const LNormArgs& a, int batch, hipStream_t s);
+hipError_t launch_l_norm_closed(const LNormGroups& g, hipStream_t s);
 
 // Per-matrix Newton-Schulz pre-scale c = 1 / (sqrt(sum psisq) + eps) and
 // ||Psi||_F^2: out[z*2] = c, out[z*2+1] = ||Psi||^2.
