@@ -182,13 +182,24 @@ def stream_ceiling(N, torch, mib):
     return out
 
 
-def normalize_rooflines(cls, ceiling):
+def one_pass_columns(m, n):
+    """Whether the library normalizes the columns of an m x n matrix in one
+    pass: 16-byte aligned rows and columns of at most 2048 rows padded to a
+    multiple of 256 (a strip of them then fits on one CU); longer columns
+    take a statistics pass and a normalize pass that reads M and W again."""
+    return n % 4 == 0 and -(-m // 256) * 256 <= 2048
+
+
+def normalize_rooflines(cls, ceiling, shapes):
     """Normalization rooflines per orientation on the algorithmic 18 B per
     element (read G, M_prev, W; write M and fp16 Psi), with the fraction of
-    the measured ceiling of the same byte mix; the column-active pass also
-    on the 26 B it moves (statistics 16 B + apply 10 B) against the ceiling
-    of those two mixes."""
+    the measured ceiling of the same byte mix; the column-active class also
+    on the bytes it moves (18 B per element of one-pass matrices, 26 B =
+    statistics 16 B + apply 10 B of two-pass ones) against the ceilings of
+    those mixes."""
     out = {}
+    total = sum(m * n for m, n in shapes)
+    two_pass = sum(m * n for m, n in shapes if not one_pass_columns(m, n)) / total if total else 0.0
     for name, label in (("normalize", "row-active"), ("normalize_col", "column-active")):
         r = roofline_of(cls.get(name), "hbm")
         if not r:
@@ -200,9 +211,12 @@ def normalize_rooflines(cls, ceiling):
             r["frac_of_ceiling"] = round(r["achieved"] / c0, 4)
             if name == "normalize_col":
                 sec = cls[name]["ms"] / 1e3
-                moved = cls[name]["bytes"] * 26.0 / 18.0
-                t_ceil = cls[name]["bytes"] / 18.0 * (16.0 / (ceiling["1"]["gb_per_s"] * 1e9) +
-                                                      10.0 / (ceiling["2"]["gb_per_s"] * 1e9))
+                elems = cls[name]["bytes"] / 18.0
+                moved = elems * (18.0 + 8.0 * two_pass)
+                t_ceil = elems * ((1.0 - two_pass) * 18.0 / (c0 * 1e9) +
+                                  two_pass * (16.0 / (ceiling["1"]["gb_per_s"] * 1e9) +
+                                              10.0 / (ceiling["2"]["gb_per_s"] * 1e9)))
+                r["two_pass_element_share"] = round(two_pass, 4)
                 r["moved_gbs"] = round(moved / sec / 1e9, 1)
                 r["moved_frac_of_ceiling"] = round(t_ceil / sec, 4)
         out[name] = r
@@ -479,7 +493,7 @@ def main():
         if roof and v in traffic:
             roof["traffic"] = round(traffic[v]["bytes_per_launch"], 1)
             roof["traffic_detail"] = traffic[v]
-        norm_roof = normalize_rooflines(cls, ceiling)
+        norm_roof = normalize_rooflines(cls, ceiling, wl.shapes)
         total_dev = sum(c["ms"] for c in cls.values())
         res[v] = {
             "steps_per_s": round(1e3 / r["ms_per_step"], 3),

@@ -485,6 +485,177 @@ __global__ void __launch_bounds__(kColThreads) normalize_cols_apply(NormArgs a, 
 }
 
 // ---------------------------------------------------------------------------
+// Column-active orientation in one pass, for padded columns of at most
+// kFusedNR * 4096 / SW rows: one block of kFusedThreads threads per strip of
+// SW columns (SW / 4 threads per row, 16 bytes each, at most kFusedNR rows
+// per thread).  The strip of the new M (in registers) and of W (in LDS)
+// stays on the CU between the column sums and the Psi store, so G, M_prev
+// and W are read once: 18
+// bytes per element, as in the row-active kernels, against the 26 of the
+// two-pass path.  As there, <m, w> and ||w||^2 give c, x is formed in fp64
+// and rounded to fp32 in the registers, and ||x||^2 is summed from the
+// formed x.
+constexpr int kFusedThreads = 1024, kFusedNR = 8;
+
+// Sums NQ per-column quantities (four adjacent columns per thread) over the
+// rows of the block in a fixed order: lanes of a wave first, then the waves.
+// On return tot[q][c] holds the strip's sum for column c in every thread.
+template <int SW, int NQ>
+__device__ __forceinline__ void strip_col_sums(double (&v)[NQ][4], double (*part)[NQ][SW], double (*tot)[SW]) {
+    constexpr int TPR = SW / 4;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+            for (int o = TPR; o < 64; o <<= 1) v[q][e] += __shfl_xor(v[q][e], o, 64);
+    if (lane < TPR) {
+#pragma unroll
+        for (int q = 0; q < NQ; ++q)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) part[wave][q][lane * 4 + e] = v[q][e];
+    }
+    __syncthreads();
+    if (threadIdx.x < NQ * SW) {
+        const int q = threadIdx.x / SW, c = threadIdx.x % SW;
+        double t = 0.0;
+        for (int w = 0; w < kFusedThreads / 64; ++w) t += part[w][q][c];
+        tot[q][c] = t;
+    }
+    __syncthreads();
+}
+
+template <int SW, bool DBG>
+__global__ void __launch_bounds__(kFusedThreads) normalize_cols_fused(NormArgs a, int nr) {
+    constexpr int TPR = SW / 4, RPI = kFusedThreads / TPR, WAVES = kFusedThreads / 64;
+    // Workgroups are dispatched round-robin over the 8 XCDs; each XCD takes
+    // one contiguous run of strips instead, so neighbouring strips (which
+    // share 128-byte lines) meet in the same L2.  The ragged tail keeps its
+    // order.
+    int lin = blockIdx.x + gridDim.x * blockIdx.y;
+    const int per = (int)(gridDim.x * gridDim.y) >> 3;
+    if (lin < (per << 3)) lin = (lin & 7) * per + (lin >> 3);
+    const int strip = lin % gridDim.x, z = lin / gridDim.x;
+    const int tid = threadIdx.x, cx = tid % TPR, ry = tid / TPR;
+    const int col0 = strip * SW + cx * 4;
+    const bool live = col0 < a.cols;   // cols % 4 == 0: all four columns are real
+    float* W = a.ptrs.w[z];
+    float* M = a.ptrs.m[z];
+    const float* G = a.ptrs.g[z];
+    // W of row slot r of this thread: wl[r][tid] (consecutive threads,
+    // consecutive 16 bytes).
+    __shared__ float4 wl[kFusedNR][kFusedThreads];
+    float mv[kFusedNR][4];
+    double s2[2][4] = {};   // <m, w>, ||w||^2 per column
+    int bad = 0;
+#pragma unroll
+    for (int r0 = 0; r0 < kFusedNR; r0 += kColBatch) {
+        float4 mp[kColBatch], g[kColBatch], w[kColBatch];
+#pragma unroll
+        for (int u = 0; u < kColBatch; ++u) {
+            const int r = r0 + u, i = ry + r * RPI;
+            mp[u] = g[u] = w[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (r < nr && i < a.rows && live) {
+                const int64_t o = (int64_t)i * a.cols + col0;
+                mp[u] = *reinterpret_cast<const float4*>(M + o);
+                g[u] = *reinterpret_cast<const float4*>(G + o);
+                w[u] = *reinterpret_cast<const float4*>(W + o);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kColBatch; ++u) {
+            const int r = r0 + u, i = ry + r * RPI;
+            float pv[4] = {mp[u].x, mp[u].y, mp[u].z, mp[u].w}, gv[4] = {g[u].x, g[u].y, g[u].z, g[u].w};
+            float wq[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
+            if (a.nfin) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    pv[e] = finite_or_zero(pv[e], bad);
+                    gv[e] = finite_or_zero(gv[e], bad);
+                    wq[e] = finite_or_zero(wq[e], bad);
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) mv[r][e] = fmaf(a.mu, pv[e], gv[e]);
+            if (r < nr) wl[r][tid] = make_float4(wq[0], wq[1], wq[2], wq[3]);
+            if (r < nr && i < a.rows && live) {
+                *reinterpret_cast<float4*>(M + (int64_t)i * a.cols + col0) =
+                    make_float4(mv[r][0], mv[r][1], mv[r][2], mv[r][3]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const double md = mv[r][e], wd = wq[e];
+                    s2[0][e] = fma(md, wd, s2[0][e]);
+                    s2[1][e] = fma(wd, wd, s2[1][e]);
+                }
+            }
+        }
+    }
+    __shared__ double part2[WAVES][2][SW], tot2[2][SW];
+    __shared__ double part1[WAVES][1][SW], tot1[1][SW];
+    strip_col_sums<SW, 2>(s2, part2, tot2);
+    double cf[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) cf[e] = tangent_coef(a.tangent, tot2[0][cx * 4 + e], tot2[1][cx * 4 + e]);
+    // x replaces m in the registers (rounded to fp32 after it is formed, so
+    // its relative error is u32 whatever the cancellation was).
+    double s1[1][4] = {};
+#pragma unroll
+    for (int r = 0; r < kFusedNR; ++r) {
+        const int i = ry + r * RPI;
+        if (r < nr && i < a.rows && live) {
+            const float4 w4 = wl[r][tid];
+            const float wq[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const double x = tangent_x(mv[r][e], wq[e], cf[e]);
+                s1[0][e] = fma(x, x, s1[0][e]);
+                mv[r][e] = (float)x;
+            }
+        }
+    }
+    strip_col_sums<SW, 1>(s1, part1, tot1);
+    float invf[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) invf[e] = (float)(1.0 / fmax(sqrt(tot1[0][cx * 4 + e]), (double)a.eps));
+    if (tid < SW && strip * SW + tid < a.cols) {
+        const int64_t col = (int64_t)strip * SW + tid;
+        const double n2 = tot1[0][tid], inv = 1.0 / fmax(sqrt(n2), (double)a.eps);
+        a.psisq[(int64_t)z * a.stride_psisq + col] = (float)(n2 * inv * inv);
+        if (a.xsq) a.xsq[(int64_t)z * a.stride_psisq + col] = (float)n2;
+    }
+    if (a.nfin) {
+        __shared__ int redbad[WAVES];
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) bad += __shfl_xor(bad, o, 64);
+        if ((tid & 63) == 0) redbad[tid >> 6] = bad;
+        __syncthreads();
+        if (tid == 0 && strip * SW < a.cols) {
+            int t = 0;
+            for (int q = 0; q < WAVES; ++q) t += redbad[q];
+            a.nfin[(int64_t)z * a.stride_nfin + strip] = t;
+        }
+    }
+    half_t* P = a.psi + (int64_t)z * a.stride_psi;
+#pragma unroll
+    for (int r = 0; r < kFusedNR; ++r) {
+        const int i = ry + r * RPI;
+        if (r < nr && i < a.rows_pad) {
+            float p[4] = {0.f, 0.f, 0.f, 0.f};
+            if (i < a.rows && live) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) p[e] = mv[r][e] * invf[e];
+                if constexpr (DBG)
+                    *reinterpret_cast<float4*>(a.psi32 + (int64_t)z * a.stride_psi32 + (int64_t)i * a.cols + col0) =
+                        make_float4(p[0], p[1], p[2], p[3]);
+            }
+            half_t h[4] = {(half_t)p[0], (half_t)p[1], (half_t)p[2], (half_t)p[3]};
+            *reinterpret_cast<uint2*>(P + (int64_t)i * a.ld_psi + col0) = *reinterpret_cast<const uint2*>(h);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Muon input, pass 1: M <- mu M + G over the whole matrix, with the block's
 // sum of M^2 (fp64 in each thread, fixed-order block reduction) written to
 // part[z * stride_part + block].
@@ -850,8 +1021,16 @@ __global__ void __launch_bounds__(256) psi_colscale_kernel(half_t* psi, int64_t 
 // Count slots per matrix, as the launches write them: one per real row in the
 // row-active kernels, one per stats block (row chunk x column block) in the
 // column-active stats pass (its vector width as launch_normalize_cols picks).
+int cols_fused_width(const NormArgs& a) {
+    if (!(a.vec_ok && a.cols % 4 == 0 && a.ld_psi % 64 == 0)) return 0;
+    for (int sw = 64; sw >= 16; sw >>= 1)
+        if (a.rows_pad * sw <= (int64_t)kFusedNR * kFusedThreads * 4) return sw;
+    return 0;
+}
+
 int64_t nonfinite_slots(const NormArgs& a, bool row_active, int row_chunk) {
     if (row_active) return a.rows;
+    if (const int sw = cols_fused_width(a)) return (a.cols + sw - 1) / sw;
     const int nchunks = (a.rows + row_chunk - 1) / row_chunk;
     const int vw = (a.vec_ok && a.cols % 4 == 0 && a.ld_psi % 4 == 0) ? 4 : 1;
     return (int64_t)nchunks * ((a.cols + 64 * vw - 1) / (64 * vw));
@@ -936,7 +1115,24 @@ hipError_t cols_launch(const NormArgs& a, int batch, double* partials, int row_c
     return hipGetLastError();
 }
 
+template <int SW>
+hipError_t cols_fused_launch(const NormArgs& a, int batch, hipStream_t s) {
+    constexpr int rpi = kFusedThreads / (SW / 4);
+    const int nr = (int)((a.rows_pad + rpi - 1) / rpi);
+    if (nr > kFusedNR || a.ld_psi % SW) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)(a.ld_psi / SW), batch);
+    if (a.psi32) hipLaunchKernelGGL((normalize_cols_fused<SW, true>), grid, dim3(kFusedThreads), 0, s, a, nr);
+    else hipLaunchKernelGGL((normalize_cols_fused<SW, false>), grid, dim3(kFusedThreads), 0, s, a, nr);
+    return hipGetLastError();
+}
+
 hipError_t launch_normalize_cols(const NormArgs& a, int batch, double* partials, int row_chunk, hipStream_t s) {
+    switch (cols_fused_width(a)) {
+        case 64: return cols_fused_launch<64>(a, batch, s);
+        case 32: return cols_fused_launch<32>(a, batch, s);
+        case 16: return cols_fused_launch<16>(a, batch, s);
+        default: break;
+    }
     if (a.vec_ok && a.cols % 4 == 0 && a.ld_psi % 4 == 0) return cols_launch<4>(a, batch, partials, row_chunk, s);
     return cols_launch<1>(a, batch, partials, row_chunk, s);
 }

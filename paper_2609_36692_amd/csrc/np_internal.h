@@ -200,7 +200,11 @@ struct IdxChunk { int idx[kChunk]; };
 hipError_t launch_count_reduce(const int* nfin, int64_t slots, int64_t stride, const IdxChunk& idx, int count,
                                long long* status, hipStream_t s);
 hipError_t launch_normalize_rows(const NormArgs& a, int batch, hipStream_t s);
-// Column-active orientation: stats pass + normalize pass.
+// Column-active orientation: one pass where a strip of SW columns of M and
+// W fits the registers of one block (cols_fused_width(a) = SW, padded
+// columns of at most 2048 rows, 16-byte aligned rows), else a statistics
+// pass and a normalize pass over `partials`.
+int cols_fused_width(const NormArgs& a);
 hipError_t launch_normalize_cols(const NormArgs& a, int batch, double* partials,
                                  int row_chunk, hipStream_t s);
 int64_t normalize_cols_partials(int rows, int cols_pad, int row_chunk);

@@ -120,6 +120,33 @@ def test_momentum_and_psi(ctx, shape, t):
     assert np.allclose(np.linalg.norm(psi.astype(np.float64), axis=axis), 1.0, atol=1e-5)
 
 
+# Column-active normalization runs in one pass where a strip of columns of M
+# and W fits on one CU (16-byte aligned rows, columns of at most 2048 padded
+# rows, in strips of 64, 32 or 16 columns by length) and in two passes
+# elsewhere: shapes at both ends of every strip width, just past the last
+# one, and unaligned rows.  Psi, M and the whole NormPre-G update, with and
+# without the fp32 debug copy of Psi.
+COL_SHAPES = [(1, 300), (512, 200), (513, 100), (1024, 64), (1025, 36), (2048, 40), (2049, 40), (2048, 41)]
+
+
+@pytest.mark.parametrize("shape", COL_SHAPES)
+def test_column_active_normalization(ctx, shape):
+    _say(f"column-active normalize shape={shape}")
+    mat = _inputs(shape)
+    ref = oracle(mat, "G", 1)
+    res = run_step(ctx, "G", [mat], 1)[0]
+    assert O.relative_fro(res["m"].numpy(), ref["momentum"]) < 1e-6
+    psi = N.normpre_debug_fetch(ctx, 0, N.NORMPRE_DEBUG_PSI, shape[0] * shape[1]).reshape(shape)
+    err = O.relative_fro(psi, ref["psi"])
+    record(f"column-active normalize {shape}", "Psi rel-Frobenius", err, TOL_PSI)
+    assert err < TOL_PSI
+    assert np.allclose(np.linalg.norm(psi.astype(np.float64), axis=0), 1.0, atol=1e-5)
+    check_update(f"column-active G {shape} (debug copy)", res["u"], ref["update"], TOL_G)
+    plain = run_step(ctx, "G", [mat], 1, debug=False)[0]
+    check_update(f"column-active G {shape}", plain["u"], ref["update"], TOL_G)
+    assert np.array_equal(plain["u"], res["u"])
+
+
 # ----------------------------------------------------------- NormPre-G
 @pytest.mark.parametrize("shape", SHAPES)
 @pytest.mark.parametrize("t", [0, 1])
@@ -684,9 +711,9 @@ def _sanitized(mat):
 @pytest.mark.parametrize("t", [0, 1])
 def test_check_finite(ctx, variant, t):
     _say(f"finite check {variant} t={t}")
-    shapes = [(257, 513), (256, 1024), (300, 200)]
+    shapes = [(257, 513), (256, 1024), (300, 200), (1500, 64)]
     clean = [_inputs(sh, "lowrank", seed=70 + i) for i, sh in enumerate(shapes)]
-    plan = [(5, 3, 1), (0, 0, 0), (1, 7, 2)]
+    plan = [(5, 3, 1), (0, 0, 0), (1, 7, 2), (2, 2, 3)]
     mats, where = [], []
     for i, (m, (ng, nm, nw)) in enumerate(zip(clean, plan)):
         pm, pos = _poison(m, 80 + i, ng, nm, nw)
