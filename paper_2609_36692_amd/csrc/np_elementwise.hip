@@ -490,11 +490,10 @@ __global__ void __launch_bounds__(kColThreads) normalize_cols_apply(NormArgs a, 
 // SW columns (SW / 4 threads per row, 16 bytes each, at most kFusedNR rows
 // per thread).  The strip of the new M (in registers) and of W (in LDS)
 // stays on the CU between the column sums and the Psi store, so G, M_prev
-// and W are read once: 18
-// bytes per element, as in the row-active kernels, against the 26 of the
-// two-pass path.  As there, <m, w> and ||w||^2 give c, x is formed in fp64
-// and rounded to fp32 in the registers, and ||x||^2 is summed from the
-// formed x.
+// and W are read once: 18 bytes per element, as in the row-active kernels,
+// against the 26 of the two-pass path.  As there, <m, w> and ||w||^2 give c,
+// x is formed in fp64 and rounded to fp32 in the registers, and ||x||^2 is
+// summed from the formed x.
 constexpr int kFusedThreads = 1024, kFusedNR = 8;
 
 // Sums NQ per-column quantities (four adjacent columns per thread) over the
