@@ -124,11 +124,11 @@ def test_momentum_and_psi(ctx, shape, t):
 # and W fits on one CU (16-byte aligned rows, columns of at most 2048 padded
 # rows, in strips of 64, 32 or 16 columns by length) and in two passes
 # elsewhere: shapes at both ends of every strip width, just past the last
-# one, and unaligned rows; (300, 1100) has 20 strips, so the XCD-ordered
-# part of its launch (16 strips) is followed by a ragged tail.  Psi, M and the
-# whole NormPre-G update, with and without the fp32 debug copy of Psi.
-COL_SHAPES = [(1, 300), (512, 200), (513, 100), (1024, 64), (1025, 36), (2048, 40), (2049, 40), (2048, 41),
-              (300, 1100)]
+# one, and unaligned rows; (200, 1100) has 20 strips of 64 columns, so the
+# XCD-ordered part of its launch (16 strips) is followed by a ragged tail.  Psi, M and the whole NormPre-G
+# update, with and without the fp32 debug copy of Psi.
+COL_SHAPES = [(1, 300), (256, 200), (257, 100), (512, 200), (513, 100), (1024, 64), (1025, 36), (2048, 40),
+              (2049, 40), (2048, 41), (200, 1100)]
 
 
 @pytest.mark.parametrize("shape", COL_SHAPES)
